@@ -1,0 +1,147 @@
+"""Pins of the oracle's decode loop (Algorithm 1) against full-model greedy decoding and the
+special cases that fix the acceptance count."""
+import numpy as np
+import pytest
+
+import synth
+from oracle.model import Decoder
+from oracle import decode
+
+SMALL = [synth.S1, synth.S_T5, synth.S_LLAMA]
+
+
+def _setup(wl, seed=0, mutate=None, k=None):
+    w = synth.workload_weights(wl, seed, threads=2)
+    if mutate:
+        mutate(w)
+    z = synth.make_visual(wl.shape, seed, 1)[0]
+    pr = synth.make_prompts(wl.shape, seed, 1, wl.prompt_len)[0]
+    return Decoder(wl.shape, w, k or wl.draft_layers), pr, z
+
+
+def test_accept_length_cases():
+    assert decode.accept_length([5, 6, 7], [5, 6, 9, 4]) == 2
+    assert decode.accept_length([5, 6, 7], [5, 6, 7, 4]) == 3
+    assert decode.accept_length([5, 6, 7], [1, 6, 7, 4]) == 0
+    assert decode.accept_length([], [3]) == 0
+
+
+@pytest.mark.parametrize("wl", SMALL, ids=lambda w: w.name)
+@pytest.mark.parametrize("seed", [0, 1])
+def test_ssd_equals_greedy_bit_exact(wl, seed):
+    dec, pr, z = _setup(wl, seed)
+    g = decode.greedy(dec, pr, z, wl.new_tokens)
+    for gamma in (1, wl.gamma, 7):
+        s = decode.ssd(dec, pr, z, wl.new_tokens, gamma)
+        assert s.tokens == g.tokens
+        assert np.array_equal(s.prefill_logits, g.prefill_logits)
+        # every verified position's logits equal the greedy step's logits bit for bit
+        pos_logits = {}
+        for r in s.rounds:
+            for i, lg in enumerate(r.target_logits[: r.accepted + 1]):
+                pos_logits[r.seq_len + i] = lg
+        base = s.rounds[0].seq_len
+        for j, lg in enumerate(g.step_logits):
+            if base + j in pos_logits:
+                assert np.array_equal(pos_logits[base + j], lg)
+        # accepted length per round in [0, gamma], emitted count exactly T
+        assert all(0 <= r.accepted <= gamma for r in s.rounds)
+        assert len(s.tokens) == wl.new_tokens
+        assert 1 + sum(r.accepted + 1 for r in s.rounds) >= wl.new_tokens
+        assert 1 + sum(r.accepted + 1 for r in s.rounds[:-1]) < wl.new_tokens
+
+
+@pytest.mark.parametrize("wl", SMALL, ids=lambda w: w.name)
+def test_other_draft_depths(wl):
+    for k in (1, wl.shape.n_layers):
+        dec, pr, z = _setup(wl, 2, k=k)
+        g = decode.greedy(dec, pr, z, 16)
+        assert decode.ssd(dec, pr, z, 16, 3).tokens == g.tokens
+
+
+def _kill_deep(wl):
+    def m(w):
+        for lw in w["layers"][wl.draft_layers:]:
+            lw["wo"][:] = 0
+            lw["w_down"][:] = 0
+            if "xo" in lw:
+                lw["xo"][:] = 0
+        w["in_w2"][:] = 0
+        w["in_b2"][:] = 0
+    return m
+
+
+@pytest.mark.parametrize("wl", SMALL, ids=lambda w: w.name)
+def test_zero_deep_layers_accept_everything(wl):
+    # s = 0 and an identity imitation network: the draft equals the full model exactly
+    dec, pr, z = _setup(wl, 0, _kill_deep(wl))
+    s = decode.ssd(dec, pr, z, wl.new_tokens, wl.gamma)
+    assert all(r.accepted == wl.gamma for r in s.rounds)
+    assert s.acceptance_rate() == 1.0
+    for r in s.rounds:
+        for i in range(wl.gamma):
+            assert np.array_equal(r.draft_logits[i], r.target_logits[i])
+
+
+@pytest.mark.parametrize("wl", SMALL, ids=lambda w: w.name)
+def test_forced_wrong_drafts_accept_nothing(wl):
+    dec, pr, z = _setup(wl, 1)
+    g = decode.greedy(dec, pr, z, wl.new_tokens)
+    vocab = wl.shape.vocab
+    s = decode.ssd(dec, pr, z, wl.new_tokens, wl.gamma,
+                   draft_policy=lambda r, i, lg: (int(np.argmax(lg)) + 1) % vocab)
+    # a wrong draft can still match by chance only if argmax+1 is the full model's token
+    assert sum(r.accepted for r in s.rounds) <= 2
+    assert s.tokens == g.tokens
+    always_bad = decode.ssd(dec, pr, z, wl.new_tokens, wl.gamma, draft_policy=lambda r, i, lg: -1)
+    assert all(r.accepted == 0 for r in always_bad.rounds)
+    assert always_bad.tokens == g.tokens
+    assert len(always_bad.rounds) == wl.new_tokens - 1
+
+
+def test_gamma_zero_is_greedy():
+    dec, pr, z = _setup(synth.S1, 0)
+    g = decode.greedy(dec, pr, z, 20)
+    s = decode.ssd(dec, pr, z, 20, 0)
+    assert s.tokens == g.tokens and all(r.accepted == 0 for r in s.rounds)
+
+
+@pytest.mark.parametrize("wl", SMALL, ids=lambda w: w.name)
+def test_stale_kv_is_never_read(wl):
+    dec, pr, z = _setup(wl, 3)
+    clean = decode.ssd(dec, pr, z, wl.new_tokens, wl.gamma)
+    poisoned = decode.ssd(dec, pr, z, wl.new_tokens, wl.gamma, poison=True)
+    assert poisoned.tokens == clean.tokens
+    for a, b in zip(clean.rounds, poisoned.rounds):
+        assert a.accepted == b.accepted
+        assert all(np.array_equal(x, y) for x, y in zip(a.target_logits, b.target_logits))
+
+
+@pytest.mark.parametrize("wl", SMALL, ids=lambda w: w.name)
+def test_draft_without_imitation_still_yields_greedy_output(wl):
+    dec, pr, z = _setup(wl, 4)
+    g = decode.greedy(dec, pr, z, wl.new_tokens)
+    s = decode.ssd(dec, pr, z, wl.new_tokens, wl.gamma, use_imitation=False)
+    assert s.tokens == g.tokens
+
+
+def test_eos_stops_the_loop():
+    dec, pr, z = _setup(synth.S1, 0)
+    g = decode.greedy(dec, pr, z, 24)
+    eos = g.tokens[5]
+    s = decode.ssd(dec, pr, z, 24, 4, eos_id=eos)
+    first = g.tokens.index(eos)
+    assert s.tokens == g.tokens[: first + 1]
+
+
+@pytest.mark.parametrize("wl", SMALL, ids=lambda w: w.name)
+def test_replay_of_own_stream_reproduces_logits(wl):
+    dec, pr, z = _setup(wl, 5)
+    s = decode.ssd(dec, pr, z, wl.new_tokens, wl.gamma)
+    lg0, rounds = decode.replay(dec, pr, z, s.tokens[0], [(r.drafts, r.targets) for r in s.rounds],
+                                wl.gamma)
+    assert np.array_equal(lg0, s.prefill_logits)
+    for a, b in zip(s.rounds, rounds):
+        assert a.accepted == b.accepted
+        assert all(np.array_equal(x, y) for x, y in zip(a.draft_logits, b.draft_logits))
+        assert all(np.array_equal(x, y) for x, y in zip(a.target_logits, b.target_logits))
