@@ -1,0 +1,205 @@
+/*
+ * ssd.h — C ABI of the self-speculative decoding library (FastVLM, arXiv 2510.22641) for
+ * MI355X (gfx950).
+ *
+ * The paper's inference problem (Algorithm 1, Sec. "Methodology", paragraph "Inference"): given
+ * the encoder output z = E(I, T0), a context y^1..y^t, a target length T and a draft length d,
+ * generate tokens with a draft model (the decoder's first n layers, the imitation network I and
+ * the shared LM head g) that proposes d tokens autoregressively, and the full decoder, which
+ * verifies them in one forward pass; the longest agreeing prefix is kept together with the full
+ * model's token at the first disagreement (or its next token when all agree).  Draft and full
+ * model share one KV cache (Sec. "Methodology", paragraph "KV cache").
+ *
+ * This library computes the four steps of that loop on the GPU:
+ *   ssd_prefill  run the full decoder over the context, fill the KV cache, emit the first token
+ *   ssd_draft    gamma draft steps (layers 1..k, I, g, argmax) from the pending token
+ *   ssd_verify   the full decoder over [pending, draft_1..draft_gamma] in one causal pass
+ *   ssd_accept   greedy acceptance; advances the valid KV length (the rollback is the reset)
+ * and, for convenience, the whole loop (ssd_generate).
+ *
+ * Conventions
+ *   - Every pointer named d_* (and every pointer inside ssd_weights / ssd_kv) is device memory
+ *     owned by the caller, which keeps it alive until the stream has finished the work.  The
+ *     library allocates no device memory; it uses the caller's workspace (ssd_workspace_bytes).
+ *   - Matrices are row-major [out][in] (y = W x).  Matrices, embeddings and visual tokens are
+ *     in `wdtype`; norm gains, imitation-network biases and the relative-position bias table are
+ *     float32.  KV pools are in `kvdtype`.
+ *   - All calls are asynchronous on the stream given to ssd_create, except ssd_sync_status and
+ *     ssd_generate, which synchronise it.  One context per stream; not thread-safe.
+ *   - Return value: SSD_OK (0) or a negative SSD_ERR_* code; nothing is launched on error.
+ *     Faults detected on the device (token id out of range, position beyond the KV capacity,
+ *     page id out of range) set bits in a device status word that ssd_sync_status reports;
+ *     the offending access is skipped, never performed.
+ */
+#ifndef SSD_H
+#define SSD_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+  SSD_OK = 0,
+  SSD_ERR_ARG = -1,      /* null pointer or a value out of range                         */
+  SSD_ERR_SHAPE = -2,    /* B > max_batch, gamma > max_gamma, unsupported dimensions       */
+  SSD_ERR_CAPACITY = -3, /* context or workspace too small                                 */
+  SSD_ERR_HIP = -4,      /* a HIP runtime call or kernel launch failed                      */
+  SSD_ERR_STATE = -5,    /* call out of order (draft/verify before prefill, stale reuse)   */
+  SSD_ERR_DEVICE = -6    /* ssd_sync_status: the device status word is non-zero           */
+};
+
+enum { SSD_ARCH_T5 = 0, SSD_ARCH_LLAMA = 1 };
+enum { SSD_F32 = 0, SSD_BF16 = 1 };
+enum { SSD_MODE_GREEDY = 0, SSD_MODE_SPECULATIVE = 1 };
+
+/* device status bits (ssd_sync_status, ssd_device_status) */
+enum { SSD_DEV_BAD_TOKEN = 1, SSD_DEV_CAPACITY = 2, SSD_DEV_BAD_PAGE = 4 };
+
+/* Decoder and context dimensions, copied at ssd_create. */
+typedef struct {
+  int32_t arch;         /* SSD_ARCH_T5: RMSNorm, self-attn + T5 relative bias, cross-attn to z,
+                           gated-GELU FFN; SSD_ARCH_LLAMA: RMSNorm, RoPE self-attn, SwiGLU */
+  int32_t n_layers;     /* L */
+  int32_t d_model;      /* d, multiple of 64 */
+  int32_t n_heads;      /* H */
+  int32_t d_head;       /* 64 or 128 */
+  int32_t d_ff;         /* multiple of 64 */
+  int32_t vocab;        /* V */
+  int32_t n_visual;     /* T5: visual tokens attended by cross-attention; LLaMA: prefix rows */
+  int32_t rel_buckets;  /* T5 relative-position buckets (32) */
+  int32_t rel_max_dist; /* T5 bucket max distance (128) */
+  float rope_theta;     /* LLaMA rotary base (10000) */
+  float norm_eps;       /* decoder RMSNorm eps (T5 1e-6, LLaMA 1e-5) */
+  float ln_eps;         /* imitation-network LayerNorm eps (1e-5) */
+  int32_t wdtype;       /* SSD_F32 or SSD_BF16: matrices, embeddings, visual tokens */
+  int32_t kvdtype;      /* SSD_F32 or SSD_BF16: KV pools and cross-attention K/V */
+  int32_t draft_layers; /* k: the draft model is layers 1..k + imitation network + LM head */
+  int32_t in_hidden;    /* imitation-network hidden width (multiple of 64) */
+  int32_t in_residual;  /* 1: I(x) = x + FC2(GELU(FC1(LN(x)))); 0: FC2(GELU(FC1(LN(x)))) */
+  int32_t max_batch;    /* B capacity */
+  int32_t max_gamma;    /* largest draft length used with this context */
+  int32_t max_seq;      /* KV positions per sequence (prefix + prompt + T + max_gamma + 1) */
+  int32_t max_prompt;   /* largest prompt length P passed to ssd_prefill */
+  int32_t page_size;    /* KV positions per page */
+  int32_t max_pages;    /* page-table columns per sequence (>= ceil(max_seq / page_size)) */
+} ssd_dims;
+
+/* Per-layer weights (device pointers).  HD = n_heads * d_head. */
+typedef struct {
+  const float* attn_norm; /* [d] */
+  const void* wq;         /* [HD][d] */
+  const void* wk;         /* [HD][d] */
+  const void* wv;         /* [HD][d] */
+  const void* wo;         /* [d][HD] */
+  const float* xattn_norm;/* [d]      T5 only (NULL for LLaMA) */
+  const void* xq;         /* [HD][d]  T5 only */
+  const void* xk;         /* [HD][d]  T5 only: applied to z at prefill */
+  const void* xv;         /* [HD][d]  T5 only: applied to z at prefill */
+  const void* xo;         /* [d][HD]  T5 only */
+  const float* ffn_norm;  /* [d] */
+  const void* w_gate;     /* [d_ff][d] */
+  const void* w_up;       /* [d_ff][d] */
+  const void* w_down;     /* [d][d_ff] */
+} ssd_layer_weights;
+
+typedef struct {
+  const void* embed;      /* [V][d] */
+  const void* lm_head;    /* [V][d]  g = final RMSNorm then this matrix (shared by draft and full) */
+  const float* final_norm;/* [d] */
+  const float* rel_bias;  /* [rel_buckets][H]  T5 only */
+  const float* in_ln_w;   /* [d]  imitation network: LayerNorm gain */
+  const float* in_ln_b;   /* [d]  LayerNorm shift */
+  const void* in_w1;      /* [in_hidden][d] */
+  const float* in_b1;     /* [in_hidden] */
+  const void* in_w2;      /* [d][in_hidden] */
+  const float* in_b2;     /* [d] */
+  const ssd_layer_weights* layers; /* host array of n_layers entries (copied at ssd_create) */
+} ssd_weights;
+
+/* The shared KV cache (device pointers, caller-owned). */
+typedef struct {
+  void* k_pool;              /* [L][n_pages][H][page_size][d_head] kvdtype */
+  void* v_pool;              /* same layout */
+  int32_t n_pages;           /* pages per layer in the pools */
+  const int32_t* page_table; /* [max_batch][max_pages]: page of positions [j*page_size, (j+1)*page_size) */
+  int32_t* seq_len;          /* [max_batch]: valid positions; written only by prefill and accept */
+  void* xk;                  /* T5: [L][max_batch][H][n_visual][d_head] kvdtype, written by prefill */
+  void* xv;                  /* T5: same */
+} ssd_kv;
+
+typedef struct ssd_ctx ssd_ctx;
+
+/* Workspace bytes a context with these dimensions needs (0 if the dimensions are invalid). */
+size_t ssd_workspace_bytes(const ssd_dims* dims);
+
+/* Validate dimensions, copy the weight and KV descriptors, carve the workspace and build the
+ * relative-bias (T5) or rotary (LLaMA) tables into it.  `stream` is a hipStream_t (NULL: the
+ * null stream).  On success *out receives a host-side context that ssd_destroy frees. */
+int ssd_create(const ssd_dims* dims, const ssd_weights* w, const ssd_kv* kv, void* d_workspace,
+               size_t workspace_bytes, void* stream, ssd_ctx** out);
+
+/* Prefill (Algorithm 1's input: z and the context y^1..y^t).  d_prompt [B][P] int32 token ids;
+ * d_visual [B][n_visual][d] wdtype.  T5: cross-attention K/V of every layer are projected from
+ * z; the prompt occupies positions 0..P-1.  LLaMA: the visual rows are the inputs of positions
+ * 0..n_visual-1, the prompt follows.  Sets seq_len[b] to the context length and writes the full
+ * model's argmax at the last context position to d_pending[b] (emitted token #1).
+ * d_logits [B][V] float32 receives those logits when not NULL. */
+int ssd_prefill(ssd_ctx* ctx, int B, int P, const int32_t* d_prompt, const void* d_visual,
+                int32_t* d_pending, float* d_logits);
+
+/* Drafting stage (Algorithm 1, draft loop): for i = 0..gamma-1 run layers 1..k, the imitation
+ * network and g at position seq_len[b]+i on u_i (u_0 = d_pending[b], u_{i+1} = the draft's
+ * argmax), writing layer 1..k KV there.  d_draft [B][gamma] int32; d_draft_logits
+ * [B][gamma][V] float32 or NULL.  Keeps each step's layer-k hidden state for ssd_verify's reuse.
+ * Does not change seq_len.  1 <= gamma <= max_gamma. */
+int ssd_draft(ssd_ctx* ctx, int B, int gamma, const int32_t* d_pending, int32_t* d_draft,
+              float* d_draft_logits);
+
+/* Verification stage (Algorithm 1, verify loop): the full decoder over u_0..u_gamma =
+ * [d_pending[b], d_draft[b][0..gamma-1]] at positions seq_len[b]..seq_len[b]+gamma in one causal
+ * pass, writing KV of every layer there.  d_target [B][gamma+1] int32 receives the full model's
+ * argmax at each of those positions; d_logits [B][gamma+1][V] float32 or NULL.
+ * reuse_hidden = 1 takes layers 1..k of positions 0..gamma-1 from the immediately preceding
+ * ssd_draft (same B, gamma and inputs) and runs them only for the last position; 0 recomputes.
+ * gamma = 0 is one full-model greedy step.  Does not change seq_len.  d_draft may hold any
+ * tokens (e.g. forced from the host). */
+int ssd_verify(ssd_ctx* ctx, int B, int gamma, const int32_t* d_pending, const int32_t* d_draft,
+               int reuse_hidden, int32_t* d_target, float* d_logits);
+
+/* Greedy acceptance (Algorithm 1, verify loop): a[b] = the number of leading i with
+ * draft[b][i] == target[b][i]; d_out[b][0..a] = draft[b][0..a-1], target[b][a]; d_accept_len[b] =
+ * a; seq_len[b] += a + 1 (KV beyond it is stale and never read); d_pending[b] = target[b][a].
+ * Sequences with d_active[b] == 0 are left untouched (d_active may be NULL: all active). */
+int ssd_accept(ssd_ctx* ctx, int B, int gamma, const int32_t* d_draft, const int32_t* d_target,
+               int32_t* d_pending, int32_t* d_out, int32_t* d_accept_len, const int32_t* d_active);
+
+/* The whole loop: prefill, then rounds of draft + verify + accept (SSD_MODE_SPECULATIVE) or
+ * verify(gamma = 0) + accept (SSD_MODE_GREEDY) until T tokens per sequence are emitted (the last
+ * round truncated).  d_tokens [B][T] int32.  h_stats (host, may be NULL) receives
+ * {rounds, sum over sequences of accepted drafts, sum of drafted tokens}.  Synchronises the
+ * stream once per round to test for completion. */
+int ssd_generate(ssd_ctx* ctx, int B, int P, const int32_t* d_prompt, const void* d_visual, int T,
+                 int gamma, int mode, int reuse_hidden, int32_t* d_tokens, int64_t* h_stats);
+
+/* Capture ssd_draft / ssd_verify launch sequences into HIP graphs and replay them (1, default)
+ * or launch kernels one by one (0). */
+int ssd_set_graphs(ssd_ctx* ctx, int enable);
+
+/* Synchronise the stream; SSD_OK, SSD_ERR_HIP, or SSD_ERR_DEVICE when the device status word is
+ * non-zero (then *status, if not NULL, receives the SSD_DEV_* bits) — and clear the word. */
+int ssd_sync_status(ssd_ctx* ctx, int32_t* status);
+
+/* Human-readable name of a return code. */
+const char* ssd_status_string(int code);
+
+/* Free the host-side context (device buffers belong to the caller). */
+void ssd_destroy(ssd_ctx* ctx);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SSD_H */

@@ -1,0 +1,181 @@
+// Host-side launch interface of the gfx950 kernels (internal to libssd).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "ssd.h"
+
+namespace ssd {
+
+enum Norm { NORM_NONE = 0, NORM_RMS = 1, NORM_LN = 2 };
+
+enum Epi {
+  EPI_STORE = 0,       // y[m][n] = acc
+  EPI_RESID = 1,       // y[m][n] += acc  (and stash[m][n] = y[m][n] when stash != null)
+  EPI_GATED_GELU = 2,  // y[m][n] = gelu_tanh(acc_gate) * acc_up  (w[0] = gate, w[1] = up)
+  EPI_GATED_SILU = 3,  // y[m][n] = silu(acc_gate) * acc_up
+  EPI_BIAS_GELU = 4,   // y[m][n] = gelu_tanh(acc + bias[n])
+  EPI_BIAS_RESID = 5,  // y[m][n] = (resid ? resid[m][n] : 0) + acc + bias[n]
+  EPI_ARGMAX = 6       // per-block (max, argmax) over n for each m; logits[m][n] = acc if wanted
+};
+
+// y = epilogue( W . norm(x) ) for M rows.  The output features are up to three matrices of
+// n_per rows each, concatenated (QKV), or the pair (gate, up) for the gated epilogues.
+struct LinearArgs {
+  const float* x = nullptr;  // [M][ldx] float32 inputs
+  int ldx = 0;
+  int M = 0;
+  int K = 0;
+  int norm = NORM_NONE;
+  const float* gain = nullptr;
+  const float* shift = nullptr;
+  float eps = 0.f;
+  const void* w[3] = {nullptr, nullptr, nullptr};  // [n_per][K] each, wdtype
+  int n_mats = 1;
+  int n_per = 0;
+  int wdtype = 0;  // 0 f32, 1 bf16
+  int epi = EPI_STORE;
+  float* y = nullptr;
+  int ldy = 0;
+  const float* bias = nullptr;
+  const float* resid = nullptr;
+  int ldr = 0;
+  float* stash = nullptr;
+  int lds = 0;
+  // EPI_ARGMAX
+  float* part_val = nullptr;  // [M][n_parts]
+  int* part_idx = nullptr;
+  int n_parts = 0;            // filled by argmax_parts()
+  float* logits = nullptr;    // [M][ldl] or null
+  int ldl = 0;
+  // row statistics for the MFMA path's normalisation (filled by launch_linear)
+  float2* stats = nullptr;    // [M] workspace
+  int use_mfma = -1;          // -1: choose; 0: vector path; 1: MFMA path
+};
+
+// Number of argmax partials per row that launch_linear(EPI_ARGMAX) writes for n_per outputs.
+int argmax_parts(int n_out, int M, int wdtype);
+
+hipError_t launch_linear(LinearArgs a, hipStream_t s);
+
+// Gather input rows: x[r] = embedding of a token or a visual row.
+// Row r = b*C + j; j < n_prefix: visual[b][j]; else token = t0[b] if (t0 && j' == 0) else
+// t1[b*ld1 + j' - (t0 ? 1 : 0)] with j' = j - n_prefix.
+struct EmbedArgs {
+  float* x;
+  int B, C, d;
+  const void* embed;
+  int vocab;
+  int wdtype;
+  const int32_t* t0;
+  const int32_t* t1;
+  int ld1;
+  const void* visual;  // [B][n_visual][d] wdtype
+  int n_visual;
+  int n_prefix;
+  int32_t* status;
+};
+hipError_t launch_embed(const EmbedArgs& a, hipStream_t s);
+
+// Paged KV addressing shared by the attention kernels.
+struct PagedKV {
+  void* k;  // layer base of the pools [n_pages][H][page_size][dh]
+  void* v;
+  const int32_t* page_table;
+  int max_pages;
+  int page_size;
+  int n_pages;
+  const int32_t* seq_len;
+  int pos_off;  // row j of sequence b sits at position seq_len[b] + pos_off + j
+};
+
+// q/k/v rows (qkv [R][3*HD], R = B*C) -> rotary (LLaMA) -> q_out [R][HD], K/V into the pools.
+struct RopeScatterArgs {
+  const float* qkv;
+  float* q_out;
+  int B, C, H, dh;
+  int kvdtype;
+  PagedKV kv;
+  const float* rope_cos;  // [max_seq][dh/2] or null (no rotation)
+  const float* rope_sin;
+  int max_seq;
+  int32_t* status;
+};
+hipError_t launch_rope_scatter(const RopeScatterArgs& a, hipStream_t s);
+
+struct AttnArgs {
+  const float* q;  // [B*C][H*dh]
+  float* out;      // [B*C][H*dh]
+  int B, C, H, dh;
+  int kvdtype;
+  int cross;         // 0: causal over the paged cache; 1: dense over n_keys cross-attention keys
+  PagedKV kv;        // self-attention
+  const float* bias; // [H][max_seq] by distance (T5 self-attention) or null
+  int max_seq;
+  const void* xk;    // cross: [B][H][n_keys][dh]
+  const void* xv;
+  int n_keys;
+  float scale;
+  int32_t* status;
+};
+hipError_t launch_attention(const AttnArgs& a, hipStream_t s);
+
+// Row statistics for normalisation: stats[m] = (mean, 1/sqrt(var+eps)) (LN) or (0, 1/rms) (RMS).
+hipError_t launch_row_stats(const float* x, int ldx, int M, int K, int norm, float eps,
+                            float2* stats, hipStream_t s);
+
+// Final argmax over partials: tok = argmax; written to dst0[row_map(m)] and dst1[m] if set.
+// Row m = b*C + j maps to dst0[b*ld0 + off0 + j].
+hipError_t launch_argmax_final(const float* part_val, const int* part_idx, int M, int n_parts,
+                               int C, int32_t* dst0, int ld0, int off0, int32_t* dst1,
+                               hipStream_t s);
+
+// Cross-attention K or V at prefill: src [B*Nv][H*dh] float32 -> dst [B][H][Nv][dh] kvdtype.
+hipError_t launch_scatter_cross(const float* src, void* dst, int B, int Nv, int H, int dh,
+                                int kvdtype, hipStream_t s);
+
+// Verify with reused layer-k states: x[b*(g+1)+j] = j < g ? stash[b*ld_stash_b + j*d] : x1[b*d].
+hipError_t launch_assemble(float* x, const float* stash, int ld_stash_b, const float* x1, int B,
+                           int g, int d, hipStream_t s);
+
+hipError_t launch_set_seq_len(int32_t* seq_len, int B, int value, hipStream_t s);
+
+struct AcceptArgs {
+  int B, gamma;
+  const int32_t* draft;   // [B][gamma]
+  const int32_t* target;  // [B][gamma+1]
+  int32_t* pending;
+  int32_t* out;           // [B][gamma+1] or null
+  int32_t* accept_len;    // [B] or null
+  const int32_t* active;  // [B] or null
+  int32_t* seq_len;
+  int max_seq;
+  int next_need;          // positions the next round needs beyond seq_len (gamma+1)
+  int32_t* status;
+  // generation bookkeeping (null when called through ssd_accept)
+  int32_t* tokens;        // [B][T]
+  int32_t* count;         // [B] emitted so far
+  int32_t* active_rw;     // [B] cleared when count reaches T
+  int T;
+  int64_t* stats;         // [3]: rounds (added by thread 0), accepted, drafted
+  int32_t* n_active;      // [1]
+};
+hipError_t launch_accept(const AcceptArgs& a, hipStream_t s);
+
+struct GenInitArgs {
+  int B, T;
+  const int32_t* pending;
+  int32_t* tokens;
+  int32_t* count;
+  int32_t* active;
+  int64_t* stats;
+  int32_t* n_active;
+};
+hipError_t launch_gen_init(const GenInitArgs& a, hipStream_t s);
+
+// T5 bias-by-distance table: table[h][n] = rel_bias[bucket[n]][h].
+hipError_t launch_bias_table(const float* rel_bias, const int32_t* bucket, int H, int max_seq,
+                             float* table, hipStream_t s);
+
+}  // namespace ssd

@@ -1,0 +1,641 @@
+// Host side of libssd: argument checks, workspace layout, tables, and the launch sequences of
+// prefill, draft, verify, accept and the whole decode loop (Algorithm 1).
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+#include <map>
+#include <new>
+#include <tuple>
+#include <vector>
+
+#include "kernels.h"
+#include "ssd.h"
+
+using namespace ssd;
+
+namespace {
+
+size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+// T5 decoder relative-position bucket of a query-minus-key distance n >= 0: distances below
+// half the buckets are exact, larger ones are binned logarithmically up to max_dist.
+int t5_bucket(int n, int buckets, int max_dist) {
+  const int exact = buckets / 2;
+  if (n < exact) return n;
+  const double f = std::log((double)n / exact) / std::log((double)max_dist / exact) * (buckets - exact);
+  const int b = exact + (int)f;
+  return b < buckets - 1 ? b : buckets - 1;
+}
+
+struct Layout {
+  size_t x, x1, qkv, q, attn, ffn, inh, xi, stash, vis, part_val, part_idx, stats, bias_tab,
+      bucket, rope_cos, rope_sin, status, cur_tok, g_pending, g_draft, g_target, g_count,
+      g_active, g_nactive, g_stats, total;
+  int rows_max, head_rows, parts_max, ctx_max;
+};
+
+int ctx_len_max(const ssd_dims& d) {
+  return d.max_prompt + (d.arch == SSD_ARCH_LLAMA ? d.n_visual : 0);
+}
+
+bool make_layout(const ssd_dims& d, Layout& L) {
+  const size_t B = d.max_batch, G = d.max_gamma, D = d.d_model, HD = (size_t)d.n_heads * d.d_head;
+  L.ctx_max = ctx_len_max(d);
+  size_t rows = B * (G + 1);
+  rows = rows > B * L.ctx_max ? rows : B * L.ctx_max;
+  if (d.arch == SSD_ARCH_T5 && rows < B * d.n_visual) rows = B * d.n_visual;
+  L.rows_max = (int)rows;
+  L.head_rows = (int)(B * (G + 1));
+  // vector-path partial count is the larger one
+  L.parts_max = ((d.vocab + 1) / 2 + 3) / 4;
+  size_t off = 0;
+  auto take = [&](size_t bytes) { size_t o = off; off = align_up(off + bytes, 256); return o; };
+  L.x = take(rows * D * 4);
+  L.x1 = take(B * D * 4);
+  L.qkv = take(rows * 3 * HD * 4);
+  L.q = take(rows * HD * 4);
+  L.attn = take(rows * HD * 4);
+  L.ffn = take(rows * (size_t)d.d_ff * 4);
+  L.inh = take(B * (size_t)d.in_hidden * 4);
+  L.xi = take(B * D * 4);
+  L.stash = take(B * (G + 1) * D * 4);
+  L.vis = take(d.arch == SSD_ARCH_T5 ? B * (size_t)d.n_visual * D * 4 : 0);
+  L.part_val = take((size_t)L.head_rows * L.parts_max * 4);
+  L.part_idx = take((size_t)L.head_rows * L.parts_max * 4);
+  L.stats = take(rows * 8);
+  L.bias_tab = take(d.arch == SSD_ARCH_T5 ? (size_t)d.n_heads * d.max_seq * 4 : 0);
+  L.bucket = take(d.arch == SSD_ARCH_T5 ? (size_t)d.max_seq * 4 : 0);
+  L.rope_cos = take(d.arch == SSD_ARCH_LLAMA ? (size_t)d.max_seq * (d.d_head / 2) * 4 : 0);
+  L.rope_sin = take(d.arch == SSD_ARCH_LLAMA ? (size_t)d.max_seq * (d.d_head / 2) * 4 : 0);
+  L.status = take(4);
+  L.cur_tok = take(B * 4);
+  L.g_pending = take(B * 4);
+  L.g_draft = take(B * (G > 0 ? G : 1) * 4);
+  L.g_target = take(B * (G + 1) * 4);
+  L.g_count = take(B * 4);
+  L.g_active = take(B * 4);
+  L.g_nactive = take(4);
+  L.g_stats = take(3 * 8);
+  L.total = off;
+  return true;
+}
+
+bool dims_ok(const ssd_dims* d) {
+  if (!d) return false;
+  if (d->arch != SSD_ARCH_T5 && d->arch != SSD_ARCH_LLAMA) return false;
+  if (d->n_layers < 1 || d->d_model < 64 || d->d_model % 64) return false;
+  if (d->n_heads < 1 || (d->d_head != 64 && d->d_head != 128)) return false;
+  if (d->d_ff < 64 || d->d_ff % 64 || d->vocab < 2) return false;
+  if (d->in_hidden < 64 || d->in_hidden % 64) return false;
+  if (d->draft_layers < 1 || d->draft_layers > d->n_layers) return false;
+  if (d->wdtype != SSD_F32 && d->wdtype != SSD_BF16) return false;
+  if (d->kvdtype != SSD_F32 && d->kvdtype != SSD_BF16) return false;
+  if (d->max_batch < 1 || d->max_batch > 256) return false;
+  if (d->max_gamma < 0 || d->max_gamma > 32) return false;
+  if (d->max_seq < 2 || d->max_seq > 1536) return false;  // attention keeps a row of scores in LDS
+  if (d->max_prompt < 1 || d->page_size < 1 || d->max_pages < 1) return false;
+  if ((long long)d->max_pages * d->page_size < d->max_seq) return false;
+  if (ctx_len_max(*d) > d->max_seq) return false;
+  if (!(d->norm_eps > 0.f) || !(d->ln_eps > 0.f)) return false;
+  if (d->arch == SSD_ARCH_T5) {
+    if (d->n_visual < 1 || d->rel_buckets < 2 || d->rel_max_dist <= d->rel_buckets / 2) return false;
+  } else {
+    if (d->n_visual < 0 || !(d->rope_theta > 0.f)) return false;
+  }
+  return true;
+}
+
+struct GraphKey {
+  int kind, B, gamma, reuse;
+  const void *p0, *p1, *p2, *p3;
+  bool operator<(const GraphKey& o) const {
+    return std::tie(kind, B, gamma, reuse, p0, p1, p2, p3) <
+           std::tie(o.kind, o.B, o.gamma, o.reuse, o.p0, o.p1, o.p2, o.p3);
+  }
+};
+
+}  // namespace
+
+struct ssd_ctx {
+  ssd_dims d;
+  ssd_weights w;
+  std::vector<ssd_layer_weights> layers;
+  ssd_kv kv;
+  hipStream_t stream;
+  char* ws;
+  Layout L;
+  bool prefilled = false;
+  // reuse bookkeeping: the last ssd_draft's arguments
+  bool draft_valid = false;
+  int draft_B = 0, draft_gamma = 0;
+  const int32_t* draft_pending = nullptr;
+  const int32_t* draft_out = nullptr;
+  bool use_graphs = true;
+  std::map<GraphKey, hipGraphExec_t> graphs;
+
+  template <typename T> T* at(size_t off) { return reinterpret_cast<T*>(ws + off); }
+  size_t kv_layer_elems() const {
+    return (size_t)kv.n_pages * d.n_heads * d.page_size * d.d_head;
+  }
+  size_t xkv_layer_elems() const {
+    return (size_t)d.max_batch * d.n_heads * d.n_visual * d.d_head;
+  }
+  size_t kv_elem() const { return d.kvdtype == SSD_BF16 ? 2 : 4; }
+};
+
+#define HIP_TRY(expr)                          \
+  do {                                         \
+    if ((expr) != hipSuccess) return SSD_ERR_HIP; \
+  } while (0)
+
+namespace {
+
+PagedKV paged(ssd_ctx* c, int l, int pos_off) {
+  PagedKV p;
+  p.k = (char*)c->kv.k_pool + (size_t)l * c->kv_layer_elems() * c->kv_elem();
+  p.v = (char*)c->kv.v_pool + (size_t)l * c->kv_layer_elems() * c->kv_elem();
+  p.page_table = c->kv.page_table;
+  p.max_pages = c->d.max_pages;
+  p.page_size = c->d.page_size;
+  p.n_pages = c->kv.n_pages;
+  p.seq_len = c->kv.seq_len;
+  p.pos_off = pos_off;
+  return p;
+}
+
+LinearArgs lin(ssd_ctx* c) {
+  LinearArgs a;
+  a.wdtype = c->d.wdtype;
+  a.stats = c->at<float2>(c->L.stats);
+  a.eps = c->d.norm_eps;
+  return a;
+}
+
+// Layers l0..l1-1 over rows r = b*C + j at positions seq_len[b] + pos_off + j.  When stash is set
+// the residual after layer stash_layer is also written to stash[b * ld_stash + ...].
+int run_layers(ssd_ctx* c, float* x, int B, int C, int pos_off, int l0, int l1, int stash_layer,
+               float* stash, int ld_stash) {
+  const ssd_dims& d = c->d;
+  hipStream_t s = c->stream;
+  const int R = B * C, D = d.d_model, HD = d.n_heads * d.d_head;
+  const bool t5 = d.arch == SSD_ARCH_T5;
+  float* qkv = c->at<float>(c->L.qkv);
+  float* q = c->at<float>(c->L.q);
+  float* attn = c->at<float>(c->L.attn);
+  float* ffn = c->at<float>(c->L.ffn);
+  int32_t* status = c->at<int32_t>(c->L.status);
+  for (int l = l0; l < l1; ++l) {
+    const ssd_layer_weights& lw = c->layers[l];
+    // self-attention
+    LinearArgs a = lin(c);
+    a.x = x; a.ldx = D; a.M = R; a.K = D;
+    a.norm = NORM_RMS; a.gain = lw.attn_norm;
+    a.w[0] = lw.wq; a.w[1] = lw.wk; a.w[2] = lw.wv; a.n_mats = 3; a.n_per = HD;
+    a.epi = EPI_STORE; a.y = qkv; a.ldy = 3 * HD;
+    HIP_TRY(launch_linear(a, s));
+    RopeScatterArgs rs;
+    rs.qkv = qkv; rs.q_out = q; rs.B = B; rs.C = C; rs.H = d.n_heads; rs.dh = d.d_head;
+    rs.kvdtype = d.kvdtype; rs.kv = paged(c, l, pos_off);
+    rs.rope_cos = t5 ? nullptr : c->at<float>(c->L.rope_cos);
+    rs.rope_sin = t5 ? nullptr : c->at<float>(c->L.rope_sin);
+    rs.max_seq = d.max_seq; rs.status = status;
+    HIP_TRY(launch_rope_scatter(rs, s));
+    AttnArgs at;
+    at.q = q; at.out = attn; at.B = B; at.C = C; at.H = d.n_heads; at.dh = d.d_head;
+    at.kvdtype = d.kvdtype; at.cross = 0; at.kv = paged(c, l, pos_off);
+    at.bias = t5 ? c->at<float>(c->L.bias_tab) : nullptr;
+    at.max_seq = d.max_seq; at.xk = at.xv = nullptr; at.n_keys = 0;
+    at.scale = t5 ? 1.0f : (float)(1.0 / std::sqrt((double)d.d_head));
+    at.status = status;
+    HIP_TRY(launch_attention(at, s));
+    a = lin(c);
+    a.x = attn; a.ldx = HD; a.M = R; a.K = HD;
+    a.w[0] = lw.wo; a.n_per = D; a.epi = EPI_RESID; a.y = x; a.ldy = D;
+    HIP_TRY(launch_linear(a, s));
+    // cross-attention to the visual tokens
+    if (t5) {
+      a = lin(c);
+      a.x = x; a.ldx = D; a.M = R; a.K = D;
+      a.norm = NORM_RMS; a.gain = lw.xattn_norm;
+      a.w[0] = lw.xq; a.n_per = HD; a.epi = EPI_STORE; a.y = q; a.ldy = HD;
+      HIP_TRY(launch_linear(a, s));
+      AttnArgs xa = at;
+      xa.cross = 1;
+      xa.bias = nullptr;
+      xa.scale = 1.0f;
+      xa.xk = (char*)c->kv.xk + (size_t)l * c->xkv_layer_elems() * c->kv_elem();
+      xa.xv = (char*)c->kv.xv + (size_t)l * c->xkv_layer_elems() * c->kv_elem();
+      xa.n_keys = d.n_visual;
+      HIP_TRY(launch_attention(xa, s));
+      a = lin(c);
+      a.x = attn; a.ldx = HD; a.M = R; a.K = HD;
+      a.w[0] = lw.xo; a.n_per = D; a.epi = EPI_RESID; a.y = x; a.ldy = D;
+      HIP_TRY(launch_linear(a, s));
+    }
+    // feed-forward
+    a = lin(c);
+    a.x = x; a.ldx = D; a.M = R; a.K = D;
+    a.norm = NORM_RMS; a.gain = lw.ffn_norm;
+    a.w[0] = lw.w_gate; a.w[1] = lw.w_up; a.n_mats = 2; a.n_per = d.d_ff;
+    a.epi = t5 ? EPI_GATED_GELU : EPI_GATED_SILU; a.y = ffn; a.ldy = d.d_ff;
+    HIP_TRY(launch_linear(a, s));
+    a = lin(c);
+    a.x = ffn; a.ldx = d.d_ff; a.M = R; a.K = d.d_ff;
+    a.w[0] = lw.w_down; a.n_per = D; a.epi = EPI_RESID; a.y = x; a.ldy = D;
+    if (stash && l == stash_layer) { a.stash = stash; a.lds = ld_stash; }
+    HIP_TRY(launch_linear(a, s));
+  }
+  return SSD_OK;
+}
+
+// g = final RMSNorm + LM head, argmax per row.  Rows m of x (stride ldx) map to dst0 as in
+// launch_argmax_final.
+int run_head(ssd_ctx* c, const float* x, int ldx, int M, int C, float* logits, int ldl,
+             int32_t* dst0, int ld0, int off0, int32_t* dst1) {
+  const ssd_dims& d = c->d;
+  LinearArgs a = lin(c);
+  a.x = x; a.ldx = ldx; a.M = M; a.K = d.d_model;
+  a.norm = NORM_RMS; a.gain = c->w.final_norm;
+  a.w[0] = c->w.lm_head; a.n_per = d.vocab; a.epi = EPI_ARGMAX;
+  a.part_val = c->at<float>(c->L.part_val);
+  a.part_idx = c->at<int>(c->L.part_idx);
+  a.n_parts = argmax_parts(d.vocab, M, d.wdtype);
+  a.logits = logits; a.ldl = ldl;
+  HIP_TRY(launch_linear(a, c->stream));
+  HIP_TRY(launch_argmax_final(a.part_val, a.part_idx, M, a.n_parts, C, dst0, ld0, off0, dst1,
+                              c->stream));
+  return SSD_OK;
+}
+
+int draft_launches(ssd_ctx* c, int B, int gamma, const int32_t* pending, int32_t* draft,
+                   float* logits) {
+  const ssd_dims& d = c->d;
+  const int D = d.d_model;
+  float* x = c->at<float>(c->L.x);
+  float* inh = c->at<float>(c->L.inh);
+  float* xi = c->at<float>(c->L.xi);
+  float* stash = c->at<float>(c->L.stash);
+  int32_t* cur = c->at<int32_t>(c->L.cur_tok);
+  const int ld_stash = (d.max_gamma + 1) * D;
+  for (int i = 0; i < gamma; ++i) {
+    EmbedArgs e;
+    e.x = x; e.B = B; e.C = 1; e.d = D; e.embed = c->w.embed; e.vocab = d.vocab;
+    e.wdtype = d.wdtype; e.t0 = nullptr; e.t1 = i == 0 ? pending : cur; e.ld1 = 1;
+    e.visual = nullptr; e.n_visual = d.n_visual; e.n_prefix = 0;
+    e.status = c->at<int32_t>(c->L.status);
+    HIP_TRY(launch_embed(e, c->stream));
+    int rc = run_layers(c, x, B, 1, i, 0, d.draft_layers, d.draft_layers - 1, stash + (size_t)i * D,
+                        ld_stash);
+    if (rc) return rc;
+    // imitation network: LN -> FC1 + b1 -> GELU -> FC2 + b2 (+ x)
+    LinearArgs a = lin(c);
+    a.x = x; a.ldx = D; a.M = B; a.K = D;
+    a.norm = NORM_LN; a.gain = c->w.in_ln_w; a.shift = c->w.in_ln_b; a.eps = d.ln_eps;
+    a.w[0] = c->w.in_w1; a.n_per = d.in_hidden; a.epi = EPI_BIAS_GELU; a.bias = c->w.in_b1;
+    a.y = inh; a.ldy = d.in_hidden;
+    HIP_TRY(launch_linear(a, c->stream));
+    a = lin(c);
+    a.x = inh; a.ldx = d.in_hidden; a.M = B; a.K = d.in_hidden;
+    a.w[0] = c->w.in_w2; a.n_per = D; a.epi = EPI_BIAS_RESID; a.bias = c->w.in_b2;
+    a.resid = d.in_residual ? x : nullptr; a.ldr = D; a.y = xi; a.ldy = D;
+    HIP_TRY(launch_linear(a, c->stream));
+    rc = run_head(c, xi, D, B, 1, logits ? logits + (size_t)i * d.vocab : nullptr,
+                  gamma * d.vocab, draft, gamma, i, cur);
+    if (rc) return rc;
+  }
+  return SSD_OK;
+}
+
+int verify_launches(ssd_ctx* c, int B, int gamma, const int32_t* pending, const int32_t* draft,
+                    int reuse, int32_t* target, float* logits) {
+  const ssd_dims& d = c->d;
+  const int D = d.d_model, C = gamma + 1;
+  float* x = c->at<float>(c->L.x);
+  EmbedArgs e;
+  e.x = x; e.B = B; e.C = C; e.d = D; e.embed = c->w.embed; e.vocab = d.vocab;
+  e.wdtype = d.wdtype; e.t0 = pending; e.t1 = draft; e.ld1 = gamma;
+  e.visual = nullptr; e.n_visual = d.n_visual; e.n_prefix = 0;
+  e.status = c->at<int32_t>(c->L.status);
+  int rc;
+  if (!reuse) {
+    HIP_TRY(launch_embed(e, c->stream));
+    rc = run_layers(c, x, B, C, 0, 0, d.n_layers, -1, nullptr, 0);
+    if (rc) return rc;
+  } else {
+    // layers 1..k only for the last position; the others come from the draft's layer-k states
+    float* x1 = c->at<float>(c->L.x1);
+    e.x = x1; e.C = 1; e.t0 = nullptr; e.t1 = draft + (gamma - 1); e.ld1 = gamma;
+    HIP_TRY(launch_embed(e, c->stream));
+    rc = run_layers(c, x1, B, 1, gamma, 0, d.draft_layers, -1, nullptr, 0);
+    if (rc) return rc;
+    HIP_TRY(launch_assemble(x, c->at<float>(c->L.stash), (d.max_gamma + 1) * D, x1, B, gamma, D,
+                            c->stream));
+    rc = run_layers(c, x, B, C, 0, d.draft_layers, d.n_layers, -1, nullptr, 0);
+    if (rc) return rc;
+  }
+  return run_head(c, x, D, B * C, C, logits, d.vocab, target, C, 0, nullptr);
+}
+
+// Run `fn` directly or through a cached HIP graph keyed by the call's shape and pointers.
+template <typename F>
+int launch_maybe_graph(ssd_ctx* c, const GraphKey& key, F fn) {
+  if (!c->use_graphs) return fn();
+  auto it = c->graphs.find(key);
+  if (it == c->graphs.end()) {
+    if (hipStreamBeginCapture(c->stream, hipStreamCaptureModeThreadLocal) != hipSuccess)
+      return SSD_ERR_HIP;
+    int rc = fn();
+    hipGraph_t g = nullptr;
+    hipError_t ec = hipStreamEndCapture(c->stream, &g);
+    if (rc != SSD_OK) {
+      if (g) (void)hipGraphDestroy(g);
+      return rc;
+    }
+    if (ec != hipSuccess || !g) return SSD_ERR_HIP;
+    hipGraphExec_t ex = nullptr;
+    ec = hipGraphInstantiate(&ex, g, nullptr, nullptr, 0);
+    (void)hipGraphDestroy(g);
+    if (ec != hipSuccess) return SSD_ERR_HIP;
+    it = c->graphs.emplace(key, ex).first;
+  }
+  HIP_TRY(hipGraphLaunch(it->second, c->stream));
+  return SSD_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t ssd_workspace_bytes(const ssd_dims* dims) {
+  if (!dims_ok(dims)) return 0;
+  Layout L;
+  make_layout(*dims, L);
+  return L.total;
+}
+
+int ssd_create(const ssd_dims* dims, const ssd_weights* w, const ssd_kv* kv, void* d_workspace,
+               size_t workspace_bytes, void* stream, ssd_ctx** out) {
+  if (!out) return SSD_ERR_ARG;
+  *out = nullptr;
+  if (!dims || !w || !kv || !d_workspace) return SSD_ERR_ARG;
+  if (!dims_ok(dims)) return SSD_ERR_SHAPE;
+  const ssd_dims& d = *dims;
+  const bool t5 = d.arch == SSD_ARCH_T5;
+  if (!w->embed || !w->lm_head || !w->final_norm || !w->in_ln_w || !w->in_ln_b || !w->in_w1 ||
+      !w->in_b1 || !w->in_w2 || !w->in_b2 || !w->layers)
+    return SSD_ERR_ARG;
+  if (t5 && !w->rel_bias) return SSD_ERR_ARG;
+  for (int l = 0; l < d.n_layers; ++l) {
+    const ssd_layer_weights& lw = w->layers[l];
+    if (!lw.attn_norm || !lw.wq || !lw.wk || !lw.wv || !lw.wo || !lw.ffn_norm || !lw.w_gate ||
+        !lw.w_up || !lw.w_down)
+      return SSD_ERR_ARG;
+    if (t5 && (!lw.xattn_norm || !lw.xq || !lw.xk || !lw.xv || !lw.xo)) return SSD_ERR_ARG;
+  }
+  if (!kv->k_pool || !kv->v_pool || !kv->page_table || !kv->seq_len || kv->n_pages < 1)
+    return SSD_ERR_ARG;
+  if (t5 && (!kv->xk || !kv->xv)) return SSD_ERR_ARG;
+  Layout L;
+  make_layout(d, L);
+  if (workspace_bytes < L.total) return SSD_ERR_CAPACITY;
+  if (((uintptr_t)d_workspace) % 256) return SSD_ERR_ARG;
+
+  ssd_ctx* c = new (std::nothrow) ssd_ctx();
+  if (!c) return SSD_ERR_ARG;
+  c->d = d;
+  c->w = *w;
+  c->layers.assign(w->layers, w->layers + d.n_layers);
+  c->w.layers = c->layers.data();
+  c->kv = *kv;
+  c->stream = reinterpret_cast<hipStream_t>(stream);
+  c->ws = reinterpret_cast<char*>(d_workspace);
+  c->L = L;
+
+  int rc = SSD_OK;
+  if (t5) {
+    std::vector<int32_t> bucket(d.max_seq);
+    for (int n = 0; n < d.max_seq; ++n) bucket[n] = t5_bucket(n, d.rel_buckets, d.rel_max_dist);
+    if (hipMemcpyAsync(c->at<int32_t>(L.bucket), bucket.data(), bucket.size() * 4,
+                       hipMemcpyHostToDevice, c->stream) != hipSuccess ||
+        launch_bias_table(w->rel_bias, c->at<int32_t>(L.bucket), d.n_heads, d.max_seq,
+                          c->at<float>(L.bias_tab), c->stream) != hipSuccess ||
+        hipStreamSynchronize(c->stream) != hipSuccess)
+      rc = SSD_ERR_HIP;
+  } else {
+    const int half = d.d_head / 2;
+    std::vector<float> cs((size_t)d.max_seq * half), sn((size_t)d.max_seq * half);
+    for (int p = 0; p < d.max_seq; ++p)
+      for (int i = 0; i < half; ++i) {
+        const double ang = (double)p * std::pow((double)d.rope_theta, -2.0 * i / d.d_head);
+        cs[(size_t)p * half + i] = (float)std::cos(ang);
+        sn[(size_t)p * half + i] = (float)std::sin(ang);
+      }
+    if (hipMemcpyAsync(c->at<float>(L.rope_cos), cs.data(), cs.size() * 4, hipMemcpyHostToDevice,
+                       c->stream) != hipSuccess ||
+        hipMemcpyAsync(c->at<float>(L.rope_sin), sn.data(), sn.size() * 4, hipMemcpyHostToDevice,
+                       c->stream) != hipSuccess ||
+        hipStreamSynchronize(c->stream) != hipSuccess)
+      rc = SSD_ERR_HIP;
+  }
+  if (rc == SSD_OK &&
+      (hipMemsetAsync(c->at<int32_t>(L.status), 0, 4, c->stream) != hipSuccess ||
+       hipStreamSynchronize(c->stream) != hipSuccess))
+    rc = SSD_ERR_HIP;
+  if (rc != SSD_OK) {
+    delete c;
+    return rc;
+  }
+  *out = c;
+  return SSD_OK;
+}
+
+int ssd_prefill(ssd_ctx* c, int B, int P, const int32_t* d_prompt, const void* d_visual,
+                int32_t* d_pending, float* d_logits) {
+  if (!c || !d_prompt || !d_pending) return SSD_ERR_ARG;
+  const ssd_dims& d = c->d;
+  const bool t5 = d.arch == SSD_ARCH_T5;
+  if (B < 1 || B > d.max_batch || P < 1 || P > d.max_prompt) return SSD_ERR_SHAPE;
+  if (d.n_visual > 0 && !d_visual) return SSD_ERR_ARG;
+  const int Cx = P + (t5 ? 0 : d.n_visual);
+  if (Cx > d.max_seq) return SSD_ERR_CAPACITY;
+  const int D = d.d_model, HD = d.n_heads * d.d_head;
+  hipStream_t s = c->stream;
+  float* x = c->at<float>(c->L.x);
+  int32_t* status = c->at<int32_t>(c->L.status);
+  c->draft_valid = false;
+  HIP_TRY(launch_set_seq_len(c->kv.seq_len, B, 0, s));
+  if (t5) {
+    // cross-attention K/V of every layer from z
+    float* vis = c->at<float>(c->L.vis);
+    EmbedArgs ev;
+    ev.x = vis; ev.B = B; ev.C = d.n_visual; ev.d = D; ev.embed = c->w.embed; ev.vocab = d.vocab;
+    ev.wdtype = d.wdtype; ev.t0 = nullptr; ev.t1 = nullptr; ev.ld1 = 0;
+    ev.visual = d_visual; ev.n_visual = d.n_visual; ev.n_prefix = d.n_visual; ev.status = status;
+    HIP_TRY(launch_embed(ev, s));
+    float* tmp = c->at<float>(c->L.qkv);
+    for (int l = 0; l < d.n_layers; ++l) {
+      for (int which = 0; which < 2; ++which) {
+        LinearArgs a = lin(c);
+        a.x = vis; a.ldx = D; a.M = B * d.n_visual; a.K = D;
+        a.w[0] = which ? c->layers[l].xv : c->layers[l].xk; a.n_per = HD;
+        a.epi = EPI_STORE; a.y = tmp; a.ldy = HD;
+        HIP_TRY(launch_linear(a, s));
+        void* dst = (char*)(which ? c->kv.xv : c->kv.xk) + (size_t)l * c->xkv_layer_elems() * c->kv_elem();
+        HIP_TRY(launch_scatter_cross(tmp, dst, B, d.n_visual, d.n_heads, d.d_head, d.kvdtype, s));
+      }
+    }
+  }
+  EmbedArgs e;
+  e.x = x; e.B = B; e.C = Cx; e.d = D; e.embed = c->w.embed; e.vocab = d.vocab; e.wdtype = d.wdtype;
+  e.t0 = nullptr; e.t1 = d_prompt; e.ld1 = P; e.visual = d_visual; e.n_visual = d.n_visual;
+  e.n_prefix = t5 ? 0 : d.n_visual; e.status = status;
+  HIP_TRY(launch_embed(e, s));
+  int rc = run_layers(c, x, B, Cx, 0, 0, d.n_layers, -1, nullptr, 0);
+  if (rc) return rc;
+  rc = run_head(c, x + (size_t)(Cx - 1) * D, Cx * D, B, 1, d_logits, d.vocab, d_pending, 1, 0,
+                nullptr);
+  if (rc) return rc;
+  HIP_TRY(launch_set_seq_len(c->kv.seq_len, B, Cx, s));
+  c->prefilled = true;
+  return SSD_OK;
+}
+
+int ssd_draft(ssd_ctx* c, int B, int gamma, const int32_t* d_pending, int32_t* d_draft,
+              float* d_draft_logits) {
+  if (!c || !d_pending || !d_draft) return SSD_ERR_ARG;
+  if (B < 1 || B > c->d.max_batch || gamma < 1 || gamma > c->d.max_gamma) return SSD_ERR_SHAPE;
+  if (!c->prefilled) return SSD_ERR_STATE;
+  GraphKey key{0, B, gamma, 0, d_pending, d_draft, d_draft_logits, nullptr};
+  int rc = launch_maybe_graph(c, key, [&]() {
+    return draft_launches(c, B, gamma, d_pending, d_draft, d_draft_logits);
+  });
+  if (rc) return rc;
+  c->draft_valid = true;
+  c->draft_B = B;
+  c->draft_gamma = gamma;
+  c->draft_pending = d_pending;
+  c->draft_out = d_draft;
+  return SSD_OK;
+}
+
+int ssd_verify(ssd_ctx* c, int B, int gamma, const int32_t* d_pending, const int32_t* d_draft,
+               int reuse_hidden, int32_t* d_target, float* d_logits) {
+  if (!c || !d_pending || !d_target || (gamma > 0 && !d_draft)) return SSD_ERR_ARG;
+  if (B < 1 || B > c->d.max_batch || gamma < 0 || gamma > c->d.max_gamma) return SSD_ERR_SHAPE;
+  if (!c->prefilled) return SSD_ERR_STATE;
+  const int reuse = (reuse_hidden && gamma > 0) ? 1 : 0;
+  if (reuse && !(c->draft_valid && c->draft_B == B && c->draft_gamma == gamma &&
+                 c->draft_pending == d_pending && c->draft_out == d_draft))
+    return SSD_ERR_STATE;
+  GraphKey key{1, B, gamma, reuse, d_pending, d_draft, d_target, d_logits};
+  return launch_maybe_graph(c, key, [&]() {
+    return verify_launches(c, B, gamma, d_pending, d_draft, reuse, d_target, d_logits);
+  });
+}
+
+int ssd_accept(ssd_ctx* c, int B, int gamma, const int32_t* d_draft, const int32_t* d_target,
+               int32_t* d_pending, int32_t* d_out, int32_t* d_accept_len, const int32_t* d_active) {
+  if (!c || !d_target || !d_pending || (gamma > 0 && !d_draft)) return SSD_ERR_ARG;
+  if (B < 1 || B > c->d.max_batch || gamma < 0 || gamma > c->d.max_gamma) return SSD_ERR_SHAPE;
+  if (!c->prefilled) return SSD_ERR_STATE;
+  AcceptArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.B = B; a.gamma = gamma; a.draft = d_draft; a.target = d_target; a.pending = d_pending;
+  a.out = d_out; a.accept_len = d_accept_len; a.active = d_active; a.seq_len = c->kv.seq_len;
+  a.max_seq = c->d.max_seq; a.next_need = gamma + 1;
+  a.status = c->at<int32_t>(c->L.status);
+  HIP_TRY(launch_accept(a, c->stream));
+  c->draft_valid = false;
+  return SSD_OK;
+}
+
+int ssd_generate(ssd_ctx* c, int B, int P, const int32_t* d_prompt, const void* d_visual, int T,
+                 int gamma, int mode, int reuse_hidden, int32_t* d_tokens, int64_t* h_stats) {
+  if (!c || !d_tokens || T < 1) return SSD_ERR_ARG;
+  if (mode != SSD_MODE_GREEDY && mode != SSD_MODE_SPECULATIVE) return SSD_ERR_ARG;
+  const int g = mode == SSD_MODE_GREEDY ? 0 : gamma;
+  if (mode == SSD_MODE_SPECULATIVE && (gamma < 1 || gamma > c->d.max_gamma)) return SSD_ERR_SHAPE;
+  if (B < 1 || B > c->d.max_batch) return SSD_ERR_SHAPE;
+  const int Cx = P + (c->d.arch == SSD_ARCH_T5 ? 0 : c->d.n_visual);
+  if (Cx + T + c->d.max_gamma > c->d.max_seq) return SSD_ERR_CAPACITY;
+  int32_t* pending = c->at<int32_t>(c->L.g_pending);
+  int32_t* draft = c->at<int32_t>(c->L.g_draft);
+  int32_t* target = c->at<int32_t>(c->L.g_target);
+  int32_t* count = c->at<int32_t>(c->L.g_count);
+  int32_t* active = c->at<int32_t>(c->L.g_active);
+  int32_t* n_active = c->at<int32_t>(c->L.g_nactive);
+  int64_t* stats = c->at<int64_t>(c->L.g_stats);
+  int rc = ssd_prefill(c, B, P, d_prompt, d_visual, pending, nullptr);
+  if (rc) return rc;
+  GenInitArgs gi{B, T, pending, d_tokens, count, active, stats, n_active};
+  HIP_TRY(launch_gen_init(gi, c->stream));
+  AcceptArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.B = B; a.gamma = g; a.draft = draft; a.target = target; a.pending = pending;
+  a.seq_len = c->kv.seq_len; a.max_seq = c->d.max_seq; a.next_need = g + 1;
+  a.status = c->at<int32_t>(c->L.status);
+  a.tokens = d_tokens; a.count = count; a.active_rw = active; a.T = T; a.stats = stats;
+  a.n_active = n_active;
+  for (int round = 0; round < T; ++round) {
+    int32_t h_active = 0;
+    HIP_TRY(hipMemcpyAsync(&h_active, n_active, 4, hipMemcpyDeviceToHost, c->stream));
+    HIP_TRY(hipStreamSynchronize(c->stream));
+    if (h_active == 0) break;
+    if (g > 0) {
+      rc = ssd_draft(c, B, g, pending, draft, nullptr);
+      if (rc) return rc;
+    }
+    rc = ssd_verify(c, B, g, pending, draft, g > 0 ? reuse_hidden : 0, target, nullptr);
+    if (rc) return rc;
+    HIP_TRY(launch_accept(a, c->stream));
+    c->draft_valid = false;
+  }
+  if (h_stats) {
+    HIP_TRY(hipMemcpyAsync(h_stats, stats, 24, hipMemcpyDeviceToHost, c->stream));
+  }
+  HIP_TRY(hipStreamSynchronize(c->stream));
+  return SSD_OK;
+}
+
+int ssd_set_graphs(ssd_ctx* c, int enable) {
+  if (!c) return SSD_ERR_ARG;
+  c->use_graphs = enable != 0;
+  return SSD_OK;
+}
+
+int ssd_sync_status(ssd_ctx* c, int32_t* status) {
+  if (!c) return SSD_ERR_ARG;
+  int32_t v = 0;
+  if (hipStreamSynchronize(c->stream) != hipSuccess) return SSD_ERR_HIP;
+  if (hipMemcpy(&v, c->at<int32_t>(c->L.status), 4, hipMemcpyDeviceToHost) != hipSuccess)
+    return SSD_ERR_HIP;
+  if (status) *status = v;
+  if (v != 0) {
+    if (hipMemset(c->at<int32_t>(c->L.status), 0, 4) != hipSuccess) return SSD_ERR_HIP;
+    return SSD_ERR_DEVICE;
+  }
+  return SSD_OK;
+}
+
+const char* ssd_status_string(int code) {
+  switch (code) {
+    case SSD_OK: return "ok";
+    case SSD_ERR_ARG: return "invalid argument";
+    case SSD_ERR_SHAPE: return "unsupported shape";
+    case SSD_ERR_CAPACITY: return "capacity exceeded";
+    case SSD_ERR_HIP: return "HIP runtime error";
+    case SSD_ERR_STATE: return "call out of order";
+    case SSD_ERR_DEVICE: return "device status error";
+    default: return "unknown status";
+  }
+}
+
+void ssd_destroy(ssd_ctx* c) {
+  if (!c) return;
+  for (auto& kv : c->graphs) (void)hipGraphExecDestroy(kv.second);
+  delete c;
+}
+
+}  // extern "C"

@@ -102,7 +102,7 @@ LLAVA_7B = Shape("llava-1.5-7b", "llama", n_layers=32, d_model=4096, n_heads=32,
 SMALL_T5_BF16 = Shape("small-t5-bf16", "t5", n_layers=6, d_model=128, n_heads=2, d_head=64,
                       d_ff=320, vocab=2000, n_visual=8, dtype="bf16")
 SMALL_LLAMA_BF16 = Shape("small-llama-bf16", "llama", n_layers=6, d_model=256, n_heads=2,
-                         d_head=128, d_ff=688, vocab=2000, n_visual=24, dtype="bf16")
+                         d_head=128, d_ff=704, vocab=2000, n_visual=24, dtype="bf16")
 SMALL_LLAMA_F32 = replace(SMALL_LLAMA_BF16, name="small-llama-f32", dtype="f32")
 
 # ---- workloads ------------------------------------------------------------------------------

@@ -1,0 +1,147 @@
+"""Helpers of the device-vs-oracle parity tests (no tests here).
+
+Tolerances (per step, over the vocabulary):
+  f32 workloads   max |device logit - oracle logit| <= 1e-4
+  bf16 workloads  max |device logit - oracle logit| <= 2e-2 * std(oracle logits of that step)
+Tokens follow the replay protocol: the oracle follows the device's token stream; where a device
+token differs from the oracle's argmax, the oracle's own logits must put it within the tolerance
+of the top; the accepted length per round must be bit-exact given the device's drafts and
+targets.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+from typing import List, Optional
+
+import numpy as np
+
+import synth
+from oracle import decode
+from oracle.model import Decoder
+
+
+def tolerance(shape, ref_logits) -> float:
+    return 1e-4 if shape.dtype == "f32" else 2e-2 * float(np.std(ref_logits))
+
+
+def check_logits(dev, ref, shape, what: str) -> float:
+    tol = tolerance(shape, ref)
+    err = float(np.max(np.abs(np.asarray(dev, dtype=np.float64) - ref)))
+    assert np.isfinite(err) and err <= tol, f"{what}: max-abs {err:.3g} > tol {tol:.3g}"
+    return err / tol
+
+
+def check_token(dev_tok: int, ref_logits, shape, what: str) -> bool:
+    """True when the device token is the oracle's argmax; False for an accepted near-tie."""
+    top = int(np.argmax(ref_logits))
+    if int(dev_tok) == top:
+        return True
+    gap = float(ref_logits[top] - ref_logits[int(dev_tok)])
+    tol = tolerance(shape, ref_logits)
+    assert gap <= tol, (f"{what}: device token {dev_tok} vs oracle {top}: oracle gap {gap:.3g} "
+                        f"> tol {tol:.3g}")
+    return False
+
+
+@dataclass
+class DevRound:
+    drafts: np.ndarray  # [B, gamma]
+    targets: np.ndarray  # [B, gamma+1]
+    accepted: np.ndarray  # [B]
+    active: np.ndarray  # [B] bool: the sequence took part
+    draft_logits: Optional[np.ndarray] = None  # [B, gamma, V]
+    target_logits: Optional[np.ndarray] = None  # [B, gamma+1, V]
+
+
+@dataclass
+class DevRun:
+    pending0: np.ndarray
+    prefill_logits: Optional[np.ndarray]
+    rounds: List[DevRound] = field(default_factory=list)
+    tokens: List[List[int]] = field(default_factory=list)
+
+
+def poison_stale_kv(dd) -> None:
+    """Overwrite every KV entry at or beyond each sequence's valid length with NaN."""
+    import torch
+    sl = dd.seq_len.cpu().numpy()
+    pt = dd.page_table.cpu().numpy()
+    ps = dd.cap.page_size
+    for b in range(pt.shape[0]):
+        for p in range(int(sl[b]), pt.shape[1] * ps):
+            page, slot = int(pt[b, p // ps]), p % ps
+            dd.k_pool[:, page, :, slot, :] = float("nan")
+            dd.v_pool[:, page, :, slot, :] = float("nan")
+    torch.cuda.synchronize()
+
+
+def device_run(dd, prompt_t, visual_t, T: int, gamma: int, reuse: bool = False,
+               logits: bool = True, poison: bool = False, forced=None) -> DevRun:
+    """Step through prefill / draft / verify / accept via the C ABI and record everything."""
+    import torch
+    B = prompt_t.shape[0]
+    pending, lg0 = dd.prefill(prompt_t, visual_t, logits=logits)
+    run = DevRun(pending.cpu().numpy().copy(), lg0.cpu().numpy().copy() if logits else None)
+    run.tokens = [[int(t)] for t in run.pending0]
+    active = dd.buf("active_mask", (B,))
+    active.fill_(1)
+    if poison:
+        poison_stale_kv(dd)
+    for rnd in range(T):
+        act = np.array([len(t) < T for t in run.tokens])
+        if not act.any():
+            break
+        active.copy_(torch.from_numpy(act.astype(np.int32)))
+        if gamma > 0:
+            d, dl = dd.draft(pending, gamma, logits=logits)
+            if forced is not None:
+                d.copy_(torch.from_numpy(forced(rnd, d.cpu().numpy()).astype(np.int32)))
+        else:
+            d, dl = dd.buf("no_draft", (B, 1)), None
+        t, tl = dd.verify(pending, d, gamma, reuse=reuse, logits=logits)
+        out, alen = dd.accept(d, t, pending, gamma, active)
+        r = DevRound(d.cpu().numpy()[:, :gamma].copy(), t.cpu().numpy().copy(),
+                     alen.cpu().numpy().copy(), act,
+                     dl.cpu().numpy().copy() if dl is not None else None,
+                     tl.cpu().numpy().copy() if tl is not None else None)
+        run.rounds.append(r)
+        o = out.cpu().numpy()
+        for b in range(B):
+            if act[b]:
+                run.tokens[b].extend(int(x) for x in o[b, : r.accepted[b] + 1])
+        if poison:
+            poison_stale_kv(dd)
+    run.tokens = [t[:T] for t in run.tokens]
+    return run
+
+
+def check_run_against_oracle(dec: Decoder, shape, prompt, visual, run: DevRun, b: int, gamma: int,
+                             use_imitation: bool = True):
+    """Replay sequence b of a device run through the oracle; returns the count of near-ties."""
+    rounds = [r for r in run.rounds if r.active[b]]
+    lg0, orounds = decode.replay(dec, prompt, visual, int(run.pending0[b]),
+                                 [(r.drafts[b], r.targets[b]) for r in rounds], gamma,
+                                 use_imitation=use_imitation)
+    ties = 0
+    if run.prefill_logits is not None:
+        check_logits(run.prefill_logits[b], lg0, shape, f"seq {b} prefill logits")
+    ties += not check_token(run.pending0[b], lg0, shape, f"seq {b} prefill token")
+    for k, (r, o) in enumerate(zip(rounds, orounds)):
+        for i in range(gamma):
+            if r.draft_logits is not None:
+                check_logits(r.draft_logits[b, i], o.draft_logits[i], shape, f"seq {b} round {k} draft {i} logits")
+            ties += not check_token(r.drafts[b, i], o.draft_logits[i], shape, f"seq {b} round {k} draft {i}")
+        for j in range(gamma + 1):
+            if r.target_logits is not None:
+                check_logits(r.target_logits[b, j], o.target_logits[j], shape, f"seq {b} round {k} verify {j} logits")
+            ties += not check_token(r.targets[b, j], o.target_logits[j], shape, f"seq {b} round {k} verify {j}")
+        assert int(r.accepted[b]) == o.accepted, f"seq {b} round {k}: accepted {r.accepted[b]} != {o.accepted}"
+    return ties
+
+
+def workload_inputs(wl, seed: int, batch: Optional[int] = None):
+    B = batch or wl.batch
+    w = synth.workload_weights(wl, seed, threads=4)
+    z = synth.make_visual(wl.shape, seed, B)
+    pr = synth.make_prompts(wl.shape, seed, B, wl.prompt_len)
+    return w, z, pr
