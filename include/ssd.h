@@ -188,6 +188,15 @@ int ssd_generate(ssd_ctx* ctx, int B, int P, const int32_t* d_prompt, const void
  * or launch kernels one by one (0). */
 int ssd_set_graphs(ssd_ctx* ctx, int enable);
 
+/* Kernel timing for roofline reports.  While enabled (and graphs are bypassed), every launch of
+ * the weight-streaming GEMV with one input row — the kernel that carries the batch-1 draft steps —
+ * is bracketed by two HIP events on the context's stream, and its algorithmic bytes (weights +
+ * input rows + output rows) are added up.  ssd_profile_read synchronises the stream and returns
+ * the number of such launches, the summed event time in seconds and the summed bytes since the
+ * previous read (any pointer may be NULL).  Costs one event pair per launch; for measurement only. */
+int ssd_profile_enable(ssd_ctx* ctx, int enable);
+int ssd_profile_read(ssd_ctx* ctx, int64_t* launches, double* seconds, double* bytes);
+
 /* Synchronise the stream; SSD_OK, SSD_ERR_HIP, or SSD_ERR_DEVICE when the device status word is
  * non-zero (then *status, if not NULL, receives the SSD_DEV_* bits) — and clear the word. */
 int ssd_sync_status(ssd_ctx* ctx, int32_t* status);

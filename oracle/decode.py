@@ -107,12 +107,14 @@ def _poison(st: State) -> None:
 
 def ssd(dec: Decoder, prompt, visual, T: int, gamma: int, capacity: Optional[int] = None,
         draft_policy: Optional[Callable[[int, int, np.ndarray], int]] = None,
-        poison: bool = False, use_imitation: bool = True, eos_id: int = -1) -> Run:
+        poison: bool = False, use_imitation: bool = True, eos_id: int = -1,
+        max_rounds: Optional[int] = None) -> Run:
     """Algorithm 1: draft gamma tokens with layers 1..k + I + g, verify them with the full decoder,
     keep the longest matching prefix plus the full model's token at the first mismatch.
 
     ``draft_policy(round, i, logits) -> token`` replaces the draft's argmax (host-forced drafts);
-    ``poison`` overwrites every KV entry beyond the valid length with NaN after each acceptance.
+    ``poison`` overwrites every KV entry beyond the valid length with NaN after each acceptance;
+    ``max_rounds`` stops early (a bounded sample of the loop, for timing).
     """
     if gamma < 0:
         raise ValueError("gamma must be >= 0")
@@ -121,6 +123,8 @@ def ssd(dec: Decoder, prompt, visual, T: int, gamma: int, capacity: Optional[int
     run = Run(tokens=[y], prefill_logits=lg)
     done = (y == eos_id)
     while len(run.tokens) < T and not done:
+        if max_rounds is not None and len(run.rounds) >= max_rounds:
+            break
         l = st.seq_len
         # drafting stage: u_0 = pending, u_{i+1} = draft's argmax at position l+i
         u = [y]

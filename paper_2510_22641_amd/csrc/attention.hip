@@ -6,9 +6,11 @@
 // for LLaMA, scaled by 1/sqrt(dh) with q and k already rotated.  Cross-attention (T5): all n_keys
 // visual keys, no mask, no bias, no scale.
 //
-// One block per (head, sequence, 8 query rows): scores for the 8 rows over all keys go to LDS,
-// one wave per row normalises them, and each wave accumulates P.V for two rows with one lane per
-// head dimension (coalesced 128-byte value rows).  Bound: bytes of K and V read (HBM/L2).
+// One block per (head, sequence, up to 8 query rows).  Every thread issues its key row and its
+// first value chunks before the first barrier (they do not depend on the scores); scores for the
+// live rows go to LDS, one wave per row turns them into softmax numerators, and P.V splits the
+// keys over all threads (16-byte value chunks, 8 loads in flight per thread) with a shuffle + LDS
+// reduction.  Bound: bytes of K and V read (HBM/L2) and one or two memory round trips.
 #include "device.h"
 #include "kernels.h"
 
@@ -34,10 +36,15 @@ __device__ __forceinline__ const KT* key_row(const AttnArgs& a, const KT* base, 
   return base + (((size_t)page * a.H + h) * a.kv.page_size + slot) * DH;
 }
 
-template <typename KT, int DH>
+template <typename KT, int DH, int QB>
 __global__ __launch_bounds__(256) void attn_kernel(const AttnArgs a, const int s_stride) {
-  extern __shared__ float S[];  // [QB][s_stride]
+  constexpr int CH = DH / 8;       // 16-byte chunks per key row (bf16) / 8-element groups
+  constexpr int KPI = 256 / CH;    // keys per block step in P.V
+  constexpr int KPW = 64 / CH;     // keys per wave step in P.V
+  constexpr int PF = 8;            // P.V loads in flight per thread
+  extern __shared__ float S[];     // [QB][s_stride] scores, then unnormalised probabilities
   __shared__ float qs[QB][DH];
+  __shared__ float red[4][QB][DH];
   __shared__ float inv_sum[QB];
 
   const int h = blockIdx.x, b = blockIdx.y, j0 = blockIdx.z * QB;
@@ -53,51 +60,80 @@ __global__ __launch_bounds__(256) void attn_kernel(const AttnArgs a, const int s
   const KT* Kb = reinterpret_cast<const KT*>(a.cross ? a.xk : a.kv.k);
   const KT* Vb = reinterpret_cast<const KT*>(a.cross ? a.xv : a.kv.v);
 
+  // issue the first key row and the first value chunks before any barrier
+  bool kok = false;
+  Vec8<KT> krow[CH];
+  if (tid < nk) {
+    const KT* kp = key_row<KT, DH>(a, Kb, b, h, tid, kok);
+    if (kok) {
+#pragma unroll
+      for (int c = 0; c < CH; ++c) krow[c].load(kp + 8 * c);
+    }
+  }
+  const int vc = tid % CH, vk0 = tid / CH;
+  Vec8<KT> vpre[PF];
+  bool vok[PF];
+#pragma unroll
+  for (int u = 0; u < PF; ++u) {
+    const int i = vk0 + KPI * u;
+    vok[u] = false;
+    if (i < nk) {
+      const KT* vp = key_row<KT, DH>(a, Vb, b, h, i, vok[u]);
+      if (vok[u]) vpre[u].load(vp + 8 * vc);
+    }
+  }
+
   for (int idx = tid; idx < QB * DH; idx += 256) {
     const int jq = idx / DH, d = idx - jq * DH;
     qs[jq][d] = jq < nq ? a.q[(size_t)(b * a.C + j0 + jq) * HD + h * DH + d] * a.scale : 0.f;
   }
   __syncthreads();
 
-  // scores
+  // scores: one key per thread per step
   for (int i = tid; i < nk; i += 256) {
-    bool ok;
-    const KT* kp = key_row<KT, DH>(a, Kb, b, h, i, ok);
+    bool ok = kok;
+    if (i != tid) {
+      const KT* kp = key_row<KT, DH>(a, Kb, b, h, i, ok);
+      if (ok) {
+#pragma unroll
+        for (int c = 0; c < CH; ++c) krow[c].load(kp + 8 * c);
+      }
+    }
     float dots[QB];
 #pragma unroll
     for (int jq = 0; jq < QB; ++jq) dots[jq] = 0.f;
     if (ok) {
 #pragma unroll
-      for (int dc = 0; dc < DH; dc += 8) {
-        Vec8<KT> kv;
-        kv.load(kp + dc);
+      for (int c = 0; c < CH; ++c) {
         float kf[8];
-        kv.to_f32(kf);
+        krow[c].to_f32(kf);
 #pragma unroll
         for (int jq = 0; jq < QB; ++jq) {
-          float t = dots[jq];
+          if (jq < nq) {
+            float t = dots[jq];
 #pragma unroll
-          for (int e = 0; e < 8; ++e) t = fmaf(qs[jq][dc + e], kf[e], t);
-          dots[jq] = t;
+            for (int e = 0; e < 8; ++e) t = fmaf(qs[jq][8 * c + e], kf[e], t);
+            dots[jq] = t;
+          }
         }
       }
     }
 #pragma unroll
     for (int jq = 0; jq < QB; ++jq) {
-      float s = dots[jq];
+      float sc = dots[jq];
       if (!ok || jq >= nq) {
-        s = -INFINITY;
+        sc = -INFINITY;
       } else if (!a.cross) {
         const int p = base + j0 + jq;
-        if (i > p) s = -INFINITY;
-        else if (a.bias && p - i < a.max_seq) s += a.bias[(size_t)h * a.max_seq + (p - i)];
+        if (i > p) sc = -INFINITY;
+        else if (a.bias && p - i < a.max_seq) sc += a.bias[(size_t)h * a.max_seq + (p - i)];
       }
-      S[jq * s_stride + i] = s;
+      S[jq * s_stride + i] = sc;
     }
   }
   __syncthreads();
 
-  // softmax, one wave per row
+  // softmax numerators, one wave per row
   for (int jq = wave; jq < nq; jq += 4) {
     float* row = S + jq * s_stride;
     float m = -INFINITY;
@@ -114,73 +150,84 @@ __global__ __launch_bounds__(256) void attn_kernel(const AttnArgs a, const int s
   }
   __syncthreads();
 
-  // P . V: wave w handles rows w and w + 4, lane handles dims lane + 64 t
-  constexpr int DT = DH / 64;
-  float acc[2][DT];
+  // P . V: thread (key group vk0, chunk vc) accumulates 8 dims of every query row
+  float acc[QB][8];
 #pragma unroll
-  for (int r = 0; r < 2; ++r)
+  for (int jq = 0; jq < QB; ++jq)
 #pragma unroll
-    for (int t = 0; t < DT; ++t) acc[r][t] = 0.f;
-  const int r0 = wave, r1 = wave + 4;
-  const float* P0 = S + r0 * s_stride;
-  const float* P1 = S + r1 * s_stride;
-  const bool has0 = r0 < nq, has1 = r1 < nq;
-  int i = 0;
-  for (; i + 4 <= nk; i += 4) {
-    float vv[4][DT];
-    bool okk[4];
+    for (int e = 0; e < 8; ++e) acc[jq][e] = 0.f;
+  for (int u0 = 0; vk0 + KPI * u0 < nk; u0 += PF) {
+    if (u0 > 0) {
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const KT* vp = key_row<KT, DH>(a, Vb, b, h, i + u, okk[u]);
-#pragma unroll
-      for (int t = 0; t < DT; ++t) vv[u][t] = okk[u] ? load_elem(vp + lane + 64 * t) : 0.f;
+      for (int u = 0; u < PF; ++u) {
+        const int i = vk0 + KPI * (u0 + u);
+        vok[u] = false;
+        if (i < nk) {
+          const KT* vp = key_row<KT, DH>(a, Vb, b, h, i, vok[u]);
+          if (vok[u]) vpre[u].load(vp + 8 * vc);
+        }
+      }
     }
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const float p0 = has0 ? P0[i + u] : 0.f;
-      const float p1 = has1 ? P1[i + u] : 0.f;
+    for (int u = 0; u < PF; ++u) {
+      const int i = vk0 + KPI * (u0 + u);
+      if (i < nk && vok[u]) {
+        float vf[8];
+        vpre[u].to_f32(vf);
 #pragma unroll
-      for (int t = 0; t < DT; ++t) {
-        acc[0][t] = fmaf(p0, vv[u][t], acc[0][t]);
-        acc[1][t] = fmaf(p1, vv[u][t], acc[1][t]);
+        for (int jq = 0; jq < QB; ++jq) {
+          if (jq < nq) {
+            const float p = S[jq * s_stride + i];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) acc[jq][e] = fmaf(p, vf[e], acc[jq][e]);
+          }
+        }
       }
     }
   }
-  for (; i < nk; ++i) {
-    bool ok;
-    const KT* vp = key_row<KT, DH>(a, Vb, b, h, i, ok);
-    const float p0 = has0 ? P0[i] : 0.f;
-    const float p1 = has1 ? P1[i] : 0.f;
+  // reduce over the key groups of the wave (lanes that share vc), then over waves
 #pragma unroll
-    for (int t = 0; t < DT; ++t) {
-      const float v = ok ? load_elem(vp + lane + 64 * t) : 0.f;
-      acc[0][t] = fmaf(p0, v, acc[0][t]);
-      acc[1][t] = fmaf(p1, v, acc[1][t]);
+  for (int jq = 0; jq < QB; ++jq)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      float v = acc[jq][e];
+#pragma unroll
+      for (int o = CH; o < 64; o <<= 1) v += __shfl_xor(v, o, SSD_WAVE);
+      acc[jq][e] = v;
     }
-  }
-  if (has0) {
-    const float s = inv_sum[r0];
-    float* o = a.out + (size_t)(b * a.C + j0 + r0) * HD + h * DH;
+  if (lane < CH) {
 #pragma unroll
-    for (int t = 0; t < DT; ++t) o[lane + 64 * t] = acc[0][t] * s;
-  }
-  if (has1) {
-    const float s = inv_sum[r1];
-    float* o = a.out + (size_t)(b * a.C + j0 + r1) * HD + h * DH;
+    for (int jq = 0; jq < QB; ++jq)
 #pragma unroll
-    for (int t = 0; t < DT; ++t) o[lane + 64 * t] = acc[1][t] * s;
+      for (int e = 0; e < 8; ++e) red[wave][jq][8 * lane + e] = acc[jq][e];
   }
+  __syncthreads();
+  for (int idx = tid; idx < nq * DH; idx += 256) {
+    const int jq = idx / DH, d = idx - jq * DH;
+    const float v = (red[0][jq][d] + red[1][jq][d]) + (red[2][jq][d] + red[3][jq][d]);
+    a.out[(size_t)(b * a.C + j0 + jq) * HD + h * DH + d] = v * inv_sum[jq];
+  }
+}
+
+template <typename KT, int DH>
+hipError_t launch_attn_dh(const AttnArgs& a, hipStream_t s) {
+  const int nk_max = a.cross ? a.n_keys : a.max_seq;
+  const int s_stride = (nk_max + 63) & ~63;
+  if (a.C == 1) {
+    dim3 grid(a.H, a.B, 1);
+    const size_t shm = (size_t)s_stride * sizeof(float);
+    hipLaunchKernelGGL((attn_kernel<KT, DH, 1>), grid, dim3(256), shm, s, a, s_stride);
+  } else {
+    dim3 grid(a.H, a.B, (a.C + QB - 1) / QB);
+    const size_t shm = (size_t)QB * s_stride * sizeof(float);
+    hipLaunchKernelGGL((attn_kernel<KT, DH, QB>), grid, dim3(256), shm, s, a, s_stride);
+  }
+  return hipGetLastError();
 }
 
 template <typename KT>
 hipError_t launch_attn_t(const AttnArgs& a, hipStream_t s) {
-  const int nk_max = a.cross ? a.n_keys : a.max_seq;
-  const int s_stride = (nk_max + 63) & ~63;
-  dim3 grid(a.H, a.B, (a.C + QB - 1) / QB);
-  const size_t shm = (size_t)QB * s_stride * sizeof(float);
-  if (a.dh == 64) hipLaunchKernelGGL((attn_kernel<KT, 64>), grid, dim3(256), shm, s, a, s_stride);
-  else hipLaunchKernelGGL((attn_kernel<KT, 128>), grid, dim3(256), shm, s, a, s_stride);
-  return hipGetLastError();
+  return a.dh == 64 ? launch_attn_dh<KT, 64>(a, s) : launch_attn_dh<KT, 128>(a, s);
 }
 
 }  // namespace

@@ -49,15 +49,32 @@ struct LinearArgs {
   int n_parts = 0;            // filled by argmax_parts()
   float* logits = nullptr;    // [M][ldl] or null
   int ldl = 0;
+  // EPI_ARGMAX finalised in-kernel by the last block (when done_counter is set): the token of
+  // row m = b*tok_C + j goes to tok_dst0[b*tok_ld0 + tok_off0 + j] and tok_dst1[m] (if set).
+  unsigned* done_counter = nullptr;  // zero before the launch, zero again after it
+  int32_t* tok_dst0 = nullptr;
+  int tok_ld0 = 0, tok_off0 = 0, tok_C = 1;
+  int32_t* tok_dst1 = nullptr;
   // row statistics for the MFMA path's normalisation (filled by launch_linear)
   float2* stats = nullptr;    // [M] workspace
   int use_mfma = -1;          // -1: choose; 0: vector path; 1: MFMA path
 };
 
-// Number of argmax partials per row that launch_linear(EPI_ARGMAX) writes for n_per outputs.
-int argmax_parts(int n_out, int M, int wdtype);
+// True when launch_linear(EPI_ARGMAX) finalises the tokens itself (else launch_argmax_final).
+bool linear_finalises_argmax(const LinearArgs& a);
 
-hipError_t launch_linear(LinearArgs a, hipStream_t s);
+// Launch y = epilogue(W . norm(x)).  For EPI_ARGMAX, *n_parts receives the number of partials
+// per row written to part_val / part_idx (their row stride).
+hipError_t launch_linear(LinearArgs a, hipStream_t s, int* n_parts = nullptr);
+
+// Upper bound of the partials per row for n_out outputs (workspace sizing).
+int argmax_parts_max(int n_out);
+
+// True when launch_linear takes the weight-streaming path with one input row per block.
+bool linear_is_gemv_m1(const LinearArgs& a);
+
+// Algorithmic HBM bytes of a launch: weights + input rows + output rows (+ residual reads).
+double linear_bytes(const LinearArgs& a);
 
 // Gather input rows: x[r] = embedding of a token or a visual row.
 // Row r = b*C + j; j < n_prefix: visual[b][j]; else token = t0[b] if (t0 && j' == 0) else

@@ -2,10 +2,13 @@
 //
 // Two paths:
 //  * gemv_kernel — weight streaming for few rows (M <= 8: the batch-1..8 draft steps and the
-//    batch-1 verify chunk).  Each wave owns two output features and reads their weight rows with
-//    16-byte loads (8 bf16 / 4+4 f32 per lane, 512 elements per wave per step), the first batch of
-//    loads issued before the block normalises its input rows into LDS; fp32 accumulation, wave
-//    reduction, fused epilogue.  Bound: HBM bytes of W.
+//    batch-1 verify chunk).  Each wave owns two output features at a time and reads their weight
+//    rows with 16-byte loads (8 bf16 / 4+4 f32 per lane; a batch is 2048 elements per row).
+//    Input rows are requested before the weights and staged in LDS with the norm gain applied;
+//    the per-row 1/rms is applied in the epilogue.  One row pair per wave: the resident waves of a
+//    CU hide the memory latency; fp32 accumulation, wave reduction, fused epilogue, and for the LM
+//    head a per-block (max, argmax) partial that launch_argmax_final reduces.
+//    Bound: HBM bytes of W.
 //  * gemm_kernel — 64x64x64 tiles on v_mfma_f32_16x16x32_bf16 with LDS staging, for larger M
 //    (prefill, batch-8 verify).  The fp32 inputs are normalised and rounded to bf16 while they are
 //    staged.
@@ -19,92 +22,212 @@ namespace ssd {
 namespace {
 
 constexpr int GV_WAVES = 4;
-constexpr int GV_LDS_FLOATS = 12288;  // 48 KB of normalised inputs per block
-
-// 512-element steps per prefetch batch: fewer when many rows keep many accumulators live
-template <int MB> struct GvU { static constexpr int value = MB >= 8 ? 2 : 4; };
+constexpr int GV_LDS_FLOATS = 36864;    // 144 KB of staged input rows per block (160 KB LDS)
 
 __device__ __forceinline__ float apply_epi_act(int epi, float g, float u) {
   return (epi == EPI_GATED_GELU ? gelu_tanh(g) : silu(g)) * u;
 }
 
-template <typename WT, int GV_U>
-__device__ __forceinline__ void load_batch(Vec8<WT> (&buf)[2][GV_U], const WT* const (&wr)[2],
-                                           int it0, int n_it, int K, int lane) {
+// Weight rows of one wave's current row pair: two consecutive rows of one of the concatenated
+// matrices, or the (gate, up) rows of one FFN feature.
+template <typename WT>
+struct RowPair {
+  const WT* w0;
+  const WT* w1;
+  int n0, n1;  // output columns (virtual rows)
+  bool ok0, ok1;
+};
+
+template <typename WT>
+__device__ __forceinline__ RowPair<WT> row_pair(const LinearArgs& a, bool gated, int n_total, int pr) {
+  RowPair<WT> r;
+  const int K = a.K;
+  if (gated) {
+    r.ok0 = r.ok1 = pr < a.n_per;
+    const int q = r.ok0 ? pr : 0;
+    r.n0 = r.n1 = pr;
+    r.w0 = reinterpret_cast<const WT*>(a.w[0]) + (size_t)q * K;
+    r.w1 = reinterpret_cast<const WT*>(a.w[1]) + (size_t)q * K;
+    return r;
+  }
+  r.n0 = 2 * pr;
+  r.n1 = 2 * pr + 1;
+  r.ok0 = r.n0 < n_total;
+  r.ok1 = r.n1 < n_total;
+  int v0 = r.ok0 ? r.n0 : 0, v1 = r.ok1 ? r.n1 : v0;
+  // locate each virtual row in its matrix without a division (at most three matrices)
+  const void* b0 = a.w[0];
+  if (v0 >= a.n_per) { v0 -= a.n_per; b0 = a.w[1]; if (v0 >= a.n_per) { v0 -= a.n_per; b0 = a.w[2]; } }
+  const void* b1 = a.w[0];
+  if (v1 >= a.n_per) { v1 -= a.n_per; b1 = a.w[1]; if (v1 >= a.n_per) { v1 -= a.n_per; b1 = a.w[2]; } }
+  r.w0 = reinterpret_cast<const WT*>(b0) + (size_t)v0 * K;
+  r.w1 = reinterpret_cast<const WT*>(b1) + (size_t)v1 * K;
+  return r;
+}
+
+// Unconditional loads (a tail piece past K re-reads the row's last 8 elements and is skipped by
+// fma_pieces): a conditional zero fill would make the compiler drain every pending load first.
+template <typename WT, int GV_KP>
+__device__ __forceinline__ void load_pieces(Vec8<WT> (&buf)[2][GV_KP], const RowPair<WT>& r, int e0,
+                                            int K, int lane) {
 #pragma unroll
-  for (int s = 0; s < 2; ++s) {
+  for (int p = 0; p < GV_KP; ++p) {
+    const int e = min(e0 + p * 512 + lane * 8, K - 8);
+    buf[0][p].load(r.w0 + e);
+    buf[1][p].load(r.w1 + e);
+  }
+}
+
+template <typename WT, int MB, int GV_KP>
+__device__ __forceinline__ void fma_pieces(const Vec8<WT> (&buf)[2][GV_KP], const float* xs, int ldxs,
+                                           int e0, int K, int lane, float (&acc)[2][MB]) {
 #pragma unroll
-    for (int u = 0; u < GV_U; ++u) {
-      const int it = it0 + u;
-      const int e = it * 512 + lane * 8;
-      if (it < n_it && e < K) buf[s][u].load(wr[s] + e);
-      else buf[s][u].zero();
+  for (int p = 0; p < GV_KP; ++p) {
+    const int e = e0 + p * 512 + lane * 8;
+    if (e < K) {
+      float w0[8], w1[8];
+      buf[0][p].to_f32(w0);
+      buf[1][p].to_f32(w1);
+#pragma unroll
+      for (int m = 0; m < MB; ++m) {
+        const float4 xa = *reinterpret_cast<const float4*>(xs + m * ldxs + e);
+        const float4 xb = *reinterpret_cast<const float4*>(xs + m * ldxs + e + 4);
+        float t0 = acc[0][m], t1 = acc[1][m];
+        t0 = fmaf(w0[0], xa.x, t0); t1 = fmaf(w1[0], xa.x, t1);
+        t0 = fmaf(w0[1], xa.y, t0); t1 = fmaf(w1[1], xa.y, t1);
+        t0 = fmaf(w0[2], xa.z, t0); t1 = fmaf(w1[2], xa.z, t1);
+        t0 = fmaf(w0[3], xa.w, t0); t1 = fmaf(w1[3], xa.w, t1);
+        t0 = fmaf(w0[4], xb.x, t0); t1 = fmaf(w1[4], xb.x, t1);
+        t0 = fmaf(w0[5], xb.y, t0); t1 = fmaf(w1[5], xb.y, t1);
+        t0 = fmaf(w0[6], xb.z, t0); t1 = fmaf(w1[6], xb.z, t1);
+        t0 = fmaf(w0[7], xb.w, t0); t1 = fmaf(w1[7], xb.w, t1);
+        acc[0][m] = t0; acc[1][m] = t1;
+      }
     }
   }
 }
 
-template <typename WT, int MB>
-__global__ __launch_bounds__(256) void gemv_kernel(const LinearArgs a, const int kc) {
-  constexpr int GV_U = GvU<MB>::value;
-  extern __shared__ float xs[];  // [MB][kc]
-  __shared__ float2 st[MB];
+// Weight-streaming GEMV for MB <= 8 input rows held in LDS (MB * K <= GV_LDS_FLOATS).
+// One row pair per wave (blockIdx.x * 4 + wave); a wave requests a whole batch (GV_KP * 512
+// elements of both rows; the whole row for K <= 6144) at once and the many resident waves of a CU
+// hide the memory latency.
+// RMSNorm is folded: LDS holds gain * x and the per-row 1/rms multiplies the dot products in the
+// epilogue; LayerNorm inputs are normalised while staged.
+template <typename WT, int MB, int GV_KP>
+__global__ __launch_bounds__(256) void gemv_kernel(const LinearArgs a) {
+  extern __shared__ float xs[];  // [MB][ldxs]
+  __shared__ float red[GV_WAVES][2 * MB];
   __shared__ float rv[GV_WAVES][MB];
   __shared__ int ri[GV_WAVES][MB];
 
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int K = a.K;
+  const int ldxs = (K + 3) & ~3;
   const int m0 = blockIdx.y * MB;
   const int mrows = min(MB, a.M - m0);
-  const int K = a.K;
   const bool gated = (a.epi == EPI_GATED_GELU || a.epi == EPI_GATED_SILU);
+  const bool argmax = a.epi == EPI_ARGMAX;
   const int n_total = gated ? a.n_per : a.n_per * a.n_mats;
-  const int gw = blockIdx.x * GV_WAVES + wave;
+  const int n_pairs = gated ? a.n_per : (n_total + 1) / 2;
+  const int pr = blockIdx.x * GV_WAVES + wave;
+  const bool rms = a.norm == NORM_RMS, ln = a.norm == NORM_LN;
 
-  const WT* wr[2];
-  int vrow[2];
-  bool ok[2];
+  // inputs first: the wait counter is in order, so they must be requested before the weights
+  float p2[MB];
 #pragma unroll
-  for (int s = 0; s < 2; ++s) {
-    if (gated) {
-      ok[s] = gw < a.n_per;
-      vrow[s] = gw;
-      wr[s] = reinterpret_cast<const WT*>(a.w[s]) + (size_t)(ok[s] ? gw : 0) * K;
-    } else {
-      const int v = 2 * gw + s;
-      ok[s] = v < n_total;
-      vrow[s] = v;
-      const int vv = ok[s] ? v : 0;
-      const int mat = vv / a.n_per;
-      const int r = vv - mat * a.n_per;
-      const void* base = mat == 0 ? a.w[0] : (mat == 1 ? a.w[1] : a.w[2]);
-      wr[s] = reinterpret_cast<const WT*>(base) + (size_t)r * K;
+  for (int m = 0; m < MB; ++m) p2[m] = 0.f;
+  if (ln) {
+    // LayerNorm: statistics first, then the normalised rows
+    float p1[MB];
+#pragma unroll
+    for (int m = 0; m < MB; ++m) p1[m] = 0.f;
+    for (int idx = tid * 4; idx < MB * ldxs; idx += 1024) {
+      const int m = idx / ldxs, k = idx - m * ldxs;
+      if (m < mrows && k < K) {
+        const float4 v = *reinterpret_cast<const float4*>(a.x + (size_t)(m0 + m) * a.ldx + k);
+#pragma unroll
+        for (int mm = 0; mm < MB; ++mm)
+          if (mm == m) {
+            p1[mm] += (v.x + v.y) + (v.z + v.w);
+            p2[mm] += (v.x * v.x + v.y * v.y) + (v.z * v.z + v.w * v.w);
+          }
+      }
+    }
+#pragma unroll
+    for (int m = 0; m < MB; ++m) { p1[m] = wave_sum(p1[m]); p2[m] = wave_sum(p2[m]); }
+    if (lane == 0) {
+#pragma unroll
+      for (int m = 0; m < MB; ++m) { red[wave][2 * m] = p1[m]; red[wave][2 * m + 1] = p2[m]; }
+    }
+    __syncthreads();
+    for (int idx = tid * 4; idx < MB * ldxs; idx += 1024) {
+      const int m = idx / ldxs, k = idx - m * ldxs;
+      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (m < mrows && k < K) {
+        const float s1 = (red[0][2 * m] + red[1][2 * m]) + (red[2][2 * m] + red[3][2 * m]);
+        const float s2 = (red[0][2 * m + 1] + red[1][2 * m + 1]) + (red[2][2 * m + 1] + red[3][2 * m + 1]);
+        const float mean = s1 / (float)K;
+        const float rstd = 1.0f / sqrtf(fmaxf(s2 / (float)K - mean * mean, 0.f) + a.eps);
+        v = *reinterpret_cast<const float4*>(a.x + (size_t)(m0 + m) * a.ldx + k);
+        const float4 g = *reinterpret_cast<const float4*>(a.gain + k);
+        const float4 b = *reinterpret_cast<const float4*>(a.shift + k);
+        v.x = (v.x - mean) * rstd * g.x + b.x;
+        v.y = (v.y - mean) * rstd * g.y + b.y;
+        v.z = (v.z - mean) * rstd * g.z + b.z;
+        v.w = (v.w - mean) * rstd * g.w + b.w;
+      }
+      *reinterpret_cast<float4*>(xs + idx) = v;
+    }
+  } else {
+    for (int idx = tid * 4; idx < MB * ldxs; idx += 1024) {
+      const int m = idx / ldxs, k = idx - m * ldxs;
+      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (m < mrows && k < K) {
+        v = *reinterpret_cast<const float4*>(a.x + (size_t)(m0 + m) * a.ldx + k);
+        if (rms) {
+#pragma unroll
+          for (int mm = 0; mm < MB; ++mm)
+            if (mm == m) p2[mm] += (v.x * v.x + v.y * v.y) + (v.z * v.z + v.w * v.w);
+          const float4 g = *reinterpret_cast<const float4*>(a.gain + k);
+          v.x *= g.x; v.y *= g.y; v.z *= g.z; v.w *= g.w;
+        }
+      }
+      *reinterpret_cast<float4*>(xs + idx) = v;
+    }
+    if (rms) {
+#pragma unroll
+      for (int m = 0; m < MB; ++m) p2[m] = wave_sum(p2[m]);
+      if (lane == 0) {
+#pragma unroll
+        for (int m = 0; m < MB; ++m) red[wave][2 * m + 1] = p2[m];
+      }
     }
   }
 
-  const int n_it = (K + 511) >> 9;
-  Vec8<WT> cur[2][GV_U];
-  load_batch<WT, GV_U>(cur, wr, 0, n_it, K, lane);  // weights do not depend on x: start streaming now
+  // the residual values this wave's epilogue adds (lane 0), then the first weights
+  const RowPair<WT> r = row_pair<WT>(a, gated, n_total, pr < n_pairs ? pr : 0);
+  const bool live = pr < n_pairs;
+  float yold[2][MB];
+  if (lane == 0 && live && (a.epi == EPI_RESID || a.epi == EPI_BIAS_RESID)) {
+    const float* src = a.epi == EPI_RESID ? a.y : a.resid;
+    const int ld = a.epi == EPI_RESID ? a.ldy : a.ldr;
+#pragma unroll
+    for (int m = 0; m < MB; ++m) {
+      yold[0][m] = (src && r.ok0 && m < mrows) ? src[(size_t)(m0 + m) * ld + r.n0] : 0.f;
+      yold[1][m] = (src && r.ok1 && m < mrows) ? src[(size_t)(m0 + m) * ld + r.n1] : 0.f;
+    }
+  }
+  Vec8<WT> w[2][GV_KP];
+  load_pieces<WT, GV_KP>(w, r, 0, K, lane);
+  __syncthreads();
 
-  // row statistics of the inputs
-  if (a.norm != NORM_NONE) {
-    for (int m = wave; m < mrows; m += GV_WAVES) {
-      const float* xr = a.x + (size_t)(m0 + m) * a.ldx;
-      float mean = 0.f;
-      if (a.norm == NORM_LN) {
-        float s1 = 0.f;
-        for (int k = lane * 4; k < K; k += 256) {
-          const float4 v = *reinterpret_cast<const float4*>(xr + k);
-          s1 += (v.x + v.y) + (v.z + v.w);
-        }
-        mean = wave_sum(s1) / (float)K;
-      }
-      float s2 = 0.f;
-      for (int k = lane * 4; k < K; k += 256) {
-        const float4 v = *reinterpret_cast<const float4*>(xr + k);
-        const float a0 = v.x - mean, a1 = v.y - mean, a2 = v.z - mean, a3 = v.w - mean;
-        s2 += (a0 * a0 + a1 * a1) + (a2 * a2 + a3 * a3);
-      }
-      s2 = wave_sum(s2);
-      if (lane == 0) st[m] = make_float2(mean, 1.0f / sqrtf(s2 / (float)K + a.eps));
+  float rscale[MB];  // per input row: 1/rms (RMSNorm folded into the epilogue) or 1
+#pragma unroll
+  for (int m = 0; m < MB; ++m) {
+    rscale[m] = 1.f;
+    if (rms) {
+      const float s2 = (red[0][2 * m + 1] + red[1][2 * m + 1]) + (red[2][2 * m + 1] + red[3][2 * m + 1]);
+      rscale[m] = 1.0f / sqrtf(s2 / (float)K + a.eps);
     }
   }
 
@@ -113,135 +236,80 @@ __global__ __launch_bounds__(256) void gemv_kernel(const LinearArgs a, const int
   for (int s = 0; s < 2; ++s)
 #pragma unroll
     for (int m = 0; m < MB; ++m) acc[s][m] = 0.f;
-
-  for (int kc0 = 0; kc0 < K; kc0 += kc) {
-    __syncthreads();
-    const int kl = min(kc, K - kc0);
-    for (int idx = threadIdx.x * 4; idx < MB * kc; idx += 256 * 4) {
-      const int m = idx / kc, k = idx - m * kc;
-      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-      if (m < mrows && k < kl) {
-        v = *reinterpret_cast<const float4*>(a.x + (size_t)(m0 + m) * a.ldx + kc0 + k);
-        if (a.norm != NORM_NONE) {
-          const float2 s = st[m];
-          const float4 g = *reinterpret_cast<const float4*>(a.gain + kc0 + k);
-          v.x = (v.x - s.x) * s.y * g.x;
-          v.y = (v.y - s.x) * s.y * g.y;
-          v.z = (v.z - s.x) * s.y * g.z;
-          v.w = (v.w - s.x) * s.y * g.w;
-          if (a.norm == NORM_LN) {
-            const float4 b = *reinterpret_cast<const float4*>(a.shift + kc0 + k);
-            v.x += b.x; v.y += b.y; v.z += b.z; v.w += b.w;
-          }
-        }
-      }
-      *reinterpret_cast<float4*>(xs + idx) = v;
-    }
-    __syncthreads();
-
-    const int it_end = min(n_it, (kc0 + kc + 511) >> 9);
-    for (int it0 = kc0 >> 9; it0 < it_end; it0 += GV_U) {
-      Vec8<WT> nxt[2][GV_U];
-      const bool more = it0 + GV_U < n_it;
-      if (more) load_batch<WT, GV_U>(nxt, wr, it0 + GV_U, n_it, K, lane);
-#pragma unroll
-      for (int u = 0; u < GV_U; ++u) {
-        const int it = it0 + u;
-        const int e = it * 512 + lane * 8;
-        if (it < it_end && e < K) {
-          const int el = e - kc0;
-          float w0[8], w1[8];
-          cur[0][u].to_f32(w0);
-          cur[1][u].to_f32(w1);
-#pragma unroll
-          for (int m = 0; m < MB; ++m) {
-            const float4 xa = *reinterpret_cast<const float4*>(xs + m * kc + el);
-            const float4 xb = *reinterpret_cast<const float4*>(xs + m * kc + el + 4);
-            float t0 = acc[0][m], t1 = acc[1][m];
-            t0 = fmaf(w0[0], xa.x, t0); t1 = fmaf(w1[0], xa.x, t1);
-            t0 = fmaf(w0[1], xa.y, t0); t1 = fmaf(w1[1], xa.y, t1);
-            t0 = fmaf(w0[2], xa.z, t0); t1 = fmaf(w1[2], xa.z, t1);
-            t0 = fmaf(w0[3], xa.w, t0); t1 = fmaf(w1[3], xa.w, t1);
-            t0 = fmaf(w0[4], xb.x, t0); t1 = fmaf(w1[4], xb.x, t1);
-            t0 = fmaf(w0[5], xb.y, t0); t1 = fmaf(w1[5], xb.y, t1);
-            t0 = fmaf(w0[6], xb.z, t0); t1 = fmaf(w1[6], xb.z, t1);
-            t0 = fmaf(w0[7], xb.w, t0); t1 = fmaf(w1[7], xb.w, t1);
-            acc[0][m] = t0; acc[1][m] = t1;
-          }
-        }
-      }
-      if (more) {
-#pragma unroll
-        for (int s = 0; s < 2; ++s)
-#pragma unroll
-          for (int u = 0; u < GV_U; ++u) cur[s][u] = nxt[s][u];
-      }
-    }
+  for (int e0 = 0; e0 < K; e0 += 512 * GV_KP) {
+    if (e0 > 0) load_pieces<WT, GV_KP>(w, r, e0, K, lane);
+    fma_pieces<WT, MB, GV_KP>(w, xs, ldxs, e0, K, lane, acc);
   }
-
-#pragma unroll
-  for (int s = 0; s < 2; ++s)
-#pragma unroll
-    for (int m = 0; m < MB; ++m) acc[s][m] = wave_sum(acc[s][m]);
-
-  if (a.epi == EPI_ARGMAX) {
-#pragma unroll
-    for (int m = 0; m < MB; ++m) {
-      float v = -INFINITY;
-      int i = INT_MAX;
-#pragma unroll
-      for (int s = 0; s < 2; ++s)
-        if (ok[s]) argmax_merge(v, i, acc[s][m], vrow[s]);
-      if (lane == 0) {
-        rv[wave][m] = v;
-        ri[wave][m] = i;
-        if (a.logits && m < mrows) {
-#pragma unroll
-          for (int s = 0; s < 2; ++s)
-            if (ok[s]) a.logits[(size_t)(m0 + m) * a.ldl + vrow[s]] = acc[s][m];
-        }
-      }
-    }
-    __syncthreads();
-    if ((int)threadIdx.x < mrows) {
-      const int m = threadIdx.x;
-      float v = rv[0][m];
-      int i = ri[0][m];
-      for (int w = 1; w < GV_WAVES; ++w) argmax_merge(v, i, rv[w][m], ri[w][m]);
-      a.part_val[(size_t)(m0 + m) * a.n_parts + blockIdx.x] = v;
-      a.part_idx[(size_t)(m0 + m) * a.n_parts + blockIdx.x] = i;
-    }
-    return;
-  }
-
-  if (lane != 0) return;
 #pragma unroll
   for (int m = 0; m < MB; ++m) {
-    if (m >= mrows) break;
-    const size_t row = (size_t)(m0 + m);
-    if (gated) {
-      if (ok[0]) a.y[row * a.ldy + vrow[0]] = apply_epi_act(a.epi, acc[0][m], acc[1][m]);
-      continue;
-    }
+    acc[0][m] = wave_sum(acc[0][m]) * rscale[m];
+    acc[1][m] = wave_sum(acc[1][m]) * rscale[m];
+  }
+  float best_v[MB];
+  int best_i[MB];
 #pragma unroll
-    for (int s = 0; s < 2; ++s) {
-      if (!ok[s]) continue;
-      const int n = vrow[s];
-      const float v = acc[s][m];
-      float* yp = a.y + row * a.ldy + n;
-      switch (a.epi) {
-        case EPI_STORE: *yp = v; break;
-        case EPI_RESID: {
-          const float t = *yp + v;
-          *yp = t;
-          if (a.stash) a.stash[row * a.lds + n] = t;
-          break;
+  for (int m = 0; m < MB; ++m) {
+    best_v[m] = -INFINITY;
+    best_i[m] = INT_MAX;
+  }
+  if (argmax) {
+    if (live) {
+#pragma unroll
+      for (int m = 0; m < MB; ++m) {
+        if (r.ok0) argmax_merge(best_v[m], best_i[m], acc[0][m], r.n0);
+        if (r.ok1) argmax_merge(best_v[m], best_i[m], acc[1][m], r.n1);
+        if (a.logits && lane == 0 && m < mrows) {
+          float* lp = a.logits + (size_t)(m0 + m) * a.ldl;
+          if (r.ok0) lp[r.n0] = acc[0][m];
+          if (r.ok1) lp[r.n1] = acc[1][m];
         }
-        case EPI_BIAS_GELU: *yp = gelu_tanh(v + a.bias[n]); break;
-        case EPI_BIAS_RESID: *yp = (a.resid ? a.resid[row * a.ldr + n] : 0.f) + (v + a.bias[n]); break;
-        default: break;
       }
     }
+  } else if (lane == 0 && live) {
+#pragma unroll
+    for (int m = 0; m < MB; ++m) {
+      if (m >= mrows) break;
+      const size_t row = (size_t)(m0 + m);
+      if (gated) {
+        if (r.ok0) a.y[row * a.ldy + r.n0] = apply_epi_act(a.epi, acc[0][m], acc[1][m]);
+        continue;
+      }
+#pragma unroll
+      for (int s = 0; s < 2; ++s) {
+        const bool ok = s ? r.ok1 : r.ok0;
+        if (!ok) continue;
+        const int n = s ? r.n1 : r.n0;
+        const float v = acc[s][m];
+        float* yp = a.y + row * a.ldy + n;
+        if (a.epi == EPI_STORE) {
+          *yp = v;
+        } else if (a.epi == EPI_RESID) {
+          const float t = yold[s][m] + v;
+          *yp = t;
+          if (a.stash) a.stash[row * a.lds + n] = t;
+        } else if (a.epi == EPI_BIAS_GELU) {
+          *yp = gelu_tanh(v + a.bias[n]);
+        } else if (a.epi == EPI_BIAS_RESID) {
+          *yp = yold[s][m] + (v + a.bias[n]);
+        }
+      }
+    }
+  }
+
+  if (!argmax) return;
+  // block's best per row -> one partial per (row, block); launch_argmax_final reduces them
+  if (lane == 0) {
+#pragma unroll
+    for (int m = 0; m < MB; ++m) { rv[wave][m] = best_v[m]; ri[wave][m] = best_i[m]; }
+  }
+  __syncthreads();
+  if (tid < mrows) {
+    const int m = tid;
+    float v = rv[0][m];
+    int i = ri[0][m];
+    for (int ww = 1; ww < GV_WAVES; ++ww) argmax_merge(v, i, rv[ww][m], ri[ww][m]);
+    a.part_val[(size_t)(m0 + m) * a.n_parts + blockIdx.x] = v;
+    a.part_idx[(size_t)(m0 + m) * a.n_parts + blockIdx.x] = i;
   }
 }
 
@@ -449,37 +517,73 @@ __global__ void row_stats_kernel(const float* x, int ldx, int M, int K, int norm
   if (lane == 0) stats[m] = make_float2(mean, 1.0f / sqrtf(s2 / (float)K + eps));
 }
 
-int pick_mb(int M, int K) {
-  int mb = 1;
-  while (mb < M && mb < 8) mb *= 2;
-  return mb;
+int device_cus() {
+  static int cus = 0;
+  if (!cus) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        cus <= 0)
+      cus = 256;
+  }
+  return cus;
 }
 
-// K-chunk staged in LDS per pass: a multiple of the prefetch batch (512 * U elements)
-int gv_kc(int mb) {
-  const int step = 512 * (mb >= 8 ? 2 : 4);
-  int kc = GV_LDS_FLOATS / mb;
-  kc = (kc / step) * step;
-  return kc < step ? step : kc;
+// Vector-path launch shape: MB input rows per block (grid.y = row blocks), blocks over row groups.
+struct GvPlan {
+  int mb, blocks;
+};
+
+GvPlan gv_plan(const LinearArgs& a) {
+  GvPlan p;
+  const int kpad = (a.K + 3) & ~3;
+  int mb = a.M < 1 ? 1 : (a.M > 8 ? 8 : a.M);
+  while (mb > 1 && mb * kpad > GV_LDS_FLOATS) --mb;
+  p.mb = mb;
+  const bool gated = (a.epi == EPI_GATED_GELU || a.epi == EPI_GATED_SILU);
+  const int n_total = gated ? a.n_per : a.n_per * a.n_mats;
+  const int n_pairs = gated ? a.n_per : (n_total + 1) / 2;
+  const int groups = (n_pairs + GV_WAVES - 1) / GV_WAVES;
+  p.blocks = groups;
+  return p;
+}
+
+template <typename WT, int MB, int KP>
+hipError_t launch_gemv_kp(const LinearArgs& a, const GvPlan& p, hipStream_t s) {
+  static bool attr = false;
+  if (!attr) {
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&gemv_kernel<WT, MB, KP>),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, GV_LDS_FLOATS * 4);
+    attr = true;
+  }
+  dim3 grid(p.blocks, (a.M + MB - 1) / MB);
+  const size_t shm = (size_t)MB * ((a.K + 3) & ~3) * sizeof(float);
+  hipLaunchKernelGGL((gemv_kernel<WT, MB, KP>), grid, dim3(256), shm, s, a);
+  return hipGetLastError();
+}
+
+// pieces per batch: the whole row up to 12 pieces (6144 elements), else batches of 8
+template <typename WT, int MB>
+hipError_t launch_gemv_mb(const LinearArgs& a, const GvPlan& p, hipStream_t s) {
+  const int pieces = (a.K + 511) / 512;
+  if (pieces <= 4) return launch_gemv_kp<WT, MB, 4>(a, p, s);
+  if (pieces <= 8 || pieces > 12) return launch_gemv_kp<WT, MB, 8>(a, p, s);
+  return launch_gemv_kp<WT, MB, 12>(a, p, s);
 }
 
 template <typename WT>
 hipError_t launch_gemv_t(const LinearArgs& a, hipStream_t s) {
-  const bool gated = (a.epi == EPI_GATED_GELU || a.epi == EPI_GATED_SILU);
-  const int n_total = gated ? a.n_per : a.n_per * a.n_mats;
-  const int waves = gated ? a.n_per : (n_total + 1) / 2;
-  const int mb = pick_mb(a.M, a.K);
-  int kc = gv_kc(mb);
-  if (a.K <= kc) kc = (a.K + 3) & ~3;  // one chunk: size the LDS to the row
-  dim3 grid((waves + GV_WAVES - 1) / GV_WAVES, (a.M + mb - 1) / mb);
-  const size_t shm = (size_t)mb * kc * sizeof(float);
-  switch (mb) {
-    case 1: hipLaunchKernelGGL((gemv_kernel<WT, 1>), grid, dim3(256), shm, s, a, kc); break;
-    case 2: hipLaunchKernelGGL((gemv_kernel<WT, 2>), grid, dim3(256), shm, s, a, kc); break;
-    case 4: hipLaunchKernelGGL((gemv_kernel<WT, 4>), grid, dim3(256), shm, s, a, kc); break;
-    default: hipLaunchKernelGGL((gemv_kernel<WT, 8>), grid, dim3(256), shm, s, a, kc); break;
+  const GvPlan p = gv_plan(a);
+  switch (p.mb) {
+    case 1: return launch_gemv_mb<WT, 1>(a, p, s);
+    case 2: return launch_gemv_mb<WT, 2>(a, p, s);
+    case 3: return launch_gemv_mb<WT, 3>(a, p, s);
+    case 4: return launch_gemv_mb<WT, 4>(a, p, s);
+    case 5: return launch_gemv_mb<WT, 5>(a, p, s);
+    case 6: return launch_gemv_mb<WT, 6>(a, p, s);
+    case 7: return launch_gemv_mb<WT, 7>(a, p, s);
+    default: return launch_gemv_mb<WT, 8>(a, p, s);
   }
-  return hipGetLastError();
 }
 
 bool want_mfma(const LinearArgs& a) {
@@ -492,13 +596,10 @@ bool want_mfma(const LinearArgs& a) {
 
 }  // namespace
 
-int argmax_parts(int n_out, int M, int wdtype) {
-  LinearArgs a;
-  a.M = M;
-  a.wdtype = wdtype;
-  if (want_mfma(a)) return (n_out + TN - 1) / TN;
-  const int waves = (n_out + 1) / 2;
-  return (waves + GV_WAVES - 1) / GV_WAVES;
+int argmax_parts_max(int n_out) {
+  const int groups = ((n_out + 1) / 2 + GV_WAVES - 1) / GV_WAVES;
+  const int tiles = (n_out + TN - 1) / TN;
+  return groups > tiles ? groups : tiles;
 }
 
 hipError_t launch_row_stats(const float* x, int ldx, int M, int K, int norm, float eps,
@@ -507,13 +608,29 @@ hipError_t launch_row_stats(const float* x, int ldx, int M, int K, int norm, flo
   return hipGetLastError();
 }
 
-hipError_t launch_linear(LinearArgs a, hipStream_t s) {
+bool linear_is_gemv_m1(const LinearArgs& a) { return !want_mfma(a) && a.M == 1; }
+
+bool linear_finalises_argmax(const LinearArgs&) { return false; }
+
+double linear_bytes(const LinearArgs& a) {
+  const bool gated = (a.epi == EPI_GATED_GELU || a.epi == EPI_GATED_SILU);
+  const double n_w = (double)a.n_per * (gated ? 2 : a.n_mats);
+  const double n_out = gated ? a.n_per : n_w;
+  const double welem = a.wdtype == 1 ? 2.0 : 4.0;
+  double bytes = n_w * a.K * welem + (double)a.M * a.K * 4.0;
+  if (a.epi == EPI_ARGMAX) bytes += a.logits ? (double)a.M * n_out * 4.0 : 0.0;
+  else bytes += (double)a.M * n_out * 4.0 * (a.epi == EPI_RESID || a.epi == EPI_BIAS_RESID ? 2.0 : 1.0);
+  return bytes;
+}
+
+hipError_t launch_linear(LinearArgs a, hipStream_t s, int* n_parts) {
   if (a.M <= 0) return hipSuccess;
   const bool gated = (a.epi == EPI_GATED_GELU || a.epi == EPI_GATED_SILU);
   const int n_out = gated ? a.n_per : a.n_per * a.n_mats;
   if (want_mfma(a)) {
     a.use_mfma = 1;
     if (a.epi == EPI_ARGMAX) a.n_parts = (n_out + TN - 1) / TN;
+    if (n_parts) *n_parts = a.n_parts;
     if (a.norm != NORM_NONE) {
       hipError_t e = launch_row_stats(a.x, a.ldx, a.M, a.K, a.norm, a.eps, a.stats, s);
       if (e != hipSuccess) return e;
@@ -524,7 +641,8 @@ hipError_t launch_linear(LinearArgs a, hipStream_t s) {
     return hipGetLastError();
   }
   a.use_mfma = 0;
-  if (a.epi == EPI_ARGMAX) a.n_parts = argmax_parts(n_out, a.M, 0);
+  if (a.epi == EPI_ARGMAX) a.n_parts = gv_plan(a).blocks;
+  if (n_parts) *n_parts = a.n_parts;
   return a.wdtype == 1 ? launch_gemv_t<bf16_t>(a, s) : launch_gemv_t<float>(a, s);
 }
 

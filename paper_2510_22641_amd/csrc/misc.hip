@@ -75,16 +75,28 @@ __global__ void rope_scatter_kernel(const RopeScatterArgs a) {
   }
 }
 
-__global__ void argmax_final_kernel(const float* pv, const int* pi, int M, int n_parts, int C,
-                                    int32_t* dst0, int ld0, int off0, int32_t* dst1) {
+__global__ __launch_bounds__(256) void argmax_final_kernel(const float* pv, const int* pi, int M,
+                                                           int n_parts, int C, int32_t* dst0,
+                                                           int ld0, int off0, int32_t* dst1) {
+  constexpr int PER = 16;  // partials per thread requested together
   __shared__ float sv[4];
   __shared__ int si[4];
   const int m = blockIdx.x;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   float v = -INFINITY;
   int i = INT_MAX;
-  for (int p = threadIdx.x; p < n_parts; p += blockDim.x)
-    argmax_merge(v, i, pv[(size_t)m * n_parts + p], pi[(size_t)m * n_parts + p]);
+  for (int p0 = 0; p0 < n_parts; p0 += 256 * PER) {
+    float vv[PER];
+    int ii[PER];
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int p = p0 + u * 256 + threadIdx.x;
+      vv[u] = p < n_parts ? pv[(size_t)m * n_parts + p] : -INFINITY;
+      ii[u] = p < n_parts ? pi[(size_t)m * n_parts + p] : INT_MAX;
+    }
+#pragma unroll
+    for (int u = 0; u < PER; ++u) argmax_merge(v, i, vv[u], ii[u]);
+  }
   wave_argmax(v, i);
   if (lane == 0) { sv[wave] = v; si[wave] = i; }
   __syncthreads();

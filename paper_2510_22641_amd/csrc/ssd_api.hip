@@ -31,8 +31,8 @@ int t5_bucket(int n, int buckets, int max_dist) {
 
 struct Layout {
   size_t x, x1, qkv, q, attn, ffn, inh, xi, stash, vis, part_val, part_idx, stats, bias_tab,
-      bucket, rope_cos, rope_sin, status, cur_tok, g_pending, g_draft, g_target, g_count,
-      g_active, g_nactive, g_stats, total;
+      bucket, rope_cos, rope_sin, status, counters, cur_tok, g_pending, g_draft, g_target,
+      g_count, g_active, g_nactive, g_stats, total;
   int rows_max, head_rows, parts_max, ctx_max;
 };
 
@@ -48,8 +48,7 @@ bool make_layout(const ssd_dims& d, Layout& L) {
   if (d.arch == SSD_ARCH_T5 && rows < B * d.n_visual) rows = B * d.n_visual;
   L.rows_max = (int)rows;
   L.head_rows = (int)(B * (G + 1));
-  // vector-path partial count is the larger one
-  L.parts_max = ((d.vocab + 1) / 2 + 3) / 4;
+  L.parts_max = argmax_parts_max(d.vocab);
   size_t off = 0;
   auto take = [&](size_t bytes) { size_t o = off; off = align_up(off + bytes, 256); return o; };
   L.x = take(rows * D * 4);
@@ -70,6 +69,7 @@ bool make_layout(const ssd_dims& d, Layout& L) {
   L.rope_cos = take(d.arch == SSD_ARCH_LLAMA ? (size_t)d.max_seq * (d.d_head / 2) * 4 : 0);
   L.rope_sin = take(d.arch == SSD_ARCH_LLAMA ? (size_t)d.max_seq * (d.d_head / 2) * 4 : 0);
   L.status = take(4);
+  L.counters = take(64 * 4);
   L.cur_tok = take(B * 4);
   L.g_pending = take(B * 4);
   L.g_draft = take(B * (G > 0 ? G : 1) * 4);
@@ -94,7 +94,7 @@ bool dims_ok(const ssd_dims* d) {
   if (d->kvdtype != SSD_F32 && d->kvdtype != SSD_BF16) return false;
   if (d->max_batch < 1 || d->max_batch > 256) return false;
   if (d->max_gamma < 0 || d->max_gamma > 32) return false;
-  if (d->max_seq < 2 || d->max_seq > 1536) return false;  // attention keeps a row of scores in LDS
+  if (d->max_seq < 2 || d->max_seq > 1024) return false;  // attention keeps rows of scores in LDS
   if (d->max_prompt < 1 || d->page_size < 1 || d->max_pages < 1) return false;
   if ((long long)d->max_pages * d->page_size < d->max_seq) return false;
   if (ctx_len_max(*d) > d->max_seq) return false;
@@ -134,6 +134,12 @@ struct ssd_ctx {
   const int32_t* draft_out = nullptr;
   bool use_graphs = true;
   std::map<GraphKey, hipGraphExec_t> graphs;
+  // kernel timing (ssd_profile_enable)
+  bool profiling = false;
+  std::vector<hipEvent_t> ev_pool;
+  size_t ev_used = 0;
+  double prof_bytes = 0.0;
+  int64_t prof_launches = 0;
 
   template <typename T> T* at(size_t off) { return reinterpret_cast<T*>(ws + off); }
   size_t kv_layer_elems() const {
@@ -165,6 +171,25 @@ PagedKV paged(ssd_ctx* c, int l, int pos_off) {
   return p;
 }
 
+// launch_linear, bracketed by events when profiling the one-row weight-streaming GEMV
+hipError_t run_linear(ssd_ctx* c, const LinearArgs& a, int* n_parts = nullptr) {
+  if (!c->profiling || !linear_is_gemv_m1(a)) return launch_linear(a, c->stream, n_parts);
+  while (c->ev_pool.size() < c->ev_used + 2) {
+    hipEvent_t e;
+    if (hipEventCreate(&e) != hipSuccess) return hipErrorOutOfMemory;
+    c->ev_pool.push_back(e);
+  }
+  hipEvent_t e0 = c->ev_pool[c->ev_used], e1 = c->ev_pool[c->ev_used + 1];
+  c->ev_used += 2;
+  hipError_t err = hipEventRecord(e0, c->stream);
+  if (err != hipSuccess) return err;
+  err = launch_linear(a, c->stream, n_parts);
+  if (err != hipSuccess) return err;
+  c->prof_bytes += linear_bytes(a);
+  c->prof_launches += 1;
+  return hipEventRecord(e1, c->stream);
+}
+
 LinearArgs lin(ssd_ctx* c) {
   LinearArgs a;
   a.wdtype = c->d.wdtype;
@@ -194,7 +219,7 @@ int run_layers(ssd_ctx* c, float* x, int B, int C, int pos_off, int l0, int l1, 
     a.norm = NORM_RMS; a.gain = lw.attn_norm;
     a.w[0] = lw.wq; a.w[1] = lw.wk; a.w[2] = lw.wv; a.n_mats = 3; a.n_per = HD;
     a.epi = EPI_STORE; a.y = qkv; a.ldy = 3 * HD;
-    HIP_TRY(launch_linear(a, s));
+    HIP_TRY(run_linear(c, a));
     RopeScatterArgs rs;
     rs.qkv = qkv; rs.q_out = q; rs.B = B; rs.C = C; rs.H = d.n_heads; rs.dh = d.d_head;
     rs.kvdtype = d.kvdtype; rs.kv = paged(c, l, pos_off);
@@ -213,14 +238,14 @@ int run_layers(ssd_ctx* c, float* x, int B, int C, int pos_off, int l0, int l1, 
     a = lin(c);
     a.x = attn; a.ldx = HD; a.M = R; a.K = HD;
     a.w[0] = lw.wo; a.n_per = D; a.epi = EPI_RESID; a.y = x; a.ldy = D;
-    HIP_TRY(launch_linear(a, s));
+    HIP_TRY(run_linear(c, a));
     // cross-attention to the visual tokens
     if (t5) {
       a = lin(c);
       a.x = x; a.ldx = D; a.M = R; a.K = D;
       a.norm = NORM_RMS; a.gain = lw.xattn_norm;
       a.w[0] = lw.xq; a.n_per = HD; a.epi = EPI_STORE; a.y = q; a.ldy = HD;
-      HIP_TRY(launch_linear(a, s));
+      HIP_TRY(run_linear(c, a));
       AttnArgs xa = at;
       xa.cross = 1;
       xa.bias = nullptr;
@@ -232,7 +257,7 @@ int run_layers(ssd_ctx* c, float* x, int B, int C, int pos_off, int l0, int l1, 
       a = lin(c);
       a.x = attn; a.ldx = HD; a.M = R; a.K = HD;
       a.w[0] = lw.xo; a.n_per = D; a.epi = EPI_RESID; a.y = x; a.ldy = D;
-      HIP_TRY(launch_linear(a, s));
+      HIP_TRY(run_linear(c, a));
     }
     // feed-forward
     a = lin(c);
@@ -240,12 +265,12 @@ int run_layers(ssd_ctx* c, float* x, int B, int C, int pos_off, int l0, int l1, 
     a.norm = NORM_RMS; a.gain = lw.ffn_norm;
     a.w[0] = lw.w_gate; a.w[1] = lw.w_up; a.n_mats = 2; a.n_per = d.d_ff;
     a.epi = t5 ? EPI_GATED_GELU : EPI_GATED_SILU; a.y = ffn; a.ldy = d.d_ff;
-    HIP_TRY(launch_linear(a, s));
+    HIP_TRY(run_linear(c, a));
     a = lin(c);
     a.x = ffn; a.ldx = d.d_ff; a.M = R; a.K = d.d_ff;
     a.w[0] = lw.w_down; a.n_per = D; a.epi = EPI_RESID; a.y = x; a.ldy = D;
     if (stash && l == stash_layer) { a.stash = stash; a.lds = ld_stash; }
-    HIP_TRY(launch_linear(a, s));
+    HIP_TRY(run_linear(c, a));
   }
   return SSD_OK;
 }
@@ -261,11 +286,14 @@ int run_head(ssd_ctx* c, const float* x, int ldx, int M, int C, float* logits, i
   a.w[0] = c->w.lm_head; a.n_per = d.vocab; a.epi = EPI_ARGMAX;
   a.part_val = c->at<float>(c->L.part_val);
   a.part_idx = c->at<int>(c->L.part_idx);
-  a.n_parts = argmax_parts(d.vocab, M, d.wdtype);
   a.logits = logits; a.ldl = ldl;
-  HIP_TRY(launch_linear(a, c->stream));
-  HIP_TRY(launch_argmax_final(a.part_val, a.part_idx, M, a.n_parts, C, dst0, ld0, off0, dst1,
-                              c->stream));
+  a.done_counter = c->at<unsigned>(c->L.counters);
+  a.tok_dst0 = dst0; a.tok_ld0 = ld0; a.tok_off0 = off0; a.tok_C = C; a.tok_dst1 = dst1;
+  int n_parts = 0;
+  HIP_TRY(run_linear(c, a, &n_parts));
+  if (!linear_finalises_argmax(a))
+    HIP_TRY(launch_argmax_final(a.part_val, a.part_idx, M, n_parts, C, dst0, ld0, off0, dst1,
+                                c->stream));
   return SSD_OK;
 }
 
@@ -295,12 +323,12 @@ int draft_launches(ssd_ctx* c, int B, int gamma, const int32_t* pending, int32_t
     a.norm = NORM_LN; a.gain = c->w.in_ln_w; a.shift = c->w.in_ln_b; a.eps = d.ln_eps;
     a.w[0] = c->w.in_w1; a.n_per = d.in_hidden; a.epi = EPI_BIAS_GELU; a.bias = c->w.in_b1;
     a.y = inh; a.ldy = d.in_hidden;
-    HIP_TRY(launch_linear(a, c->stream));
+    HIP_TRY(run_linear(c, a));
     a = lin(c);
     a.x = inh; a.ldx = d.in_hidden; a.M = B; a.K = d.in_hidden;
     a.w[0] = c->w.in_w2; a.n_per = D; a.epi = EPI_BIAS_RESID; a.bias = c->w.in_b2;
     a.resid = d.in_residual ? x : nullptr; a.ldr = D; a.y = xi; a.ldy = D;
-    HIP_TRY(launch_linear(a, c->stream));
+    HIP_TRY(run_linear(c, a));
     rc = run_head(c, xi, D, B, 1, logits ? logits + (size_t)i * d.vocab : nullptr,
                   gamma * d.vocab, draft, gamma, i, cur);
     if (rc) return rc;
@@ -341,7 +369,7 @@ int verify_launches(ssd_ctx* c, int B, int gamma, const int32_t* pending, const 
 // Run `fn` directly or through a cached HIP graph keyed by the call's shape and pointers.
 template <typename F>
 int launch_maybe_graph(ssd_ctx* c, const GraphKey& key, F fn) {
-  if (!c->use_graphs) return fn();
+  if (!c->use_graphs || c->profiling) return fn();
   auto it = c->graphs.find(key);
   if (it == c->graphs.end()) {
     if (hipStreamBeginCapture(c->stream, hipStreamCaptureModeThreadLocal) != hipSuccess)
@@ -441,6 +469,7 @@ int ssd_create(const ssd_dims* dims, const ssd_weights* w, const ssd_kv* kv, voi
   }
   if (rc == SSD_OK &&
       (hipMemsetAsync(c->at<int32_t>(L.status), 0, 4, c->stream) != hipSuccess ||
+       hipMemsetAsync(c->at<int32_t>(L.counters), 0, 64 * 4, c->stream) != hipSuccess ||
        hipStreamSynchronize(c->stream) != hipSuccess))
     rc = SSD_ERR_HIP;
   if (rc != SSD_OK) {
@@ -481,7 +510,7 @@ int ssd_prefill(ssd_ctx* c, int B, int P, const int32_t* d_prompt, const void* d
         a.x = vis; a.ldx = D; a.M = B * d.n_visual; a.K = D;
         a.w[0] = which ? c->layers[l].xv : c->layers[l].xk; a.n_per = HD;
         a.epi = EPI_STORE; a.y = tmp; a.ldy = HD;
-        HIP_TRY(launch_linear(a, s));
+        HIP_TRY(run_linear(c, a));
         void* dst = (char*)(which ? c->kv.xv : c->kv.xk) + (size_t)l * c->xkv_layer_elems() * c->kv_elem();
         HIP_TRY(launch_scatter_cross(tmp, dst, B, d.n_visual, d.n_heads, d.d_head, d.kvdtype, s));
       }
@@ -605,6 +634,30 @@ int ssd_set_graphs(ssd_ctx* c, int enable) {
   return SSD_OK;
 }
 
+int ssd_profile_enable(ssd_ctx* c, int enable) {
+  if (!c) return SSD_ERR_ARG;
+  c->profiling = enable != 0;
+  return SSD_OK;
+}
+
+int ssd_profile_read(ssd_ctx* c, int64_t* launches, double* seconds, double* bytes) {
+  if (!c) return SSD_ERR_ARG;
+  if (hipStreamSynchronize(c->stream) != hipSuccess) return SSD_ERR_HIP;
+  double total_ms = 0.0;
+  for (size_t i = 0; i + 1 < c->ev_used; i += 2) {
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, c->ev_pool[i], c->ev_pool[i + 1]) != hipSuccess) return SSD_ERR_HIP;
+    total_ms += ms;
+  }
+  if (launches) *launches = c->prof_launches;
+  if (seconds) *seconds = total_ms * 1e-3;
+  if (bytes) *bytes = c->prof_bytes;
+  c->ev_used = 0;
+  c->prof_bytes = 0.0;
+  c->prof_launches = 0;
+  return SSD_OK;
+}
+
 int ssd_sync_status(ssd_ctx* c, int32_t* status) {
   if (!c) return SSD_ERR_ARG;
   int32_t v = 0;
@@ -635,6 +688,7 @@ const char* ssd_status_string(int code) {
 void ssd_destroy(ssd_ctx* c) {
   if (!c) return;
   for (auto& kv : c->graphs) (void)hipGraphExecDestroy(kv.second);
+  for (hipEvent_t e : c->ev_pool) (void)hipEventDestroy(e);
   delete c;
 }
 

@@ -74,6 +74,9 @@ def _load():
         "ssd_generate": (c_int, [P, c_int, c_int, P, P, c_int, c_int, c_int, c_int, P,
                                  POINTER(c_int64)]),
         "ssd_set_graphs": (c_int, [P, c_int]),
+        "ssd_profile_enable": (c_int, [P, c_int]),
+        "ssd_profile_read": (c_int, [P, POINTER(c_int64), POINTER(ctypes.c_double),
+                                     POINTER(ctypes.c_double)]),
         "ssd_sync_status": (c_int, [P, POINTER(c_int32)]),
         "ssd_status_string": (ctypes.c_char_p, [c_int]),
         "ssd_destroy": (None, [P]),
@@ -87,7 +90,8 @@ def _load():
 
 _lib = _load()
 EXPORTS = ("ssd_workspace_bytes", "ssd_create", "ssd_prefill", "ssd_draft", "ssd_verify",
-           "ssd_accept", "ssd_generate", "ssd_set_graphs", "ssd_sync_status",
+           "ssd_accept", "ssd_generate", "ssd_set_graphs", "ssd_profile_enable",
+           "ssd_profile_read", "ssd_sync_status",
            "ssd_status_string", "ssd_destroy")
 
 
@@ -154,6 +158,18 @@ def ssd_generate(ctx, B, P, d_prompt, d_visual, T, gamma, mode, reuse_hidden, d_
 
 def ssd_set_graphs(ctx, enable: bool):
     _check("ssd_set_graphs", _lib.ssd_set_graphs(ctx, int(bool(enable))))
+
+
+def ssd_profile_enable(ctx, enable: bool):
+    _check("ssd_profile_enable", _lib.ssd_profile_enable(ctx, int(bool(enable))))
+
+
+def ssd_profile_read(ctx):
+    """(launches, seconds, bytes) of the profiled kernel since the previous read."""
+    n, sec, by = c_int64(0), ctypes.c_double(0), ctypes.c_double(0)
+    _check("ssd_profile_read", _lib.ssd_profile_read(ctx, ctypes.byref(n), ctypes.byref(sec),
+                                                     ctypes.byref(by)))
+    return int(n.value), float(sec.value), float(by.value)
 
 
 def ssd_sync_status(ctx):
