@@ -6,7 +6,8 @@
 
 #define SSD_WAVE 64
 
-typedef uint16_t bf16_t;
+typedef uint16_t bf16_t;  // bfloat16 storage (same typedef as kernels.h)
+
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 

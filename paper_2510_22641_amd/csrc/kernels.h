@@ -6,6 +6,8 @@
 
 #include "ssd.h"
 
+typedef uint16_t bf16_t;
+
 namespace ssd {
 
 enum Norm { NORM_NONE = 0, NORM_RMS = 1, NORM_LN = 2 };
@@ -55,6 +57,9 @@ struct LinearArgs {
   int32_t* tok_dst0 = nullptr;
   int tok_ld0 = 0, tok_off0 = 0, tok_C = 1;
   int32_t* tok_dst1 = nullptr;
+  // hi / lo bf16 planes of a gated epilogue's output (skinny path: the next MFMA operand)
+  bf16_t* y_bf16 = nullptr;
+  int ldy_bf16 = 0;
   // row statistics for the MFMA path's normalisation (filled by launch_linear)
   float2* stats = nullptr;    // [M] workspace
   int use_mfma = -1;          // -1: choose; 0: vector path; 1: MFMA path
@@ -69,6 +74,19 @@ hipError_t launch_linear(LinearArgs a, hipStream_t s, int* n_parts = nullptr);
 
 // Upper bound of the partials per row for n_out outputs (workspace sizing).
 int argmax_parts_max(int n_out);
+
+// Rows of a verify chunk (2..16) take the skinny MFMA path: the normalised inputs are written
+// once as two bf16 planes hi + lo (launch_norm_bf16, or by the producing kernel) and every block
+// reads them as MFMA B operands.  xb / ldb: plane hi rows at xb + m*ldb, plane lo rows at
+// xb + (16 + m)*ldb; a.x, a.norm are ignored.
+bool skinny_ok(int M, int K, int wdtype);
+hipError_t launch_linear_skinny(const LinearArgs& a, const bf16_t* xb, int ldb, hipStream_t s,
+                                int* n_parts = nullptr);
+
+// out[m][k] + out[16 + m][k] ~= norm(x[m])[k] as two bf16 planes (hi, lo), M <= 16 rows
+// (RMS / LN with gain (and shift), or a plain conversion).
+hipError_t launch_norm_bf16(const float* x, int ldx, int M, int K, int norm, const float* gain,
+                            const float* shift, float eps, bf16_t* out, int ldo, hipStream_t s);
 
 // True when launch_linear takes the weight-streaming path with one input row per block.
 bool linear_is_gemv_m1(const LinearArgs& a);
@@ -124,6 +142,7 @@ hipError_t launch_rope_scatter(const RopeScatterArgs& a, hipStream_t s);
 struct AttnArgs {
   const float* q;  // [B*C][H*dh]
   float* out;      // [B*C][H*dh]
+  bf16_t* out_bf16 = nullptr;  // optional hi / lo bf16 planes of out (rows < 16; lo 16 rows on)
   int B, C, H, dh;
   int kvdtype;
   int cross;         // 0: causal over the paged cache; 1: dense over n_keys cross-attention keys

@@ -9,6 +9,8 @@
 //    CU hide the memory latency; fp32 accumulation, wave reduction, fused epilogue, and for the LM
 //    head a per-block (max, argmax) partial that launch_argmax_final reduces.
 //    Bound: HBM bytes of W.
+//  * gemv_mfma_kernel — 2..16 rows (the batch-1 verify chunk): 16 features per block, weights
+//    straight from HBM and bf16 inputs from L2 into MFMA operands, no staging.
 //  * gemm_kernel — 64x64x64 tiles on v_mfma_f32_16x16x32_bf16 with LDS staging, for larger M
 //    (prefill, batch-8 verify).  The fp32 inputs are normalised and rounded to bf16 while they are
 //    staged.
@@ -78,6 +80,13 @@ __device__ __forceinline__ void load_pieces(Vec8<WT> (&buf)[2][GV_KP], const Row
   }
 }
 
+// LDS layout of the staged input rows: element k of row m sits in plane (k / 4) % 2 at
+// m * ldxs + (k / 8) * 4 + k % 4 (plane 1 starts ldxs / 2 floats later), so that the two 16-byte
+// reads of a lane's 8 consecutive elements are each contiguous across the wave (no bank conflicts).
+__device__ __forceinline__ int xs_off(int k, int ldxs) {
+  return ((k >> 3) << 2) + (k & 3) + ((k >> 2) & 1) * (ldxs >> 1);
+}
+
 template <typename WT, int MB, int GV_KP>
 __device__ __forceinline__ void fma_pieces(const Vec8<WT> (&buf)[2][GV_KP], const float* xs, int ldxs,
                                            int e0, int K, int lane, float (&acc)[2][MB]) {
@@ -88,10 +97,11 @@ __device__ __forceinline__ void fma_pieces(const Vec8<WT> (&buf)[2][GV_KP], cons
       float w0[8], w1[8];
       buf[0][p].to_f32(w0);
       buf[1][p].to_f32(w1);
+      const int o = e >> 1;  // (e / 8) * 4
 #pragma unroll
       for (int m = 0; m < MB; ++m) {
-        const float4 xa = *reinterpret_cast<const float4*>(xs + m * ldxs + e);
-        const float4 xb = *reinterpret_cast<const float4*>(xs + m * ldxs + e + 4);
+        const float4 xa = *reinterpret_cast<const float4*>(xs + m * ldxs + o);
+        const float4 xb = *reinterpret_cast<const float4*>(xs + m * ldxs + (ldxs >> 1) + o);
         float t0 = acc[0][m], t1 = acc[1][m];
         t0 = fmaf(w0[0], xa.x, t0); t1 = fmaf(w1[0], xa.x, t1);
         t0 = fmaf(w0[1], xa.y, t0); t1 = fmaf(w1[1], xa.y, t1);
@@ -122,7 +132,7 @@ __global__ __launch_bounds__(256) void gemv_kernel(const LinearArgs a) {
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int K = a.K;
-  const int ldxs = (K + 3) & ~3;
+  const int ldxs = (K + 7) & ~7;
   const int m0 = blockIdx.y * MB;
   const int mrows = min(MB, a.M - m0);
   const bool gated = (a.epi == EPI_GATED_GELU || a.epi == EPI_GATED_SILU);
@@ -176,23 +186,38 @@ __global__ __launch_bounds__(256) void gemv_kernel(const LinearArgs a) {
         v.z = (v.z - mean) * rstd * g.z + b.z;
         v.w = (v.w - mean) * rstd * g.w + b.w;
       }
-      *reinterpret_cast<float4*>(xs + idx) = v;
+      *reinterpret_cast<float4*>(xs + m * ldxs + xs_off(k, ldxs)) = v;
     }
   } else {
-    for (int idx = tid * 4; idx < MB * ldxs; idx += 1024) {
-      const int m = idx / ldxs, k = idx - m * ldxs;
-      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-      if (m < mrows && k < K) {
-        v = *reinterpret_cast<const float4*>(a.x + (size_t)(m0 + m) * a.ldx + k);
+    // 8 float4 per thread requested together (a loop with one load per trip would pay one
+    // memory round trip per trip)
+    constexpr int SB = 8;
+    for (int base = tid * 4; base < MB * ldxs; base += 1024 * SB) {
+      float4 v[SB], g[SB];
+#pragma unroll
+      for (int u = 0; u < SB; ++u) {
+        const int idx = base + u * 1024;
+        const int m = idx / ldxs, k = idx - m * ldxs;
+        v[u] = g[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (idx < MB * ldxs && m < mrows && k < K) {
+          v[u] = *reinterpret_cast<const float4*>(a.x + (size_t)(m0 + m) * a.ldx + k);
+          if (rms) g[u] = *reinterpret_cast<const float4*>(a.gain + k);
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < SB; ++u) {
+        const int idx = base + u * 1024;
+        if (idx >= MB * ldxs) break;
+        const int m = idx / ldxs, k = idx - m * ldxs;
+        float4 x4 = v[u];
         if (rms) {
 #pragma unroll
           for (int mm = 0; mm < MB; ++mm)
-            if (mm == m) p2[mm] += (v.x * v.x + v.y * v.y) + (v.z * v.z + v.w * v.w);
-          const float4 g = *reinterpret_cast<const float4*>(a.gain + k);
-          v.x *= g.x; v.y *= g.y; v.z *= g.z; v.w *= g.w;
+            if (mm == m) p2[mm] += (x4.x * x4.x + x4.y * x4.y) + (x4.z * x4.z + x4.w * x4.w);
+          x4.x *= g[u].x; x4.y *= g[u].y; x4.z *= g[u].z; x4.w *= g[u].w;
         }
+        *reinterpret_cast<float4*>(xs + m * ldxs + xs_off(k, ldxs)) = x4;
       }
-      *reinterpret_cast<float4*>(xs + idx) = v;
     }
     if (rms) {
 #pragma unroll
@@ -310,6 +335,223 @@ __global__ __launch_bounds__(256) void gemv_kernel(const LinearArgs a) {
     for (int ww = 1; ww < GV_WAVES; ++ww) argmax_merge(v, i, rv[ww][m], ri[ww][m]);
     a.part_val[(size_t)(m0 + m) * a.n_parts + blockIdx.x] = v;
     a.part_idx[(size_t)(m0 + m) * a.n_parts + blockIdx.x] = i;
+  }
+}
+
+// ---------------------------------------------------------------------------------------------
+// Skinny MFMA path: 2..16 input rows (the batch-1 verify chunk), bf16 weights.
+// The inputs arrive already normalised as two bf16 planes, x ~= hi + lo with hi = bf16(x) and
+// lo = bf16(x - hi) (rows m at xb + m * ldb and xb + (16 + m) * ldb), written by launch_norm_bf16
+// or by the producing kernel; multiplying both planes keeps the activations at about 16 mantissa
+// bits while the weights are read once.  A block owns 16 output features and its 4 waves split
+// K.  Per 64-element step a lane reads 32 contiguous bytes of one weight row (the A operands of
+// two v_mfma_f32_16x16x32_bf16) and 32 bytes of each input plane (the B operands; rows past M
+// read as zeros).  All loads of a batch are issued before the first MFMA; the four partial 16x16
+// tiles are summed through LDS before the fused epilogue.
+template <bool GATED>
+__global__ __launch_bounds__(256) void gemv_mfma_kernel(const LinearArgs a, const bf16_t* __restrict__ xb,
+                                                        const int ldb) {
+  constexpr int NB = GATED ? 2 : 1;
+  constexpr int SK = GATED ? 4 : 8;  // 64-element steps per batch
+  __shared__ float part[4][NB][16][17];
+  __shared__ float best_v[16][17];
+  __shared__ int best_i[16][17];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int K = a.K, M = a.M;
+  const int n_out = GATED ? a.n_per : a.n_per * a.n_mats;
+  const int n0 = blockIdx.x * 16;
+  const int steps = K / 64;
+  const int s_beg = (steps * wave) / 4, s_end = (steps * (wave + 1)) / 4;
+  const int row = n0 + (lane & 15);
+  const bool row_ok = row < n_out;
+  const bf16_t* wrow[NB];
+  {
+    const int rr = row_ok ? row : 0;
+    if (GATED) {
+      wrow[0] = reinterpret_cast<const bf16_t*>(a.w[0]) + (size_t)rr * K;
+      wrow[NB - 1] = reinterpret_cast<const bf16_t*>(a.w[1]) + (size_t)rr * K;
+    } else {
+      int v = rr;
+      const void* base = a.w[0];
+      if (v >= a.n_per) { v -= a.n_per; base = a.w[1]; if (v >= a.n_per) { v -= a.n_per; base = a.w[2]; } }
+      wrow[0] = reinterpret_cast<const bf16_t*>(base) + (size_t)v * K;
+    }
+  }
+  const int kq = (lane >> 4) * 16;  // this lane's 16 elements within a step
+  const int tok = lane & 15;
+  const bool tok_ok = tok < M;
+  const bf16_t* brow = xb + (size_t)(tok_ok ? tok : 0) * ldb;
+  const bf16_t* brow_lo = brow + (size_t)16 * ldb;
+
+  f32x4_t acc[NB];
+#pragma unroll
+  for (int b = 0; b < NB; ++b) acc[b] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  for (int s0 = s_beg; s0 < s_end; s0 += SK) {
+    uint4 wv[NB][SK][2], bv[SK][2], bl[SK][2];
+#pragma unroll
+    for (int u = 0; u < SK; ++u) {
+      const int st = min(s0 + u, s_end - 1);
+#pragma unroll
+      for (int b = 0; b < NB; ++b) {
+        const uint4* wp = reinterpret_cast<const uint4*>(wrow[b] + st * 64 + kq);
+        wv[b][u][0] = wp[0];
+        wv[b][u][1] = wp[1];
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < SK; ++u) {
+      const int st = min(s0 + u, s_end - 1);
+      const uint4* bp = reinterpret_cast<const uint4*>(brow + st * 64 + kq);
+      bv[u][0] = bp[0];
+      bv[u][1] = bp[1];
+      const uint4* bq = reinterpret_cast<const uint4*>(brow_lo + st * 64 + kq);
+      bl[u][0] = bq[0];
+      bl[u][1] = bq[1];
+    }
+#pragma unroll
+    for (int u = 0; u < SK; ++u) {
+      if (s0 + u >= s_end) break;
+      const uint4 z = make_uint4(0, 0, 0, 0);
+      const uint4 b0 = tok_ok ? bv[u][0] : z, b1 = tok_ok ? bv[u][1] : z;
+      const uint4 c0 = tok_ok ? bl[u][0] : z, c1 = tok_ok ? bl[u][1] : z;
+#pragma unroll
+      for (int b = 0; b < NB; ++b) {
+        const bf16x8_t w0 = *reinterpret_cast<const bf16x8_t*>(&wv[b][u][0]);
+        const bf16x8_t w1 = *reinterpret_cast<const bf16x8_t*>(&wv[b][u][1]);
+        acc[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w0, *reinterpret_cast<const bf16x8_t*>(&b0), acc[b], 0, 0, 0);
+        acc[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w0, *reinterpret_cast<const bf16x8_t*>(&c0), acc[b], 0, 0, 0);
+        acc[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w1, *reinterpret_cast<const bf16x8_t*>(&b1), acc[b], 0, 0, 0);
+        acc[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w1, *reinterpret_cast<const bf16x8_t*>(&c1), acc[b], 0, 0, 0);
+      }
+    }
+  }
+  // D[feature][token]: lane holds features 4 * (lane / 16) + e, token lane % 16
+#pragma unroll
+  for (int b = 0; b < NB; ++b)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) part[wave][b][4 * (lane >> 4) + e][lane & 15] = acc[b][e];
+  __syncthreads();
+
+  // epilogue: thread (feature f, token t)
+  const int f = tid >> 4, t = tid & 15;
+  const int n = n0 + f;
+  const float v = (part[0][0][f][t] + part[1][0][f][t]) + (part[2][0][f][t] + part[3][0][f][t]);
+  const bool ok = t < M && n < n_out;
+  if (a.epi == EPI_ARGMAX) {
+    best_v[t][f] = ok ? v : -INFINITY;
+    best_i[t][f] = ok ? n : INT_MAX;
+    if (ok && a.logits) a.logits[(size_t)t * a.ldl + n] = v;
+    __syncthreads();
+    if (tid < M) {
+      float bvv = -INFINITY;
+      int bi = INT_MAX;
+      for (int ff = 0; ff < 16; ++ff) argmax_merge(bvv, bi, best_v[tid][ff], best_i[tid][ff]);
+      a.part_val[(size_t)tid * a.n_parts + blockIdx.x] = bvv;
+      a.part_idx[(size_t)tid * a.n_parts + blockIdx.x] = bi;
+    }
+    return;
+  }
+  if (!ok) return;
+  if (GATED) {
+    const float u = (part[0][NB - 1][f][t] + part[1][NB - 1][f][t]) + (part[2][NB - 1][f][t] + part[3][NB - 1][f][t]);
+    const float act = apply_epi_act(a.epi, v, u);
+    if (a.y) a.y[(size_t)t * a.ldy + n] = act;
+    if (a.y_bf16) {
+      const uint32_t hi = f32_to_bf16(act);
+      a.y_bf16[(size_t)t * a.ldy_bf16 + n] = (bf16_t)hi;
+      a.y_bf16[(size_t)(16 + t) * a.ldy_bf16 + n] = (bf16_t)f32_to_bf16(act - bf16_to_f32(hi));
+    }
+    return;
+  }
+  float* yp = a.y + (size_t)t * a.ldy + n;
+  switch (a.epi) {
+    case EPI_STORE: *yp = v; break;
+    case EPI_RESID: {
+      const float tt = *yp + v;
+      *yp = tt;
+      if (a.stash) a.stash[(size_t)t * a.lds + n] = tt;
+      break;
+    }
+    case EPI_BIAS_GELU: *yp = gelu_tanh(v + a.bias[n]); break;
+    case EPI_BIAS_RESID: *yp = (a.resid ? a.resid[(size_t)t * a.ldr + n] : 0.f) + (v + a.bias[n]); break;
+    default: break;
+  }
+}
+
+// out[m][k] = hi, out[16 + m][k] = lo with hi + lo ~= norm(x[m])[k] (bf16 planes) — one block per
+// row; the row stays in registers for K <= 4096.
+__global__ __launch_bounds__(256) void norm_bf16_kernel(const float* __restrict__ x, int ldx, int K,
+                                                        int norm, const float* __restrict__ gain,
+                                                        const float* __restrict__ shift, float eps,
+                                                        bf16_t* __restrict__ out, int ldo) {
+  constexpr int PT = 4;  // float4 per thread kept in registers
+  __shared__ float red[4][2];
+  const int m = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const float* xr = x + (size_t)m * ldx;
+  bf16_t* orow = out + (size_t)m * ldo;
+  float4 v[PT];
+  float s1 = 0.f, s2 = 0.f;
+  const bool fits = K <= 1024 * PT;
+#pragma unroll
+  for (int u = 0; u < PT; ++u) {
+    const int k = (tid + 256 * u) * 4;
+    v[u] = k < K ? *reinterpret_cast<const float4*>(xr + k) : make_float4(0.f, 0.f, 0.f, 0.f);
+  }
+  if (!fits) {
+    for (int k = (tid + 256 * PT) * 4; k < K; k += 1024) {
+      const float4 w = *reinterpret_cast<const float4*>(xr + k);
+      s1 += (w.x + w.y) + (w.z + w.w);
+      s2 += (w.x * w.x + w.y * w.y) + (w.z * w.z + w.w * w.w);
+    }
+  }
+#pragma unroll
+  for (int u = 0; u < PT; ++u) {
+    s1 += (v[u].x + v[u].y) + (v[u].z + v[u].w);
+    s2 += (v[u].x * v[u].x + v[u].y * v[u].y) + (v[u].z * v[u].z + v[u].w * v[u].w);
+  }
+  s1 = wave_sum(s1);
+  s2 = wave_sum(s2);
+  if (lane == 0) { red[wave][0] = s1; red[wave][1] = s2; }
+  __syncthreads();
+  const float t1 = (red[0][0] + red[1][0]) + (red[2][0] + red[3][0]);
+  const float t2 = (red[0][1] + red[1][1]) + (red[2][1] + red[3][1]);
+  float mean = 0.f, rstd = 1.f;
+  if (norm == NORM_LN) {
+    mean = t1 / (float)K;
+    rstd = 1.0f / sqrtf(fmaxf(t2 / (float)K - mean * mean, 0.f) + eps);
+  } else if (norm == NORM_RMS) {
+    rstd = 1.0f / sqrtf(t2 / (float)K + eps);
+  }
+  auto emit = [&](int k, float4 w) {
+    float f[4] = {w.x, w.y, w.z, w.w};
+    if (norm != NORM_NONE) {
+      const float4 g = *reinterpret_cast<const float4*>(gain + k);
+      const float gg[4] = {g.x, g.y, g.z, g.w};
+      float bb[4] = {0.f, 0.f, 0.f, 0.f};
+      if (norm == NORM_LN) {
+        const float4 b = *reinterpret_cast<const float4*>(shift + k);
+        bb[0] = b.x; bb[1] = b.y; bb[2] = b.z; bb[3] = b.w;
+      }
+#pragma unroll
+      for (int e = 0; e < 4; ++e) f[e] = (f[e] - mean) * rstd * gg[e] + bb[e];
+    }
+    uint32_t h[4], l[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      h[e] = f32_to_bf16(f[e]);
+      l[e] = f32_to_bf16(f[e] - bf16_to_f32(h[e]));
+    }
+    *reinterpret_cast<uint2*>(orow + k) = make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16));
+    *reinterpret_cast<uint2*>(orow + (size_t)16 * ldo + k) = make_uint2(l[0] | (l[1] << 16), l[2] | (l[3] << 16));
+  };
+#pragma unroll
+  for (int u = 0; u < PT; ++u) {
+    const int k = (tid + 256 * u) * 4;
+    if (k < K) emit(k, v[u]);
+  }
+  if (!fits) {
+    for (int k = (tid + 256 * PT) * 4; k < K; k += 1024) emit(k, *reinterpret_cast<const float4*>(xr + k));
   }
 }
 
@@ -536,7 +778,7 @@ struct GvPlan {
 
 GvPlan gv_plan(const LinearArgs& a) {
   GvPlan p;
-  const int kpad = (a.K + 3) & ~3;
+  const int kpad = (a.K + 7) & ~7;
   int mb = a.M < 1 ? 1 : (a.M > 8 ? 8 : a.M);
   while (mb > 1 && mb * kpad > GV_LDS_FLOATS) --mb;
   p.mb = mb;
@@ -557,7 +799,7 @@ hipError_t launch_gemv_kp(const LinearArgs& a, const GvPlan& p, hipStream_t s) {
     attr = true;
   }
   dim3 grid(p.blocks, (a.M + MB - 1) / MB);
-  const size_t shm = (size_t)MB * ((a.K + 3) & ~3) * sizeof(float);
+  const size_t shm = (size_t)MB * ((a.K + 7) & ~7) * sizeof(float);
   hipLaunchKernelGGL((gemv_kernel<WT, MB, KP>), grid, dim3(256), shm, s, a);
   return hipGetLastError();
 }
@@ -598,8 +840,30 @@ bool want_mfma(const LinearArgs& a) {
 
 int argmax_parts_max(int n_out) {
   const int groups = ((n_out + 1) / 2 + GV_WAVES - 1) / GV_WAVES;
-  const int tiles = (n_out + TN - 1) / TN;
+  const int tiles = (n_out + 15) / 16;
   return groups > tiles ? groups : tiles;
+}
+
+bool skinny_ok(int M, int K, int wdtype) { return wdtype == 1 && M >= 2 && M <= 16 && K % 64 == 0; }
+
+hipError_t launch_linear_skinny(const LinearArgs& a, const bf16_t* xb, int ldb, hipStream_t s,
+                                int* n_parts) {
+  const bool gated = (a.epi == EPI_GATED_GELU || a.epi == EPI_GATED_SILU);
+  const int n_out = gated ? a.n_per : a.n_per * a.n_mats;
+  const int tiles = (n_out + 15) / 16;
+  LinearArgs b = a;
+  if (b.epi == EPI_ARGMAX) b.n_parts = tiles;
+  if (n_parts) *n_parts = b.n_parts;
+  if (gated) hipLaunchKernelGGL((gemv_mfma_kernel<true>), dim3(tiles), dim3(256), 0, s, b, xb, ldb);
+  else hipLaunchKernelGGL((gemv_mfma_kernel<false>), dim3(tiles), dim3(256), 0, s, b, xb, ldb);
+  return hipGetLastError();
+}
+
+hipError_t launch_norm_bf16(const float* x, int ldx, int M, int K, int norm, const float* gain,
+                            const float* shift, float eps, bf16_t* out, int ldo, hipStream_t s) {
+  hipLaunchKernelGGL(norm_bf16_kernel, dim3(M), dim3(256), 0, s, x, ldx, K, norm, gain, shift, eps,
+                     out, ldo);
+  return hipGetLastError();
 }
 
 hipError_t launch_row_stats(const float* x, int ldx, int M, int K, int norm, float eps,

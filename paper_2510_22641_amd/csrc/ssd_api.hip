@@ -31,6 +31,7 @@ int t5_bucket(int n, int buckets, int max_dist) {
 
 struct Layout {
   size_t x, x1, qkv, q, attn, ffn, inh, xi, stash, vis, part_val, part_idx, stats, bias_tab,
+      bf_x, bf_attn, bf_ffn,
       bucket, rope_cos, rope_sin, status, counters, cur_tok, g_pending, g_draft, g_target,
       g_count, g_active, g_nactive, g_stats, total;
   int rows_max, head_rows, parts_max, ctx_max;
@@ -64,6 +65,11 @@ bool make_layout(const ssd_dims& d, Layout& L) {
   L.part_val = take((size_t)L.head_rows * L.parts_max * 4);
   L.part_idx = take((size_t)L.head_rows * L.parts_max * 4);
   L.stats = take(rows * 8);
+  // bf16 operands of the skinny MFMA path (at most 16 rows)
+  const size_t dmax = D > (size_t)d.in_hidden ? D : (size_t)d.in_hidden;
+  L.bf_x = take(32 * dmax * 2);  // hi and lo planes of 16 rows each
+  L.bf_attn = take(32 * HD * 2);
+  L.bf_ffn = take(32 * (size_t)d.d_ff * 2);
   L.bias_tab = take(d.arch == SSD_ARCH_T5 ? (size_t)d.n_heads * d.max_seq * 4 : 0);
   L.bucket = take(d.arch == SSD_ARCH_T5 ? (size_t)d.max_seq * 4 : 0);
   L.rope_cos = take(d.arch == SSD_ARCH_LLAMA ? (size_t)d.max_seq * (d.d_head / 2) * 4 : 0);
@@ -206,11 +212,28 @@ int run_layers(ssd_ctx* c, float* x, int B, int C, int pos_off, int l0, int l1, 
   hipStream_t s = c->stream;
   const int R = B * C, D = d.d_model, HD = d.n_heads * d.d_head;
   const bool t5 = d.arch == SSD_ARCH_T5;
+  // 2..16 rows in bf16: MFMA with operands written once as bf16 (the verify chunk)
+  const bool skinny = skinny_ok(R, D, d.wdtype) && skinny_ok(R, HD, d.wdtype) &&
+                      skinny_ok(R, d.d_ff, d.wdtype);
   float* qkv = c->at<float>(c->L.qkv);
   float* q = c->at<float>(c->L.q);
   float* attn = c->at<float>(c->L.attn);
   float* ffn = c->at<float>(c->L.ffn);
+  bf16_t* bx = c->at<bf16_t>(c->L.bf_x);
+  bf16_t* battn = c->at<bf16_t>(c->L.bf_attn);
+  bf16_t* bffn = c->at<bf16_t>(c->L.bf_ffn);
   int32_t* status = c->at<int32_t>(c->L.status);
+  // one linear layer: skinny (bf16 input xb) or the vector / tile paths (fp32 input a.x)
+  auto linear = [&](LinearArgs& a, const bf16_t* xb, int ldb) -> hipError_t {
+    if (!skinny) return run_linear(c, a);
+    if (a.norm != NORM_NONE) {
+      hipError_t e = launch_norm_bf16(a.x, a.ldx, a.M, a.K, a.norm, a.gain, a.shift, a.eps, bx, a.K, s);
+      if (e != hipSuccess) return e;
+      xb = bx;
+      ldb = a.K;
+    }
+    return launch_linear_skinny(a, xb, ldb, s);
+  };
   for (int l = l0; l < l1; ++l) {
     const ssd_layer_weights& lw = c->layers[l];
     // self-attention
@@ -219,7 +242,7 @@ int run_layers(ssd_ctx* c, float* x, int B, int C, int pos_off, int l0, int l1, 
     a.norm = NORM_RMS; a.gain = lw.attn_norm;
     a.w[0] = lw.wq; a.w[1] = lw.wk; a.w[2] = lw.wv; a.n_mats = 3; a.n_per = HD;
     a.epi = EPI_STORE; a.y = qkv; a.ldy = 3 * HD;
-    HIP_TRY(run_linear(c, a));
+    HIP_TRY(linear(a, nullptr, 0));
     RopeScatterArgs rs;
     rs.qkv = qkv; rs.q_out = q; rs.B = B; rs.C = C; rs.H = d.n_heads; rs.dh = d.d_head;
     rs.kvdtype = d.kvdtype; rs.kv = paged(c, l, pos_off);
@@ -228,7 +251,8 @@ int run_layers(ssd_ctx* c, float* x, int B, int C, int pos_off, int l0, int l1, 
     rs.max_seq = d.max_seq; rs.status = status;
     HIP_TRY(launch_rope_scatter(rs, s));
     AttnArgs at;
-    at.q = q; at.out = attn; at.B = B; at.C = C; at.H = d.n_heads; at.dh = d.d_head;
+    at.q = q; at.out = attn; at.out_bf16 = skinny ? battn : nullptr;
+    at.B = B; at.C = C; at.H = d.n_heads; at.dh = d.d_head;
     at.kvdtype = d.kvdtype; at.cross = 0; at.kv = paged(c, l, pos_off);
     at.bias = t5 ? c->at<float>(c->L.bias_tab) : nullptr;
     at.max_seq = d.max_seq; at.xk = at.xv = nullptr; at.n_keys = 0;
@@ -238,14 +262,14 @@ int run_layers(ssd_ctx* c, float* x, int B, int C, int pos_off, int l0, int l1, 
     a = lin(c);
     a.x = attn; a.ldx = HD; a.M = R; a.K = HD;
     a.w[0] = lw.wo; a.n_per = D; a.epi = EPI_RESID; a.y = x; a.ldy = D;
-    HIP_TRY(run_linear(c, a));
+    HIP_TRY(linear(a, battn, HD));
     // cross-attention to the visual tokens
     if (t5) {
       a = lin(c);
       a.x = x; a.ldx = D; a.M = R; a.K = D;
       a.norm = NORM_RMS; a.gain = lw.xattn_norm;
       a.w[0] = lw.xq; a.n_per = HD; a.epi = EPI_STORE; a.y = q; a.ldy = HD;
-      HIP_TRY(run_linear(c, a));
+      HIP_TRY(linear(a, nullptr, 0));
       AttnArgs xa = at;
       xa.cross = 1;
       xa.bias = nullptr;
@@ -257,7 +281,7 @@ int run_layers(ssd_ctx* c, float* x, int B, int C, int pos_off, int l0, int l1, 
       a = lin(c);
       a.x = attn; a.ldx = HD; a.M = R; a.K = HD;
       a.w[0] = lw.xo; a.n_per = D; a.epi = EPI_RESID; a.y = x; a.ldy = D;
-      HIP_TRY(run_linear(c, a));
+      HIP_TRY(linear(a, battn, HD));
     }
     // feed-forward
     a = lin(c);
@@ -265,12 +289,13 @@ int run_layers(ssd_ctx* c, float* x, int B, int C, int pos_off, int l0, int l1, 
     a.norm = NORM_RMS; a.gain = lw.ffn_norm;
     a.w[0] = lw.w_gate; a.w[1] = lw.w_up; a.n_mats = 2; a.n_per = d.d_ff;
     a.epi = t5 ? EPI_GATED_GELU : EPI_GATED_SILU; a.y = ffn; a.ldy = d.d_ff;
-    HIP_TRY(run_linear(c, a));
+    if (skinny) { a.y = nullptr; a.y_bf16 = bffn; a.ldy_bf16 = d.d_ff; }
+    HIP_TRY(linear(a, nullptr, 0));
     a = lin(c);
     a.x = ffn; a.ldx = d.d_ff; a.M = R; a.K = d.d_ff;
     a.w[0] = lw.w_down; a.n_per = D; a.epi = EPI_RESID; a.y = x; a.ldy = D;
     if (stash && l == stash_layer) { a.stash = stash; a.lds = ld_stash; }
-    HIP_TRY(run_linear(c, a));
+    HIP_TRY(linear(a, bffn, d.d_ff));
   }
   return SSD_OK;
 }
@@ -290,7 +315,14 @@ int run_head(ssd_ctx* c, const float* x, int ldx, int M, int C, float* logits, i
   a.done_counter = c->at<unsigned>(c->L.counters);
   a.tok_dst0 = dst0; a.tok_ld0 = ld0; a.tok_off0 = off0; a.tok_C = C; a.tok_dst1 = dst1;
   int n_parts = 0;
-  HIP_TRY(run_linear(c, a, &n_parts));
+  if (skinny_ok(M, d.d_model, d.wdtype)) {
+    bf16_t* bx = c->at<bf16_t>(c->L.bf_x);
+    HIP_TRY(launch_norm_bf16(x, ldx, M, d.d_model, NORM_RMS, c->w.final_norm, nullptr, d.norm_eps,
+                             bx, d.d_model, c->stream));
+    HIP_TRY(launch_linear_skinny(a, bx, d.d_model, c->stream, &n_parts));
+  } else {
+    HIP_TRY(run_linear(c, a, &n_parts));
+  }
   if (!linear_finalises_argmax(a))
     HIP_TRY(launch_argmax_final(a.part_val, a.part_idx, M, n_parts, C, dst0, ld0, off0, dst1,
                                 c->stream));

@@ -115,7 +115,7 @@ C1 = Workload("c1-tiny-t5-f32", TINY_T5, batch=1, prompt_len=8, draft_layers=1, 
 C2 = Workload("c2-flant5-base", FLANT5_BASE, batch=1, prompt_len=16, draft_layers=4, gamma=4,
               new_tokens=64, deep_scale=0.2)
 C3 = Workload("c3-flant5-xl", FLANT5_XL, batch=1, prompt_len=8, draft_layers=6, gamma=5,
-              new_tokens=128, deep_scale=0.1)
+              new_tokens=128, deep_scale=0.04)  # oracle alpha 0.707 at seed 0 (tune_scale)
 C5 = Workload("c5-llava-7b", LLAVA_7B, batch=1, prompt_len=32, draft_layers=8, gamma=5,
               new_tokens=256, deep_scale=0.1)
 
