@@ -150,7 +150,8 @@ def main():
              "GBps": round(step_bytes / step_s / 1e9, 1),
              "frac": round(step_bytes / step_s / 1e9 / HBM_PEAK_GBS, 4)}
 
-    # dominant kernel: every launch of the one-row weight-streaming GEMV, bracketed by events
+    # dominant kernel: every launch of the one-row weight-streaming GEMV instantiation that rocprof
+    # names gemv_kernel<T, 1, 4>, timed by events bound to its own dispatch
     abi.ssd_profile_enable(dd.ctx, True)
     abi.ssd_profile_read(dd.ctx)
     for _ in range(max(1, args.steps // 2)):
@@ -160,7 +161,8 @@ def main():
     per_launch_bytes = nbytes / max(1, n_launch)
     avg_s = secs / max(1, n_launch)
     achieved = per_launch_bytes / avg_s / 1e9
-    roofline = {"bound": "hbm", "kernel": "gemv_kernel<bf16,1> (one-row weight-streaming GEMV)",
+    kname = "gemv_kernel<%s, 1, 4>" % ("unsigned short" if sh.dtype == "bf16" else "float")
+    roofline = {"bound": "hbm", "kernel": kname + " (one-row weight-streaming GEMV)",
                 "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
                 "bytes_per_launch": int(per_launch_bytes), "avg_launch_us": round(avg_s * 1e6, 3),

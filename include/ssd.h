@@ -189,11 +189,13 @@ int ssd_generate(ssd_ctx* ctx, int B, int P, const int32_t* d_prompt, const void
 int ssd_set_graphs(ssd_ctx* ctx, int enable);
 
 /* Kernel timing for roofline reports.  While enabled (and graphs are bypassed), every launch of
- * the weight-streaming GEMV with one input row — the kernel that carries the batch-1 draft steps —
- * is bracketed by two HIP events on the context's stream, and its algorithmic bytes (weights +
- * input rows + output rows) are added up.  ssd_profile_read synchronises the stream and returns
- * the number of such launches, the summed event time in seconds and the summed bytes since the
- * previous read (any pointer may be NULL).  Costs one event pair per launch; for measurement only. */
+ * the weight-streaming GEMV with one input row and rows of at most 2048 elements
+ * (gemv_kernel<T, 1, 4>, the kernel that carries most of a batch-1 draft step) is launched with
+ * two HIP events bound to its own dispatch on the context's stream, so their elapsed time is the
+ * kernel's execution time; its algorithmic bytes (weights + input rows + output rows) are added
+ * up.  ssd_profile_read synchronises the stream and returns the number of such launches, the
+ * summed kernel time in seconds and the summed bytes since the previous read (any pointer may be
+ * NULL).  Costs one event pair per launch; for measurement only. */
 int ssd_profile_enable(ssd_ctx* ctx, int enable);
 int ssd_profile_read(ssd_ctx* ctx, int64_t* launches, double* seconds, double* bytes);
 

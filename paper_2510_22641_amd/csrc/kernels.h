@@ -12,6 +12,18 @@ namespace ssd {
 
 enum Norm { NORM_NONE = 0, NORM_RMS = 1, NORM_LN = 2 };
 
+// Paged KV addressing shared by the QKV epilogue and the attention kernels.
+struct PagedKV {
+  void* k;  // layer base of the pools [n_pages][H][page_size][dh]
+  void* v;
+  const int32_t* page_table;
+  int max_pages;
+  int page_size;
+  int n_pages;
+  const int32_t* seq_len;
+  int pos_off;  // row j of sequence b sits at position seq_len[b] + pos_off + j
+};
+
 enum Epi {
   EPI_STORE = 0,       // y[m][n] = acc
   EPI_RESID = 1,       // y[m][n] += acc  (and stash[m][n] = y[m][n] when stash != null)
@@ -19,7 +31,9 @@ enum Epi {
   EPI_GATED_SILU = 3,  // y[m][n] = silu(acc_gate) * acc_up
   EPI_BIAS_GELU = 4,   // y[m][n] = gelu_tanh(acc + bias[n])
   EPI_BIAS_RESID = 5,  // y[m][n] = (resid ? resid[m][n] : 0) + acc + bias[n]
-  EPI_ARGMAX = 6       // per-block (max, argmax) over n for each m; logits[m][n] = acc if wanted
+  EPI_ARGMAX = 6,      // per-block (max, argmax) over n for each m; logits[m][n] = acc if wanted
+  EPI_QKV = 7          // w = (wq, wk, wv): rotary on q and k (when rope_cos is set), q -> y[m][.],
+                       // k and v into the paged pools at the row's position (vector path only)
 };
 
 // y = epilogue( W . norm(x) ) for M rows.  The output features are up to three matrices of
@@ -51,12 +65,12 @@ struct LinearArgs {
   int n_parts = 0;            // filled by argmax_parts()
   float* logits = nullptr;    // [M][ldl] or null
   int ldl = 0;
-  // EPI_ARGMAX finalised in-kernel by the last block (when done_counter is set): the token of
-  // row m = b*tok_C + j goes to tok_dst0[b*tok_ld0 + tok_off0 + j] and tok_dst1[m] (if set).
-  unsigned* done_counter = nullptr;  // zero before the launch, zero again after it
-  int32_t* tok_dst0 = nullptr;
-  int tok_ld0 = 0, tok_off0 = 0, tok_C = 1;
-  int32_t* tok_dst1 = nullptr;
+  // EPI_QKV: row m = b*C + j sits at position kv.seq_len[b] + kv.pos_off + j
+  PagedKV kv = {};
+  int C = 1, n_heads = 0, d_head = 0, kvdtype = 0, max_seq = 0;
+  const float* rope_cos = nullptr;  // [max_seq][d_head/2] or null (no rotation)
+  const float* rope_sin = nullptr;
+  int32_t* status = nullptr;        // SSD_DEV_CAPACITY / SSD_DEV_BAD_PAGE bits
   // hi / lo bf16 planes of a gated epilogue's output (skinny path: the next MFMA operand)
   bf16_t* y_bf16 = nullptr;
   int ldy_bf16 = 0;
@@ -65,12 +79,19 @@ struct LinearArgs {
   int use_mfma = -1;          // -1: choose; 0: vector path; 1: MFMA path
 };
 
-// True when launch_linear(EPI_ARGMAX) finalises the tokens itself (else launch_argmax_final).
-bool linear_finalises_argmax(const LinearArgs& a);
+// Kernel-level timing of the profiled instantiation (the one-row GEMV with whole rows of up to
+// 2048 elements per batch, gemv_kernel<WT, 1, 4>): when start / stop are set and the launch takes
+// that kernel, it is launched with the events bound to its own dispatch (hipExtLaunchKernel), so
+// their elapsed time is the kernel's execution time; `timed` reports whether it happened.
+struct LaunchTiming {
+  hipEvent_t start = nullptr, stop = nullptr;
+  bool timed = false;
+};
 
 // Launch y = epilogue(W . norm(x)).  For EPI_ARGMAX, *n_parts receives the number of partials
 // per row written to part_val / part_idx (their row stride).
-hipError_t launch_linear(LinearArgs a, hipStream_t s, int* n_parts = nullptr);
+hipError_t launch_linear(LinearArgs a, hipStream_t s, int* n_parts = nullptr,
+                         LaunchTiming* timing = nullptr);
 
 // Upper bound of the partials per row for n_out outputs (workspace sizing).
 int argmax_parts_max(int n_out);
@@ -88,8 +109,9 @@ hipError_t launch_linear_skinny(const LinearArgs& a, const bf16_t* xb, int ldb, 
 hipError_t launch_norm_bf16(const float* x, int ldx, int M, int K, int norm, const float* gain,
                             const float* shift, float eps, bf16_t* out, int ldo, hipStream_t s);
 
-// True when launch_linear takes the weight-streaming path with one input row per block.
-bool linear_is_gemv_m1(const LinearArgs& a);
+
+// True when launch_linear takes the weight-streaming vector path (the one that has EPI_QKV).
+bool linear_is_vector(const LinearArgs& a);
 
 // Algorithmic HBM bytes of a launch: weights + input rows + output rows (+ residual reads).
 double linear_bytes(const LinearArgs& a);
@@ -112,18 +134,6 @@ struct EmbedArgs {
   int32_t* status;
 };
 hipError_t launch_embed(const EmbedArgs& a, hipStream_t s);
-
-// Paged KV addressing shared by the attention kernels.
-struct PagedKV {
-  void* k;  // layer base of the pools [n_pages][H][page_size][dh]
-  void* v;
-  const int32_t* page_table;
-  int max_pages;
-  int page_size;
-  int n_pages;
-  const int32_t* seq_len;
-  int pos_off;  // row j of sequence b sits at position seq_len[b] + pos_off + j
-};
 
 // q/k/v rows (qkv [R][3*HD], R = B*C) -> rotary (LLaMA) -> q_out [R][HD], K/V into the pools.
 struct RopeScatterArgs {

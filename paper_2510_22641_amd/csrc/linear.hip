@@ -17,6 +17,8 @@
 #include "device.h"
 #include "kernels.h"
 
+#include <hip/hip_ext.h>
+
 #include <climits>
 
 namespace ssd {
@@ -52,6 +54,21 @@ __device__ __forceinline__ RowPair<WT> row_pair(const LinearArgs& a, bool gated,
     r.w1 = reinterpret_cast<const WT*>(a.w[1]) + (size_t)q * K;
     return r;
   }
+  if (a.epi == EPI_QKV) {
+    // the pair (i, i + d_head/2) of one head of one matrix: the rotary pair
+    const int hd2 = a.n_per >> 1, half = a.d_head >> 1;
+    r.ok0 = r.ok1 = pr < 3 * hd2;
+    const int q = r.ok0 ? pr : 0;
+    const int mat = q >= hd2 ? (q >= 2 * hd2 ? 2 : 1) : 0;
+    const int loc = q - mat * hd2;
+    const int h = loc / half, i = loc - h * half;
+    const int c0 = h * a.d_head + i;
+    r.n0 = mat * a.n_per + c0;
+    r.n1 = r.n0 + half;
+    r.w0 = reinterpret_cast<const WT*>(a.w[mat]) + (size_t)c0 * K;
+    r.w1 = r.w0 + (size_t)half * K;
+    return r;
+  }
   r.n0 = 2 * pr;
   r.n1 = 2 * pr + 1;
   r.ok0 = r.n0 < n_total;
@@ -65,6 +82,63 @@ __device__ __forceinline__ RowPair<WT> row_pair(const LinearArgs& a, bool gated,
   r.w0 = reinterpret_cast<const WT*>(b0) + (size_t)v0 * K;
   r.w1 = reinterpret_cast<const WT*>(b1) + (size_t)v1 * K;
   return r;
+}
+
+// EPI_QKV epilogue of one rotary pair (columns c0 and c0 + d_head/2 of q, k or v) for the
+// block's input rows: rotate q and k by the row's position, then store q to y and k / v into
+// their page.  A position past the cache or an unmapped page sets a status bit and skips the KV
+// store.
+template <typename KT>
+__device__ __forceinline__ void store_kv_pair(const LinearArgs& a, int page, int slot, int h, int i,
+                                              int half, bool is_v, float e0, float e1) {
+  KT* base = reinterpret_cast<KT*>(is_v ? a.kv.v : a.kv.k) +
+             (((size_t)page * a.n_heads + h) * a.kv.page_size + slot) * a.d_head;
+  store_elem(base + i, e0);
+  store_elem(base + i + half, e1);
+}
+
+template <int MB>
+__device__ __forceinline__ void qkv_epilogue(const LinearArgs& a, int n0, const float (&acc)[2][MB],
+                                             int m0, int mrows) {
+  const int HD = a.n_per, half = a.d_head >> 1;
+  const int mat = n0 >= HD ? (n0 >= 2 * HD ? 2 : 1) : 0;
+  const int c0 = n0 - mat * HD;
+  const int h = c0 / a.d_head, i = c0 - h * a.d_head;
+#pragma unroll
+  for (int m = 0; m < MB; ++m) {
+    if (m >= mrows) break;
+    const int row = m0 + m;
+    const int b = row / a.C, j = row - b * a.C;
+    const int pos = a.kv.seq_len[b] + a.kv.pos_off + j;
+    float e0 = acc[0][m], e1 = acc[1][m];
+    if (mat < 2 && a.rope_cos) {
+      const int tp = pos < 0 ? 0 : (pos >= a.max_seq ? a.max_seq - 1 : pos);
+      const float cs = a.rope_cos[(size_t)tp * half + i], sn = a.rope_sin[(size_t)tp * half + i];
+      const float r0 = e0 * cs - e1 * sn, r1 = e1 * cs + e0 * sn;
+      e0 = r0;
+      e1 = r1;
+    }
+    if (mat == 0) {
+      a.y[(size_t)row * a.ldy + c0] = e0;
+      a.y[(size_t)row * a.ldy + c0 + half] = e1;
+      continue;
+    }
+    const int pg_i = pos >= 0 ? pos / a.kv.page_size : -1;
+    int page = -1;
+    if (pos < 0 || pos >= a.max_seq || pg_i >= a.kv.max_pages) {
+      atomicOr(a.status, SSD_DEV_CAPACITY);
+    } else {
+      page = a.kv.page_table[(size_t)b * a.kv.max_pages + pg_i];
+      if (page < 0 || page >= a.kv.n_pages) {
+        atomicOr(a.status, SSD_DEV_BAD_PAGE);
+        page = -1;
+      }
+    }
+    if (page < 0) continue;
+    const int slot = pos - pg_i * a.kv.page_size;
+    if (a.kvdtype == 1) store_kv_pair<bf16_t>(a, page, slot, h, i, half, mat == 2, e0, e1);
+    else store_kv_pair<float>(a, page, slot, h, i, half, mat == 2, e0, e1);
+  }
 }
 
 // Unconditional loads (a tail piece past K re-reads the row's last 8 elements and is skipped by
@@ -290,6 +364,8 @@ __global__ __launch_bounds__(256) void gemv_kernel(const LinearArgs a) {
         }
       }
     }
+  } else if (lane == 0 && live && a.epi == EPI_QKV) {
+    qkv_epilogue<MB>(a, r.n0, acc, m0, mrows);
   } else if (lane == 0 && live) {
 #pragma unroll
     for (int m = 0; m < MB; ++m) {
@@ -791,7 +867,7 @@ GvPlan gv_plan(const LinearArgs& a) {
 }
 
 template <typename WT, int MB, int KP>
-hipError_t launch_gemv_kp(const LinearArgs& a, const GvPlan& p, hipStream_t s) {
+hipError_t launch_gemv_kp(const LinearArgs& a, const GvPlan& p, hipStream_t s, LaunchTiming* t) {
   static bool attr = false;
   if (!attr) {
     (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&gemv_kernel<WT, MB, KP>),
@@ -800,31 +876,37 @@ hipError_t launch_gemv_kp(const LinearArgs& a, const GvPlan& p, hipStream_t s) {
   }
   dim3 grid(p.blocks, (a.M + MB - 1) / MB);
   const size_t shm = (size_t)MB * ((a.K + 7) & ~7) * sizeof(float);
-  hipLaunchKernelGGL((gemv_kernel<WT, MB, KP>), grid, dim3(256), shm, s, a);
+  if (MB == 1 && KP == 4 && t && t->start && t->stop) {
+    hipExtLaunchKernelGGL((gemv_kernel<WT, MB, KP>), grid, dim3(256), (uint32_t)shm, s, t->start,
+                          t->stop, 0u, a);
+    t->timed = true;
+  } else {
+    hipLaunchKernelGGL((gemv_kernel<WT, MB, KP>), grid, dim3(256), shm, s, a);
+  }
   return hipGetLastError();
 }
 
 // pieces per batch: the whole row up to 12 pieces (6144 elements), else batches of 8
 template <typename WT, int MB>
-hipError_t launch_gemv_mb(const LinearArgs& a, const GvPlan& p, hipStream_t s) {
+hipError_t launch_gemv_mb(const LinearArgs& a, const GvPlan& p, hipStream_t s, LaunchTiming* t) {
   const int pieces = (a.K + 511) / 512;
-  if (pieces <= 4) return launch_gemv_kp<WT, MB, 4>(a, p, s);
-  if (pieces <= 8 || pieces > 12) return launch_gemv_kp<WT, MB, 8>(a, p, s);
-  return launch_gemv_kp<WT, MB, 12>(a, p, s);
+  if (pieces <= 4) return launch_gemv_kp<WT, MB, 4>(a, p, s, t);
+  if (pieces <= 8 || pieces > 12) return launch_gemv_kp<WT, MB, 8>(a, p, s, t);
+  return launch_gemv_kp<WT, MB, 12>(a, p, s, t);
 }
 
 template <typename WT>
-hipError_t launch_gemv_t(const LinearArgs& a, hipStream_t s) {
+hipError_t launch_gemv_t(const LinearArgs& a, hipStream_t s, LaunchTiming* t) {
   const GvPlan p = gv_plan(a);
   switch (p.mb) {
-    case 1: return launch_gemv_mb<WT, 1>(a, p, s);
-    case 2: return launch_gemv_mb<WT, 2>(a, p, s);
-    case 3: return launch_gemv_mb<WT, 3>(a, p, s);
-    case 4: return launch_gemv_mb<WT, 4>(a, p, s);
-    case 5: return launch_gemv_mb<WT, 5>(a, p, s);
-    case 6: return launch_gemv_mb<WT, 6>(a, p, s);
-    case 7: return launch_gemv_mb<WT, 7>(a, p, s);
-    default: return launch_gemv_mb<WT, 8>(a, p, s);
+    case 1: return launch_gemv_mb<WT, 1>(a, p, s, t);
+    case 2: return launch_gemv_mb<WT, 2>(a, p, s, t);
+    case 3: return launch_gemv_mb<WT, 3>(a, p, s, t);
+    case 4: return launch_gemv_mb<WT, 4>(a, p, s, t);
+    case 5: return launch_gemv_mb<WT, 5>(a, p, s, t);
+    case 6: return launch_gemv_mb<WT, 6>(a, p, s, t);
+    case 7: return launch_gemv_mb<WT, 7>(a, p, s, t);
+    default: return launch_gemv_mb<WT, 8>(a, p, s, t);
   }
 }
 
@@ -872,9 +954,7 @@ hipError_t launch_row_stats(const float* x, int ldx, int M, int K, int norm, flo
   return hipGetLastError();
 }
 
-bool linear_is_gemv_m1(const LinearArgs& a) { return !want_mfma(a) && a.M == 1; }
-
-bool linear_finalises_argmax(const LinearArgs&) { return false; }
+bool linear_is_vector(const LinearArgs& a) { return !want_mfma(a); }
 
 double linear_bytes(const LinearArgs& a) {
   const bool gated = (a.epi == EPI_GATED_GELU || a.epi == EPI_GATED_SILU);
@@ -887,7 +967,7 @@ double linear_bytes(const LinearArgs& a) {
   return bytes;
 }
 
-hipError_t launch_linear(LinearArgs a, hipStream_t s, int* n_parts) {
+hipError_t launch_linear(LinearArgs a, hipStream_t s, int* n_parts, LaunchTiming* timing) {
   if (a.M <= 0) return hipSuccess;
   const bool gated = (a.epi == EPI_GATED_GELU || a.epi == EPI_GATED_SILU);
   const int n_out = gated ? a.n_per : a.n_per * a.n_mats;
@@ -907,7 +987,7 @@ hipError_t launch_linear(LinearArgs a, hipStream_t s, int* n_parts) {
   a.use_mfma = 0;
   if (a.epi == EPI_ARGMAX) a.n_parts = gv_plan(a).blocks;
   if (n_parts) *n_parts = a.n_parts;
-  return a.wdtype == 1 ? launch_gemv_t<bf16_t>(a, s) : launch_gemv_t<float>(a, s);
+  return a.wdtype == 1 ? launch_gemv_t<bf16_t>(a, s, timing) : launch_gemv_t<float>(a, s, timing);
 }
 
 }  // namespace ssd

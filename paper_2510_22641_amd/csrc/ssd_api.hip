@@ -32,7 +32,7 @@ int t5_bucket(int n, int buckets, int max_dist) {
 struct Layout {
   size_t x, x1, qkv, q, attn, ffn, inh, xi, stash, vis, part_val, part_idx, stats, bias_tab,
       bf_x, bf_attn, bf_ffn,
-      bucket, rope_cos, rope_sin, status, counters, cur_tok, g_pending, g_draft, g_target,
+      bucket, rope_cos, rope_sin, status, cur_tok, g_pending, g_draft, g_target,
       g_count, g_active, g_nactive, g_stats, total;
   int rows_max, head_rows, parts_max, ctx_max;
 };
@@ -75,7 +75,6 @@ bool make_layout(const ssd_dims& d, Layout& L) {
   L.rope_cos = take(d.arch == SSD_ARCH_LLAMA ? (size_t)d.max_seq * (d.d_head / 2) * 4 : 0);
   L.rope_sin = take(d.arch == SSD_ARCH_LLAMA ? (size_t)d.max_seq * (d.d_head / 2) * 4 : 0);
   L.status = take(4);
-  L.counters = take(64 * 4);
   L.cur_tok = take(B * 4);
   L.g_pending = take(B * 4);
   L.g_draft = take(B * (G > 0 ? G : 1) * 4);
@@ -177,23 +176,24 @@ PagedKV paged(ssd_ctx* c, int l, int pos_off) {
   return p;
 }
 
-// launch_linear, bracketed by events when profiling the one-row weight-streaming GEMV
+// launch_linear; when profiling, the launches of the profiled GEMV instantiation carry a pair of
+// events bound to their own dispatch (kernel execution time, as a kernel trace reports it)
 hipError_t run_linear(ssd_ctx* c, const LinearArgs& a, int* n_parts = nullptr) {
-  if (!c->profiling || !linear_is_gemv_m1(a)) return launch_linear(a, c->stream, n_parts);
+  if (!c->profiling) return launch_linear(a, c->stream, n_parts);
   while (c->ev_pool.size() < c->ev_used + 2) {
     hipEvent_t e;
     if (hipEventCreate(&e) != hipSuccess) return hipErrorOutOfMemory;
     c->ev_pool.push_back(e);
   }
-  hipEvent_t e0 = c->ev_pool[c->ev_used], e1 = c->ev_pool[c->ev_used + 1];
+  LaunchTiming t;
+  t.start = c->ev_pool[c->ev_used];
+  t.stop = c->ev_pool[c->ev_used + 1];
+  hipError_t err = launch_linear(a, c->stream, n_parts, &t);
+  if (err != hipSuccess || !t.timed) return err;
   c->ev_used += 2;
-  hipError_t err = hipEventRecord(e0, c->stream);
-  if (err != hipSuccess) return err;
-  err = launch_linear(a, c->stream, n_parts);
-  if (err != hipSuccess) return err;
   c->prof_bytes += linear_bytes(a);
   c->prof_launches += 1;
-  return hipEventRecord(e1, c->stream);
+  return hipSuccess;
 }
 
 LinearArgs lin(ssd_ctx* c) {
@@ -241,15 +241,24 @@ int run_layers(ssd_ctx* c, float* x, int B, int C, int pos_off, int l0, int l1, 
     a.x = x; a.ldx = D; a.M = R; a.K = D;
     a.norm = NORM_RMS; a.gain = lw.attn_norm;
     a.w[0] = lw.wq; a.w[1] = lw.wk; a.w[2] = lw.wv; a.n_mats = 3; a.n_per = HD;
-    a.epi = EPI_STORE; a.y = qkv; a.ldy = 3 * HD;
-    HIP_TRY(linear(a, nullptr, 0));
-    RopeScatterArgs rs;
-    rs.qkv = qkv; rs.q_out = q; rs.B = B; rs.C = C; rs.H = d.n_heads; rs.dh = d.d_head;
-    rs.kvdtype = d.kvdtype; rs.kv = paged(c, l, pos_off);
-    rs.rope_cos = t5 ? nullptr : c->at<float>(c->L.rope_cos);
-    rs.rope_sin = t5 ? nullptr : c->at<float>(c->L.rope_sin);
-    rs.max_seq = d.max_seq; rs.status = status;
-    HIP_TRY(launch_rope_scatter(rs, s));
+    a.epi = EPI_QKV; a.y = q; a.ldy = HD;
+    a.kv = paged(c, l, pos_off); a.C = C; a.n_heads = d.n_heads; a.d_head = d.d_head;
+    a.kvdtype = d.kvdtype; a.max_seq = d.max_seq; a.status = status;
+    a.rope_cos = t5 ? nullptr : c->at<float>(c->L.rope_cos);
+    a.rope_sin = t5 ? nullptr : c->at<float>(c->L.rope_sin);
+    if (!skinny && linear_is_vector(a)) {
+      // rotary and the KV store fused into the projection's epilogue
+      HIP_TRY(run_linear(c, a));
+    } else {
+      a.epi = EPI_STORE; a.y = qkv; a.ldy = 3 * HD;
+      HIP_TRY(linear(a, nullptr, 0));
+      RopeScatterArgs rs;
+      rs.qkv = qkv; rs.q_out = q; rs.B = B; rs.C = C; rs.H = d.n_heads; rs.dh = d.d_head;
+      rs.kvdtype = d.kvdtype; rs.kv = a.kv;
+      rs.rope_cos = a.rope_cos; rs.rope_sin = a.rope_sin;
+      rs.max_seq = d.max_seq; rs.status = status;
+      HIP_TRY(launch_rope_scatter(rs, s));
+    }
     AttnArgs at;
     at.q = q; at.out = attn; at.out_bf16 = skinny ? battn : nullptr;
     at.B = B; at.C = C; at.H = d.n_heads; at.dh = d.d_head;
@@ -312,8 +321,6 @@ int run_head(ssd_ctx* c, const float* x, int ldx, int M, int C, float* logits, i
   a.part_val = c->at<float>(c->L.part_val);
   a.part_idx = c->at<int>(c->L.part_idx);
   a.logits = logits; a.ldl = ldl;
-  a.done_counter = c->at<unsigned>(c->L.counters);
-  a.tok_dst0 = dst0; a.tok_ld0 = ld0; a.tok_off0 = off0; a.tok_C = C; a.tok_dst1 = dst1;
   int n_parts = 0;
   if (skinny_ok(M, d.d_model, d.wdtype)) {
     bf16_t* bx = c->at<bf16_t>(c->L.bf_x);
@@ -323,9 +330,8 @@ int run_head(ssd_ctx* c, const float* x, int ldx, int M, int C, float* logits, i
   } else {
     HIP_TRY(run_linear(c, a, &n_parts));
   }
-  if (!linear_finalises_argmax(a))
-    HIP_TRY(launch_argmax_final(a.part_val, a.part_idx, M, n_parts, C, dst0, ld0, off0, dst1,
-                                c->stream));
+  HIP_TRY(launch_argmax_final(a.part_val, a.part_idx, M, n_parts, C, dst0, ld0, off0, dst1,
+                              c->stream));
   return SSD_OK;
 }
 
@@ -501,7 +507,6 @@ int ssd_create(const ssd_dims* dims, const ssd_weights* w, const ssd_kv* kv, voi
   }
   if (rc == SSD_OK &&
       (hipMemsetAsync(c->at<int32_t>(L.status), 0, 4, c->stream) != hipSuccess ||
-       hipMemsetAsync(c->at<int32_t>(L.counters), 0, 64 * 4, c->stream) != hipSuccess ||
        hipStreamSynchronize(c->stream) != hipSuccess))
     rc = SSD_ERR_HIP;
   if (rc != SSD_OK) {
