@@ -29,16 +29,16 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published
 
 
-def draft_step_bytes(shape, k: int, ctx: int) -> float:
+def draft_step_bytes(shape, k: int, ctx: int, kv_bytes: int = 4) -> float:
     """Algorithmic bytes of one batch-1 draft step at context length ctx (weights read once,
-    KV of layers 1..k read, one position's K/V written)."""
+    KV of layers 1..k read, one position's K/V written; kv_bytes per cached element)."""
     we = 2 if shape.dtype == "bf16" else 4
     d, hd, f, V, h = shape.d_model, shape.hd, shape.d_ff, shape.vocab, shape.in_width
     layer = (4 * d * hd + 3 * d * f) * we + 3 * d * 4  # QKVO + FFN + norm gains
-    kv = 2 * ctx * hd * we + 2 * hd * we
+    kv = 2 * ctx * hd * kv_bytes + 2 * hd * kv_bytes
     if shape.arch == "t5":
         layer += 2 * d * hd * we + d * 4
-        kv += 2 * shape.n_visual * hd * we
+        kv += 2 * shape.n_visual * hd * kv_bytes
     imit = 2 * d * h * we + (h + 3 * d) * 4
     head = V * d * we + d * 4
     return k * (layer + kv) + imit + head
@@ -145,23 +145,29 @@ def main():
         torch.cuda.synchronize()
         times.append(e0.elapsed_time(e1) * 1e-3 / g)
     step_s = float(np.median(times))
-    step_bytes = draft_step_bytes(sh, wl.draft_layers, int(np.median(ctxs)) + g // 2)
+    step_bytes = draft_step_bytes(sh, wl.draft_layers, int(np.median(ctxs)) + g // 2,
+                                  dd.k_pool.element_size())
     draft = {"us": round(step_s * 1e6, 2), "bytes": int(step_bytes),
              "GBps": round(step_bytes / step_s / 1e9, 1),
              "frac": round(step_bytes / step_s / 1e9 / HBM_PEAK_GBS, 4)}
 
-    # dominant kernel: every launch of the one-row weight-streaming GEMV instantiation that rocprof
-    # names gemv_kernel<T, 1, 4>, timed by events bound to its own dispatch
+    # dominant kernel: every launch of the one-row weight-streaming GEMV instantiation that streams
+    # the d_model-wide matrices (rocprof's gemv_kernel<T, 1, KP>), timed by events bound to its
+    # own dispatch
     abi.ssd_profile_enable(dd.ctx, True)
     abi.ssd_profile_read(dd.ctx)
     for _ in range(max(1, args.steps // 2)):
         dd.generate(pt, vt, T, g, speculative=True, reuse=True)
     n_launch, secs, nbytes = abi.ssd_profile_read(dd.ctx)
     abi.ssd_profile_enable(dd.ctx, False)
-    per_launch_bytes = nbytes / max(1, n_launch)
-    avg_s = secs / max(1, n_launch)
+    if n_launch == 0 or secs <= 0:
+        raise RuntimeError("no launch of the profiled GEMV was timed")
+    per_launch_bytes = nbytes / n_launch
+    avg_s = secs / n_launch
     achieved = per_launch_bytes / avg_s / 1e9
-    kname = "gemv_kernel<%s, 1, 4>" % ("unsigned short" if sh.dtype == "bf16" else "float")
+    pieces = (sh.d_model + 511) // 512
+    kp = 4 if pieces <= 4 else (12 if 8 < pieces <= 12 else 8)
+    kname = "gemv_kernel<%s, 1, %d>" % ("unsigned short" if sh.dtype == "bf16" else "float", kp)
     roofline = {"bound": "hbm", "kernel": kname + " (one-row weight-streaming GEMV)",
                 "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
@@ -186,7 +192,8 @@ def main():
         "warmup": args.warmup, "ms_per_step": round(dt / args.steps * 1e3, 3),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
         "data": "synthetic (seeded random-init decoder, N(0,1) visual tokens, uniform prompt ids)",
-        "config": {"workload": wl.name, "decoder": f"T5-style L{sh.n_layers} d{sh.d_model} "
+        "config": {"workload": wl.name, "decoder": f"{'T5' if sh.arch == 't5' else 'LLaMA'}-style "
+                   f"L{sh.n_layers} d{sh.d_model} "
                    f"H{sh.n_heads}x{sh.d_head} ff{sh.d_ff} V{sh.vocab}", "batch": B,
                    "prompt": wl.prompt_len, "visual_tokens": sh.n_visual,
                    "draft_layers": wl.draft_layers, "gamma": g, "new_tokens": T,

@@ -189,8 +189,9 @@ int ssd_generate(ssd_ctx* ctx, int B, int P, const int32_t* d_prompt, const void
 int ssd_set_graphs(ssd_ctx* ctx, int enable);
 
 /* Kernel timing for roofline reports.  While enabled (and graphs are bypassed), every launch of
- * the weight-streaming GEMV with one input row and rows of at most 2048 elements
- * (gemv_kernel<T, 1, 4>, the kernel that carries most of a batch-1 draft step) is launched with
+ * the weight-streaming GEMV instantiation with one input row that streams the d_model-wide
+ * matrices (gemv_kernel<T, 1, KP>, KP = 4 for d_model <= 2048, 12 for 4096 < d_model <= 6144,
+ * else 8: the kernel that carries most of a batch-1 draft step) is launched with
  * two HIP events bound to its own dispatch on the context's stream, so their elapsed time is the
  * kernel's execution time; its algorithmic bytes (weights + input rows + output rows) are added
  * up.  ssd_profile_read synchronises the stream and returns the number of such launches, the

@@ -70,6 +70,7 @@ def main(argv=None):
         w = synth.make_weights(wl.shape, seed, 1.0, wl.boundary)
         dec = Decoder(wl.shape, w, wl.draft_layers)
         del w
+        print(f"{wl.name} seed={seed}: decoder ready ({time.time() - t0:.0f}s)", flush=True)
         z = synth.make_visual(wl.shape, seed, 1)[0]
         pr = synth.make_prompts(wl.shape, seed, 1, wl.prompt_len)[0]
         scaled = [(n, l, tid, kind) for n, l, tid, kind in tensor_list(wl.shape)

@@ -29,13 +29,17 @@ __device__ __forceinline__ void unpack_bf16x8(const uint4& r, float* f) {
   f[6] = __uint_as_float(r.w << 16); f[7] = __uint_as_float(r.w & 0xffff0000u);
 }
 
-__device__ __forceinline__ uint4 pack_bf16x8(const float* f) {
-  uint4 r;
-  r.x = f32_to_bf16(f[0]) | (f32_to_bf16(f[1]) << 16);
-  r.y = f32_to_bf16(f[2]) | (f32_to_bf16(f[3]) << 16);
-  r.z = f32_to_bf16(f[4]) | (f32_to_bf16(f[5]) << 16);
-  r.w = f32_to_bf16(f[6]) | (f32_to_bf16(f[7]) << 16);
-  return r;
+// Split eight floats into bf16 planes hi = bf16(f), lo = bf16(f - hi): hi + lo carries about 16
+// mantissa bits, so two bf16 MFMAs over (hi, lo) act on near-fp32 activations.
+__device__ __forceinline__ void split_bf16x8(const float* f, uint4& hi, uint4& lo) {
+  uint32_t h[8], l[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    h[e] = f32_to_bf16(f[e]);
+    l[e] = f32_to_bf16(f[e] - bf16_to_f32(h[e]));
+  }
+  hi = make_uint4(h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16), h[6] | (h[7] << 16));
+  lo = make_uint4(l[0] | (l[1] << 16), l[2] | (l[3] << 16), l[4] | (l[5] << 16), l[6] | (l[7] << 16));
 }
 
 // Eight consecutive elements of a weight (or KV) row, as raw registers until converted.

@@ -79,14 +79,18 @@ struct LinearArgs {
   int use_mfma = -1;          // -1: choose; 0: vector path; 1: MFMA path
 };
 
-// Kernel-level timing of the profiled instantiation (the one-row GEMV with whole rows of up to
-// 2048 elements per batch, gemv_kernel<WT, 1, 4>): when start / stop are set and the launch takes
-// that kernel, it is launched with the events bound to its own dispatch (hipExtLaunchKernel), so
-// their elapsed time is the kernel's execution time; `timed` reports whether it happened.
+// Kernel-level timing of one instantiation of the one-row GEMV, gemv_kernel<WT, 1, kp>: when
+// start / stop are set and the launch takes that kernel, it is launched with the events bound to
+// its own dispatch (hipExtLaunchKernel), so their elapsed time is the kernel's execution time;
+// `timed` reports whether it happened.
 struct LaunchTiming {
   hipEvent_t start = nullptr, stop = nullptr;
+  int kp = 4;
   bool timed = false;
 };
+
+// Pieces per batch (the KP of gemv_kernel) the vector path uses for rows of K elements.
+int gemv_pieces(int K);
 
 // Launch y = epilogue(W . norm(x)).  For EPI_ARGMAX, *n_parts receives the number of partials
 // per row written to part_val / part_idx (their row stride).
@@ -197,7 +201,7 @@ struct AcceptArgs {
   const int32_t* active;  // [B] or null
   int32_t* seq_len;
   int max_seq;
-  int next_need;          // positions the next round needs beyond seq_len (gamma+1)
+  int next_need;          // positions a following round needs beyond seq_len (0: none known)
   int32_t* status;
   // generation bookkeeping (null when called through ssd_accept)
   int32_t* tokens;        // [B][T]

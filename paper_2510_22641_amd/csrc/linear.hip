@@ -632,13 +632,15 @@ __global__ __launch_bounds__(256) void norm_bf16_kernel(const float* __restrict_
 }
 
 // ---------------------------------------------------------------------------------------------
-// MFMA tile path
+// MFMA tile path: 64x64 output tiles, K in steps of 64 staged through LDS.  The activations
+// (normalised on the fly) are staged as bf16 hi / lo planes and each 16x16x32 step issues two
+// MFMAs against the same weight fragment, so the products see near-fp32 inputs.
 constexpr int TM = 64, TN = 64, TK = 64, TKP = TK + 8;
 
 template <bool GATED>
 __global__ __launch_bounds__(256) void gemm_kernel(const LinearArgs a) {
   constexpr int NB = GATED ? 2 : 1;
-  __shared__ __attribute__((aligned(16))) bf16_t As[TM][TKP];
+  __shared__ __attribute__((aligned(16))) bf16_t As[2][TM][TKP];  // hi, lo planes
   __shared__ __attribute__((aligned(16))) bf16_t Bs[NB][TN][TKP];
   __shared__ float am_v[TM][TN / 16];
   __shared__ int am_i[TM][TN / 16];
@@ -689,7 +691,9 @@ __global__ __launch_bounds__(256) void gemm_kernel(const LinearArgs a) {
 #pragma unroll
       for (int q = 0; q < 16; ++q) f[q] = 0.f;
     }
-    const uint4 pa0 = pack_bf16x8(f), pa1 = pack_bf16x8(f + 8);
+    uint4 pa0, pa1, pl0, pl1;
+    split_bf16x8(f, pa0, pl0);
+    split_bf16x8(f + 8, pa1, pl1);
     uint4 pb[NB][2];
 #pragma unroll
     for (int b = 0; b < NB; ++b) {
@@ -702,8 +706,10 @@ __global__ __launch_bounds__(256) void gemm_kernel(const LinearArgs a) {
       }
     }
     __syncthreads();
-    *reinterpret_cast<uint4*>(&As[lr][lk]) = pa0;
-    *reinterpret_cast<uint4*>(&As[lr][lk + 8]) = pa1;
+    *reinterpret_cast<uint4*>(&As[0][lr][lk]) = pa0;
+    *reinterpret_cast<uint4*>(&As[0][lr][lk + 8]) = pa1;
+    *reinterpret_cast<uint4*>(&As[1][lr][lk]) = pl0;
+    *reinterpret_cast<uint4*>(&As[1][lr][lk + 8]) = pl1;
 #pragma unroll
     for (int b = 0; b < NB; ++b) {
       *reinterpret_cast<uint4*>(&Bs[b][lr][lk]) = pb[b][0];
@@ -713,10 +719,12 @@ __global__ __launch_bounds__(256) void gemm_kernel(const LinearArgs a) {
 #pragma unroll
     for (int ks = 0; ks < TK; ks += 32) {
       const int kk = ks + (lane >> 4) * 8;
-      bf16x8_t af[2], bfr[NB][2];
+      bf16x8_t af[2][2], bfr[NB][2];
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
-        af[i] = *reinterpret_cast<const bf16x8_t*>(&As[wm + 16 * i + (lane & 15)][kk]);
+      for (int pl = 0; pl < 2; ++pl)
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+          af[pl][i] = *reinterpret_cast<const bf16x8_t*>(&As[pl][wm + 16 * i + (lane & 15)][kk]);
 #pragma unroll
       for (int b = 0; b < NB; ++b)
 #pragma unroll
@@ -727,8 +735,10 @@ __global__ __launch_bounds__(256) void gemm_kernel(const LinearArgs a) {
 #pragma unroll
         for (int i = 0; i < 2; ++i)
 #pragma unroll
-          for (int j = 0; j < 2; ++j)
-            acc[b][i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[b][j], acc[b][i][j], 0, 0, 0);
+          for (int j = 0; j < 2; ++j) {
+            acc[b][i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[0][i], bfr[b][j], acc[b][i][j], 0, 0, 0);
+            acc[b][i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[1][i], bfr[b][j], acc[b][i][j], 0, 0, 0);
+          }
     }
   }
 
@@ -876,7 +886,7 @@ hipError_t launch_gemv_kp(const LinearArgs& a, const GvPlan& p, hipStream_t s, L
   }
   dim3 grid(p.blocks, (a.M + MB - 1) / MB);
   const size_t shm = (size_t)MB * ((a.K + 7) & ~7) * sizeof(float);
-  if (MB == 1 && KP == 4 && t && t->start && t->stop) {
+  if (MB == 1 && t && KP == t->kp && t->start && t->stop) {
     hipExtLaunchKernelGGL((gemv_kernel<WT, MB, KP>), grid, dim3(256), (uint32_t)shm, s, t->start,
                           t->stop, 0u, a);
     t->timed = true;
@@ -887,12 +897,25 @@ hipError_t launch_gemv_kp(const LinearArgs& a, const GvPlan& p, hipStream_t s, L
 }
 
 // pieces per batch: the whole row up to 12 pieces (6144 elements), else batches of 8
+}  // namespace
+
+// whole rows up to 12 pieces of 512 elements (6144) in one batch, else batches of 8
+int gemv_pieces(int K) {
+  const int pieces = (K + 511) / 512;
+  if (pieces <= 4) return 4;
+  if (pieces <= 8 || pieces > 12) return 8;
+  return 12;
+}
+
+namespace {
+
 template <typename WT, int MB>
 hipError_t launch_gemv_mb(const LinearArgs& a, const GvPlan& p, hipStream_t s, LaunchTiming* t) {
-  const int pieces = (a.K + 511) / 512;
-  if (pieces <= 4) return launch_gemv_kp<WT, MB, 4>(a, p, s, t);
-  if (pieces <= 8 || pieces > 12) return launch_gemv_kp<WT, MB, 8>(a, p, s, t);
-  return launch_gemv_kp<WT, MB, 12>(a, p, s, t);
+  switch (gemv_pieces(a.K)) {
+    case 4: return launch_gemv_kp<WT, MB, 4>(a, p, s, t);
+    case 12: return launch_gemv_kp<WT, MB, 12>(a, p, s, t);
+    default: return launch_gemv_kp<WT, MB, 8>(a, p, s, t);
+  }
 }
 
 template <typename WT>

@@ -188,6 +188,7 @@ hipError_t run_linear(ssd_ctx* c, const LinearArgs& a, int* n_parts = nullptr) {
   LaunchTiming t;
   t.start = c->ev_pool[c->ev_used];
   t.stop = c->ev_pool[c->ev_used + 1];
+  t.kp = gemv_pieces(c->d.d_model);  // the instantiation that streams the d_model-wide matrices
   hipError_t err = launch_linear(a, c->stream, n_parts, &t);
   if (err != hipSuccess || !t.timed) return err;
   c->ev_used += 2;
@@ -610,7 +611,8 @@ int ssd_accept(ssd_ctx* c, int B, int gamma, const int32_t* d_draft, const int32
   std::memset(&a, 0, sizeof(a));
   a.B = B; a.gamma = gamma; a.draft = d_draft; a.target = d_target; a.pending = d_pending;
   a.out = d_out; a.accept_len = d_accept_len; a.active = d_active; a.seq_len = c->kv.seq_len;
-  a.max_seq = c->d.max_seq; a.next_need = gamma + 1;
+  // the caller decides whether another round follows: only a length past the cache is flagged
+  a.max_seq = c->d.max_seq; a.next_need = 0;
   a.status = c->at<int32_t>(c->L.status);
   HIP_TRY(launch_accept(a, c->stream));
   c->draft_valid = false;

@@ -76,8 +76,10 @@ def poison_stale_kv(dd) -> None:
 
 
 def device_run(dd, prompt_t, visual_t, T: int, gamma: int, reuse: bool = False,
-               logits: bool = True, poison: bool = False, forced=None) -> DevRun:
-    """Step through prefill / draft / verify / accept via the C ABI and record everything."""
+               logits: bool = True, poison: bool = False, forced=None,
+               max_rounds: Optional[int] = None) -> DevRun:
+    """Step through prefill / draft / verify / accept via the C ABI and record everything
+    (at most ``max_rounds`` rounds when given)."""
     import torch
     B = prompt_t.shape[0]
     pending, lg0 = dd.prefill(prompt_t, visual_t, logits=logits)
@@ -87,7 +89,7 @@ def device_run(dd, prompt_t, visual_t, T: int, gamma: int, reuse: bool = False,
     active.fill_(1)
     if poison:
         poison_stale_kv(dd)
-    for rnd in range(T):
+    for rnd in range(T if max_rounds is None else min(T, max_rounds)):
         act = np.array([len(t) < T for t in run.tokens])
         if not act.any():
             break
@@ -116,9 +118,10 @@ def device_run(dd, prompt_t, visual_t, T: int, gamma: int, reuse: bool = False,
 
 
 def check_run_against_oracle(dec: Decoder, shape, prompt, visual, run: DevRun, b: int, gamma: int,
-                             use_imitation: bool = True):
-    """Replay sequence b of a device run through the oracle; returns the count of near-ties."""
-    rounds = [r for r in run.rounds if r.active[b]]
+                             use_imitation: bool = True, max_rounds: Optional[int] = None):
+    """Replay sequence b of a device run (its first ``max_rounds`` rounds when given) through
+    the oracle; returns the count of near-ties."""
+    rounds = [r for r in run.rounds if r.active[b]][:max_rounds]
     lg0, orounds = decode.replay(dec, prompt, visual, int(run.pending0[b]),
                                  [(r.drafts[b], r.targets[b]) for r in rounds], gamma,
                                  use_imitation=use_imitation)

@@ -182,3 +182,28 @@ def test_error_codes_and_device_status():
     rc, st = dd.sync_status()
     assert rc == abi.SSD_ERR_DEVICE and st & abi.SSD_DEV_BAD_TOKEN
     assert dd.sync_status() == (0, 0)
+
+
+def test_positions_past_the_cache_are_reported_not_written():
+    """Greedy steps fill the cache to its last position; a draft of gamma tokens then reaches
+    past it: the KV stores beyond max_seq are skipped and the device status says so.  Rounds
+    that stay inside the cache never raise the bit, including a final round that ends at the
+    last position."""
+    from paper_2510_22641_amd import ssd as abi
+    wl = synth.S1
+    dd, dec, pr, z, pt, vt = _setup(wl, seed=4)
+    max_seq = dd.cap.max_seq
+    pending, _ = dd.prefill(pt, vt)
+    nd = dd.buf("no_draft", (1, 1))
+    while int(dd.seq_len[0].item()) < max_seq - 1:
+        t, _ = dd.verify(pending, nd, 0)
+        dd.accept(nd, t, pending, 0)
+    assert dd.sync_status() == (0, 0)
+    k_before = dd.k_pool.clone()
+    dd.draft(pending, wl.gamma)
+    rc, st = dd.sync_status()
+    assert rc == abi.SSD_ERR_DEVICE and st == abi.SSD_DEV_CAPACITY
+    # only the one in-range position (max_seq - 1) of layers 1..k was written
+    changed = (dd.k_pool != k_before).reshape(dd.k_pool.shape[0], -1).any(dim=1).cpu().numpy()
+    assert changed[: wl.draft_layers].all() and not changed[wl.draft_layers:].any()
+    assert dd.sync_status() == (0, 0)
