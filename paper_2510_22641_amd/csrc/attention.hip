@@ -6,7 +6,8 @@
 // for LLaMA, scaled by 1/sqrt(dh) with q and k already rotated.  Cross-attention (T5): all n_keys
 // visual keys, no mask, no bias, no scale.
 //
-// One block per (head, sequence, up to 8 query rows).  Every thread issues its key row and its
+// One block per (head, sequence, query row) for chunks of up to 16 rows, else per (head,
+// sequence, 8 query rows).  Every thread issues its key row and its
 // first value chunks before the first barrier (they do not depend on the scores); scores for the
 // live rows go to LDS, one wave per row turns them into softmax numerators, and P.V splits the
 // keys over all threads (16-byte value chunks, 8 loads in flight per thread) with a shuffle + LDS
@@ -220,8 +221,10 @@ template <typename KT, int DH>
 hipError_t launch_attn_dh(const AttnArgs& a, hipStream_t s) {
   const int nk_max = a.cross ? a.n_keys : a.max_seq;
   const int s_stride = (nk_max + 63) & ~63;
-  if (a.C == 1) {
-    dim3 grid(a.H, a.B, 1);
+  if (a.C <= 16) {
+    // decode steps and verify chunks: one block per (head, sequence, query row); the rows of a
+    // chunk re-read the same keys from L2, and 16x more blocks keep the chip busy
+    dim3 grid(a.H, a.B, a.C);
     const size_t shm = (size_t)s_stride * sizeof(float);
     hipLaunchKernelGGL((attn_kernel<KT, DH, 1>), grid, dim3(256), shm, s, a, s_stride);
   } else {

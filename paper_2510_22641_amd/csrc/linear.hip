@@ -465,16 +465,8 @@ __global__ __launch_bounds__(256) void gemv_mfma_kernel(const LinearArgs a, cons
   for (int b = 0; b < NB; ++b) acc[b] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   for (int s0 = s_beg; s0 < s_end; s0 += SK) {
     uint4 wv[NB][SK][2], bv[SK][2], bl[SK][2];
-#pragma unroll
-    for (int u = 0; u < SK; ++u) {
-      const int st = min(s0 + u, s_end - 1);
-#pragma unroll
-      for (int b = 0; b < NB; ++b) {
-        const uint4* wp = reinterpret_cast<const uint4*>(wrow[b] + st * 64 + kq);
-        wv[b][u][0] = wp[0];
-        wv[b][u][1] = wp[1];
-      }
-    }
+    // activations first (L2-resident, they arrive early), then the weights in step order: the
+    // wait counter retires loads in issue order, so step u waits only for its own weights
 #pragma unroll
     for (int u = 0; u < SK; ++u) {
       const int st = min(s0 + u, s_end - 1);
@@ -487,10 +479,23 @@ __global__ __launch_bounds__(256) void gemv_mfma_kernel(const LinearArgs a, cons
     }
 #pragma unroll
     for (int u = 0; u < SK; ++u) {
-      if (s0 + u >= s_end) break;
+      const int st = min(s0 + u, s_end - 1);
+#pragma unroll
+      for (int b = 0; b < NB; ++b) {
+        const uint4* wp = reinterpret_cast<const uint4*>(wrow[b] + st * 64 + kq);
+        wv[b][u][0] = wp[0];
+        wv[b][u][1] = wp[1];
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);  // keep the whole batch in flight before the first MFMA
+#pragma unroll
+    for (int u = 0; u < SK; ++u) {
+      // a step past this wave's range re-read a clamped step: zero operands instead of a branch
+      // (a branch would let the compiler sink the loads into it and serialise the batch)
+      const bool use = tok_ok && (s0 + u < s_end);
       const uint4 z = make_uint4(0, 0, 0, 0);
-      const uint4 b0 = tok_ok ? bv[u][0] : z, b1 = tok_ok ? bv[u][1] : z;
-      const uint4 c0 = tok_ok ? bl[u][0] : z, c1 = tok_ok ? bl[u][1] : z;
+      const uint4 b0 = use ? bv[u][0] : z, b1 = use ? bv[u][1] : z;
+      const uint4 c0 = use ? bl[u][0] : z, c1 = use ? bl[u][1] : z;
 #pragma unroll
       for (int b = 0; b < NB; ++b) {
         const bf16x8_t w0 = *reinterpret_cast<const bf16x8_t*>(&wv[b][u][0]);
