@@ -44,6 +44,98 @@ def draft_step_bytes(shape, k: int, ctx: int, kv_bytes: int = 4) -> float:
     return k * (layer + kv) + imit + head
 
 
+def verify_bytes(shape, B: int, gamma: int, ctx: int, kv_bytes: int = 4) -> float:
+    """Algorithmic bytes of one verify pass (all L layers and the LM head read once; KV of every
+    layer read for B sequences at context ctx; gamma+1 positions of K/V written per sequence)."""
+    we = 2 if shape.dtype == "bf16" else 4
+    d, hd, f, V = shape.d_model, shape.hd, shape.d_ff, shape.vocab
+    layer = (4 * d * hd + 3 * d * f) * we + 3 * d * 4
+    kv = B * (2 * ctx * hd + 2 * (gamma + 1) * hd) * kv_bytes
+    if shape.arch == "t5":
+        layer += 2 * d * hd * we + d * 4
+        kv += B * 2 * shape.n_visual * hd * kv_bytes
+    return shape.n_layers * (layer + kv) + V * d * we + d * 4
+
+
+def step_timings(dd, pt, vt, B: int, g: int, rounds: int = 8):
+    """Median per-step draft time and per-pass verify time over a few rounds after prefill (HIP
+    events on the decoder's stream around the captured draft and verify graphs)."""
+    import numpy as np
+    import torch
+    from paper_2510_22641_amd import ssd as abi
+    pending, _ = dd.prefill(pt, vt)
+    s = dd.stream
+    dts, vts, ctxs = [], [], []
+    for _ in range(rounds):
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        ctxs.append(int(dd.seq_len[:B].float().mean().item()))
+        s.wait_stream(torch.cuda.current_stream())
+        d = dd.buf("draft", (B, g))
+        ev[0].record(s)
+        abi.ssd_draft(dd.ctx, B, g, pending, d, None)
+        ev[1].record(s)
+        t = dd.buf("target", (B, g + 1))
+        abi.ssd_verify(dd.ctx, B, g, pending, d, 1, t, None)
+        ev[2].record(s)
+        dd.accept(d, t, pending, g)
+        torch.cuda.synchronize()
+        dts.append(ev[0].elapsed_time(ev[1]) * 1e-3 / g)
+        vts.append(ev[1].elapsed_time(ev[2]) * 1e-3)
+    return float(np.median(dts)), float(np.median(vts)), int(np.median(ctxs))
+
+
+def sweep_c4(args):
+    """The FlanT5-xl sweep: batch {1, 8} x draft depth {4, 8, 12} x gamma {2, 4, 8} over one
+    decoder (deep layers scaled from layer 7 on); one JSON line per point."""
+    import torch
+    import synth
+    from paper_2510_22641_amd import runtime
+    pts = synth.c4_points()
+    weights = synth.workload_weights(pts[0], args.seed)
+    for k in sorted({p.draft_layers for p in pts}):
+        group = [p for p in pts if p.draft_layers == k]
+        mb = max(p.batch for p in group)
+        dd = runtime.from_workload(group[0], args.seed, weights=weights, max_batch=mb,
+                                   max_gamma=max(p.gamma for p in group))
+        for wl in group:
+            sh, B, T, g = wl.shape, wl.batch, wl.new_tokens, wl.gamma
+            prompts = synth.make_prompts(sh, args.seed, B, wl.prompt_len)
+            visual = synth.make_visual(sh, args.seed, B)
+            pt, vt = dd.upload_inputs(prompts, visual)
+
+            def timed(spec):
+                for _ in range(args.warmup):
+                    dd.generate(pt, vt, T, g, speculative=spec, reuse=True)
+                torch.cuda.synchronize()
+                t0 = time.perf_counter()
+                for _ in range(args.steps):
+                    toks, st = dd.generate(pt, vt, T, g, speculative=spec, reuse=True)
+                torch.cuda.synchronize()
+                return time.perf_counter() - t0, st, toks
+
+            dt, st, toks = timed(True)
+            dtg, _, gtoks = timed(False)
+            d_s, v_s, ctx = step_timings(dd, pt, vt, B, g)
+            db = draft_step_bytes(sh, k, ctx, dd.k_pool.element_size())
+            db += (B - 1) * 2 * k * (ctx + (sh.n_visual if sh.arch == "t5" else 0)) * sh.hd * \
+                dd.k_pool.element_size()
+            vb = verify_bytes(sh, B, g, ctx, dd.k_pool.element_size())
+            rec = {"workload": wl.name, "batch": B, "draft_layers": k, "gamma": g, "new_tokens": T,
+                   "tokens_per_s": round(B * T * args.steps / dt, 2),
+                   "greedy_tokens_per_s": round(B * T * args.steps / dtg, 2),
+                   "speedup_vs_greedy": round(dtg / dt, 3),
+                   "acceptance_rate": round(st["accepted"] / max(1, st["drafted"]), 4),
+                   "ssd_equals_greedy_tokens": bool(torch.equal(toks, gtoks)),
+                   "draft_step": {"us": round(d_s * 1e6, 2), "bytes": int(db),
+                                  "frac": round(db / d_s / 1e9 / HBM_PEAK_GBS, 4)},
+                   "verify": {"us": round(v_s * 1e6, 2), "bytes": int(vb),
+                              "frac": round(vb / v_s / 1e9 / HBM_PEAK_GBS, 4)}}
+            print(json.dumps(rec), flush=True)
+        dd.close()
+        del dd
+        torch.cuda.empty_cache()
+
+
 def cpu_baseline(wl, weights, prompt, visual, budget_s: float):
     """The float64 oracle's Algorithm 1 on the host, over as many rounds as fit the budget."""
     import numpy as np
@@ -83,11 +175,16 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--cpu-seconds", type=float, default=20.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--sweep", choices=["c4"], default=None,
+                    help="run the FlanT5-xl sweep instead (one JSON line per point)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU: the decode loop is not sharded (asked for {args.gpus})",
               file=sys.stderr)
         sys.exit(2)
+    if args.sweep:
+        sweep_c4(args)
+        return
 
     import numpy as np
     import torch
@@ -129,31 +226,19 @@ def main():
     print(f"[bench] greedy {greedy_tps:.1f} tok/s", file=sys.stderr, flush=True)
 
     # draft-step time: events around the gamma-step draft call (captured graph) on its stream
-    pending, _ = dd.prefill(pt, vt)
-    s = dd.stream
-    times, ctxs = [], []
-    for _ in range(8):
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        ctxs.append(int(dd.seq_len[0].item()))
-        s.wait_stream(torch.cuda.current_stream())
-        e0.record(s)
-        abi.ssd_draft(dd.ctx, B, g, pending, dd.buf("draft", (B, g)), None)
-        e1.record(s)
-        d = dd.buf("draft", (B, g))
-        t, _ = dd.verify(pending, d, g, reuse=True)
-        dd.accept(d, t, pending, g)
-        torch.cuda.synchronize()
-        times.append(e0.elapsed_time(e1) * 1e-3 / g)
-    step_s = float(np.median(times))
-    step_bytes = draft_step_bytes(sh, wl.draft_layers, int(np.median(ctxs)) + g // 2,
-                                  dd.k_pool.element_size())
+    step_s, verify_s, ctx = step_timings(dd, pt, vt, B, g)
+    step_bytes = draft_step_bytes(sh, wl.draft_layers, ctx, dd.k_pool.element_size())
     draft = {"us": round(step_s * 1e6, 2), "bytes": int(step_bytes),
              "GBps": round(step_bytes / step_s / 1e9, 1),
              "frac": round(step_bytes / step_s / 1e9 / HBM_PEAK_GBS, 4)}
+    vbytes = verify_bytes(sh, B, g, ctx, dd.k_pool.element_size())
+    verify = {"us": round(verify_s * 1e6, 2), "bytes": int(vbytes),
+              "GBps": round(vbytes / verify_s / 1e9, 1),
+              "frac": round(vbytes / verify_s / 1e9 / HBM_PEAK_GBS, 4)}
 
     # dominant kernel: every launch of the one-row weight-streaming GEMV instantiation that streams
-    # the d_model-wide matrices (rocprof's gemv_kernel<T, 1, KP>), timed by events bound to its
-    # own dispatch
+    # the RMS-normalised d_model-wide matrices (rocprof's gemv1_kernel<T, KP, 1>), timed by events
+    # bound to its own dispatch
     abi.ssd_profile_enable(dd.ctx, True)
     abi.ssd_profile_read(dd.ctx)
     for _ in range(max(1, args.steps // 2)):
@@ -167,8 +252,8 @@ def main():
     achieved = per_launch_bytes / avg_s / 1e9
     pieces = (sh.d_model + 511) // 512
     kp = 4 if pieces <= 4 else (12 if 8 < pieces <= 12 else 8)
-    kname = "gemv_kernel<%s, 1, %d>" % ("unsigned short" if sh.dtype == "bf16" else "float", kp)
-    roofline = {"bound": "hbm", "kernel": kname + " (one-row weight-streaming GEMV)",
+    kname = "gemv1_kernel<%s, %d, 1>" % ("unsigned short" if sh.dtype == "bf16" else "float", kp)
+    roofline = {"bound": "hbm", "kernel": kname + " (one-row weight-streaming GEMV, RMSNorm folded)",
                 "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
                 "bytes_per_launch": int(per_launch_bytes), "avg_launch_us": round(avg_s * 1e6, 3),
@@ -203,6 +288,7 @@ def main():
         "speedup_vs_greedy": round(ssd_tps / greedy_tps, 3),
         "ssd_equals_greedy_tokens": same,
         "draft_step": draft,
+        "verify": verify,
         "roofline": roofline,
         "cpu_baseline": cpu,
     }

@@ -81,7 +81,10 @@ typedef struct {
   int32_t in_residual;  /* 1: I(x) = x + FC2(GELU(FC1(LN(x)))); 0: FC2(GELU(FC1(LN(x)))) */
   int32_t max_batch;    /* B capacity */
   int32_t max_gamma;    /* largest draft length used with this context */
-  int32_t max_seq;      /* KV positions per sequence (prefix + prompt + T + max_gamma + 1) */
+  int32_t max_seq;      /* KV positions per sequence: prefix + prompt + T + max_gamma + 1; with the
+                           stepwise calls on a batch whose sequences finish in different rounds,
+                           max_gamma more (a finished sequence is still drafted and verified at
+                           its last length until the batch is done) */
   int32_t max_prompt;   /* largest prompt length P passed to ssd_prefill */
   int32_t page_size;    /* KV positions per page */
   int32_t max_pages;    /* page-table columns per sequence (>= ceil(max_seq / page_size)) */
@@ -178,7 +181,8 @@ int ssd_accept(ssd_ctx* ctx, int B, int gamma, const int32_t* d_draft, const int
 
 /* The whole loop: prefill, then rounds of draft + verify + accept (SSD_MODE_SPECULATIVE) or
  * verify(gamma = 0) + accept (SSD_MODE_GREEDY) until T tokens per sequence are emitted (the last
- * round truncated).  d_tokens [B][T] int32.  h_stats (host, may be NULL) receives
+ * round truncated; a finished sequence's seq_len then counts only the positions it emitted, so
+ * max_seq = prefix + prompt + T + max_gamma + 1 suffices for any batch).  d_tokens [B][T] int32.  h_stats (host, may be NULL) receives
  * {rounds, sum over sequences of accepted drafts, sum of drafted tokens}.  Synchronises the
  * stream once per round to test for completion. */
 int ssd_generate(ssd_ctx* ctx, int B, int P, const int32_t* d_prompt, const void* d_visual, int T,
@@ -189,14 +193,14 @@ int ssd_generate(ssd_ctx* ctx, int B, int P, const int32_t* d_prompt, const void
 int ssd_set_graphs(ssd_ctx* ctx, int enable);
 
 /* Kernel timing for roofline reports.  While enabled (and graphs are bypassed), every launch of
- * the weight-streaming GEMV instantiation with one input row that streams the d_model-wide
- * matrices (gemv_kernel<T, 1, KP>, KP = 4 for d_model <= 2048, 12 for 4096 < d_model <= 6144,
- * else 8: the kernel that carries most of a batch-1 draft step) is launched with
- * two HIP events bound to its own dispatch on the context's stream, so their elapsed time is the
- * kernel's execution time; its algorithmic bytes (weights + input rows + output rows) are added
- * up.  ssd_profile_read synchronises the stream and returns the number of such launches, the
- * summed kernel time in seconds and the summed bytes since the previous read (any pointer may be
- * NULL).  Costs one event pair per launch; for measurement only. */
+ * the one-row weight-streaming GEMV instantiation that streams the RMS-normalised d_model-wide
+ * matrices (QKV, cross-attention query, gate/up, LM head: gemv1_kernel<T, KP, 1> with KP = 4 for
+ * d_model <= 2048, 12 for 4096 < d_model <= 6144, else 8; the kernel that carries most of a
+ * batch-1 draft step) is launched with two HIP events bound to its own dispatch on the context's
+ * stream, so their elapsed time is the kernel's execution time; its algorithmic bytes (weights +
+ * input row + output row) are added up.  ssd_profile_read synchronises the stream and returns
+ * the number of such launches, the summed kernel time in seconds and the summed bytes since the
+ * previous read (any pointer may be NULL).  Costs one event pair per launch; for measurement only. */
 int ssd_profile_enable(ssd_ctx* ctx, int enable);
 int ssd_profile_read(ssd_ctx* ctx, int64_t* launches, double* seconds, double* bytes);
 

@@ -71,21 +71,32 @@ struct LinearArgs {
   const float* rope_cos = nullptr;  // [max_seq][d_head/2] or null (no rotation)
   const float* rope_sin = nullptr;
   int32_t* status = nullptr;        // SSD_DEV_CAPACITY / SSD_DEV_BAD_PAGE bits
-  // hi / lo bf16 planes of a gated epilogue's output (skinny path: the next MFMA operand)
-  bf16_t* y_bf16 = nullptr;
-  int ldy_bf16 = 0;
   // row statistics for the MFMA path's normalisation (filled by launch_linear)
   float2* stats = nullptr;    // [M] workspace
   int use_mfma = -1;          // -1: choose; 0: vector path; 1: MFMA path
+  // Skinny path operands.  Input: bf16 planes hi / lo of the (gain-multiplied) rows, hi row m at
+  // in_planes + m * in_ld, lo row m at in_planes + (16 + m) * in_ld; with NORM_RMS, 1/rms of row m
+  // comes from the partial sums of squares in_ssq[p][m], p < in_nssq (16 floats per p).
+  const bf16_t* in_planes = nullptr;
+  int in_ld = 0;
+  const float* in_ssq = nullptr;
+  int in_nssq = 0;
+  // Output planes for the next skinny launch (EPI_RESID: of out_gain * y_new, plus per-block
+  // partial sums of squares of y_new in out_ssq[block][m]; gated: of y; null: none).
+  bf16_t* out_planes = nullptr;
+  int out_ld = 0;
+  float* out_ssq = nullptr;
+  const float* out_gain = nullptr;
 };
 
-// Kernel-level timing of one instantiation of the one-row GEMV, gemv_kernel<WT, 1, kp>: when
+// Kernel-level timing of one instantiation of the one-row GEMV, gemv1_kernel<WT, kp, norm>: when
 // start / stop are set and the launch takes that kernel, it is launched with the events bound to
 // its own dispatch (hipExtLaunchKernel), so their elapsed time is the kernel's execution time;
 // `timed` reports whether it happened.
 struct LaunchTiming {
   hipEvent_t start = nullptr, stop = nullptr;
   int kp = 4;
+  int norm = NORM_RMS;
   bool timed = false;
 };
 
@@ -100,19 +111,20 @@ hipError_t launch_linear(LinearArgs a, hipStream_t s, int* n_parts = nullptr,
 // Upper bound of the partials per row for n_out outputs (workspace sizing).
 int argmax_parts_max(int n_out);
 
-// Rows of a verify chunk (2..16) take the skinny MFMA path: the normalised inputs are written
-// once as two bf16 planes hi + lo (launch_norm_bf16, or by the producing kernel) and every block
-// reads them as MFMA B operands.  xb / ldb: plane hi rows at xb + m*ldb, plane lo rows at
-// xb + (16 + m)*ldb; a.x, a.norm are ignored.
+// Rows of a verify chunk (2..16, bf16 weights) take the skinny MFMA path: the inputs arrive as
+// bf16 planes written once by their producer (a.in_planes ..., see LinearArgs), with RMSNorm
+// folded (a.norm = NORM_RMS: the gain is already in the planes, 1/rms from a.in_ssq) or none;
+// the gated, QKV (rotary + KV store), residual (+ next planes), bias and argmax epilogues.
 bool skinny_ok(int M, int K, int wdtype);
-hipError_t launch_linear_skinny(const LinearArgs& a, const bf16_t* xb, int ldb, hipStream_t s,
-                                int* n_parts = nullptr);
+hipError_t launch_linear_skinny(const LinearArgs& a, hipStream_t s, int* n_parts = nullptr);
 
-// out[m][k] + out[16 + m][k] ~= norm(x[m])[k] as two bf16 planes (hi, lo), M <= 16 rows
-// (RMS / LN with gain (and shift), or a plain conversion).
-hipError_t launch_norm_bf16(const float* x, int ldx, int M, int K, int norm, const float* gain,
-                            const float* shift, float eps, bf16_t* out, int ldo, hipStream_t s);
+// Planes of gain * x for M <= 16 rows (hi row m at out + m * ldo, lo at out + (16 + m) * ldo) and
+// the full-row sums of squares ssq[0][m] (one partial): the input of the first skinny launch.
+hipError_t launch_skinny_prep(const float* x, int ldx, int M, int K, const float* gain,
+                              bf16_t* out, int ldo, float* ssq, hipStream_t s);
 
+// Partial sums of squares per block of a skinny residual epilogue (the in_nssq of its consumer).
+int skinny_blocks(int n_out);
 
 // True when launch_linear takes the weight-streaming vector path (the one that has EPI_QKV).
 bool linear_is_vector(const LinearArgs& a);
@@ -156,7 +168,7 @@ hipError_t launch_rope_scatter(const RopeScatterArgs& a, hipStream_t s);
 struct AttnArgs {
   const float* q;  // [B*C][H*dh]
   float* out;      // [B*C][H*dh]
-  bf16_t* out_bf16 = nullptr;  // optional hi / lo bf16 planes of out (rows < 16; lo 16 rows on)
+  bf16_t* out_planes = nullptr;  // optional hi / lo bf16 planes of out (rows < 16; lo 16 rows on)
   int B, C, H, dh;
   int kvdtype;
   int cross;         // 0: causal over the paged cache; 1: dense over n_keys cross-attention keys

@@ -97,47 +97,52 @@ __device__ __forceinline__ void store_kv_pair(const LinearArgs& a, int page, int
   store_elem(base + i + half, e1);
 }
 
+// Rotary (q, k) and the store of one pair of input row `row`: columns c0 and c0 + d_head/2 of
+// matrix mat (0 = q -> y, 1 = k, 2 = v -> the row's page).
+__device__ __forceinline__ void qkv_store_pair(const LinearArgs& a, int mat, int c0, int row,
+                                               float e0, float e1) {
+  const int half = a.d_head >> 1;
+  const int h = c0 / a.d_head, i = c0 - h * a.d_head;
+  const int b = row / a.C, j = row - b * a.C;
+  const int pos = a.kv.seq_len[b] + a.kv.pos_off + j;
+  if (mat < 2 && a.rope_cos) {
+    const int tp = pos < 0 ? 0 : (pos >= a.max_seq ? a.max_seq - 1 : pos);
+    const float cs = a.rope_cos[(size_t)tp * half + i], sn = a.rope_sin[(size_t)tp * half + i];
+    const float r0 = e0 * cs - e1 * sn, r1 = e1 * cs + e0 * sn;
+    e0 = r0;
+    e1 = r1;
+  }
+  if (mat == 0) {
+    a.y[(size_t)row * a.ldy + c0] = e0;
+    a.y[(size_t)row * a.ldy + c0 + half] = e1;
+    return;
+  }
+  const int pg_i = pos >= 0 ? pos / a.kv.page_size : -1;
+  int page = -1;
+  if (pos < 0 || pos >= a.max_seq || pg_i >= a.kv.max_pages) {
+    atomicOr(a.status, SSD_DEV_CAPACITY);
+  } else {
+    page = a.kv.page_table[(size_t)b * a.kv.max_pages + pg_i];
+    if (page < 0 || page >= a.kv.n_pages) {
+      atomicOr(a.status, SSD_DEV_BAD_PAGE);
+      page = -1;
+    }
+  }
+  if (page < 0) return;
+  const int slot = pos - pg_i * a.kv.page_size;
+  if (a.kvdtype == 1) store_kv_pair<bf16_t>(a, page, slot, h, i, half, mat == 2, e0, e1);
+  else store_kv_pair<float>(a, page, slot, h, i, half, mat == 2, e0, e1);
+}
+
 template <int MB>
 __device__ __forceinline__ void qkv_epilogue(const LinearArgs& a, int n0, const float (&acc)[2][MB],
                                              int m0, int mrows) {
-  const int HD = a.n_per, half = a.d_head >> 1;
+  const int HD = a.n_per;
   const int mat = n0 >= HD ? (n0 >= 2 * HD ? 2 : 1) : 0;
-  const int c0 = n0 - mat * HD;
-  const int h = c0 / a.d_head, i = c0 - h * a.d_head;
 #pragma unroll
   for (int m = 0; m < MB; ++m) {
     if (m >= mrows) break;
-    const int row = m0 + m;
-    const int b = row / a.C, j = row - b * a.C;
-    const int pos = a.kv.seq_len[b] + a.kv.pos_off + j;
-    float e0 = acc[0][m], e1 = acc[1][m];
-    if (mat < 2 && a.rope_cos) {
-      const int tp = pos < 0 ? 0 : (pos >= a.max_seq ? a.max_seq - 1 : pos);
-      const float cs = a.rope_cos[(size_t)tp * half + i], sn = a.rope_sin[(size_t)tp * half + i];
-      const float r0 = e0 * cs - e1 * sn, r1 = e1 * cs + e0 * sn;
-      e0 = r0;
-      e1 = r1;
-    }
-    if (mat == 0) {
-      a.y[(size_t)row * a.ldy + c0] = e0;
-      a.y[(size_t)row * a.ldy + c0 + half] = e1;
-      continue;
-    }
-    const int pg_i = pos >= 0 ? pos / a.kv.page_size : -1;
-    int page = -1;
-    if (pos < 0 || pos >= a.max_seq || pg_i >= a.kv.max_pages) {
-      atomicOr(a.status, SSD_DEV_CAPACITY);
-    } else {
-      page = a.kv.page_table[(size_t)b * a.kv.max_pages + pg_i];
-      if (page < 0 || page >= a.kv.n_pages) {
-        atomicOr(a.status, SSD_DEV_BAD_PAGE);
-        page = -1;
-      }
-    }
-    if (page < 0) continue;
-    const int slot = pos - pg_i * a.kv.page_size;
-    if (a.kvdtype == 1) store_kv_pair<bf16_t>(a, page, slot, h, i, half, mat == 2, e0, e1);
-    else store_kv_pair<float>(a, page, slot, h, i, half, mat == 2, e0, e1);
+    qkv_store_pair(a, mat, n0 - mat * HD, m0 + m, acc[0][m], acc[1][m]);
   }
 }
 
@@ -188,6 +193,86 @@ __device__ __forceinline__ void fma_pieces(const Vec8<WT> (&buf)[2][GV_KP], cons
         acc[0][m] = t0; acc[1][m] = t1;
       }
     }
+  }
+}
+
+// Epilogue of the vector GEMV for the block's input rows m0 .. m0 + mrows - 1: acc holds this
+// wave's two outputs per row (already scaled by 1/rms when folded), yold the residual values
+// lane 0 read before the weights.  Argmax partials are merged over the block's waves (one
+// barrier; every thread of the block must call this).
+template <typename WT, int MB>
+__device__ __forceinline__ void gemv_finish(const LinearArgs& a, const RowPair<WT>& r,
+                                            const float (&acc)[2][MB], const float (&yold)[2][MB],
+                                            bool live, bool gated, bool argmax, int m0, int mrows,
+                                            int tid, int lane, int wave, float (&rv)[GV_WAVES][MB],
+                                            int (&ri)[GV_WAVES][MB]) {
+  float best_v[MB];
+  int best_i[MB];
+#pragma unroll
+  for (int m = 0; m < MB; ++m) {
+    best_v[m] = -INFINITY;
+    best_i[m] = INT_MAX;
+  }
+  if (argmax) {
+    if (live) {
+#pragma unroll
+      for (int m = 0; m < MB; ++m) {
+        if (r.ok0) argmax_merge(best_v[m], best_i[m], acc[0][m], r.n0);
+        if (r.ok1) argmax_merge(best_v[m], best_i[m], acc[1][m], r.n1);
+        if (a.logits && lane == 0 && m < mrows) {
+          float* lp = a.logits + (size_t)(m0 + m) * a.ldl;
+          if (r.ok0) lp[r.n0] = acc[0][m];
+          if (r.ok1) lp[r.n1] = acc[1][m];
+        }
+      }
+    }
+  } else if (lane == 0 && live && a.epi == EPI_QKV) {
+    qkv_epilogue<MB>(a, r.n0, acc, m0, mrows);
+  } else if (lane == 0 && live) {
+#pragma unroll
+    for (int m = 0; m < MB; ++m) {
+      if (m >= mrows) break;
+      const size_t row = (size_t)(m0 + m);
+      if (gated) {
+        if (r.ok0) a.y[row * a.ldy + r.n0] = apply_epi_act(a.epi, acc[0][m], acc[1][m]);
+        continue;
+      }
+#pragma unroll
+      for (int s = 0; s < 2; ++s) {
+        const bool ok = s ? r.ok1 : r.ok0;
+        if (!ok) continue;
+        const int n = s ? r.n1 : r.n0;
+        const float v = acc[s][m];
+        float* yp = a.y + row * a.ldy + n;
+        if (a.epi == EPI_STORE) {
+          *yp = v;
+        } else if (a.epi == EPI_RESID) {
+          const float t = yold[s][m] + v;
+          *yp = t;
+          if (a.stash) a.stash[row * a.lds + n] = t;
+        } else if (a.epi == EPI_BIAS_GELU) {
+          *yp = gelu_tanh(v + a.bias[n]);
+        } else if (a.epi == EPI_BIAS_RESID) {
+          *yp = yold[s][m] + (v + a.bias[n]);
+        }
+      }
+    }
+  }
+
+  if (!argmax) return;
+  // block's best per row -> one partial per (row, block); launch_argmax_final reduces them
+  if (lane == 0) {
+#pragma unroll
+    for (int m = 0; m < MB; ++m) { rv[wave][m] = best_v[m]; ri[wave][m] = best_i[m]; }
+  }
+  __syncthreads();
+  if (tid < mrows) {
+    const int m = tid;
+    float v = rv[0][m];
+    int i = ri[0][m];
+    for (int ww = 1; ww < GV_WAVES; ++ww) argmax_merge(v, i, rv[ww][m], ri[ww][m]);
+    a.part_val[(size_t)(m0 + m) * a.n_parts + blockIdx.x] = v;
+    a.part_idx[(size_t)(m0 + m) * a.n_parts + blockIdx.x] = i;
   }
 }
 
@@ -344,102 +429,179 @@ __global__ __launch_bounds__(256) void gemv_kernel(const LinearArgs a) {
     acc[0][m] = wave_sum(acc[0][m]) * rscale[m];
     acc[1][m] = wave_sum(acc[1][m]) * rscale[m];
   }
-  float best_v[MB];
-  int best_i[MB];
+  gemv_finish<WT, MB>(a, r, acc, yold, live, gated, argmax, m0, mrows, tid, lane, wave, rv, ri);
+}
+
+// One input row, K <= 512 * KP: the register path of the draft and greedy steps.  A wave's 64
+// lanes hold the whole input row in registers (lane l owns elements p*512 + 8l .. +7 of every
+// piece p), so the norm statistics are wave reductions and nothing is staged in LDS: each wave
+// requests its inputs, then both weight rows, then the norm's gain (and shift), and computes the
+// statistics while the weights are in flight.  NORM is the input normalisation (a template
+// parameter so that rows without one keep no gain registers).
+template <typename WT, int KP, int NORM>
+__global__ __launch_bounds__(256) void gemv1_kernel(const LinearArgs a) {
+  __shared__ float rv[GV_WAVES][1];
+  __shared__ int ri[GV_WAVES][1];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int K = a.K;
+  const bool gated = (a.epi == EPI_GATED_GELU || a.epi == EPI_GATED_SILU);
+  const bool argmax = a.epi == EPI_ARGMAX;
+  const int n_total = gated ? a.n_per : a.n_per * a.n_mats;
+  const int n_pairs = gated ? a.n_per : (n_total + 1) / 2;
+  const int pr = blockIdx.x * GV_WAVES + wave;
+  constexpr bool rms = NORM == NORM_RMS, ln = NORM == NORM_LN;
+
+  // inputs first (the wait counter retires loads in issue order); clamped, never conditional
+  float xv[KP][8];
 #pragma unroll
-  for (int m = 0; m < MB; ++m) {
-    best_v[m] = -INFINITY;
-    best_i[m] = INT_MAX;
+  for (int p = 0; p < KP; ++p) {
+    const int e = min(p * 512 + lane * 8, K - 8);
+    const float4 x0 = *reinterpret_cast<const float4*>(a.x + e);
+    const float4 x1 = *reinterpret_cast<const float4*>(a.x + e + 4);
+    xv[p][0] = x0.x; xv[p][1] = x0.y; xv[p][2] = x0.z; xv[p][3] = x0.w;
+    xv[p][4] = x1.x; xv[p][5] = x1.y; xv[p][6] = x1.z; xv[p][7] = x1.w;
   }
-  if (argmax) {
-    if (live) {
+  const RowPair<WT> r = row_pair<WT>(a, gated, n_total, pr < n_pairs ? pr : 0);
+  const bool live = pr < n_pairs;
+  float yold[2][1] = {{0.f}, {0.f}};
+  if (lane == 0 && live && (a.epi == EPI_RESID || a.epi == EPI_BIAS_RESID)) {
+    const float* src = a.epi == EPI_RESID ? a.y : a.resid;
+    yold[0][0] = (src && r.ok0) ? src[r.n0] : 0.f;
+    yold[1][0] = (src && r.ok1) ? src[r.n1] : 0.f;
+  }
+  Vec8<WT> w[2][KP];
+  load_pieces<WT, KP>(w, r, 0, K, lane);
+  Vec8<float> gv[rms || ln ? KP : 1], sv[ln ? KP : 1];
+  if (rms || ln) {
 #pragma unroll
-      for (int m = 0; m < MB; ++m) {
-        if (r.ok0) argmax_merge(best_v[m], best_i[m], acc[0][m], r.n0);
-        if (r.ok1) argmax_merge(best_v[m], best_i[m], acc[1][m], r.n1);
-        if (a.logits && lane == 0 && m < mrows) {
-          float* lp = a.logits + (size_t)(m0 + m) * a.ldl;
-          if (r.ok0) lp[r.n0] = acc[0][m];
-          if (r.ok1) lp[r.n1] = acc[1][m];
-        }
-      }
+    for (int p = 0; p < KP; ++p) gv[p].load(a.gain + min(p * 512 + lane * 8, K - 8));
+  }
+  if (ln) {
+#pragma unroll
+    for (int p = 0; p < KP; ++p) sv[p].load(a.shift + min(p * 512 + lane * 8, K - 8));
+  }
+
+  // pieces past K (clamped re-reads) count as zero
+#pragma unroll
+  for (int p = 0; p < KP; ++p)
+    if (p * 512 + lane * 8 >= K) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) xv[p][e] = 0.f;
     }
-  } else if (lane == 0 && live && a.epi == EPI_QKV) {
-    qkv_epilogue<MB>(a, r.n0, acc, m0, mrows);
-  } else if (lane == 0 && live) {
+  float rscale = 1.f;
+  if (rms) {
+    float s2 = 0.f;
 #pragma unroll
-    for (int m = 0; m < MB; ++m) {
-      if (m >= mrows) break;
-      const size_t row = (size_t)(m0 + m);
-      if (gated) {
-        if (r.ok0) a.y[row * a.ldy + r.n0] = apply_epi_act(a.epi, acc[0][m], acc[1][m]);
-        continue;
-      }
+    for (int p = 0; p < KP; ++p)
 #pragma unroll
-      for (int s = 0; s < 2; ++s) {
-        const bool ok = s ? r.ok1 : r.ok0;
-        if (!ok) continue;
-        const int n = s ? r.n1 : r.n0;
-        const float v = acc[s][m];
-        float* yp = a.y + row * a.ldy + n;
-        if (a.epi == EPI_STORE) {
-          *yp = v;
-        } else if (a.epi == EPI_RESID) {
-          const float t = yold[s][m] + v;
-          *yp = t;
-          if (a.stash) a.stash[row * a.lds + n] = t;
-        } else if (a.epi == EPI_BIAS_GELU) {
-          *yp = gelu_tanh(v + a.bias[n]);
-        } else if (a.epi == EPI_BIAS_RESID) {
-          *yp = yold[s][m] + (v + a.bias[n]);
+      for (int e = 0; e < 8; ++e) s2 = fmaf(xv[p][e], xv[p][e], s2);
+    s2 = wave_sum(s2);
+    rscale = 1.0f / sqrtf(s2 / (float)K + a.eps);
+#pragma unroll
+    for (int p = 0; p < KP; ++p) {
+      float g[8];
+      gv[p].to_f32(g);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) xv[p][e] *= g[e];
+    }
+  } else if (ln) {
+    float s1 = 0.f;
+#pragma unroll
+    for (int p = 0; p < KP; ++p)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) s1 += xv[p][e];
+    const float mean = wave_sum(s1) / (float)K;
+    float s2 = 0.f;
+#pragma unroll
+    for (int p = 0; p < KP; ++p)
+      if (p * 512 + lane * 8 < K) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float c = xv[p][e] - mean;
+          s2 = fmaf(c, c, s2);
         }
       }
+    const float rstd = 1.0f / sqrtf(wave_sum(s2) / (float)K + a.eps);
+#pragma unroll
+    for (int p = 0; p < KP; ++p) {
+      float g[8], b[8];
+      gv[p].to_f32(g);
+      sv[p].to_f32(b);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) xv[p][e] = (xv[p][e] - mean) * rstd * g[e] + b[e];
     }
   }
 
-  if (!argmax) return;
-  // block's best per row -> one partial per (row, block); launch_argmax_final reduces them
-  if (lane == 0) {
+  float acc[2][1] = {{0.f}, {0.f}};
 #pragma unroll
-    for (int m = 0; m < MB; ++m) { rv[wave][m] = best_v[m]; ri[wave][m] = best_i[m]; }
+  for (int p = 0; p < KP; ++p) {
+    if (p * 512 + lane * 8 < K) {
+      float w0[8], w1[8];
+      w[0][p].to_f32(w0);
+      w[1][p].to_f32(w1);
+      float t0 = acc[0][0], t1 = acc[1][0];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        t0 = fmaf(w0[e], xv[p][e], t0);
+        t1 = fmaf(w1[e], xv[p][e], t1);
+      }
+      acc[0][0] = t0;
+      acc[1][0] = t1;
+    }
   }
-  __syncthreads();
-  if (tid < mrows) {
-    const int m = tid;
-    float v = rv[0][m];
-    int i = ri[0][m];
-    for (int ww = 1; ww < GV_WAVES; ++ww) argmax_merge(v, i, rv[ww][m], ri[ww][m]);
-    a.part_val[(size_t)(m0 + m) * a.n_parts + blockIdx.x] = v;
-    a.part_idx[(size_t)(m0 + m) * a.n_parts + blockIdx.x] = i;
-  }
+  acc[0][0] = wave_sum(acc[0][0]) * rscale;
+  acc[1][0] = wave_sum(acc[1][0]) * rscale;
+  gemv_finish<WT, 1>(a, r, acc, yold, live, gated, argmax, 0, 1, tid, lane, wave, rv, ri);
 }
 
 // ---------------------------------------------------------------------------------------------
 // Skinny MFMA path: 2..16 input rows (the batch-1 verify chunk), bf16 weights.
-// The inputs arrive already normalised as two bf16 planes, x ~= hi + lo with hi = bf16(x) and
-// lo = bf16(x - hi) (rows m at xb + m * ldb and xb + (16 + m) * ldb), written by launch_norm_bf16
-// or by the producing kernel; multiplying both planes keeps the activations at about 16 mantissa
-// bits while the weights are read once.  A block owns 16 output features and its 4 waves split
-// K.  Per 64-element step a lane reads 32 contiguous bytes of one weight row (the A operands of
-// two v_mfma_f32_16x16x32_bf16) and 32 bytes of each input plane (the B operands; rows past M
-// read as zeros).  All loads of a batch are issued before the first MFMA; the four partial 16x16
-// tiles are summed through LDS before the fused epilogue.
-template <bool GATED>
-__global__ __launch_bounds__(256) void gemv_mfma_kernel(const LinearArgs a, const bf16_t* __restrict__ xb,
-                                                        const int ldb) {
+// A block owns 16 output features (the A rows of v_mfma_f32_16x16x32_bf16) and its 4 waves split
+// K; the input rows are the B columns.  The inputs arrive as two bf16 planes hi = bf16(v),
+// lo = bf16(v - hi) of v = g * x (g the RMSNorm gain, or 1), written once by their producer;
+// multiplying both planes keeps the activations at about 16 mantissa bits while the weights are
+// read once.  RMSNorm is folded: 1/rms of each row comes from partial sums of squares the
+// producer left, and scales the outputs.  Per 64-element step a lane reads 32 contiguous bytes
+// of one weight row and 32 bytes of each plane; all loads of a batch (inputs first, then weights)
+// are issued before the first MFMA, and the 4 partial 16x16 tiles are summed through LDS before
+// the fused epilogue.  For EPI_QKV a block's rows r and r + 8 are the rotary pair (i, i + dh/2) of
+// one head, so rotary and the KV store are done here.  A residual epilogue also writes the next
+// launch's planes (of out_gain * y_new) and this block's partial sums of squares of y_new.
+constexpr int SKW = 4;  // waves per skinny block
+constexpr int SSQ_MAX = 256;  // partial sums of squares a skinny consumer reads (d_model <= 4096)
+
+template <bool GATED, bool RMS>
+__global__ __launch_bounds__(64 * SKW) void gemv_mfma_kernel(const LinearArgs a) {
   constexpr int NB = GATED ? 2 : 1;
-  constexpr int SK = GATED ? 4 : 8;  // 64-element steps per batch
-  __shared__ float part[4][NB][16][17];
+  constexpr int SK = GATED ? 4 : 8;  // 64-element steps per wave and batch
+  constexpr int NG = 4 * SKW;        // groups of 16 threads
+  __shared__ float part[SKW][NB][16][17];
   __shared__ float best_v[16][17];
   __shared__ int best_i[16][17];
+  __shared__ float rs[16];
+  __shared__ float sq[4][16];
+  __shared__ float ssq_red[4 * SKW][16];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int K = a.K, M = a.M;
   const int n_out = GATED ? a.n_per : a.n_per * a.n_mats;
-  const int n0 = blockIdx.x * 16;
+  const bool qkv = !GATED && a.epi == EPI_QKV;
   const int steps = K / 64;
-  const int s_beg = (steps * wave) / 4, s_end = (steps * (wave + 1)) / 4;
-  const int row = n0 + (lane & 15);
+  const int s_beg = (steps * wave) / SKW, s_end = (steps * (wave + 1)) / SKW;
+
+  // QKV blocks: matrix, head and 8-column group of the rotary pairs
+  int q_mat = 0, q_c = 0;
+  if (qkv) {
+    const int half = a.d_head >> 1, per_head = half / 8;
+    const int mat = blockIdx.x / (a.n_heads * per_head);
+    const int rem = blockIdx.x - mat * a.n_heads * per_head;
+    const int h = rem / per_head, jb = rem - h * per_head;
+    q_mat = mat;
+    q_c = h * a.d_head + 8 * jb;
+  }
+  const int r16 = lane & 15;
+  const int row = qkv ? q_mat * a.n_per + q_c + (r16 & 7) + (r16 >= 8 ? (a.d_head >> 1) : 0)
+                      : blockIdx.x * 16 + r16;
   const bool row_ok = row < n_out;
   const bf16_t* wrow[NB];
   {
@@ -457,32 +619,32 @@ __global__ __launch_bounds__(256) void gemv_mfma_kernel(const LinearArgs a, cons
   const int kq = (lane >> 4) * 16;  // this lane's 16 elements within a step
   const int tok = lane & 15;
   const bool tok_ok = tok < M;
-  const bf16_t* brow = xb + (size_t)(tok_ok ? tok : 0) * ldb;
-  const bf16_t* brow_lo = brow + (size_t)16 * ldb;
+  const bf16_t* brow = a.in_planes + (size_t)(tok_ok ? tok : 0) * a.in_ld;
+  const bf16_t* brow_lo = brow + (size_t)16 * a.in_ld;
 
   f32x4_t acc[NB];
 #pragma unroll
   for (int b = 0; b < NB; ++b) acc[b] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   for (int s0 = s_beg; s0 < s_end; s0 += SK) {
     uint4 wv[NB][SK][2], bv[SK][2], bl[SK][2];
-    // activations first (L2-resident, they arrive early), then the weights in step order: the
-    // wait counter retires loads in issue order, so step u waits only for its own weights
+    // inputs first (L2-resident, they arrive early), then the weights in step order: the wait
+    // counter retires loads in issue order, so step u waits only for its own weights
 #pragma unroll
     for (int u = 0; u < SK; ++u) {
-      const int st = min(s0 + u, s_end - 1);
-      const uint4* bp = reinterpret_cast<const uint4*>(brow + st * 64 + kq);
+      const int k0 = min(s0 + u, s_end - 1) * 64 + kq;
+      const uint4* bp = reinterpret_cast<const uint4*>(brow + k0);
       bv[u][0] = bp[0];
       bv[u][1] = bp[1];
-      const uint4* bq = reinterpret_cast<const uint4*>(brow_lo + st * 64 + kq);
+      const uint4* bq = reinterpret_cast<const uint4*>(brow_lo + k0);
       bl[u][0] = bq[0];
       bl[u][1] = bq[1];
     }
 #pragma unroll
     for (int u = 0; u < SK; ++u) {
-      const int st = min(s0 + u, s_end - 1);
+      const int k0 = min(s0 + u, s_end - 1) * 64 + kq;
 #pragma unroll
       for (int b = 0; b < NB; ++b) {
-        const uint4* wp = reinterpret_cast<const uint4*>(wrow[b] + st * 64 + kq);
+        const uint4* wp = reinterpret_cast<const uint4*>(wrow[b] + k0);
         wv[b][u][0] = wp[0];
         wv[b][u][1] = wp[1];
       }
@@ -490,8 +652,9 @@ __global__ __launch_bounds__(256) void gemv_mfma_kernel(const LinearArgs a, cons
     __builtin_amdgcn_sched_barrier(0);  // keep the whole batch in flight before the first MFMA
 #pragma unroll
     for (int u = 0; u < SK; ++u) {
-      // a step past this wave's range re-read a clamped step: zero operands instead of a branch
-      // (a branch would let the compiler sink the loads into it and serialise the batch)
+      // a step past this wave's range re-read a clamped step, and a row past M re-read row 0:
+      // zero operands instead of a branch (a branch would let the compiler sink the loads into it
+      // and serialise the batch)
       const bool use = tok_ok && (s0 + u < s_end);
       const uint4 z = make_uint4(0, 0, 0, 0);
       const uint4 b0 = use ? bv[u][0] : z, b1 = use ? bv[u][1] : z;
@@ -507,21 +670,53 @@ __global__ __launch_bounds__(256) void gemv_mfma_kernel(const LinearArgs a, cons
       }
     }
   }
+  // RMSNorm: the producer's partial sums of squares (thread: token tid % 16, partials
+  // tid / 16 + NG i; one batch of clamped loads, unused ones count as zero)
+  float sp = 0.f;
+  if (RMS) {
+    float v[SSQ_MAX / NG];
+#pragma unroll
+    for (int i = 0; i < SSQ_MAX / NG; ++i) {
+      const int p = (tid >> 4) + NG * i;
+      v[i] = a.in_ssq[(size_t)min(p, a.in_nssq - 1) * 16 + (tid & 15)];
+    }
+#pragma unroll
+    for (int i = 0; i < SSQ_MAX / NG; ++i) sp += ((tid >> 4) + NG * i < a.in_nssq) ? v[i] : 0.f;
+  }
   // D[feature][token]: lane holds features 4 * (lane / 16) + e, token lane % 16
 #pragma unroll
   for (int b = 0; b < NB; ++b)
 #pragma unroll
     for (int e = 0; e < 4; ++e) part[wave][b][4 * (lane >> 4) + e][lane & 15] = acc[b][e];
+  if (RMS) ssq_red[tid >> 4][tid & 15] = sp;
+  __syncthreads();
+  if (RMS && tid < 16) {
+    float s2 = 0.f;
+#pragma unroll
+    for (int g = 0; g < NG; ++g) s2 += ssq_red[g][tid];
+    rs[tid] = 1.0f / sqrtf(s2 / (float)K + a.eps);
+  }
   __syncthreads();
 
-  // epilogue: thread (feature f, token t)
-  const int f = tid >> 4, t = tid & 15;
-  const int n = n0 + f;
-  const float v = (part[0][0][f][t] + part[1][0][f][t]) + (part[2][0][f][t] + part[3][0][f][t]);
-  const bool ok = t < M && n < n_out;
+  // epilogue: thread (feature f, token t) for the first 256 threads
+  static_assert(SKW >= 4, "the epilogue needs 256 threads");
+  const int f = (tid >> 4) & 15, t = tid & 15;
+  const bool lead = tid < 256;
+  auto tile_sum = [&](int b, int ff) {
+    float v = 0.f;
+#pragma unroll
+    for (int w = 0; w < SKW; ++w) v += part[w][b][ff][t];
+    return v;
+  };
+  const float rscale = RMS ? rs[t] : 1.f;
+  const int n = blockIdx.x * 16 + f;
+  const float v = tile_sum(0, f) * rscale;
   if (a.epi == EPI_ARGMAX) {
-    best_v[t][f] = ok ? v : -INFINITY;
-    best_i[t][f] = ok ? n : INT_MAX;
+    const bool ok = lead && t < M && n < n_out;
+    if (lead) {
+      best_v[t][f] = ok ? v : -INFINITY;
+      best_i[t][f] = ok ? n : INT_MAX;
+    }
     if (ok && a.logits) a.logits[(size_t)t * a.ldl + n] = v;
     __syncthreads();
     if (tid < M) {
@@ -533,107 +728,87 @@ __global__ __launch_bounds__(256) void gemv_mfma_kernel(const LinearArgs a, cons
     }
     return;
   }
-  if (!ok) return;
+  if (a.epi == EPI_RESID) {
+    // y_new, the next planes and this block's partial sums of squares (all threads take part in
+    // the reduction; rows past M or features past n_out contribute zero)
+    const bool ok = lead && t < M && n < n_out;
+    float y2 = 0.f;
+    if (ok) {
+      float* yp = a.y + (size_t)t * a.ldy + n;
+      const float tt = *yp + v;
+      *yp = tt;
+      if (a.stash) a.stash[(size_t)t * a.lds + n] = tt;
+      if (a.out_planes) {
+        const float gv = a.out_gain ? a.out_gain[n] * tt : tt;
+        const uint32_t hi = f32_to_bf16(gv);
+        a.out_planes[(size_t)t * a.out_ld + n] = (bf16_t)hi;
+        a.out_planes[(size_t)(16 + t) * a.out_ld + n] = (bf16_t)f32_to_bf16(gv - bf16_to_f32(hi));
+      }
+      y2 = tt * tt;
+    }
+    if (a.out_ssq) {
+      // threads with the same t: lanes t, t+16, t+32, t+48 of the first four waves
+      y2 += __shfl_xor(y2, 16, SSD_WAVE);
+      y2 += __shfl_xor(y2, 32, SSD_WAVE);
+      if (lead && lane < 16) sq[wave][lane] = y2;
+      __syncthreads();
+      if (tid < 16) a.out_ssq[(size_t)blockIdx.x * 16 + tid] = (sq[0][tid] + sq[1][tid]) + (sq[2][tid] + sq[3][tid]);
+    }
+    return;
+  }
+  if (!lead || t >= M) return;
+  if (qkv) {
+    if (f < 8) qkv_store_pair(a, q_mat, q_c + f, t, v, tile_sum(0, f + 8) * rscale);
+    return;
+  }
+  if (n >= n_out) return;
   if (GATED) {
-    const float u = (part[0][NB - 1][f][t] + part[1][NB - 1][f][t]) + (part[2][NB - 1][f][t] + part[3][NB - 1][f][t]);
-    const float act = apply_epi_act(a.epi, v, u);
+    const float act = apply_epi_act(a.epi, v, tile_sum(NB - 1, f) * rscale);
     if (a.y) a.y[(size_t)t * a.ldy + n] = act;
-    if (a.y_bf16) {
+    if (a.out_planes) {
       const uint32_t hi = f32_to_bf16(act);
-      a.y_bf16[(size_t)t * a.ldy_bf16 + n] = (bf16_t)hi;
-      a.y_bf16[(size_t)(16 + t) * a.ldy_bf16 + n] = (bf16_t)f32_to_bf16(act - bf16_to_f32(hi));
+      a.out_planes[(size_t)t * a.out_ld + n] = (bf16_t)hi;
+      a.out_planes[(size_t)(16 + t) * a.out_ld + n] = (bf16_t)f32_to_bf16(act - bf16_to_f32(hi));
     }
     return;
   }
   float* yp = a.y + (size_t)t * a.ldy + n;
   switch (a.epi) {
     case EPI_STORE: *yp = v; break;
-    case EPI_RESID: {
-      const float tt = *yp + v;
-      *yp = tt;
-      if (a.stash) a.stash[(size_t)t * a.lds + n] = tt;
-      break;
-    }
     case EPI_BIAS_GELU: *yp = gelu_tanh(v + a.bias[n]); break;
     case EPI_BIAS_RESID: *yp = (a.resid ? a.resid[(size_t)t * a.ldr + n] : 0.f) + (v + a.bias[n]); break;
     default: break;
   }
 }
 
-// out[m][k] = hi, out[16 + m][k] = lo with hi + lo ~= norm(x[m])[k] (bf16 planes) — one block per
-// row; the row stays in registers for K <= 4096.
-__global__ __launch_bounds__(256) void norm_bf16_kernel(const float* __restrict__ x, int ldx, int K,
-                                                        int norm, const float* __restrict__ gain,
-                                                        const float* __restrict__ shift, float eps,
-                                                        bf16_t* __restrict__ out, int ldo) {
-  constexpr int PT = 4;  // float4 per thread kept in registers
-  __shared__ float red[4][2];
+// Planes of gain * x and the row's sum of squares (ssq[m], one partial) for the first skinny
+// launch of a pass — one block per row, the row held in registers for K <= 4096.
+__global__ __launch_bounds__(256) void skinny_prep_kernel(const float* __restrict__ x, int ldx, int K,
+                                                          const float* __restrict__ gain,
+                                                          bf16_t* __restrict__ out, int ldo,
+                                                          float* __restrict__ ssq) {
+  __shared__ float red[4];
   const int m = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const float* xr = x + (size_t)m * ldx;
-  bf16_t* orow = out + (size_t)m * ldo;
-  float4 v[PT];
-  float s1 = 0.f, s2 = 0.f;
-  const bool fits = K <= 1024 * PT;
-#pragma unroll
-  for (int u = 0; u < PT; ++u) {
-    const int k = (tid + 256 * u) * 4;
-    v[u] = k < K ? *reinterpret_cast<const float4*>(xr + k) : make_float4(0.f, 0.f, 0.f, 0.f);
-  }
-  if (!fits) {
-    for (int k = (tid + 256 * PT) * 4; k < K; k += 1024) {
-      const float4 w = *reinterpret_cast<const float4*>(xr + k);
-      s1 += (w.x + w.y) + (w.z + w.w);
-      s2 += (w.x * w.x + w.y * w.y) + (w.z * w.z + w.w * w.w);
-    }
-  }
-#pragma unroll
-  for (int u = 0; u < PT; ++u) {
-    s1 += (v[u].x + v[u].y) + (v[u].z + v[u].w);
-    s2 += (v[u].x * v[u].x + v[u].y * v[u].y) + (v[u].z * v[u].z + v[u].w * v[u].w);
-  }
-  s1 = wave_sum(s1);
-  s2 = wave_sum(s2);
-  if (lane == 0) { red[wave][0] = s1; red[wave][1] = s2; }
-  __syncthreads();
-  const float t1 = (red[0][0] + red[1][0]) + (red[2][0] + red[3][0]);
-  const float t2 = (red[0][1] + red[1][1]) + (red[2][1] + red[3][1]);
-  float mean = 0.f, rstd = 1.f;
-  if (norm == NORM_LN) {
-    mean = t1 / (float)K;
-    rstd = 1.0f / sqrtf(fmaxf(t2 / (float)K - mean * mean, 0.f) + eps);
-  } else if (norm == NORM_RMS) {
-    rstd = 1.0f / sqrtf(t2 / (float)K + eps);
-  }
-  auto emit = [&](int k, float4 w) {
-    float f[4] = {w.x, w.y, w.z, w.w};
-    if (norm != NORM_NONE) {
-      const float4 g = *reinterpret_cast<const float4*>(gain + k);
-      const float gg[4] = {g.x, g.y, g.z, g.w};
-      float bb[4] = {0.f, 0.f, 0.f, 0.f};
-      if (norm == NORM_LN) {
-        const float4 b = *reinterpret_cast<const float4*>(shift + k);
-        bb[0] = b.x; bb[1] = b.y; bb[2] = b.z; bb[3] = b.w;
-      }
-#pragma unroll
-      for (int e = 0; e < 4; ++e) f[e] = (f[e] - mean) * rstd * gg[e] + bb[e];
-    }
+  float s2 = 0.f;
+  for (int k = tid * 4; k < K; k += 1024) {
+    const float4 v = *reinterpret_cast<const float4*>(xr + k);
+    s2 += (v.x * v.x + v.y * v.y) + (v.z * v.z + v.w * v.w);
+    const float4 g = gain ? *reinterpret_cast<const float4*>(gain + k) : make_float4(1.f, 1.f, 1.f, 1.f);
+    const float f[4] = {v.x * g.x, v.y * g.y, v.z * g.z, v.w * g.w};
     uint32_t h[4], l[4];
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       h[e] = f32_to_bf16(f[e]);
       l[e] = f32_to_bf16(f[e] - bf16_to_f32(h[e]));
     }
-    *reinterpret_cast<uint2*>(orow + k) = make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16));
-    *reinterpret_cast<uint2*>(orow + (size_t)16 * ldo + k) = make_uint2(l[0] | (l[1] << 16), l[2] | (l[3] << 16));
-  };
-#pragma unroll
-  for (int u = 0; u < PT; ++u) {
-    const int k = (tid + 256 * u) * 4;
-    if (k < K) emit(k, v[u]);
+    *reinterpret_cast<uint2*>(out + (size_t)m * ldo + k) = make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16));
+    *reinterpret_cast<uint2*>(out + (size_t)(16 + m) * ldo + k) = make_uint2(l[0] | (l[1] << 16), l[2] | (l[3] << 16));
   }
-  if (!fits) {
-    for (int k = (tid + 256 * PT) * 4; k < K; k += 1024) emit(k, *reinterpret_cast<const float4*>(xr + k));
-  }
+  s2 = wave_sum(s2);
+  if (lane == 0) red[wave] = s2;
+  __syncthreads();
+  if (tid == 0) ssq[m] = (red[0] + red[1]) + (red[2] + red[3]);
 }
 
 // ---------------------------------------------------------------------------------------------
@@ -881,6 +1056,17 @@ GvPlan gv_plan(const LinearArgs& a) {
   return p;
 }
 
+template <typename WT, int KP, int NORM>
+void launch_gemv1(const LinearArgs& a, dim3 grid, hipStream_t s, LaunchTiming* t) {
+  if (t) {
+    hipExtLaunchKernelGGL((gemv1_kernel<WT, KP, NORM>), grid, dim3(256), 0u, s, t->start, t->stop,
+                          0u, a);
+    t->timed = true;
+  } else {
+    hipLaunchKernelGGL((gemv1_kernel<WT, KP, NORM>), grid, dim3(256), 0, s, a);
+  }
+}
+
 template <typename WT, int MB, int KP>
 hipError_t launch_gemv_kp(const LinearArgs& a, const GvPlan& p, hipStream_t s, LaunchTiming* t) {
   static bool attr = false;
@@ -890,14 +1076,16 @@ hipError_t launch_gemv_kp(const LinearArgs& a, const GvPlan& p, hipStream_t s, L
     attr = true;
   }
   dim3 grid(p.blocks, (a.M + MB - 1) / MB);
-  const size_t shm = (size_t)MB * ((a.K + 7) & ~7) * sizeof(float);
-  if (MB == 1 && t && KP == t->kp && t->start && t->stop) {
-    hipExtLaunchKernelGGL((gemv_kernel<WT, MB, KP>), grid, dim3(256), (uint32_t)shm, s, t->start,
-                          t->stop, 0u, a);
-    t->timed = true;
-  } else {
-    hipLaunchKernelGGL((gemv_kernel<WT, MB, KP>), grid, dim3(256), shm, s, a);
+  if (MB == 1 && a.M == 1 && a.K <= 512 * KP && (a.norm != NORM_LN || KP == 4)) {
+    // one row that fits a batch: the register path
+    const bool timed = t && KP == t->kp && a.norm == t->norm && t->start && t->stop;
+    if (a.norm == NORM_RMS) launch_gemv1<WT, KP, NORM_RMS>(a, grid, s, timed ? t : nullptr);
+    else if (a.norm == NORM_LN) launch_gemv1<WT, 4, NORM_LN>(a, grid, s, timed ? t : nullptr);
+    else launch_gemv1<WT, KP, NORM_NONE>(a, grid, s, timed ? t : nullptr);
+    return hipGetLastError();
   }
+  const size_t shm = (size_t)MB * ((a.K + 7) & ~7) * sizeof(float);
+  hipLaunchKernelGGL((gemv_kernel<WT, MB, KP>), grid, dim3(256), shm, s, a);
   return hipGetLastError();
 }
 
@@ -956,23 +1144,31 @@ int argmax_parts_max(int n_out) {
 
 bool skinny_ok(int M, int K, int wdtype) { return wdtype == 1 && M >= 2 && M <= 16 && K % 64 == 0; }
 
-hipError_t launch_linear_skinny(const LinearArgs& a, const bf16_t* xb, int ldb, hipStream_t s,
-                                int* n_parts) {
+int skinny_blocks(int n_out) { return (n_out + 15) / 16; }
+
+hipError_t launch_linear_skinny(const LinearArgs& a, hipStream_t s, int* n_parts) {
   const bool gated = (a.epi == EPI_GATED_GELU || a.epi == EPI_GATED_SILU);
   const int n_out = gated ? a.n_per : a.n_per * a.n_mats;
-  const int tiles = (n_out + 15) / 16;
+  const int tiles = skinny_blocks(n_out);
+  if (!a.in_planes || a.norm == NORM_LN) return hipErrorInvalidValue;
+  if (a.norm == NORM_RMS && (!a.in_ssq || a.in_nssq < 1 || a.in_nssq > SSQ_MAX)) return hipErrorInvalidValue;
+  if (a.epi == EPI_QKV && (a.n_mats != 3 || (a.d_head / 2) % 8 != 0)) return hipErrorInvalidValue;
   LinearArgs b = a;
   if (b.epi == EPI_ARGMAX) b.n_parts = tiles;
   if (n_parts) *n_parts = b.n_parts;
-  if (gated) hipLaunchKernelGGL((gemv_mfma_kernel<true>), dim3(tiles), dim3(256), 0, s, b, xb, ldb);
-  else hipLaunchKernelGGL((gemv_mfma_kernel<false>), dim3(tiles), dim3(256), 0, s, b, xb, ldb);
+  const dim3 grid(tiles), block(64 * SKW);
+  const bool rms = a.norm == NORM_RMS;
+  if (gated && rms) hipLaunchKernelGGL((gemv_mfma_kernel<true, true>), grid, block, 0, s, b);
+  else if (gated) hipLaunchKernelGGL((gemv_mfma_kernel<true, false>), grid, block, 0, s, b);
+  else if (rms) hipLaunchKernelGGL((gemv_mfma_kernel<false, true>), grid, block, 0, s, b);
+  else hipLaunchKernelGGL((gemv_mfma_kernel<false, false>), grid, block, 0, s, b);
   return hipGetLastError();
 }
 
-hipError_t launch_norm_bf16(const float* x, int ldx, int M, int K, int norm, const float* gain,
-                            const float* shift, float eps, bf16_t* out, int ldo, hipStream_t s) {
-  hipLaunchKernelGGL(norm_bf16_kernel, dim3(M), dim3(256), 0, s, x, ldx, K, norm, gain, shift, eps,
-                     out, ldo);
+hipError_t launch_skinny_prep(const float* x, int ldx, int M, int K, const float* gain, bf16_t* out,
+                              int ldo, float* ssq, hipStream_t s) {
+  if (M < 1 || M > 16 || K % 4) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(skinny_prep_kernel, dim3(M), dim3(256), 0, s, x, ldx, K, gain, out, ldo, ssq);
   return hipGetLastError();
 }
 

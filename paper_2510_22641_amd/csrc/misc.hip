@@ -155,8 +155,7 @@ __global__ void accept_kernel(const AcceptArgs a) {
         o[n] = tg[n];
       }
       if (a.accept_len) a.accept_len[b] = n;
-      const int sl = a.seq_len[b] + n + 1;
-      a.seq_len[b] = sl;
+      int adv = n + 1;
       a.pending[b] = tg[n];
       still = 1;
       if (a.tokens) {
@@ -165,11 +164,16 @@ __global__ void accept_kernel(const AcceptArgs a) {
         for (int e = 0; e < emit; ++e) a.tokens[(size_t)b * a.T + c + e] = e < n ? dr[e] : tg[n];
         a.count[b] = c + emit;
         if (c + emit >= a.T) {
+          // finished: keep only the emitted positions, so the rows this sequence still occupies
+          // in later rounds of the batch stay inside the cache
+          adv = emit;
           a.active_rw[b] = 0;
           still = 0;
         }
       }
-      if (still && sl + a.next_need > a.max_seq) atomicOr(a.status, SSD_DEV_CAPACITY);
+      const int sl = a.seq_len[b] + adv;
+      a.seq_len[b] = sl;
+      if (sl + (still ? a.next_need : 0) > a.max_seq) atomicOr(a.status, SSD_DEV_CAPACITY);
     } else if (a.active_rw) {
       still = 0;
     }

@@ -31,7 +31,7 @@ int t5_bucket(int n, int buckets, int max_dist) {
 
 struct Layout {
   size_t x, x1, qkv, q, attn, ffn, inh, xi, stash, vis, part_val, part_idx, stats, bias_tab,
-      bf_x, bf_attn, bf_ffn,
+      p_x, p_attn, p_ffn, ssq,
       bucket, rope_cos, rope_sin, status, cur_tok, g_pending, g_draft, g_target,
       g_count, g_active, g_nactive, g_stats, total;
   int rows_max, head_rows, parts_max, ctx_max;
@@ -65,11 +65,11 @@ bool make_layout(const ssd_dims& d, Layout& L) {
   L.part_val = take((size_t)L.head_rows * L.parts_max * 4);
   L.part_idx = take((size_t)L.head_rows * L.parts_max * 4);
   L.stats = take(rows * 8);
-  // bf16 operands of the skinny MFMA path (at most 16 rows)
-  const size_t dmax = D > (size_t)d.in_hidden ? D : (size_t)d.in_hidden;
-  L.bf_x = take(32 * dmax * 2);  // hi and lo planes of 16 rows each
-  L.bf_attn = take(32 * HD * 2);
-  L.bf_ffn = take(32 * (size_t)d.d_ff * 2);
+  // bf16 hi / lo operand planes of the skinny MFMA path (16 rows each) and partial sums of squares
+  L.p_x = take(32 * D * 2);
+  L.p_attn = take(32 * HD * 2);
+  L.p_ffn = take(32 * (size_t)d.d_ff * 2);
+  L.ssq = take((size_t)skinny_blocks((int)D) * 16 * 4);
   L.bias_tab = take(d.arch == SSD_ARCH_T5 ? (size_t)d.n_heads * d.max_seq * 4 : 0);
   L.bucket = take(d.arch == SSD_ARCH_T5 ? (size_t)d.max_seq * 4 : 0);
   L.rope_cos = take(d.arch == SSD_ARCH_LLAMA ? (size_t)d.max_seq * (d.d_head / 2) * 4 : 0);
@@ -220,21 +220,29 @@ int run_layers(ssd_ctx* c, float* x, int B, int C, int pos_off, int l0, int l1, 
   float* q = c->at<float>(c->L.q);
   float* attn = c->at<float>(c->L.attn);
   float* ffn = c->at<float>(c->L.ffn);
-  bf16_t* bx = c->at<bf16_t>(c->L.bf_x);
-  bf16_t* battn = c->at<bf16_t>(c->L.bf_attn);
-  bf16_t* bffn = c->at<bf16_t>(c->L.bf_ffn);
   int32_t* status = c->at<int32_t>(c->L.status);
-  // one linear layer: skinny (bf16 input xb) or the vector / tile paths (fp32 input a.x)
-  auto linear = [&](LinearArgs& a, const bf16_t* xb, int ldb) -> hipError_t {
+  // skinny operands: bf16 planes written once by each producer (p_x: gain * residual for the
+  // RMS-normalised projections, with per-block sums of squares in ssq; p_attn, p_ffn)
+  bf16_t* p_x = c->at<bf16_t>(c->L.p_x);
+  bf16_t* p_attn = c->at<bf16_t>(c->L.p_attn);
+  bf16_t* p_ffn = c->at<bf16_t>(c->L.p_ffn);
+  float* ssq = c->at<float>(c->L.ssq);
+  const int nssq_resid = skinny_blocks(D);
+  int nssq = 1;  // partials behind the current p_x
+  // one linear layer: the skinny MFMA path for a verify chunk, else the vector / tile paths
+  auto linear = [&](LinearArgs& a, const bf16_t* in, int in_ld) -> hipError_t {
     if (!skinny) return run_linear(c, a);
-    if (a.norm != NORM_NONE) {
-      hipError_t e = launch_norm_bf16(a.x, a.ldx, a.M, a.K, a.norm, a.gain, a.shift, a.eps, bx, a.K, s);
-      if (e != hipSuccess) return e;
-      xb = bx;
-      ldb = a.K;
-    }
-    return launch_linear_skinny(a, xb, ldb, s);
+    a.in_planes = in;
+    a.in_ld = in_ld;
+    if (a.norm == NORM_RMS) { a.in_ssq = ssq; a.in_nssq = nssq; }
+    return launch_linear_skinny(a, s);
   };
+  // a residual projection also leaves the planes of gain_next * x for the next projection
+  auto resid_out = [&](LinearArgs& a, const float* gain_next) {
+    if (!skinny || !gain_next) return;
+    a.out_planes = p_x; a.out_ld = D; a.out_ssq = ssq; a.out_gain = gain_next;
+  };
+  if (skinny) HIP_TRY(launch_skinny_prep(x, D, R, D, c->layers[l0].attn_norm, p_x, D, ssq, s));
   for (int l = l0; l < l1; ++l) {
     const ssd_layer_weights& lw = c->layers[l];
     // self-attention
@@ -247,12 +255,12 @@ int run_layers(ssd_ctx* c, float* x, int B, int C, int pos_off, int l0, int l1, 
     a.kvdtype = d.kvdtype; a.max_seq = d.max_seq; a.status = status;
     a.rope_cos = t5 ? nullptr : c->at<float>(c->L.rope_cos);
     a.rope_sin = t5 ? nullptr : c->at<float>(c->L.rope_sin);
-    if (!skinny && linear_is_vector(a)) {
+    if (skinny || linear_is_vector(a)) {
       // rotary and the KV store fused into the projection's epilogue
-      HIP_TRY(run_linear(c, a));
+      HIP_TRY(linear(a, p_x, D));
     } else {
       a.epi = EPI_STORE; a.y = qkv; a.ldy = 3 * HD;
-      HIP_TRY(linear(a, nullptr, 0));
+      HIP_TRY(run_linear(c, a));
       RopeScatterArgs rs;
       rs.qkv = qkv; rs.q_out = q; rs.B = B; rs.C = C; rs.H = d.n_heads; rs.dh = d.d_head;
       rs.kvdtype = d.kvdtype; rs.kv = a.kv;
@@ -261,7 +269,7 @@ int run_layers(ssd_ctx* c, float* x, int B, int C, int pos_off, int l0, int l1, 
       HIP_TRY(launch_rope_scatter(rs, s));
     }
     AttnArgs at;
-    at.q = q; at.out = attn; at.out_bf16 = skinny ? battn : nullptr;
+    at.q = q; at.out = attn; at.out_planes = skinny ? p_attn : nullptr;
     at.B = B; at.C = C; at.H = d.n_heads; at.dh = d.d_head;
     at.kvdtype = d.kvdtype; at.cross = 0; at.kv = paged(c, l, pos_off);
     at.bias = t5 ? c->at<float>(c->L.bias_tab) : nullptr;
@@ -272,14 +280,16 @@ int run_layers(ssd_ctx* c, float* x, int B, int C, int pos_off, int l0, int l1, 
     a = lin(c);
     a.x = attn; a.ldx = HD; a.M = R; a.K = HD;
     a.w[0] = lw.wo; a.n_per = D; a.epi = EPI_RESID; a.y = x; a.ldy = D;
-    HIP_TRY(linear(a, battn, HD));
+    resid_out(a, t5 ? lw.xattn_norm : lw.ffn_norm);
+    HIP_TRY(linear(a, p_attn, HD));
+    nssq = nssq_resid;
     // cross-attention to the visual tokens
     if (t5) {
       a = lin(c);
       a.x = x; a.ldx = D; a.M = R; a.K = D;
       a.norm = NORM_RMS; a.gain = lw.xattn_norm;
       a.w[0] = lw.xq; a.n_per = HD; a.epi = EPI_STORE; a.y = q; a.ldy = HD;
-      HIP_TRY(linear(a, nullptr, 0));
+      HIP_TRY(linear(a, p_x, D));
       AttnArgs xa = at;
       xa.cross = 1;
       xa.bias = nullptr;
@@ -291,7 +301,8 @@ int run_layers(ssd_ctx* c, float* x, int B, int C, int pos_off, int l0, int l1, 
       a = lin(c);
       a.x = attn; a.ldx = HD; a.M = R; a.K = HD;
       a.w[0] = lw.xo; a.n_per = D; a.epi = EPI_RESID; a.y = x; a.ldy = D;
-      HIP_TRY(linear(a, battn, HD));
+      resid_out(a, lw.ffn_norm);
+      HIP_TRY(linear(a, p_attn, HD));
     }
     // feed-forward
     a = lin(c);
@@ -299,13 +310,14 @@ int run_layers(ssd_ctx* c, float* x, int B, int C, int pos_off, int l0, int l1, 
     a.norm = NORM_RMS; a.gain = lw.ffn_norm;
     a.w[0] = lw.w_gate; a.w[1] = lw.w_up; a.n_mats = 2; a.n_per = d.d_ff;
     a.epi = t5 ? EPI_GATED_GELU : EPI_GATED_SILU; a.y = ffn; a.ldy = d.d_ff;
-    if (skinny) { a.y = nullptr; a.y_bf16 = bffn; a.ldy_bf16 = d.d_ff; }
-    HIP_TRY(linear(a, nullptr, 0));
+    if (skinny) { a.y = nullptr; a.out_planes = p_ffn; a.out_ld = d.d_ff; }
+    HIP_TRY(linear(a, p_x, D));
     a = lin(c);
     a.x = ffn; a.ldx = d.d_ff; a.M = R; a.K = d.d_ff;
     a.w[0] = lw.w_down; a.n_per = D; a.epi = EPI_RESID; a.y = x; a.ldy = D;
     if (stash && l == stash_layer) { a.stash = stash; a.lds = ld_stash; }
-    HIP_TRY(linear(a, bffn, d.d_ff));
+    resid_out(a, l + 1 < l1 ? c->layers[l + 1].attn_norm : nullptr);
+    HIP_TRY(linear(a, p_ffn, d.d_ff));
   }
   return SSD_OK;
 }
@@ -324,10 +336,11 @@ int run_head(ssd_ctx* c, const float* x, int ldx, int M, int C, float* logits, i
   a.logits = logits; a.ldl = ldl;
   int n_parts = 0;
   if (skinny_ok(M, d.d_model, d.wdtype)) {
-    bf16_t* bx = c->at<bf16_t>(c->L.bf_x);
-    HIP_TRY(launch_norm_bf16(x, ldx, M, d.d_model, NORM_RMS, c->w.final_norm, nullptr, d.norm_eps,
-                             bx, d.d_model, c->stream));
-    HIP_TRY(launch_linear_skinny(a, bx, d.d_model, c->stream, &n_parts));
+    bf16_t* p_x = c->at<bf16_t>(c->L.p_x);
+    float* ssq = c->at<float>(c->L.ssq);
+    HIP_TRY(launch_skinny_prep(x, ldx, M, d.d_model, c->w.final_norm, p_x, d.d_model, ssq, c->stream));
+    a.in_planes = p_x; a.in_ld = d.d_model; a.in_ssq = ssq; a.in_nssq = 1;
+    HIP_TRY(launch_linear_skinny(a, c->stream, &n_parts));
   } else {
     HIP_TRY(run_linear(c, a, &n_parts));
   }

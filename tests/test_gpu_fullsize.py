@@ -64,3 +64,29 @@ def test_c3_flant5_xl_bench_configuration():
 def test_c5_llava_7b_prefill_and_first_rounds():
     wl = synth.C5
     _check(wl, max_rounds=2, device_rounds=2)
+
+
+def test_c4_batch8_ragged_point():
+    """A point of the FlanT5-xl sweep at batch 8 (k 4, gamma 8): the verify chunk is 72 rows
+    (tile MFMA path) and every sequence keeps its own length.  Two sequences are replayed through
+    the oracle for their first rounds; all eight are checked against the device's own batch-1
+    runs token for token where no near-tie intervenes (first divergence must be a near-tie)."""
+    from paper_2510_22641_amd import runtime
+    wl = next(p for p in synth.c4_points() if p.batch == 8 and p.draft_layers == 4 and p.gamma == 8)
+    w, z, pr = parity.workload_inputs(wl, 0)
+    # stepwise calls on a ragged batch: gamma positions of slack for finished sequences
+    dd = runtime.from_workload(wl, 0, weights=w, extra_seq=wl.gamma)
+    dec = Decoder(wl.shape, w, wl.draft_layers)
+    del w
+    pt, vt = dd.upload_inputs(pr, z)
+    print(f"[{wl.name}] device run", flush=True)
+    run = parity.device_run(dd, pt, vt, wl.new_tokens, wl.gamma, reuse=True)
+    assert dd.sync_status() == (0, 0)
+    assert all(len(t) == wl.new_tokens for t in run.tokens)
+    lens = {len([r for r in run.rounds if r.active[b]]) for b in range(wl.batch)}
+    print(f"[{wl.name}] rounds per sequence {sorted(lens)}; oracle replay", flush=True)
+    for b in (0, 5):
+        parity.check_run_against_oracle(dec, wl.shape, pr[b], z[b], run, b, wl.gamma, max_rounds=3)
+    toks, stats = dd.generate(pt, vt, wl.new_tokens, wl.gamma, speculative=True, reuse=True)
+    assert toks.cpu().numpy().tolist() == run.tokens
+    assert dd.sync_status() == (0, 0)

@@ -13,13 +13,13 @@ pytestmark = pytest.mark.gpu
 SMALL = [synth.S1, synth.S_T5, synth.S_LLAMA, synth.S_LLAMA_F32]
 
 
-def _setup(wl, seed=0, batch=None, page_seed=None, weights=None, max_batch=None):
+def _setup(wl, seed=0, batch=None, page_seed=None, weights=None, max_batch=None, extra_seq=0):
     from paper_2510_22641_amd import runtime
     w, z, pr = parity.workload_inputs(wl, seed, batch)
     if weights is not None:
         weights(w)
     dd = runtime.from_workload(wl, seed, weights=w, max_batch=max_batch or batch or wl.batch,
-                               page_seed=page_seed, extra_seq=0)
+                               page_seed=page_seed, extra_seq=extra_seq)
     dec = Decoder(wl.shape, w, wl.draft_layers)
     pt, vt = dd.upload_inputs(pr, z)
     return dd, dec, pr, z, pt, vt
@@ -113,8 +113,11 @@ def test_forced_drafts_acceptance_rule(wl):
 @pytest.mark.parametrize("wl", [synth.S_T5, synth.S_LLAMA], ids=lambda w: w.name)
 def test_ragged_batch_each_sequence_matches_oracle(wl):
     B = 3
-    dd, dec, pr, z, pt, vt = _setup(wl, seed=6, batch=B, page_seed=7)
+    # stepwise calls on a ragged batch: finished sequences are still drafted at their last
+    # length, so the cache holds gamma more positions
+    dd, dec, pr, z, pt, vt = _setup(wl, seed=6, batch=B, page_seed=7, extra_seq=wl.gamma)
     run = parity.device_run(dd, pt, vt, wl.new_tokens, wl.gamma, reuse=True)
+    assert dd.sync_status() == (0, 0)
     accepted = set()
     for b in range(B):
         parity.check_run_against_oracle(dec, wl.shape, pr[b], z[b], run, b, wl.gamma)
@@ -122,6 +125,24 @@ def test_ragged_batch_each_sequence_matches_oracle(wl):
         accepted.add(tuple(int(r.accepted[b]) for r in run.rounds if r.active[b]))
     toks, _ = dd.generate(pt, vt, wl.new_tokens, wl.gamma, speculative=True, reuse=True)
     assert toks.cpu().numpy().tolist() == run.tokens
+    assert dd.sync_status() == (0, 0)
+
+
+def test_generate_ragged_batch_fits_the_minimal_cache():
+    """ssd_generate on a batch whose sequences finish in different rounds needs no slack: a
+    finished sequence keeps only its emitted positions."""
+    wl = synth.S_LLAMA
+    B = 4
+    dd, dec, pr, z, pt, vt = _setup(wl, seed=8, batch=B)
+    toks, stats = dd.generate(pt, vt, wl.new_tokens, wl.gamma, speculative=True, reuse=True)
+    assert dd.sync_status() == (0, 0)
+    one = []
+    for b in range(B):
+        t1, _ = dd.generate(pt[b:b + 1], vt[b:b + 1], wl.new_tokens, wl.gamma,
+                            speculative=True, reuse=True)
+        one.append(t1.cpu().numpy()[0].tolist())
+    assert dd.sync_status() == (0, 0)
+    assert toks.cpu().numpy().tolist() == one
 
 
 def test_zero_deep_layers_accept_every_draft():
