@@ -57,6 +57,27 @@ def verify_bytes(shape, B: int, gamma: int, ctx: int, kv_bytes: int = 4) -> floa
     return shape.n_layers * (layer + kv) + V * d * we + d * 4
 
 
+def counted_traffic(kernel: str):
+    """HBM bytes per launch of the dominant kernel from the committed rocprofv3 counter summary
+    (FETCH_SIZE and WRITE_SIZE runs scaled by a copy-kernel reading), or None when the summary is
+    missing or the kernel source has changed since the counters were taken."""
+    import hashlib
+    import re
+    path = os.path.join(ROOT, "profiles", "gemv1_c3_flant5_xl_hbm_traffic.md")
+    src = os.path.join(ROOT, "paper_2510_22641_amd", "csrc", "linear.hip")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    if f"`{kernel}`" not in text:
+        return None
+    fields = dict(re.findall(r"^([a-z_0-9]+): (\S+)$", text, re.M))
+    if fields.get("kernel_source_sha256") != hashlib.sha256(open(src, "rb").read()).hexdigest():
+        return None
+    return {"bytes": int(fields["traffic_bytes_per_launch"]),
+            "algorithmic_bytes": int(fields["algorithmic_bytes_per_launch"]),
+            "launches": int(fields["launches"]), "source": os.path.relpath(path, ROOT)}
+
+
 def step_timings(dd, pt, vt, B: int, g: int, rounds: int = 8):
     """Median per-step draft time and per-pass verify time over a few rounds after prefill (HIP
     events on the decoder's stream around the captured draft and verify graphs)."""
@@ -177,6 +198,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--sweep", choices=["c4"], default=None,
                     help="run the FlanT5-xl sweep instead (one JSON line per point)")
+    ap.add_argument("--copy-bytes", type=int, default=0,
+                    help="only copy this many bytes device to device three times (the reference "
+                         "reading for the HBM byte counters) and exit")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU: the decode loop is not sharded (asked for {args.gpus})",
@@ -184,6 +208,16 @@ def main():
         sys.exit(2)
     if args.sweep:
         sweep_c4(args)
+        return
+    if args.copy_bytes:
+        import torch
+        src = torch.ones(args.copy_bytes // 4, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes": src.numel() * 4, "copies": 3}))
         return
 
     import numpy as np
@@ -253,9 +287,13 @@ def main():
     pieces = (sh.d_model + 511) // 512
     kp = 4 if pieces <= 4 else (12 if 8 < pieces <= 12 else 8)
     kname = "gemv1_kernel<%s, %d, 1>" % ("unsigned short" if sh.dtype == "bf16" else "float", kp)
+    counted = counted_traffic(kname) if wl.name == "c3-flant5-xl" else None
     roofline = {"bound": "hbm", "kernel": kname + " (one-row weight-streaming GEMV, RMSNorm folded)",
                 "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                "frac": round(achieved / HBM_PEAK_GBS, 4),
+                "traffic": counted["bytes"] if counted else None,
+                "traffic_algorithmic": counted["algorithmic_bytes"] if counted else None,
+                "traffic_source": counted["source"] if counted else None,
                 "bytes_per_launch": int(per_launch_bytes), "avg_launch_us": round(avg_s * 1e6, 3),
                 "launches": n_launch}
 

@@ -208,11 +208,11 @@ __global__ __launch_bounds__(256) void attn_kernel(const AttnArgs a, const int s
     const float v = (red[0][jq][d] + red[1][jq][d]) + (red[2][jq][d] + red[3][jq][d]);
     const size_t o = (size_t)(b * a.C + j0 + jq) * HD + h * DH + d;
     a.out[o] = v * inv_sum[jq];
-    if (a.out_planes) {  // hi / lo bf16 planes for the skinny MFMA consumer (rows < 16)
+    if (a.out_planes) {  // hi / lo bf16 planes for the skinny MFMA consumer (rows < plane_rows)
       const float y = v * inv_sum[jq];
       const uint32_t hi = f32_to_bf16(y);
       a.out_planes[o] = (bf16_t)hi;
-      a.out_planes[o + (size_t)16 * HD] = (bf16_t)f32_to_bf16(y - bf16_to_f32(hi));
+      a.out_planes[o + (size_t)a.plane_rows * HD] = (bf16_t)f32_to_bf16(y - bf16_to_f32(hi));
     }
   }
 }

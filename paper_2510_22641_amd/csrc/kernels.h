@@ -74,15 +74,17 @@ struct LinearArgs {
   // row statistics for the MFMA path's normalisation (filled by launch_linear)
   float2* stats = nullptr;    // [M] workspace
   int use_mfma = -1;          // -1: choose; 0: vector path; 1: MFMA path
-  // Skinny path operands.  Input: bf16 planes hi / lo of the (gain-multiplied) rows, hi row m at
-  // in_planes + m * in_ld, lo row m at in_planes + (16 + m) * in_ld; with NORM_RMS, 1/rms of row m
-  // comes from the partial sums of squares in_ssq[p][m], p < in_nssq (16 floats per p).
+  // Skinny path operands, in buffers of plane_rows rows (a multiple of 16, >= M).  Input: bf16
+  // planes hi / lo of the (gain-multiplied) rows, hi row m at in_planes + m * in_ld, lo row m at
+  // in_planes + (plane_rows + m) * in_ld; with NORM_RMS, 1/rms of row m comes from the partial sums
+  // of squares in_ssq[p * plane_rows + m], p < in_nssq.
+  int plane_rows = 16;
   const bf16_t* in_planes = nullptr;
   int in_ld = 0;
   const float* in_ssq = nullptr;
   int in_nssq = 0;
   // Output planes for the next skinny launch (EPI_RESID: of out_gain * y_new, plus per-block
-  // partial sums of squares of y_new in out_ssq[block][m]; gated: of y; null: none).
+  // partial sums of squares of y_new in out_ssq[block * plane_rows + m]; gated: of y; null: none).
   bf16_t* out_planes = nullptr;
   int out_ld = 0;
   float* out_ssq = nullptr;
@@ -111,17 +113,19 @@ hipError_t launch_linear(LinearArgs a, hipStream_t s, int* n_parts = nullptr,
 // Upper bound of the partials per row for n_out outputs (workspace sizing).
 int argmax_parts_max(int n_out);
 
-// Rows of a verify chunk (2..16, bf16 weights) take the skinny MFMA path: the inputs arrive as
-// bf16 planes written once by their producer (a.in_planes ..., see LinearArgs), with RMSNorm
-// folded (a.norm = NORM_RMS: the gain is already in the planes, 1/rms from a.in_ssq) or none;
-// the gated, QKV (rotary + KV store), residual (+ next planes), bias and argmax epilogues.
+// Rows of a verify chunk (2..128, bf16 weights) take the skinny MFMA path (16 rows per block
+// row of the grid): the inputs arrive as bf16 planes written once by their producer (a.in_planes
+// ..., see LinearArgs), with RMSNorm folded (a.norm = NORM_RMS: the gain is already in the planes,
+// 1/rms from a.in_ssq) or none; the gated, QKV (rotary + KV store), residual (+ next planes), bias
+// and argmax epilogues.
 bool skinny_ok(int M, int K, int wdtype);
 hipError_t launch_linear_skinny(const LinearArgs& a, hipStream_t s, int* n_parts = nullptr);
 
-// Planes of gain * x for M <= 16 rows (hi row m at out + m * ldo, lo at out + (16 + m) * ldo) and
-// the full-row sums of squares ssq[0][m] (one partial): the input of the first skinny launch.
+// Planes of gain * x for M <= plane_rows rows (hi row m at out + m * ldo, lo at
+// out + (plane_rows + m) * ldo) and the full-row sums of squares ssq[m] (one partial): the input
+// of the first skinny launch of a pass.
 hipError_t launch_skinny_prep(const float* x, int ldx, int M, int K, const float* gain,
-                              bf16_t* out, int ldo, float* ssq, hipStream_t s);
+                              bf16_t* out, int ldo, int plane_rows, float* ssq, hipStream_t s);
 
 // Partial sums of squares per block of a skinny residual epilogue (the in_nssq of its consumer).
 int skinny_blocks(int n_out);
@@ -168,7 +172,8 @@ hipError_t launch_rope_scatter(const RopeScatterArgs& a, hipStream_t s);
 struct AttnArgs {
   const float* q;  // [B*C][H*dh]
   float* out;      // [B*C][H*dh]
-  bf16_t* out_planes = nullptr;  // optional hi / lo bf16 planes of out (rows < 16; lo 16 rows on)
+  bf16_t* out_planes = nullptr;  // optional hi / lo bf16 planes of out (lo plane_rows rows on)
+  int plane_rows = 16;
   int B, C, H, dh;
   int kvdtype;
   int cross;         // 0: causal over the paged cache; 1: dense over n_keys cross-attention keys

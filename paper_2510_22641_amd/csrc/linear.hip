@@ -1,19 +1,20 @@
 // Linear layers y = epilogue(W . norm(x)) for the decoder, the imitation network and the LM head.
 //
-// Two paths:
-//  * gemv_kernel — weight streaming for few rows (M <= 8: the batch-1..8 draft steps and the
-//    batch-1 verify chunk).  Each wave owns two output features at a time and reads their weight
-//    rows with 16-byte loads (8 bf16 / 4+4 f32 per lane; a batch is 2048 elements per row).
-//    Input rows are requested before the weights and staged in LDS with the norm gain applied;
-//    the per-row 1/rms is applied in the epilogue.  One row pair per wave: the resident waves of a
-//    CU hide the memory latency; fp32 accumulation, wave reduction, fused epilogue, and for the LM
-//    head a per-block (max, argmax) partial that launch_argmax_final reduces.
-//    Bound: HBM bytes of W.
-//  * gemv_mfma_kernel — 2..16 rows (the batch-1 verify chunk): 16 features per block, weights
-//    straight from HBM and bf16 inputs from L2 into MFMA operands, no staging.
+// Paths:
+//  * gemv1_kernel — one input row (the batch-1 draft and greedy steps): a wave holds the whole
+//    input row in registers and streams two weight rows with 16-byte loads; the norm statistics
+//    are wave reductions (RMSNorm folded into the epilogue as 1/rms).  Bound: HBM bytes of W.
+//  * gemv_kernel — weight streaming for 2..8 rows in float32 (or rows longer than a batch): the
+//    input rows are staged in LDS with the gain applied, one row pair per wave.
+//  * gemv_mfma_kernel — 2..128 rows with bf16 weights (the verify chunk, batch-8 draft steps):
+//    16 features x 16 rows per block on v_mfma_f32_16x16x32_bf16, weights straight from HBM,
+//    inputs as bf16 hi / lo planes written once by their producer.  Bound: HBM bytes of W.
 //  * gemm_kernel — 64x64x64 tiles on v_mfma_f32_16x16x32_bf16 with LDS staging, for larger M
-//    (prefill, batch-8 verify).  The fp32 inputs are normalised and rounded to bf16 while they are
-//    staged.
+//    (prefill).  The fp32 inputs are normalised and split into bf16 hi / lo planes while staged.
+//
+// Every path accumulates in fp32 and ends in a fused epilogue (store, residual (+ stash), gated
+// activation, bias + GELU, bias + residual, per-block (max, argmax) partials for the LM head, or
+// QKV with rotary and the paged KV store).
 #include "device.h"
 #include "kernels.h"
 
@@ -555,7 +556,7 @@ __global__ __launch_bounds__(256) void gemv1_kernel(const LinearArgs a) {
 }
 
 // ---------------------------------------------------------------------------------------------
-// Skinny MFMA path: 2..16 input rows (the batch-1 verify chunk), bf16 weights.
+// Skinny MFMA path: 2..128 input rows (the verify chunk), bf16 weights, 16 rows per grid row.
 // A block owns 16 output features (the A rows of v_mfma_f32_16x16x32_bf16) and its 4 waves split
 // K; the input rows are the B columns.  The inputs arrive as two bf16 planes hi = bf16(v),
 // lo = bf16(v - hi) of v = g * x (g the RMSNorm gain, or 1), written once by their producer;
@@ -617,10 +618,12 @@ __global__ __launch_bounds__(64 * SKW) void gemv_mfma_kernel(const LinearArgs a)
     }
   }
   const int kq = (lane >> 4) * 16;  // this lane's 16 elements within a step
-  const int tok = lane & 15;
+  const int t0 = blockIdx.y * 16;   // this block's first input row
+  const int tok = t0 + (lane & 15);
   const bool tok_ok = tok < M;
+  const int PR = a.plane_rows;
   const bf16_t* brow = a.in_planes + (size_t)(tok_ok ? tok : 0) * a.in_ld;
-  const bf16_t* brow_lo = brow + (size_t)16 * a.in_ld;
+  const bf16_t* brow_lo = brow + (size_t)PR * a.in_ld;
 
   f32x4_t acc[NB];
 #pragma unroll
@@ -678,7 +681,7 @@ __global__ __launch_bounds__(64 * SKW) void gemv_mfma_kernel(const LinearArgs a)
 #pragma unroll
     for (int i = 0; i < SSQ_MAX / NG; ++i) {
       const int p = (tid >> 4) + NG * i;
-      v[i] = a.in_ssq[(size_t)min(p, a.in_nssq - 1) * 16 + (tid & 15)];
+      v[i] = a.in_ssq[(size_t)min(p, a.in_nssq - 1) * PR + t0 + (tid & 15)];
     }
 #pragma unroll
     for (int i = 0; i < SSQ_MAX / NG; ++i) sp += ((tid >> 4) + NG * i < a.in_nssq) ? v[i] : 0.f;
@@ -698,9 +701,9 @@ __global__ __launch_bounds__(64 * SKW) void gemv_mfma_kernel(const LinearArgs a)
   }
   __syncthreads();
 
-  // epilogue: thread (feature f, token t) for the first 256 threads
+  // epilogue: thread (feature f, row t0 + t) for the first 256 threads
   static_assert(SKW >= 4, "the epilogue needs 256 threads");
-  const int f = (tid >> 4) & 15, t = tid & 15;
+  const int f = (tid >> 4) & 15, t = tid & 15, tg = t0 + t;
   const bool lead = tid < 256;
   auto tile_sum = [&](int b, int ff) {
     float v = 0.f;
@@ -712,37 +715,37 @@ __global__ __launch_bounds__(64 * SKW) void gemv_mfma_kernel(const LinearArgs a)
   const int n = blockIdx.x * 16 + f;
   const float v = tile_sum(0, f) * rscale;
   if (a.epi == EPI_ARGMAX) {
-    const bool ok = lead && t < M && n < n_out;
+    const bool ok = lead && tg < M && n < n_out;
     if (lead) {
       best_v[t][f] = ok ? v : -INFINITY;
       best_i[t][f] = ok ? n : INT_MAX;
     }
-    if (ok && a.logits) a.logits[(size_t)t * a.ldl + n] = v;
+    if (ok && a.logits) a.logits[(size_t)tg * a.ldl + n] = v;
     __syncthreads();
-    if (tid < M) {
+    if (tid < 16 && t0 + tid < M) {
       float bvv = -INFINITY;
       int bi = INT_MAX;
       for (int ff = 0; ff < 16; ++ff) argmax_merge(bvv, bi, best_v[tid][ff], best_i[tid][ff]);
-      a.part_val[(size_t)tid * a.n_parts + blockIdx.x] = bvv;
-      a.part_idx[(size_t)tid * a.n_parts + blockIdx.x] = bi;
+      a.part_val[(size_t)(t0 + tid) * a.n_parts + blockIdx.x] = bvv;
+      a.part_idx[(size_t)(t0 + tid) * a.n_parts + blockIdx.x] = bi;
     }
     return;
   }
   if (a.epi == EPI_RESID) {
     // y_new, the next planes and this block's partial sums of squares (all threads take part in
     // the reduction; rows past M or features past n_out contribute zero)
-    const bool ok = lead && t < M && n < n_out;
+    const bool ok = lead && tg < M && n < n_out;
     float y2 = 0.f;
     if (ok) {
-      float* yp = a.y + (size_t)t * a.ldy + n;
+      float* yp = a.y + (size_t)tg * a.ldy + n;
       const float tt = *yp + v;
       *yp = tt;
-      if (a.stash) a.stash[(size_t)t * a.lds + n] = tt;
+      if (a.stash) a.stash[(size_t)tg * a.lds + n] = tt;
       if (a.out_planes) {
         const float gv = a.out_gain ? a.out_gain[n] * tt : tt;
         const uint32_t hi = f32_to_bf16(gv);
-        a.out_planes[(size_t)t * a.out_ld + n] = (bf16_t)hi;
-        a.out_planes[(size_t)(16 + t) * a.out_ld + n] = (bf16_t)f32_to_bf16(gv - bf16_to_f32(hi));
+        a.out_planes[(size_t)tg * a.out_ld + n] = (bf16_t)hi;
+        a.out_planes[(size_t)(PR + tg) * a.out_ld + n] = (bf16_t)f32_to_bf16(gv - bf16_to_f32(hi));
       }
       y2 = tt * tt;
     }
@@ -752,40 +755,40 @@ __global__ __launch_bounds__(64 * SKW) void gemv_mfma_kernel(const LinearArgs a)
       y2 += __shfl_xor(y2, 32, SSD_WAVE);
       if (lead && lane < 16) sq[wave][lane] = y2;
       __syncthreads();
-      if (tid < 16) a.out_ssq[(size_t)blockIdx.x * 16 + tid] = (sq[0][tid] + sq[1][tid]) + (sq[2][tid] + sq[3][tid]);
+      if (tid < 16) a.out_ssq[(size_t)blockIdx.x * PR + t0 + tid] = (sq[0][tid] + sq[1][tid]) + (sq[2][tid] + sq[3][tid]);
     }
     return;
   }
-  if (!lead || t >= M) return;
+  if (!lead || tg >= M) return;
   if (qkv) {
-    if (f < 8) qkv_store_pair(a, q_mat, q_c + f, t, v, tile_sum(0, f + 8) * rscale);
+    if (f < 8) qkv_store_pair(a, q_mat, q_c + f, tg, v, tile_sum(0, f + 8) * rscale);
     return;
   }
   if (n >= n_out) return;
   if (GATED) {
     const float act = apply_epi_act(a.epi, v, tile_sum(NB - 1, f) * rscale);
-    if (a.y) a.y[(size_t)t * a.ldy + n] = act;
+    if (a.y) a.y[(size_t)tg * a.ldy + n] = act;
     if (a.out_planes) {
       const uint32_t hi = f32_to_bf16(act);
-      a.out_planes[(size_t)t * a.out_ld + n] = (bf16_t)hi;
-      a.out_planes[(size_t)(16 + t) * a.out_ld + n] = (bf16_t)f32_to_bf16(act - bf16_to_f32(hi));
+      a.out_planes[(size_t)tg * a.out_ld + n] = (bf16_t)hi;
+      a.out_planes[(size_t)(PR + tg) * a.out_ld + n] = (bf16_t)f32_to_bf16(act - bf16_to_f32(hi));
     }
     return;
   }
-  float* yp = a.y + (size_t)t * a.ldy + n;
+  float* yp = a.y + (size_t)tg * a.ldy + n;
   switch (a.epi) {
     case EPI_STORE: *yp = v; break;
     case EPI_BIAS_GELU: *yp = gelu_tanh(v + a.bias[n]); break;
-    case EPI_BIAS_RESID: *yp = (a.resid ? a.resid[(size_t)t * a.ldr + n] : 0.f) + (v + a.bias[n]); break;
+    case EPI_BIAS_RESID: *yp = (a.resid ? a.resid[(size_t)tg * a.ldr + n] : 0.f) + (v + a.bias[n]); break;
     default: break;
   }
 }
 
 // Planes of gain * x and the row's sum of squares (ssq[m], one partial) for the first skinny
-// launch of a pass — one block per row, the row held in registers for K <= 4096.
+// launch of a pass — one block per row.
 __global__ __launch_bounds__(256) void skinny_prep_kernel(const float* __restrict__ x, int ldx, int K,
                                                           const float* __restrict__ gain,
-                                                          bf16_t* __restrict__ out, int ldo,
+                                                          bf16_t* __restrict__ out, int ldo, int PR,
                                                           float* __restrict__ ssq) {
   __shared__ float red[4];
   const int m = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -803,7 +806,7 @@ __global__ __launch_bounds__(256) void skinny_prep_kernel(const float* __restric
       l[e] = f32_to_bf16(f[e] - bf16_to_f32(h[e]));
     }
     *reinterpret_cast<uint2*>(out + (size_t)m * ldo + k) = make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16));
-    *reinterpret_cast<uint2*>(out + (size_t)(16 + m) * ldo + k) = make_uint2(l[0] | (l[1] << 16), l[2] | (l[3] << 16));
+    *reinterpret_cast<uint2*>(out + (size_t)(PR + m) * ldo + k) = make_uint2(l[0] | (l[1] << 16), l[2] | (l[3] << 16));
   }
   s2 = wave_sum(s2);
   if (lane == 0) red[wave] = s2;
@@ -1142,7 +1145,7 @@ int argmax_parts_max(int n_out) {
   return groups > tiles ? groups : tiles;
 }
 
-bool skinny_ok(int M, int K, int wdtype) { return wdtype == 1 && M >= 2 && M <= 16 && K % 64 == 0; }
+bool skinny_ok(int M, int K, int wdtype) { return wdtype == 1 && M >= 2 && M <= 128 && K % 64 == 0; }
 
 int skinny_blocks(int n_out) { return (n_out + 15) / 16; }
 
@@ -1150,13 +1153,13 @@ hipError_t launch_linear_skinny(const LinearArgs& a, hipStream_t s, int* n_parts
   const bool gated = (a.epi == EPI_GATED_GELU || a.epi == EPI_GATED_SILU);
   const int n_out = gated ? a.n_per : a.n_per * a.n_mats;
   const int tiles = skinny_blocks(n_out);
-  if (!a.in_planes || a.norm == NORM_LN) return hipErrorInvalidValue;
+  if (!a.in_planes || a.norm == NORM_LN || a.plane_rows % 16 || a.M > a.plane_rows) return hipErrorInvalidValue;
   if (a.norm == NORM_RMS && (!a.in_ssq || a.in_nssq < 1 || a.in_nssq > SSQ_MAX)) return hipErrorInvalidValue;
   if (a.epi == EPI_QKV && (a.n_mats != 3 || (a.d_head / 2) % 8 != 0)) return hipErrorInvalidValue;
   LinearArgs b = a;
   if (b.epi == EPI_ARGMAX) b.n_parts = tiles;
   if (n_parts) *n_parts = b.n_parts;
-  const dim3 grid(tiles), block(64 * SKW);
+  const dim3 grid(tiles, (a.M + 15) / 16), block(64 * SKW);
   const bool rms = a.norm == NORM_RMS;
   if (gated && rms) hipLaunchKernelGGL((gemv_mfma_kernel<true, true>), grid, block, 0, s, b);
   else if (gated) hipLaunchKernelGGL((gemv_mfma_kernel<true, false>), grid, block, 0, s, b);
@@ -1166,9 +1169,10 @@ hipError_t launch_linear_skinny(const LinearArgs& a, hipStream_t s, int* n_parts
 }
 
 hipError_t launch_skinny_prep(const float* x, int ldx, int M, int K, const float* gain, bf16_t* out,
-                              int ldo, float* ssq, hipStream_t s) {
-  if (M < 1 || M > 16 || K % 4) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(skinny_prep_kernel, dim3(M), dim3(256), 0, s, x, ldx, K, gain, out, ldo, ssq);
+                              int ldo, int plane_rows, float* ssq, hipStream_t s) {
+  if (M < 1 || M > plane_rows || K % 4) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(skinny_prep_kernel, dim3(M), dim3(256), 0, s, x, ldx, K, gain, out, ldo,
+                     plane_rows, ssq);
   return hipGetLastError();
 }
 

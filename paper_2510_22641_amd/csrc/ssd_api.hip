@@ -34,7 +34,7 @@ struct Layout {
       p_x, p_attn, p_ffn, ssq,
       bucket, rope_cos, rope_sin, status, cur_tok, g_pending, g_draft, g_target,
       g_count, g_active, g_nactive, g_stats, total;
-  int rows_max, head_rows, parts_max, ctx_max;
+  int rows_max, head_rows, parts_max, ctx_max, plane_rows;
 };
 
 int ctx_len_max(const ssd_dims& d) {
@@ -65,11 +65,18 @@ bool make_layout(const ssd_dims& d, Layout& L) {
   L.part_val = take((size_t)L.head_rows * L.parts_max * 4);
   L.part_idx = take((size_t)L.head_rows * L.parts_max * 4);
   L.stats = take(rows * 8);
-  // bf16 hi / lo operand planes of the skinny MFMA path (16 rows each) and partial sums of squares
-  L.p_x = take(32 * D * 2);
-  L.p_attn = take(32 * HD * 2);
-  L.p_ffn = take(32 * (size_t)d.d_ff * 2);
-  L.ssq = take((size_t)skinny_blocks((int)D) * 16 * 4);
+  // bf16 hi / lo operand planes of the skinny MFMA path (plane_rows rows each: the largest verify
+  // chunk, rounded up to 16, at most 128) and its partial sums of squares
+  {
+    size_t pr = B * (G + 1);
+    pr = pr < 16 ? 16 : (pr > 128 ? 128 : (pr + 15) / 16 * 16);
+    L.plane_rows = (int)pr;
+  }
+  const size_t PRz = (size_t)L.plane_rows;
+  L.p_x = take(2 * PRz * D * 2);
+  L.p_attn = take(2 * PRz * HD * 2);
+  L.p_ffn = take(2 * PRz * (size_t)d.d_ff * 2);
+  L.ssq = take((size_t)skinny_blocks((int)D) * PRz * 4);
   L.bias_tab = take(d.arch == SSD_ARCH_T5 ? (size_t)d.n_heads * d.max_seq * 4 : 0);
   L.bucket = take(d.arch == SSD_ARCH_T5 ? (size_t)d.max_seq * 4 : 0);
   L.rope_cos = take(d.arch == SSD_ARCH_LLAMA ? (size_t)d.max_seq * (d.d_head / 2) * 4 : 0);
@@ -214,7 +221,8 @@ int run_layers(ssd_ctx* c, float* x, int B, int C, int pos_off, int l0, int l1, 
   const int R = B * C, D = d.d_model, HD = d.n_heads * d.d_head;
   const bool t5 = d.arch == SSD_ARCH_T5;
   // 2..16 rows in bf16: MFMA with operands written once as bf16 (the verify chunk)
-  const bool skinny = skinny_ok(R, D, d.wdtype) && skinny_ok(R, HD, d.wdtype) &&
+  const int PR = c->L.plane_rows;
+  const bool skinny = R <= PR && skinny_ok(R, D, d.wdtype) && skinny_ok(R, HD, d.wdtype) &&
                       skinny_ok(R, d.d_ff, d.wdtype);
   float* qkv = c->at<float>(c->L.qkv);
   float* q = c->at<float>(c->L.q);
@@ -234,6 +242,7 @@ int run_layers(ssd_ctx* c, float* x, int B, int C, int pos_off, int l0, int l1, 
     if (!skinny) return run_linear(c, a);
     a.in_planes = in;
     a.in_ld = in_ld;
+    a.plane_rows = PR;
     if (a.norm == NORM_RMS) { a.in_ssq = ssq; a.in_nssq = nssq; }
     return launch_linear_skinny(a, s);
   };
@@ -242,7 +251,7 @@ int run_layers(ssd_ctx* c, float* x, int B, int C, int pos_off, int l0, int l1, 
     if (!skinny || !gain_next) return;
     a.out_planes = p_x; a.out_ld = D; a.out_ssq = ssq; a.out_gain = gain_next;
   };
-  if (skinny) HIP_TRY(launch_skinny_prep(x, D, R, D, c->layers[l0].attn_norm, p_x, D, ssq, s));
+  if (skinny) HIP_TRY(launch_skinny_prep(x, D, R, D, c->layers[l0].attn_norm, p_x, D, PR, ssq, s));
   for (int l = l0; l < l1; ++l) {
     const ssd_layer_weights& lw = c->layers[l];
     // self-attention
@@ -269,7 +278,7 @@ int run_layers(ssd_ctx* c, float* x, int B, int C, int pos_off, int l0, int l1, 
       HIP_TRY(launch_rope_scatter(rs, s));
     }
     AttnArgs at;
-    at.q = q; at.out = attn; at.out_planes = skinny ? p_attn : nullptr;
+    at.q = q; at.out = attn; at.out_planes = skinny ? p_attn : nullptr; at.plane_rows = PR;
     at.B = B; at.C = C; at.H = d.n_heads; at.dh = d.d_head;
     at.kvdtype = d.kvdtype; at.cross = 0; at.kv = paged(c, l, pos_off);
     at.bias = t5 ? c->at<float>(c->L.bias_tab) : nullptr;
@@ -335,11 +344,13 @@ int run_head(ssd_ctx* c, const float* x, int ldx, int M, int C, float* logits, i
   a.part_idx = c->at<int>(c->L.part_idx);
   a.logits = logits; a.ldl = ldl;
   int n_parts = 0;
-  if (skinny_ok(M, d.d_model, d.wdtype)) {
+  if (M <= c->L.plane_rows && skinny_ok(M, d.d_model, d.wdtype)) {
     bf16_t* p_x = c->at<bf16_t>(c->L.p_x);
     float* ssq = c->at<float>(c->L.ssq);
-    HIP_TRY(launch_skinny_prep(x, ldx, M, d.d_model, c->w.final_norm, p_x, d.d_model, ssq, c->stream));
-    a.in_planes = p_x; a.in_ld = d.d_model; a.in_ssq = ssq; a.in_nssq = 1;
+    const int PR = c->L.plane_rows;
+    HIP_TRY(launch_skinny_prep(x, ldx, M, d.d_model, c->w.final_norm, p_x, d.d_model, PR, ssq,
+                               c->stream));
+    a.in_planes = p_x; a.in_ld = d.d_model; a.in_ssq = ssq; a.in_nssq = 1; a.plane_rows = PR;
     HIP_TRY(launch_linear_skinny(a, c->stream, &n_parts));
   } else {
     HIP_TRY(run_linear(c, a, &n_parts));
