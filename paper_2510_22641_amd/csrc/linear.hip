@@ -625,6 +625,24 @@ __global__ __launch_bounds__(64 * SKW) void gemv_mfma_kernel(const LinearArgs a)
   const bf16_t* brow = a.in_planes + (size_t)(tok_ok ? tok : 0) * a.in_ld;
   const bf16_t* brow_lo = brow + (size_t)PR * a.in_ld;
 
+  // values the epilogue needs, requested before the main batch (the wait counter retires loads
+  // in issue order, so they are in registers by the time the weights are): the producer's partial
+  // sums of squares (RMSNorm; thread: row t0 + tid % 16, partials tid / 16 + NG i) and the old
+  // residual value of this thread's output (clamped loads, never conditional)
+  float sv[RMS ? SSQ_MAX / NG : 1];
+  if (RMS) {
+#pragma unroll
+    for (int i = 0; i < SSQ_MAX / NG; ++i) {
+      const int p = (tid >> 4) + NG * i;
+      sv[i] = a.in_ssq[(size_t)min(p, a.in_nssq - 1) * PR + t0 + (tid & 15)];
+    }
+  }
+  float y_old = 0.f;
+  if (a.epi == EPI_RESID) {
+    const int ry = min(t0 + (tid & 15), M - 1), ny = min((int)blockIdx.x * 16 + ((tid >> 4) & 15), n_out - 1);
+    y_old = a.y[(size_t)ry * a.ldy + ny];
+  }
+
   f32x4_t acc[NB];
 #pragma unroll
   for (int b = 0; b < NB; ++b) acc[b] = f32x4_t{0.f, 0.f, 0.f, 0.f};
@@ -673,18 +691,10 @@ __global__ __launch_bounds__(64 * SKW) void gemv_mfma_kernel(const LinearArgs a)
       }
     }
   }
-  // RMSNorm: the producer's partial sums of squares (thread: token tid % 16, partials
-  // tid / 16 + NG i; one batch of clamped loads, unused ones count as zero)
   float sp = 0.f;
   if (RMS) {
-    float v[SSQ_MAX / NG];
 #pragma unroll
-    for (int i = 0; i < SSQ_MAX / NG; ++i) {
-      const int p = (tid >> 4) + NG * i;
-      v[i] = a.in_ssq[(size_t)min(p, a.in_nssq - 1) * PR + t0 + (tid & 15)];
-    }
-#pragma unroll
-    for (int i = 0; i < SSQ_MAX / NG; ++i) sp += ((tid >> 4) + NG * i < a.in_nssq) ? v[i] : 0.f;
+    for (int i = 0; i < SSQ_MAX / NG; ++i) sp += ((tid >> 4) + NG * i < a.in_nssq) ? sv[i] : 0.f;
   }
   // D[feature][token]: lane holds features 4 * (lane / 16) + e, token lane % 16
 #pragma unroll
@@ -737,9 +747,8 @@ __global__ __launch_bounds__(64 * SKW) void gemv_mfma_kernel(const LinearArgs a)
     const bool ok = lead && tg < M && n < n_out;
     float y2 = 0.f;
     if (ok) {
-      float* yp = a.y + (size_t)tg * a.ldy + n;
-      const float tt = *yp + v;
-      *yp = tt;
+      const float tt = y_old + v;
+      a.y[(size_t)tg * a.ldy + n] = tt;
       if (a.stash) a.stash[(size_t)tg * a.lds + n] = tt;
       if (a.out_planes) {
         const float gv = a.out_gain ? a.out_gain[n] * tt : tt;
