@@ -232,21 +232,23 @@ def main():
     weights = synth.workload_weights(wl, args.seed)
     prompts = synth.make_prompts(sh, args.seed, wl.batch, wl.prompt_len)
     visual = synth.make_visual(sh, args.seed, wl.batch)
-    dd = runtime.from_workload(wl, args.seed, weights=weights)
+    # capacity for the dynamic draft length too (up to gamma + 9 drafts a round)
+    dd = runtime.from_workload(wl, args.seed, weights=weights, max_gamma=wl.gamma + 9)
     pt, vt = dd.upload_inputs(prompts, visual)
     torch.cuda.synchronize()
     print(f"[bench] setup {time.time() - t_setup:.1f}s", file=sys.stderr, flush=True)
 
     B, T, g = wl.batch, wl.new_tokens, wl.gamma
 
-    def timed(speculative: bool, steps: int, warmup: int):
+    def timed(speculative: bool, steps: int, warmup: int, dynamic: bool = False):
         for _ in range(warmup):
-            dd.generate(pt, vt, T, g, speculative=speculative, reuse=True)
+            dd.generate(pt, vt, T, g, speculative=speculative, reuse=True, dynamic=dynamic)
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         stats = None
         for _ in range(steps):
-            toks, stats = dd.generate(pt, vt, T, g, speculative=speculative, reuse=True)
+            toks, stats = dd.generate(pt, vt, T, g, speculative=speculative, reuse=True,
+                                      dynamic=dynamic)
         torch.cuda.synchronize()
         return time.perf_counter() - t0, stats, toks
 
@@ -258,6 +260,15 @@ def main():
     greedy_tps = B * T * args.steps / dtg
     same = bool(torch.equal(toks_ssd, toks_greedy))
     print(f"[bench] greedy {greedy_tps:.1f} tok/s", file=sys.stderr, flush=True)
+    # the context-length draft schedule d(t) (d(0) = gamma), same decoder and inputs
+    dtd, std, toks_dyn = timed(True, args.steps, 1, dynamic=True)
+    dyn = {"tokens_per_s": round(B * T * args.steps / dtd, 2),
+           "speedup_vs_greedy": round(dtg / dtd, 3),
+           "acceptance_rate": round(std["accepted"] / max(1, std["drafted"]), 4),
+           "rounds": std["rounds"], "drafted": std["drafted"],
+           "equals_greedy_tokens": bool(torch.equal(toks_dyn, toks_greedy)),
+           "schedule": f"d(t) = {g} + floor(10 sigmoid(0.01 (t - {dd.cap.max_seq}/2)))"}
+    print(f"[bench] dynamic d(t) {dyn['tokens_per_s']:.1f} tok/s", file=sys.stderr, flush=True)
 
     # draft-step time: events around the gamma-step draft call (captured graph) on its stream
     step_s, verify_s, ctx = step_timings(dd, pt, vt, B, g)
@@ -325,6 +336,7 @@ def main():
         "greedy_tokens_per_s": round(greedy_tps, 2),
         "speedup_vs_greedy": round(ssd_tps / greedy_tps, 3),
         "ssd_equals_greedy_tokens": same,
+        "dynamic_gamma": dyn,
         "draft_step": draft,
         "verify": verify,
         "roofline": roofline,

@@ -53,7 +53,7 @@ enum {
 
 enum { SSD_ARCH_T5 = 0, SSD_ARCH_LLAMA = 1 };
 enum { SSD_F32 = 0, SSD_BF16 = 1 };
-enum { SSD_MODE_GREEDY = 0, SSD_MODE_SPECULATIVE = 1 };
+enum { SSD_MODE_GREEDY = 0, SSD_MODE_SPECULATIVE = 1, SSD_MODE_SPECULATIVE_DYNAMIC = 2 };
 
 /* device status bits (ssd_sync_status, ssd_device_status) */
 enum { SSD_DEV_BAD_TOKEN = 1, SSD_DEV_CAPACITY = 2, SSD_DEV_BAD_PAGE = 4 };
@@ -182,11 +182,19 @@ int ssd_accept(ssd_ctx* ctx, int B, int gamma, const int32_t* d_draft, const int
 /* The whole loop: prefill, then rounds of draft + verify + accept (SSD_MODE_SPECULATIVE) or
  * verify(gamma = 0) + accept (SSD_MODE_GREEDY) until T tokens per sequence are emitted (the last
  * round truncated; a finished sequence's seq_len then counts only the positions it emitted, so
- * max_seq = prefix + prompt + T + max_gamma + 1 suffices for any batch).  d_tokens [B][T] int32.  h_stats (host, may be NULL) receives
- * {rounds, sum over sequences of accepted drafts, sum of drafted tokens}.  Synchronises the
- * stream once per round to test for completion. */
+ * max_seq = prefix + prompt + T + max_gamma + 1 suffices for any batch).  d_tokens [B][T] int32.
+ * SSD_MODE_SPECULATIVE_DYNAMIC drafts ssd_dynamic_gamma(t, gamma, max_seq) tokens per round
+ * (appendix on the choice of d: d grows with the context length t), t = the shortest context
+ * length among the sequences still active at the start of the round; gamma + 9 <= max_gamma.
+ * h_stats (host, may be NULL) receives {rounds, sum over sequences of accepted drafts, sum of
+ * drafted tokens}.  Synchronises the stream once per round to test for completion. */
 int ssd_generate(ssd_ctx* ctx, int B, int P, const int32_t* d_prompt, const void* d_visual, int T,
                  int gamma, int mode, int reuse_hidden, int32_t* d_tokens, int64_t* h_stats);
+
+/* Draft length at context length t (appendix on the choice of d): d0 + floor(10 * sigmoid(0.01 *
+ * (t - n_max / 2))); n_max is the maximum sequence length.  In [d0, d0 + 9] for 0 <= t <= n_max
+ * (d0 + 10 only where the double-precision logistic rounds to 1).  Host function. */
+int ssd_dynamic_gamma(int t, int d0, int n_max);
 
 /* Capture ssd_draft / ssd_verify launch sequences into HIP graphs and replay them (1, default)
  * or launch kernels one by one (0). */

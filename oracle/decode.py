@@ -19,6 +19,7 @@ two produce bit-identical tokens and logits (the self-check in tests/test_oracle
 """
 from __future__ import annotations
 
+import math
 from dataclasses import dataclass, field
 from typing import Callable, List, Optional, Sequence
 
@@ -30,6 +31,14 @@ from .model import Decoder, State
 def argmax(logits: np.ndarray) -> int:
     """Greedy choice; equal maxima resolve to the lowest index."""
     return int(np.argmax(logits))
+
+
+def dynamic_draft_length(t: int, d0: int, n_max: int) -> int:
+    """Draft length at context length t (appendix on the choice of d): d(0) plus the floor of ten
+    times the logistic function of 0.01 (t - N/2), N the maximum sequence length."""
+    x = -0.01 * (t - n_max / 2.0)
+    e = math.exp(x) if x < 700.0 else math.inf  # IEEE: 1 / (1 + inf) = 0 far below N/2
+    return d0 + math.floor(10.0 / (1.0 + e))
 
 
 def accept_length(drafts: Sequence[int], targets: Sequence[int]) -> int:
@@ -108,13 +117,16 @@ def _poison(st: State) -> None:
 def ssd(dec: Decoder, prompt, visual, T: int, gamma: int, capacity: Optional[int] = None,
         draft_policy: Optional[Callable[[int, int, np.ndarray], int]] = None,
         poison: bool = False, use_imitation: bool = True, eos_id: int = -1,
-        max_rounds: Optional[int] = None) -> Run:
+        max_rounds: Optional[int] = None,
+        gamma_fn: Optional[Callable[[int], int]] = None) -> Run:
     """Algorithm 1: draft gamma tokens with layers 1..k + I + g, verify them with the full decoder,
     keep the longest matching prefix plus the full model's token at the first mismatch.
 
     ``draft_policy(round, i, logits) -> token`` replaces the draft's argmax (host-forced drafts);
     ``poison`` overwrites every KV entry beyond the valid length with NaN after each acceptance;
-    ``max_rounds`` stops early (a bounded sample of the loop, for timing).
+    ``max_rounds`` stops early (a bounded sample of the loop, for timing);
+    ``gamma_fn(l) -> d`` drafts d tokens in a round that starts at context length l (the dynamic
+    draft length; ``gamma`` then only sizes the cache).
     """
     if gamma < 0:
         raise ValueError("gamma must be >= 0")
@@ -126,18 +138,19 @@ def ssd(dec: Decoder, prompt, visual, T: int, gamma: int, capacity: Optional[int
         if max_rounds is not None and len(run.rounds) >= max_rounds:
             break
         l = st.seq_len
+        g = gamma if gamma_fn is None else int(gamma_fn(l))
         # drafting stage: u_0 = pending, u_{i+1} = draft's argmax at position l+i
         u = [y]
         drafts, dlog = [], []
-        for i in range(gamma):
+        for i in range(g):
             lg, _ = dec.draft_step(st, u[i], l + i, use_imitation)
             t = argmax(lg) if draft_policy is None else int(draft_policy(len(run.rounds), i, lg))
             drafts.append(t)
             dlog.append(lg)
             u.append(t)
-        # verification stage: the full decoder over u_0..u_gamma at positions l..l+gamma
+        # verification stage: the full decoder over u_0..u_g at positions l..l+g
         targets, tlog = [], []
-        for i in range(gamma + 1):
+        for i in range(g + 1):
             lg, _ = dec.full_step(st, u[i], l + i)
             targets.append(argmax(lg))
             tlog.append(lg)

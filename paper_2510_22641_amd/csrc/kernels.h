@@ -226,7 +226,7 @@ struct AcceptArgs {
   int32_t* active_rw;     // [B] cleared when count reaches T
   int T;
   int64_t* stats;         // [3]: rounds (added by thread 0), accepted, drafted
-  int32_t* n_active;      // [1]
+  int32_t* n_active;      // [2]: sequences still active, shortest seq_len among them
 };
 hipError_t launch_accept(const AcceptArgs& a, hipStream_t s);
 
@@ -237,7 +237,8 @@ struct GenInitArgs {
   int32_t* count;
   int32_t* active;
   int64_t* stats;
-  int32_t* n_active;
+  int32_t* n_active;        // [2]: sequences active, shortest seq_len among them
+  const int32_t* seq_len;
 };
 hipError_t launch_gen_init(const GenInitArgs& a, hipStream_t s);
 

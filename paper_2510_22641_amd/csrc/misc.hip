@@ -136,6 +136,7 @@ __global__ void set_seq_len_kernel(int32_t* seq_len, int B, int value) {
 __global__ void accept_kernel(const AcceptArgs a) {
   __shared__ int acc_n[256];
   __shared__ int act_after[256];
+  __shared__ int len_after[256];
   const int b = threadIdx.x;
   const int g = a.gamma;
   int n = 0;
@@ -180,18 +181,23 @@ __global__ void accept_kernel(const AcceptArgs a) {
   }
   acc_n[b] = did ? n : -1;
   act_after[b] = still;
+  len_after[b] = (b < a.B && still) ? a.seq_len[b] : INT_MAX;
   __syncthreads();
   if (b == 0 && a.stats) {
     long long sa = 0, sd = 0;
-    int na = 0;
+    int na = 0, lmin = INT_MAX;
     for (int t = 0; t < a.B && t < 256; ++t) {
       if (acc_n[t] >= 0) { sa += acc_n[t]; sd += g; }
       na += act_after[t];
+      lmin = min(lmin, len_after[t]);
     }
     a.stats[0] += 1;
     a.stats[1] += sa;
     a.stats[2] += sd;
-    if (a.n_active) a.n_active[0] = na;
+    if (a.n_active) {
+      a.n_active[0] = na;
+      a.n_active[1] = na ? lmin : 0;
+    }
   }
 }
 
@@ -207,9 +213,13 @@ __global__ void gen_init_kernel(const GenInitArgs a) {
   }
   __syncthreads();
   if (b == 0) {
-    int na = 0;
-    for (int t = 0; t < a.B && t < 256; ++t) na += act[t];
+    int na = 0, lmin = INT_MAX;
+    for (int t = 0; t < a.B && t < 256; ++t) {
+      na += act[t];
+      if (act[t]) lmin = min(lmin, a.seq_len[t]);
+    }
     a.n_active[0] = na;
+    a.n_active[1] = na ? lmin : 0;
     a.stats[0] = a.stats[1] = a.stats[2] = 0;
   }
 }

@@ -88,7 +88,7 @@ bool make_layout(const ssd_dims& d, Layout& L) {
   L.g_target = take(B * (G + 1) * 4);
   L.g_count = take(B * 4);
   L.g_active = take(B * 4);
-  L.g_nactive = take(4);
+  L.g_nactive = take(8);
   L.g_stats = take(3 * 8);
   L.total = off;
   return true;
@@ -643,12 +643,19 @@ int ssd_accept(ssd_ctx* c, int B, int gamma, const int32_t* d_draft, const int32
   return SSD_OK;
 }
 
+int ssd_dynamic_gamma(int t, int d0, int n_max) {
+  const double sig = 1.0 / (1.0 + std::exp(-0.01 * ((double)t - 0.5 * (double)n_max)));
+  return d0 + (int)std::floor(10.0 * sig);
+}
+
 int ssd_generate(ssd_ctx* c, int B, int P, const int32_t* d_prompt, const void* d_visual, int T,
                  int gamma, int mode, int reuse_hidden, int32_t* d_tokens, int64_t* h_stats) {
   if (!c || !d_tokens || T < 1) return SSD_ERR_ARG;
-  if (mode != SSD_MODE_GREEDY && mode != SSD_MODE_SPECULATIVE) return SSD_ERR_ARG;
-  const int g = mode == SSD_MODE_GREEDY ? 0 : gamma;
-  if (mode == SSD_MODE_SPECULATIVE && (gamma < 1 || gamma > c->d.max_gamma)) return SSD_ERR_SHAPE;
+  if (mode != SSD_MODE_GREEDY && mode != SSD_MODE_SPECULATIVE && mode != SSD_MODE_SPECULATIVE_DYNAMIC)
+    return SSD_ERR_ARG;
+  const bool dynamic = mode == SSD_MODE_SPECULATIVE_DYNAMIC;
+  const int g_max = mode == SSD_MODE_GREEDY ? 0 : (dynamic ? gamma + 9 : gamma);
+  if (mode != SSD_MODE_GREEDY && (gamma < 1 || g_max > c->d.max_gamma)) return SSD_ERR_SHAPE;
   if (B < 1 || B > c->d.max_batch) return SSD_ERR_SHAPE;
   const int Cx = P + (c->d.arch == SSD_ARCH_T5 ? 0 : c->d.n_visual);
   if (Cx + T + c->d.max_gamma > c->d.max_seq) return SSD_ERR_CAPACITY;
@@ -661,20 +668,24 @@ int ssd_generate(ssd_ctx* c, int B, int P, const int32_t* d_prompt, const void* 
   int64_t* stats = c->at<int64_t>(c->L.g_stats);
   int rc = ssd_prefill(c, B, P, d_prompt, d_visual, pending, nullptr);
   if (rc) return rc;
-  GenInitArgs gi{B, T, pending, d_tokens, count, active, stats, n_active};
+  GenInitArgs gi{B, T, pending, d_tokens, count, active, stats, n_active, c->kv.seq_len};
   HIP_TRY(launch_gen_init(gi, c->stream));
   AcceptArgs a;
   std::memset(&a, 0, sizeof(a));
-  a.B = B; a.gamma = g; a.draft = draft; a.target = target; a.pending = pending;
-  a.seq_len = c->kv.seq_len; a.max_seq = c->d.max_seq; a.next_need = g + 1;
+  a.B = B; a.draft = draft; a.target = target; a.pending = pending;
+  a.seq_len = c->kv.seq_len; a.max_seq = c->d.max_seq; a.next_need = g_max + 1;
   a.status = c->at<int32_t>(c->L.status);
   a.tokens = d_tokens; a.count = count; a.active_rw = active; a.T = T; a.stats = stats;
   a.n_active = n_active;
   for (int round = 0; round < T; ++round) {
-    int32_t h_active = 0;
-    HIP_TRY(hipMemcpyAsync(&h_active, n_active, 4, hipMemcpyDeviceToHost, c->stream));
+    int32_t h_active[2] = {0, 0};
+    HIP_TRY(hipMemcpyAsync(h_active, n_active, 8, hipMemcpyDeviceToHost, c->stream));
     HIP_TRY(hipStreamSynchronize(c->stream));
-    if (h_active == 0) break;
+    if (h_active[0] == 0) break;
+    const int g = mode == SSD_MODE_GREEDY ? 0
+                  : (dynamic ? ssd_dynamic_gamma(h_active[1], gamma, c->d.max_seq) : gamma);
+    if (g > c->d.max_gamma) return SSD_ERR_SHAPE;
+    a.gamma = g;
     if (g > 0) {
       rc = ssd_draft(c, B, g, pending, draft, nullptr);
       if (rc) return rc;

@@ -211,10 +211,12 @@ class DeviceDecoder:
         return out, alen
 
     def generate(self, prompt, visual, T: int, gamma: int, speculative: bool = True,
-                 reuse: bool = True):
+                 reuse: bool = True, dynamic: bool = False):
+        """ssd_generate; with dynamic=True gamma is d(0) of the context-length schedule."""
         B, P = prompt.shape
         tokens = self.ivec(B, T)
-        mode = abi.SSD_MODE_SPECULATIVE if speculative else abi.SSD_MODE_GREEDY
+        mode = abi.SSD_MODE_GREEDY if not speculative else (
+            abi.SSD_MODE_SPECULATIVE_DYNAMIC if dynamic else abi.SSD_MODE_SPECULATIVE)
         stats = self._call(abi.ssd_generate, self.ctx, B, P, prompt, visual, T, gamma, mode, reuse, tokens)
         return tokens, stats
 

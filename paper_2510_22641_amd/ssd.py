@@ -17,7 +17,7 @@ SSD_OK, SSD_ERR_ARG, SSD_ERR_SHAPE, SSD_ERR_CAPACITY, SSD_ERR_HIP, SSD_ERR_STATE
     0, -1, -2, -3, -4, -5, -6
 SSD_ARCH_T5, SSD_ARCH_LLAMA = 0, 1
 SSD_F32, SSD_BF16 = 0, 1
-SSD_MODE_GREEDY, SSD_MODE_SPECULATIVE = 0, 1
+SSD_MODE_GREEDY, SSD_MODE_SPECULATIVE, SSD_MODE_SPECULATIVE_DYNAMIC = 0, 1, 2
 SSD_DEV_BAD_TOKEN, SSD_DEV_CAPACITY, SSD_DEV_BAD_PAGE = 1, 2, 4
 
 
@@ -73,6 +73,7 @@ def _load():
         "ssd_accept": (c_int, [P, c_int, c_int, P, P, P, P, P, P]),
         "ssd_generate": (c_int, [P, c_int, c_int, P, P, c_int, c_int, c_int, c_int, P,
                                  POINTER(c_int64)]),
+        "ssd_dynamic_gamma": (c_int, [c_int, c_int, c_int]),
         "ssd_set_graphs": (c_int, [P, c_int]),
         "ssd_profile_enable": (c_int, [P, c_int]),
         "ssd_profile_read": (c_int, [P, POINTER(c_int64), POINTER(ctypes.c_double),
@@ -90,7 +91,7 @@ def _load():
 
 _lib = _load()
 EXPORTS = ("ssd_workspace_bytes", "ssd_create", "ssd_prefill", "ssd_draft", "ssd_verify",
-           "ssd_accept", "ssd_generate", "ssd_set_graphs", "ssd_profile_enable",
+           "ssd_accept", "ssd_generate", "ssd_dynamic_gamma", "ssd_set_graphs", "ssd_profile_enable",
            "ssd_profile_read", "ssd_sync_status",
            "ssd_status_string", "ssd_destroy")
 
@@ -154,6 +155,10 @@ def ssd_generate(ctx, B, P, d_prompt, d_visual, T, gamma, mode, reuse_hidden, d_
     _check("ssd_generate", _lib.ssd_generate(ctx, B, P, _p(d_prompt), _p(d_visual), T, gamma,
                                              mode, int(reuse_hidden), _p(d_tokens), stats))
     return {"rounds": int(stats[0]), "accepted": int(stats[1]), "drafted": int(stats[2])}
+
+
+def ssd_dynamic_gamma(t: int, d0: int, n_max: int) -> int:
+    return int(_lib.ssd_dynamic_gamma(int(t), int(d0), int(n_max)))
 
 
 def ssd_set_graphs(ctx, enable: bool):

@@ -71,3 +71,16 @@ def test_workspace_and_dimension_checks():
     assert abi.status_string(abi.SSD_ERR_CAPACITY) == "capacity exceeded"
     with pytest.raises(abi.SSDError):
         abi.ssd_prefill(None, 1, 1, 0, 0, 0)
+
+
+def test_dynamic_draft_length_matches_the_oracle():
+    """The library's host-side schedule (ssd_dynamic_gamma) equals the oracle's d(t)."""
+    from oracle import decode
+    lib = ctypes.CDLL(_built())
+    f = lib.ssd_dynamic_gamma
+    f.restype = ctypes.c_int
+    f.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int]
+    for n_max in (142, 512, 870, 4096):
+        for d0 in (1, 5):
+            for t in range(0, 5000, 7):
+                assert f(t, d0, n_max) == decode.dynamic_draft_length(t, d0, n_max), (t, d0, n_max)

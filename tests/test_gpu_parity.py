@@ -228,3 +228,41 @@ def test_positions_past_the_cache_are_reported_not_written():
     changed = (dd.k_pool != k_before).reshape(dd.k_pool.shape[0], -1).any(dim=1).cpu().numpy()
     assert changed[: wl.draft_layers].all() and not changed[wl.draft_layers:].any()
     assert dd.sync_status() == (0, 0)
+
+
+@pytest.mark.parametrize("wl", [synth.S_T5, synth.S_LLAMA], ids=lambda w: w.name)
+def test_bf16_kv_cache_option(wl):
+    """The bf16 KV cache (kv_dtype="bf16", not the default) also stays within the tolerance at
+    these sizes: every logit of a speculative run against the oracle."""
+    from paper_2510_22641_amd import runtime
+    w, z, pr = parity.workload_inputs(wl, 5)
+    dd = runtime.from_workload(wl, 5, weights=w, kv_dtype="bf16", page_seed=2)
+    assert dd.k_pool.dtype.itemsize == 2
+    dec = Decoder(wl.shape, w, wl.draft_layers)
+    pt, vt = dd.upload_inputs(pr, z)
+    run = parity.device_run(dd, pt, vt, wl.new_tokens, wl.gamma, reuse=True)
+    parity.check_run_against_oracle(dec, wl.shape, pr[0], z[0], run, 0, wl.gamma)
+    assert dd.sync_status() == (0, 0)
+
+
+@pytest.mark.parametrize("wl", [synth.S1, synth.S_LLAMA_F32], ids=lambda w: w.name)
+def test_dynamic_draft_length_generate_matches_oracle(wl):
+    """ssd_generate with the context-length schedule (d(0) = 2, up to 11 drafts a round): the
+    tokens, round count, accepted and drafted totals equal the oracle's Algorithm 1 with the same
+    schedule (float32 workloads: no near-ties at these sizes)."""
+    from paper_2510_22641_amd import runtime
+    from oracle import decode as odec
+    d0 = 2
+    w, z, pr = parity.workload_inputs(wl, 3)
+    dd = runtime.from_workload(wl, 3, weights=w, max_gamma=d0 + 9)
+    dec = Decoder(wl.shape, w, wl.draft_layers)
+    pt, vt = dd.upload_inputs(pr, z)
+    toks, stats = dd.generate(pt, vt, wl.new_tokens, d0, speculative=True, reuse=True, dynamic=True)
+    n_max = dd.cap.max_seq
+    ref = odec.ssd(dec, pr[0], z[0], wl.new_tokens, d0 + 9,
+                   gamma_fn=lambda l: odec.dynamic_draft_length(l, d0, n_max))
+    assert toks.cpu().numpy()[0].tolist() == ref.tokens
+    assert stats["rounds"] == len(ref.rounds)
+    assert stats["accepted"] == sum(r.accepted for r in ref.rounds)
+    assert stats["drafted"] == sum(len(r.drafts) for r in ref.rounds)
+    assert dd.sync_status() == (0, 0)

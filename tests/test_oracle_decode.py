@@ -145,3 +145,36 @@ def test_replay_of_own_stream_reproduces_logits(wl):
         assert a.accepted == b.accepted
         assert all(np.array_equal(x, y) for x, y in zip(a.draft_logits, b.draft_logits))
         assert all(np.array_equal(x, y) for x, y in zip(a.target_logits, b.target_logits))
+
+
+def test_dynamic_draft_length_closed_forms():
+    """d(t) = d0 + floor(10 * sigmoid(0.01 (t - N/2))): d0 + 5 at the midpoint, d0 far below it,
+    at most d0 + 9 for every t <= N (the logistic stays below 1 there), d0 + 10 only where the
+    double-precision logistic rounds to exactly 1 (t - N/2 > ~3700), non-decreasing, hand values."""
+    f = decode.dynamic_draft_length
+    assert f(71, 5, 142) == 10
+    assert f(-100000, 5, 142) == 5 and f(100000, 5, 142) == 15
+    for n_max in (142, 512, 4096):
+        assert max(f(t, 5, n_max) for t in range(0, n_max + 1)) <= 14
+    # t = 0, N = 142: 10 / (1 + e^0.71) = 3.296...
+    assert f(0, 5, 142) == 8 and f(0, 1, 142) == 4
+    vals = [f(t, 5, 512) for t in range(0, 4000)]
+    assert all(b >= a for a, b in zip(vals, vals[1:])) and set(vals) == set(range(5, 16))
+    # the logistic crosses 0.9 at x = ln 9: one step below and above the boundary
+    x9 = 100.0 * np.log(9.0) + 256.0
+    assert f(int(np.floor(x9)), 0, 512) == 8 and f(int(np.ceil(x9)), 0, 512) == 9
+
+
+@pytest.mark.parametrize("wl", [synth.S1, synth.S_LLAMA], ids=lambda w: w.name)
+def test_dynamic_draft_length_ssd_equals_greedy(wl):
+    """With the context-length schedule each round drafts d(l) tokens, and the output is still
+    the full model's greedy output bit for bit."""
+    dec, pr, z = _setup(wl, seed=3)
+    n_max = wl.max_seq() + 9
+    fn = lambda l: decode.dynamic_draft_length(l, 2, n_max)  # noqa: E731
+    run = decode.ssd(dec, pr, z, wl.new_tokens, 11, gamma_fn=fn)
+    g = decode.greedy(dec, pr, z, wl.new_tokens)
+    assert run.tokens == g.tokens
+    for r in run.rounds:
+        assert len(r.drafts) == fn(r.seq_len)
+        assert 0 <= r.accepted <= len(r.drafts)
