@@ -38,7 +38,7 @@ __device__ __forceinline__ const KT* key_row(const AttnArgs& a, const KT* base, 
 }
 
 template <typename KT, int DH, int QB>
-__global__ __launch_bounds__(256) void attn_kernel(const AttnArgs a, const int s_stride) {
+__global__ __launch_bounds__(256) void attn_kernel(const AttnArgs a, const int s_stride, const int ks) {
   constexpr int CH = DH / 8;       // 16-byte chunks per key row (bf16) / 8-element groups
   constexpr int KPI = 256 / CH;    // keys per block step in P.V
   constexpr int KPW = 64 / CH;     // keys per wave step in P.V
@@ -47,13 +47,20 @@ __global__ __launch_bounds__(256) void attn_kernel(const AttnArgs a, const int s
   __shared__ float qs[QB][DH];
   __shared__ float red[4][QB][DH];
   __shared__ float inv_sum[QB];
+  __shared__ float row_max[QB], row_sum[QB];
 
-  const int h = blockIdx.x, b = blockIdx.y, j0 = blockIdx.z * QB;
+  // blockIdx.z = query group * ks + key split: this block's keys are [k0, k0 + nk) of the group's
+  // causal range (ks = 1: all of them)
+  const int h = blockIdx.x, b = blockIdx.y;
+  const int zq = blockIdx.z / ks, split = blockIdx.z - zq * ks, j0 = zq * QB;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int nq = min(QB, a.C - j0);
   const int HD = a.H * DH;
   const int base = a.cross ? 0 : a.kv.seq_len[b] + a.kv.pos_off;
-  int nk = a.cross ? a.n_keys : base + j0 + nq;
+  const int nk_all = a.cross ? a.n_keys : base + j0 + nq;
+  const int per = (nk_all + ks - 1) / ks;
+  const int k0 = min(nk_all, split * per);
+  int nk = min(nk_all, k0 + per) - k0;
   if (nk > s_stride) {
     if (tid == 0) atomicOr(a.status, SSD_DEV_CAPACITY);
     nk = s_stride;
@@ -65,7 +72,7 @@ __global__ __launch_bounds__(256) void attn_kernel(const AttnArgs a, const int s
   bool kok = false;
   Vec8<KT> krow[CH];
   if (tid < nk) {
-    const KT* kp = key_row<KT, DH>(a, Kb, b, h, tid, kok);
+    const KT* kp = key_row<KT, DH>(a, Kb, b, h, k0 + tid, kok);
     if (kok) {
 #pragma unroll
       for (int c = 0; c < CH; ++c) krow[c].load(kp + 8 * c);
@@ -79,7 +86,7 @@ __global__ __launch_bounds__(256) void attn_kernel(const AttnArgs a, const int s
     const int i = vk0 + KPI * u;
     vok[u] = false;
     if (i < nk) {
-      const KT* vp = key_row<KT, DH>(a, Vb, b, h, i, vok[u]);
+      const KT* vp = key_row<KT, DH>(a, Vb, b, h, k0 + i, vok[u]);
       if (vok[u]) vpre[u].load(vp + 8 * vc);
     }
   }
@@ -90,11 +97,11 @@ __global__ __launch_bounds__(256) void attn_kernel(const AttnArgs a, const int s
   }
   __syncthreads();
 
-  // scores: one key per thread per step
+  // scores: one key per thread per step (i relative to k0)
   for (int i = tid; i < nk; i += 256) {
     bool ok = kok;
     if (i != tid) {
-      const KT* kp = key_row<KT, DH>(a, Kb, b, h, i, ok);
+      const KT* kp = key_row<KT, DH>(a, Kb, b, h, k0 + i, ok);
       if (ok) {
 #pragma unroll
         for (int c = 0; c < CH; ++c) krow[c].load(kp + 8 * c);
@@ -125,9 +132,9 @@ __global__ __launch_bounds__(256) void attn_kernel(const AttnArgs a, const int s
       if (!ok || jq >= nq) {
         sc = -INFINITY;
       } else if (!a.cross) {
-        const int p = base + j0 + jq;
-        if (i > p) sc = -INFINITY;
-        else if (a.bias && p - i < a.max_seq) sc += a.bias[(size_t)h * a.max_seq + (p - i)];
+        const int p = base + j0 + jq, ki = k0 + i;
+        if (ki > p) sc = -INFINITY;
+        else if (a.bias && p - ki < a.max_seq) sc += a.bias[(size_t)h * a.max_seq + (p - ki)];
       }
       S[jq * s_stride + i] = sc;
     }
@@ -147,7 +154,11 @@ __global__ __launch_bounds__(256) void attn_kernel(const AttnArgs a, const int s
       sum += e;
     }
     sum = wave_sum(sum);
-    if (lane == 0) inv_sum[jq] = sum > 0.f ? 1.0f / sum : 0.f;
+    if (lane == 0) {
+      inv_sum[jq] = sum > 0.f ? 1.0f / sum : 0.f;
+      row_max[jq] = m;
+      row_sum[jq] = sum;
+    }
   }
   __syncthreads();
 
@@ -164,7 +175,7 @@ __global__ __launch_bounds__(256) void attn_kernel(const AttnArgs a, const int s
         const int i = vk0 + KPI * (u0 + u);
         vok[u] = false;
         if (i < nk) {
-          const KT* vp = key_row<KT, DH>(a, Vb, b, h, i, vok[u]);
+          const KT* vp = key_row<KT, DH>(a, Vb, b, h, k0 + i, vok[u]);
           if (vok[u]) vpre[u].load(vp + 8 * vc);
         }
       }
@@ -206,6 +217,16 @@ __global__ __launch_bounds__(256) void attn_kernel(const AttnArgs a, const int s
   for (int idx = tid; idx < nq * DH; idx += 256) {
     const int jq = idx / DH, d = idx - jq * DH;
     const float v = (red[0][jq][d] + red[1][jq][d]) + (red[2][jq][d] + red[3][jq][d]);
+    if (ks > 1) {
+      // partial of this key split: unnormalised output, row max and sum (attn_combine_kernel)
+      float* pp = a.part + (((size_t)(b * a.C + j0 + jq) * a.H + h) * ks + split) * (DH + 2);
+      pp[d] = v;
+      if (d == 0) {
+        pp[DH] = row_max[jq];
+        pp[DH + 1] = row_sum[jq];
+      }
+      continue;
+    }
     const size_t o = (size_t)(b * a.C + j0 + jq) * HD + h * DH + d;
     a.out[o] = v * inv_sum[jq];
     if (a.out_planes) {  // hi / lo bf16 planes for the skinny MFMA consumer (rows < plane_rows)
@@ -217,20 +238,63 @@ __global__ __launch_bounds__(256) void attn_kernel(const AttnArgs a, const int s
   }
 }
 
+// Merge the key splits of one (head, row): out = sum_s e^(m_s - m) o_s / sum_s e^(m_s - m) l_s.
+template <int DH>
+__global__ __launch_bounds__(DH) void attn_combine_kernel(const AttnArgs a, const int ks) {
+  const int h = blockIdx.x, r = blockIdx.y, d = threadIdx.x;
+  const int HD = a.H * DH;
+  const float* pp = a.part + ((size_t)r * a.H + h) * ks * (DH + 2);
+  float m = -INFINITY;
+  for (int sp = 0; sp < ks; ++sp) m = fmaxf(m, pp[sp * (DH + 2) + DH]);
+  float l = 0.f, o = 0.f;
+  for (int sp = 0; sp < ks; ++sp) {
+    const float ms = pp[sp * (DH + 2) + DH];
+    const float w = ms == -INFINITY ? 0.f : expf(ms - m);
+    l = fmaf(w, pp[sp * (DH + 2) + DH + 1], l);
+    o = fmaf(w, pp[sp * (DH + 2) + d], o);
+  }
+  const float y = l > 0.f ? o / l : 0.f;
+  const size_t oi = (size_t)r * HD + h * DH + d;
+  a.out[oi] = y;
+  if (a.out_planes) {
+    const uint32_t hi = f32_to_bf16(y);
+    a.out_planes[oi] = (bf16_t)hi;
+    a.out_planes[oi + (size_t)a.plane_rows * HD] = (bf16_t)f32_to_bf16(y - bf16_to_f32(hi));
+  }
+}
+
+// Key splits for a launch of up to 16 query rows: long self-attention contexts (capacity of 256
+// keys and more) are split so that about 512 blocks share the keys, at least 128 keys a split.
+int attn_splits(const AttnArgs& a) {
+  if (a.cross || a.C > 16 || !a.part || a.B * a.C > a.part_rows || a.max_seq < 256) return 1;
+  const int want = (512 + a.H * a.B * a.C - 1) / (a.H * a.B * a.C);
+  const int by_len = (a.max_seq + 127) / 128;
+  int ks = want < by_len ? want : by_len;
+  if (ks > ATTN_SPLITS_MAX) ks = ATTN_SPLITS_MAX;
+  return ks < 1 ? 1 : ks;
+}
+
 template <typename KT, int DH>
 hipError_t launch_attn_dh(const AttnArgs& a, hipStream_t s) {
   const int nk_max = a.cross ? a.n_keys : a.max_seq;
-  const int s_stride = (nk_max + 63) & ~63;
   if (a.C <= 16) {
-    // decode steps and verify chunks: one block per (head, sequence, query row); the rows of a
-    // chunk re-read the same keys from L2, and 16x more blocks keep the chip busy
-    dim3 grid(a.H, a.B, a.C);
+    // decode steps and verify chunks: one block per (head, sequence, query row[, key split]); the
+    // rows of a chunk re-read the same keys from L2, and more blocks keep the chip busy
+    const int ks = attn_splits(a);
+    const int s_stride = (((nk_max + ks - 1) / ks) + 63) & ~63;
+    dim3 grid(a.H, a.B, a.C * ks);
     const size_t shm = (size_t)s_stride * sizeof(float);
-    hipLaunchKernelGGL((attn_kernel<KT, DH, 1>), grid, dim3(256), shm, s, a, s_stride);
+    hipLaunchKernelGGL((attn_kernel<KT, DH, 1>), grid, dim3(256), shm, s, a, s_stride, ks);
+    if (ks > 1) {
+      hipError_t e = hipGetLastError();
+      if (e != hipSuccess) return e;
+      hipLaunchKernelGGL((attn_combine_kernel<DH>), dim3(a.H, a.B * a.C), dim3(DH), 0, s, a, ks);
+    }
   } else {
+    const int s_stride = (nk_max + 63) & ~63;
     dim3 grid(a.H, a.B, (a.C + QB - 1) / QB);
     const size_t shm = (size_t)QB * s_stride * sizeof(float);
-    hipLaunchKernelGGL((attn_kernel<KT, DH, QB>), grid, dim3(256), shm, s, a, s_stride);
+    hipLaunchKernelGGL((attn_kernel<KT, DH, QB>), grid, dim3(256), shm, s, a, s_stride, 1);
   }
   return hipGetLastError();
 }

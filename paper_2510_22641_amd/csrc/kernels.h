@@ -169,11 +169,16 @@ struct RopeScatterArgs {
 };
 hipError_t launch_rope_scatter(const RopeScatterArgs& a, hipStream_t s);
 
+constexpr int ATTN_SPLITS_MAX = 8;
+
 struct AttnArgs {
   const float* q;  // [B*C][H*dh]
   float* out;      // [B*C][H*dh]
   bf16_t* out_planes = nullptr;  // optional hi / lo bf16 planes of out (lo plane_rows rows on)
   int plane_rows = 16;
+  // key-split partials (long contexts): [part_rows][H][ATTN_SPLITS_MAX][dh + 2] floats, or null
+  float* part = nullptr;
+  int part_rows = 0;
   int B, C, H, dh;
   int kvdtype;
   int cross;         // 0: causal over the paged cache; 1: dense over n_keys cross-attention keys

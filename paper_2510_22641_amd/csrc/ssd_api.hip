@@ -31,10 +31,10 @@ int t5_bucket(int n, int buckets, int max_dist) {
 
 struct Layout {
   size_t x, x1, qkv, q, attn, ffn, inh, xi, stash, vis, part_val, part_idx, stats, bias_tab,
-      p_x, p_attn, p_ffn, ssq,
+      p_x, p_attn, p_ffn, ssq, attn_part,
       bucket, rope_cos, rope_sin, status, cur_tok, g_pending, g_draft, g_target,
       g_count, g_active, g_nactive, g_stats, total;
-  int rows_max, head_rows, parts_max, ctx_max, plane_rows;
+  int rows_max, head_rows, parts_max, ctx_max, plane_rows, attn_rows;
 };
 
 int ctx_len_max(const ssd_dims& d) {
@@ -77,6 +77,9 @@ bool make_layout(const ssd_dims& d, Layout& L) {
   L.p_attn = take(2 * PRz * HD * 2);
   L.p_ffn = take(2 * PRz * (size_t)d.d_ff * 2);
   L.ssq = take((size_t)skinny_blocks((int)D) * PRz * 4);
+  // key-split partials of the long-context attention (up to 16 query rows per sequence)
+  L.attn_rows = (int)(B * 16);
+  L.attn_part = take((size_t)L.attn_rows * d.n_heads * ATTN_SPLITS_MAX * (d.d_head + 2) * 4);
   L.bias_tab = take(d.arch == SSD_ARCH_T5 ? (size_t)d.n_heads * d.max_seq * 4 : 0);
   L.bucket = take(d.arch == SSD_ARCH_T5 ? (size_t)d.max_seq * 4 : 0);
   L.rope_cos = take(d.arch == SSD_ARCH_LLAMA ? (size_t)d.max_seq * (d.d_head / 2) * 4 : 0);
@@ -279,6 +282,7 @@ int run_layers(ssd_ctx* c, float* x, int B, int C, int pos_off, int l0, int l1, 
     }
     AttnArgs at;
     at.q = q; at.out = attn; at.out_planes = skinny ? p_attn : nullptr; at.plane_rows = PR;
+    at.part = c->at<float>(c->L.attn_part); at.part_rows = c->L.attn_rows;
     at.B = B; at.C = C; at.H = d.n_heads; at.dh = d.d_head;
     at.kvdtype = d.kvdtype; at.cross = 0; at.kv = paged(c, l, pos_off);
     at.bias = t5 ? c->at<float>(c->L.bias_tab) : nullptr;

@@ -266,3 +266,14 @@ def test_dynamic_draft_length_generate_matches_oracle(wl):
     assert stats["accepted"] == sum(r.accepted for r in ref.rounds)
     assert stats["drafted"] == sum(len(r.drafts) for r in ref.rounds)
     assert dd.sync_status() == (0, 0)
+
+
+@pytest.mark.parametrize("wl", [synth.S_T5, synth.S_LLAMA], ids=lambda w: w.name)
+def test_long_capacity_splits_attention_keys(wl):
+    """A cache of 256 positions or more splits each head's keys over several blocks whose partial
+    (max, sum, output) are merged by a second kernel: the whole run still matches the oracle."""
+    dd, dec, pr, z, pt, vt = _setup(wl, seed=12, page_seed=5, extra_seq=250)
+    assert dd.cap.max_seq >= 256
+    run = parity.device_run(dd, pt, vt, wl.new_tokens, wl.gamma, reuse=True)
+    parity.check_run_against_oracle(dec, wl.shape, pr[0], z[0], run, 0, wl.gamma)
+    assert dd.sync_status() == (0, 0)
