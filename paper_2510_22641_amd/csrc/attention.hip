@@ -6,8 +6,9 @@
 // for LLaMA, scaled by 1/sqrt(dh) with q and k already rotated.  Cross-attention (T5): all n_keys
 // visual keys, no mask, no bias, no scale.
 //
-// One block per (head, sequence, query row) for chunks of up to 16 rows, else per (head,
-// sequence, 8 query rows).  Every thread issues its key row and its
+// One block per (head, sequence, query row) for single rows and short-context chunks of up to 16
+// rows, else per (head, sequence, 8 query rows); long contexts split each head's keys over several
+// blocks whose partials attn_combine_kernel merges.  Every thread issues its key row and its
 // first value chunks before the first barrier (they do not depend on the scores); scores for the
 // live rows go to LDS, one wave per row turns them into softmax numerators, and P.V splits the
 // keys over all threads (16-byte value chunks, 8 loads in flight per thread) with a shuffle + LDS
@@ -263,11 +264,13 @@ __global__ __launch_bounds__(DH) void attn_combine_kernel(const AttnArgs a, cons
   }
 }
 
-// Key splits for a launch of up to 16 query rows: long self-attention contexts (capacity of 256
-// keys and more) are split so that about 512 blocks share the keys, at least 128 keys a split.
-int attn_splits(const AttnArgs& a) {
+// Key splits of a launch with `groups` query blocks per sequence: long self-attention contexts
+// (capacity of 256 keys and more, up to 16 query rows) are split so that about 512 blocks share
+// the keys, at least 128 keys a split.
+int attn_splits(const AttnArgs& a, int groups) {
   if (a.cross || a.C > 16 || !a.part || a.B * a.C > a.part_rows || a.max_seq < 256) return 1;
-  const int want = (512 + a.H * a.B * a.C - 1) / (a.H * a.B * a.C);
+  const int blocks = a.H * a.B * groups;
+  const int want = (512 + blocks - 1) / blocks;
   const int by_len = (a.max_seq + 127) / 128;
   int ks = want < by_len ? want : by_len;
   if (ks > ATTN_SPLITS_MAX) ks = ATTN_SPLITS_MAX;
@@ -277,24 +280,31 @@ int attn_splits(const AttnArgs& a) {
 template <typename KT, int DH>
 hipError_t launch_attn_dh(const AttnArgs& a, hipStream_t s) {
   const int nk_max = a.cross ? a.n_keys : a.max_seq;
-  if (a.C <= 16) {
-    // decode steps and verify chunks: one block per (head, sequence, query row[, key split]); the
-    // rows of a chunk re-read the same keys from L2, and more blocks keep the chip busy
-    const int ks = attn_splits(a);
+  const bool long_ctx = !a.cross && a.max_seq >= 256;
+  int ks = 1;
+  if (a.C == 1 || (a.C <= 16 && !long_ctx)) {
+    // decode steps and short-context verify chunks: one block per (head, sequence, query row
+    // [, key split]); the rows of a chunk re-read the same few keys from L2, and more blocks keep
+    // the chip busy
+    ks = attn_splits(a, a.C);
     const int s_stride = (((nk_max + ks - 1) / ks) + 63) & ~63;
     dim3 grid(a.H, a.B, a.C * ks);
     const size_t shm = (size_t)s_stride * sizeof(float);
     hipLaunchKernelGGL((attn_kernel<KT, DH, 1>), grid, dim3(256), shm, s, a, s_stride, ks);
-    if (ks > 1) {
-      hipError_t e = hipGetLastError();
-      if (e != hipSuccess) return e;
-      hipLaunchKernelGGL((attn_combine_kernel<DH>), dim3(a.H, a.B * a.C), dim3(DH), 0, s, a, ks);
-    }
   } else {
-    const int s_stride = (nk_max + 63) & ~63;
-    dim3 grid(a.H, a.B, (a.C + QB - 1) / QB);
+    // prefill blocks and long-context verify chunks: up to QB rows of a sequence share each key
+    // load (and long contexts split their keys)
+    const int groups = (a.C + QB - 1) / QB;
+    ks = attn_splits(a, groups);
+    const int s_stride = (((nk_max + ks - 1) / ks) + 63) & ~63;
+    dim3 grid(a.H, a.B, groups * ks);
     const size_t shm = (size_t)QB * s_stride * sizeof(float);
-    hipLaunchKernelGGL((attn_kernel<KT, DH, QB>), grid, dim3(256), shm, s, a, s_stride, 1);
+    hipLaunchKernelGGL((attn_kernel<KT, DH, QB>), grid, dim3(256), shm, s, a, s_stride, ks);
+  }
+  if (ks > 1) {
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((attn_combine_kernel<DH>), dim3(a.H, a.B * a.C), dim3(DH), 0, s, a, ks);
   }
   return hipGetLastError();
 }
