@@ -829,6 +829,168 @@ __global__ __launch_bounds__(256) void skinny_prep_kernel(const float* __restric
 // MFMAs against the same weight fragment, so the products see near-fp32 inputs.
 constexpr int TM = 64, TN = 64, TK = 64, TKP = TK + 8;
 
+// Larger MFMA tiles for long row blocks (prefill): 128 rows x BN features per block, K in steps
+// of 32, double-buffered in LDS.  The next step's inputs (RMS-normalised when RMS, then split into
+// bf16 hi / lo planes) and weights are fetched into registers while the current step computes, so
+// there is one barrier per step.  4 waves in a 2 x 2 grid, each 64 rows x BN/2 features of 16x16
+// MFMA tiles.  Row statistics come from launch_row_stats.
+constexpr int G2M = 128, G2K = 32, G2KP = G2K + 8;
+
+template <bool GATED, int BN, bool RMS>
+__global__ __launch_bounds__(256) void gemm2_kernel(const LinearArgs a) {
+  constexpr int NB = GATED ? 2 : 1;
+  constexpr int TJ = BN / 32;                // 16-wide feature tiles per wave
+  constexpr int BTPR = 256 / BN;             // threads per weight row in staging
+  constexpr int BKPT = G2K / BTPR;           // weight elements per thread and row
+  constexpr int BQ = BKPT / 8;               // 16-byte pieces of them
+  extern __shared__ __attribute__((aligned(16))) bf16_t g2s[];
+  bf16_t* Ah = g2s;                                   // [2][G2M][G2KP]
+  bf16_t* Al = Ah + 2 * G2M * G2KP;                   // [2][G2M][G2KP]
+  bf16_t* Bs = Al + 2 * G2M * G2KP;                   // [2][NB][BN][G2KP]
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  // row tiles vary fastest: the blocks that share a weight tile run back to back and re-read it
+  // from L2 / the Infinity Cache
+  const int m0 = blockIdx.x * G2M, n0 = blockIdx.y * BN;
+  const int K = a.K, M = a.M;
+  const int n_out = GATED ? a.n_per : a.n_per * a.n_mats;
+  const int mat = GATED ? 0 : n0 / a.n_per;  // tiles never straddle matrices (n_per % BN == 0)
+  const int nbase = GATED ? n0 : n0 - mat * a.n_per;
+  const bf16_t* w0 = reinterpret_cast<const bf16_t*>(GATED ? a.w[0] : (mat == 0 ? a.w[0] : (mat == 1 ? a.w[1] : a.w[2])));
+  const bf16_t* w1 = reinterpret_cast<const bf16_t*>(a.w[1]);
+
+  // staging roles: input row ar, 16 elements from ak; weight row br, BKPT elements from bk
+  const int ar = tid >> 1, ak = (tid & 1) * 16;
+  const int am = min(m0 + ar, M - 1);
+  const bool arow = m0 + ar < M;
+  const float rstd = RMS ? a.stats[am].y : 1.f;
+  const int br = tid / BTPR, bk = (tid % BTPR) * BKPT;
+  const int bn = min(nbase + br, a.n_per - 1);
+  const float* xrow = a.x + (size_t)am * a.ldx + ak;
+  const float* grow = a.gain + ak;
+  const bf16_t* wrow0 = w0 + (size_t)bn * K + bk;
+  const bf16_t* wrow1 = w1 + (size_t)bn * K + bk;
+
+  f32x4_t acc[NB][4][TJ];
+#pragma unroll
+  for (int b = 0; b < NB; ++b)
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < TJ; ++j) acc[b][i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  const int nk = K / G2K;
+  const int kk = (lane >> 4) * 8;
+  // kt = -1 only stages step 0
+  for (int kt = -1; kt < nk; ++kt) {
+    const bool next = kt + 1 < nk;
+    // the next step's operands (the last step re-reads its own: unconditional loads keep them in
+    // registers)
+    float4 xa[4], ga[4];
+    uint4 wa[BQ], wg[BQ];
+    {
+      const int k0 = min(kt + 1, nk - 1) * G2K;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) xa[q] = reinterpret_cast<const float4*>(xrow + k0)[q];
+#pragma unroll
+      for (int q = 0; q < BQ; ++q) wa[q] = reinterpret_cast<const uint4*>(wrow0 + k0)[q];
+#pragma unroll
+      for (int q = 0; q < BQ; ++q) wg[q] = GATED ? reinterpret_cast<const uint4*>(wrow1 + k0)[q] : wa[q];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) ga[q] = RMS ? reinterpret_cast<const float4*>(grow + k0)[q] : xa[q];
+    }
+    if (kt >= 0) {
+      const int buf = kt & 1;
+      bf16x8_t fh[4], fl[4], fb[NB][TJ];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const size_t r = ((size_t)buf * G2M + wm * 64 + 16 * i + (lane & 15)) * G2KP + kk;
+        fh[i] = *reinterpret_cast<const bf16x8_t*>(Ah + r);
+        fl[i] = *reinterpret_cast<const bf16x8_t*>(Al + r);
+      }
+#pragma unroll
+      for (int b = 0; b < NB; ++b)
+#pragma unroll
+        for (int j = 0; j < TJ; ++j)
+          fb[b][j] = *reinterpret_cast<const bf16x8_t*>(
+              Bs + (((size_t)buf * NB + b) * BN + wn * (BN / 2) + 16 * j + (lane & 15)) * G2KP + kk);
+#pragma unroll
+      for (int b = 0; b < NB; ++b)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int j = 0; j < TJ; ++j) {
+            acc[b][i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fh[i], fb[b][j], acc[b][i][j], 0, 0, 0);
+            acc[b][i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fl[i], fb[b][j], acc[b][i][j], 0, 0, 0);
+          }
+    }
+    if (next) {
+      const int buf = (kt + 1) & 1;
+      float f[16];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        float4 v = xa[q];
+        if (RMS) {
+          v.x *= rstd * ga[q].x; v.y *= rstd * ga[q].y; v.z *= rstd * ga[q].z; v.w *= rstd * ga[q].w;
+        }
+        f[4 * q] = arow ? v.x : 0.f;
+        f[4 * q + 1] = arow ? v.y : 0.f;
+        f[4 * q + 2] = arow ? v.z : 0.f;
+        f[4 * q + 3] = arow ? v.w : 0.f;
+      }
+      uint4 h0, l0, h1, l1;
+      split_bf16x8(f, h0, l0);
+      split_bf16x8(f + 8, h1, l1);
+      uint4* ah = reinterpret_cast<uint4*>(Ah + ((size_t)buf * G2M + ar) * G2KP + ak);
+      uint4* al = reinterpret_cast<uint4*>(Al + ((size_t)buf * G2M + ar) * G2KP + ak);
+      ah[0] = h0;
+      ah[1] = h1;
+      al[0] = l0;
+      al[1] = l1;
+      uint4* bp = reinterpret_cast<uint4*>(Bs + (((size_t)buf * NB) * BN + br) * G2KP + bk);
+#pragma unroll
+      for (int q = 0; q < BQ; ++q) bp[q] = wa[q];
+      if (GATED) {
+        uint4* bq = reinterpret_cast<uint4*>(Bs + (((size_t)buf * NB + 1) * BN + br) * G2KP + bk);
+#pragma unroll
+        for (int q = 0; q < BQ; ++q) bq[q] = wg[q];
+      }
+    }
+    __syncthreads();
+  }
+
+  // epilogue: lane holds D[4 * (lane / 16) + e][lane % 16] of each 16x16 tile
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < TJ; ++j)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int m = m0 + wm * 64 + 16 * i + 4 * (lane >> 4) + e;
+        const int n = n0 + wn * (BN / 2) + 16 * j + (lane & 15);
+        if (m >= M || n >= n_out) continue;
+        const float v = acc[0][i][j][e];
+        float* yp = a.y + (size_t)m * a.ldy + n;
+        if (GATED) {
+          *yp = apply_epi_act(a.epi, v, acc[NB - 1][i][j][e]);
+          continue;
+        }
+        switch (a.epi) {
+          case EPI_STORE: *yp = v; break;
+          case EPI_RESID: {
+            const float t = *yp + v;
+            *yp = t;
+            if (a.stash) a.stash[(size_t)m * a.lds + n] = t;
+            break;
+          }
+          case EPI_BIAS_GELU: *yp = gelu_tanh(v + a.bias[n]); break;
+          case EPI_BIAS_RESID: *yp = (a.resid ? a.resid[(size_t)m * a.ldr + n] : 0.f) + (v + a.bias[n]); break;
+          default: break;
+        }
+      }
+}
+
 template <bool GATED>
 __global__ __launch_bounds__(256) void gemm_kernel(const LinearArgs a) {
   constexpr int NB = GATED ? 2 : 1;
@@ -1204,6 +1366,24 @@ double linear_bytes(const LinearArgs& a) {
   return bytes;
 }
 
+template <bool GATED, int BN, bool RMS>
+void launch_gemm2_n(const LinearArgs& a, dim3 grid, hipStream_t s) {
+  constexpr int NB = GATED ? 2 : 1;
+  const size_t shm = ((size_t)4 * G2M * G2KP + (size_t)2 * NB * BN * G2KP) * sizeof(bf16_t);
+  static bool attr = false;
+  if (!attr) {
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm2_kernel<GATED, BN, RMS>),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)shm);
+    attr = true;
+  }
+  hipLaunchKernelGGL((gemm2_kernel<GATED, BN, RMS>), grid, dim3(256), shm, s, a);
+}
+
+template <bool GATED, int BN>
+void launch_gemm2(const LinearArgs& a, dim3 grid, hipStream_t s) {
+  launch_gemm2_n<GATED, BN, true>(a, grid, s);
+}
+
 hipError_t launch_linear(LinearArgs a, hipStream_t s, int* n_parts, LaunchTiming* timing) {
   if (a.M <= 0) return hipSuccess;
   const bool gated = (a.epi == EPI_GATED_GELU || a.epi == EPI_GATED_SILU);
@@ -1215,6 +1395,18 @@ hipError_t launch_linear(LinearArgs a, hipStream_t s, int* n_parts, LaunchTiming
     if (a.norm != NORM_NONE) {
       hipError_t e = launch_row_stats(a.x, a.ldx, a.M, a.K, a.norm, a.eps, a.stats, s);
       if (e != hipSuccess) return e;
+    }
+    // long row blocks with a normalised input (QKV, cross query, gate/up): 128-row tiles with
+    // double buffering (measured faster than the 64x64 tiles there; the residual projections keep
+    // the 64x64 tiles, whose larger grids hide the memory latency better)
+    if (a.epi != EPI_ARGMAX && a.norm == NORM_RMS && a.M > 64 && a.K % G2K == 0) {
+      const int bn = gated ? 64 : 128;
+      if (a.n_mats == 1 || gated || a.n_per % bn == 0) {
+        dim3 grid((a.M + G2M - 1) / G2M, (n_out + bn - 1) / bn);
+        if (gated) launch_gemm2<true, 64>(a, grid, s);
+        else launch_gemm2<false, 128>(a, grid, s);
+        return hipGetLastError();
+      }
     }
     dim3 grid((n_out + TN - 1) / TN, (a.M + TM - 1) / TM);
     if (gated) hipLaunchKernelGGL((gemm_kernel<true>), grid, dim3(256), 0, s, a);
