@@ -57,6 +57,17 @@ def verify_bytes(shape, B: int, gamma: int, ctx: int, kv_bytes: int = 4) -> floa
     return shape.n_layers * (layer + kv) + V * d * we + d * 4
 
 
+def dominant_kernel_name(sh) -> str:
+    """rocprof name of the one-row GEMV instantiation that streams the RMS-normalised d_model-wide
+    matrices (the kernel the library times while profiling)."""
+    d = sh.d_model
+    if sh.dtype == "bf16" and 2048 <= d <= 6144 and d % 8 == 0:
+        return "gemv1k_kernel<unsigned short, %d, 1>" % ((d + 2047) // 2048)
+    pieces = (d + 511) // 512
+    kp = 4 if pieces <= 4 else (12 if 8 < pieces <= 12 else 8)
+    return "gemv1_kernel<%s, %d, 1>" % ("unsigned short" if sh.dtype == "bf16" else "float", kp)
+
+
 def counted_traffic(kernel: str):
     """HBM bytes per launch of the dominant kernel from the committed rocprofv3 counter summary
     (FETCH_SIZE and WRITE_SIZE runs scaled by a copy-kernel reading), or None when the summary is
@@ -281,9 +292,8 @@ def main():
               "GBps": round(vbytes / verify_s / 1e9, 1),
               "frac": round(vbytes / verify_s / 1e9 / HBM_PEAK_GBS, 4)}
 
-    # dominant kernel: every launch of the one-row weight-streaming GEMV instantiation that streams
-    # the RMS-normalised d_model-wide matrices (rocprof's gemv1_kernel<T, KP, 1>), timed by events
-    # bound to its own dispatch
+    # dominant kernel: every launch of the one-row weight-streaming GEMV that streams the
+    # RMS-normalised d_model-wide matrices, timed by events bound to its own dispatch
     abi.ssd_profile_enable(dd.ctx, True)
     abi.ssd_profile_read(dd.ctx)
     for _ in range(max(1, args.steps // 2)):
@@ -295,9 +305,7 @@ def main():
     per_launch_bytes = nbytes / n_launch
     avg_s = secs / n_launch
     achieved = per_launch_bytes / avg_s / 1e9
-    pieces = (sh.d_model + 511) // 512
-    kp = 4 if pieces <= 4 else (12 if 8 < pieces <= 12 else 8)
-    kname = "gemv1_kernel<%s, %d, 1>" % ("unsigned short" if sh.dtype == "bf16" else "float", kp)
+    kname = dominant_kernel_name(sh)
     counted = counted_traffic(kname) if wl.name == "c3-flant5-xl" else None
     roofline = {"bound": "hbm", "kernel": kname + " (one-row weight-streaming GEMV, RMSNorm folded)",
                 "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",

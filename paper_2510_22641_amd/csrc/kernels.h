@@ -91,13 +91,14 @@ struct LinearArgs {
   const float* out_gain = nullptr;
 };
 
-// Kernel-level timing of one instantiation of the one-row GEMV, gemv1_kernel<WT, kp, norm>: when
-// start / stop are set and the launch takes that kernel, it is launched with the events bound to
-// its own dispatch (hipExtLaunchKernel), so their elapsed time is the kernel's execution time;
-// `timed` reports whether it happened.
+// Kernel-level timing of the one-row GEMV launches with K inputs and input normalisation `norm`
+// (gemv1k_kernel for bf16 rows of 2048..6144, else gemv1_kernel): when start / stop are set and
+// the launch is one of those, it is launched with the events bound to its own dispatch
+// (hipExtLaunchKernel), so their elapsed time is the kernel's execution time; `timed` reports
+// whether it happened.
 struct LaunchTiming {
   hipEvent_t start = nullptr, stop = nullptr;
-  int kp = 4;
+  int K = 0;
   int norm = NORM_RMS;
   bool timed = false;
 };

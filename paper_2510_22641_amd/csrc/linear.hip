@@ -555,6 +555,142 @@ __global__ __launch_bounds__(256) void gemv1_kernel(const LinearArgs a) {
   gemv_finish<WT, 1>(a, r, acc, yold, live, gated, argmax, 0, 1, tid, lane, wave, rv, ri);
 }
 
+// One input row, 2048 <= K <= 2048 * KP (no LayerNorm): the K range is split
+// over the block's four waves instead of its rows.  A block owns the four row pairs of gemv1
+// (eight weight rows); wave w reads elements p * 2048 + 512 w + 8 lane .. +7 of the input, of the
+// gain and of all eight rows, so that each wave requests a quarter of the input and gain bytes
+// gemv1 does for the same weight bytes (those extra requests, not the weights, limit gemv1).  The
+// eight partial dot products of a lane are reduced over the wave by halving exchanges (three
+// swaps leave each group of eight lanes one row), then over the waves through LDS; RMSNorm is
+// folded as in gemv1 with the sum of squares reduced the same way.  Wave w finishes row pair w
+// with gemv1's epilogue.
+template <typename WT, int KP, int NORM>
+__global__ __launch_bounds__(256) void gemv1k_kernel(const LinearArgs a) {
+  static_assert(NORM != NORM_LN, "LayerNorm rows take gemv1_kernel");
+  __shared__ float part[GV_WAVES][9];
+  __shared__ float rv[GV_WAVES][1];
+  __shared__ int ri[GV_WAVES][1];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int K = a.K;
+  const bool gated = (a.epi == EPI_GATED_GELU || a.epi == EPI_GATED_SILU);
+  const bool argmax = a.epi == EPI_ARGMAX;
+  const int n_total = gated ? a.n_per : a.n_per * a.n_mats;
+  const int n_pairs = gated ? a.n_per : (n_total + 1) / 2;
+  constexpr bool rms = NORM == NORM_RMS;
+
+  // inputs first (the wait counter retires loads in issue order); clamped, never conditional
+  float xv[KP][8];
+#pragma unroll
+  for (int p = 0; p < KP; ++p) {
+    const int e = min(p * 2048 + wave * 512 + lane * 8, K - 8);
+    const float4 x0 = *reinterpret_cast<const float4*>(a.x + e);
+    const float4 x1 = *reinterpret_cast<const float4*>(a.x + e + 4);
+    xv[p][0] = x0.x; xv[p][1] = x0.y; xv[p][2] = x0.z; xv[p][3] = x0.w;
+    xv[p][4] = x1.x; xv[p][5] = x1.y; xv[p][6] = x1.z; xv[p][7] = x1.w;
+  }
+  const int pr = blockIdx.x * GV_WAVES + wave;
+  const RowPair<WT> r = row_pair<WT>(a, gated, n_total, pr < n_pairs ? pr : 0);
+  const bool live = pr < n_pairs;
+  float yold[2][1] = {{0.f}, {0.f}};
+  if (lane == 0 && live && (a.epi == EPI_RESID || a.epi == EPI_BIAS_RESID)) {
+    const float* src = a.epi == EPI_RESID ? a.y : a.resid;
+    yold[0][0] = (src && r.ok0) ? src[r.n0] : 0.f;
+    yold[1][0] = (src && r.ok1) ? src[r.n1] : 0.f;
+  }
+  Vec8<WT> w[GV_WAVES][2][KP];
+#pragma unroll
+  for (int q = 0; q < GV_WAVES; ++q) {
+    const int pq = blockIdx.x * GV_WAVES + q;
+    const RowPair<WT> rq = row_pair<WT>(a, gated, n_total, pq < n_pairs ? pq : 0);
+#pragma unroll
+    for (int p = 0; p < KP; ++p) {
+      const int e = min(p * 2048 + wave * 512 + lane * 8, K - 8);
+      w[q][0][p].load(rq.w0 + e);
+      w[q][1][p].load(rq.w1 + e);
+    }
+  }
+  Vec8<float> gv[rms ? KP : 1];
+  if (rms) {
+#pragma unroll
+    for (int p = 0; p < KP; ++p) gv[p].load(a.gain + min(p * 2048 + wave * 512 + lane * 8, K - 8));
+  }
+
+  // pieces past K (clamped re-reads) count as zero
+#pragma unroll
+  for (int p = 0; p < KP; ++p)
+    if (p * 2048 + wave * 512 + lane * 8 >= K) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) xv[p][e] = 0.f;
+    }
+  float s2 = 0.f;
+  if (rms) {
+#pragma unroll
+    for (int p = 0; p < KP; ++p)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) s2 = fmaf(xv[p][e], xv[p][e], s2);
+    s2 = wave_sum(s2);
+#pragma unroll
+    for (int p = 0; p < KP; ++p) {
+      float g[8];
+      gv[p].to_f32(g);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) xv[p][e] *= g[e];
+    }
+  }
+
+  // acc[2q + s]: row s of pair q
+  float acc[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) acc[i] = 0.f;
+#pragma unroll
+  for (int q = 0; q < GV_WAVES; ++q)
+#pragma unroll
+    for (int p = 0; p < KP; ++p) {
+      float w0[8], w1[8];
+      w[q][0][p].to_f32(w0);
+      w[q][1][p].to_f32(w1);
+      float t0 = acc[2 * q], t1 = acc[2 * q + 1];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        t0 = fmaf(w0[e], xv[p][e], t0);
+        t1 = fmaf(w1[e], xv[p][e], t1);
+      }
+      acc[2 * q] = t0;
+      acc[2 * q + 1] = t1;
+    }
+  // halving exchanges: after the swaps over lane bits 5, 4, 3 lane l holds a partial of row
+  // (l >> 3) & 7, summed over its group of eight lanes by the last three steps
+  const bool b5 = lane & 32, b4 = lane & 16, b3 = lane & 8;
+  float u[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const float mine = b5 ? acc[i + 4] : acc[i], other = b5 ? acc[i] : acc[i + 4];
+    u[i] = mine + __shfl_xor(other, 32, SSD_WAVE);
+  }
+  float t[2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const float mine = b4 ? u[i + 2] : u[i], other = b4 ? u[i] : u[i + 2];
+    t[i] = mine + __shfl_xor(other, 16, SSD_WAVE);
+  }
+  float sres = (b3 ? t[1] : t[0]) + __shfl_xor(b3 ? t[0] : t[1], 8, SSD_WAVE);
+  sres += __shfl_xor(sres, 4, SSD_WAVE);
+  sres += __shfl_xor(sres, 2, SSD_WAVE);
+  sres += __shfl_xor(sres, 1, SSD_WAVE);
+  if ((lane & 7) == 0) part[wave][lane >> 3] = sres;
+  if (rms && lane == 0) part[wave][8] = s2;
+  __syncthreads();
+  float rscale = 1.f;
+  if (rms) {
+    const float tot = (part[0][8] + part[1][8]) + (part[2][8] + part[3][8]);
+    rscale = 1.0f / sqrtf(tot / (float)K + a.eps);
+  }
+  float res[2][1];
+  res[0][0] = ((part[0][2 * wave] + part[1][2 * wave]) + (part[2][2 * wave] + part[3][2 * wave])) * rscale;
+  res[1][0] = ((part[0][2 * wave + 1] + part[1][2 * wave + 1]) + (part[2][2 * wave + 1] + part[3][2 * wave + 1])) * rscale;
+  gemv_finish<WT, 1>(a, r, res, yold, live, gated, argmax, 0, 1, tid, lane, wave, rv, ri);
+}
+
 // ---------------------------------------------------------------------------------------------
 // Skinny MFMA path: 2..128 input rows (the verify chunk), bf16 weights, 16 rows per grid row.
 // A block owns 16 output features (the A rows of v_mfma_f32_16x16x32_bf16) and its 4 waves split
@@ -1241,6 +1377,35 @@ void launch_gemv1(const LinearArgs& a, dim3 grid, hipStream_t s, LaunchTiming* t
   }
 }
 
+template <int KP, int NORM>
+void launch_gemv1k(const LinearArgs& a, dim3 grid, hipStream_t s, LaunchTiming* t) {
+  if (t) {
+    hipExtLaunchKernelGGL((gemv1k_kernel<bf16_t, KP, NORM>), grid, dim3(256), 0u, s, t->start,
+                          t->stop, 0u, a);
+    t->timed = true;
+  } else {
+    hipLaunchKernelGGL((gemv1k_kernel<bf16_t, KP, NORM>), grid, dim3(256), 0, s, a);
+  }
+}
+
+// One bf16 row with 2048 <= K <= 6144 and no LayerNorm: the K-split kernel (same grid as gemv1).
+bool use_gemv1k(const LinearArgs& a) {
+  return a.M == 1 && a.wdtype == 1 && a.norm != NORM_LN && a.K >= 2048 && a.K <= 3 * 2048 &&
+         a.K % 8 == 0;
+}
+
+hipError_t launch_gemv1k_any(const LinearArgs& a, hipStream_t s, LaunchTiming* t) {
+  const dim3 grid(gv_plan(a).blocks);
+  const bool timed = t && a.K == t->K && a.norm == t->norm && t->start && t->stop;
+  LaunchTiming* tt = timed ? t : nullptr;
+  const int kp = (a.K + 2047) / 2048;
+  const bool rms = a.norm == NORM_RMS;
+  if (kp == 1) rms ? launch_gemv1k<1, NORM_RMS>(a, grid, s, tt) : launch_gemv1k<1, NORM_NONE>(a, grid, s, tt);
+  else if (kp == 2) rms ? launch_gemv1k<2, NORM_RMS>(a, grid, s, tt) : launch_gemv1k<2, NORM_NONE>(a, grid, s, tt);
+  else rms ? launch_gemv1k<3, NORM_RMS>(a, grid, s, tt) : launch_gemv1k<3, NORM_NONE>(a, grid, s, tt);
+  return hipGetLastError();
+}
+
 template <typename WT, int MB, int KP>
 hipError_t launch_gemv_kp(const LinearArgs& a, const GvPlan& p, hipStream_t s, LaunchTiming* t) {
   static bool attr = false;
@@ -1252,7 +1417,7 @@ hipError_t launch_gemv_kp(const LinearArgs& a, const GvPlan& p, hipStream_t s, L
   dim3 grid(p.blocks, (a.M + MB - 1) / MB);
   if (MB == 1 && a.M == 1 && a.K <= 512 * KP && (a.norm != NORM_LN || KP == 4)) {
     // one row that fits a batch: the register path
-    const bool timed = t && KP == t->kp && a.norm == t->norm && t->start && t->stop;
+    const bool timed = t && a.K == t->K && a.norm == t->norm && t->start && t->stop;
     if (a.norm == NORM_RMS) launch_gemv1<WT, KP, NORM_RMS>(a, grid, s, timed ? t : nullptr);
     else if (a.norm == NORM_LN) launch_gemv1<WT, 4, NORM_LN>(a, grid, s, timed ? t : nullptr);
     else launch_gemv1<WT, KP, NORM_NONE>(a, grid, s, timed ? t : nullptr);
@@ -1416,6 +1581,7 @@ hipError_t launch_linear(LinearArgs a, hipStream_t s, int* n_parts, LaunchTiming
   a.use_mfma = 0;
   if (a.epi == EPI_ARGMAX) a.n_parts = gv_plan(a).blocks;
   if (n_parts) *n_parts = a.n_parts;
+  if (use_gemv1k(a)) return launch_gemv1k_any(a, s, timing);
   return a.wdtype == 1 ? launch_gemv_t<bf16_t>(a, s, timing) : launch_gemv_t<float>(a, s, timing);
 }
 

@@ -198,7 +198,7 @@ hipError_t run_linear(ssd_ctx* c, const LinearArgs& a, int* n_parts = nullptr) {
   LaunchTiming t;
   t.start = c->ev_pool[c->ev_used];
   t.stop = c->ev_pool[c->ev_used + 1];
-  t.kp = gemv_pieces(c->d.d_model);  // the instantiation that streams the d_model-wide matrices
+  t.K = c->d.d_model;  // the one-row launches over the d_model-wide matrices
   hipError_t err = launch_linear(a, c->stream, n_parts, &t);
   if (err != hipSuccess || !t.timed) return err;
   c->ev_used += 2;
