@@ -29,14 +29,27 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published
 
 
-def draft_step_bytes(shape, k: int, ctx: int, kv_bytes: int = 4) -> float:
+def cross_folded(shape, max_batch: int) -> bool:
+    """Whether the library folds the T5 cross-attention of a context into two float32 matrices
+    per layer (one-sequence contexts with a supported number of visual keys)."""
+    nv = shape.n_visual
+    return (shape.arch == "t5" and max_batch == 1 and nv in (8, 16, 32, 64)
+            and nv <= shape.d_head and shape.n_heads * nv <= 6144
+            and shape.d_model <= 6144)
+
+
+def draft_step_bytes(shape, k: int, ctx: int, kv_bytes: int = 4, folded: bool = False) -> float:
     """Algorithmic bytes of one batch-1 draft step at context length ctx (weights read once,
-    KV of layers 1..k read, one position's K/V written; kv_bytes per cached element)."""
+    KV of layers 1..k read, one position's K/V written; kv_bytes per cached element).  With the
+    cross-attention folded, its two float32 matrices replace the cross query / output weights and
+    the visual K/V."""
     we = 2 if shape.dtype == "bf16" else 4
     d, hd, f, V, h = shape.d_model, shape.hd, shape.d_ff, shape.vocab, shape.in_width
     layer = (4 * d * hd + 3 * d * f) * we + 3 * d * 4  # QKVO + FFN + norm gains
     kv = 2 * ctx * hd * kv_bytes + 2 * hd * kv_bytes
-    if shape.arch == "t5":
+    if shape.arch == "t5" and folded:
+        layer += 2 * shape.n_heads * shape.n_visual * d * 4 + d * 4
+    elif shape.arch == "t5":
         layer += 2 * d * hd * we + d * 4
         kv += 2 * shape.n_visual * hd * kv_bytes
     imit = 2 * d * h * we + (h + 3 * d) * 4
@@ -64,7 +77,7 @@ def dominant_kernel_name(sh) -> str:
     if sh.dtype == "bf16" and 2048 <= d <= 6144 and d % 8 == 0:
         return "gemv1k_kernel<unsigned short, %d, 1>" % ((d + 2047) // 2048)
     pieces = (d + 511) // 512
-    kp = 4 if pieces <= 4 else (12 if 8 < pieces <= 12 else 8)
+    kp = 2 if pieces <= 2 else 4 if pieces <= 4 else (12 if 8 < pieces <= 12 else 8)
     return "gemv1_kernel<%s, %d, 1>" % ("unsigned short" if sh.dtype == "bf16" else "float", kp)
 
 
@@ -148,7 +161,7 @@ def sweep_c4(args):
             dt, st, toks = timed(True)
             dtg, _, gtoks = timed(False)
             d_s, v_s, ctx = step_timings(dd, pt, vt, B, g)
-            db = draft_step_bytes(sh, k, ctx, dd.k_pool.element_size())
+            db = draft_step_bytes(sh, k, ctx, dd.k_pool.element_size(), cross_folded(sh, mb))
             db += (B - 1) * 2 * k * (ctx + (sh.n_visual if sh.arch == "t5" else 0)) * sh.hd * \
                 dd.k_pool.element_size()
             vb = verify_bytes(sh, B, g, ctx, dd.k_pool.element_size())
@@ -283,7 +296,8 @@ def main():
 
     # draft-step time: events around the gamma-step draft call (captured graph) on its stream
     step_s, verify_s, ctx = step_timings(dd, pt, vt, B, g)
-    step_bytes = draft_step_bytes(sh, wl.draft_layers, ctx, dd.k_pool.element_size())
+    step_bytes = draft_step_bytes(sh, wl.draft_layers, ctx, dd.k_pool.element_size(),
+                                  cross_folded(sh, dd.cap.max_batch))
     draft = {"us": round(step_s * 1e6, 2), "bytes": int(step_bytes),
              "GBps": round(step_bytes / step_s / 1e9, 1),
              "frac": round(step_bytes / step_s / 1e9 / HBM_PEAK_GBS, 4)}

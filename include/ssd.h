@@ -204,8 +204,8 @@ int ssd_set_graphs(ssd_ctx* ctx, int enable);
  * the one-row weight-streaming GEMV that streams the RMS-normalised d_model-wide matrices (QKV,
  * cross-attention query, gate/up, LM head; the kernel that carries most of a batch-1 draft step:
  * gemv1k_kernel<unsigned short, KP, 1> with KP = ceil(d_model / 2048) for bf16 weights and
- * 2048 <= d_model <= 6144, else gemv1_kernel<T, KP, 1> with KP = 4 for d_model <= 2048, 12 for
- * 4096 < d_model <= 6144, else 8) is launched with two HIP events bound to its own dispatch on
+ * 2048 <= d_model <= 6144, else gemv1_kernel<T, KP, 1> with KP = 2 for d_model <= 1024, 4 for
+ * d_model <= 2048, 12 for 4096 < d_model <= 6144, else 8) is launched with two HIP events bound to its own dispatch on
  * the context's stream, so their elapsed time is the kernel's execution time; its algorithmic
  * bytes (weights + input row + output row) are added up.  ssd_profile_read synchronises the stream and returns
  * the number of such launches, the summed kernel time in seconds and the summed bytes since the

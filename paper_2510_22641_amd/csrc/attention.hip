@@ -314,7 +314,102 @@ hipError_t launch_attn_t(const AttnArgs& a, hipStream_t s) {
   return a.dh == 64 ? launch_attn_dh<KT, 64>(a, s) : launch_attn_dh<KT, 128>(a, s);
 }
 
+// Folded cross-attention, query side: fq[h*NV + j][k] = sum_e K[h][j][e] * Wq[h*dh + e][k].
+// Block (column tile, head h): thread t owns column k; the head's keys sit in LDS and every
+// weight element is read once (coalesced along k).
+template <typename KT, typename WT, int NV>
+__global__ __launch_bounds__(256) void fold_q_kernel(const KT* __restrict__ xk,
+                                                     const WT* __restrict__ wq, float* __restrict__ fq,
+                                                     int dh, int d) {
+  __shared__ float ks[NV][129];
+  const int h = blockIdx.y, k = blockIdx.x * 256 + threadIdx.x;
+  for (int i = threadIdx.x; i < NV * dh; i += 256) {
+    const int j = i / dh, e = i - j * dh;
+    ks[j][e] = load_elem(xk + ((size_t)h * NV + j) * dh + e);
+  }
+  __syncthreads();
+  if (k >= d) return;
+  float acc[NV];
+#pragma unroll
+  for (int j = 0; j < NV; ++j) acc[j] = 0.f;
+  for (int e = 0; e < dh; ++e) {
+    const float w = load_elem(wq + ((size_t)h * dh + e) * d + k);
+#pragma unroll
+    for (int j = 0; j < NV; ++j) acc[j] = fmaf(ks[j][e], w, acc[j]);
+  }
+#pragma unroll
+  for (int j = 0; j < NV; ++j) fq[((size_t)h * NV + j) * d + k] = acc[j];
+}
+
+// Folded cross-attention, output side: fo[n][h*NV + j] = sum_e Wo[n][h*dh + e] * V[h][j][e].
+// Block (row tile, head h): thread t owns output row n and reads its dh weights of head h.
+template <typename KT, typename WT, int NV>
+__global__ __launch_bounds__(256) void fold_o_kernel(const KT* __restrict__ xv,
+                                                     const WT* __restrict__ wo, float* __restrict__ fo,
+                                                     int H, int dh, int d) {
+  __shared__ float vs[NV][129];
+  const int h = blockIdx.y, n = blockIdx.x * 256 + threadIdx.x;
+  for (int i = threadIdx.x; i < NV * dh; i += 256) {
+    const int j = i / dh, e = i - j * dh;
+    vs[j][e] = load_elem(xv + ((size_t)h * NV + j) * dh + e);
+  }
+  __syncthreads();
+  if (n >= d) return;
+  const int HD = H * dh;
+  float acc[NV];
+#pragma unroll
+  for (int j = 0; j < NV; ++j) acc[j] = 0.f;
+  for (int e = 0; e < dh; ++e) {
+    const float w = load_elem(wo + (size_t)n * HD + (size_t)h * dh + e);
+#pragma unroll
+    for (int j = 0; j < NV; ++j) acc[j] = fmaf(vs[j][e], w, acc[j]);
+  }
+  float* dst = fo + (size_t)n * H * NV + (size_t)h * NV;
+#pragma unroll
+  for (int j = 0; j < NV; ++j) dst[j] = acc[j];
+}
+
+template <typename KT, typename WT, int NV>
+hipError_t launch_fold_t(const void* xk, const void* xv, const void* wq, const void* wo, int H,
+                         int dh, int d, float* fq, float* fo, hipStream_t s) {
+  const dim3 grid((d + 255) / 256, H);
+  hipLaunchKernelGGL((fold_q_kernel<KT, WT, NV>), grid, dim3(256), 0, s,
+                     reinterpret_cast<const KT*>(xk), reinterpret_cast<const WT*>(wq), fq, dh, d);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((fold_o_kernel<KT, WT, NV>), grid, dim3(256), 0, s,
+                     reinterpret_cast<const KT*>(xv), reinterpret_cast<const WT*>(wo), fo, H, dh, d);
+  return hipGetLastError();
+}
+
+template <int NV>
+hipError_t launch_fold_nv(const void* xk, const void* xv, int kvdtype, const void* wq,
+                          const void* wo, int wdtype, int H, int dh, int d, float* fq, float* fo,
+                          hipStream_t s) {
+  if (kvdtype == 1)
+    return wdtype == 1 ? launch_fold_t<bf16_t, bf16_t, NV>(xk, xv, wq, wo, H, dh, d, fq, fo, s)
+                       : launch_fold_t<bf16_t, float, NV>(xk, xv, wq, wo, H, dh, d, fq, fo, s);
+  return wdtype == 1 ? launch_fold_t<float, bf16_t, NV>(xk, xv, wq, wo, H, dh, d, fq, fo, s)
+                     : launch_fold_t<float, float, NV>(xk, xv, wq, wo, H, dh, d, fq, fo, s);
+}
+
 }  // namespace
+
+bool cross_fold_ok(int nv, int dh) {
+  return (nv == 8 || nv == 16 || nv == 32 || nv == 64) && dh <= 128;
+}
+
+hipError_t launch_cross_fold(const void* xk, const void* xv, int kvdtype, const void* wq,
+                             const void* wo, int wdtype, int H, int nv, int dh, int d, float* fq,
+                             float* fo, hipStream_t s) {
+  if (!cross_fold_ok(nv, dh) || H < 1 || d < 1) return hipErrorInvalidValue;
+  switch (nv) {
+    case 8: return launch_fold_nv<8>(xk, xv, kvdtype, wq, wo, wdtype, H, dh, d, fq, fo, s);
+    case 16: return launch_fold_nv<16>(xk, xv, kvdtype, wq, wo, wdtype, H, dh, d, fq, fo, s);
+    case 32: return launch_fold_nv<32>(xk, xv, kvdtype, wq, wo, wdtype, H, dh, d, fq, fo, s);
+    default: return launch_fold_nv<64>(xk, xv, kvdtype, wq, wo, wdtype, H, dh, d, fq, fo, s);
+  }
+}
 
 hipError_t launch_attention(const AttnArgs& a, hipStream_t s) {
   if (a.B <= 0 || a.C <= 0) return hipSuccess;

@@ -10,7 +10,10 @@ typedef uint16_t bf16_t;
 
 namespace ssd {
 
-enum Norm { NORM_NONE = 0, NORM_RMS = 1, NORM_LN = 2 };
+// Input transform of a linear layer: none, RMSNorm (gain), LayerNorm (gain, shift), or a softmax
+// over consecutive groups of LinearArgs::group inputs (the folded cross-attention's probabilities;
+// one-row vector path only).
+enum Norm { NORM_NONE = 0, NORM_RMS = 1, NORM_LN = 2, NORM_SOFTMAX = 3 };
 
 // Paged KV addressing shared by the QKV epilogue and the attention kernels.
 struct PagedKV {
@@ -47,6 +50,7 @@ struct LinearArgs {
   const float* gain = nullptr;
   const float* shift = nullptr;
   float eps = 0.f;
+  int group = 0;  // NORM_SOFTMAX: inputs per softmax group (8, 16, 32 or 64)
   const void* w[3] = {nullptr, nullptr, nullptr};  // [n_per][K] each, wdtype
   int n_mats = 1;
   int n_per = 0;
@@ -91,8 +95,8 @@ struct LinearArgs {
   const float* out_gain = nullptr;
 };
 
-// Kernel-level timing of the one-row GEMV launches with K inputs and input normalisation `norm`
-// (gemv1k_kernel for bf16 rows of 2048..6144, else gemv1_kernel): when start / stop are set and
+// Kernel-level timing of the one-row GEMV launches with K inputs, input normalisation `norm` and
+// weight type `wdtype` (gemv1k_kernel for bf16 rows of 2048..6144, else gemv1_kernel): when start / stop are set and
 // the launch is one of those, it is launched with the events bound to its own dispatch
 // (hipExtLaunchKernel), so their elapsed time is the kernel's execution time; `timed` reports
 // whether it happened.
@@ -100,6 +104,7 @@ struct LaunchTiming {
   hipEvent_t start = nullptr, stop = nullptr;
   int K = 0;
   int norm = NORM_RMS;
+  int wdtype = 1;
   bool timed = false;
 };
 
@@ -193,6 +198,16 @@ struct AttnArgs {
   int32_t* status;
 };
 hipError_t launch_attention(const AttnArgs& a, hipStream_t s);
+
+// Cross-attention of one sequence folded into two float32 matrices per layer (T5; the visual keys
+// and values are fixed once prefilled):
+//   fq[h*nv + j][k] = sum_e K[h][j][e] * Wq[h*dh + e][k]   ([H*nv][d]: scores = fq . norm(x))
+//   fo[n][h*nv + j] = sum_e Wo[n][h*dh + e] * V[h][j][e]   ([d][H*nv]: out = fo . softmax(scores))
+// xk / xv: [H][nv][dh] of kvdtype; wq [H*dh][d], wo [d][H*dh] of wdtype.
+bool cross_fold_ok(int nv, int dh);
+hipError_t launch_cross_fold(const void* xk, const void* xv, int kvdtype, const void* wq,
+                             const void* wo, int wdtype, int H, int nv, int dh, int d, float* fq,
+                             float* fo, hipStream_t s);
 
 // Row statistics for normalisation: stats[m] = (mean, 1/sqrt(var+eps)) (LN) or (0, 1/rms) (RMS).
 hipError_t launch_row_stats(const float* x, int ldx, int M, int K, int norm, float eps,

@@ -437,8 +437,9 @@ __global__ __launch_bounds__(256) void gemv_kernel(const LinearArgs a) {
 // lanes hold the whole input row in registers (lane l owns elements p*512 + 8l .. +7 of every
 // piece p), so the norm statistics are wave reductions and nothing is staged in LDS: each wave
 // requests its inputs, then both weight rows, then the norm's gain (and shift), and computes the
-// statistics while the weights are in flight.  NORM is the input normalisation (a template
-// parameter so that rows without one keep no gain registers).
+// statistics while the weights are in flight.  NORM is the input transform (a template parameter
+// so that rows without one keep no gain registers); NORM_SOFTMAX turns the row into per-group
+// softmax probabilities (the folded cross-attention's second product).
 template <typename WT, int KP, int NORM>
 __global__ __launch_bounds__(256) void gemv1_kernel(const LinearArgs a) {
   __shared__ float rv[GV_WAVES][1];
@@ -482,6 +483,28 @@ __global__ __launch_bounds__(256) void gemv1_kernel(const LinearArgs a) {
     for (int p = 0; p < KP; ++p) sv[p].load(a.shift + min(p * 512 + lane * 8, K - 8));
   }
 
+  if (NORM == NORM_SOFTMAX) {
+    // softmax over groups of a.group inputs: a group is a.group / 8 consecutive lanes of a piece
+    // (512 is a multiple of the group, so groups never straddle pieces, and K of whole groups)
+    const int gl = a.group >> 3;
+#pragma unroll
+    for (int p = 0; p < KP; ++p) {
+      float m = xv[p][0];
+#pragma unroll
+      for (int e = 1; e < 8; ++e) m = fmaxf(m, xv[p][e]);
+      for (int o = 1; o < gl; o <<= 1) m = fmaxf(m, __shfl_xor(m, o, SSD_WAVE));
+      float sum = 0.f;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        xv[p][e] = expf(xv[p][e] - m);
+        sum += xv[p][e];
+      }
+      for (int o = 1; o < gl; o <<= 1) sum += __shfl_xor(sum, o, SSD_WAVE);
+      const float inv = 1.0f / sum;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) xv[p][e] *= inv;
+    }
+  }
   // pieces past K (clamped re-reads) count as zero
 #pragma unroll
   for (int p = 0; p < KP; ++p)
@@ -1390,13 +1413,14 @@ void launch_gemv1k(const LinearArgs& a, dim3 grid, hipStream_t s, LaunchTiming* 
 
 // One bf16 row with 2048 <= K <= 6144 and no LayerNorm: the K-split kernel (same grid as gemv1).
 bool use_gemv1k(const LinearArgs& a) {
-  return a.M == 1 && a.wdtype == 1 && a.norm != NORM_LN && a.K >= 2048 && a.K <= 3 * 2048 &&
-         a.K % 8 == 0;
+  return a.M == 1 && a.wdtype == 1 && (a.norm == NORM_NONE || a.norm == NORM_RMS) &&
+         a.K >= 2048 && a.K <= 3 * 2048 && a.K % 8 == 0;
 }
 
 hipError_t launch_gemv1k_any(const LinearArgs& a, hipStream_t s, LaunchTiming* t) {
   const dim3 grid(gv_plan(a).blocks);
-  const bool timed = t && a.K == t->K && a.norm == t->norm && t->start && t->stop;
+  const bool timed = t && a.K == t->K && a.norm == t->norm && a.wdtype == t->wdtype && t->start &&
+                     t->stop;
   LaunchTiming* tt = timed ? t : nullptr;
   const int kp = (a.K + 2047) / 2048;
   const bool rms = a.norm == NORM_RMS;
@@ -1415,25 +1439,29 @@ hipError_t launch_gemv_kp(const LinearArgs& a, const GvPlan& p, hipStream_t s, L
     attr = true;
   }
   dim3 grid(p.blocks, (a.M + MB - 1) / MB);
-  if (MB == 1 && a.M == 1 && a.K <= 512 * KP && (a.norm != NORM_LN || KP == 4)) {
+  if (MB == 1 && a.M == 1 && (a.norm == NORM_LN ? a.K <= 2048 : a.K <= 512 * KP)) {
     // one row that fits a batch: the register path
-    const bool timed = t && a.K == t->K && a.norm == t->norm && t->start && t->stop;
+    const bool timed = t && a.K == t->K && a.norm == t->norm &&
+                       (int)(sizeof(WT) == 2) == t->wdtype && t->start && t->stop;
     if (a.norm == NORM_RMS) launch_gemv1<WT, KP, NORM_RMS>(a, grid, s, timed ? t : nullptr);
     else if (a.norm == NORM_LN) launch_gemv1<WT, 4, NORM_LN>(a, grid, s, timed ? t : nullptr);
+    else if (a.norm == NORM_SOFTMAX) launch_gemv1<WT, KP, NORM_SOFTMAX>(a, grid, s, nullptr);
     else launch_gemv1<WT, KP, NORM_NONE>(a, grid, s, timed ? t : nullptr);
     return hipGetLastError();
   }
+  if (a.norm == NORM_SOFTMAX) return hipErrorInvalidValue;
   const size_t shm = (size_t)MB * ((a.K + 7) & ~7) * sizeof(float);
   hipLaunchKernelGGL((gemv_kernel<WT, MB, KP>), grid, dim3(256), shm, s, a);
   return hipGetLastError();
 }
 
-// pieces per batch: the whole row up to 12 pieces (6144 elements), else batches of 8
 }  // namespace
 
-// whole rows up to 12 pieces of 512 elements (6144) in one batch, else batches of 8
+// whole rows up to 12 pieces of 512 elements (6144) in one batch (2 or 4 pieces for short rows),
+// else batches of 8
 int gemv_pieces(int K) {
   const int pieces = (K + 511) / 512;
+  if (pieces <= 2) return 2;
   if (pieces <= 4) return 4;
   if (pieces <= 8 || pieces > 12) return 8;
   return 12;
@@ -1444,6 +1472,7 @@ namespace {
 template <typename WT, int MB>
 hipError_t launch_gemv_mb(const LinearArgs& a, const GvPlan& p, hipStream_t s, LaunchTiming* t) {
   switch (gemv_pieces(a.K)) {
+    case 2: return launch_gemv_kp<WT, MB, 2>(a, p, s, t);
     case 4: return launch_gemv_kp<WT, MB, 4>(a, p, s, t);
     case 12: return launch_gemv_kp<WT, MB, 12>(a, p, s, t);
     default: return launch_gemv_kp<WT, MB, 8>(a, p, s, t);
@@ -1551,6 +1580,11 @@ void launch_gemm2(const LinearArgs& a, dim3 grid, hipStream_t s) {
 
 hipError_t launch_linear(LinearArgs a, hipStream_t s, int* n_parts, LaunchTiming* timing) {
   if (a.M <= 0) return hipSuccess;
+  // the softmax input transform exists on the one-row register path only
+  if (a.norm == NORM_SOFTMAX &&
+      (a.M != 1 || a.K > 6144 || (a.group != 8 && a.group != 16 && a.group != 32 && a.group != 64) ||
+       a.K % a.group))
+    return hipErrorInvalidValue;
   const bool gated = (a.epi == EPI_GATED_GELU || a.epi == EPI_GATED_SILU);
   const int n_out = gated ? a.n_per : a.n_per * a.n_mats;
   if (want_mfma(a)) {

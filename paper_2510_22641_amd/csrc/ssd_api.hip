@@ -31,7 +31,7 @@ int t5_bucket(int n, int buckets, int max_dist) {
 
 struct Layout {
   size_t x, x1, qkv, q, attn, ffn, inh, xi, stash, vis, part_val, part_idx, stats, bias_tab,
-      p_x, p_attn, p_ffn, ssq, attn_part,
+      p_x, p_attn, p_ffn, ssq, attn_part, fold_q, fold_o,
       bucket, rope_cos, rope_sin, status, cur_tok, g_pending, g_draft, g_target,
       g_count, g_active, g_nactive, g_stats, total;
   int rows_max, head_rows, parts_max, ctx_max, plane_rows, attn_rows;
@@ -39,6 +39,15 @@ struct Layout {
 
 int ctx_len_max(const ssd_dims& d) {
   return d.max_prompt + (d.arch == SSD_ARCH_LLAMA ? d.n_visual : 0);
+}
+
+// One-sequence T5 contexts fold the cross-attention into two float32 matrices per layer (the
+// visual keys are fixed after prefill): one-row steps then take two weight-streaming launches for
+// it instead of a query projection, an attention launch and an output projection.  Needs a
+// softmax group the one-row kernel supports and scores that fit the query buffer.
+bool fold_cross(const ssd_dims& d) {
+  return d.arch == SSD_ARCH_T5 && d.max_batch == 1 && cross_fold_ok(d.n_visual, d.d_head) &&
+         d.n_visual <= d.d_head && (size_t)d.n_heads * d.n_visual <= 6144 && d.d_model <= 6144;
 }
 
 bool make_layout(const ssd_dims& d, Layout& L) {
@@ -80,6 +89,11 @@ bool make_layout(const ssd_dims& d, Layout& L) {
   // key-split partials of the long-context attention (up to 16 query rows per sequence)
   L.attn_rows = (int)(B * 16);
   L.attn_part = take((size_t)L.attn_rows * d.n_heads * ATTN_SPLITS_MAX * (d.d_head + 2) * 4);
+  {
+    const size_t fold = fold_cross(d) ? (size_t)d.n_layers * d.n_heads * d.n_visual * D * 4 : 0;
+    L.fold_q = take(fold);
+    L.fold_o = take(fold);
+  }
   L.bias_tab = take(d.arch == SSD_ARCH_T5 ? (size_t)d.n_heads * d.max_seq * 4 : 0);
   L.bucket = take(d.arch == SSD_ARCH_T5 ? (size_t)d.max_seq * 4 : 0);
   L.rope_cos = take(d.arch == SSD_ARCH_LLAMA ? (size_t)d.max_seq * (d.d_head / 2) * 4 : 0);
@@ -142,6 +156,7 @@ struct ssd_ctx {
   char* ws;
   Layout L;
   bool prefilled = false;
+  bool fold_ready = false;  // fold_q / fold_o hold the prefilled sequence's cross-attention
   // reuse bookkeeping: the last ssd_draft's arguments
   bool draft_valid = false;
   int draft_B = 0, draft_gamma = 0;
@@ -164,6 +179,7 @@ struct ssd_ctx {
     return (size_t)d.max_batch * d.n_heads * d.n_visual * d.d_head;
   }
   size_t kv_elem() const { return d.kvdtype == SSD_BF16 ? 2 : 4; }
+  size_t fold_layer_elems() const { return (size_t)d.n_heads * d.n_visual * d.d_model; }
 };
 
 #define HIP_TRY(expr)                          \
@@ -297,7 +313,22 @@ int run_layers(ssd_ctx* c, float* x, int B, int C, int pos_off, int l0, int l1, 
     HIP_TRY(linear(a, p_attn, HD));
     nssq = nssq_resid;
     // cross-attention to the visual tokens
-    if (t5) {
+    if (t5 && c->fold_ready && R == 1) {
+      // folded: scores = fold_q . rmsnorm(x), then x += fold_o . softmax(scores) per head
+      const int HN = d.n_heads * d.n_visual;
+      a = lin(c);
+      a.x = x; a.ldx = D; a.M = 1; a.K = D;
+      a.norm = NORM_RMS; a.gain = lw.xattn_norm;
+      a.w[0] = c->at<float>(c->L.fold_q) + (size_t)l * c->fold_layer_elems(); a.wdtype = SSD_F32;
+      a.n_per = HN; a.epi = EPI_STORE; a.y = q; a.ldy = HD;
+      HIP_TRY(run_linear(c, a));
+      a = lin(c);
+      a.x = q; a.ldx = HD; a.M = 1; a.K = HN;
+      a.norm = NORM_SOFTMAX; a.group = d.n_visual;
+      a.w[0] = c->at<float>(c->L.fold_o) + (size_t)l * c->fold_layer_elems(); a.wdtype = SSD_F32;
+      a.n_per = D; a.epi = EPI_RESID; a.y = x; a.ldy = D;
+      HIP_TRY(run_linear(c, a));
+    } else if (t5) {
       a = lin(c);
       a.x = x; a.ldx = D; a.M = R; a.K = D;
       a.norm = NORM_RMS; a.gain = lw.xattn_norm;
@@ -580,7 +611,16 @@ int ssd_prefill(ssd_ctx* c, int B, int P, const int32_t* d_prompt, const void* d
         void* dst = (char*)(which ? c->kv.xv : c->kv.xk) + (size_t)l * c->xkv_layer_elems() * c->kv_elem();
         HIP_TRY(launch_scatter_cross(tmp, dst, B, d.n_visual, d.n_heads, d.d_head, d.kvdtype, s));
       }
+      if (fold_cross(d)) {
+        const size_t off = (size_t)l * c->xkv_layer_elems() * c->kv_elem();
+        HIP_TRY(launch_cross_fold((char*)c->kv.xk + off, (char*)c->kv.xv + off, d.kvdtype,
+                                  c->layers[l].xq, c->layers[l].xo, d.wdtype, d.n_heads,
+                                  d.n_visual, d.d_head, D,
+                                  c->at<float>(c->L.fold_q) + (size_t)l * c->fold_layer_elems(),
+                                  c->at<float>(c->L.fold_o) + (size_t)l * c->fold_layer_elems(), s));
+      }
     }
+    c->fold_ready = fold_cross(d);
   }
   EmbedArgs e;
   e.x = x; e.B = B; e.C = Cx; e.d = D; e.embed = c->w.embed; e.vocab = d.vocab; e.wdtype = d.wdtype;

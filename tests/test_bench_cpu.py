@@ -22,6 +22,19 @@ def test_draft_step_bytes_flant5_xl():
     assert 8.2e8 < bench.draft_step_bytes(sh, k, ctx) < 8.5e8
 
 
+def test_draft_step_bytes_flant5_xl_folded_cross_attention():
+    sh = synth.FLANT5_XL
+    d, f, V, ctx, k, H, nv = 2048, 5120, 32128, 72, 6, 32, 32
+    assert bench.cross_folded(sh, 1) and not bench.cross_folded(sh, 8)
+    assert not bench.cross_folded(synth.LLAVA_7B, 1)
+    # the cross query / output weights and visual K/V give way to two float32 [H*nv][d] matrices
+    layer = (4 * d * d + 3 * d * f) * 2 + 3 * d * 4 + 2 * H * nv * d * 4 + d * 4
+    kv = 2 * ctx * d * 4 + 2 * d * 4
+    imit = 2 * d * d * 2 + (d + 3 * d) * 4
+    head = V * d * 2 + d * 4
+    assert bench.draft_step_bytes(sh, k, ctx, 4, True) == k * (layer + kv) + imit + head
+
+
 def test_verify_bytes_llava():
     sh = synth.LLAVA_7B
     d, f, V, L, ctx, g = 4096, 11008, 32000, 32, 700, 5

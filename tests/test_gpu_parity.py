@@ -277,3 +277,30 @@ def test_long_capacity_splits_attention_keys(wl):
     run = parity.device_run(dd, pt, vt, wl.new_tokens, wl.gamma, reuse=True)
     parity.check_run_against_oracle(dec, wl.shape, pr[0], z[0], run, 0, wl.gamma)
     assert dd.sync_status() == (0, 0)
+
+
+@pytest.mark.parametrize("wl", [synth.S1, synth.S_T5], ids=lambda w: w.name)
+def test_folded_cross_attention_matches_unfolded_and_oracle(wl):
+    """A one-sequence T5 context folds the cross-attention into two float32 matrices per layer,
+    used by its one-row steps; a two-sequence context keeps the query projection, attention launch
+    and output projection.  Both runs follow the oracle, and while their token streams agree their
+    per-step draft and target logits agree within the tolerance."""
+    runs = []
+    for mb in (1, 2):
+        dd, dec, pr, z, pt, vt = _setup(wl, seed=4, page_seed=3, max_batch=mb)
+        run = parity.device_run(dd, pt, vt, wl.new_tokens, wl.gamma, reuse=True)
+        parity.check_run_against_oracle(dec, wl.shape, pr[0], z[0], run, 0, wl.gamma)
+        assert dd.sync_status() == (0, 0)
+        runs.append(run)
+    folded, unfolded = runs
+    parity.check_logits(folded.prefill_logits[0], unfolded.prefill_logits[0].astype(np.float64),
+                        wl.shape, "prefill")
+    compared = 0
+    for i, (ra, rb) in enumerate(zip(folded.rounds, unfolded.rounds)):
+        if not (np.array_equal(ra.drafts, rb.drafts) and np.array_equal(ra.targets, rb.targets)):
+            break
+        for j in range(ra.draft_logits.shape[1]):
+            parity.check_logits(ra.draft_logits[0, j], rb.draft_logits[0, j].astype(np.float64),
+                                wl.shape, f"round {i} draft {j}")
+        compared += 1
+    assert compared >= 1
