@@ -66,7 +66,10 @@ __device__ __forceinline__ RowPair<WT> row_pair(const LinearArgs& a, bool gated,
     const int c0 = h * a.d_head + i;
     r.n0 = mat * a.n_per + c0;
     r.n1 = r.n0 + half;
-    r.w0 = reinterpret_cast<const WT*>(a.w[mat]) + (size_t)c0 * K;
+    // select among the three matrix pointers (an indexed a.w[mat] would be fetched from the
+    // argument buffer by a vector load, making the weight loads wait for the inputs)
+    const void* base = mat == 0 ? a.w[0] : (mat == 1 ? a.w[1] : a.w[2]);
+    r.w0 = reinterpret_cast<const WT*>(base) + (size_t)c0 * K;
     r.w1 = r.w0 + (size_t)half * K;
     return r;
   }
@@ -98,18 +101,47 @@ __device__ __forceinline__ void store_kv_pair(const LinearArgs& a, int page, int
   store_elem(base + i + half, e1);
 }
 
-// Rotary (q, k) and the store of one pair of input row `row`: columns c0 and c0 + d_head/2 of
-// matrix mat (0 = q -> y, 1 = k, 2 = v -> the row's page).
-__device__ __forceinline__ void qkv_store_pair(const LinearArgs& a, int mat, int c0, int row,
-                                               float e0, float e1) {
-  const int half = a.d_head >> 1;
-  const int h = c0 / a.d_head, i = c0 - h * a.d_head;
+// Where the pair (c0, c0 + d_head/2) of input row `row` goes: the row's position, its rotary
+// factors and the page entry that holds it.  Split in two so that a kernel can request the
+// sequence length before its weights and the dependent page-table and rotary entries right after
+// them (every load is clamped to a valid address; validity is decided at the store).
+struct QkvPre {
+  int pos, page;
+  float cs, sn;
+};
+
+__device__ __forceinline__ int qkv_pos(const LinearArgs& a, int row) {
   const int b = row / a.C, j = row - b * a.C;
-  const int pos = a.kv.seq_len[b] + a.kv.pos_off + j;
+  return a.kv.seq_len[b] + a.kv.pos_off + j;
+}
+
+__device__ __forceinline__ QkvPre qkv_pre(const LinearArgs& a, int mat, int c0, int row, int pos) {
+  QkvPre p;
+  p.pos = pos;
+  p.cs = 1.f;
+  p.sn = 0.f;
+  const int half = a.d_head >> 1;
+  const int i = c0 % a.d_head;
   if (mat < 2 && a.rope_cos) {
     const int tp = pos < 0 ? 0 : (pos >= a.max_seq ? a.max_seq - 1 : pos);
-    const float cs = a.rope_cos[(size_t)tp * half + i], sn = a.rope_sin[(size_t)tp * half + i];
-    const float r0 = e0 * cs - e1 * sn, r1 = e1 * cs + e0 * sn;
+    p.cs = a.rope_cos[(size_t)tp * half + i];
+    p.sn = a.rope_sin[(size_t)tp * half + i];
+  }
+  const int b = row / a.C;
+  const int pg_i = pos >= 0 ? pos / a.kv.page_size : 0;
+  p.page = a.kv.page_table[(size_t)b * a.kv.max_pages + min(pg_i, a.kv.max_pages - 1)];
+  return p;
+}
+
+// Rotary (q, k) and the store of one pair of input row `row`: columns c0 and c0 + d_head/2 of
+// matrix mat (0 = q -> y, 1 = k, 2 = v -> the row's page).  A position past the cache or an
+// unmapped page sets a status bit and skips the KV store.
+__device__ __forceinline__ void qkv_store_pre(const LinearArgs& a, int mat, int c0, int row,
+                                              const QkvPre& p, float e0, float e1) {
+  const int half = a.d_head >> 1;
+  const int h = c0 / a.d_head, i = c0 - h * a.d_head;
+  if (mat < 2 && a.rope_cos) {
+    const float r0 = e0 * p.cs - e1 * p.sn, r1 = e1 * p.cs + e0 * p.sn;
     e0 = r0;
     e1 = r1;
   }
@@ -118,21 +150,23 @@ __device__ __forceinline__ void qkv_store_pair(const LinearArgs& a, int mat, int
     a.y[(size_t)row * a.ldy + c0 + half] = e1;
     return;
   }
-  const int pg_i = pos >= 0 ? pos / a.kv.page_size : -1;
-  int page = -1;
-  if (pos < 0 || pos >= a.max_seq || pg_i >= a.kv.max_pages) {
+  const int pos = p.pos;
+  if (pos < 0 || pos >= a.max_seq || pos / a.kv.page_size >= a.kv.max_pages) {
     atomicOr(a.status, SSD_DEV_CAPACITY);
-  } else {
-    page = a.kv.page_table[(size_t)b * a.kv.max_pages + pg_i];
-    if (page < 0 || page >= a.kv.n_pages) {
-      atomicOr(a.status, SSD_DEV_BAD_PAGE);
-      page = -1;
-    }
+    return;
   }
-  if (page < 0) return;
-  const int slot = pos - pg_i * a.kv.page_size;
-  if (a.kvdtype == 1) store_kv_pair<bf16_t>(a, page, slot, h, i, half, mat == 2, e0, e1);
-  else store_kv_pair<float>(a, page, slot, h, i, half, mat == 2, e0, e1);
+  if (p.page < 0 || p.page >= a.kv.n_pages) {
+    atomicOr(a.status, SSD_DEV_BAD_PAGE);
+    return;
+  }
+  const int slot = pos % a.kv.page_size;
+  if (a.kvdtype == 1) store_kv_pair<bf16_t>(a, p.page, slot, h, i, half, mat == 2, e0, e1);
+  else store_kv_pair<float>(a, p.page, slot, h, i, half, mat == 2, e0, e1);
+}
+
+__device__ __forceinline__ void qkv_store_pair(const LinearArgs& a, int mat, int c0, int row,
+                                               float e0, float e1) {
+  qkv_store_pre(a, mat, c0, row, qkv_pre(a, mat, c0, row, qkv_pos(a, row)), e0, e1);
 }
 
 template <int MB>
@@ -206,7 +240,8 @@ __device__ __forceinline__ void gemv_finish(const LinearArgs& a, const RowPair<W
                                             const float (&acc)[2][MB], const float (&yold)[2][MB],
                                             bool live, bool gated, bool argmax, int m0, int mrows,
                                             int tid, int lane, int wave, float (&rv)[GV_WAVES][MB],
-                                            int (&ri)[GV_WAVES][MB]) {
+                                            int (&ri)[GV_WAVES][MB], const QkvPre& pre = {},
+                                            bool use_pre = false) {
   float best_v[MB];
   int best_i[MB];
 #pragma unroll
@@ -228,7 +263,12 @@ __device__ __forceinline__ void gemv_finish(const LinearArgs& a, const RowPair<W
       }
     }
   } else if (lane == 0 && live && a.epi == EPI_QKV) {
-    qkv_epilogue<MB>(a, r.n0, acc, m0, mrows);
+    if (use_pre) {
+      const int HD = a.n_per, mat = r.n0 >= HD ? (r.n0 >= 2 * HD ? 2 : 1) : 0;
+      qkv_store_pre(a, mat, r.n0 - mat * HD, m0, pre, acc[0][0], acc[1][0]);
+    } else {
+      qkv_epilogue<MB>(a, r.n0, acc, m0, mrows);
+    }
   } else if (lane == 0 && live) {
 #pragma unroll
     for (int m = 0; m < MB; ++m) {
@@ -283,6 +323,9 @@ __device__ __forceinline__ void gemv_finish(const LinearArgs& a, const RowPair<W
 // hide the memory latency.
 // RMSNorm is folded: LDS holds gain * x and the per-row 1/rms multiplies the dot products in the
 // epilogue; LayerNorm inputs are normalised while staged.
+// (The wave index goes through readfirstlane in these kernels so that the compiler treats the
+// wave's row choice as uniform: the matrix pointers then come from scalar registers instead of
+// vector loads of the argument buffer that would wait for the inputs.)
 template <typename WT, int MB, int GV_KP>
 __global__ __launch_bounds__(256) void gemv_kernel(const LinearArgs a) {
   extern __shared__ float xs[];  // [MB][ldxs]
@@ -290,7 +333,7 @@ __global__ __launch_bounds__(256) void gemv_kernel(const LinearArgs a) {
   __shared__ float rv[GV_WAVES][MB];
   __shared__ int ri[GV_WAVES][MB];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int K = a.K;
   const int ldxs = (K + 7) & ~7;
   const int m0 = blockIdx.y * MB;
@@ -444,7 +487,7 @@ template <typename WT, int KP, int NORM>
 __global__ __launch_bounds__(256) void gemv1_kernel(const LinearArgs a) {
   __shared__ float rv[GV_WAVES][1];
   __shared__ int ri[GV_WAVES][1];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int K = a.K;
   const bool gated = (a.epi == EPI_GATED_GELU || a.epi == EPI_GATED_SILU);
   const bool argmax = a.epi == EPI_ARGMAX;
@@ -465,6 +508,8 @@ __global__ __launch_bounds__(256) void gemv1_kernel(const LinearArgs a) {
   }
   const RowPair<WT> r = row_pair<WT>(a, gated, n_total, pr < n_pairs ? pr : 0);
   const bool live = pr < n_pairs;
+  const bool qkv = a.epi == EPI_QKV;
+  const int qpos = qkv ? qkv_pos(a, 0) : 0;  // requested before the weights
   float yold[2][1] = {{0.f}, {0.f}};
   if (lane == 0 && live && (a.epi == EPI_RESID || a.epi == EPI_BIAS_RESID)) {
     const float* src = a.epi == EPI_RESID ? a.y : a.resid;
@@ -473,6 +518,11 @@ __global__ __launch_bounds__(256) void gemv1_kernel(const LinearArgs a) {
   }
   Vec8<WT> w[2][KP];
   load_pieces<WT, KP>(w, r, 0, K, lane);
+  QkvPre pre = {};
+  if (qkv) {
+    const int HD = a.n_per, mat = r.n0 >= HD ? (r.n0 >= 2 * HD ? 2 : 1) : 0;
+    pre = qkv_pre(a, mat, r.n0 - mat * HD, 0, qpos);
+  }
   Vec8<float> gv[rms || ln ? KP : 1], sv[ln ? KP : 1];
   if (rms || ln) {
 #pragma unroll
@@ -575,7 +625,8 @@ __global__ __launch_bounds__(256) void gemv1_kernel(const LinearArgs a) {
   }
   acc[0][0] = wave_sum(acc[0][0]) * rscale;
   acc[1][0] = wave_sum(acc[1][0]) * rscale;
-  gemv_finish<WT, 1>(a, r, acc, yold, live, gated, argmax, 0, 1, tid, lane, wave, rv, ri);
+  gemv_finish<WT, 1>(a, r, acc, yold, live, gated, argmax, 0, 1, tid, lane, wave, rv, ri, pre,
+                     qkv);
 }
 
 // One input row, 2048 <= K <= 2048 * KP (no LayerNorm): the K range is split
@@ -593,7 +644,7 @@ __global__ __launch_bounds__(256) void gemv1k_kernel(const LinearArgs a) {
   __shared__ float part[GV_WAVES][9];
   __shared__ float rv[GV_WAVES][1];
   __shared__ int ri[GV_WAVES][1];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int K = a.K;
   const bool gated = (a.epi == EPI_GATED_GELU || a.epi == EPI_GATED_SILU);
   const bool argmax = a.epi == EPI_ARGMAX;
@@ -614,6 +665,8 @@ __global__ __launch_bounds__(256) void gemv1k_kernel(const LinearArgs a) {
   const int pr = blockIdx.x * GV_WAVES + wave;
   const RowPair<WT> r = row_pair<WT>(a, gated, n_total, pr < n_pairs ? pr : 0);
   const bool live = pr < n_pairs;
+  const bool qkv = a.epi == EPI_QKV;
+  const int qpos = qkv ? qkv_pos(a, 0) : 0;  // requested before the weights
   float yold[2][1] = {{0.f}, {0.f}};
   if (lane == 0 && live && (a.epi == EPI_RESID || a.epi == EPI_BIAS_RESID)) {
     const float* src = a.epi == EPI_RESID ? a.y : a.resid;
@@ -636,6 +689,11 @@ __global__ __launch_bounds__(256) void gemv1k_kernel(const LinearArgs a) {
   if (rms) {
 #pragma unroll
     for (int p = 0; p < KP; ++p) gv[p].load(a.gain + min(p * 2048 + wave * 512 + lane * 8, K - 8));
+  }
+  QkvPre pre = {};
+  if (qkv) {
+    const int HD = a.n_per, mat = r.n0 >= HD ? (r.n0 >= 2 * HD ? 2 : 1) : 0;
+    pre = qkv_pre(a, mat, r.n0 - mat * HD, 0, qpos);
   }
 
   // pieces past K (clamped re-reads) count as zero
@@ -711,7 +769,8 @@ __global__ __launch_bounds__(256) void gemv1k_kernel(const LinearArgs a) {
   float res[2][1];
   res[0][0] = ((part[0][2 * wave] + part[1][2 * wave]) + (part[2][2 * wave] + part[3][2 * wave])) * rscale;
   res[1][0] = ((part[0][2 * wave + 1] + part[1][2 * wave + 1]) + (part[2][2 * wave + 1] + part[3][2 * wave + 1])) * rscale;
-  gemv_finish<WT, 1>(a, r, res, yold, live, gated, argmax, 0, 1, tid, lane, wave, rv, ri);
+  gemv_finish<WT, 1>(a, r, res, yold, live, gated, argmax, 0, 1, tid, lane, wave, rv, ri, pre,
+                     qkv);
 }
 
 // ---------------------------------------------------------------------------------------------
@@ -742,7 +801,7 @@ __global__ __launch_bounds__(64 * SKW) void gemv_mfma_kernel(const LinearArgs a)
   __shared__ float sq[4][16];
   __shared__ float ssq_red[4 * SKW][16];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int K = a.K, M = a.M;
   const int n_out = GATED ? a.n_per : a.n_per * a.n_mats;
   const bool qkv = !GATED && a.epi == EPI_QKV;
