@@ -87,7 +87,7 @@ def counted_traffic(kernel: str):
     missing or the kernel source has changed since the counters were taken."""
     import hashlib
     import re
-    path = os.path.join(ROOT, "profiles", "gemv1_c3_flant5_xl_hbm_traffic.md")
+    path = os.path.join(ROOT, "profiles", "gemv1k_c3_flant5_xl_hbm_traffic.md")
     src = os.path.join(ROOT, "paper_2510_22641_amd", "csrc", "linear.hip")
     if not os.path.exists(path):
         return None
@@ -137,9 +137,9 @@ def sweep_c4(args):
     from paper_2510_22641_amd import runtime
     pts = synth.c4_points()
     weights = synth.workload_weights(pts[0], args.seed)
-    for k in sorted({p.draft_layers for p in pts}):
-        group = [p for p in pts if p.draft_layers == k]
-        mb = max(p.batch for p in group)
+    # one context per (draft depth, batch): a one-sequence context folds the cross-attention
+    for k, mb in sorted({(p.draft_layers, p.batch) for p in pts}):
+        group = [p for p in pts if p.draft_layers == k and p.batch == mb]
         dd = runtime.from_workload(group[0], args.seed, weights=weights, max_batch=mb,
                                    max_gamma=max(p.gamma for p in group))
         for wl in group:
