@@ -220,6 +220,9 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--cpu-seconds", type=float, default=20.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--persistent", type=int, choices=[0, 1], default=None,
+                    help="force the persistent one-row pass on (1) or off (0); default: the "
+                         "library's choice")
     ap.add_argument("--sweep", choices=["c4"], default=None,
                     help="run the FlanT5-xl sweep instead (one JSON line per point)")
     ap.add_argument("--copy-bytes", type=int, default=0,
@@ -258,6 +261,8 @@ def main():
     visual = synth.make_visual(sh, args.seed, wl.batch)
     # capacity for the dynamic draft length too (up to gamma + 9 drafts a round)
     dd = runtime.from_workload(wl, args.seed, weights=weights, max_gamma=wl.gamma + 9)
+    if args.persistent is not None:
+        dd.set_persistent(bool(args.persistent))
     pt, vt = dd.upload_inputs(prompts, visual)
     torch.cuda.synchronize()
     print(f"[bench] setup {time.time() - t_setup:.1f}s", file=sys.stderr, flush=True)

@@ -55,8 +55,9 @@ enum { SSD_ARCH_T5 = 0, SSD_ARCH_LLAMA = 1 };
 enum { SSD_F32 = 0, SSD_BF16 = 1 };
 enum { SSD_MODE_GREEDY = 0, SSD_MODE_SPECULATIVE = 1, SSD_MODE_SPECULATIVE_DYNAMIC = 2 };
 
-/* device status bits (ssd_sync_status, ssd_device_status) */
-enum { SSD_DEV_BAD_TOKEN = 1, SSD_DEV_CAPACITY = 2, SSD_DEV_BAD_PAGE = 4 };
+/* device status bits (ssd_sync_status, ssd_device_status); SSD_DEV_SYNC: a grid-barrier wait of
+ * the persistent one-row pass exceeded its bound (ssd_set_persistent) */
+enum { SSD_DEV_BAD_TOKEN = 1, SSD_DEV_CAPACITY = 2, SSD_DEV_BAD_PAGE = 4, SSD_DEV_SYNC = 8 };
 
 /* Decoder and context dimensions, copied at ssd_create. */
 typedef struct {
@@ -200,7 +201,22 @@ int ssd_dynamic_gamma(int t, int d0, int n_max);
  * or launch kernels one by one (0). */
 int ssd_set_graphs(ssd_ctx* ctx, int enable);
 
-/* Kernel timing for roofline reports.  While enabled (and graphs are bypassed), every launch of
+/* One-row passes of one-sequence calls (B = 1) — each draft step of ssd_draft, ssd_verify with
+ * gamma = 0 (a greedy step) and the one-row part of a reusing ssd_verify — run as ONE persistent
+ * kernel launch (one block per compute unit, phases separated by grid barriers) instead of a
+ * chain of kernels (1), or as the chain (0, default: on MI355X the chain is faster).  The persistent pass exists when the
+ * shapes allow it (every row the pass stages fits 12288 floats, d_model <= 6144, T5: the
+ * cross-attention is folded, i.e. max_batch = 1 and 8/16/32/64 visual tokens) and the device
+ * keeps one block per compute unit resident; T5 contexts use it after ssd_prefill.  Both paths
+ * compute the same decoder (the same parity tolerances apply).  A barrier wait that exceeds its
+ * bound (about a second) sets SSD_DEV_SYNC; the context must then be re-created.  Returns 1 when
+ * the persistent pass will be used, 0 when not, SSD_ERR_ARG for a null context. */
+int ssd_set_persistent(ssd_ctx* ctx, int enable);
+
+/* Kernel timing for roofline reports.  With the persistent pass active (ssd_set_persistent), the
+ * timed launches are the persistent draft steps and the bytes are the pass's weights, input rows
+ * and output rows (KV-cache reads are not counted).  Otherwise, while enabled (and graphs are
+ * bypassed), every launch of
  * the one-row weight-streaming GEMV that streams the RMS-normalised d_model-wide matrices (QKV,
  * cross-attention query, gate/up, LM head; the kernel that carries most of a batch-1 draft step:
  * gemv1k_kernel<unsigned short, KP, 1> with KP = ceil(d_model / 2048) for bf16 weights and

@@ -33,7 +33,7 @@ struct Layout {
   size_t x, x1, qkv, q, attn, ffn, inh, xi, stash, vis, part_val, part_idx, stats, bias_tab,
       p_x, p_attn, p_ffn, ssq, attn_part, fold_q, fold_o,
       bucket, rope_cos, rope_sin, status, cur_tok, g_pending, g_draft, g_target,
-      g_count, g_active, g_nactive, g_stats, total;
+      g_count, g_active, g_nactive, g_stats, step_prog, step_arena, step_sync, total;
   int rows_max, head_rows, parts_max, ctx_max, plane_rows, attn_rows;
 };
 
@@ -48,6 +48,47 @@ int ctx_len_max(const ssd_dims& d) {
 bool fold_cross(const ssd_dims& d) {
   return d.arch == SSD_ARCH_T5 && d.max_batch == 1 && cross_fold_ok(d.n_visual, d.d_head) &&
          d.n_visual <= d.d_head && (size_t)d.n_heads * d.n_visual <= 6144 && d.d_model <= 6144;
+}
+
+// Persistent one-row passes (step.hip): one phase list per kind of pass.
+enum { STEP_DRAFT = 0, STEP_GREEDY = 1, STEP_VROW = 2, STEP_KINDS = 3 };
+
+// synchronisation area of the persistent passes (bytes from L.step_sync)
+constexpr size_t SYNC_FLAGS = 0, SYNC_ABORT = 1040, SYNC_COUNTER = 1044, SYNC_PART_VAL = 1280,
+                 SYNC_PART_IDX = 2304, SYNC_BYTES = 3328;
+
+int step_keys_per_split(const ssd_dims& d) {
+  return 16 * step_attn_passes(d.d_head, d.kvdtype == SSD_BF16 ? 2 : 4);
+}
+
+int step_splits(const ssd_dims& d) {
+  const int ks = step_keys_per_split(d);
+  return (d.max_seq + ks - 1) / ks;
+}
+
+int step_max_phases(const ssd_dims& d) { return d.n_layers * 8 + 4; }
+
+// Shapes the persistent pass handles: every staged row fits its LDS buffers, the residual row
+// its LDS copy, and (T5) the cross-attention is folded with a softmax group the stager supports.
+bool step_dims_ok(const ssd_dims& d) {
+  const int HD = d.n_heads * d.d_head;
+  auto kok = [](int K) { return K >= 8 && K <= STEP_XS_MAX && K % 8 == 0; };
+  if (d.d_model > STEP_XRES_MAX) return false;
+  if (!kok(d.d_model) || !kok(HD) || !kok(d.d_ff) || !kok(d.in_hidden)) return false;
+  if (d.arch == SSD_ARCH_T5) {
+    if (!fold_cross(d) || !kok(d.n_heads * d.n_visual)) return false;
+    if (d.n_visual != 8 && d.n_visual != 16 && d.n_visual != 32 && d.n_visual != 64) return false;
+  }
+  return step_splits(d) <= STEP_MAX_SPLITS;
+}
+
+// Upper bound of the floats one pass writes to its arena (every phase output at a fresh address).
+size_t step_arena_floats(const ssd_dims& d) {
+  const size_t HD = (size_t)d.n_heads * d.d_head, D = d.d_model, S = step_splits(d);
+  auto a = [](size_t n) { return align_up(n, 64); };
+  size_t per = a(HD) + a((size_t)d.n_heads * S * (d.d_head + 4)) + a(HD) + a(D) + a(d.d_ff) + a(D);
+  if (d.arch == SSD_ARCH_T5) per += a((size_t)d.n_heads * d.n_visual) + a(D);
+  return per * d.n_layers + a(d.in_hidden) + a(D) + 256;
 }
 
 bool make_layout(const ssd_dims& d, Layout& L) {
@@ -107,6 +148,12 @@ bool make_layout(const ssd_dims& d, Layout& L) {
   L.g_active = take(B * 4);
   L.g_nactive = take(8);
   L.g_stats = take(3 * 8);
+  {
+    const bool st = step_dims_ok(d);
+    L.step_prog = take(st ? (size_t)STEP_KINDS * step_max_phases(d) * sizeof(StepPhase) : 0);
+    L.step_arena = take(st ? step_arena_floats(d) * 4 : 0);
+    L.step_sync = take(st ? SYNC_BYTES : 0);
+  }
   L.total = off;
   return true;
 }
@@ -164,6 +211,12 @@ struct ssd_ctx {
   const int32_t* draft_out = nullptr;
   bool use_graphs = true;
   std::map<GraphKey, hipGraphExec_t> graphs;
+  // persistent one-row passes: built at creation when the shape and the device allow them;
+  // off unless asked for (slower than the chain of kernels on MI355X, see step.hip)
+  bool step_ok = false;
+  bool use_step = false;
+  int step_n[STEP_KINDS] = {0, 0, 0};
+  double step_bytes[STEP_KINDS] = {0.0, 0.0, 0.0};
   // kernel timing (ssd_profile_enable)
   bool profiling = false;
   std::vector<hipEvent_t> ev_pool;
@@ -229,6 +282,198 @@ LinearArgs lin(ssd_ctx* c) {
   a.stats = c->at<float2>(c->L.stats);
   a.eps = c->d.norm_eps;
   return a;
+}
+
+// Phase list of a persistent one-row pass (batch 1):
+//   STEP_DRAFT   embed(token) -> layers 1..k (the residual after layer k also to the stash) ->
+//                imitation network -> g -> argmax;
+//   STEP_GREEDY  embed(token) -> layers 1..L -> g -> argmax;
+//   STEP_VROW    embed(token) -> layers 1..k, the residual after layer k to x1.
+// Per layer: QKV (+ rotary, KV store) | attention split over keys | [merge] | W_o + residual |
+// (T5) folded cross-attention scores | folded cross-attention output + residual | gate/up |
+// down + residual.  Every phase output goes to a fresh address of the arena.
+std::vector<StepPhase> step_program(ssd_ctx* c, int kind, double* bytes, bool* fits) {
+  const ssd_dims& d = c->d;
+  const bool t5 = d.arch == SSD_ARCH_T5;
+  const int D = d.d_model, H = d.n_heads, dh = d.d_head, HD = H * dh;
+  const int S = step_splits(d);
+  float* arena = c->at<float>(c->L.step_arena);
+  size_t off = 0;
+  auto out = [&](size_t n) {
+    float* p = arena + off;
+    off += align_up(n, 64);
+    return p;
+  };
+  std::vector<StepPhase> P;
+  double total = 0.0;
+  auto push = [&](StepPhase ph) {
+    if (ph.type == SP_GEMV) {
+      const bool gated = ph.epi == EPI_GATED_GELU || ph.epi == EPI_GATED_SILU;
+      const double rows = gated ? 2.0 * ph.n_per : (double)ph.n_per * ph.n_mats;
+      const double outs = ph.epi == EPI_ARGMAX ? 0.0 : (gated ? (double)ph.n_per : rows);
+      ph.bytes = rows * ph.K * (ph.wdtype == SSD_F32 ? 4.0 : 2.0) + 4.0 * ph.K + 4.0 * outs +
+                 (ph.epi == EPI_RESID ? 4.0 * outs : 0.0);
+    }
+    total += ph.bytes;
+    P.push_back(ph);
+  };
+  auto pairs = [](int n) { return (n + 1) / 2; };
+  const int nl = kind == STEP_GREEDY ? d.n_layers : d.draft_layers;
+  const float* xcur = nullptr;  // the residual row; null: the token's embedding
+  for (int l = 0; l < nl; ++l) {
+    const ssd_layer_weights& lw = c->layers[l];
+    StepPhase q;
+    if (xcur) { q.in_kind = SI_VEC; q.x = xcur; } else { q.in_kind = SI_EMBED; }
+    q.K = D; q.norm = NORM_RMS; q.gain = lw.attn_norm; q.eps = d.norm_eps; q.in_resid = 1;
+    q.w[0] = lw.wq; q.w[1] = lw.wk; q.w[2] = lw.wv; q.n_mats = 3; q.n_per = HD;
+    q.wdtype = d.wdtype; q.epi = EPI_QKV; q.n_tasks = 3 * HD / 2; q.y = out(HD); q.layer = l;
+    push(q);
+    StepPhase at;
+    at.type = SP_ATTN; at.q = q.y; at.part = out((size_t)H * S * (dh + 4)); at.n_splits = S;
+    at.keys_per_split = step_keys_per_split(d); at.layer = l; at.n_tasks = H * S;
+    push(at);
+    StepPhase o;
+    if (S <= STEP_INLINE_SPLITS) {
+      o.in_kind = SI_ATTN; o.x = at.part; o.n_splits = S;
+    } else {
+      StepPhase cb;
+      cb.type = SP_COMBINE; cb.part = at.part; cb.n_splits = S; cb.n_tasks = H; cb.y = out(HD);
+      push(cb);
+      o.in_kind = SI_VEC; o.x = cb.y;
+    }
+    o.K = HD; o.norm = NORM_NONE; o.w[0] = lw.wo; o.n_per = D; o.wdtype = d.wdtype;
+    o.epi = EPI_RESID; o.n_tasks = pairs(D); o.y = out(D);
+    push(o);
+    xcur = o.y;
+    if (t5) {
+      const int HN = H * d.n_visual;
+      StepPhase fq;
+      fq.in_kind = SI_VEC; fq.x = xcur; fq.K = D; fq.norm = NORM_RMS; fq.gain = lw.xattn_norm;
+      fq.eps = d.norm_eps; fq.in_resid = 1;
+      fq.w[0] = c->at<float>(c->L.fold_q) + (size_t)l * c->fold_layer_elems(); fq.n_per = HN;
+      fq.wdtype = SSD_F32; fq.epi = EPI_STORE; fq.n_tasks = pairs(HN); fq.y = out(HN);
+      push(fq);
+      StepPhase fo;
+      fo.in_kind = SI_VEC; fo.x = fq.y; fo.K = HN; fo.norm = NORM_SOFTMAX; fo.group = d.n_visual;
+      fo.w[0] = c->at<float>(c->L.fold_o) + (size_t)l * c->fold_layer_elems(); fo.n_per = D;
+      fo.wdtype = SSD_F32; fo.epi = EPI_RESID; fo.n_tasks = pairs(D); fo.y = out(D);
+      push(fo);
+      xcur = fo.y;
+    }
+    StepPhase gu;
+    gu.in_kind = SI_VEC; gu.x = xcur; gu.K = D; gu.norm = NORM_RMS; gu.gain = lw.ffn_norm;
+    gu.eps = d.norm_eps; gu.in_resid = 1;
+    gu.w[0] = lw.w_gate; gu.w[1] = lw.w_up; gu.n_mats = 2; gu.n_per = d.d_ff; gu.wdtype = d.wdtype;
+    gu.epi = t5 ? EPI_GATED_GELU : EPI_GATED_SILU; gu.n_tasks = d.d_ff; gu.y = out(d.d_ff);
+    push(gu);
+    StepPhase dn;
+    dn.in_kind = SI_VEC; dn.x = gu.y; dn.K = d.d_ff; dn.norm = NORM_NONE;
+    dn.w[0] = lw.w_down; dn.n_per = D; dn.wdtype = d.wdtype; dn.epi = EPI_RESID;
+    dn.n_tasks = pairs(D);
+    dn.y = (kind == STEP_VROW && l == nl - 1) ? c->at<float>(c->L.x1) : out(D);
+    dn.to_stash = (kind == STEP_DRAFT && l == nl - 1) ? 1 : 0;
+    push(dn);
+    xcur = dn.y;
+  }
+  if (kind == STEP_DRAFT) {
+    // imitation network: LN -> FC1 + b1 -> GELU -> FC2 + b2 (+ the residual)
+    StepPhase i1;
+    i1.in_kind = SI_VEC; i1.x = xcur; i1.K = D; i1.norm = NORM_LN; i1.gain = c->w.in_ln_w;
+    i1.shift = c->w.in_ln_b; i1.eps = d.ln_eps; i1.in_resid = 1;
+    i1.w[0] = c->w.in_w1; i1.n_per = d.in_hidden; i1.wdtype = d.wdtype; i1.epi = EPI_BIAS_GELU;
+    i1.bias = c->w.in_b1; i1.n_tasks = pairs(d.in_hidden); i1.y = out(d.in_hidden);
+    push(i1);
+    StepPhase i2;
+    i2.in_kind = SI_VEC; i2.x = i1.y; i2.K = d.in_hidden; i2.norm = NORM_NONE;
+    i2.w[0] = c->w.in_w2; i2.n_per = D; i2.wdtype = d.wdtype; i2.epi = EPI_BIAS_RESID;
+    i2.bias = c->w.in_b2; i2.bias_resid = d.in_residual ? 1 : 0; i2.n_tasks = pairs(D);
+    i2.y = out(D);
+    push(i2);
+    xcur = i2.y;
+  }
+  if (kind != STEP_VROW) {
+    StepPhase hd;
+    hd.in_kind = SI_VEC; hd.x = xcur; hd.K = D; hd.norm = NORM_RMS; hd.gain = c->w.final_norm;
+    hd.eps = d.norm_eps; hd.w[0] = c->w.lm_head; hd.n_per = d.vocab; hd.wdtype = d.wdtype;
+    hd.epi = EPI_ARGMAX; hd.n_tasks = pairs(d.vocab);
+    push(hd);
+  }
+  *bytes = total;
+  *fits = off <= step_arena_floats(d) && (int)P.size() <= step_max_phases(d);
+  return P;
+}
+
+// Build the phase lists into the workspace and clear the synchronisation area.
+int build_step_programs(ssd_ctx* c) {
+  c->step_ok = false;
+  if (!step_dims_ok(c->d) || step_blocks() <= 0) return SSD_OK;
+  StepPhase* prog = c->at<StepPhase>(c->L.step_prog);
+  for (int kind = 0; kind < STEP_KINDS; ++kind) {
+    bool fits = false;
+    double bytes = 0.0;
+    std::vector<StepPhase> P = step_program(c, kind, &bytes, &fits);
+    if (!fits) return SSD_OK;
+    HIP_TRY(hipMemcpyAsync(prog + (size_t)kind * step_max_phases(c->d), P.data(),
+                           P.size() * sizeof(StepPhase), hipMemcpyHostToDevice, c->stream));
+    c->step_n[kind] = (int)P.size();
+    c->step_bytes[kind] = bytes;
+  }
+  HIP_TRY(hipMemsetAsync(c->ws + c->L.step_sync, 0, SYNC_BYTES, c->stream));
+  HIP_TRY(hipStreamSynchronize(c->stream));
+  c->step_ok = true;
+  return SSD_OK;
+}
+
+// One-row passes of a one-sequence call take the persistent kernel (T5 once the cross-attention
+// is folded, i.e. after prefill).
+bool use_step_now(const ssd_ctx* c, int B) {
+  return c->step_ok && c->use_step && B == 1 &&
+         (c->d.arch == SSD_ARCH_LLAMA || c->fold_ready);
+}
+
+StepArgs step_args(ssd_ctx* c, int kind) {
+  const ssd_dims& d = c->d;
+  StepArgs a;
+  a.phases = c->at<StepPhase>(c->L.step_prog) + (size_t)kind * step_max_phases(d);
+  a.n_phases = c->step_n[kind];
+  char* sync = c->ws + c->L.step_sync;
+  a.flags = reinterpret_cast<uint32_t*>(sync + SYNC_FLAGS);
+  a.abort_word = reinterpret_cast<uint32_t*>(sync + SYNC_ABORT);
+  a.counter = reinterpret_cast<uint32_t*>(sync + SYNC_COUNTER);
+  a.part_val = reinterpret_cast<float*>(sync + SYNC_PART_VAL);
+  a.part_idx = reinterpret_cast<int*>(sync + SYNC_PART_IDX);
+  a.spin_limit = 1u << 21;
+  a.embed = c->w.embed; a.vocab = d.vocab; a.d_model = d.d_model; a.wdtype = d.wdtype;
+  a.seq_len = c->kv.seq_len;
+  a.k_pool = c->kv.k_pool; a.v_pool = c->kv.v_pool; a.layer_elems = c->kv_layer_elems();
+  a.page_table = c->kv.page_table; a.max_pages = d.max_pages; a.page_size = d.page_size;
+  a.n_pages = c->kv.n_pages; a.n_heads = d.n_heads; a.d_head = d.d_head; a.max_seq = d.max_seq;
+  const bool t5 = d.arch == SSD_ARCH_T5;
+  a.rope_cos = t5 ? nullptr : c->at<float>(c->L.rope_cos);
+  a.rope_sin = t5 ? nullptr : c->at<float>(c->L.rope_sin);
+  a.bias_tab = t5 ? c->at<float>(c->L.bias_tab) : nullptr;
+  a.attn_scale = t5 ? 1.0f : (float)(1.0 / std::sqrt((double)d.d_head));
+  a.status = c->at<int32_t>(c->L.status);
+  return a;
+}
+
+// Launch a persistent pass; when profiling, draft-step launches carry events bound to their own
+// dispatch and add the pass's algorithmic bytes (weights and rows; the KV reads are not counted).
+int run_step(ssd_ctx* c, int kind, const StepArgs& a) {
+  if (!c->profiling || kind != STEP_DRAFT) {
+    HIP_TRY(launch_step(a, c->d.kvdtype, c->stream));
+    return SSD_OK;
+  }
+  while (c->ev_pool.size() < c->ev_used + 2) {
+    hipEvent_t e;
+    HIP_TRY(hipEventCreate(&e));
+    c->ev_pool.push_back(e);
+  }
+  HIP_TRY(launch_step(a, c->d.kvdtype, c->stream, c->ev_pool[c->ev_used], c->ev_pool[c->ev_used + 1]));
+  c->ev_used += 2;
+  c->prof_bytes += c->step_bytes[kind];
+  c->prof_launches += 1;
+  return SSD_OK;
 }
 
 // Layers l0..l1-1 over rows r = b*C + j at positions seq_len[b] + pos_off + j.  When stash is set
@@ -405,6 +650,20 @@ int draft_launches(ssd_ctx* c, int B, int gamma, const int32_t* pending, int32_t
   float* stash = c->at<float>(c->L.stash);
   int32_t* cur = c->at<int32_t>(c->L.cur_tok);
   const int ld_stash = (d.max_gamma + 1) * D;
+  if (use_step_now(c, B)) {
+    for (int i = 0; i < gamma; ++i) {
+      StepArgs a = step_args(c, STEP_DRAFT);
+      a.tok = i == 0 ? pending : cur;
+      a.pos_off = i;
+      a.stash = stash + (size_t)i * D;
+      a.dst0 = draft + i;
+      a.dst1 = cur;
+      a.logits = logits ? logits + (size_t)i * d.vocab : nullptr;
+      const int rc = run_step(c, STEP_DRAFT, a);
+      if (rc) return rc;
+    }
+    return SSD_OK;
+  }
   for (int i = 0; i < gamma; ++i) {
     EmbedArgs e;
     e.x = x; e.B = B; e.C = 1; e.d = D; e.embed = c->w.embed; e.vocab = d.vocab;
@@ -445,6 +704,16 @@ int verify_launches(ssd_ctx* c, int B, int gamma, const int32_t* pending, const 
   e.visual = nullptr; e.n_visual = d.n_visual; e.n_prefix = 0;
   e.status = c->at<int32_t>(c->L.status);
   int rc;
+  if (gamma == 0 && use_step_now(c, B)) {
+    // one greedy step: the whole decoder, g and the argmax in one persistent pass
+    StepArgs a = step_args(c, STEP_GREEDY);
+    a.tok = pending;
+    a.pos_off = 0;
+    a.dst0 = target;
+    a.dst1 = nullptr;
+    a.logits = logits;
+    return run_step(c, STEP_GREEDY, a);
+  }
   if (!reuse) {
     HIP_TRY(launch_embed(e, c->stream));
     rc = run_layers(c, x, B, C, 0, 0, d.n_layers, -1, nullptr, 0);
@@ -452,9 +721,16 @@ int verify_launches(ssd_ctx* c, int B, int gamma, const int32_t* pending, const 
   } else {
     // layers 1..k only for the last position; the others come from the draft's layer-k states
     float* x1 = c->at<float>(c->L.x1);
-    e.x = x1; e.C = 1; e.t0 = nullptr; e.t1 = draft + (gamma - 1); e.ld1 = gamma;
-    HIP_TRY(launch_embed(e, c->stream));
-    rc = run_layers(c, x1, B, 1, gamma, 0, d.draft_layers, -1, nullptr, 0);
+    if (use_step_now(c, B)) {
+      StepArgs a = step_args(c, STEP_VROW);
+      a.tok = draft + (gamma - 1);
+      a.pos_off = gamma;
+      rc = run_step(c, STEP_VROW, a);
+    } else {
+      e.x = x1; e.C = 1; e.t0 = nullptr; e.t1 = draft + (gamma - 1); e.ld1 = gamma;
+      HIP_TRY(launch_embed(e, c->stream));
+      rc = run_layers(c, x1, B, 1, gamma, 0, d.draft_layers, -1, nullptr, 0);
+    }
     if (rc) return rc;
     HIP_TRY(launch_assemble(x, c->at<float>(c->L.stash), (d.max_gamma + 1) * D, x1, B, gamma, D,
                             c->stream));
@@ -569,6 +845,7 @@ int ssd_create(const ssd_dims* dims, const ssd_weights* w, const ssd_kv* kv, voi
       (hipMemsetAsync(c->at<int32_t>(L.status), 0, 4, c->stream) != hipSuccess ||
        hipStreamSynchronize(c->stream) != hipSuccess))
     rc = SSD_ERR_HIP;
+  if (rc == SSD_OK) rc = build_step_programs(c);
   if (rc != SSD_OK) {
     delete c;
     return rc;
@@ -750,6 +1027,17 @@ int ssd_set_graphs(ssd_ctx* c, int enable) {
   if (!c) return SSD_ERR_ARG;
   c->use_graphs = enable != 0;
   return SSD_OK;
+}
+
+int ssd_set_persistent(ssd_ctx* c, int enable) {
+  if (!c) return SSD_ERR_ARG;
+  if (c->use_step != (enable != 0)) {
+    // captured launch sequences differ between the two paths
+    for (auto& kv : c->graphs) (void)hipGraphExecDestroy(kv.second);
+    c->graphs.clear();
+  }
+  c->use_step = enable != 0;
+  return (c->step_ok && c->use_step) ? 1 : 0;
 }
 
 int ssd_profile_enable(ssd_ctx* c, int enable) {

@@ -223,6 +223,10 @@ class DeviceDecoder:
     def set_graphs(self, enable: bool):
         abi.ssd_set_graphs(self.ctx, enable)
 
+    def set_persistent(self, enable: bool) -> bool:
+        """One-row passes of one-sequence calls as one persistent launch; True when active."""
+        return abi.ssd_set_persistent(self.ctx, enable)
+
     def sync_status(self):
         torch.cuda.current_stream(self.device).synchronize()
         return abi.ssd_sync_status(self.ctx)
