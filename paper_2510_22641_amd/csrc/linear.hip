@@ -775,26 +775,32 @@ __global__ __launch_bounds__(256) void gemv1k_kernel(const LinearArgs a) {
 
 // ---------------------------------------------------------------------------------------------
 // Skinny MFMA path: 2..128 input rows (the verify chunk), bf16 weights, 16 rows per grid row.
-// A block owns 16 output features (the A rows of v_mfma_f32_16x16x32_bf16) and its 4 waves split
-// K; the input rows are the B columns.  The inputs arrive as two bf16 planes hi = bf16(v),
-// lo = bf16(v - hi) of v = g * x (g the RMSNorm gain, or 1), written once by their producer;
-// multiplying both planes keeps the activations at about 16 mantissa bits while the weights are
-// read once.  RMSNorm is folded: 1/rms of each row comes from partial sums of squares the
-// producer left, and scales the outputs.  Per 64-element step a lane reads 32 contiguous bytes
-// of one weight row and 32 bytes of each plane; all loads of a batch (inputs first, then weights)
-// are issued before the first MFMA, and the 4 partial 16x16 tiles are summed through LDS before
-// the fused epilogue.  For EPI_QKV a block's rows r and r + 8 are the rotary pair (i, i + dh/2) of
-// one head, so rotary and the KV store are done here.  A residual epilogue also writes the next
-// launch's planes (of out_gain * y_new) and this block's partial sums of squares of y_new.
+// A block owns NT tiles of 16 output features (the A rows of v_mfma_f32_16x16x32_bf16) and its 4
+// waves split K; the input rows are the B columns, and every activation fragment a wave loads
+// feeds the MFMAs of all NT tiles.  One tile per block for the projections (their grids, 128-384
+// blocks, need the parallelism); four for the many tiles of the LM head, where the shared
+// activation loads pay (measured at the FlanT5-xl verify shapes, 6 rows: W_o 7.0 us with one tile
+// against 15.7 with four; LM head 39 against 35).  The inputs arrive as two bf16 planes
+// hi = bf16(v), lo = bf16(v - hi) of v = g * x (g the RMSNorm gain, or 1), written once by their
+// producer; multiplying both planes keeps the activations at about 16 mantissa bits while the
+// weights are read once.  RMSNorm is folded: 1/rms of each row comes from partial sums of squares
+// the producer left, and scales the outputs.  Per 64-element step a lane reads 32 contiguous
+// bytes of one row of each tile and 32 bytes of each plane; all loads of a batch (inputs first,
+// then weights) are issued before the first MFMA, and the 4 partial tiles are summed through LDS
+// before the fused epilogue.  For EPI_QKV a tile's rows r and r + 8 are the rotary pair
+// (i, i + dh/2) of one head, so rotary and the KV store are done here.  A residual epilogue also
+// writes the next launch's planes (of out_gain * y_new) and per-tile partial sums of squares of
+// y_new.
 constexpr int SKW = 4;  // waves per skinny block
 constexpr int SSQ_MAX = 256;  // partial sums of squares a skinny consumer reads (d_model <= 4096)
 
-template <bool GATED, bool RMS>
+template <bool GATED, bool RMS, int NT>
 __global__ __launch_bounds__(64 * SKW) void gemv_mfma_kernel(const LinearArgs a) {
   constexpr int NB = GATED ? 2 : 1;
-  constexpr int SK = GATED ? 4 : 8;  // 64-element steps per wave and batch
-  constexpr int NG = 4 * SKW;        // groups of 16 threads
-  __shared__ float part[SKW][NB][16][17];
+  constexpr int SK = (8 / (NT * NB)) > 0 ? 8 / (NT * NB) : 1;  // 64-element steps per batch
+  constexpr int NG = 4 * SKW;                                 // groups of 16 threads
+  __shared__ float part[SKW][NB][NT][16][17];
+  __shared__ float fin[NB][NT][16][17];
   __shared__ float best_v[16][17];
   __shared__ int best_i[16][17];
   __shared__ float rs[16];
@@ -804,35 +810,43 @@ __global__ __launch_bounds__(64 * SKW) void gemv_mfma_kernel(const LinearArgs a)
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int K = a.K, M = a.M;
   const int n_out = GATED ? a.n_per : a.n_per * a.n_mats;
+  const int tiles = (n_out + 15) / 16;
   const bool qkv = !GATED && a.epi == EPI_QKV;
+  const int grp = blockIdx.x;
   const int steps = K / 64;
   const int s_beg = (steps * wave) / SKW, s_end = (steps * (wave + 1)) / SKW;
+  const int half = a.d_head >> 1, per_head = qkv ? half / 8 : 1;
 
-  // QKV blocks: matrix, head and 8-column group of the rotary pairs
-  int q_mat = 0, q_c = 0;
-  if (qkv) {
-    const int half = a.d_head >> 1, per_head = half / 8;
-    const int mat = blockIdx.x / (a.n_heads * per_head);
-    const int rem = blockIdx.x - mat * a.n_heads * per_head;
+  // QKV tiles: matrix, head and 8-column group of the rotary pairs
+  auto qkv_tile = [&](int vt, int& mat, int& c) {
+    const int m = vt / (a.n_heads * per_head);
+    const int rem = vt - m * a.n_heads * per_head;
     const int h = rem / per_head, jb = rem - h * per_head;
-    q_mat = mat;
-    q_c = h * a.d_head + 8 * jb;
-  }
+    mat = m;
+    c = h * a.d_head + 8 * jb;
+  };
   const int r16 = lane & 15;
-  const int row = qkv ? q_mat * a.n_per + q_c + (r16 & 7) + (r16 >= 8 ? (a.d_head >> 1) : 0)
-                      : blockIdx.x * 16 + r16;
-  const bool row_ok = row < n_out;
-  const bf16_t* wrow[NB];
-  {
-    const int rr = row_ok ? row : 0;
+  const bf16_t* wrow[NB][NT];
+#pragma unroll
+  for (int j = 0; j < NT; ++j) {
+    const int vt = grp * NT + j;
+    int row;
+    if (qkv) {
+      int m, c;
+      qkv_tile(vt < tiles ? vt : 0, m, c);
+      row = m * a.n_per + c + (r16 & 7) + (r16 >= 8 ? half : 0);
+    } else {
+      row = vt * 16 + r16;
+    }
+    const int rr = (vt < tiles && row < n_out) ? row : 0;
     if (GATED) {
-      wrow[0] = reinterpret_cast<const bf16_t*>(a.w[0]) + (size_t)rr * K;
-      wrow[NB - 1] = reinterpret_cast<const bf16_t*>(a.w[1]) + (size_t)rr * K;
+      wrow[0][j] = reinterpret_cast<const bf16_t*>(a.w[0]) + (size_t)rr * K;
+      wrow[NB - 1][j] = reinterpret_cast<const bf16_t*>(a.w[1]) + (size_t)rr * K;
     } else {
       int v = rr;
       const void* base = a.w[0];
       if (v >= a.n_per) { v -= a.n_per; base = a.w[1]; if (v >= a.n_per) { v -= a.n_per; base = a.w[2]; } }
-      wrow[0] = reinterpret_cast<const bf16_t*>(base) + (size_t)v * K;
+      wrow[0][j] = reinterpret_cast<const bf16_t*>(base) + (size_t)v * K;
     }
   }
   const int kq = (lane >> 4) * 16;  // this lane's 16 elements within a step
@@ -844,9 +858,8 @@ __global__ __launch_bounds__(64 * SKW) void gemv_mfma_kernel(const LinearArgs a)
   const bf16_t* brow_lo = brow + (size_t)PR * a.in_ld;
 
   // values the epilogue needs, requested before the main batch (the wait counter retires loads
-  // in issue order, so they are in registers by the time the weights are): the producer's partial
-  // sums of squares (RMSNorm; thread: row t0 + tid % 16, partials tid / 16 + NG i) and the old
-  // residual value of this thread's output (clamped loads, never conditional)
+  // in issue order): the producer's partial sums of squares (RMSNorm; thread: row t0 + tid % 16,
+  // partials tid / 16 + NG i) and the old residual values of this thread's outputs
   float sv[RMS ? SSQ_MAX / NG : 1];
   if (RMS) {
 #pragma unroll
@@ -855,17 +868,24 @@ __global__ __launch_bounds__(64 * SKW) void gemv_mfma_kernel(const LinearArgs a)
       sv[i] = a.in_ssq[(size_t)min(p, a.in_nssq - 1) * PR + t0 + (tid & 15)];
     }
   }
-  float y_old = 0.f;
-  if (a.epi == EPI_RESID) {
-    const int ry = min(t0 + (tid & 15), M - 1), ny = min((int)blockIdx.x * 16 + ((tid >> 4) & 15), n_out - 1);
-    y_old = a.y[(size_t)ry * a.ldy + ny];
+  float y_old[NT];
+#pragma unroll
+  for (int j = 0; j < NT; ++j) {
+    y_old[j] = 0.f;
+    if (a.epi == EPI_RESID) {
+      const int ry = min(t0 + (tid & 15), M - 1);
+      const int ny = min((grp * NT + j) * 16 + ((tid >> 4) & 15), n_out - 1);
+      y_old[j] = a.y[(size_t)ry * a.ldy + ny];
+    }
   }
 
-  f32x4_t acc[NB];
+  f32x4_t acc[NB][NT];
 #pragma unroll
-  for (int b = 0; b < NB; ++b) acc[b] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  for (int b = 0; b < NB; ++b)
+#pragma unroll
+    for (int j = 0; j < NT; ++j) acc[b][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   for (int s0 = s_beg; s0 < s_end; s0 += SK) {
-    uint4 wv[NB][SK][2], bv[SK][2], bl[SK][2];
+    uint4 wv[NB][NT][SK][2], bv[SK][2], bl[SK][2];
     // inputs first (L2-resident, they arrive early), then the weights in step order: the wait
     // counter retires loads in issue order, so step u waits only for its own weights
 #pragma unroll
@@ -882,11 +902,13 @@ __global__ __launch_bounds__(64 * SKW) void gemv_mfma_kernel(const LinearArgs a)
     for (int u = 0; u < SK; ++u) {
       const int k0 = min(s0 + u, s_end - 1) * 64 + kq;
 #pragma unroll
-      for (int b = 0; b < NB; ++b) {
-        const uint4* wp = reinterpret_cast<const uint4*>(wrow[b] + k0);
-        wv[b][u][0] = wp[0];
-        wv[b][u][1] = wp[1];
-      }
+      for (int j = 0; j < NT; ++j)
+#pragma unroll
+        for (int b = 0; b < NB; ++b) {
+          const uint4* wp = reinterpret_cast<const uint4*>(wrow[b][j] + k0);
+          wv[b][j][u][0] = wp[0];
+          wv[b][j][u][1] = wp[1];
+        }
     }
     __builtin_amdgcn_sched_barrier(0);  // keep the whole batch in flight before the first MFMA
 #pragma unroll
@@ -899,14 +921,16 @@ __global__ __launch_bounds__(64 * SKW) void gemv_mfma_kernel(const LinearArgs a)
       const uint4 b0 = use ? bv[u][0] : z, b1 = use ? bv[u][1] : z;
       const uint4 c0 = use ? bl[u][0] : z, c1 = use ? bl[u][1] : z;
 #pragma unroll
-      for (int b = 0; b < NB; ++b) {
-        const bf16x8_t w0 = *reinterpret_cast<const bf16x8_t*>(&wv[b][u][0]);
-        const bf16x8_t w1 = *reinterpret_cast<const bf16x8_t*>(&wv[b][u][1]);
-        acc[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w0, *reinterpret_cast<const bf16x8_t*>(&b0), acc[b], 0, 0, 0);
-        acc[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w0, *reinterpret_cast<const bf16x8_t*>(&c0), acc[b], 0, 0, 0);
-        acc[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w1, *reinterpret_cast<const bf16x8_t*>(&b1), acc[b], 0, 0, 0);
-        acc[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w1, *reinterpret_cast<const bf16x8_t*>(&c1), acc[b], 0, 0, 0);
-      }
+      for (int j = 0; j < NT; ++j)
+#pragma unroll
+        for (int b = 0; b < NB; ++b) {
+          const bf16x8_t w0 = *reinterpret_cast<const bf16x8_t*>(&wv[b][j][u][0]);
+          const bf16x8_t w1 = *reinterpret_cast<const bf16x8_t*>(&wv[b][j][u][1]);
+          acc[b][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w0, *reinterpret_cast<const bf16x8_t*>(&b0), acc[b][j], 0, 0, 0);
+          acc[b][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w0, *reinterpret_cast<const bf16x8_t*>(&c0), acc[b][j], 0, 0, 0);
+          acc[b][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w1, *reinterpret_cast<const bf16x8_t*>(&b1), acc[b][j], 0, 0, 0);
+          acc[b][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w1, *reinterpret_cast<const bf16x8_t*>(&c1), acc[b][j], 0, 0, 0);
+        }
     }
   }
   float sp = 0.f;
@@ -918,9 +942,32 @@ __global__ __launch_bounds__(64 * SKW) void gemv_mfma_kernel(const LinearArgs a)
 #pragma unroll
   for (int b = 0; b < NB; ++b)
 #pragma unroll
-    for (int e = 0; e < 4; ++e) part[wave][b][4 * (lane >> 4) + e][lane & 15] = acc[b][e];
+    for (int j = 0; j < NT; ++j)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) part[wave][b][j][4 * (lane >> 4) + e][lane & 15] = acc[b][j][e];
   if (RMS) ssq_red[tid >> 4][tid & 15] = sp;
   __syncthreads();
+
+  // the block's tiles summed over its waves: thread (feature f, row t) of the first 256 threads
+  static_assert(SKW >= 4, "the epilogue needs 256 threads");
+  const int f = (tid >> 4) & 15, t = tid & 15, tg = t0 + t;
+  const bool lead = tid < 256;
+  float tsum[NB][NT];
+#pragma unroll
+  for (int b = 0; b < NB; ++b)
+#pragma unroll
+    for (int j = 0; j < NT; ++j) {
+      float v = 0.f;
+#pragma unroll
+      for (int w = 0; w < SKW; ++w) v += part[w][b][j][f][t];
+      tsum[b][j] = v;
+    }
+  if (lead) {
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+#pragma unroll
+      for (int j = 0; j < NT; ++j) fin[b][j][f][t] = tsum[b][j];
+  }
   if (RMS && tid < 16) {
     float s2 = 0.f;
 #pragma unroll
@@ -929,85 +976,83 @@ __global__ __launch_bounds__(64 * SKW) void gemv_mfma_kernel(const LinearArgs a)
   }
   __syncthreads();
 
-  // epilogue: thread (feature f, row t0 + t) for the first 256 threads
-  static_assert(SKW >= 4, "the epilogue needs 256 threads");
-  const int f = (tid >> 4) & 15, t = tid & 15, tg = t0 + t;
-  const bool lead = tid < 256;
-  auto tile_sum = [&](int b, int ff) {
-    float v = 0.f;
-#pragma unroll
-    for (int w = 0; w < SKW; ++w) v += part[w][b][ff][t];
-    return v;
-  };
   const float rscale = RMS ? rs[t] : 1.f;
-  const int n = blockIdx.x * 16 + f;
-  const float v = tile_sum(0, f) * rscale;
-  if (a.epi == EPI_ARGMAX) {
-    const bool ok = lead && tg < M && n < n_out;
-    if (lead) {
-      best_v[t][f] = ok ? v : -INFINITY;
-      best_i[t][f] = ok ? n : INT_MAX;
-    }
-    if (ok && a.logits) a.logits[(size_t)tg * a.ldl + n] = v;
-    __syncthreads();
-    if (tid < 16 && t0 + tid < M) {
-      float bvv = -INFINITY;
-      int bi = INT_MAX;
-      for (int ff = 0; ff < 16; ++ff) argmax_merge(bvv, bi, best_v[tid][ff], best_i[tid][ff]);
-      a.part_val[(size_t)(t0 + tid) * a.n_parts + blockIdx.x] = bvv;
-      a.part_idx[(size_t)(t0 + tid) * a.n_parts + blockIdx.x] = bi;
-    }
-    return;
-  }
-  if (a.epi == EPI_RESID) {
-    // y_new, the next planes and this block's partial sums of squares (all threads take part in
-    // the reduction; rows past M or features past n_out contribute zero)
-    const bool ok = lead && tg < M && n < n_out;
-    float y2 = 0.f;
-    if (ok) {
-      const float tt = y_old + v;
-      a.y[(size_t)tg * a.ldy + n] = tt;
-      if (a.stash) a.stash[(size_t)tg * a.lds + n] = tt;
-      if (a.out_planes) {
-        const float gv = a.out_gain ? a.out_gain[n] * tt : tt;
-        const uint32_t hi = f32_to_bf16(gv);
-        a.out_planes[(size_t)tg * a.out_ld + n] = (bf16_t)hi;
-        a.out_planes[(size_t)(PR + tg) * a.out_ld + n] = (bf16_t)f32_to_bf16(gv - bf16_to_f32(hi));
+  for (int j = 0; j < NT; ++j) {
+    const int vt = grp * NT + j;
+    if (vt >= tiles) break;  // uniform over the block
+    const int n = vt * 16 + f;
+    const float v = fin[0][j][f][t] * rscale;
+    if (a.epi == EPI_ARGMAX) {
+      const bool ok = lead && tg < M && n < n_out;
+      if (lead) {
+        best_v[t][f] = ok ? v : -INFINITY;
+        best_i[t][f] = ok ? n : INT_MAX;
       }
-      y2 = tt * tt;
-    }
-    if (a.out_ssq) {
-      // threads with the same t: lanes t, t+16, t+32, t+48 of the first four waves
-      y2 += __shfl_xor(y2, 16, SSD_WAVE);
-      y2 += __shfl_xor(y2, 32, SSD_WAVE);
-      if (lead && lane < 16) sq[wave][lane] = y2;
+      if (ok && a.logits) a.logits[(size_t)tg * a.ldl + n] = v;
       __syncthreads();
-      if (tid < 16) a.out_ssq[(size_t)blockIdx.x * PR + t0 + tid] = (sq[0][tid] + sq[1][tid]) + (sq[2][tid] + sq[3][tid]);
+      if (tid < 16 && t0 + tid < M) {
+        float bvv = -INFINITY;
+        int bi = INT_MAX;
+        for (int ff = 0; ff < 16; ++ff) argmax_merge(bvv, bi, best_v[tid][ff], best_i[tid][ff]);
+        a.part_val[(size_t)(t0 + tid) * a.n_parts + vt] = bvv;
+        a.part_idx[(size_t)(t0 + tid) * a.n_parts + vt] = bi;
+      }
+      __syncthreads();
+      continue;
     }
-    return;
-  }
-  if (!lead || tg >= M) return;
-  if (qkv) {
-    if (f < 8) qkv_store_pair(a, q_mat, q_c + f, tg, v, tile_sum(0, f + 8) * rscale);
-    return;
-  }
-  if (n >= n_out) return;
-  if (GATED) {
-    const float act = apply_epi_act(a.epi, v, tile_sum(NB - 1, f) * rscale);
-    if (a.y) a.y[(size_t)tg * a.ldy + n] = act;
-    if (a.out_planes) {
-      const uint32_t hi = f32_to_bf16(act);
-      a.out_planes[(size_t)tg * a.out_ld + n] = (bf16_t)hi;
-      a.out_planes[(size_t)(PR + tg) * a.out_ld + n] = (bf16_t)f32_to_bf16(act - bf16_to_f32(hi));
+    if (a.epi == EPI_RESID) {
+      // y_new, the next planes and this tile's partial sums of squares (all threads take part in
+      // the reduction; rows past M or features past n_out contribute zero)
+      const bool ok = lead && tg < M && n < n_out;
+      float y2 = 0.f;
+      if (ok) {
+        const float tt = y_old[j] + v;
+        a.y[(size_t)tg * a.ldy + n] = tt;
+        if (a.stash) a.stash[(size_t)tg * a.lds + n] = tt;
+        if (a.out_planes) {
+          const float gv = a.out_gain ? a.out_gain[n] * tt : tt;
+          const uint32_t hi = f32_to_bf16(gv);
+          a.out_planes[(size_t)tg * a.out_ld + n] = (bf16_t)hi;
+          a.out_planes[(size_t)(PR + tg) * a.out_ld + n] = (bf16_t)f32_to_bf16(gv - bf16_to_f32(hi));
+        }
+        y2 = tt * tt;
+      }
+      if (a.out_ssq) {
+        // threads with the same t: lanes t, t+16, t+32, t+48 of the first four waves
+        y2 += __shfl_xor(y2, 16, SSD_WAVE);
+        y2 += __shfl_xor(y2, 32, SSD_WAVE);
+        if (lead && lane < 16) sq[wave][lane] = y2;
+        __syncthreads();
+        if (tid < 16) a.out_ssq[(size_t)vt * PR + t0 + tid] = (sq[0][tid] + sq[1][tid]) + (sq[2][tid] + sq[3][tid]);
+        __syncthreads();
+      }
+      continue;
     }
-    return;
-  }
-  float* yp = a.y + (size_t)tg * a.ldy + n;
-  switch (a.epi) {
-    case EPI_STORE: *yp = v; break;
-    case EPI_BIAS_GELU: *yp = gelu_tanh(v + a.bias[n]); break;
-    case EPI_BIAS_RESID: *yp = (a.resid ? a.resid[(size_t)tg * a.ldr + n] : 0.f) + (v + a.bias[n]); break;
-    default: break;
+    if (!lead || tg >= M) continue;
+    if (qkv) {
+      int m, c;
+      qkv_tile(vt, m, c);
+      if (f < 8) qkv_store_pair(a, m, c + f, tg, v, fin[0][j][f + 8][t] * rscale);
+      continue;
+    }
+    if (n >= n_out) continue;
+    if (GATED) {
+      const float act = apply_epi_act(a.epi, v, fin[NB - 1][j][f][t] * rscale);
+      if (a.y) a.y[(size_t)tg * a.ldy + n] = act;
+      if (a.out_planes) {
+        const uint32_t hi = f32_to_bf16(act);
+        a.out_planes[(size_t)tg * a.out_ld + n] = (bf16_t)hi;
+        a.out_planes[(size_t)(PR + tg) * a.out_ld + n] = (bf16_t)f32_to_bf16(act - bf16_to_f32(hi));
+      }
+      continue;
+    }
+    float* yp = a.y + (size_t)tg * a.ldy + n;
+    switch (a.epi) {
+      case EPI_STORE: *yp = v; break;
+      case EPI_BIAS_GELU: *yp = gelu_tanh(v + a.bias[n]); break;
+      case EPI_BIAS_RESID: *yp = (a.resid ? a.resid[(size_t)tg * a.ldr + n] : 0.f) + (v + a.bias[n]); break;
+      default: break;
+    }
   }
 }
 
@@ -1583,12 +1628,19 @@ hipError_t launch_linear_skinny(const LinearArgs& a, hipStream_t s, int* n_parts
   LinearArgs b = a;
   if (b.epi == EPI_ARGMAX) b.n_parts = tiles;
   if (n_parts) *n_parts = b.n_parts;
-  const dim3 grid(tiles, (a.M + 15) / 16), block(64 * SKW);
   const bool rms = a.norm == NORM_RMS;
-  if (gated && rms) hipLaunchKernelGGL((gemv_mfma_kernel<true, true>), grid, block, 0, s, b);
-  else if (gated) hipLaunchKernelGGL((gemv_mfma_kernel<true, false>), grid, block, 0, s, b);
-  else if (rms) hipLaunchKernelGGL((gemv_mfma_kernel<false, true>), grid, block, 0, s, b);
-  else hipLaunchKernelGGL((gemv_mfma_kernel<false, false>), grid, block, 0, s, b);
+  const dim3 block(64 * SKW);
+  if (a.epi == EPI_ARGMAX) {
+    const dim3 grid((tiles + 3) / 4, (a.M + 15) / 16);
+    if (rms) hipLaunchKernelGGL((gemv_mfma_kernel<false, true, 4>), grid, block, 0, s, b);
+    else hipLaunchKernelGGL((gemv_mfma_kernel<false, false, 4>), grid, block, 0, s, b);
+    return hipGetLastError();
+  }
+  const dim3 grid(tiles, (a.M + 15) / 16);
+  if (gated && rms) hipLaunchKernelGGL((gemv_mfma_kernel<true, true, 1>), grid, block, 0, s, b);
+  else if (gated) hipLaunchKernelGGL((gemv_mfma_kernel<true, false, 1>), grid, block, 0, s, b);
+  else if (rms) hipLaunchKernelGGL((gemv_mfma_kernel<false, true, 1>), grid, block, 0, s, b);
+  else hipLaunchKernelGGL((gemv_mfma_kernel<false, false, 1>), grid, block, 0, s, b);
   return hipGetLastError();
 }
 
