@@ -213,6 +213,18 @@ int ssd_set_graphs(ssd_ctx* ctx, int enable);
  * the persistent pass will be used, 0 when not, SSD_ERR_ARG for a null context. */
 int ssd_set_persistent(ssd_ctx* ctx, int enable);
 
+/* Hidden-state export, for fitting the imitation network offline on the decoder's own states
+ * (a stand-in for the paper's imitation training, Sec. "Deep Representation Imitation"; not on
+ * the decode path).  While set (all three non-NULL), every ssd_draft also copies, for its
+ * gamma steps, the imitation network's hidden features gelu(W1 LN(x_k) + b1) to
+ * d_phi [B][gamma][in_hidden] and the layer-k residual rows x_k to d_xk [B][gamma][d_model], and
+ * every ssd_verify copies its final residual rows (after the last layer, before g's norm) to
+ * d_xl [B][gamma + 1][d_model], float32, device memory owned by the caller (sized for the
+ * largest B and gamma used).  Row i of a draft and row i of the verify that follows it are the
+ * same position.  All NULL disables; a mix of NULL and non-NULL is SSD_ERR_ARG.  The persistent
+ * one-row pass is not used while the export is set. */
+int ssd_set_hidden_export(ssd_ctx* ctx, float* d_phi, float* d_xk, float* d_xl);
+
 /* Kernel timing for roofline reports.  With the persistent pass active (ssd_set_persistent), the
  * timed launches are the persistent draft steps and the bytes are the pass's weights, input rows
  * and output rows (KV-cache reads are not counted).  Otherwise, while enabled (and graphs are

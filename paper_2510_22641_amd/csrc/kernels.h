@@ -229,6 +229,10 @@ hipError_t launch_assemble(float* x, const float* stash, int ld_stash_b, const f
 
 hipError_t launch_set_seq_len(int32_t* seq_len, int B, int value, hipStream_t s);
 
+// dst[r][0..cols) = src[r][0..cols) for r < rows (row strides ldd, lds floats).
+hipError_t launch_copy_rows(float* dst, int ldd, const float* src, int lds, int rows, int cols,
+                            hipStream_t s);
+
 struct AcceptArgs {
   int B, gamma;
   const int32_t* draft;   // [B][gamma]

@@ -128,6 +128,12 @@ __global__ void assemble_kernel(float* x, const float* stash, int ld_stash_b, co
   for (int k = threadIdx.x; k < d; k += blockDim.x) x[(size_t)r * d + k] = src[k];
 }
 
+// dst row r (stride ldd) = src row r (stride lds), cols floats each; one block per row
+__global__ void copy_rows_kernel(float* dst, int ldd, const float* src, int lds, int cols) {
+  const size_t r = blockIdx.x;
+  for (int k = threadIdx.x; k < cols; k += blockDim.x) dst[r * ldd + k] = src[r * lds + k];
+}
+
 __global__ void set_seq_len_kernel(int32_t* seq_len, int B, int value) {
   const int b = blockIdx.x * blockDim.x + threadIdx.x;
   if (b < B) seq_len[b] = value;
@@ -273,6 +279,13 @@ hipError_t launch_assemble(float* x, const float* stash, int ld_stash_b, const f
                            int g, int d, hipStream_t s) {
   hipLaunchKernelGGL(assemble_kernel, dim3(B * (g + 1)), dim3(256), 0, s, x, stash, ld_stash_b, x1,
                      B, g, d);
+  return hipGetLastError();
+}
+
+hipError_t launch_copy_rows(float* dst, int ldd, const float* src, int lds, int rows, int cols,
+                            hipStream_t s) {
+  if (rows <= 0 || cols <= 0) return hipSuccess;
+  hipLaunchKernelGGL(copy_rows_kernel, dim3(rows), dim3(256), 0, s, dst, ldd, src, lds, cols);
   return hipGetLastError();
 }
 

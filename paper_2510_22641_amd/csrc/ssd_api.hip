@@ -211,6 +211,11 @@ struct ssd_ctx {
   const int32_t* draft_out = nullptr;
   bool use_graphs = true;
   std::map<GraphKey, hipGraphExec_t> graphs;
+  // hidden-state export (ssd_set_hidden_export): imitation-network features and layer-k rows of
+  // each draft step, final rows of each verify
+  float* ex_phi = nullptr;
+  float* ex_xk = nullptr;
+  float* ex_xl = nullptr;
   // persistent one-row passes: built at creation when the shape and the device allow them;
   // off unless asked for (slower than the chain of kernels on MI355X, see step.hip)
   bool step_ok = false;
@@ -427,7 +432,7 @@ int build_step_programs(ssd_ctx* c) {
 // One-row passes of a one-sequence call take the persistent kernel (T5 once the cross-attention
 // is folded, i.e. after prefill).
 bool use_step_now(const ssd_ctx* c, int B) {
-  return c->step_ok && c->use_step && B == 1 &&
+  return c->step_ok && c->use_step && B == 1 && !c->ex_phi &&
          (c->d.arch == SSD_ARCH_LLAMA || c->fold_ready);
 }
 
@@ -681,6 +686,13 @@ int draft_launches(ssd_ctx* c, int B, int gamma, const int32_t* pending, int32_t
     a.w[0] = c->w.in_w1; a.n_per = d.in_hidden; a.epi = EPI_BIAS_GELU; a.bias = c->w.in_b1;
     a.y = inh; a.ldy = d.in_hidden;
     HIP_TRY(run_linear(c, a));
+    if (c->ex_phi) {
+      // export: the imitation network's hidden features of step i, [B][gamma][in_hidden]
+      HIP_TRY(launch_copy_rows(c->ex_phi + (size_t)i * d.in_hidden, gamma * d.in_hidden, inh,
+                               d.in_hidden, B, d.in_hidden, c->stream));
+      HIP_TRY(launch_copy_rows(c->ex_xk + (size_t)i * D, gamma * D, stash + (size_t)i * D, ld_stash,
+                               B, D, c->stream));
+    }
     a = lin(c);
     a.x = inh; a.ldx = d.in_hidden; a.M = B; a.K = d.in_hidden;
     a.w[0] = c->w.in_w2; a.n_per = D; a.epi = EPI_BIAS_RESID; a.bias = c->w.in_b2;
@@ -736,6 +748,10 @@ int verify_launches(ssd_ctx* c, int B, int gamma, const int32_t* pending, const 
                             c->stream));
     rc = run_layers(c, x, B, C, 0, d.draft_layers, d.n_layers, -1, nullptr, 0);
     if (rc) return rc;
+  }
+  if (c->ex_xl) {
+    // export: the final residual rows (before g's norm), [B][gamma + 1][d_model]
+    HIP_TRY(launch_copy_rows(c->ex_xl, D, x, D, B * C, D, c->stream));
   }
   return run_head(c, x, D, B * C, C, logits, d.vocab, target, C, 0, nullptr);
 }
@@ -1038,6 +1054,21 @@ int ssd_set_persistent(ssd_ctx* c, int enable) {
   }
   c->use_step = enable != 0;
   return (c->step_ok && c->use_step) ? 1 : 0;
+}
+
+int ssd_set_hidden_export(ssd_ctx* c, float* d_phi, float* d_xk, float* d_xl) {
+  if (!c) return SSD_ERR_ARG;
+  const bool on = d_phi || d_xk || d_xl;
+  if (on && !(d_phi && d_xk && d_xl)) return SSD_ERR_ARG;
+  if (c->ex_phi != d_phi || c->ex_xk != d_xk || c->ex_xl != d_xl) {
+    // captured launch sequences differ with and without the export
+    for (auto& kv : c->graphs) (void)hipGraphExecDestroy(kv.second);
+    c->graphs.clear();
+  }
+  c->ex_phi = d_phi;
+  c->ex_xk = d_xk;
+  c->ex_xl = d_xl;
+  return SSD_OK;
 }
 
 int ssd_profile_enable(ssd_ctx* c, int enable) {

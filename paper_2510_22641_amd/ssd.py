@@ -76,6 +76,7 @@ def _load():
         "ssd_dynamic_gamma": (c_int, [c_int, c_int, c_int]),
         "ssd_set_graphs": (c_int, [P, c_int]),
         "ssd_set_persistent": (c_int, [P, c_int]),
+        "ssd_set_hidden_export": (c_int, [P, P, P, P]),
         "ssd_profile_enable": (c_int, [P, c_int]),
         "ssd_profile_read": (c_int, [P, POINTER(c_int64), POINTER(ctypes.c_double),
                                      POINTER(ctypes.c_double)]),
@@ -92,7 +93,7 @@ def _load():
 
 _lib = _load()
 EXPORTS = ("ssd_workspace_bytes", "ssd_create", "ssd_prefill", "ssd_draft", "ssd_verify",
-           "ssd_accept", "ssd_generate", "ssd_dynamic_gamma", "ssd_set_graphs", "ssd_set_persistent",
+           "ssd_accept", "ssd_generate", "ssd_dynamic_gamma", "ssd_set_graphs", "ssd_set_persistent", "ssd_set_hidden_export",
            "ssd_profile_enable",
            "ssd_profile_read", "ssd_sync_status",
            "ssd_status_string", "ssd_destroy")
@@ -173,6 +174,10 @@ def ssd_set_persistent(ctx, enable: bool) -> bool:
     if rc < 0:
         raise SSDError("ssd_set_persistent", rc)
     return rc == 1
+
+
+def ssd_set_hidden_export(ctx, d_phi, d_xk, d_xl):
+    _check("ssd_set_hidden_export", _lib.ssd_set_hidden_export(ctx, _p(d_phi), _p(d_xk), _p(d_xl)))
 
 
 def ssd_profile_enable(ctx, enable: bool):
