@@ -11,6 +11,8 @@ Contents
              network and the shared LM head g, evaluated position by position
   decode.py  prefill, full-model greedy decoding, Algorithm 1 (self-speculative imitation
              decoding, greedy) and a replay mode that follows a device run's token stream
+  sampling.py  the sampling variant of the loop (speculative sampling, uniforms as inputs),
+             plain sampling from the full model, and its replay mode
 
 Precision: float64 throughout, on the float32 (bf16-representable, in bf16 workloads) values
 produced by ``synth``.

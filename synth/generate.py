@@ -33,6 +33,7 @@ from .configs import Shape, Workload
 GLOBAL = 10_000
 VISUAL = 20_000
 PROMPT = 30_000
+UNIFORM = 40_000
 
 # tensor id, name, kind
 _GLOBAL_TENSORS = [
@@ -176,4 +177,13 @@ def make_prompts(shape: Shape, seed: int, batch: int, prompt_len: int) -> np.nda
     out = np.empty((batch, prompt_len), dtype=np.int32)
     for b in range(batch):
         out[b] = _rng(seed, PROMPT + b, 0).integers(0, shape.vocab, prompt_len)
+    return out
+
+
+def make_uniforms(seed: int, batch: int, rounds: int, per_round: int) -> np.ndarray:
+    """[batch, rounds, per_round] float32 uniforms in [0, 1): the random draws of sampled
+    decoding, an input to both the device path and the oracle."""
+    out = np.empty((batch, rounds, per_round), dtype=np.float32)
+    for b in range(batch):
+        out[b] = _rng(seed, UNIFORM + b, 0).random((rounds, per_round), dtype=np.float32)
     return out
