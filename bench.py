@@ -181,6 +181,38 @@ def sweep_c4(args):
         torch.cuda.empty_cache()
 
 
+def sampled_decode(dd, pt, vt, T: int, gamma: int, tau: float, uniforms):
+    """One sequence decoded with speculative sampling (gamma > 0) or plain sampling from the full
+    model (gamma = 0: a one-row verify and the rule's extra sample), uniforms [rounds, 2 gamma + 1];
+    a host read of the accepted count per round.  Returns (seconds, tokens, accepted, drafted)."""
+    import numpy as np
+    import torch
+    ud = dd.buf("u_draft", (1, max(gamma, 1)), torch.float32)
+    ua = dd.buf("u_accept", (1, gamma + 1), torch.float32)
+    u_dev = torch.from_numpy(np.ascontiguousarray(uniforms, dtype=np.float32)).to(ud.device)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    pending, _ = dd.prefill(pt, vt)
+    emitted, r, acc, drafted = 1, 0, 0, 0
+    while emitted < T:
+        if gamma > 0:
+            ud.copy_(u_dev[r:r + 1, :gamma])
+        ua.copy_(u_dev[r:r + 1, gamma:])
+        if gamma > 0:
+            d, dl = dd.draft_sample(pending, gamma, ud, tau)
+        else:
+            d, dl = dd.buf("no_draft", (1, 1)), None
+        t, tl = dd.verify(pending, d, gamma, reuse=gamma > 0, logits=True)
+        _, alen = dd.accept_sample(d, dl, tl, ua, tau, pending, gamma)
+        a = int(alen.cpu()[0])
+        emitted += a + 1
+        acc += a
+        drafted += gamma
+        r += 1
+    torch.cuda.synchronize()
+    return time.perf_counter() - t0, min(emitted, T), acc, drafted
+
+
 def cpu_baseline(wl, weights, prompt, visual, budget_s: float):
     """The float64 oracle's Algorithm 1 on the host, over as many rounds as fit the budget."""
     import numpy as np
@@ -223,6 +255,8 @@ def main():
     ap.add_argument("--fit-prompts", type=int, default=16,
                     help="sequences (seeds 1000..) whose states fit the imitation network's second "
                          "layer before a second measurement (0: skip)")
+    ap.add_argument("--sample-temps", default="1.0,0.1",
+                    help="temperatures of the speculative-sampling measurement (empty: skip)")
     ap.add_argument("--persistent", type=int, choices=[0, 1], default=None,
                     help="force the persistent one-row pass on (1) or off (0); default: the "
                          "library's choice")
@@ -338,6 +372,26 @@ def main():
                 "bytes_per_launch": int(per_launch_bytes), "avg_launch_us": round(avg_s * 1e6, 3),
                 "launches": n_launch}
 
+    # speculative sampling against plain sampling from the full model, same build and uniforms
+    sampling = []
+    for tau in [float(x) for x in args.sample_temps.split(",") if x.strip()]:
+        u_ssd = synth.make_uniforms(args.seed, 1, T, 2 * g + 1)[0]
+        u_full = synth.make_uniforms(args.seed + 1, 1, T, 1)[0]
+        sampled_decode(dd, pt[:1], vt[:1], T, g, tau, u_ssd)  # warm-up (graph capture)
+        sampled_decode(dd, pt[:1], vt[:1], T, 0, tau, u_full)
+        ts, ns, acc, dr = 0.0, 0, 0, 0
+        tf, nf = 0.0, 0
+        for _ in range(args.steps):
+            t1, n1, a1, d1 = sampled_decode(dd, pt[:1], vt[:1], T, g, tau, u_ssd)
+            t2, n2, _, _ = sampled_decode(dd, pt[:1], vt[:1], T, 0, tau, u_full)
+            ts, ns, acc, dr, tf, nf = ts + t1, ns + n1, acc + a1, dr + d1, tf + t2, nf + n2
+        sampling.append({"temperature": tau, "tokens_per_s": round(ns / ts, 2),
+                         "acceptance_rate": round(acc / max(1, dr), 4),
+                         "full_model_sampling_tokens_per_s": round(nf / tf, 2),
+                         "speedup_vs_full_model_sampling": round((ns / ts) / (nf / tf), 3),
+                         "loop": "host-driven rounds (one accepted-count read per round)"})
+        print(f"[bench] sampling tau {tau}: {sampling[-1]}", file=sys.stderr, flush=True)
+
     # the imitation network's second layer fitted on the decoder's own states (other sequences),
     # then the same job measured again; the headline keeps the configured network
     fit = None
@@ -398,6 +452,7 @@ def main():
         "speedup_vs_greedy": round(ssd_tps / greedy_tps, 3),
         "ssd_equals_greedy_tokens": same,
         "dynamic_gamma": dyn,
+        "speculative_sampling": sampling or None,
         "fitted_imitation": fit,
         "draft_step": draft,
         "verify": verify,

@@ -180,6 +180,34 @@ int ssd_verify(ssd_ctx* ctx, int B, int gamma, const int32_t* d_pending, const i
 int ssd_accept(ssd_ctx* ctx, int B, int gamma, const int32_t* d_draft, const int32_t* d_target,
                int32_t* d_pending, int32_t* d_out, int32_t* d_accept_len, const int32_t* d_active);
 
+/* Sampling variant of the loop (speculative sampling; the paper's decoder may sample its next
+ * token instead of taking the argmax, Sec. "SSD Setup for VLMs").  Distributions at temperature
+ * `temperature` (> 0): softmax(logits / temperature).  Randomness is an input: a sample from
+ * weights w with uniform u in [0, 1) is the inverse CDF, the smallest k with
+ * w_0 + ... + w_k > u * sum(w).
+ *
+ * ssd_draft_sample: ssd_draft with each draft token sampled from the draft's distribution
+ * (d_u [B][gamma]: the uniform of step i of sequence b at [b][i]); d_draft_logits
+ * [B][gamma][V] float32 is required (the acceptance needs it).  A following ssd_verify may reuse
+ * the layer-k states as after ssd_draft.
+ *
+ * ssd_accept_sample: the speculative-sampling rule on the drafts of ssd_draft_sample and the
+ * full model's logits from ssd_verify (d_target_logits [B][gamma+1][V], required).  Draft i is
+ * accepted when u[b][i] * q_i(draft_i) < p_i(draft_i), q_i the draft's and p_i the full model's
+ * distribution at the same position (probability min(1, p/q)); the first rejected position
+ * emits a sample from the normalised residual max(0, p_i - q_i) (p_i if it vanishes) drawn with
+ * u[b][gamma], and a round whose drafts all pass emits a sample from p_gamma drawn with
+ * u[b][gamma] (d_u [B][gamma + 1]).  Outputs as ssd_accept: d_out[b][0..a] = the a accepted
+ * drafts and the sampled token, d_accept_len[b] = a, seq_len[b] += a + 1, d_pending[b] = the
+ * sampled token; sequences with d_active[b] == 0 are left untouched.  The output sequence then
+ * follows the full model's sampling distribution. */
+int ssd_draft_sample(ssd_ctx* ctx, int B, int gamma, const int32_t* d_pending, const float* d_u,
+                     float temperature, int32_t* d_draft, float* d_draft_logits);
+int ssd_accept_sample(ssd_ctx* ctx, int B, int gamma, const int32_t* d_draft,
+                      const float* d_draft_logits, const float* d_target_logits, const float* d_u,
+                      float temperature, int32_t* d_pending, int32_t* d_out,
+                      int32_t* d_accept_len, const int32_t* d_active);
+
 /* The whole loop: prefill, then rounds of draft + verify + accept (SSD_MODE_SPECULATIVE) or
  * verify(gamma = 0) + accept (SSD_MODE_GREEDY) until T tokens per sequence are emitted (the last
  * round truncated; a finished sequence's seq_len then counts only the positions it emitted, so

@@ -255,6 +255,30 @@ struct AcceptArgs {
 };
 hipError_t launch_accept(const AcceptArgs& a, hipStream_t s);
 
+// Speculative sampling (sample.hip).
+struct AcceptSampleArgs {
+  int B = 0, gamma = 0, vocab = 0;
+  const int32_t* draft = nullptr;          // [B][gamma]
+  const float* draft_logits = nullptr;     // [B][gamma][vocab]
+  const float* target_logits = nullptr;    // [B][gamma + 1][vocab]
+  const float* u = nullptr;                // [B][gamma + 1]: acceptance tests, then the sample
+  float inv_tau = 1.f;
+  int32_t* pending = nullptr;
+  int32_t* out = nullptr;                  // [B][gamma + 1] or null
+  int32_t* accept_len = nullptr;           // [B] or null
+  const int32_t* active = nullptr;         // [B] or null
+  int32_t* seq_len = nullptr;
+  int max_seq = 0;
+  int32_t* status = nullptr;
+};
+hipError_t launch_accept_sample(const AcceptSampleArgs& a, hipStream_t s);
+
+// Row m = b * C + j of logits (stride ldl): token sampled from softmax(row / tau) with uniform
+// u[b * ldu + uoff + j], written to dst0[b * ld0 + off0 + j] and dst1[m] (if set).
+hipError_t launch_sample_rows(const float* logits, int ldl, int M, int V, float tau,
+                              const float* u, int ldu, int uoff, int C, int32_t* dst0, int ld0,
+                              int off0, int32_t* dst1, hipStream_t s);
+
 struct GenInitArgs {
   int B, T;
   const int32_t* pending;

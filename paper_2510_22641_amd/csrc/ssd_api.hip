@@ -619,7 +619,8 @@ int run_layers(ssd_ctx* c, float* x, int B, int C, int pos_off, int l0, int l1, 
 // g = final RMSNorm + LM head, argmax per row.  Rows m of x (stride ldx) map to dst0 as in
 // launch_argmax_final.
 int run_head(ssd_ctx* c, const float* x, int ldx, int M, int C, float* logits, int ldl,
-             int32_t* dst0, int ld0, int off0, int32_t* dst1) {
+             int32_t* dst0, int ld0, int off0, int32_t* dst1, const float* u = nullptr,
+             int ldu = 0, int uoff = 0, float tau = 0.f) {
   const ssd_dims& d = c->d;
   LinearArgs a = lin(c);
   a.x = x; a.ldx = ldx; a.M = M; a.K = d.d_model;
@@ -640,13 +641,19 @@ int run_head(ssd_ctx* c, const float* x, int ldx, int M, int C, float* logits, i
   } else {
     HIP_TRY(run_linear(c, a, &n_parts));
   }
+  if (u) {
+    // sampled tokens: inverse CDF of softmax(logits / tau) per row (the logits are written above)
+    HIP_TRY(launch_sample_rows(logits, ldl, M, d.vocab, tau, u, ldu, uoff, C, dst0, ld0, off0,
+                               dst1, c->stream));
+    return SSD_OK;
+  }
   HIP_TRY(launch_argmax_final(a.part_val, a.part_idx, M, n_parts, C, dst0, ld0, off0, dst1,
                               c->stream));
   return SSD_OK;
 }
 
 int draft_launches(ssd_ctx* c, int B, int gamma, const int32_t* pending, int32_t* draft,
-                   float* logits) {
+                   float* logits, const float* u = nullptr, float tau = 0.f) {
   const ssd_dims& d = c->d;
   const int D = d.d_model;
   float* x = c->at<float>(c->L.x);
@@ -655,7 +662,7 @@ int draft_launches(ssd_ctx* c, int B, int gamma, const int32_t* pending, int32_t
   float* stash = c->at<float>(c->L.stash);
   int32_t* cur = c->at<int32_t>(c->L.cur_tok);
   const int ld_stash = (d.max_gamma + 1) * D;
-  if (use_step_now(c, B)) {
+  if (use_step_now(c, B) && !u) {
     for (int i = 0; i < gamma; ++i) {
       StepArgs a = step_args(c, STEP_DRAFT);
       a.tok = i == 0 ? pending : cur;
@@ -699,7 +706,7 @@ int draft_launches(ssd_ctx* c, int B, int gamma, const int32_t* pending, int32_t
     a.resid = d.in_residual ? x : nullptr; a.ldr = D; a.y = xi; a.ldy = D;
     HIP_TRY(run_linear(c, a));
     rc = run_head(c, xi, D, B, 1, logits ? logits + (size_t)i * d.vocab : nullptr,
-                  gamma * d.vocab, draft, gamma, i, cur);
+                  gamma * d.vocab, draft, gamma, i, cur, u, gamma, i, tau);
     if (rc) return rc;
   }
   return SSD_OK;
@@ -945,6 +952,48 @@ int ssd_draft(ssd_ctx* c, int B, int gamma, const int32_t* d_pending, int32_t* d
   c->draft_gamma = gamma;
   c->draft_pending = d_pending;
   c->draft_out = d_draft;
+  return SSD_OK;
+}
+
+int ssd_draft_sample(ssd_ctx* c, int B, int gamma, const int32_t* d_pending, const float* d_u,
+                     float temperature, int32_t* d_draft, float* d_draft_logits) {
+  if (!c || !d_pending || !d_draft || !d_u || !d_draft_logits) return SSD_ERR_ARG;
+  if (!(temperature > 0.f) || !std::isfinite(temperature)) return SSD_ERR_ARG;
+  if (B < 1 || B > c->d.max_batch || gamma < 1 || gamma > c->d.max_gamma) return SSD_ERR_SHAPE;
+  if (!c->prefilled) return SSD_ERR_STATE;
+  int tbits = 0;
+  std::memcpy(&tbits, &temperature, sizeof(tbits));
+  GraphKey key{3, B, gamma, tbits, d_pending, d_draft, d_draft_logits, d_u};
+  int rc = launch_maybe_graph(c, key, [&]() {
+    return draft_launches(c, B, gamma, d_pending, d_draft, d_draft_logits, d_u, temperature);
+  });
+  if (rc) return rc;
+  c->draft_valid = true;
+  c->draft_B = B;
+  c->draft_gamma = gamma;
+  c->draft_pending = d_pending;
+  c->draft_out = d_draft;
+  return SSD_OK;
+}
+
+int ssd_accept_sample(ssd_ctx* c, int B, int gamma, const int32_t* d_draft,
+                      const float* d_draft_logits, const float* d_target_logits, const float* d_u,
+                      float temperature, int32_t* d_pending, int32_t* d_out,
+                      int32_t* d_accept_len, const int32_t* d_active) {
+  if (!c || !d_target_logits || !d_pending || !d_u ||
+      (gamma > 0 && (!d_draft || !d_draft_logits)))
+    return SSD_ERR_ARG;
+  if (!(temperature > 0.f) || !std::isfinite(temperature)) return SSD_ERR_ARG;
+  if (B < 1 || B > c->d.max_batch || gamma < 0 || gamma > c->d.max_gamma) return SSD_ERR_SHAPE;
+  if (!c->prefilled) return SSD_ERR_STATE;
+  AcceptSampleArgs a;
+  a.B = B; a.gamma = gamma; a.vocab = c->d.vocab; a.draft = d_draft;
+  a.draft_logits = d_draft_logits; a.target_logits = d_target_logits; a.u = d_u;
+  a.inv_tau = 1.0f / temperature; a.pending = d_pending; a.out = d_out;
+  a.accept_len = d_accept_len; a.active = d_active; a.seq_len = c->kv.seq_len;
+  a.max_seq = c->d.max_seq; a.status = c->at<int32_t>(c->L.status);
+  HIP_TRY(launch_accept_sample(a, c->stream));
+  c->draft_valid = false;
   return SSD_OK;
 }
 

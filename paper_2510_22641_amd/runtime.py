@@ -210,6 +210,25 @@ class DeviceDecoder:
         self._call(abi.ssd_accept, self.ctx, B, gamma, draft, target, pending, out, alen, active)
         return out, alen
 
+    def draft_sample(self, pending: torch.Tensor, gamma: int, u: torch.Tensor, temperature: float):
+        """Sampled drafts (u [B, gamma] float32 uniforms); returns (draft, draft logits)."""
+        B = pending.shape[0]
+        d = self.buf("draft", (B, gamma))
+        lg = self.buf("draft_logits", (B, gamma, self.shape.vocab), torch.float32)
+        self._call(abi.ssd_draft_sample, self.ctx, B, gamma, pending, u, temperature, d, lg)
+        return d, lg
+
+    def accept_sample(self, draft, draft_logits, target_logits, u: torch.Tensor,
+                      temperature: float, pending, gamma: int, active=None):
+        """Speculative-sampling acceptance (u [B, gamma + 1]); overwrites ``pending`` in place and
+        returns (out, accept_len)."""
+        B = pending.shape[0]
+        out = self.buf("accept_out", (B, gamma + 1))
+        alen = self.buf("accept_len", (B,))
+        self._call(abi.ssd_accept_sample, self.ctx, B, gamma, draft, draft_logits, target_logits,
+                   u, temperature, pending, out, alen, active)
+        return out, alen
+
     def generate(self, prompt, visual, T: int, gamma: int, speculative: bool = True,
                  reuse: bool = True, dynamic: bool = False):
         """ssd_generate; with dynamic=True gamma is d(0) of the context-length schedule."""

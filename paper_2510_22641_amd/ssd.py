@@ -71,6 +71,8 @@ def _load():
         "ssd_draft": (c_int, [P, c_int, c_int, P, P, P]),
         "ssd_verify": (c_int, [P, c_int, c_int, P, P, c_int, P, P]),
         "ssd_accept": (c_int, [P, c_int, c_int, P, P, P, P, P, P]),
+        "ssd_draft_sample": (c_int, [P, c_int, c_int, P, P, ctypes.c_float, P, P]),
+        "ssd_accept_sample": (c_int, [P, c_int, c_int, P, P, P, P, ctypes.c_float, P, P, P, P]),
         "ssd_generate": (c_int, [P, c_int, c_int, P, P, c_int, c_int, c_int, c_int, P,
                                  POINTER(c_int64)]),
         "ssd_dynamic_gamma": (c_int, [c_int, c_int, c_int]),
@@ -93,7 +95,7 @@ def _load():
 
 _lib = _load()
 EXPORTS = ("ssd_workspace_bytes", "ssd_create", "ssd_prefill", "ssd_draft", "ssd_verify",
-           "ssd_accept", "ssd_generate", "ssd_dynamic_gamma", "ssd_set_graphs", "ssd_set_persistent", "ssd_set_hidden_export",
+           "ssd_accept", "ssd_draft_sample", "ssd_accept_sample", "ssd_generate", "ssd_dynamic_gamma", "ssd_set_graphs", "ssd_set_persistent", "ssd_set_hidden_export",
            "ssd_profile_enable",
            "ssd_profile_read", "ssd_sync_status",
            "ssd_status_string", "ssd_destroy")
@@ -151,6 +153,19 @@ def ssd_accept(ctx, B, gamma, d_draft, d_target, d_pending, d_out=None, d_accept
                d_active=None):
     _check("ssd_accept", _lib.ssd_accept(ctx, B, gamma, _p(d_draft), _p(d_target), _p(d_pending),
                                          _p(d_out), _p(d_accept_len), _p(d_active)))
+
+
+def ssd_draft_sample(ctx, B, gamma, d_pending, d_u, temperature, d_draft, d_draft_logits):
+    _check("ssd_draft_sample", _lib.ssd_draft_sample(ctx, B, gamma, _p(d_pending), _p(d_u),
+                                                     float(temperature), _p(d_draft),
+                                                     _p(d_draft_logits)))
+
+
+def ssd_accept_sample(ctx, B, gamma, d_draft, d_draft_logits, d_target_logits, d_u, temperature,
+                      d_pending, d_out=None, d_accept_len=None, d_active=None):
+    _check("ssd_accept_sample", _lib.ssd_accept_sample(
+        ctx, B, gamma, _p(d_draft), _p(d_draft_logits), _p(d_target_logits), _p(d_u),
+        float(temperature), _p(d_pending), _p(d_out), _p(d_accept_len), _p(d_active)))
 
 
 def ssd_generate(ctx, B, P, d_prompt, d_visual, T, gamma, mode, reuse_hidden, d_tokens):

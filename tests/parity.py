@@ -148,3 +148,104 @@ def workload_inputs(wl, seed: int, batch: Optional[int] = None):
     z = synth.make_visual(wl.shape, seed, B)
     pr = synth.make_prompts(wl.shape, seed, B, wl.prompt_len)
     return w, z, pr
+
+
+# ---- the sampling variant (speculative sampling) --------------------------------------------
+
+@dataclass
+class SampledDevRound:
+    drafts: np.ndarray        # [gamma]
+    accepted: int
+    token: int
+    draft_logits: np.ndarray  # [gamma, V]
+    target_logits: np.ndarray  # [gamma+1, V]
+
+
+@dataclass
+class SampledDevRun:
+    pending0: int
+    rounds: List[SampledDevRound] = field(default_factory=list)
+    tokens: List[int] = field(default_factory=list)
+
+
+def device_run_sampled(dd, prompt_t, visual_t, T: int, gamma: int, tau: float, uniforms,
+                       reuse: bool = True) -> SampledDevRun:
+    """One sequence through prefill / ssd_draft_sample / ssd_verify / ssd_accept_sample with
+    uniforms [rounds, 2 gamma + 1] (draft samples, acceptance tests, the extra sample)."""
+    import torch
+    pending, _ = dd.prefill(prompt_t, visual_t)
+    run = SampledDevRun(int(pending.cpu().numpy()[0]))
+    run.tokens = [run.pending0]
+    r = 0
+    while len(run.tokens) < T:
+        u = np.asarray(uniforms[r], dtype=np.float32)
+        ud = torch.from_numpy(u[None, :gamma].copy()).to(pending.device)
+        ua = torch.from_numpy(u[None, gamma:].copy()).to(pending.device)
+        d, dl = dd.draft_sample(pending, gamma, ud, tau)
+        t, tl = dd.verify(pending, d, gamma, reuse=reuse, logits=True)
+        out, alen = dd.accept_sample(d, dl, tl, ua, tau, pending, gamma)
+        a = int(alen.cpu().numpy()[0])
+        o = out.cpu().numpy()[0]
+        run.rounds.append(SampledDevRound(d.cpu().numpy()[0].copy(), a, int(o[a]),
+                                          dl.cpu().numpy()[0].copy(), tl.cpu().numpy()[0].copy()))
+        run.tokens.extend(int(x) for x in o[: a + 1])
+        r += 1
+    run.tokens = run.tokens[:T]
+    return run
+
+
+def _check_cdf_pick(k: int, weights, u: float, ftol: float, what: str) -> bool:
+    """The device's inverse-CDF pick k from weights with uniform u, where the oracle's cumulative
+    distribution may be off by ftol: u must lie within ftol of k's interval.  True when k is
+    exactly the oracle's pick."""
+    from oracle import sampling
+    w = np.asarray(weights, dtype=np.float64)
+    c = np.cumsum(w) / w.sum()
+    lo = c[k - 1] if k > 0 else 0.0
+    assert w[k] > 0 or ftol > 0, f"{what}: picked a zero-weight entry {k}"
+    assert lo - ftol <= u <= c[k] + ftol, (f"{what}: device picked {k}, u {u:.6f} outside "
+                                          f"[{lo:.6f}, {c[k]:.6f}] +- {ftol:.2g}")
+    return k == sampling.sample_index(w, u)
+
+
+def check_sampled_run(dec, shape, prompt, visual, run: SampledDevRun, gamma: int, tau: float,
+                      uniforms) -> int:
+    """Replay a sampled device run through the oracle; returns the count of decisions taken
+    within the tolerance band (where the oracle's own decision differs)."""
+    from oracle import sampling
+    orounds = sampling.replay_sampled(dec, prompt, visual, run.pending0,
+                                      [(r.drafts, r.accepted, r.token) for r in run.rounds], gamma)
+    close = 0
+    for k, (r, o) in enumerate(zip(run.rounds, orounds)):
+        u = np.asarray(uniforms[k], dtype=np.float64)
+        q_rows, p_rows, ftols = [], [], []
+        for i in range(gamma):
+            check_logits(r.draft_logits[i], o.draft_logits[i], shape, f"round {k} draft {i} logits")
+            q_rows.append(sampling.distribution(o.draft_logits[i], tau))
+        for j in range(gamma + 1):
+            check_logits(r.target_logits[j], o.target_logits[j], shape, f"round {k} verify {j} logits")
+            p_rows.append(sampling.distribution(o.target_logits[j], tau))
+            ftols.append(4.0 * tolerance(shape, o.target_logits[j]) / tau + 1e-6)
+        ftol = max(ftols + [4.0 * tolerance(shape, lg) / tau + 1e-6 for lg in o.draft_logits])
+        for i in range(gamma):
+            close += not _check_cdf_pick(int(r.drafts[i]), q_rows[i], u[i], ftol,
+                                         f"round {k} draft {i}")
+        # acceptance decisions: the oracle's, except within the tolerance band
+        for i in range(min(r.accepted + 1, gamma)):
+            x = int(r.drafts[i])
+            lhs, rhs = u[gamma + i] * q_rows[i][x], p_rows[i][x]
+            dev_accept = i < r.accepted
+            if (lhs < rhs) != dev_accept:
+                assert abs(np.log(max(lhs, 1e-300)) - np.log(max(rhs, 1e-300))) <= 2 * ftol, (
+                    f"round {k} draft {i}: device {'accepted' if dev_accept else 'rejected'}, "
+                    f"oracle u q = {lhs:.3g} vs p = {rhs:.3g}")
+                close += 1
+        a = r.accepted
+        if a < gamma:
+            w = np.maximum(p_rows[a] - q_rows[a], 0.0)
+            if not w.sum() > 0:
+                w = p_rows[a]
+        else:
+            w = p_rows[gamma]
+        close += not _check_cdf_pick(int(r.token), w, u[2 * gamma], 2 * ftol, f"round {k} token")
+    return close
