@@ -374,7 +374,9 @@ def main():
 
     # speculative sampling against plain sampling from the full model, same build and uniforms
     sampling = []
-    for tau in [float(x) for x in args.sample_temps.split(",") if x.strip()]:
+    temps = [] if args.sample_temps.strip() in ("", "=", "none") else \
+        [float(x) for x in args.sample_temps.split(",") if x.strip()]
+    for tau in temps:
         u_ssd = synth.make_uniforms(args.seed, 1, T, 2 * g + 1)[0]
         u_full = synth.make_uniforms(args.seed + 1, 1, T, 1)[0]
         sampled_decode(dd, pt[:1], vt[:1], T, g, tau, u_ssd)  # warm-up (graph capture)
