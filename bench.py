@@ -140,25 +140,28 @@ def sweep_c4(args):
     # one context per (draft depth, batch): a one-sequence context folds the cross-attention
     for k, mb in sorted({(p.draft_layers, p.batch) for p in pts}):
         group = [p for p in pts if p.draft_layers == k and p.batch == mb]
+        gm = max(p.gamma for p in group)
+        # room for drafts made ahead (2 gamma positions past a round's start)
         dd = runtime.from_workload(group[0], args.seed, weights=weights, max_batch=mb,
-                                   max_gamma=max(p.gamma for p in group))
+                                   max_gamma=gm, extra_seq=gm)
         for wl in group:
             sh, B, T, g = wl.shape, wl.batch, wl.new_tokens, wl.gamma
             prompts = synth.make_prompts(sh, args.seed, B, wl.prompt_len)
             visual = synth.make_visual(sh, args.seed, B)
             pt, vt = dd.upload_inputs(prompts, visual)
 
-            def timed(spec):
+            def timed(spec, ahead=False):
                 for _ in range(args.warmup):
-                    dd.generate(pt, vt, T, g, speculative=spec, reuse=True)
+                    dd.generate(pt, vt, T, g, speculative=spec, reuse=True, ahead=ahead)
                 torch.cuda.synchronize()
                 t0 = time.perf_counter()
                 for _ in range(args.steps):
-                    toks, st = dd.generate(pt, vt, T, g, speculative=spec, reuse=True)
+                    toks, st = dd.generate(pt, vt, T, g, speculative=spec, reuse=True, ahead=ahead)
                 torch.cuda.synchronize()
                 return time.perf_counter() - t0, st, toks
 
             dt, st, toks = timed(True)
+            dta, sta, toksa = timed(True, ahead=True)
             dtg, _, gtoks = timed(False)
             d_s, v_s, ctx = step_timings(dd, pt, vt, B, g)
             db = draft_step_bytes(sh, k, ctx, dd.k_pool.element_size(), cross_folded(sh, mb))
@@ -171,6 +174,8 @@ def sweep_c4(args):
                    "speedup_vs_greedy": round(dtg / dt, 3),
                    "acceptance_rate": round(st["accepted"] / max(1, st["drafted"]), 4),
                    "ssd_equals_greedy_tokens": bool(torch.equal(toks, gtoks)),
+                   "drafting_ahead_tokens_per_s": round(B * T * args.steps / dta, 2),
+                   "drafting_ahead_equals_one_stream": bool(torch.equal(toksa, toks)) and sta == st,
                    "draft_step": {"us": round(d_s * 1e6, 2), "bytes": int(db),
                                   "frac": round(db / d_s / 1e9 / HBM_PEAK_GBS, 4)},
                    "verify": {"us": round(v_s * 1e6, 2), "bytes": int(vb),
@@ -260,6 +265,9 @@ def main():
     ap.add_argument("--persistent", type=int, choices=[0, 1], default=None,
                     help="force the persistent one-row pass on (1) or off (0); default: the "
                          "library's choice")
+    ap.add_argument("--schedule", choices=["ahead", "one-stream"], default="one-stream",
+                    help="headline schedule of the decode loop: the next round drafted on a "
+                         "second stream during each verify pass, or one stream")
     ap.add_argument("--sweep", choices=["c4"], default=None,
                     help="run the FlanT5-xl sweep instead (one JSON line per point)")
     ap.add_argument("--copy-bytes", type=int, default=0,
@@ -306,20 +314,33 @@ def main():
 
     B, T, g = wl.batch, wl.new_tokens, wl.gamma
 
-    def timed(speculative: bool, steps: int, warmup: int, dynamic: bool = False):
+    def timed(speculative: bool, steps: int, warmup: int, dynamic: bool = False,
+              ahead: bool = False):
         for _ in range(warmup):
-            dd.generate(pt, vt, T, g, speculative=speculative, reuse=True, dynamic=dynamic)
+            dd.generate(pt, vt, T, g, speculative=speculative, reuse=True, dynamic=dynamic,
+                        ahead=ahead)
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         stats = None
         for _ in range(steps):
             toks, stats = dd.generate(pt, vt, T, g, speculative=speculative, reuse=True,
-                                      dynamic=dynamic)
+                                      dynamic=dynamic, ahead=ahead)
         torch.cuda.synchronize()
         return time.perf_counter() - t0, stats, toks
 
-    dt, st, toks_ssd = timed(True, args.steps, args.warmup)
-    ssd_tps = B * T * args.steps / dt
+    # Algorithm 1 on one stream, and with the next round drafted on a second stream while each
+    # verify pass runs (same tokens and acceptance, checked below)
+    dt1, st1, toks_one = timed(True, args.steps, args.warmup)
+    one_tps = B * T * args.steps / dt1
+    print(f"[bench] ssd one stream {one_tps:.1f} tok/s", file=sys.stderr, flush=True)
+    dta, sta, toks_ahead = timed(True, args.steps, args.warmup, ahead=True)
+    ahead_tps = B * T * args.steps / dta
+    print(f"[bench] ssd drafting ahead {ahead_tps:.1f} tok/s", file=sys.stderr, flush=True)
+    ahead_same = bool(torch.equal(toks_ahead, toks_one)) and sta == st1
+    if args.schedule == "ahead":
+        dt, st, toks_ssd, ssd_tps = dta, sta, toks_ahead, ahead_tps
+    else:
+        dt, st, toks_ssd, ssd_tps = dt1, st1, toks_one, one_tps
     alpha = st["accepted"] / max(1, st["drafted"])
     print(f"[bench] ssd {ssd_tps:.1f} tok/s alpha {alpha:.3f}", file=sys.stderr, flush=True)
     dtg, _, toks_greedy = timed(False, args.steps, 1)
@@ -450,6 +471,12 @@ def main():
                    "draft_layers": wl.draft_layers, "gamma": g, "new_tokens": T,
                    "deep_scale": wl.deep_scale, "parallelism": "none (1 GPU)"},
         "acceptance_rate": round(alpha, 4),
+        "schedule": ("next round drafted on a second stream during each verify pass"
+                     if args.schedule == "ahead" else "one stream"),
+        "one_stream_tokens_per_s": round(one_tps, 2),
+        "drafting_ahead_tokens_per_s": round(ahead_tps, 2),
+        "drafting_ahead_equals_one_stream": ahead_same,
+        "rounds": st["rounds"],
         "greedy_tokens_per_s": round(greedy_tps, 2),
         "speedup_vs_greedy": round(ssd_tps / greedy_tps, 3),
         "ssd_equals_greedy_tokens": same,

@@ -53,7 +53,12 @@ enum {
 
 enum { SSD_ARCH_T5 = 0, SSD_ARCH_LLAMA = 1 };
 enum { SSD_F32 = 0, SSD_BF16 = 1 };
-enum { SSD_MODE_GREEDY = 0, SSD_MODE_SPECULATIVE = 1, SSD_MODE_SPECULATIVE_DYNAMIC = 2 };
+enum {
+  SSD_MODE_GREEDY = 0,
+  SSD_MODE_SPECULATIVE = 1,
+  SSD_MODE_SPECULATIVE_DYNAMIC = 2,
+  SSD_MODE_SPECULATIVE_AHEAD = 3
+};
 
 /* device status bits (ssd_sync_status, ssd_device_status); SSD_DEV_SYNC: a grid-barrier wait of
  * the persistent one-row pass exceeded its bound (ssd_set_persistent) */
@@ -215,6 +220,16 @@ int ssd_accept_sample(ssd_ctx* ctx, int B, int gamma, const int32_t* d_draft,
  * SSD_MODE_SPECULATIVE_DYNAMIC drafts ssd_dynamic_gamma(t, gamma, max_seq) tokens per round
  * (appendix on the choice of d: d grows with the context length t), t = the shortest context
  * length among the sequences still active at the start of the round; gamma + 9 <= max_gamma.
+ * SSD_MODE_SPECULATIVE_AHEAD is Algorithm 1 with fixed gamma and the layer-k reuse (reuse_hidden
+ * is implied), scheduled over two streams: while the verify pass of a round runs on the context's
+ * stream, a second stream owned by the library (created on first use, default priority) drafts
+ * the next round on the assumption that all gamma drafts pass and that the full model's extra
+ * token equals the draft model's next token after the last draft (the imitation network and g on
+ * the verify pass's layer-k row of the last position).  When every sequence still active meets
+ * both, the next round skips its draft steps; otherwise it drafts as usual.  Tokens, acceptance
+ * and h_stats are identical to SSD_MODE_SPECULATIVE with reuse; only the time differs.  Needs
+ * prefix + prompt + T + 2 gamma <= max_seq (else SSD_ERR_CAPACITY) and no hidden-state export
+ * (else SSD_ERR_STATE).
  * h_stats (host, may be NULL) receives {rounds, sum over sequences of accepted drafts, sum of
  * drafted tokens}.  Synchronises the stream once per round to test for completion. */
 int ssd_generate(ssd_ctx* ctx, int B, int P, const int32_t* d_prompt, const void* d_visual, int T,

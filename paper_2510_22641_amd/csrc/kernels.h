@@ -251,7 +251,10 @@ struct AcceptArgs {
   int32_t* active_rw;     // [B] cleared when count reaches T
   int T;
   int64_t* stats;         // [3]: rounds (added by thread 0), accepted, drafted
-  int32_t* n_active;      // [2]: sequences still active, shortest seq_len among them
+  int32_t* n_active;      // [3]: sequences still active, shortest seq_len among them, and (with
+                          // guess) 1 when every sequence still active accepted all gamma drafts
+                          // and its new pending token equals guess[b], else 0
+  const int32_t* guess;   // [B] or null: the token the drafts made ahead start from
 };
 hipError_t launch_accept(const AcceptArgs& a, hipStream_t s);
 

@@ -143,11 +143,13 @@ __global__ void accept_kernel(const AcceptArgs a) {
   __shared__ int acc_n[256];
   __shared__ int act_after[256];
   __shared__ int len_after[256];
+  __shared__ int ahead_ok[256];
   const int b = threadIdx.x;
   const int g = a.gamma;
   int n = 0;
   int still = 0;
   bool did = false;
+  int ok = 1;
   if (b < a.B) {
     bool act = a.active ? (a.active[b] != 0) : true;
     if (a.active_rw) act = act && (a.active_rw[b] != 0);
@@ -181,6 +183,7 @@ __global__ void accept_kernel(const AcceptArgs a) {
       const int sl = a.seq_len[b] + adv;
       a.seq_len[b] = sl;
       if (sl + (still ? a.next_need : 0) > a.max_seq) atomicOr(a.status, SSD_DEV_CAPACITY);
+      if (still && a.guess) ok = (n == g && tg[n] == a.guess[b]) ? 1 : 0;
     } else if (a.active_rw) {
       still = 0;
     }
@@ -188,6 +191,7 @@ __global__ void accept_kernel(const AcceptArgs a) {
   acc_n[b] = did ? n : -1;
   act_after[b] = still;
   len_after[b] = (b < a.B && still) ? a.seq_len[b] : INT_MAX;
+  ahead_ok[b] = ok;
   __syncthreads();
   if (b == 0 && a.stats) {
     long long sa = 0, sd = 0;
@@ -203,6 +207,11 @@ __global__ void accept_kernel(const AcceptArgs a) {
     if (a.n_active) {
       a.n_active[0] = na;
       a.n_active[1] = na ? lmin : 0;
+      if (a.guess) {
+        int all = na > 0 ? 1 : 0;
+        for (int t = 0; t < a.B && t < 256; ++t) all &= ahead_ok[t];
+        a.n_active[2] = all;
+      }
     }
   }
 }
@@ -226,6 +235,7 @@ __global__ void gen_init_kernel(const GenInitArgs a) {
     }
     a.n_active[0] = na;
     a.n_active[1] = na ? lmin : 0;
+    a.n_active[2] = 0;
     a.stats[0] = a.stats[1] = a.stats[2] = 0;
   }
 }

@@ -33,7 +33,8 @@ struct Layout {
   size_t x, x1, qkv, q, attn, ffn, inh, xi, stash, vis, part_val, part_idx, stats, bias_tab,
       p_x, p_attn, p_ffn, ssq, attn_part, fold_q, fold_o,
       bucket, rope_cos, rope_sin, status, cur_tok, g_pending, g_draft, g_target,
-      g_count, g_active, g_nactive, g_stats, step_prog, step_arena, step_sync, total;
+      g_count, g_active, g_nactive, g_stats, g_draft2, g_guess, step_prog, step_arena, step_sync,
+      total;
   int rows_max, head_rows, parts_max, ctx_max, plane_rows, attn_rows;
 };
 
@@ -91,7 +92,12 @@ size_t step_arena_floats(const ssd_dims& d) {
   return per * d.n_layers + a(d.in_hidden) + a(D) + 256;
 }
 
-bool make_layout(const ssd_dims& d, Layout& L) {
+// Workspace layout.  The scratch a chain of launches writes (residual rows, projections, operand
+// planes, argmax partials, the layer-k stash ...) comes in two lanes: lane 0 for every call on the
+// context's stream, lane 1 (sized for one-row steps of the batch) for the drafts made ahead on the
+// second stream while a verify pass runs (SSD_MODE_SPECULATIVE_AHEAD).  L1 is L with the lane
+// fields moved to lane 1; tables, folded cross-attention and the loop state are shared.
+bool make_layout(const ssd_dims& d, Layout& L, Layout& L1) {
   const size_t B = d.max_batch, G = d.max_gamma, D = d.d_model, HD = (size_t)d.n_heads * d.d_head;
   L.ctx_max = ctx_len_max(d);
   size_t rows = B * (G + 1);
@@ -100,21 +106,6 @@ bool make_layout(const ssd_dims& d, Layout& L) {
   L.rows_max = (int)rows;
   L.head_rows = (int)(B * (G + 1));
   L.parts_max = argmax_parts_max(d.vocab);
-  size_t off = 0;
-  auto take = [&](size_t bytes) { size_t o = off; off = align_up(off + bytes, 256); return o; };
-  L.x = take(rows * D * 4);
-  L.x1 = take(B * D * 4);
-  L.qkv = take(rows * 3 * HD * 4);
-  L.q = take(rows * HD * 4);
-  L.attn = take(rows * HD * 4);
-  L.ffn = take(rows * (size_t)d.d_ff * 4);
-  L.inh = take(B * (size_t)d.in_hidden * 4);
-  L.xi = take(B * D * 4);
-  L.stash = take(B * (G + 1) * D * 4);
-  L.vis = take(d.arch == SSD_ARCH_T5 ? B * (size_t)d.n_visual * D * 4 : 0);
-  L.part_val = take((size_t)L.head_rows * L.parts_max * 4);
-  L.part_idx = take((size_t)L.head_rows * L.parts_max * 4);
-  L.stats = take(rows * 8);
   // bf16 hi / lo operand planes of the skinny MFMA path (plane_rows rows each: the largest verify
   // chunk, rounded up to 16, at most 128) and its partial sums of squares
   {
@@ -122,14 +113,33 @@ bool make_layout(const ssd_dims& d, Layout& L) {
     pr = pr < 16 ? 16 : (pr > 128 ? 128 : (pr + 15) / 16 * 16);
     L.plane_rows = (int)pr;
   }
-  const size_t PRz = (size_t)L.plane_rows;
-  L.p_x = take(2 * PRz * D * 2);
-  L.p_attn = take(2 * PRz * HD * 2);
-  L.p_ffn = take(2 * PRz * (size_t)d.d_ff * 2);
-  L.ssq = take((size_t)skinny_blocks((int)D) * PRz * 4);
   // key-split partials of the long-context attention (up to 16 query rows per sequence)
   L.attn_rows = (int)(B * 16);
-  L.attn_part = take((size_t)L.attn_rows * d.n_heads * ATTN_SPLITS_MAX * (d.d_head + 2) * 4);
+  size_t off = 0;
+  auto take = [&](size_t bytes) { size_t o = off; off = align_up(off + bytes, 256); return o; };
+  auto lane = [&](Layout& X, size_t R, size_t head_rows) {
+    const size_t PRz = (size_t)L.plane_rows;
+    X.x = take(R * D * 4);
+    X.x1 = take(B * D * 4);
+    X.qkv = take(R * 3 * HD * 4);
+    X.q = take(R * HD * 4);
+    X.attn = take(R * HD * 4);
+    X.ffn = take(R * (size_t)d.d_ff * 4);
+    X.inh = take(B * (size_t)d.in_hidden * 4);
+    X.xi = take(B * D * 4);
+    X.stash = take(B * (G + 1) * D * 4);
+    X.part_val = take(head_rows * L.parts_max * 4);
+    X.part_idx = take(head_rows * L.parts_max * 4);
+    X.stats = take(R * 8);
+    X.p_x = take(2 * PRz * D * 2);
+    X.p_attn = take(2 * PRz * HD * 2);
+    X.p_ffn = take(2 * PRz * (size_t)d.d_ff * 2);
+    X.ssq = take((size_t)skinny_blocks((int)D) * PRz * 4);
+    X.attn_part = take((size_t)L.attn_rows * d.n_heads * ATTN_SPLITS_MAX * (d.d_head + 2) * 4);
+    X.cur_tok = take(B * 4);
+  };
+  lane(L, rows, (size_t)L.head_rows);
+  L.vis = take(d.arch == SSD_ARCH_T5 ? B * (size_t)d.n_visual * D * 4 : 0);
   {
     const size_t fold = fold_cross(d) ? (size_t)d.n_layers * d.n_heads * d.n_visual * D * 4 : 0;
     L.fold_q = take(fold);
@@ -140,13 +150,14 @@ bool make_layout(const ssd_dims& d, Layout& L) {
   L.rope_cos = take(d.arch == SSD_ARCH_LLAMA ? (size_t)d.max_seq * (d.d_head / 2) * 4 : 0);
   L.rope_sin = take(d.arch == SSD_ARCH_LLAMA ? (size_t)d.max_seq * (d.d_head / 2) * 4 : 0);
   L.status = take(4);
-  L.cur_tok = take(B * 4);
   L.g_pending = take(B * 4);
   L.g_draft = take(B * (G > 0 ? G : 1) * 4);
+  L.g_draft2 = take(B * (G > 0 ? G : 1) * 4);
+  L.g_guess = take(B * 4);
   L.g_target = take(B * (G + 1) * 4);
   L.g_count = take(B * 4);
   L.g_active = take(B * 4);
-  L.g_nactive = take(8);
+  L.g_nactive = take(16);
   L.g_stats = take(3 * 8);
   {
     const bool st = step_dims_ok(d);
@@ -154,7 +165,9 @@ bool make_layout(const ssd_dims& d, Layout& L) {
     L.step_arena = take(st ? step_arena_floats(d) * 4 : 0);
     L.step_sync = take(st ? SYNC_BYTES : 0);
   }
-  L.total = off;
+  L1 = L;
+  lane(L1, B, B);
+  L.total = L1.total = off;
   return true;
 }
 
@@ -202,6 +215,11 @@ struct ssd_ctx {
   hipStream_t stream;
   char* ws;
   Layout L;
+  // drafts made ahead while a verify pass runs: lane-1 scratch, a second stream (created on first
+  // use, default priority) and the fork / join events between the two streams
+  Layout L1;
+  hipStream_t stream1 = nullptr;
+  hipEvent_t ev_fork = nullptr, ev_join = nullptr;
   bool prefilled = false;
   bool fold_ready = false;  // fold_q / fold_o hold the prefilled sequence's cross-attention
   // reuse bookkeeping: the last ssd_draft's arguments
@@ -246,6 +264,21 @@ struct ssd_ctx {
   } while (0)
 
 namespace {
+
+// The launches of its scope go to lane 1: the second stream and the lane-1 scratch.
+struct OnLane1 {
+  ssd_ctx* c;
+  Layout L;
+  hipStream_t s;
+  explicit OnLane1(ssd_ctx* ctx) : c(ctx), L(ctx->L), s(ctx->stream) {
+    c->L = c->L1;
+    c->stream = c->stream1;
+  }
+  ~OnLane1() {
+    c->L = L;
+    c->stream = s;
+  }
+};
 
 PagedKV paged(ssd_ctx* c, int l, int pos_off) {
   PagedKV p;
@@ -652,21 +685,47 @@ int run_head(ssd_ctx* c, const float* x, int ldx, int M, int C, float* logits, i
   return SSD_OK;
 }
 
+// Imitation network on the layer-k rows xk [B][D]: LN -> FC1 + b1 -> GELU into inh, then
+// FC2 + b2 (+ xk when residual) into xi.  `between` runs after FC1 (the hidden-state export).
+template <typename F>
+int run_imitation(ssd_ctx* c, const float* xk, int B, F between) {
+  const ssd_dims& d = c->d;
+  const int D = d.d_model;
+  float* inh = c->at<float>(c->L.inh);
+  LinearArgs a = lin(c);
+  a.x = xk; a.ldx = D; a.M = B; a.K = D;
+  a.norm = NORM_LN; a.gain = c->w.in_ln_w; a.shift = c->w.in_ln_b; a.eps = d.ln_eps;
+  a.w[0] = c->w.in_w1; a.n_per = d.in_hidden; a.epi = EPI_BIAS_GELU; a.bias = c->w.in_b1;
+  a.y = inh; a.ldy = d.in_hidden;
+  HIP_TRY(run_linear(c, a));
+  HIP_TRY(between());
+  a = lin(c);
+  a.x = inh; a.ldx = d.in_hidden; a.M = B; a.K = d.in_hidden;
+  a.w[0] = c->w.in_w2; a.n_per = D; a.epi = EPI_BIAS_RESID; a.bias = c->w.in_b2;
+  a.resid = d.in_residual ? xk : nullptr; a.ldr = D; a.y = c->at<float>(c->L.xi); a.ldy = D;
+  HIP_TRY(run_linear(c, a));
+  return SSD_OK;
+}
+
+// gamma draft steps from `pending`; step i runs at positions seq_len + pos_base + i and leaves
+// its layer-k rows in stash_out (the lane's stash when null).  allow_step = false keeps the
+// chain of kernels (the persistent pass needs the whole device).
 int draft_launches(ssd_ctx* c, int B, int gamma, const int32_t* pending, int32_t* draft,
-                   float* logits, const float* u = nullptr, float tau = 0.f) {
+                   float* logits, const float* u = nullptr, float tau = 0.f, int pos_base = 0,
+                   float* stash_out = nullptr, bool allow_step = true) {
   const ssd_dims& d = c->d;
   const int D = d.d_model;
   float* x = c->at<float>(c->L.x);
   float* inh = c->at<float>(c->L.inh);
   float* xi = c->at<float>(c->L.xi);
-  float* stash = c->at<float>(c->L.stash);
+  float* stash = stash_out ? stash_out : c->at<float>(c->L.stash);
   int32_t* cur = c->at<int32_t>(c->L.cur_tok);
   const int ld_stash = (d.max_gamma + 1) * D;
-  if (use_step_now(c, B) && !u) {
+  if (allow_step && use_step_now(c, B) && !u) {
     for (int i = 0; i < gamma; ++i) {
       StepArgs a = step_args(c, STEP_DRAFT);
       a.tok = i == 0 ? pending : cur;
-      a.pos_off = i;
+      a.pos_off = pos_base + i;
       a.stash = stash + (size_t)i * D;
       a.dst0 = draft + i;
       a.dst1 = cur;
@@ -683,28 +742,19 @@ int draft_launches(ssd_ctx* c, int B, int gamma, const int32_t* pending, int32_t
     e.visual = nullptr; e.n_visual = d.n_visual; e.n_prefix = 0;
     e.status = c->at<int32_t>(c->L.status);
     HIP_TRY(launch_embed(e, c->stream));
-    int rc = run_layers(c, x, B, 1, i, 0, d.draft_layers, d.draft_layers - 1, stash + (size_t)i * D,
-                        ld_stash);
+    int rc = run_layers(c, x, B, 1, pos_base + i, 0, d.draft_layers, d.draft_layers - 1,
+                        stash + (size_t)i * D, ld_stash);
     if (rc) return rc;
-    // imitation network: LN -> FC1 + b1 -> GELU -> FC2 + b2 (+ x)
-    LinearArgs a = lin(c);
-    a.x = x; a.ldx = D; a.M = B; a.K = D;
-    a.norm = NORM_LN; a.gain = c->w.in_ln_w; a.shift = c->w.in_ln_b; a.eps = d.ln_eps;
-    a.w[0] = c->w.in_w1; a.n_per = d.in_hidden; a.epi = EPI_BIAS_GELU; a.bias = c->w.in_b1;
-    a.y = inh; a.ldy = d.in_hidden;
-    HIP_TRY(run_linear(c, a));
-    if (c->ex_phi) {
+    rc = run_imitation(c, x, B, [&]() -> hipError_t {
+      if (!c->ex_phi) return hipSuccess;
       // export: the imitation network's hidden features of step i, [B][gamma][in_hidden]
-      HIP_TRY(launch_copy_rows(c->ex_phi + (size_t)i * d.in_hidden, gamma * d.in_hidden, inh,
-                               d.in_hidden, B, d.in_hidden, c->stream));
-      HIP_TRY(launch_copy_rows(c->ex_xk + (size_t)i * D, gamma * D, stash + (size_t)i * D, ld_stash,
-                               B, D, c->stream));
-    }
-    a = lin(c);
-    a.x = inh; a.ldx = d.in_hidden; a.M = B; a.K = d.in_hidden;
-    a.w[0] = c->w.in_w2; a.n_per = D; a.epi = EPI_BIAS_RESID; a.bias = c->w.in_b2;
-    a.resid = d.in_residual ? x : nullptr; a.ldr = D; a.y = xi; a.ldy = D;
-    HIP_TRY(run_linear(c, a));
+      hipError_t err = launch_copy_rows(c->ex_phi + (size_t)i * d.in_hidden, gamma * d.in_hidden,
+                                        inh, d.in_hidden, B, d.in_hidden, c->stream);
+      if (err != hipSuccess) return err;
+      return launch_copy_rows(c->ex_xk + (size_t)i * D, gamma * D, stash + (size_t)i * D, ld_stash,
+                              B, D, c->stream);
+    });
+    if (rc) return rc;
     rc = run_head(c, xi, D, B, 1, logits ? logits + (size_t)i * d.vocab : nullptr,
                   gamma * d.vocab, draft, gamma, i, cur, u, gamma, i, tau);
     if (rc) return rc;
@@ -712,17 +762,63 @@ int draft_launches(ssd_ctx* c, int B, int gamma, const int32_t* pending, int32_t
   return SSD_OK;
 }
 
+// The next round's drafts, made while the verify pass of this round runs (lane 1).  They assume
+// that every draft of this round passes and that the full model's extra token equals the draft
+// model's own next token: the imitation network and g on xk_last (the layer-k rows of this
+// round's last position, from the verify pass) give that token (`guess`); gamma draft steps from
+// it, at positions seq_len + gamma + 1 + i, fill `draft` and `stash`.
+int ahead_launches(ssd_ctx* c, int B, int gamma, const float* xk_last, int32_t* guess,
+                   int32_t* draft, float* stash) {
+  const int D = c->d.d_model;
+  int rc = run_imitation(c, xk_last, B, []() { return hipSuccess; });
+  if (rc) return rc;
+  rc = run_head(c, c->at<float>(c->L.xi), D, B, 1, nullptr, 0, guess, 1, 0, nullptr);
+  if (rc) return rc;
+  return draft_launches(c, B, gamma, guess, draft, nullptr, nullptr, 0.f, gamma + 1, stash, false);
+}
+
+// Verify with the layer-k reuse, first part: layers 1..k for the last position only (into x1);
+// the other positions' layer-k rows are the draft's.
+int verify_last_row(ssd_ctx* c, int B, int gamma, const int32_t* draft) {
+  const ssd_dims& d = c->d;
+  float* x1 = c->at<float>(c->L.x1);
+  if (use_step_now(c, B)) {
+    StepArgs a = step_args(c, STEP_VROW);
+    a.tok = draft + (gamma - 1);
+    a.pos_off = gamma;
+    return run_step(c, STEP_VROW, a);
+  }
+  EmbedArgs e;
+  e.x = x1; e.B = B; e.C = 1; e.d = d.d_model; e.embed = c->w.embed; e.vocab = d.vocab;
+  e.wdtype = d.wdtype; e.t0 = nullptr; e.t1 = draft + (gamma - 1); e.ld1 = gamma;
+  e.visual = nullptr; e.n_visual = d.n_visual; e.n_prefix = 0;
+  e.status = c->at<int32_t>(c->L.status);
+  HIP_TRY(launch_embed(e, c->stream));
+  return run_layers(c, x1, B, 1, gamma, 0, d.draft_layers, -1, nullptr, 0);
+}
+
+// Second part: the gamma + 1 rows (stash rows 0..gamma-1, then x1) through layers k+1..L, g and
+// the argmax per row.
+int verify_deep(ssd_ctx* c, int B, int gamma, const float* stash, int32_t* target, float* logits) {
+  const ssd_dims& d = c->d;
+  const int D = d.d_model, C = gamma + 1;
+  float* x = c->at<float>(c->L.x);
+  HIP_TRY(launch_assemble(x, stash, (d.max_gamma + 1) * D, c->at<float>(c->L.x1), B, gamma, D,
+                          c->stream));
+  int rc = run_layers(c, x, B, C, 0, d.draft_layers, d.n_layers, -1, nullptr, 0);
+  if (rc) return rc;
+  if (c->ex_xl) {
+    // export: the final residual rows (before g's norm), [B][gamma + 1][d_model]
+    HIP_TRY(launch_copy_rows(c->ex_xl, D, x, D, B * C, D, c->stream));
+  }
+  return run_head(c, x, D, B * C, C, logits, d.vocab, target, C, 0, nullptr);
+}
+
 int verify_launches(ssd_ctx* c, int B, int gamma, const int32_t* pending, const int32_t* draft,
                     int reuse, int32_t* target, float* logits) {
   const ssd_dims& d = c->d;
   const int D = d.d_model, C = gamma + 1;
   float* x = c->at<float>(c->L.x);
-  EmbedArgs e;
-  e.x = x; e.B = B; e.C = C; e.d = D; e.embed = c->w.embed; e.vocab = d.vocab;
-  e.wdtype = d.wdtype; e.t0 = pending; e.t1 = draft; e.ld1 = gamma;
-  e.visual = nullptr; e.n_visual = d.n_visual; e.n_prefix = 0;
-  e.status = c->at<int32_t>(c->L.status);
-  int rc;
   if (gamma == 0 && use_step_now(c, B)) {
     // one greedy step: the whole decoder, g and the argmax in one persistent pass
     StepArgs a = step_args(c, STEP_GREEDY);
@@ -733,31 +829,20 @@ int verify_launches(ssd_ctx* c, int B, int gamma, const int32_t* pending, const 
     a.logits = logits;
     return run_step(c, STEP_GREEDY, a);
   }
-  if (!reuse) {
-    HIP_TRY(launch_embed(e, c->stream));
-    rc = run_layers(c, x, B, C, 0, 0, d.n_layers, -1, nullptr, 0);
+  if (reuse) {
+    const int rc = verify_last_row(c, B, gamma, draft);
     if (rc) return rc;
-  } else {
-    // layers 1..k only for the last position; the others come from the draft's layer-k states
-    float* x1 = c->at<float>(c->L.x1);
-    if (use_step_now(c, B)) {
-      StepArgs a = step_args(c, STEP_VROW);
-      a.tok = draft + (gamma - 1);
-      a.pos_off = gamma;
-      rc = run_step(c, STEP_VROW, a);
-    } else {
-      e.x = x1; e.C = 1; e.t0 = nullptr; e.t1 = draft + (gamma - 1); e.ld1 = gamma;
-      HIP_TRY(launch_embed(e, c->stream));
-      rc = run_layers(c, x1, B, 1, gamma, 0, d.draft_layers, -1, nullptr, 0);
-    }
-    if (rc) return rc;
-    HIP_TRY(launch_assemble(x, c->at<float>(c->L.stash), (d.max_gamma + 1) * D, x1, B, gamma, D,
-                            c->stream));
-    rc = run_layers(c, x, B, C, 0, d.draft_layers, d.n_layers, -1, nullptr, 0);
-    if (rc) return rc;
+    return verify_deep(c, B, gamma, c->at<float>(c->L.stash), target, logits);
   }
+  EmbedArgs e;
+  e.x = x; e.B = B; e.C = C; e.d = D; e.embed = c->w.embed; e.vocab = d.vocab;
+  e.wdtype = d.wdtype; e.t0 = pending; e.t1 = draft; e.ld1 = gamma;
+  e.visual = nullptr; e.n_visual = d.n_visual; e.n_prefix = 0;
+  e.status = c->at<int32_t>(c->L.status);
+  HIP_TRY(launch_embed(e, c->stream));
+  const int rc = run_layers(c, x, B, C, 0, 0, d.n_layers, -1, nullptr, 0);
+  if (rc) return rc;
   if (c->ex_xl) {
-    // export: the final residual rows (before g's norm), [B][gamma + 1][d_model]
     HIP_TRY(launch_copy_rows(c->ex_xl, D, x, D, B * C, D, c->stream));
   }
   return run_head(c, x, D, B * C, C, logits, d.vocab, target, C, 0, nullptr);
@@ -795,8 +880,8 @@ extern "C" {
 
 size_t ssd_workspace_bytes(const ssd_dims* dims) {
   if (!dims_ok(dims)) return 0;
-  Layout L;
-  make_layout(*dims, L);
+  Layout L, L1;
+  make_layout(*dims, L, L1);
   return L.total;
 }
 
@@ -822,8 +907,8 @@ int ssd_create(const ssd_dims* dims, const ssd_weights* w, const ssd_kv* kv, voi
   if (!kv->k_pool || !kv->v_pool || !kv->page_table || !kv->seq_len || kv->n_pages < 1)
     return SSD_ERR_ARG;
   if (t5 && (!kv->xk || !kv->xv)) return SSD_ERR_ARG;
-  Layout L;
-  make_layout(d, L);
+  Layout L, L1;
+  make_layout(d, L, L1);
   if (workspace_bytes < L.total) return SSD_ERR_CAPACITY;
   if (((uintptr_t)d_workspace) % 256) return SSD_ERR_ARG;
 
@@ -837,6 +922,7 @@ int ssd_create(const ssd_dims* dims, const ssd_weights* w, const ssd_kv* kv, voi
   c->stream = reinterpret_cast<hipStream_t>(stream);
   c->ws = reinterpret_cast<char*>(d_workspace);
   c->L = L;
+  c->L1 = L1;
 
   int rc = SSD_OK;
   if (t5) {
@@ -1037,14 +1123,28 @@ int ssd_dynamic_gamma(int t, int d0, int n_max) {
 int ssd_generate(ssd_ctx* c, int B, int P, const int32_t* d_prompt, const void* d_visual, int T,
                  int gamma, int mode, int reuse_hidden, int32_t* d_tokens, int64_t* h_stats) {
   if (!c || !d_tokens || T < 1) return SSD_ERR_ARG;
-  if (mode != SSD_MODE_GREEDY && mode != SSD_MODE_SPECULATIVE && mode != SSD_MODE_SPECULATIVE_DYNAMIC)
+  if (mode != SSD_MODE_GREEDY && mode != SSD_MODE_SPECULATIVE &&
+      mode != SSD_MODE_SPECULATIVE_DYNAMIC && mode != SSD_MODE_SPECULATIVE_AHEAD)
     return SSD_ERR_ARG;
   const bool dynamic = mode == SSD_MODE_SPECULATIVE_DYNAMIC;
+  const bool ahead = mode == SSD_MODE_SPECULATIVE_AHEAD;
   const int g_max = mode == SSD_MODE_GREEDY ? 0 : (dynamic ? gamma + 9 : gamma);
   if (mode != SSD_MODE_GREEDY && (gamma < 1 || g_max > c->d.max_gamma)) return SSD_ERR_SHAPE;
   if (B < 1 || B > c->d.max_batch) return SSD_ERR_SHAPE;
   const int Cx = P + (c->d.arch == SSD_ARCH_T5 ? 0 : c->d.n_visual);
   if (Cx + T + c->d.max_gamma > c->d.max_seq) return SSD_ERR_CAPACITY;
+  // drafts made ahead write up to 2 gamma positions past the round's start
+  if (ahead && Cx + T + 2 * gamma > c->d.max_seq) return SSD_ERR_CAPACITY;
+  if (ahead && c->ex_phi) return SSD_ERR_STATE;
+  if (ahead && !c->stream1) {
+    if (hipStreamCreateWithFlags(&c->stream1, hipStreamNonBlocking) != hipSuccess) {
+      c->stream1 = nullptr;
+      return SSD_ERR_HIP;
+    }
+    if (hipEventCreateWithFlags(&c->ev_fork, hipEventDisableTiming) != hipSuccess ||
+        hipEventCreateWithFlags(&c->ev_join, hipEventDisableTiming) != hipSuccess)
+      return SSD_ERR_HIP;
+  }
   int32_t* pending = c->at<int32_t>(c->L.g_pending);
   int32_t* draft = c->at<int32_t>(c->L.g_draft);
   int32_t* target = c->at<int32_t>(c->L.g_target);
@@ -1063,11 +1163,61 @@ int ssd_generate(ssd_ctx* c, int B, int P, const int32_t* d_prompt, const void* 
   a.status = c->at<int32_t>(c->L.status);
   a.tokens = d_tokens; a.count = count; a.active_rw = active; a.T = T; a.stats = stats;
   a.n_active = n_active;
+  // drafts made ahead: two (draft tokens, layer-k stash) pairs used in turn
+  int32_t* drafts[2] = {draft, c->at<int32_t>(c->L.g_draft2)};
+  float* stashes[2] = {c->at<float>(c->L.stash), c->at<float>(c->L1.stash)};
+  int32_t* guess = c->at<int32_t>(c->L.g_guess);
+  const float* x1 = c->at<float>(c->L.x1);
+  int cur = 0;
+  if (ahead) {
+    a.guess = guess;
+    a.next_need = 2 * gamma + 1;
+  }
   for (int round = 0; round < T; ++round) {
-    int32_t h_active[2] = {0, 0};
-    HIP_TRY(hipMemcpyAsync(h_active, n_active, 8, hipMemcpyDeviceToHost, c->stream));
+    int32_t h_active[3] = {0, 0, 0};
+    HIP_TRY(hipMemcpyAsync(h_active, n_active, 12, hipMemcpyDeviceToHost, c->stream));
     HIP_TRY(hipStreamSynchronize(c->stream));
     if (h_active[0] == 0) break;
+    if (ahead) {
+      // the previous round's drafts made ahead hold when it accepted everything and its extra
+      // token was the one they started from; otherwise draft from the new pending token
+      if (h_active[2]) {
+        cur ^= 1;
+      } else {
+        GraphKey kd{4, B, gamma, 0, pending, drafts[cur], stashes[cur], nullptr};
+        rc = launch_maybe_graph(c, kd, [&]() {
+          return draft_launches(c, B, gamma, pending, drafts[cur], nullptr, nullptr, 0.f, 0,
+                                stashes[cur]);
+        });
+        if (rc) return rc;
+      }
+      GraphKey kl{5, B, gamma, 0, drafts[cur], nullptr, nullptr, nullptr};
+      rc = launch_maybe_graph(c, kl, [&]() { return verify_last_row(c, B, gamma, drafts[cur]); });
+      if (rc) return rc;
+      HIP_TRY(hipEventRecord(c->ev_fork, c->stream));
+      HIP_TRY(hipStreamWaitEvent(c->stream1, c->ev_fork, 0));
+      {
+        OnLane1 lane1(c);
+        GraphKey ka{6, B, gamma, 1, guess, drafts[cur ^ 1], stashes[cur ^ 1], x1};
+        rc = launch_maybe_graph(c, ka, [&]() {
+          return ahead_launches(c, B, gamma, x1, guess, drafts[cur ^ 1], stashes[cur ^ 1]);
+        });
+      }
+      if (rc) return rc;
+      HIP_TRY(hipEventRecord(c->ev_join, c->stream1));
+      GraphKey kv{7, B, gamma, 0, stashes[cur], target, nullptr, nullptr};
+      rc = launch_maybe_graph(c, kv, [&]() {
+        return verify_deep(c, B, gamma, stashes[cur], target, nullptr);
+      });
+      if (rc) return rc;
+      // the accept moves seq_len, which the drafts made ahead read: after they finish
+      HIP_TRY(hipStreamWaitEvent(c->stream, c->ev_join, 0));
+      a.gamma = gamma;
+      a.draft = drafts[cur];
+      HIP_TRY(launch_accept(a, c->stream));
+      c->draft_valid = false;
+      continue;
+    }
     const int g = mode == SSD_MODE_GREEDY ? 0
                   : (dynamic ? ssd_dynamic_gamma(h_active[1], gamma, c->d.max_seq) : gamma);
     if (g > c->d.max_gamma) return SSD_ERR_SHAPE;
@@ -1173,8 +1323,12 @@ const char* ssd_status_string(int code) {
 
 void ssd_destroy(ssd_ctx* c) {
   if (!c) return;
+  if (c->stream1) (void)hipStreamSynchronize(c->stream1);
   for (auto& kv : c->graphs) (void)hipGraphExecDestroy(kv.second);
   for (hipEvent_t e : c->ev_pool) (void)hipEventDestroy(e);
+  if (c->ev_fork) (void)hipEventDestroy(c->ev_fork);
+  if (c->ev_join) (void)hipEventDestroy(c->ev_join);
+  if (c->stream1) (void)hipStreamDestroy(c->stream1);
   delete c;
 }
 

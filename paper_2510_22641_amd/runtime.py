@@ -230,12 +230,16 @@ class DeviceDecoder:
         return out, alen
 
     def generate(self, prompt, visual, T: int, gamma: int, speculative: bool = True,
-                 reuse: bool = True, dynamic: bool = False):
-        """ssd_generate; with dynamic=True gamma is d(0) of the context-length schedule."""
+                 reuse: bool = True, dynamic: bool = False, ahead: bool = False):
+        """ssd_generate; with dynamic=True gamma is d(0) of the context-length schedule; with
+        ahead=True the next round is drafted on a second stream during each verify pass."""
         B, P = prompt.shape
         tokens = self.ivec(B, T)
+        if ahead and (dynamic or not speculative):
+            raise ValueError("drafting ahead takes a fixed draft length")
         mode = abi.SSD_MODE_GREEDY if not speculative else (
-            abi.SSD_MODE_SPECULATIVE_DYNAMIC if dynamic else abi.SSD_MODE_SPECULATIVE)
+            abi.SSD_MODE_SPECULATIVE_DYNAMIC if dynamic else
+            abi.SSD_MODE_SPECULATIVE_AHEAD if ahead else abi.SSD_MODE_SPECULATIVE)
         stats = self._call(abi.ssd_generate, self.ctx, B, P, prompt, visual, T, gamma, mode, reuse, tokens)
         return tokens, stats
 

@@ -18,6 +18,7 @@ SSD_OK, SSD_ERR_ARG, SSD_ERR_SHAPE, SSD_ERR_CAPACITY, SSD_ERR_HIP, SSD_ERR_STATE
 SSD_ARCH_T5, SSD_ARCH_LLAMA = 0, 1
 SSD_F32, SSD_BF16 = 0, 1
 SSD_MODE_GREEDY, SSD_MODE_SPECULATIVE, SSD_MODE_SPECULATIVE_DYNAMIC = 0, 1, 2
+SSD_MODE_SPECULATIVE_AHEAD = 3
 SSD_DEV_BAD_TOKEN, SSD_DEV_CAPACITY, SSD_DEV_BAD_PAGE, SSD_DEV_SYNC = 1, 2, 4, 8
 
 
