@@ -791,13 +791,17 @@ __global__ __launch_bounds__(256) void gemv1k_kernel(const LinearArgs a) {
 // (i, i + dh/2) of one head, so rotary and the KV store are done here.  A residual epilogue also
 // writes the next launch's planes (of out_gain * y_new) and per-tile partial sums of squares of
 // y_new.
+// PACK (at most 8 input rows): the B operand's 16 columns carry the hi plane of rows 0..7 in
+// columns 0..7 and the lo plane in columns 8..15, so one activation load and one MFMA per 32
+// elements cover both planes (half the loads and MFMAs of the two-plane form); the epilogue adds
+// column t + 8 to column t.
 constexpr int SKW = 4;  // waves per skinny block
 constexpr int SSQ_MAX = 256;  // partial sums of squares a skinny consumer reads (d_model <= 4096)
 
-template <bool GATED, bool RMS, int NT>
+// SK: 64-element steps per batch of loads (chosen by the launcher from the steps of a wave).
+template <bool GATED, bool RMS, int NT, bool PACK, int SK>
 __global__ __launch_bounds__(64 * SKW) void gemv_mfma_kernel(const LinearArgs a) {
   constexpr int NB = GATED ? 2 : 1;
-  constexpr int SK = (8 / (NT * NB)) > 0 ? 8 / (NT * NB) : 1;  // 64-element steps per batch
   constexpr int NG = 4 * SKW;                                 // groups of 16 threads
   __shared__ float part[SKW][NB][NT][16][17];
   __shared__ float fin[NB][NT][16][17];
@@ -851,10 +855,12 @@ __global__ __launch_bounds__(64 * SKW) void gemv_mfma_kernel(const LinearArgs a)
   }
   const int kq = (lane >> 4) * 16;  // this lane's 16 elements within a step
   const int t0 = blockIdx.y * 16;   // this block's first input row
-  const int tok = t0 + (lane & 15);
+  // B column lane % 16: input row t0 + lane % 16, or (PACK) row lane % 8 of the hi (columns
+  // 0..7) or lo (columns 8..15) plane
+  const int tok = PACK ? (lane & 7) : t0 + (lane & 15);
   const bool tok_ok = tok < M;
   const int PR = a.plane_rows;
-  const bf16_t* brow = a.in_planes + (size_t)(tok_ok ? tok : 0) * a.in_ld;
+  const bf16_t* brow = a.in_planes + ((size_t)(PACK && (lane & 8) ? PR : 0) + (tok_ok ? tok : 0)) * a.in_ld;
   const bf16_t* brow_lo = brow + (size_t)PR * a.in_ld;
 
   // values the epilogue needs, requested before the main batch (the wait counter retires loads
@@ -894,9 +900,11 @@ __global__ __launch_bounds__(64 * SKW) void gemv_mfma_kernel(const LinearArgs a)
       const uint4* bp = reinterpret_cast<const uint4*>(brow + k0);
       bv[u][0] = bp[0];
       bv[u][1] = bp[1];
-      const uint4* bq = reinterpret_cast<const uint4*>(brow_lo + k0);
-      bl[u][0] = bq[0];
-      bl[u][1] = bq[1];
+      if (!PACK) {
+        const uint4* bq = reinterpret_cast<const uint4*>(brow_lo + k0);
+        bl[u][0] = bq[0];
+        bl[u][1] = bq[1];
+      }
     }
 #pragma unroll
     for (int u = 0; u < SK; ++u) {
@@ -919,7 +927,7 @@ __global__ __launch_bounds__(64 * SKW) void gemv_mfma_kernel(const LinearArgs a)
       const bool use = tok_ok && (s0 + u < s_end);
       const uint4 z = make_uint4(0, 0, 0, 0);
       const uint4 b0 = use ? bv[u][0] : z, b1 = use ? bv[u][1] : z;
-      const uint4 c0 = use ? bl[u][0] : z, c1 = use ? bl[u][1] : z;
+      const uint4 c0 = (use && !PACK) ? bl[u][0] : z, c1 = (use && !PACK) ? bl[u][1] : z;
 #pragma unroll
       for (int j = 0; j < NT; ++j)
 #pragma unroll
@@ -927,9 +935,11 @@ __global__ __launch_bounds__(64 * SKW) void gemv_mfma_kernel(const LinearArgs a)
           const bf16x8_t w0 = *reinterpret_cast<const bf16x8_t*>(&wv[b][j][u][0]);
           const bf16x8_t w1 = *reinterpret_cast<const bf16x8_t*>(&wv[b][j][u][1]);
           acc[b][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w0, *reinterpret_cast<const bf16x8_t*>(&b0), acc[b][j], 0, 0, 0);
-          acc[b][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w0, *reinterpret_cast<const bf16x8_t*>(&c0), acc[b][j], 0, 0, 0);
+          if (!PACK)
+            acc[b][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w0, *reinterpret_cast<const bf16x8_t*>(&c0), acc[b][j], 0, 0, 0);
           acc[b][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w1, *reinterpret_cast<const bf16x8_t*>(&b1), acc[b][j], 0, 0, 0);
-          acc[b][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w1, *reinterpret_cast<const bf16x8_t*>(&c1), acc[b][j], 0, 0, 0);
+          if (!PACK)
+            acc[b][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w1, *reinterpret_cast<const bf16x8_t*>(&c1), acc[b][j], 0, 0, 0);
         }
     }
   }
@@ -968,6 +978,11 @@ __global__ __launch_bounds__(64 * SKW) void gemv_mfma_kernel(const LinearArgs a)
 #pragma unroll
       for (int j = 0; j < NT; ++j) fin[b][j][f][t] = tsum[b][j];
   }
+  // output (feature ff, input row tt) of tile j: with PACK the hi and lo columns added (only
+  // tt < 8 is used then)
+  auto out_at = [&](int b, int j, int ff, int tt) {
+    return PACK ? fin[b][j][ff][tt] + fin[b][j][ff][(tt + 8) & 15] : fin[b][j][ff][tt];
+  };
   if (RMS && tid < 16) {
     float s2 = 0.f;
 #pragma unroll
@@ -981,7 +996,7 @@ __global__ __launch_bounds__(64 * SKW) void gemv_mfma_kernel(const LinearArgs a)
     const int vt = grp * NT + j;
     if (vt >= tiles) break;  // uniform over the block
     const int n = vt * 16 + f;
-    const float v = fin[0][j][f][t] * rscale;
+    const float v = out_at(0, j, f, t) * rscale;
     if (a.epi == EPI_ARGMAX) {
       const bool ok = lead && tg < M && n < n_out;
       if (lead) {
@@ -1032,12 +1047,12 @@ __global__ __launch_bounds__(64 * SKW) void gemv_mfma_kernel(const LinearArgs a)
     if (qkv) {
       int m, c;
       qkv_tile(vt, m, c);
-      if (f < 8) qkv_store_pair(a, m, c + f, tg, v, fin[0][j][f + 8][t] * rscale);
+      if (f < 8) qkv_store_pair(a, m, c + f, tg, v, out_at(0, j, f + 8, t) * rscale);
       continue;
     }
     if (n >= n_out) continue;
     if (GATED) {
-      const float act = apply_epi_act(a.epi, v, fin[NB - 1][j][f][t] * rscale);
+      const float act = apply_epi_act(a.epi, v, out_at(NB - 1, j, f, t) * rscale);
       if (a.y) a.y[(size_t)tg * a.ldy + n] = act;
       if (a.out_planes) {
         const uint32_t hi = f32_to_bf16(act);
@@ -1618,6 +1633,61 @@ bool skinny_ok(int M, int K, int wdtype) { return wdtype == 1 && M >= 2 && M <= 
 
 int skinny_blocks(int n_out) { return (n_out + 15) / 16; }
 
+// (only the depths the launcher can pick for each variant are instantiated)
+template <bool PACK, int SK>
+void launch_skinny_sk(const LinearArgs& b, bool gated, bool rms, int tiles, dim3 block,
+                      hipStream_t s) {
+  constexpr int cap1 = PACK ? 12 : 8, cap_g = PACK ? 8 : 4, cap4 = PACK ? 4 : 2;
+  if (b.epi == EPI_ARGMAX) {
+    if constexpr (SK <= cap4) {
+      const dim3 grid((tiles + 3) / 4, (b.M + 15) / 16);
+      if (rms) hipLaunchKernelGGL((gemv_mfma_kernel<false, true, 4, PACK, SK>), grid, block, 0, s, b);
+      else hipLaunchKernelGGL((gemv_mfma_kernel<false, false, 4, PACK, SK>), grid, block, 0, s, b);
+    }
+    return;
+  }
+  const dim3 grid(tiles, (b.M + 15) / 16);
+  if (gated) {
+    if constexpr (SK <= cap_g) {
+      if (rms) hipLaunchKernelGGL((gemv_mfma_kernel<true, true, 1, PACK, SK>), grid, block, 0, s, b);
+      else hipLaunchKernelGGL((gemv_mfma_kernel<true, false, 1, PACK, SK>), grid, block, 0, s, b);
+    }
+    return;
+  }
+  if constexpr (SK <= cap1) {
+    if (rms) hipLaunchKernelGGL((gemv_mfma_kernel<false, true, 1, PACK, SK>), grid, block, 0, s, b);
+    else hipLaunchKernelGGL((gemv_mfma_kernel<false, false, 1, PACK, SK>), grid, block, 0, s, b);
+  }
+}
+
+// Steps per batch: as many as the registers allow (the two-plane form: 8 weight-and-input steps
+// per tile and matrix; PACK, with one input plane: 12 for one weight matrix, 8 for the gated
+// pair, 4 for the LM head's four tiles), then balanced so that the wave's last batch is not a
+// short one padded with clamped re-reads.
+template <bool PACK>
+hipError_t launch_skinny_as(const LinearArgs& b, bool gated, bool rms, int tiles, dim3 block,
+                            hipStream_t s) {
+  const int nt = b.epi == EPI_ARGMAX ? 4 : 1, nb = gated ? 2 : 1;
+  const int cap = PACK ? (nt * nb == 1 ? 12 : (nb == 2 ? 8 : 4)) : (8 / (nt * nb) > 0 ? 8 / (nt * nb) : 1);
+  const int spw = (b.K / 64 + SKW - 1) / SKW;
+  const int batches = (spw + cap - 1) / cap;
+  const int want = (spw + batches - 1) / batches;
+  // instantiated depths: 1, 2, 4, 8, 10, 12 (the smallest not below `want`, at most the cap)
+  const int opts[6] = {1, 2, 4, 8, 10, 12};
+  int sk = cap;
+  for (int i = 0; i < 6; ++i)
+    if (opts[i] >= want && opts[i] <= cap) { sk = opts[i]; break; }
+  switch (sk) {
+    case 1: launch_skinny_sk<PACK, 1>(b, gated, rms, tiles, block, s); break;
+    case 2: launch_skinny_sk<PACK, 2>(b, gated, rms, tiles, block, s); break;
+    case 4: launch_skinny_sk<PACK, 4>(b, gated, rms, tiles, block, s); break;
+    case 8: launch_skinny_sk<PACK, 8>(b, gated, rms, tiles, block, s); break;
+    case 10: launch_skinny_sk<PACK, 10>(b, gated, rms, tiles, block, s); break;
+    default: launch_skinny_sk<PACK, 12>(b, gated, rms, tiles, block, s); break;
+  }
+  return hipGetLastError();
+}
+
 hipError_t launch_linear_skinny(const LinearArgs& a, hipStream_t s, int* n_parts) {
   const bool gated = (a.epi == EPI_GATED_GELU || a.epi == EPI_GATED_SILU);
   const int n_out = gated ? a.n_per : a.n_per * a.n_mats;
@@ -1630,18 +1700,8 @@ hipError_t launch_linear_skinny(const LinearArgs& a, hipStream_t s, int* n_parts
   if (n_parts) *n_parts = b.n_parts;
   const bool rms = a.norm == NORM_RMS;
   const dim3 block(64 * SKW);
-  if (a.epi == EPI_ARGMAX) {
-    const dim3 grid((tiles + 3) / 4, (a.M + 15) / 16);
-    if (rms) hipLaunchKernelGGL((gemv_mfma_kernel<false, true, 4>), grid, block, 0, s, b);
-    else hipLaunchKernelGGL((gemv_mfma_kernel<false, false, 4>), grid, block, 0, s, b);
-    return hipGetLastError();
-  }
-  const dim3 grid(tiles, (a.M + 15) / 16);
-  if (gated && rms) hipLaunchKernelGGL((gemv_mfma_kernel<true, true, 1>), grid, block, 0, s, b);
-  else if (gated) hipLaunchKernelGGL((gemv_mfma_kernel<true, false, 1>), grid, block, 0, s, b);
-  else if (rms) hipLaunchKernelGGL((gemv_mfma_kernel<false, true, 1>), grid, block, 0, s, b);
-  else hipLaunchKernelGGL((gemv_mfma_kernel<false, false, 1>), grid, block, 0, s, b);
-  return hipGetLastError();
+  if (a.M <= 8) return launch_skinny_as<true>(b, gated, rms, tiles, block, s);
+  return launch_skinny_as<false>(b, gated, rms, tiles, block, s);
 }
 
 hipError_t launch_skinny_prep(const float* x, int ldx, int M, int K, const float* gain, bf16_t* out,
