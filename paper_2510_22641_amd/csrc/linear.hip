@@ -1530,10 +1530,12 @@ void launch_gemv1k(const LinearArgs& a, dim3 grid, hipStream_t s, LaunchTiming* 
   }
 }
 
-// One bf16 row with 2048 <= K <= 6144 and no LayerNorm: the K-split kernel (same grid as gemv1).
+// One bf16 row with 2048 <= K <= 6144 and no LayerNorm, or up to 12288 without a norm (the
+// LLaMA-7B down projection, K = 11008): the K-split kernel (same grid as gemv1).
 bool use_gemv1k(const LinearArgs& a) {
-  return a.M == 1 && a.wdtype == 1 && (a.norm == NORM_NONE || a.norm == NORM_RMS) &&
-         a.K >= 2048 && a.K <= 3 * 2048 && a.K % 8 == 0;
+  if (a.M != 1 || a.wdtype != 1 || a.K < 2048 || a.K % 8) return false;
+  if (a.norm == NORM_RMS) return a.K <= 3 * 2048;
+  return a.norm == NORM_NONE && a.K <= 6 * 2048;
 }
 
 hipError_t launch_gemv1k_any(const LinearArgs& a, hipStream_t s, LaunchTiming* t) {
@@ -1545,7 +1547,10 @@ hipError_t launch_gemv1k_any(const LinearArgs& a, hipStream_t s, LaunchTiming* t
   const bool rms = a.norm == NORM_RMS;
   if (kp == 1) rms ? launch_gemv1k<1, NORM_RMS>(a, grid, s, tt) : launch_gemv1k<1, NORM_NONE>(a, grid, s, tt);
   else if (kp == 2) rms ? launch_gemv1k<2, NORM_RMS>(a, grid, s, tt) : launch_gemv1k<2, NORM_NONE>(a, grid, s, tt);
-  else rms ? launch_gemv1k<3, NORM_RMS>(a, grid, s, tt) : launch_gemv1k<3, NORM_NONE>(a, grid, s, tt);
+  else if (kp == 3) rms ? launch_gemv1k<3, NORM_RMS>(a, grid, s, tt) : launch_gemv1k<3, NORM_NONE>(a, grid, s, tt);
+  else if (kp == 4) launch_gemv1k<4, NORM_NONE>(a, grid, s, tt);
+  else if (kp == 5) launch_gemv1k<5, NORM_NONE>(a, grid, s, tt);
+  else launch_gemv1k<6, NORM_NONE>(a, grid, s, tt);
   return hipGetLastError();
 }
 
