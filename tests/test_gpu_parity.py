@@ -304,3 +304,17 @@ def test_folded_cross_attention_matches_unfolded_and_oracle(wl):
                                 wl.shape, f"round {i} draft {j}")
         compared += 1
     assert compared >= 1
+
+def test_wide_ffn_rows_take_the_k_split_gemv():
+    """A LLaMA-style decoder whose FFN is 6208 wide: the one-row down projection (K = 6208, four
+    2048-element pieces, the last one ragged) runs on the K-split GEMV without a norm, as the
+    LLaMA-7B shape's K = 11008 does.  Drafts, verify logits and greedy steps follow the oracle."""
+    from dataclasses import replace
+    wide = replace(synth.SMALL_LLAMA_BF16, name="small-llama-wide-ffn", n_layers=3, d_ff=6208)
+    wl = synth.S_LLAMA.with_(name="s-llama-wide-ffn", shape=wide, new_tokens=16)
+    dd, dec, pr, z, pt, vt = _setup(wl, seed=12, page_seed=5)
+    run = parity.device_run(dd, pt, vt, wl.new_tokens, wl.gamma, reuse=True)
+    parity.check_run_against_oracle(dec, wl.shape, pr[0], z[0], run, 0, wl.gamma)
+    greedy = parity.device_run(dd, pt, vt, wl.new_tokens, 0)
+    parity.check_run_against_oracle(dec, wl.shape, pr[0], z[0], greedy, 0, 0)
+    assert dd.sync_status() == (0, 0)
