@@ -238,14 +238,19 @@ def cpu_baseline(wl, weights, prompt, visual, budget_s: float):
     t_prefill = time.perf_counter() - t0
     per_round = max(t_one - t_prefill, 1e-3)
     rounds = int(max(1, min(wl.new_tokens, (budget_s - t_prefill) / per_round)))
-    t0 = time.perf_counter()
-    run = decode.ssd(dec, prompt, visual, wl.new_tokens, wl.gamma, max_rounds=rounds)
-    dt = time.perf_counter() - t0
-    n = len(run.tokens)
+    # whole jobs (or one job cut to the budget's rounds) until about the budget is spent
+    dt, n, jobs, n_rounds = 0.0, 0, 0, 0
+    while True:
+        t0 = time.perf_counter()
+        run = decode.ssd(dec, prompt, visual, wl.new_tokens, wl.gamma, max_rounds=rounds)
+        t_job = time.perf_counter() - t0
+        dt, n, jobs, n_rounds = dt + t_job, n + len(run.tokens), jobs + 1, n_rounds + len(run.rounds)
+        if dt + t_job > 1.25 * budget_s:
+            break
     return {"value": round(n / dt, 4), "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
-            "sample": (f"{wl.name} seed 0: float64 oracle, prefill + {len(run.rounds)} rounds of "
-                       f"Algorithm 1 (gamma {wl.gamma}), {n} tokens emitted in {dt:.1f} s; "
-                       f"host affinity {len(os.sched_getaffinity(0))} cpus")}
+            "sample": (f"{wl.name} seed 0: float64 oracle, {jobs} job(s) of prefill + "
+                       f"{n_rounds // jobs} rounds of Algorithm 1 (gamma {wl.gamma}), {n} tokens "
+                       f"emitted in {dt:.1f} s; host affinity {len(os.sched_getaffinity(0))} cpus")}
 
 
 def main():
