@@ -70,6 +70,42 @@ def verify_bytes(shape, B: int, gamma: int, ctx: int, kv_bytes: int = 4) -> floa
     return shape.n_layers * (layer + kv) + V * d * we + d * 4
 
 
+MFMA_BF16_PEAK_TFS = 2500.0  # MI355X dense bf16 matrix peak, published
+
+
+def prefill_flops(shape, B: int, P: int) -> float:
+    """Algorithmic flops of one prefill: every projection at 2 flops per weight and context row,
+    causal self-attention (QK and PV over the lower triangle), T5 cross K/V of the visual rows and
+    cross-attention of the prompt rows, the LM head for the last row."""
+    d, hd, f, V = shape.d_model, shape.hd, shape.d_ff, shape.vocab
+    rows = P + (shape.n_visual if shape.arch == "llama" else 0)
+    per_layer = 2.0 * (4 * d * hd + 3 * d * f) * rows + 2.0 * rows * rows * hd
+    if shape.arch == "t5":
+        nv = shape.n_visual
+        per_layer += 2.0 * 2 * d * hd * nv + 2.0 * 2 * d * hd * rows + 4.0 * rows * nv * hd
+    return B * (shape.n_layers * per_layer + 2.0 * V * d)
+
+
+def prefill_timing(dd, pt, vt, reps: int = 3) -> float:
+    """Median seconds of one prefill call (HIP events on the decoder's stream)."""
+    import numpy as np
+    import torch
+    from paper_2510_22641_amd import ssd as abi
+    B, P = pt.shape
+    pending = dd.buf("pending", (B,))
+    s = dd.stream
+    ts = []
+    for _ in range(reps + 1):
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        s.wait_stream(torch.cuda.current_stream())
+        ev[0].record(s)
+        abi.ssd_prefill(dd.ctx, B, P, pt, vt, pending, None)
+        ev[1].record(s)
+        torch.cuda.synchronize()
+        ts.append(ev[0].elapsed_time(ev[1]) * 1e-3)
+    return float(np.median(ts[1:]))
+
+
 def dominant_kernel_name(sh) -> str:
     """rocprof name of the one-row GEMV instantiation that streams the RMS-normalised d_model-wide
     matrices (the kernel the library times while profiling)."""
@@ -362,6 +398,14 @@ def main():
            "schedule": f"d(t) = {g} + floor(10 sigmoid(0.01 (t - {dd.cap.max_seq}/2)))"}
     print(f"[bench] dynamic d(t) {dyn['tokens_per_s']:.1f} tok/s", file=sys.stderr, flush=True)
 
+    # prefill alone (its projections on MFMA tiles once the context exceeds the skinny chunk)
+    pf_s = prefill_timing(dd, pt, vt)
+    pf_flops = prefill_flops(sh, B, wl.prompt_len)
+    prefill = {"ms": round(pf_s * 1e3, 3), "tflop": round(pf_flops / 1e12, 4),
+               "tflops_per_s": round(pf_flops / pf_s / 1e12, 1),
+               "frac_of_bf16_mfma_peak": round(pf_flops / pf_s / 1e12 / MFMA_BF16_PEAK_TFS, 4)}
+    print(f"[bench] prefill {prefill}", file=sys.stderr, flush=True)
+
     # draft-step time: events around the gamma-step draft call (captured graph) on its stream
     step_s, verify_s, ctx = step_timings(dd, pt, vt, B, g)
     step_bytes = draft_step_bytes(sh, wl.draft_layers, ctx, dd.k_pool.element_size(),
@@ -488,6 +532,7 @@ def main():
         "dynamic_gamma": dyn,
         "speculative_sampling": sampling or None,
         "fitted_imitation": fit,
+        "prefill": prefill,
         "draft_step": draft,
         "verify": verify,
         "roofline": roofline,

@@ -93,6 +93,12 @@ struct LinearArgs {
   int out_ld = 0;
   float* out_ssq = nullptr;
   const float* out_gain = nullptr;
+  // Tile path (rows past the skinny capacity): a buffer for the bf16 hi / lo planes of the
+  // (gain-multiplied) input rows, gemm_plane_rows rows of at most gemm_plane_ld elements per
+  // plane; null keeps the tile kernels that split the inputs themselves.
+  bf16_t* gemm_planes = nullptr;
+  int gemm_plane_rows = 0;
+  int gemm_plane_ld = 0;
 };
 
 // Kernel-level timing of the one-row GEMV launches with K inputs, input normalisation `norm` and

@@ -1269,6 +1269,210 @@ __global__ __launch_bounds__(256) void gemm2_kernel(const LinearArgs a) {
       }
 }
 
+// Prefill GEMM on bf16 operand planes: the input rows arrive as hi / lo planes of g * x written
+// once by plane_prep_kernel (which also leaves 1/rms of each row in stats[m].y), so a K step
+// stages bf16 only and nothing is re-normalised per column tile.  A block owns TMR rows x BN
+// features (x2 matrices when gated) on a 2 x 2 grid of waves; K advances in steps of 32 through
+// double-buffered LDS (one barrier a step), and each thread keeps the global loads of the next D
+// steps in flight in a rotating set of registers, so a step's memory round trip overlaps D steps
+// of MFMA work instead of one.  RMSNorm scales the outputs by 1/rms.
+constexpr int G3K = 32, G3KP = G3K + 8, G3D = 4;  // G3D: the slot code below assumes 4
+
+template <bool GATED, int TMR, int BN, bool RMS>
+__global__ __launch_bounds__(256) void gemm3_kernel(const LinearArgs a) {
+  constexpr int NB = GATED ? 2 : 1;
+  constexpr int IF = TMR / 32;        // 16-row fragments per wave (the wave covers TMR / 2 rows)
+  constexpr int TJ = BN / 32;         // 16-feature fragments per wave (BN / 2 features)
+  constexpr int AQ = TMR / 64;        // 16-byte pieces of each plane a thread stages per step
+  constexpr int BQ = BN / 64;         // 16-byte pieces of each weight matrix a thread stages
+  constexpr int ATPR = 256 / TMR;     // threads per input row in staging
+  constexpr int BTPR = 256 / BN;      // threads per weight row in staging
+  extern __shared__ __attribute__((aligned(16))) bf16_t g3s[];
+  bf16_t* Ah = g3s;                          // [2][TMR][G3KP]
+  bf16_t* Al = Ah + 2 * TMR * G3KP;          // [2][TMR][G3KP]
+  bf16_t* Bs = Al + 2 * TMR * G3KP;          // [2][NB][BN][G3KP]
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  // row tiles vary fastest: the blocks that share a weight tile run back to back
+  const int m0 = blockIdx.x * TMR, n0 = blockIdx.y * BN;
+  const int K = a.K, M = a.M;
+  const int n_out = GATED ? a.n_per : a.n_per * a.n_mats;
+  const int mat = GATED ? 0 : n0 / a.n_per;  // tiles never straddle matrices (n_per % BN == 0)
+  const int nbase = GATED ? n0 : n0 - mat * a.n_per;
+  const bf16_t* w0 = reinterpret_cast<const bf16_t*>(GATED ? a.w[0] : (mat == 0 ? a.w[0] : (mat == 1 ? a.w[1] : a.w[2])));
+  const bf16_t* w1 = reinterpret_cast<const bf16_t*>(a.w[1]);
+
+  // staging roles: input row ar (clamped: rows past M are computed and never stored), AQ * 8
+  // elements from ak; weight row br, BQ * 8 elements from bk
+  const int ar = tid / ATPR, ak = (tid % ATPR) * (AQ * 8);
+  const int br = tid / BTPR, bk = (tid % BTPR) * (BQ * 8);
+  const bf16_t* hrow = a.in_planes + (size_t)min(m0 + ar, M - 1) * a.in_ld + ak;
+  const bf16_t* lrow = hrow + (size_t)a.plane_rows * a.in_ld;
+  const int bn = min(nbase + br, a.n_per - 1);
+  const bf16_t* wrow0 = w0 + (size_t)bn * K + bk;
+  const bf16_t* wrow1 = w1 + (size_t)bn * K + bk;
+
+  f32x4_t acc[NB][IF][TJ];
+#pragma unroll
+  for (int b = 0; b < NB; ++b)
+#pragma unroll
+    for (int i = 0; i < IF; ++i)
+#pragma unroll
+      for (int j = 0; j < TJ; ++j) acc[b][i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  const int nk = K / G3K;
+  typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
+  u32x4_t rh[G3D][AQ], rl[G3D][AQ], rw[G3D][NB][BQ];
+  // (macros, so that every slot index is a constant and the ring stays in registers)
+#define G3_FETCH(SLOT, STEP)                                                               \
+  do {                                                                                     \
+    const int k0_ = min((STEP), nk - 1) * G3K;                                             \
+    _Pragma("unroll") for (int q = 0; q < AQ; ++q) {                                       \
+      rh[SLOT][q] = reinterpret_cast<const u32x4_t*>(hrow + k0_)[q];                         \
+      rl[SLOT][q] = reinterpret_cast<const u32x4_t*>(lrow + k0_)[q];                         \
+    }                                                                                      \
+    _Pragma("unroll") for (int q = 0; q < BQ; ++q) {                                       \
+      rw[SLOT][0][q] = reinterpret_cast<const u32x4_t*>(wrow0 + k0_)[q];                     \
+      if (GATED) rw[SLOT][NB - 1][q] = reinterpret_cast<const u32x4_t*>(wrow1 + k0_)[q];     \
+    }                                                                                      \
+  } while (0)
+#define G3_STAGE(SLOT, BUF)                                                                \
+  do {                                                                                     \
+    u32x4_t* ah_ = reinterpret_cast<u32x4_t*>(Ah + ((size_t)(BUF) * TMR + ar) * G3KP + ak);    \
+    u32x4_t* al_ = reinterpret_cast<u32x4_t*>(Al + ((size_t)(BUF) * TMR + ar) * G3KP + ak);    \
+    _Pragma("unroll") for (int q = 0; q < AQ; ++q) {                                       \
+      ah_[q] = rh[SLOT][q];                                                                \
+      al_[q] = rl[SLOT][q];                                                                \
+    }                                                                                      \
+    _Pragma("unroll") for (int b = 0; b < NB; ++b) {                                       \
+      u32x4_t* bp_ = reinterpret_cast<u32x4_t*>(Bs + (((size_t)(BUF) * NB + b) * BN + br) * G3KP + bk); \
+      _Pragma("unroll") for (int q = 0; q < BQ; ++q) bp_[q] = rw[SLOT][b][q];              \
+    }                                                                                      \
+  } while (0)
+
+  // prologue: steps 0..D-1 in flight, step 0 staged
+  G3_FETCH(0, 0);
+  G3_FETCH(1, 1);
+  G3_FETCH(2, 2);
+  G3_FETCH(3, 3);
+  G3_STAGE(0, 0);
+  G3_FETCH(0, G3D);
+  __syncthreads();
+
+  const int kk = (lane >> 4) * 8;
+  // one K step: MFMAs on LDS buffer step & 1, then slot NEXT (holding step + 1) staged into the
+  // other buffer and refilled with step + 1 + D; unrolled by hand over the four slots (a loop
+  // with a barrier in its body is not unrolled, and a variable slot would put the ring in memory)
+#define G3_BODY(NEXT)                                                                      \
+  if (step < nk) {                                                                         \
+    const int buf = step & 1;                                                              \
+    bf16x8_t fh[IF], fl[IF], fb[NB][TJ];                                                   \
+    _Pragma("unroll") for (int i = 0; i < IF; ++i) {                                       \
+      const size_t r = ((size_t)buf * TMR + wm * (TMR / 2) + 16 * i + (lane & 15)) * G3KP + kk; \
+      fh[i] = *reinterpret_cast<const bf16x8_t*>(Ah + r);                                  \
+      fl[i] = *reinterpret_cast<const bf16x8_t*>(Al + r);                                  \
+    }                                                                                      \
+    _Pragma("unroll") for (int b = 0; b < NB; ++b)                                         \
+    _Pragma("unroll") for (int j = 0; j < TJ; ++j)                                         \
+      fb[b][j] = *reinterpret_cast<const bf16x8_t*>(                                       \
+          Bs + (((size_t)buf * NB + b) * BN + wn * (BN / 2) + 16 * j + (lane & 15)) * G3KP + kk); \
+    _Pragma("unroll") for (int b = 0; b < NB; ++b)                                         \
+    _Pragma("unroll") for (int i = 0; i < IF; ++i)                                         \
+    _Pragma("unroll") for (int j = 0; j < TJ; ++j) {                                       \
+      acc[b][i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fh[i], fb[b][j], acc[b][i][j], 0, 0, 0); \
+      acc[b][i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fl[i], fb[b][j], acc[b][i][j], 0, 0, 0); \
+    }                                                                                      \
+    if (step + 1 < nk) {                                                                   \
+      G3_STAGE(NEXT, buf ^ 1);                                                             \
+      G3_FETCH(NEXT, step + 1 + G3D);                                                      \
+    }                                                                                      \
+    __syncthreads();                                                                       \
+  }
+  for (int kt = 0; kt < nk; kt += G3D) {
+    int step = kt;
+    G3_BODY(1)
+    step = kt + 1;
+    G3_BODY(2)
+    step = kt + 2;
+    G3_BODY(3)
+    step = kt + 3;
+    G3_BODY(0)
+  }
+#undef G3_BODY
+
+  // epilogue: lane holds D[4 * (lane / 16) + e][lane % 16] of each 16x16 tile
+#pragma unroll
+  for (int i = 0; i < IF; ++i)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int m = m0 + wm * (TMR / 2) + 16 * i + 4 * (lane >> 4) + e;
+      if (m >= M) continue;
+      const float rsc = RMS ? a.stats[m].y : 1.f;
+#pragma unroll
+      for (int j = 0; j < TJ; ++j) {
+        const int n = n0 + wn * (BN / 2) + 16 * j + (lane & 15);
+        if (n >= n_out) continue;
+        const float v = acc[0][i][j][e] * rsc;
+        float* yp = a.y + (size_t)m * a.ldy + n;
+        if (GATED) {
+          *yp = apply_epi_act(a.epi, v, acc[NB - 1][i][j][e] * rsc);
+          continue;
+        }
+        switch (a.epi) {
+          case EPI_STORE: *yp = v; break;
+          case EPI_RESID: {
+            const float t = *yp + v;
+            *yp = t;
+            if (a.stash) a.stash[(size_t)m * a.lds + n] = t;
+            break;
+          }
+          case EPI_BIAS_GELU: *yp = gelu_tanh(v + a.bias[n]); break;
+          case EPI_BIAS_RESID: *yp = (a.resid ? a.resid[(size_t)m * a.ldr + n] : 0.f) + (v + a.bias[n]); break;
+          default: break;
+        }
+      }
+    }
+}
+
+#undef G3_FETCH
+#undef G3_STAGE
+
+// Planes of g * x (g = gain, or 1) for rows 0..M-1 and, with a gain (RMSNorm), 1/rms of each row
+// in stats[m].y; one block per row.  hi of row m at out + m * ldo, lo plane_rows rows later.
+__global__ __launch_bounds__(256) void plane_prep_kernel(const float* __restrict__ x, int ldx, int K,
+                                                         const float* __restrict__ gain, float eps,
+                                                         bf16_t* __restrict__ out, int ldo,
+                                                         int plane_rows, float2* __restrict__ stats) {
+  __shared__ float red[4];
+  const int m = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const float* xr = x + (size_t)m * ldx;
+  float s2 = 0.f;
+  for (int k = tid * 8; k < K; k += 2048) {
+    float f[8];
+    const float4 v0 = *reinterpret_cast<const float4*>(xr + k);
+    const float4 v1 = *reinterpret_cast<const float4*>(xr + k + 4);
+    f[0] = v0.x; f[1] = v0.y; f[2] = v0.z; f[3] = v0.w; f[4] = v1.x; f[5] = v1.y; f[6] = v1.z; f[7] = v1.w;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) s2 = fmaf(f[e], f[e], s2);
+    if (gain) {
+      const float4 g0 = *reinterpret_cast<const float4*>(gain + k);
+      const float4 g1 = *reinterpret_cast<const float4*>(gain + k + 4);
+      f[0] *= g0.x; f[1] *= g0.y; f[2] *= g0.z; f[3] *= g0.w;
+      f[4] *= g1.x; f[5] *= g1.y; f[6] *= g1.z; f[7] *= g1.w;
+    }
+    uint4 h, l;
+    split_bf16x8(f, h, l);
+    *reinterpret_cast<uint4*>(out + (size_t)m * ldo + k) = h;
+    *reinterpret_cast<uint4*>(out + (size_t)(plane_rows + m) * ldo + k) = l;
+  }
+  if (!gain) return;
+  s2 = wave_sum(s2);
+  if (lane == 0) red[wave] = s2;
+  __syncthreads();
+  if (tid == 0) stats[m] = make_float2(0.f, 1.0f / sqrtf(((red[0] + red[1]) + (red[2] + red[3])) / (float)K + eps));
+}
+
 template <bool GATED>
 __global__ __launch_bounds__(256) void gemm_kernel(const LinearArgs a) {
   constexpr int NB = GATED ? 2 : 1;
@@ -1754,6 +1958,42 @@ void launch_gemm2(const LinearArgs& a, dim3 grid, hipStream_t s) {
   launch_gemm2_n<GATED, BN, true>(a, grid, s);
 }
 
+template <bool GATED, int TMR, int BN>
+void launch_gemm3_t(const LinearArgs& a, bool rms, hipStream_t s) {
+  constexpr int NB = GATED ? 2 : 1;
+  const size_t shm = ((size_t)2 * TMR * G3KP * 2 + (size_t)2 * NB * BN * G3KP) * sizeof(bf16_t);
+  const int n_out = GATED ? a.n_per : a.n_per * a.n_mats;
+  const dim3 grid((a.M + TMR - 1) / TMR, (n_out + BN - 1) / BN);
+  if (rms) hipLaunchKernelGGL((gemm3_kernel<GATED, TMR, BN, true>), grid, dim3(256), shm, s, a);
+  else hipLaunchKernelGGL((gemm3_kernel<GATED, TMR, BN, false>), grid, dim3(256), shm, s, a);
+}
+
+// The plane GEMM when its buffer is there and the shape fits: RMSNorm or no norm, no argmax, K in
+// whole steps, tiles that never straddle matrices.  128 x 128 tiles (gated: 128 x 64 per matrix)
+// when they give at least 256 blocks, else 64 x 64.
+bool try_gemm3(LinearArgs a, hipStream_t s, hipError_t* err) {
+  const bool gated = (a.epi == EPI_GATED_GELU || a.epi == EPI_GATED_SILU);
+  if (!a.gemm_planes || a.wdtype != 1 || a.epi == EPI_ARGMAX || a.epi == EPI_QKV) return false;
+  if (a.norm != NORM_NONE && a.norm != NORM_RMS) return false;
+  if (a.K % G3K || a.K > a.gemm_plane_ld || a.M > a.gemm_plane_rows || a.ldx % 4) return false;
+  const int n_out = gated ? a.n_per : a.n_per * a.n_mats;
+  const bool big = gated || (long long)((a.M + 127) / 128) * ((n_out + 127) / 128) >= 256;
+  const int bn = gated ? 64 : (big ? 128 : 64);
+  if (!gated && a.n_mats > 1 && a.n_per % bn) return false;
+  const bool rms = a.norm == NORM_RMS;
+  hipLaunchKernelGGL(plane_prep_kernel, dim3(a.M), dim3(256), 0, s, a.x, a.ldx, a.K,
+                     rms ? a.gain : nullptr, a.eps, a.gemm_planes, a.gemm_plane_ld,
+                     a.gemm_plane_rows, a.stats);
+  a.in_planes = a.gemm_planes;
+  a.in_ld = a.gemm_plane_ld;
+  a.plane_rows = a.gemm_plane_rows;
+  if (gated) launch_gemm3_t<true, 128, 64>(a, rms, s);
+  else if (big) launch_gemm3_t<false, 128, 128>(a, rms, s);
+  else launch_gemm3_t<false, 64, 64>(a, rms, s);
+  *err = hipGetLastError();
+  return true;
+}
+
 hipError_t launch_linear(LinearArgs a, hipStream_t s, int* n_parts, LaunchTiming* timing) {
   if (a.M <= 0) return hipSuccess;
   // the softmax input transform exists on the one-row register path only
@@ -1767,6 +2007,8 @@ hipError_t launch_linear(LinearArgs a, hipStream_t s, int* n_parts, LaunchTiming
     a.use_mfma = 1;
     if (a.epi == EPI_ARGMAX) a.n_parts = (n_out + TN - 1) / TN;
     if (n_parts) *n_parts = a.n_parts;
+    hipError_t e3 = hipSuccess;
+    if (try_gemm3(a, s, &e3)) return e3;
     if (a.norm != NORM_NONE) {
       hipError_t e = launch_row_stats(a.x, a.ldx, a.M, a.K, a.norm, a.eps, a.stats, s);
       if (e != hipSuccess) return e;

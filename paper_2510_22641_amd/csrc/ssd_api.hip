@@ -34,8 +34,9 @@ struct Layout {
       p_x, p_attn, p_ffn, ssq, attn_part, fold_q, fold_o,
       bucket, rope_cos, rope_sin, status, cur_tok, g_pending, g_draft, g_target,
       g_count, g_active, g_nactive, g_stats, g_draft2, g_guess, step_prog, step_arena, step_sync,
-      total;
+      gplanes, total;
   int rows_max, head_rows, parts_max, ctx_max, plane_rows, attn_rows;
+  int gplane_rows = 0, gplane_ld = 0;  // tile-path input planes (0 rows: none)
 };
 
 int ctx_len_max(const ssd_dims& d) {
@@ -139,6 +140,15 @@ bool make_layout(const ssd_dims& d, Layout& L, Layout& L1) {
     X.cur_tok = take(B * 4);
   };
   lane(L, rows, (size_t)L.head_rows);
+  // bf16 hi / lo planes of a context block's input rows for the tile GEMM (prefill)
+  {
+    int ld = (int)D;
+    if ((int)HD > ld) ld = (int)HD;
+    if (d.d_ff > ld) ld = d.d_ff;
+    L.gplane_ld = (ld + 7) / 8 * 8;
+    L.gplane_rows = (int)rows;
+    L.gplanes = take((size_t)2 * rows * L.gplane_ld * 2);
+  }
   L.vis = take(d.arch == SSD_ARCH_T5 ? B * (size_t)d.n_visual * D * 4 : 0);
   {
     const size_t fold = fold_cross(d) ? (size_t)d.n_layers * d.n_heads * d.n_visual * D * 4 : 0;
@@ -167,6 +177,7 @@ bool make_layout(const ssd_dims& d, Layout& L, Layout& L1) {
   }
   L1 = L;
   lane(L1, B, B);
+  L1.gplane_rows = 0;  // the second stream runs one-row steps only
   L.total = L1.total = off;
   return true;
 }
@@ -318,6 +329,11 @@ LinearArgs lin(ssd_ctx* c) {
   LinearArgs a;
   a.wdtype = c->d.wdtype;
   a.stats = c->at<float2>(c->L.stats);
+  if (c->L.gplane_rows > 0) {
+    a.gemm_planes = c->at<bf16_t>(c->L.gplanes);
+    a.gemm_plane_rows = c->L.gplane_rows;
+    a.gemm_plane_ld = c->L.gplane_ld;
+  }
   a.eps = c->d.norm_eps;
   return a;
 }
