@@ -315,39 +315,59 @@ hipError_t launch_attn_t(const AttnArgs& a, hipStream_t s) {
 }
 
 // Folded cross-attention, query side: fq[h*NV + j][k] = sum_e K[h][j][e] * Wq[h*dh + e][k].
-// Block (column tile, head h): thread t owns column k; the head's keys sit in LDS and every
-// weight element is read once (coalesced along k).
+// Block (column tile of 512, head h): lane l of every wave owns columns 8l .. 8l + 7 of the tile
+// (one 16-byte load of Wq per e) and wave w the keys j = w, w + 4, ... (the four waves read the
+// same weights, from L2 after the first); the head's keys sit in LDS.
 template <typename KT, typename WT, int NV>
 __global__ __launch_bounds__(256) void fold_q_kernel(const KT* __restrict__ xk,
                                                      const WT* __restrict__ wq, float* __restrict__ fq,
                                                      int dh, int d) {
-  __shared__ float ks[NV][129];
-  const int h = blockIdx.y, k = blockIdx.x * 256 + threadIdx.x;
+  constexpr int JW = (NV + 3) / 4;  // keys per wave
+  __shared__ __attribute__((aligned(16))) float ks[NV][128 + 4];
+  const int h = blockIdx.y, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int k = blockIdx.x * 512 + lane * 8;
   for (int i = threadIdx.x; i < NV * dh; i += 256) {
     const int j = i / dh, e = i - j * dh;
     ks[j][e] = load_elem(xk + ((size_t)h * NV + j) * dh + e);
   }
   __syncthreads();
-  if (k >= d) return;
-  float acc[NV];
+  if (k >= d) return;  // d is a multiple of 8
+  float acc[JW][8];
 #pragma unroll
-  for (int j = 0; j < NV; ++j) acc[j] = 0.f;
+  for (int t = 0; t < JW; ++t)
+#pragma unroll
+    for (int c = 0; c < 8; ++c) acc[t][c] = 0.f;
   for (int e = 0; e < dh; ++e) {
-    const float w = load_elem(wq + ((size_t)h * dh + e) * d + k);
+    float w[8];
+    Vec8<WT> v8;
+    v8.load(wq + ((size_t)h * dh + e) * d + k);
+    v8.to_f32(w);
 #pragma unroll
-    for (int j = 0; j < NV; ++j) acc[j] = fmaf(ks[j][e], w, acc[j]);
+    for (int t = 0; t < JW; ++t) {
+      const int j = wave + 4 * t;
+      const float kv = j < NV ? ks[j][e] : 0.f;
+#pragma unroll
+      for (int c = 0; c < 8; ++c) acc[t][c] = fmaf(kv, w[c], acc[t][c]);
+    }
   }
 #pragma unroll
-  for (int j = 0; j < NV; ++j) fq[((size_t)h * NV + j) * d + k] = acc[j];
+  for (int t = 0; t < JW; ++t) {
+    const int j = wave + 4 * t;
+    if (j >= NV) continue;
+    float* dst = fq + ((size_t)h * NV + j) * d + k;
+    *reinterpret_cast<float4*>(dst) = make_float4(acc[t][0], acc[t][1], acc[t][2], acc[t][3]);
+    *reinterpret_cast<float4*>(dst + 4) = make_float4(acc[t][4], acc[t][5], acc[t][6], acc[t][7]);
+  }
 }
 
 // Folded cross-attention, output side: fo[n][h*NV + j] = sum_e Wo[n][h*dh + e] * V[h][j][e].
-// Block (row tile, head h): thread t owns output row n and reads its dh weights of head h.
+// Block (row tile, head h): thread t owns output row n and reads its dh weights of head h (a
+// contiguous run, eight elements per load); the head's values sit in LDS, read four e at a time.
 template <typename KT, typename WT, int NV>
 __global__ __launch_bounds__(256) void fold_o_kernel(const KT* __restrict__ xv,
                                                      const WT* __restrict__ wo, float* __restrict__ fo,
                                                      int H, int dh, int d) {
-  __shared__ float vs[NV][129];
+  __shared__ __attribute__((aligned(16))) float vs[NV][128 + 4];
   const int h = blockIdx.y, n = blockIdx.x * 256 + threadIdx.x;
   for (int i = threadIdx.x; i < NV * dh; i += 256) {
     const int j = i / dh, e = i - j * dh;
@@ -356,13 +376,24 @@ __global__ __launch_bounds__(256) void fold_o_kernel(const KT* __restrict__ xv,
   __syncthreads();
   if (n >= d) return;
   const int HD = H * dh;
+  const WT* wr = wo + (size_t)n * HD + (size_t)h * dh;
   float acc[NV];
 #pragma unroll
   for (int j = 0; j < NV; ++j) acc[j] = 0.f;
-  for (int e = 0; e < dh; ++e) {
-    const float w = load_elem(wo + (size_t)n * HD + (size_t)h * dh + e);
+  for (int e0 = 0; e0 < dh; e0 += 8) {
+    float w[8];
+    Vec8<WT> v8;
+    v8.load(wr + e0);
+    v8.to_f32(w);
 #pragma unroll
-    for (int j = 0; j < NV; ++j) acc[j] = fmaf(vs[j][e], w, acc[j]);
+    for (int j = 0; j < NV; ++j) {
+      const float4 a0 = *reinterpret_cast<const float4*>(&vs[j][e0]);
+      const float4 a1 = *reinterpret_cast<const float4*>(&vs[j][e0 + 4]);
+      float t = acc[j];
+      t = fmaf(a0.x, w[0], t); t = fmaf(a0.y, w[1], t); t = fmaf(a0.z, w[2], t); t = fmaf(a0.w, w[3], t);
+      t = fmaf(a1.x, w[4], t); t = fmaf(a1.y, w[5], t); t = fmaf(a1.z, w[6], t); t = fmaf(a1.w, w[7], t);
+      acc[j] = t;
+    }
   }
   float* dst = fo + (size_t)n * H * NV + (size_t)h * NV;
 #pragma unroll
@@ -373,7 +404,7 @@ template <typename KT, typename WT, int NV>
 hipError_t launch_fold_t(const void* xk, const void* xv, const void* wq, const void* wo, int H,
                          int dh, int d, float* fq, float* fo, hipStream_t s) {
   const dim3 grid((d + 255) / 256, H);
-  hipLaunchKernelGGL((fold_q_kernel<KT, WT, NV>), grid, dim3(256), 0, s,
+  hipLaunchKernelGGL((fold_q_kernel<KT, WT, NV>), dim3((d + 511) / 512, H), dim3(256), 0, s,
                      reinterpret_cast<const KT*>(xk), reinterpret_cast<const WT*>(wq), fq, dh, d);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
@@ -402,7 +433,7 @@ bool cross_fold_ok(int nv, int dh) {
 hipError_t launch_cross_fold(const void* xk, const void* xv, int kvdtype, const void* wq,
                              const void* wo, int wdtype, int H, int nv, int dh, int d, float* fq,
                              float* fo, hipStream_t s) {
-  if (!cross_fold_ok(nv, dh) || H < 1 || d < 1) return hipErrorInvalidValue;
+  if (!cross_fold_ok(nv, dh) || H < 1 || d < 1 || d % 8) return hipErrorInvalidValue;
   switch (nv) {
     case 8: return launch_fold_nv<8>(xk, xv, kvdtype, wq, wo, wdtype, H, dh, d, fq, fo, s);
     case 16: return launch_fold_nv<16>(xk, xv, kvdtype, wq, wo, wdtype, H, dh, d, fq, fo, s);

@@ -111,6 +111,9 @@ bool make_layout(const ssd_dims& d, Layout& L, Layout& L1) {
   // chunk, rounded up to 16, at most 128) and its partial sums of squares
   {
     size_t pr = B * (G + 1);
+    // (T5: the visual rows too, so the prefill's cross K/V projections take the skinny path)
+    if (d.arch == SSD_ARCH_T5 && B * (size_t)d.n_visual <= 128 && B * (size_t)d.n_visual > pr)
+      pr = B * (size_t)d.n_visual;
     pr = pr < 16 ? 16 : (pr > 128 ? 128 : (pr + 15) / 16 * 16);
     L.plane_rows = (int)pr;
   }
@@ -1003,13 +1006,24 @@ int ssd_prefill(ssd_ctx* c, int B, int P, const int32_t* d_prompt, const void* d
     ev.visual = d_visual; ev.n_visual = d.n_visual; ev.n_prefix = d.n_visual; ev.status = status;
     HIP_TRY(launch_embed(ev, s));
     float* tmp = c->at<float>(c->L.qkv);
+    // the visual rows as skinny operand planes once for all 2L projections, when they fit
+    const int MV = B * d.n_visual, PR = c->L.plane_rows;
+    const bool sk = MV <= PR && skinny_ok(MV, D, d.wdtype) && skinny_ok(MV, HD, d.wdtype);
+    bf16_t* p_x = c->at<bf16_t>(c->L.p_x);
+    if (sk)
+      HIP_TRY(launch_skinny_prep(vis, D, MV, D, nullptr, p_x, D, PR, c->at<float>(c->L.ssq), s));
     for (int l = 0; l < d.n_layers; ++l) {
       for (int which = 0; which < 2; ++which) {
         LinearArgs a = lin(c);
-        a.x = vis; a.ldx = D; a.M = B * d.n_visual; a.K = D;
+        a.x = vis; a.ldx = D; a.M = MV; a.K = D;
         a.w[0] = which ? c->layers[l].xv : c->layers[l].xk; a.n_per = HD;
         a.epi = EPI_STORE; a.y = tmp; a.ldy = HD;
-        HIP_TRY(run_linear(c, a));
+        if (sk) {
+          a.in_planes = p_x; a.in_ld = D; a.plane_rows = PR;
+          HIP_TRY(launch_linear_skinny(a, s));
+        } else {
+          HIP_TRY(run_linear(c, a));
+        }
         void* dst = (char*)(which ? c->kv.xv : c->kv.xk) + (size_t)l * c->xkv_layer_elems() * c->kv_elem();
         HIP_TRY(launch_scatter_cross(tmp, dst, B, d.n_visual, d.n_heads, d.d_head, d.kvdtype, s));
       }
