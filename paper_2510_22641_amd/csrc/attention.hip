@@ -337,17 +337,23 @@ __global__ __launch_bounds__(256) void fold_q_kernel(const KT* __restrict__ xk,
   for (int t = 0; t < JW; ++t)
 #pragma unroll
     for (int c = 0; c < 8; ++c) acc[t][c] = 0.f;
-  for (int e = 0; e < dh; ++e) {
-    float w[8];
-    Vec8<WT> v8;
-    v8.load(wq + ((size_t)h * dh + e) * d + k);
-    v8.to_f32(w);
+  // EB rows of Wq requested at once (dh is a multiple of 16), then their products
+  constexpr int EB = NV >= 64 ? 8 : 16;
+  for (int e0 = 0; e0 < dh; e0 += EB) {
+    Vec8<WT> v8[EB];
 #pragma unroll
-    for (int t = 0; t < JW; ++t) {
-      const int j = wave + 4 * t;
-      const float kv = j < NV ? ks[j][e] : 0.f;
+    for (int u = 0; u < EB; ++u) v8[u].load(wq + ((size_t)h * dh + e0 + u) * d + k);
 #pragma unroll
-      for (int c = 0; c < 8; ++c) acc[t][c] = fmaf(kv, w[c], acc[t][c]);
+    for (int u = 0; u < EB; ++u) {
+      float w[8];
+      v8[u].to_f32(w);
+#pragma unroll
+      for (int t = 0; t < JW; ++t) {
+        const int j = wave + 4 * t;
+        const float kv = j < NV ? ks[j][e0 + u] : 0.f;
+#pragma unroll
+        for (int c = 0; c < 8; ++c) acc[t][c] = fmaf(kv, w[c], acc[t][c]);
+      }
     }
   }
 #pragma unroll
@@ -380,11 +386,20 @@ __global__ __launch_bounds__(256) void fold_o_kernel(const KT* __restrict__ xv,
   float acc[NV];
 #pragma unroll
   for (int j = 0; j < NV; ++j) acc[j] = 0.f;
-  for (int e0 = 0; e0 < dh; e0 += 8) {
+  // OB pieces of eight of the row's dh weights requested at once (dh is 64 or 128), then their
+  // products
+  constexpr int OB = NV >= 64 ? 4 : 8;
+  for (int p0 = 0; p0 * 8 < dh; p0 += OB) {
+  Vec8<WT> v8[OB];
+#pragma unroll
+  for (int u = 0; u < OB; ++u)
+    if ((p0 + u) * 8 < dh) v8[u].load(wr + (p0 + u) * 8);
+#pragma unroll
+  for (int u = 0; u < OB; ++u) {
+    if ((p0 + u) * 8 >= dh) break;
+    const int e0 = (p0 + u) * 8;
     float w[8];
-    Vec8<WT> v8;
-    v8.load(wr + e0);
-    v8.to_f32(w);
+    v8[u].to_f32(w);
 #pragma unroll
     for (int j = 0; j < NV; ++j) {
       const float4 a0 = *reinterpret_cast<const float4*>(&vs[j][e0]);
@@ -394,6 +409,7 @@ __global__ __launch_bounds__(256) void fold_o_kernel(const KT* __restrict__ xv,
       t = fmaf(a1.x, w[4], t); t = fmaf(a1.y, w[5], t); t = fmaf(a1.z, w[6], t); t = fmaf(a1.w, w[7], t);
       acc[j] = t;
     }
+  }
   }
   float* dst = fo + (size_t)n * H * NV + (size_t)h * NV;
 #pragma unroll
