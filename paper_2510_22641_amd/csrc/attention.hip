@@ -38,6 +38,22 @@ __device__ __forceinline__ const KT* key_row(const AttnArgs& a, const KT* base, 
   return base + (((size_t)page * a.H + h) * a.kv.page_size + slot) * DH;
 }
 
+// Page-table entry of key i of sequence b (clamped to the table; validated where it is used).
+__device__ __forceinline__ int key_page(const AttnArgs& a, int b, int i) {
+  const int pg_i = min(i / a.kv.page_size, a.kv.max_pages - 1);
+  return a.kv.page_table[(size_t)b * a.kv.max_pages + pg_i];
+}
+
+// key_row for a page-table entry already loaded.
+template <typename KT, int DH>
+__device__ __forceinline__ const KT* key_row_at(const AttnArgs& a, const KT* base, int h, int i,
+                                                int page, bool& ok) {
+  ok = i / a.kv.page_size < a.kv.max_pages && page >= 0 && page < a.kv.n_pages;
+  if (!ok) page = 0;
+  const int slot = i - (i / a.kv.page_size) * a.kv.page_size;
+  return base + (((size_t)page * a.H + h) * a.kv.page_size + slot) * DH;
+}
+
 template <typename KT, int DH, int QB>
 __global__ __launch_bounds__(256) void attn_kernel(const AttnArgs a, const int s_stride, const int ks) {
   constexpr int CH = DH / 8;       // 16-byte chunks per key row (bf16) / 8-element groups
@@ -57,6 +73,17 @@ __global__ __launch_bounds__(256) void attn_kernel(const AttnArgs a, const int s
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int nq = min(QB, a.C - j0);
   const int HD = a.H * DH;
+  // with one key split the keys start at 0: the page-table entries of this thread's first key
+  // row and value chunks are requested together with the sequence length, not after it
+  const bool pre = ks == 1 && !a.cross;
+  constexpr int PF0 = 8;  // value chunks prefetched per thread (PF below)
+  const int vk00 = tid / (DH / 8), kpi0 = 256 / (DH / 8);
+  int kpg = 0, vpg[PF0];
+  if (pre) {
+    kpg = key_page(a, b, tid);
+#pragma unroll
+    for (int u = 0; u < PF0; ++u) vpg[u] = key_page(a, b, vk00 + kpi0 * u);
+  }
   const int base = a.cross ? 0 : a.kv.seq_len[b] + a.kv.pos_off;
   const int nk_all = a.cross ? a.n_keys : base + j0 + nq;
   const int per = (nk_all + ks - 1) / ks;
@@ -73,13 +100,15 @@ __global__ __launch_bounds__(256) void attn_kernel(const AttnArgs a, const int s
   bool kok = false;
   Vec8<KT> krow[CH];
   if (tid < nk) {
-    const KT* kp = key_row<KT, DH>(a, Kb, b, h, k0 + tid, kok);
+    const KT* kp = pre ? key_row_at<KT, DH>(a, Kb, h, tid, kpg, kok)
+                       : key_row<KT, DH>(a, Kb, b, h, k0 + tid, kok);
     if (kok) {
 #pragma unroll
       for (int c = 0; c < CH; ++c) krow[c].load(kp + 8 * c);
     }
   }
   const int vc = tid % CH, vk0 = tid / CH;
+  static_assert(PF == PF0, "value prefetch depth");
   Vec8<KT> vpre[PF];
   bool vok[PF];
 #pragma unroll
@@ -87,7 +116,8 @@ __global__ __launch_bounds__(256) void attn_kernel(const AttnArgs a, const int s
     const int i = vk0 + KPI * u;
     vok[u] = false;
     if (i < nk) {
-      const KT* vp = key_row<KT, DH>(a, Vb, b, h, k0 + i, vok[u]);
+      const KT* vp = pre ? key_row_at<KT, DH>(a, Vb, h, i, vpg[u], vok[u])
+                         : key_row<KT, DH>(a, Vb, b, h, k0 + i, vok[u]);
       if (vok[u]) vpre[u].load(vp + 8 * vc);
     }
   }
