@@ -224,6 +224,11 @@ hipError_t launch_row_stats(const float* x, int ldx, int M, int K, int norm, flo
 hipError_t launch_argmax_final(const float* part_val, const int* part_idx, int M, int n_parts,
                                int C, int32_t* dst0, int ld0, int off0, int32_t* dst1,
                                hipStream_t s);
+// The same, and the chosen token's embedding row (embed [vocab][d] in wdtype) into x_out row m.
+hipError_t launch_argmax_final_embed(const float* part_val, const int* part_idx, int M,
+                                     int n_parts, int C, int32_t* dst0, int ld0, int off0,
+                                     int32_t* dst1, const void* embed, int wdtype, int d,
+                                     float* x_out, hipStream_t s);
 
 // Cross-attention K or V at prefill: src [B*Nv][H*dh] float32 -> dst [B][H][Nv][dh] kvdtype.
 hipError_t launch_scatter_cross(const float* src, void* dst, int B, int Nv, int H, int dh,

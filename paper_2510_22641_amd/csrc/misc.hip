@@ -75,12 +75,15 @@ __global__ void rope_scatter_kernel(const RopeScatterArgs a) {
   }
 }
 
+template <typename WT>
 __global__ __launch_bounds__(256) void argmax_final_kernel(const float* pv, const int* pi, int M,
                                                            int n_parts, int C, int32_t* dst0,
-                                                           int ld0, int off0, int32_t* dst1) {
+                                                           int ld0, int off0, int32_t* dst1,
+                                                           const WT* embed, int d, float* x_out) {
   constexpr int PER = 16;  // partials per thread requested together
   __shared__ float sv[4];
   __shared__ int si[4];
+  __shared__ int tok;
   const int m = blockIdx.x;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   float v = -INFINITY;
@@ -106,7 +109,13 @@ __global__ __launch_bounds__(256) void argmax_final_kernel(const float* pv, cons
     const int b = m / C, j = m - b * C;
     dst0[(size_t)b * ld0 + off0 + j] = i;
     if (dst1) dst1[m] = i;
+    tok = i;
   }
+  if (!x_out) return;
+  // the chosen token's embedding row, the next draft step's input (row m of x_out)
+  __syncthreads();
+  const WT* src = embed + (size_t)tok * d;
+  for (int k = threadIdx.x; k < d; k += blockDim.x) x_out[(size_t)m * d + k] = load_elem(src + k);
 }
 
 template <typename KT>
@@ -268,8 +277,25 @@ hipError_t launch_argmax_final(const float* part_val, const int* part_idx, int M
                                int C, int32_t* dst0, int ld0, int off0, int32_t* dst1,
                                hipStream_t s) {
   if (M <= 0) return hipSuccess;
-  hipLaunchKernelGGL(argmax_final_kernel, dim3(M), dim3(256), 0, s, part_val, part_idx, M, n_parts,
-                     C, dst0, ld0, off0, dst1);
+  hipLaunchKernelGGL(argmax_final_kernel<float>, dim3(M), dim3(256), 0, s, part_val, part_idx, M,
+                     n_parts, C, dst0, ld0, off0, dst1, nullptr, 0, nullptr);
+  return hipGetLastError();
+}
+
+hipError_t launch_argmax_final_embed(const float* part_val, const int* part_idx, int M,
+                                     int n_parts, int C, int32_t* dst0, int ld0, int off0,
+                                     int32_t* dst1, const void* embed, int wdtype, int d,
+                                     float* x_out, hipStream_t s) {
+  if (M <= 0) return hipSuccess;
+  if (!embed || !x_out || d < 1) return hipErrorInvalidValue;
+  if (wdtype == 1)
+    hipLaunchKernelGGL(argmax_final_kernel<bf16_t>, dim3(M), dim3(256), 0, s, part_val, part_idx,
+                       M, n_parts, C, dst0, ld0, off0, dst1,
+                       reinterpret_cast<const bf16_t*>(embed), d, x_out);
+  else
+    hipLaunchKernelGGL(argmax_final_kernel<float>, dim3(M), dim3(256), 0, s, part_val, part_idx,
+                       M, n_parts, C, dst0, ld0, off0, dst1,
+                       reinterpret_cast<const float*>(embed), d, x_out);
   return hipGetLastError();
 }
 

@@ -670,9 +670,11 @@ int run_layers(ssd_ctx* c, float* x, int B, int C, int pos_off, int l0, int l1, 
 
 // g = final RMSNorm + LM head, argmax per row.  Rows m of x (stride ldx) map to dst0 as in
 // launch_argmax_final.
+// embed_out (argmax only): the chosen tokens' embedding rows [M][d_model], the next draft step's
+// input, written by the final argmax.
 int run_head(ssd_ctx* c, const float* x, int ldx, int M, int C, float* logits, int ldl,
              int32_t* dst0, int ld0, int off0, int32_t* dst1, const float* u = nullptr,
-             int ldu = 0, int uoff = 0, float tau = 0.f) {
+             int ldu = 0, int uoff = 0, float tau = 0.f, float* embed_out = nullptr) {
   const ssd_dims& d = c->d;
   LinearArgs a = lin(c);
   a.x = x; a.ldx = ldx; a.M = M; a.K = d.d_model;
@@ -697,6 +699,11 @@ int run_head(ssd_ctx* c, const float* x, int ldx, int M, int C, float* logits, i
     // sampled tokens: inverse CDF of softmax(logits / tau) per row (the logits are written above)
     HIP_TRY(launch_sample_rows(logits, ldl, M, d.vocab, tau, u, ldu, uoff, C, dst0, ld0, off0,
                                dst1, c->stream));
+    return SSD_OK;
+  }
+  if (embed_out) {
+    HIP_TRY(launch_argmax_final_embed(a.part_val, a.part_idx, M, n_parts, C, dst0, ld0, off0, dst1,
+                                      c->w.embed, d.wdtype, d.d_model, embed_out, c->stream));
     return SSD_OK;
   }
   HIP_TRY(launch_argmax_final(a.part_val, a.part_idx, M, n_parts, C, dst0, ld0, off0, dst1,
@@ -754,13 +761,17 @@ int draft_launches(ssd_ctx* c, int B, int gamma, const int32_t* pending, int32_t
     }
     return SSD_OK;
   }
+  // greedy drafts: the final argmax of step i also writes step i + 1's embedding rows into x
+  const bool fuse_embed = !u;
   for (int i = 0; i < gamma; ++i) {
-    EmbedArgs e;
-    e.x = x; e.B = B; e.C = 1; e.d = D; e.embed = c->w.embed; e.vocab = d.vocab;
-    e.wdtype = d.wdtype; e.t0 = nullptr; e.t1 = i == 0 ? pending : cur; e.ld1 = 1;
-    e.visual = nullptr; e.n_visual = d.n_visual; e.n_prefix = 0;
-    e.status = c->at<int32_t>(c->L.status);
-    HIP_TRY(launch_embed(e, c->stream));
+    if (i == 0 || !fuse_embed) {
+      EmbedArgs e;
+      e.x = x; e.B = B; e.C = 1; e.d = D; e.embed = c->w.embed; e.vocab = d.vocab;
+      e.wdtype = d.wdtype; e.t0 = nullptr; e.t1 = i == 0 ? pending : cur; e.ld1 = 1;
+      e.visual = nullptr; e.n_visual = d.n_visual; e.n_prefix = 0;
+      e.status = c->at<int32_t>(c->L.status);
+      HIP_TRY(launch_embed(e, c->stream));
+    }
     int rc = run_layers(c, x, B, 1, pos_base + i, 0, d.draft_layers, d.draft_layers - 1,
                         stash + (size_t)i * D, ld_stash);
     if (rc) return rc;
@@ -775,7 +786,8 @@ int draft_launches(ssd_ctx* c, int B, int gamma, const int32_t* pending, int32_t
     });
     if (rc) return rc;
     rc = run_head(c, xi, D, B, 1, logits ? logits + (size_t)i * d.vocab : nullptr,
-                  gamma * d.vocab, draft, gamma, i, cur, u, gamma, i, tau);
+                  gamma * d.vocab, draft, gamma, i, cur, u, gamma, i, tau,
+                  fuse_embed && i + 1 < gamma ? x : nullptr);
     if (rc) return rc;
   }
   return SSD_OK;
