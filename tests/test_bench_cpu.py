@@ -51,3 +51,28 @@ def test_gpus_other_than_one_exit_with_a_message(capsys, monkeypatch):
     except SystemExit as e:
         assert e.code == 2
     assert "one GPU" in capsys.readouterr().err
+
+
+def test_prefill_flops_llava_matches_the_parameter_count():
+    """LLaVA-1.5-7B shape, 576 visual + 32 prompt rows: 2 flops per weight per row over the
+    6.48e9 parameters the 32 layers touch, plus causal attention (QK and PV over the lower
+    triangle) and the head for the last row, about 7.97 TFLOP."""
+    sh = synth.LLAVA_7B
+    d, f, V, L, rows = 4096, 11008, 32000, 32, 608
+    params = L * (4 * d * d + 3 * d * f)
+    attn = L * 2 * rows * rows * d  # 2 (QK, PV) x 2 flops x rows^2 / 2 x (H x dh = d)
+    expect = 2.0 * params * rows + attn + 2.0 * V * d
+    got = bench.prefill_flops(sh, 1, 32)
+    assert abs(got - expect) / expect < 1e-12
+    assert 7.9e12 < got < 8.05e12
+
+
+def test_prefill_flops_flant5_xl_counts_the_visual_projections():
+    """FlanT5-xl, 8 prompt rows and 32 visual rows: the prompt through the self-attention and FFN
+    projections and the cross query / output, the visual rows through the cross K / V
+    projections, self-attention over the prompt and cross-attention to the visual rows."""
+    sh = synth.FLANT5_XL
+    d, f, V, L, P, nv = 2048, 5120, 32128, 24, 8, 32
+    per_layer = (2.0 * (4 * d * d + 3 * d * f) * P + 2.0 * P * P * d
+                 + 2.0 * 2 * d * d * nv + 2.0 * 2 * d * d * P + 4.0 * P * nv * d)
+    assert bench.prefill_flops(sh, 1, P) == L * per_layer + 2.0 * V * d
