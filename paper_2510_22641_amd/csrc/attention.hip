@@ -130,6 +130,10 @@ __global__ __launch_bounds__(256) void attn_kernel(const AttnArgs a, const int s
 
   // scores: one key per thread per step (i relative to k0)
   for (int i = tid; i < nk; i += 256) {
+    // query blocks and 512-byte key rows: the query reads stay inside the loop (hoisted out of
+    // it they pin up to 8 rows of registers, and spill with float keys at dh 128); a one-row
+    // block with a short key row keeps them hoisted
+    if constexpr (QB > 1 || DH * sizeof(KT) > 256) asm volatile("" ::: "memory");
     bool ok = kok;
     if (i != tid) {
       const KT* kp = key_row<KT, DH>(a, Kb, b, h, k0 + i, ok);
