@@ -279,15 +279,28 @@ __global__ __launch_bounds__(DH) void attn_combine_kernel(const AttnArgs a, cons
   const int h = blockIdx.x, r = blockIdx.y, d = threadIdx.x;
   const int HD = a.H * DH;
   const float* pp = a.part + ((size_t)r * a.H + h) * ks * (DH + 2);
-  float m = -INFINITY;
-  for (int sp = 0; sp < ks; ++sp) m = fmaxf(m, pp[sp * (DH + 2) + DH]);
-  float l = 0.f, o = 0.f;
-  for (int sp = 0; sp < ks; ++sp) {
-    const float ms = pp[sp * (DH + 2) + DH];
-    const float w = ms == -INFINITY ? 0.f : expf(ms - m);
-    l = fmaf(w, pp[sp * (DH + 2) + DH + 1], l);
-    o = fmaf(w, pp[sp * (DH + 2) + d], o);
+  // every split's max, sum and output requested before the first is used (one memory round trip
+  // instead of one per split); indexes past ks re-read the last split and are not used
+  float ms[ATTN_SPLITS_MAX], ls[ATTN_SPLITS_MAX], os[ATTN_SPLITS_MAX];
+#pragma unroll
+  for (int sp = 0; sp < ATTN_SPLITS_MAX; ++sp) {
+    const float* q = pp + (size_t)min(sp, ks - 1) * (DH + 2);
+    ms[sp] = q[DH];
+    ls[sp] = q[DH + 1];
+    os[sp] = q[d];
   }
+  float m = -INFINITY;
+#pragma unroll
+  for (int sp = 0; sp < ATTN_SPLITS_MAX; ++sp)
+    if (sp < ks) m = fmaxf(m, ms[sp]);
+  float l = 0.f, o = 0.f;
+#pragma unroll
+  for (int sp = 0; sp < ATTN_SPLITS_MAX; ++sp)
+    if (sp < ks) {
+      const float w = ms[sp] == -INFINITY ? 0.f : expf(ms[sp] - m);
+      l = fmaf(w, ls[sp], l);
+      o = fmaf(w, os[sp], o);
+    }
   const float y = l > 0.f ? o / l : 0.f;
   const size_t oi = (size_t)r * HD + h * DH + d;
   a.out[oi] = y;
