@@ -73,20 +73,23 @@ __global__ __launch_bounds__(256) void attn_kernel(const AttnArgs a, const int s
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int nq = min(QB, a.C - j0);
   const int HD = a.H * DH;
-  // with one key split the keys start at 0: the page-table entries of this thread's first key
-  // row and value chunks are requested together with the sequence length, not after it
-  const bool pre = ks == 1 && !a.cross;
+  // self-attention key ranges do not depend on the sequence length (one split: from 0; several:
+  // fixed ranges of ceil(max_seq / ks) keys, the last ones empty while the context is short), so
+  // the page-table entries of this thread's first key row and value chunks are requested
+  // together with the sequence length, not after it
+  const bool pre = !a.cross;
+  const int kfix = ks == 1 ? 0 : (a.max_seq + ks - 1) / ks;
   constexpr int PF0 = 8;  // value chunks prefetched per thread (PF below)
   const int vk00 = tid / (DH / 8), kpi0 = 256 / (DH / 8);
   int kpg = 0, vpg[PF0];
   if (pre) {
-    kpg = key_page(a, b, tid);
+    kpg = key_page(a, b, split * kfix + tid);
 #pragma unroll
-    for (int u = 0; u < PF0; ++u) vpg[u] = key_page(a, b, vk00 + kpi0 * u);
+    for (int u = 0; u < PF0; ++u) vpg[u] = key_page(a, b, split * kfix + vk00 + kpi0 * u);
   }
   const int base = a.cross ? 0 : a.kv.seq_len[b] + a.kv.pos_off;
   const int nk_all = a.cross ? a.n_keys : base + j0 + nq;
-  const int per = (nk_all + ks - 1) / ks;
+  const int per = ks == 1 ? nk_all : kfix;
   const int k0 = min(nk_all, split * per);
   int nk = min(nk_all, k0 + per) - k0;
   if (nk > s_stride) {
@@ -100,7 +103,7 @@ __global__ __launch_bounds__(256) void attn_kernel(const AttnArgs a, const int s
   bool kok = false;
   Vec8<KT> krow[CH];
   if (tid < nk) {
-    const KT* kp = pre ? key_row_at<KT, DH>(a, Kb, h, tid, kpg, kok)
+    const KT* kp = pre ? key_row_at<KT, DH>(a, Kb, h, k0 + tid, kpg, kok)
                        : key_row<KT, DH>(a, Kb, b, h, k0 + tid, kok);
     if (kok) {
 #pragma unroll
@@ -116,7 +119,7 @@ __global__ __launch_bounds__(256) void attn_kernel(const AttnArgs a, const int s
     const int i = vk0 + KPI * u;
     vok[u] = false;
     if (i < nk) {
-      const KT* vp = pre ? key_row_at<KT, DH>(a, Vb, h, i, vpg[u], vok[u])
+      const KT* vp = pre ? key_row_at<KT, DH>(a, Vb, h, k0 + i, vpg[u], vok[u])
                          : key_row<KT, DH>(a, Vb, b, h, k0 + i, vok[u]);
       if (vok[u]) vpre[u].load(vp + 8 * vc);
     }
