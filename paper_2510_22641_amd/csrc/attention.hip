@@ -153,14 +153,14 @@ __global__ __launch_bounds__(256) void attn_kernel(const AttnArgs a, const int s
       for (int c = 0; c < CH; ++c) {
         float kf[8];
         krow[c].to_f32(kf);
+        // every row of the block (rows past nq hold zeros and are masked below): no branch
+        // between the LDS reads of the rows, so they are issued together
 #pragma unroll
         for (int jq = 0; jq < QB; ++jq) {
-          if (jq < nq) {
-            float t = dots[jq];
+          float t = dots[jq];
 #pragma unroll
-            for (int e = 0; e < 8; ++e) t = fmaf(qs[jq][8 * c + e], kf[e], t);
-            dots[jq] = t;
-          }
+          for (int e = 0; e < 8; ++e) t = fmaf(qs[jq][8 * c + e], kf[e], t);
+          dots[jq] = t;
         }
       }
     }
@@ -226,11 +226,11 @@ __global__ __launch_bounds__(256) void attn_kernel(const AttnArgs a, const int s
         vpre[u].to_f32(vf);
 #pragma unroll
         for (int jq = 0; jq < QB; ++jq) {
-          if (jq < nq) {
-            const float p = S[jq * s_stride + i];
+          // rows past nq (scores never turned into probabilities) contribute nothing
+          const float sp = S[jq * s_stride + i];
+          const float p = jq < nq ? sp : 0.f;
 #pragma unroll
-            for (int e = 0; e < 8; ++e) acc[jq][e] = fmaf(p, vf[e], acc[jq][e]);
-          }
+          for (int e = 0; e < 8; ++e) acc[jq][e] = fmaf(p, vf[e], acc[jq][e]);
         }
       }
     }
