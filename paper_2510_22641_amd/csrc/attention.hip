@@ -54,7 +54,37 @@ __device__ __forceinline__ const KT* key_row_at(const AttnArgs& a, const KT* bas
   return base + (((size_t)page * a.H + h) * a.kv.page_size + slot) * DH;
 }
 
-template <typename KT, int DH, int QB>
+// Buffer-resource loads of key / value rows: 32-bit byte offsets from a pool base, and an offset
+// past the resource's range (ATTN_OOB) returns zeros without a memory access, so masked lanes
+// need no branch and cost no traffic.
+typedef uint32_t attn_u32x4 __attribute__((ext_vector_type(4)));
+constexpr uint32_t ATTN_OOB = 0x80000000u;
+constexpr size_t ATTN_RS_MAX = 0x7fff0000u;
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t attn_rsrc(const void* p, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), 0, (int)bytes, 0x00020000);
+}
+
+// Bytes of the key (or value) pool a launch may read from its base.
+template <typename KT, int DH>
+__host__ __device__ size_t attn_pool_bytes(const AttnArgs& a) {
+  const size_t row = (size_t)DH * sizeof(KT);
+  return a.cross ? (size_t)a.B * a.H * a.n_keys * row
+                 : (size_t)a.kv.n_pages * a.H * a.kv.page_size * row;
+}
+__device__ __forceinline__ void load_rs(Vec8<bf16_t>& v, __amdgpu_buffer_rsrc_t r, uint32_t off) {
+  const attn_u32x4 t = __builtin_bit_cast(attn_u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+  v.r = make_uint4(t.x, t.y, t.z, t.w);
+}
+__device__ __forceinline__ void load_rs(Vec8<float>& v, __amdgpu_buffer_rsrc_t r, uint32_t off) {
+  const attn_u32x4 t0 = __builtin_bit_cast(attn_u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+  const attn_u32x4 t1 =
+      __builtin_bit_cast(attn_u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off + 16u, 0, 0));
+  v.a = make_float4(__uint_as_float(t0.x), __uint_as_float(t0.y), __uint_as_float(t0.z), __uint_as_float(t0.w));
+  v.b = make_float4(__uint_as_float(t1.x), __uint_as_float(t1.y), __uint_as_float(t1.z), __uint_as_float(t1.w));
+}
+
+// RS: the layer's key and value pools span less than 2 GiB and are read with buffer loads.
+template <typename KT, int DH, int QB, bool RS>
 __global__ __launch_bounds__(256) void attn_kernel(const AttnArgs a, const int s_stride, const int ks) {
   constexpr int CH = DH / 8;       // 16-byte chunks per key row (bf16) / 8-element groups
   constexpr int KPI = 256 / CH;    // keys per block step in P.V
@@ -73,21 +103,44 @@ __global__ __launch_bounds__(256) void attn_kernel(const AttnArgs a, const int s
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int nq = min(QB, a.C - j0);
   const int HD = a.H * DH;
+  // Every load of the prologue is issued on every path (a masked lane reads zeros or a valid
+  // row, never skips the load): the wait counter retires loads in issue order, and a load skipped
+  // on one path makes the compiler wait for everything issued before the next one.
+  // The query rows first (they depend on nothing), then the page-table entries, the sequence
+  // length, the key row, the value chunks and the position bias.
+  constexpr int QPT = (QB * DH + 255) / 256;  // query elements per thread
+  float qv[QPT];
+#pragma unroll
+  for (int t = 0; t < QPT; ++t) {
+    const int idx = min(tid + 256 * t, QB * DH - 1);
+    const int jq = min(idx / DH, nq - 1), d = idx - (idx / DH) * DH;
+    qv[t] = a.q[(size_t)(b * a.C + j0 + jq) * HD + h * DH + d];
+  }
+  // the sequence length as a vector load issued now (a scalar load would be issued where it is
+  // first used, after the key and value loads, and the bias would wait for it); cross-attention
+  // reads a placeholder
+  int vzero;
+  asm volatile("v_mov_b32 %0, 0" : "=v"(vzero));
+  const int* slp = a.cross ? reinterpret_cast<const int*>(a.q) : a.kv.seq_len + b;
+  const int seq_len_v = slp[vzero];
   // self-attention key ranges do not depend on the sequence length (one split: from 0; several:
   // fixed ranges of ceil(max_seq / ks) keys, the last ones empty while the context is short), so
   // the page-table entries of this thread's first key row and value chunks are requested
   // together with the sequence length, not after it
   const bool pre = !a.cross;
-  const int kfix = ks == 1 ? 0 : (a.max_seq + ks - 1) / ks;
+  const int kfix = ks == 1 ? 0 : (a.max_seq + ks - 1) / ks, kbase = split * kfix;
   constexpr int PF0 = 8;  // value chunks prefetched per thread (PF below)
   const int vk00 = tid / (DH / 8), kpi0 = 256 / (DH / 8);
   int kpg = 0, vpg[PF0];
   if (pre) {
-    kpg = key_page(a, b, split * kfix + tid);
+    kpg = key_page(a, b, kbase + tid);
 #pragma unroll
-    for (int u = 0; u < PF0; ++u) vpg[u] = key_page(a, b, split * kfix + vk00 + kpi0 * u);
+    for (int u = 0; u < PF0; ++u) vpg[u] = key_page(a, b, kbase + vk00 + kpi0 * u);
   }
-  const int base = a.cross ? 0 : a.kv.seq_len[b] + a.kv.pos_off;
+  const KT* Kb = reinterpret_cast<const KT*>(a.cross ? a.xk : a.kv.k);
+  const KT* Vb = reinterpret_cast<const KT*>(a.cross ? a.xv : a.kv.v);
+
+  const int base = a.cross ? 0 : __builtin_amdgcn_readfirstlane(seq_len_v) + a.kv.pos_off;
   const int nk_all = a.cross ? a.n_keys : base + j0 + nq;
   const int per = ks == 1 ? nk_all : kfix;
   const int k0 = min(nk_all, split * per);
@@ -96,16 +149,25 @@ __global__ __launch_bounds__(256) void attn_kernel(const AttnArgs a, const int s
     if (tid == 0) atomicOr(a.status, SSD_DEV_CAPACITY);
     nk = s_stride;
   }
-  const KT* Kb = reinterpret_cast<const KT*>(a.cross ? a.xk : a.kv.k);
-  const KT* Vb = reinterpret_cast<const KT*>(a.cross ? a.xv : a.kv.v);
 
-  // issue the first key row and the first value chunks before any barrier
+  // the first key row and the first value chunks, before any barrier.  Self-attention addresses
+  // them from the split's fixed start (a non-empty split starts there) and the page-table
+  // entries.  Lanes past nk (and rows of a missing page) are masked: buffer loads with an
+  // out-of-range offset (RS), else a clamped valid row.
+  const int clast = a.n_keys - 1;
+  const uint32_t pool_rs = RS ? (uint32_t)attn_pool_bytes<KT, DH>(a) : 0u;
+  const __amdgpu_buffer_rsrc_t krs = attn_rsrc(Kb, pool_rs), vrs = attn_rsrc(Vb, pool_rs);
   bool kok = false;
   Vec8<KT> krow[CH];
-  if (tid < nk) {
-    const KT* kp = pre ? key_row_at<KT, DH>(a, Kb, h, k0 + tid, kpg, kok)
-                       : key_row<KT, DH>(a, Kb, b, h, k0 + tid, kok);
-    if (kok) {
+  {
+    const KT* kp = pre ? key_row_at<KT, DH>(a, Kb, h, kbase + tid, kpg, kok)
+                       : key_row<KT, DH>(a, Kb, b, h, min(tid, clast), kok);
+    kok = kok && tid < nk;
+    if constexpr (RS) {
+      const uint32_t off = kok ? (uint32_t)((size_t)(kp - Kb) * sizeof(KT)) : ATTN_OOB;
+#pragma unroll
+      for (int c = 0; c < CH; ++c) load_rs(krow[c], krs, off + 8u * c * sizeof(KT));
+    } else {
 #pragma unroll
       for (int c = 0; c < CH; ++c) krow[c].load(kp + 8 * c);
     }
@@ -117,17 +179,35 @@ __global__ __launch_bounds__(256) void attn_kernel(const AttnArgs a, const int s
 #pragma unroll
   for (int u = 0; u < PF; ++u) {
     const int i = vk0 + KPI * u;
-    vok[u] = false;
-    if (i < nk) {
-      const KT* vp = pre ? key_row_at<KT, DH>(a, Vb, h, k0 + i, vpg[u], vok[u])
-                         : key_row<KT, DH>(a, Vb, b, h, k0 + i, vok[u]);
-      if (vok[u]) vpre[u].load(vp + 8 * vc);
+    const KT* vp = pre ? key_row_at<KT, DH>(a, Vb, h, kbase + i, vpg[u], vok[u])
+                       : key_row<KT, DH>(a, Vb, b, h, min(i, clast), vok[u]);
+    vok[u] = vok[u] && i < nk;
+    if constexpr (RS) {
+      const uint32_t off = vok[u] ? (uint32_t)((size_t)(vp - Vb + 8 * vc) * sizeof(KT)) : ATTN_OOB;
+      load_rs(vpre[u], vrs, off);
+    } else {
+      vpre[u].load(vp + 8 * vc);
+    }
+  }
+  // T5 position bias of this thread's first key for each query row (LLaMA and cross-attention:
+  // a placeholder read of the query)
+  float bpre[QB];
+  {
+    const float* bsrc = (a.bias && !a.cross) ? a.bias + (size_t)h * a.max_seq : a.q;
+#pragma unroll
+    for (int jq = 0; jq < QB; ++jq) {
+      const int dist = base + j0 + jq - (k0 + tid);
+      bpre[jq] = bsrc[(a.bias && !a.cross) ? min(max(dist, 0), a.max_seq - 1) : 0];
     }
   }
 
-  for (int idx = tid; idx < QB * DH; idx += 256) {
-    const int jq = idx / DH, d = idx - jq * DH;
-    qs[jq][d] = jq < nq ? a.q[(size_t)(b * a.C + j0 + jq) * HD + h * DH + d] * a.scale : 0.f;
+#pragma unroll
+  for (int t = 0; t < QPT; ++t) {
+    const int idx = tid + 256 * t;
+    if (idx < QB * DH) {
+      const int jq = idx / DH, d = idx - jq * DH;
+      qs[jq][d] = jq < nq ? qv[t] * a.scale : 0.f;
+    }
   }
   __syncthreads();
 
@@ -172,7 +252,8 @@ __global__ __launch_bounds__(256) void attn_kernel(const AttnArgs a, const int s
       } else if (!a.cross) {
         const int p = base + j0 + jq, ki = k0 + i;
         if (ki > p) sc = -INFINITY;
-        else if (a.bias && p - ki < a.max_seq) sc += a.bias[(size_t)h * a.max_seq + (p - ki)];
+        else if (a.bias && p - ki < a.max_seq)
+          sc += i == tid ? bpre[jq] : a.bias[(size_t)h * a.max_seq + (p - ki)];
       }
       S[jq * s_stride + i] = sc;
     }
@@ -331,6 +412,7 @@ template <typename KT, int DH>
 hipError_t launch_attn_dh(const AttnArgs& a, hipStream_t s) {
   const int nk_max = a.cross ? a.n_keys : a.max_seq;
   const bool long_ctx = !a.cross && a.max_seq >= 256;
+  const bool rs = attn_pool_bytes<KT, DH>(a) <= ATTN_RS_MAX;
   int ks = 1;
   if (a.C == 1 || (a.C <= 16 && !long_ctx)) {
     // decode steps and short-context verify chunks: one block per (head, sequence, query row
@@ -340,7 +422,10 @@ hipError_t launch_attn_dh(const AttnArgs& a, hipStream_t s) {
     const int s_stride = (((nk_max + ks - 1) / ks) + 63) & ~63;
     dim3 grid(a.H, a.B, a.C * ks);
     const size_t shm = (size_t)s_stride * sizeof(float);
-    hipLaunchKernelGGL((attn_kernel<KT, DH, 1>), grid, dim3(256), shm, s, a, s_stride, ks);
+    if (rs)
+      hipLaunchKernelGGL((attn_kernel<KT, DH, 1, true>), grid, dim3(256), shm, s, a, s_stride, ks);
+    else
+      hipLaunchKernelGGL((attn_kernel<KT, DH, 1, false>), grid, dim3(256), shm, s, a, s_stride, ks);
   } else {
     // prefill blocks and long-context verify chunks: up to QB rows of a sequence share each key
     // load (and long contexts split their keys)
@@ -349,7 +434,10 @@ hipError_t launch_attn_dh(const AttnArgs& a, hipStream_t s) {
     const int s_stride = (((nk_max + ks - 1) / ks) + 63) & ~63;
     dim3 grid(a.H, a.B, groups * ks);
     const size_t shm = (size_t)QB * s_stride * sizeof(float);
-    hipLaunchKernelGGL((attn_kernel<KT, DH, QB>), grid, dim3(256), shm, s, a, s_stride, ks);
+    if (rs)
+      hipLaunchKernelGGL((attn_kernel<KT, DH, QB, true>), grid, dim3(256), shm, s, a, s_stride, ks);
+    else
+      hipLaunchKernelGGL((attn_kernel<KT, DH, QB, false>), grid, dim3(256), shm, s, a, s_stride, ks);
   }
   if (ks > 1) {
     hipError_t e = hipGetLastError();

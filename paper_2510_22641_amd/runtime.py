@@ -26,6 +26,7 @@ class Capacity:
     max_seq: int
     max_prompt: int
     page_size: int = 16
+    spare_pages: int = 0  # pool pages beyond those the page table can reach at once
 
 
 class DeviceDecoder:
@@ -97,12 +98,14 @@ class DeviceDecoder:
         dims = self.dims()
         self._dims = dims
         H, dh, L = sh.n_heads, sh.d_head, sh.n_layers
-        n_pages = cap.max_batch * dims.max_pages
+        n_table = cap.max_batch * dims.max_pages
+        n_pages = n_table + cap.spare_pages
         self.k_pool = torch.zeros((L, n_pages, H, cap.page_size, dh), dtype=self.kvdtype, device=dev)
         self.v_pool = torch.zeros_like(self.k_pool)
         pages = np.arange(n_pages, dtype=np.int32)
         if self.page_seed is not None:  # scatter sequences over the pool to exercise the table
             pages = np.random.default_rng(self.page_seed).permutation(pages).astype(np.int32)
+        pages = pages[:n_table]
         self.page_table = torch.from_numpy(pages.reshape(cap.max_batch, dims.max_pages)).to(dev)
         self.seq_len = torch.zeros(cap.max_batch, dtype=torch.int32, device=dev)
         if sh.arch == "t5":
@@ -258,14 +261,14 @@ class DeviceDecoder:
 def from_workload(wl, seed: int, device: str = "cuda", max_batch: Optional[int] = None,
                   max_gamma: Optional[int] = None, extra_seq: int = 0, page_seed: Optional[int] = None,
                   kv_dtype: Optional[str] = None, weights: Optional[Dict] = None,
-                  draft_layers: Optional[int] = None) -> DeviceDecoder:
+                  draft_layers: Optional[int] = None, spare_pages: int = 0) -> DeviceDecoder:
     """Build a DeviceDecoder for a synth workload, streaming its seeded tensors to the device."""
     import synth
     sh = wl.shape
     mg = max_gamma if max_gamma is not None else max(wl.gamma, 1)
     cap = Capacity(max_batch=max_batch or wl.batch, max_gamma=mg,
                    max_seq=sh.prefix_len() + wl.prompt_len + wl.new_tokens + mg + 1 + extra_seq,
-                   max_prompt=wl.prompt_len)
+                   max_prompt=wl.prompt_len, spare_pages=spare_pages)
     dd = DeviceDecoder(sh, draft_layers or wl.draft_layers, cap, device=device, kv_dtype=kv_dtype,
                        page_seed=page_seed)
     if weights is not None:

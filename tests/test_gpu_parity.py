@@ -279,6 +279,34 @@ def test_long_capacity_splits_attention_keys(wl):
     assert dd.sync_status() == (0, 0)
 
 
+def test_kv_pool_beyond_2gib_matches_small_pool():
+    """Layer pools of more than 2 GiB (sequences scattered over 200k spare pages, about a third
+    of them past the 2 GiB offset): the attention addresses them with 64-bit pointers instead of
+    32-bit buffer offsets, and the run equals the one on a small pool token for token and in its
+    acceptance (the same values enter the same arithmetic)."""
+    import torch
+    from paper_2510_22641_amd import runtime
+    wl = synth.S_LLAMA_F32
+    sh = wl.shape
+    runs = []
+    for spare in (0, 200_000):
+        w, z, pr = parity.workload_inputs(wl, 13)
+        dd = runtime.from_workload(wl, 13, weights=w, page_seed=5, extra_seq=250,
+                                   spare_pages=spare)
+        layer_bytes = dd.k_pool[0].numel() * dd.k_pool.element_size()
+        assert (layer_bytes > 2 ** 31) == (spare > 0)
+        assert dd.cap.max_seq >= 256  # key splits too
+        pt, vt = dd.upload_inputs(pr, z)
+        toks, st = dd.generate(pt, vt, wl.new_tokens, wl.gamma, speculative=True, reuse=True)
+        runs.append((toks.cpu().numpy().tolist(), st))
+        assert dd.sync_status() == (0, 0)
+        dd.close()
+        del dd
+        torch.cuda.empty_cache()
+    assert runs[0] == runs[1]
+    assert sh.d_head == 128 and sh.dtype == "f32"
+
+
 @pytest.mark.parametrize("wl", [synth.S1, synth.S_T5], ids=lambda w: w.name)
 def test_folded_cross_attention_matches_unfolded_and_oracle(wl):
     """A one-sequence T5 context folds the cross-attention into two float32 matrices per layer,
