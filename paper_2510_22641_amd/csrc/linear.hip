@@ -1723,21 +1723,23 @@ void launch_gemv1(const LinearArgs& a, dim3 grid, hipStream_t s, LaunchTiming* t
   }
 }
 
-template <int KP, int NORM>
+template <int KP, int NORM, typename WT = bf16_t>
 void launch_gemv1k(const LinearArgs& a, dim3 grid, hipStream_t s, LaunchTiming* t) {
   if (t) {
-    hipExtLaunchKernelGGL((gemv1k_kernel<bf16_t, KP, NORM>), grid, dim3(256), 0u, s, t->start,
+    hipExtLaunchKernelGGL((gemv1k_kernel<WT, KP, NORM>), grid, dim3(256), 0u, s, t->start,
                           t->stop, 0u, a);
     t->timed = true;
   } else {
-    hipLaunchKernelGGL((gemv1k_kernel<bf16_t, KP, NORM>), grid, dim3(256), 0, s, a);
+    hipLaunchKernelGGL((gemv1k_kernel<WT, KP, NORM>), grid, dim3(256), 0, s, a);
   }
 }
 
 // One bf16 row with 2048 <= K <= 6144 and no LayerNorm, or up to 12288 without a norm (the
-// LLaMA-7B down projection, K = 11008): the K-split kernel (same grid as gemv1).
+// LLaMA-7B down projection, K = 11008): the K-split kernel (same grid as gemv1).  float32
+// weights at K = 2048 too (the folded cross-attention scores of a FlanT5-xl-sized layer).
 bool use_gemv1k(const LinearArgs& a) {
-  if (a.M != 1 || a.wdtype != 1 || a.K < 2048 || a.K % 8) return false;
+  if (a.M != 1 || a.K < 2048 || a.K % 8) return false;
+  if (a.wdtype != 1) return a.K == 2048 && (a.norm == NORM_RMS || a.norm == NORM_NONE);
   if (a.norm == NORM_RMS) return a.K <= 3 * 2048;
   return a.norm == NORM_NONE && a.K <= 6 * 2048;
 }
@@ -1749,7 +1751,10 @@ hipError_t launch_gemv1k_any(const LinearArgs& a, hipStream_t s, LaunchTiming* t
   LaunchTiming* tt = timed ? t : nullptr;
   const int kp = (a.K + 2047) / 2048;
   const bool rms = a.norm == NORM_RMS;
-  if (kp == 1) rms ? launch_gemv1k<1, NORM_RMS>(a, grid, s, tt) : launch_gemv1k<1, NORM_NONE>(a, grid, s, tt);
+  if (a.wdtype != 1) {
+    rms ? launch_gemv1k<1, NORM_RMS, float>(a, grid, s, tt)
+        : launch_gemv1k<1, NORM_NONE, float>(a, grid, s, tt);
+  } else if (kp == 1) rms ? launch_gemv1k<1, NORM_RMS>(a, grid, s, tt) : launch_gemv1k<1, NORM_NONE>(a, grid, s, tt);
   else if (kp == 2) rms ? launch_gemv1k<2, NORM_RMS>(a, grid, s, tt) : launch_gemv1k<2, NORM_NONE>(a, grid, s, tt);
   else if (kp == 3) rms ? launch_gemv1k<3, NORM_RMS>(a, grid, s, tt) : launch_gemv1k<3, NORM_NONE>(a, grid, s, tt);
   else if (kp == 4) launch_gemv1k<4, NORM_NONE>(a, grid, s, tt);
