@@ -128,6 +128,25 @@ def test_ragged_batch_each_sequence_matches_oracle(wl):
     assert dd.sync_status() == (0, 0)
 
 
+@pytest.mark.parametrize("wl", [synth.S_T5, synth.S_LLAMA], ids=lambda w: w.name)
+def test_ragged_batch_with_key_splits_matches_oracle(wl):
+    """A ragged batch in a cache of 256 positions or more: each head's keys are split into fixed
+    ranges of ceil(capacity / splits), so while the contexts are short the later splits of every
+    sequence are empty (their partials carry no weight in the merge), and the sequences reach
+    their split boundaries in different rounds.  Every sequence follows the oracle."""
+    B = 3
+    dd, dec, pr, z, pt, vt = _setup(wl, seed=6, batch=B, page_seed=7, extra_seq=250 + wl.gamma)
+    assert dd.cap.max_seq >= 256
+    run = parity.device_run(dd, pt, vt, wl.new_tokens, wl.gamma, reuse=True)
+    assert dd.sync_status() == (0, 0)
+    for b in range(B):
+        parity.check_run_against_oracle(dec, wl.shape, pr[b], z[b], run, b, wl.gamma)
+        assert len(run.tokens[b]) == wl.new_tokens
+    toks, _ = dd.generate(pt, vt, wl.new_tokens, wl.gamma, speculative=True, reuse=True)
+    assert toks.cpu().numpy().tolist() == run.tokens
+    assert dd.sync_status() == (0, 0)
+
+
 def test_generate_ragged_batch_fits_the_minimal_cache():
     """ssd_generate on a batch whose sequences finish in different rounds needs no slack: a
     finished sequence keeps only its emitted positions."""
