@@ -262,9 +262,10 @@ struct AcceptArgs {
   int32_t* active_rw;     // [B] cleared when count reaches T
   int T;
   int64_t* stats;         // [3]: rounds (added by thread 0), accepted, drafted
-  int32_t* n_active;      // [3]: sequences still active, shortest seq_len among them, and (with
+  int32_t* n_active;      // [4]: sequences still active, shortest seq_len among them, (with
                           // guess) 1 when every sequence still active accepted all gamma drafts
-                          // and its new pending token equals guess[b], else 0
+                          // and its new pending token equals guess[b] else 0, and the most
+                          // tokens an active sequence still needs
   const int32_t* guess;   // [B] or null: the token the drafts made ahead start from
 };
 hipError_t launch_accept(const AcceptArgs& a, hipStream_t s);
@@ -300,7 +301,7 @@ struct GenInitArgs {
   int32_t* count;
   int32_t* active;
   int64_t* stats;
-  int32_t* n_active;        // [2]: sequences active, shortest seq_len among them
+  int32_t* n_active;        // [4]: as AcceptArgs::n_active
   const int32_t* seq_len;
 };
 hipError_t launch_gen_init(const GenInitArgs& a, hipStream_t s);

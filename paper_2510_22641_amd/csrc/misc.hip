@@ -153,6 +153,7 @@ __global__ void accept_kernel(const AcceptArgs a) {
   __shared__ int act_after[256];
   __shared__ int len_after[256];
   __shared__ int ahead_ok[256];
+  __shared__ int need_after[256];
   const int b = threadIdx.x;
   const int g = a.gamma;
   int n = 0;
@@ -200,15 +201,17 @@ __global__ void accept_kernel(const AcceptArgs a) {
   acc_n[b] = did ? n : -1;
   act_after[b] = still;
   len_after[b] = (b < a.B && still) ? a.seq_len[b] : INT_MAX;
+  need_after[b] = (b < a.B && still && a.tokens) ? a.T - a.count[b] : 0;
   ahead_ok[b] = ok;
   __syncthreads();
   if (b == 0 && a.stats) {
     long long sa = 0, sd = 0;
-    int na = 0, lmin = INT_MAX;
+    int na = 0, lmin = INT_MAX, need = 0;
     for (int t = 0; t < a.B && t < 256; ++t) {
       if (acc_n[t] >= 0) { sa += acc_n[t]; sd += g; }
       na += act_after[t];
       lmin = min(lmin, len_after[t]);
+      need = max(need, need_after[t]);
     }
     a.stats[0] += 1;
     a.stats[1] += sa;
@@ -216,6 +219,7 @@ __global__ void accept_kernel(const AcceptArgs a) {
     if (a.n_active) {
       a.n_active[0] = na;
       a.n_active[1] = na ? lmin : 0;
+      a.n_active[3] = need;
       if (a.guess) {
         int all = na > 0 ? 1 : 0;
         for (int t = 0; t < a.B && t < 256; ++t) all &= ahead_ok[t];
@@ -245,6 +249,7 @@ __global__ void gen_init_kernel(const GenInitArgs a) {
     a.n_active[0] = na;
     a.n_active[1] = na ? lmin : 0;
     a.n_active[2] = 0;
+    a.n_active[3] = na ? a.T - 1 : 0;  // tokens the longest-running sequence still needs
     a.stats[0] = a.stats[1] = a.stats[2] = 0;
   }
 }

@@ -1215,9 +1215,10 @@ int ssd_generate(ssd_ctx* c, int B, int P, const int32_t* d_prompt, const void* 
     a.guess = guess;
     a.next_need = 2 * gamma + 1;
   }
-  for (int round = 0; round < T; ++round) {
-    int32_t h_active[3] = {0, 0, 0};
-    HIP_TRY(hipMemcpyAsync(h_active, n_active, 12, hipMemcpyDeviceToHost, c->stream));
+  int round = 0;
+  while (round < T) {
+    int32_t h_active[4] = {0, 0, 0, 0};
+    HIP_TRY(hipMemcpyAsync(h_active, n_active, 16, hipMemcpyDeviceToHost, c->stream));
     HIP_TRY(hipStreamSynchronize(c->stream));
     if (h_active[0] == 0) break;
     if (ahead) {
@@ -1258,20 +1259,28 @@ int ssd_generate(ssd_ctx* c, int B, int P, const int32_t* d_prompt, const void* 
       a.draft = drafts[cur];
       HIP_TRY(launch_accept(a, c->stream));
       c->draft_valid = false;
+      ++round;
       continue;
     }
     const int g = mode == SSD_MODE_GREEDY ? 0
                   : (dynamic ? ssd_dynamic_gamma(h_active[1], gamma, c->d.max_seq) : gamma);
     if (g > c->d.max_gamma) return SSD_ERR_SHAPE;
     a.gamma = g;
-    if (g > 0) {
-      rc = ssd_draft(c, B, g, pending, draft, nullptr);
+    // a round emits at most g + 1 tokens per sequence, so with a fixed g the next
+    // ceil(need / (g + 1)) rounds are all needed (need: the most tokens an active sequence still
+    // lacks) and go out without a read-back in between; d(t) reads the lengths every round
+    int k = dynamic ? 1 : (h_active[3] + g) / (g + 1);
+    if (k < 1) k = 1;
+    for (int r = 0; r < k && round < T; ++r, ++round) {
+      if (g > 0) {
+        rc = ssd_draft(c, B, g, pending, draft, nullptr);
+        if (rc) return rc;
+      }
+      rc = ssd_verify(c, B, g, pending, draft, g > 0 ? reuse_hidden : 0, target, nullptr);
       if (rc) return rc;
+      HIP_TRY(launch_accept(a, c->stream));
+      c->draft_valid = false;
     }
-    rc = ssd_verify(c, B, g, pending, draft, g > 0 ? reuse_hidden : 0, target, nullptr);
-    if (rc) return rc;
-    HIP_TRY(launch_accept(a, c->stream));
-    c->draft_valid = false;
   }
   if (h_stats) {
     HIP_TRY(hipMemcpyAsync(h_stats, stats, 24, hipMemcpyDeviceToHost, c->stream));
