@@ -231,7 +231,10 @@ int ssd_accept_sample(ssd_ctx* ctx, int B, int gamma, const int32_t* d_draft,
  * prefix + prompt + T + 2 gamma <= max_seq (else SSD_ERR_CAPACITY) and no hidden-state export
  * (else SSD_ERR_STATE).
  * h_stats (host, may be NULL) receives {rounds, sum over sequences of accepted drafts, sum of
- * drafted tokens}.  Synchronises the stream once per round to test for completion. */
+ * drafted tokens}.  Synchronises the stream to test for completion: with a fixed gamma (and in
+ * greedy mode) once per batch of rounds, a batch being the ceil(L / (gamma + 1)) rounds that are
+ * certainly needed (L: the most tokens a sequence still active lacks); in the dynamic and
+ * drafting-ahead modes once per round. */
 int ssd_generate(ssd_ctx* ctx, int B, int P, const int32_t* d_prompt, const void* d_visual, int T,
                  int gamma, int mode, int reuse_hidden, int32_t* d_tokens, int64_t* h_stats);
 
