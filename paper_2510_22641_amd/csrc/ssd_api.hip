@@ -234,6 +234,7 @@ struct ssd_ctx {
   Layout L1;
   hipStream_t stream1 = nullptr;
   hipEvent_t ev_fork = nullptr, ev_join = nullptr;
+  int32_t* h_status = nullptr;  // pinned [4]: ssd_generate's read-back of the active counts
   bool prefilled = false;
   bool fold_ready = false;  // fold_q / fold_o hold the prefilled sequence's cross-attention
   // reuse bookkeeping: the last ssd_draft's arguments
@@ -1215,11 +1216,19 @@ int ssd_generate(ssd_ctx* c, int B, int P, const int32_t* d_prompt, const void* 
     a.guess = guess;
     a.next_need = 2 * gamma + 1;
   }
+  // the read-back lands in pinned memory (allocated on first use), a direct copy
+  if (!c->h_status &&
+      hipHostMalloc(reinterpret_cast<void**>(&c->h_status), 16, hipHostMallocDefault) != hipSuccess) {
+    c->h_status = nullptr;  // pageable stack memory then
+    (void)hipGetLastError();
+  }
   int round = 0;
   while (round < T) {
     int32_t h_active[4] = {0, 0, 0, 0};
-    HIP_TRY(hipMemcpyAsync(h_active, n_active, 16, hipMemcpyDeviceToHost, c->stream));
+    int32_t* dst = c->h_status ? c->h_status : h_active;
+    HIP_TRY(hipMemcpyAsync(dst, n_active, 16, hipMemcpyDeviceToHost, c->stream));
     HIP_TRY(hipStreamSynchronize(c->stream));
+    if (dst != h_active) std::memcpy(h_active, dst, 16);
     if (h_active[0] == 0) break;
     if (ahead) {
       // the previous round's drafts made ahead hold when it accepted everything and its extra
@@ -1380,6 +1389,7 @@ void ssd_destroy(ssd_ctx* c) {
   if (c->ev_fork) (void)hipEventDestroy(c->ev_fork);
   if (c->ev_join) (void)hipEventDestroy(c->ev_join);
   if (c->stream1) (void)hipStreamDestroy(c->stream1);
+  if (c->h_status) (void)hipHostFree(c->h_status);
   delete c;
 }
 
