@@ -188,3 +188,96 @@ def test_draft_logits_are_head_of_imitation_of_layer_k():
     assert np.array_equal(xk, xk_full)
     assert np.array_equal(lg, dec.head(dec.imitation(xk[None]))[0])
     assert np.array_equal(dec.draft_step(a, 7, 0, use_imitation=False)[0], dec.head(xk[None])[0])
+
+
+def _golden_bucket_of():
+    """distance -> bucket from the integer thresholds in tests/golden/t5_buckets.txt"""
+    import os
+    firsts = []
+    with open(os.path.join(os.path.dirname(__file__), "golden", "t5_buckets.txt")) as f:
+        for line in f:
+            if line.strip() and not line.startswith("#"):
+                b, n = map(int, line.split())
+                firsts.append((n, b))
+
+    def bucket(n):
+        return max(b for first, b in firsts if first <= n)
+    return bucket
+
+
+def test_t5_layer_by_explicit_loops():
+    # One whole T5 decoder layer over positions 0..4 (with 3 visual tokens), written out with
+    # scalar loops over heads, keys and visual tokens, independent of ops.attend and of the
+    # oracle's bucket function.  The relative-bias table holds a distinct N(0,1) value per
+    # (bucket, head) and the attention projections are scaled so that q.k is O(1): a dropped
+    # bias, a 1/sqrt(dh) scale on self- or cross-attention scores, or the cross keys taken from
+    # W_xv instead of W_xk each move the output far beyond the tolerance.
+    import math
+    shape = T5
+    w = _weights(shape, seed=12)
+    rng = np.random.default_rng(12)
+    w["rel_bias"] = rng.standard_normal((shape.rel_buckets, shape.n_heads))
+    for name in ("wq", "wk", "xq", "xk"):
+        w["layers"][0][name] = w["layers"][0][name] * 8.0
+    dec = Decoder(shape, w, 1)
+    z = synth.make_visual(shape, 12, 1)[0].astype(np.float64)
+    st = dec.new_state(8)
+    dec.set_visual(st, z)
+    toks = [3, 41, 17, 8, 29]
+    x = dec.embed(toks)
+    got = dec.layer(0, x.copy(), list(range(len(toks))), st)
+
+    lw = {n: np.asarray(a, dtype=np.float64) for n, a in w["layers"][0].items()}
+    H, dh, eps, nv = shape.n_heads, shape.d_head, shape.norm_eps, shape.n_visual
+    bucket = _golden_bucket_of()
+    table = np.asarray(w["rel_bias"], dtype=np.float64)
+
+    def rms(row, gain):
+        ms = sum(float(v) * float(v) for v in row) / len(row)
+        return np.array([gain[i] * row[i] / math.sqrt(ms + eps) for i in range(len(row))])
+
+    def softmax_list(s):
+        m = max(s)
+        e = [math.exp(v - m) for v in s]
+        t = sum(e)
+        return [v / t for v in e]
+
+    P = len(toks)
+    hs = [rms(x[p], lw["attn_norm"]) for p in range(P)]
+    qs = [lw["wq"] @ hs[p] for p in range(P)]
+    ks = [lw["wk"] @ hs[p] for p in range(P)]
+    vs = [lw["wv"] @ hs[p] for p in range(P)]
+    zk = [lw["xk"] @ z[j] for j in range(nv)]
+    zv = [lw["xv"] @ z[j] for j in range(nv)]
+    want = np.empty_like(x)
+    for p in range(P):
+        o = np.zeros(H * dh)
+        for h in range(H):
+            sl = slice(h * dh, (h + 1) * dh)
+            s = []
+            for j in range(p + 1):
+                dot = sum(qs[p][sl][e] * ks[j][sl][e] for e in range(dh))
+                s.append(dot + table[bucket(p - j), h])  # unscaled, plus the relative bias
+            pr = softmax_list(s)
+            for j in range(p + 1):
+                o[sl] += pr[j] * vs[j][sl]
+        y = x[p] + lw["wo"] @ o
+        hq = rms(y, lw["xattn_norm"])
+        xq = lw["xq"] @ hq
+        o = np.zeros(H * dh)
+        for h in range(H):
+            sl = slice(h * dh, (h + 1) * dh)
+            s = [sum(xq[sl][e] * zk[j][sl][e] for e in range(dh)) for j in range(nv)]
+            pr = softmax_list(s)  # no scale, no bias, no mask
+            for j in range(nv):
+                o[sl] += pr[j] * zv[j][sl]
+        y = y + lw["xo"] @ o
+        hf = rms(y, lw["ffn_norm"])
+        g = lw["w_gate"] @ hf
+        u = lw["w_up"] @ hf
+        c = math.sqrt(2.0 / math.pi)
+        a = np.array([0.5 * g[i] * (1.0 + math.tanh(c * (g[i] + 0.044715 * g[i] ** 3))) * u[i]
+                      for i in range(len(g))])
+        want[p] = y + lw["w_down"] @ a
+    # the scores matter: the bias and the q.k products both move the attention weights by O(1)
+    assert np.max(np.abs(want - got)) < 1e-12 * max(1.0, np.max(np.abs(want)))
