@@ -177,27 +177,25 @@ def sweep_c4(args):
     for k, mb in sorted({(p.draft_layers, p.batch) for p in pts}):
         group = [p for p in pts if p.draft_layers == k and p.batch == mb]
         gm = max(p.gamma for p in group)
-        # room for drafts made ahead (2 gamma positions past a round's start)
         dd = runtime.from_workload(group[0], args.seed, weights=weights, max_batch=mb,
-                                   max_gamma=gm, extra_seq=gm)
+                                   max_gamma=gm)
         for wl in group:
             sh, B, T, g = wl.shape, wl.batch, wl.new_tokens, wl.gamma
             prompts = synth.make_prompts(sh, args.seed, B, wl.prompt_len)
             visual = synth.make_visual(sh, args.seed, B)
             pt, vt = dd.upload_inputs(prompts, visual)
 
-            def timed(spec, ahead=False):
+            def timed(spec):
                 for _ in range(args.warmup):
-                    dd.generate(pt, vt, T, g, speculative=spec, reuse=True, ahead=ahead)
+                    dd.generate(pt, vt, T, g, speculative=spec, reuse=True)
                 torch.cuda.synchronize()
                 t0 = time.perf_counter()
                 for _ in range(args.steps):
-                    toks, st = dd.generate(pt, vt, T, g, speculative=spec, reuse=True, ahead=ahead)
+                    toks, st = dd.generate(pt, vt, T, g, speculative=spec, reuse=True)
                 torch.cuda.synchronize()
                 return time.perf_counter() - t0, st, toks
 
             dt, st, toks = timed(True)
-            dta, sta, toksa = timed(True, ahead=True)
             dtg, _, gtoks = timed(False)
             d_s, v_s, ctx = step_timings(dd, pt, vt, B, g)
             db = draft_step_bytes(sh, k, ctx, dd.k_pool.element_size(), cross_folded(sh, mb))
@@ -210,8 +208,6 @@ def sweep_c4(args):
                    "speedup_vs_greedy": round(dtg / dt, 3),
                    "acceptance_rate": round(st["accepted"] / max(1, st["drafted"]), 4),
                    "ssd_equals_greedy_tokens": bool(torch.equal(toks, gtoks)),
-                   "drafting_ahead_tokens_per_s": round(B * T * args.steps / dta, 2),
-                   "drafting_ahead_equals_one_stream": bool(torch.equal(toksa, toks)) and sta == st,
                    "draft_step": {"us": round(d_s * 1e6, 2), "bytes": int(db),
                                   "frac": round(db / d_s / 1e9 / HBM_PEAK_GBS, 4)},
                    "verify": {"us": round(v_s * 1e6, 2), "bytes": int(vb),
@@ -303,12 +299,6 @@ def main():
                          "layer before a second measurement (0: skip)")
     ap.add_argument("--sample-temps", default="1.0,0.1",
                     help="temperatures of the speculative-sampling measurement (empty: skip)")
-    ap.add_argument("--persistent", type=int, choices=[0, 1], default=None,
-                    help="force the persistent one-row pass on (1) or off (0); default: the "
-                         "library's choice")
-    ap.add_argument("--schedule", choices=["ahead", "one-stream"], default="one-stream",
-                    help="headline schedule of the decode loop: the next round drafted on a "
-                         "second stream during each verify pass, or one stream")
     ap.add_argument("--sweep", choices=["c4"], default=None,
                     help="run the FlanT5-xl sweep instead (one JSON line per point)")
     ap.add_argument("--copy-bytes", type=int, default=0,
@@ -347,41 +337,27 @@ def main():
     visual = synth.make_visual(sh, args.seed, wl.batch)
     # capacity for the dynamic draft length too (up to gamma + 9 drafts a round)
     dd = runtime.from_workload(wl, args.seed, weights=weights, max_gamma=wl.gamma + 9)
-    if args.persistent is not None:
-        dd.set_persistent(bool(args.persistent))
     pt, vt = dd.upload_inputs(prompts, visual)
     torch.cuda.synchronize()
     print(f"[bench] setup {time.time() - t_setup:.1f}s", file=sys.stderr, flush=True)
 
     B, T, g = wl.batch, wl.new_tokens, wl.gamma
 
-    def timed(speculative: bool, steps: int, warmup: int, dynamic: bool = False,
-              ahead: bool = False):
+    def timed(speculative: bool, steps: int, warmup: int, dynamic: bool = False):
         for _ in range(warmup):
-            dd.generate(pt, vt, T, g, speculative=speculative, reuse=True, dynamic=dynamic,
-                        ahead=ahead)
+            dd.generate(pt, vt, T, g, speculative=speculative, reuse=True, dynamic=dynamic)
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         stats = None
         for _ in range(steps):
             toks, stats = dd.generate(pt, vt, T, g, speculative=speculative, reuse=True,
-                                      dynamic=dynamic, ahead=ahead)
+                                      dynamic=dynamic)
         torch.cuda.synchronize()
         return time.perf_counter() - t0, stats, toks
 
-    # Algorithm 1 on one stream, and with the next round drafted on a second stream while each
-    # verify pass runs (same tokens and acceptance, checked below)
-    dt1, st1, toks_one = timed(True, args.steps, args.warmup)
-    one_tps = B * T * args.steps / dt1
-    print(f"[bench] ssd one stream {one_tps:.1f} tok/s", file=sys.stderr, flush=True)
-    dta, sta, toks_ahead = timed(True, args.steps, args.warmup, ahead=True)
-    ahead_tps = B * T * args.steps / dta
-    print(f"[bench] ssd drafting ahead {ahead_tps:.1f} tok/s", file=sys.stderr, flush=True)
-    ahead_same = bool(torch.equal(toks_ahead, toks_one)) and sta == st1
-    if args.schedule == "ahead":
-        dt, st, toks_ssd, ssd_tps = dta, sta, toks_ahead, ahead_tps
-    else:
-        dt, st, toks_ssd, ssd_tps = dt1, st1, toks_one, one_tps
+    # Algorithm 1 (the timed steps)
+    dt, st, toks_ssd = timed(True, args.steps, args.warmup)
+    ssd_tps = B * T * args.steps / dt
     alpha = st["accepted"] / max(1, st["drafted"])
     print(f"[bench] ssd {ssd_tps:.1f} tok/s alpha {alpha:.3f}", file=sys.stderr, flush=True)
     dtg, _, toks_greedy = timed(False, args.steps, 1)
@@ -520,11 +496,6 @@ def main():
                    "draft_layers": wl.draft_layers, "gamma": g, "new_tokens": T,
                    "deep_scale": wl.deep_scale, "parallelism": "none (1 GPU)"},
         "acceptance_rate": round(alpha, 4),
-        "schedule": ("next round drafted on a second stream during each verify pass"
-                     if args.schedule == "ahead" else "one stream"),
-        "one_stream_tokens_per_s": round(one_tps, 2),
-        "drafting_ahead_tokens_per_s": round(ahead_tps, 2),
-        "drafting_ahead_equals_one_stream": ahead_same,
         "rounds": st["rounds"],
         "greedy_tokens_per_s": round(greedy_tps, 2),
         "speedup_vs_greedy": round(ssd_tps / greedy_tps, 3),

@@ -56,13 +56,11 @@ enum { SSD_F32 = 0, SSD_BF16 = 1 };
 enum {
   SSD_MODE_GREEDY = 0,
   SSD_MODE_SPECULATIVE = 1,
-  SSD_MODE_SPECULATIVE_DYNAMIC = 2,
-  SSD_MODE_SPECULATIVE_AHEAD = 3
+  SSD_MODE_SPECULATIVE_DYNAMIC = 2
 };
 
-/* device status bits (ssd_sync_status, ssd_device_status); SSD_DEV_SYNC: a grid-barrier wait of
- * the persistent one-row pass exceeded its bound (ssd_set_persistent) */
-enum { SSD_DEV_BAD_TOKEN = 1, SSD_DEV_CAPACITY = 2, SSD_DEV_BAD_PAGE = 4, SSD_DEV_SYNC = 8 };
+/* device status bits (ssd_sync_status; ssd_generate returns SSD_ERR_DEVICE when one is set) */
+enum { SSD_DEV_BAD_TOKEN = 1, SSD_DEV_CAPACITY = 2, SSD_DEV_BAD_PAGE = 4 };
 
 /* Decoder and context dimensions, copied at ssd_create. */
 typedef struct {
@@ -220,21 +218,14 @@ int ssd_accept_sample(ssd_ctx* ctx, int B, int gamma, const int32_t* d_draft,
  * SSD_MODE_SPECULATIVE_DYNAMIC drafts ssd_dynamic_gamma(t, gamma, max_seq) tokens per round
  * (appendix on the choice of d: d grows with the context length t), t = the shortest context
  * length among the sequences still active at the start of the round; gamma + 9 <= max_gamma.
- * SSD_MODE_SPECULATIVE_AHEAD is Algorithm 1 with fixed gamma and the layer-k reuse (reuse_hidden
- * is implied), scheduled over two streams: while the verify pass of a round runs on the context's
- * stream, a second stream owned by the library (created on first use, default priority) drafts
- * the next round on the assumption that all gamma drafts pass and that the full model's extra
- * token equals the draft model's next token after the last draft (the imitation network and g on
- * the verify pass's layer-k row of the last position).  When every sequence still active meets
- * both, the next round skips its draft steps; otherwise it drafts as usual.  Tokens, acceptance
- * and h_stats are identical to SSD_MODE_SPECULATIVE with reuse; only the time differs.  Needs
- * prefix + prompt + T + 2 gamma <= max_seq (else SSD_ERR_CAPACITY) and no hidden-state export
- * (else SSD_ERR_STATE).
  * h_stats (host, may be NULL) receives {rounds, sum over sequences of accepted drafts, sum of
  * drafted tokens}.  Synchronises the stream to test for completion: with a fixed gamma (and in
  * greedy mode) once per batch of rounds, a batch being the ceil(L / (gamma + 1)) rounds that are
- * certainly needed (L: the most tokens a sequence still active lacks); in the dynamic and
- * drafting-ahead modes once per round. */
+ * certainly needed (L: the most tokens a sequence still active lacks); in the dynamic mode once
+ * per round.  Each of these read-backs also carries the device status word: when it is non-zero
+ * (a bad token id, a position past the cache, an unmapped page), no further round is launched and
+ * SSD_ERR_DEVICE is returned, as it is when the word is set after the last round; the word is
+ * left set for ssd_sync_status to report and clear. */
 int ssd_generate(ssd_ctx* ctx, int B, int P, const int32_t* d_prompt, const void* d_visual, int T,
                  int gamma, int mode, int reuse_hidden, int32_t* d_tokens, int64_t* h_stats);
 
@@ -247,18 +238,6 @@ int ssd_dynamic_gamma(int t, int d0, int n_max);
  * or launch kernels one by one (0). */
 int ssd_set_graphs(ssd_ctx* ctx, int enable);
 
-/* One-row passes of one-sequence calls (B = 1) — each draft step of ssd_draft, ssd_verify with
- * gamma = 0 (a greedy step) and the one-row part of a reusing ssd_verify — run as ONE persistent
- * kernel launch (one block per compute unit, phases separated by grid barriers) instead of a
- * chain of kernels (1), or as the chain (0, default: on MI355X the chain is faster).  The persistent pass exists when the
- * shapes allow it (every row the pass stages fits 12288 floats, d_model <= 6144, T5: the
- * cross-attention is folded, i.e. max_batch = 1 and 8/16/32/64 visual tokens) and the device
- * keeps one block per compute unit resident; T5 contexts use it after ssd_prefill.  Both paths
- * compute the same decoder (the same parity tolerances apply).  A barrier wait that exceeds its
- * bound (about a second) sets SSD_DEV_SYNC; the context must then be re-created.  Returns 1 when
- * the persistent pass will be used, 0 when not, SSD_ERR_ARG for a null context. */
-int ssd_set_persistent(ssd_ctx* ctx, int enable);
-
 /* Hidden-state export, for fitting the imitation network offline on the decoder's own states
  * (a stand-in for the paper's imitation training, Sec. "Deep Representation Imitation"; not on
  * the decode path).  While set (all three non-NULL), every ssd_draft also copies, for its
@@ -267,14 +246,10 @@ int ssd_set_persistent(ssd_ctx* ctx, int enable);
  * every ssd_verify copies its final residual rows (after the last layer, before g's norm) to
  * d_xl [B][gamma + 1][d_model], float32, device memory owned by the caller (sized for the
  * largest B and gamma used).  Row i of a draft and row i of the verify that follows it are the
- * same position.  All NULL disables; a mix of NULL and non-NULL is SSD_ERR_ARG.  The persistent
- * one-row pass is not used while the export is set. */
+ * same position.  All NULL disables; a mix of NULL and non-NULL is SSD_ERR_ARG. */
 int ssd_set_hidden_export(ssd_ctx* ctx, float* d_phi, float* d_xk, float* d_xl);
 
-/* Kernel timing for roofline reports.  With the persistent pass active (ssd_set_persistent), the
- * timed launches are the persistent draft steps and the bytes are the pass's weights, input rows
- * and output rows (KV-cache reads are not counted).  Otherwise, while enabled (and graphs are
- * bypassed), every launch of
+/* Kernel timing for roofline reports.  While enabled (and graphs are bypassed), every launch of
  * the one-row weight-streaming GEMV that streams the RMS-normalised d_model-wide matrices (QKV,
  * cross-attention query, gate/up, LM head; the kernel that carries most of a batch-1 draft step:
  * gemv1k_kernel<unsigned short, KP, 1> with KP = ceil(d_model / 2048) for bf16 weights and

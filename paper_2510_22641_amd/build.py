@@ -20,7 +20,7 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libssd.so")
-SOURCES = ["linear.hip", "attention.hip", "misc.hip", "step.hip", "sample.hip", "ssd_api.hip"]
+SOURCES = ["linear.hip", "attention.hip", "misc.hip", "sample.hip", "ssd_api.hip"]
 ARCH = "gfx950"
 
 

@@ -262,11 +262,9 @@ struct AcceptArgs {
   int32_t* active_rw;     // [B] cleared when count reaches T
   int T;
   int64_t* stats;         // [3]: rounds (added by thread 0), accepted, drafted
-  int32_t* n_active;      // [4]: sequences still active, shortest seq_len among them, (with
-                          // guess) 1 when every sequence still active accepted all gamma drafts
-                          // and its new pending token equals guess[b] else 0, and the most
-                          // tokens an active sequence still needs
-  const int32_t* guess;   // [B] or null: the token the drafts made ahead start from
+  int32_t* n_active;      // [4]: sequences still active, shortest seq_len among them, the
+                          // device status word, and the most tokens an active sequence still
+                          // needs
 };
 hipError_t launch_accept(const AcceptArgs& a, hipStream_t s);
 
@@ -303,6 +301,7 @@ struct GenInitArgs {
   int64_t* stats;
   int32_t* n_active;        // [4]: as AcceptArgs::n_active
   const int32_t* seq_len;
+  int32_t* status;
 };
 hipError_t launch_gen_init(const GenInitArgs& a, hipStream_t s);
 
@@ -310,110 +309,5 @@ hipError_t launch_gen_init(const GenInitArgs& a, hipStream_t s);
 hipError_t launch_bias_table(const float* rel_bias, const int32_t* bucket, int H, int max_seq,
                              float* table, hipStream_t s);
 
-
-// ---------------------------------------------------------------------------------------------
-// Persistent one-row pass (batch 1): a whole draft step, greedy step or the one-row part of a
-// reusing verify in one launch of one block per compute unit, its phases separated by grid
-// barriers (step.hip).
-
-constexpr int STEP_XS_MAX = 12288;   // floats of a staged input row (K <= this)
-constexpr int STEP_XRES_MAX = 6144;  // floats of the block's copy of the residual row (d_model)
-constexpr int STEP_MAX_BLOCKS = 256;
-constexpr int STEP_INLINE_SPLITS = 8;  // attention splits merged while staging the next input
-constexpr int STEP_MAX_SPLITS = 64;
-
-// Passes of 16 keys per attention split of the persistent pass (keys per split = 16 * passes):
-// a lane holds dh / 4 elements of each key and value row, in at most 8 + 8 16-byte loads.
-constexpr int step_attn_passes(int d_head, int kv_bytes) {
-  return (d_head * kv_bytes / 64) >= 8 ? 1 : 8 / (d_head * kv_bytes / 64);
-}
-
-enum StepPhaseType { SP_GEMV = 0, SP_ATTN = 1, SP_COMBINE = 2 };
-enum StepInput {
-  SI_VEC = 0,    // the input row x[0..K)
-  SI_EMBED = 1,  // the embedding row of the launch's token (StepArgs::tok)
-  SI_ATTN = 2    // attention key-split partials x = [H][S][dh + 4], merged while staged
-};
-
-struct StepPhase {
-  int type = SP_GEMV;
-  // input of a GEMV phase
-  int in_kind = SI_VEC;
-  const float* x = nullptr;
-  int K = 0;
-  int norm = NORM_NONE;   // NORM_NONE / NORM_RMS / NORM_LN / NORM_SOFTMAX
-  const float* gain = nullptr;
-  const float* shift = nullptr;
-  float eps = 0.f;
-  int group = 0;          // NORM_SOFTMAX: inputs per softmax group (8, 16, 32 or 64)
-  int in_resid = 0;       // the raw input is the residual row (kept in LDS for later epilogues)
-  // weights and epilogue
-  const void* w[3] = {nullptr, nullptr, nullptr};
-  int n_mats = 1;
-  int n_per = 0;
-  int wdtype = 1;
-  int epi = EPI_STORE;    // STORE, RESID (y = residual + acc), GATED_*, BIAS_GELU, BIAS_RESID,
-                          // ARGMAX, QKV
-  int n_tasks = 0;        // row pairs (GEMV), (head, split) pairs (ATTN) or heads (COMBINE)
-  float* y = nullptr;     // output row
-  const float* bias = nullptr;
-  int bias_resid = 0;     // EPI_BIAS_RESID: add the residual row
-  int to_stash = 0;       // EPI_RESID: also write the new residual to StepArgs::stash
-  int layer = 0;          // QKV / ATTN: KV-pool layer
-  // attention: q [H*dh] -> partials part [H][n_splits][dh + 4] (output, max, sum, 2 unused)
-  const float* q = nullptr;
-  float* part = nullptr;
-  int n_splits = 0;
-  int keys_per_split = 0;
-  // algorithmic bytes (weights + rows read and written), for timing reports
-  double bytes = 0.0;
-};
-
-struct StepArgs {
-  const StepPhase* phases = nullptr;
-  int n_phases = 0;
-  // synchronisation state (workspace): flags [STEP_MAX_BLOCKS + 4], abort word, arrival counter,
-  // per-block argmax partials
-  uint32_t* flags = nullptr;
-  uint32_t* abort_word = nullptr;
-  uint32_t* counter = nullptr;
-  float* part_val = nullptr;
-  int* part_idx = nullptr;
-  uint32_t spin_limit = 0;
-  // the token whose embedding starts the pass
-  const int32_t* tok = nullptr;
-  const void* embed = nullptr;
-  int vocab = 0;
-  int d_model = 0;
-  int wdtype = 1;
-  // positions and the paged cache
-  const int32_t* seq_len = nullptr;
-  int pos_off = 0;
-  void* k_pool = nullptr;   // pool base; layer l at + l * layer_elems elements
-  void* v_pool = nullptr;
-  size_t layer_elems = 0;
-  const int32_t* page_table = nullptr;
-  int max_pages = 0, page_size = 0, n_pages = 0;
-  int n_heads = 0, d_head = 0, max_seq = 0;
-  const float* rope_cos = nullptr;  // [max_seq][d_head/2] or null
-  const float* rope_sin = nullptr;
-  const float* bias_tab = nullptr;  // T5 [H][max_seq] or null
-  float attn_scale = 1.f;
-  // outputs
-  float* stash = nullptr;    // EPI_RESID with to_stash
-  int32_t* dst0 = nullptr;   // argmax token (ARGMAX phase)
-  int32_t* dst1 = nullptr;
-  float* logits = nullptr;   // [vocab] or null
-  int32_t* status = nullptr;
-};
-
-// Blocks of a persistent launch on this device (one per compute unit, at most STEP_MAX_BLOCKS),
-// or 0 when the device cannot keep that many blocks resident at once.
-int step_blocks();
-
-// Launch the persistent pass (KV pools in kvdtype); with start / stop events, they are bound
-// to the launch's own dispatch.
-hipError_t launch_step(const StepArgs& a, int kvdtype, hipStream_t s, hipEvent_t start = nullptr,
-                       hipEvent_t stop = nullptr);
 
 }  // namespace ssd

@@ -152,14 +152,12 @@ __global__ void accept_kernel(const AcceptArgs a) {
   __shared__ int acc_n[256];
   __shared__ int act_after[256];
   __shared__ int len_after[256];
-  __shared__ int ahead_ok[256];
   __shared__ int need_after[256];
   const int b = threadIdx.x;
   const int g = a.gamma;
   int n = 0;
   int still = 0;
   bool did = false;
-  int ok = 1;
   if (b < a.B) {
     bool act = a.active ? (a.active[b] != 0) : true;
     if (a.active_rw) act = act && (a.active_rw[b] != 0);
@@ -193,7 +191,6 @@ __global__ void accept_kernel(const AcceptArgs a) {
       const int sl = a.seq_len[b] + adv;
       a.seq_len[b] = sl;
       if (sl + (still ? a.next_need : 0) > a.max_seq) atomicOr(a.status, SSD_DEV_CAPACITY);
-      if (still && a.guess) ok = (n == g && tg[n] == a.guess[b]) ? 1 : 0;
     } else if (a.active_rw) {
       still = 0;
     }
@@ -202,7 +199,6 @@ __global__ void accept_kernel(const AcceptArgs a) {
   act_after[b] = still;
   len_after[b] = (b < a.B && still) ? a.seq_len[b] : INT_MAX;
   need_after[b] = (b < a.B && still && a.tokens) ? a.T - a.count[b] : 0;
-  ahead_ok[b] = ok;
   __syncthreads();
   if (b == 0 && a.stats) {
     long long sa = 0, sd = 0;
@@ -220,11 +216,9 @@ __global__ void accept_kernel(const AcceptArgs a) {
       a.n_active[0] = na;
       a.n_active[1] = na ? lmin : 0;
       a.n_active[3] = need;
-      if (a.guess) {
-        int all = na > 0 ? 1 : 0;
-        for (int t = 0; t < a.B && t < 256; ++t) all &= ahead_ok[t];
-        a.n_active[2] = all;
-      }
+      // the device status word (an atomic read: the bits come from atomics of this and
+      // earlier launches)
+      a.n_active[2] = a.status ? atomicOr(a.status, 0) : 0;
     }
   }
 }
@@ -248,7 +242,7 @@ __global__ void gen_init_kernel(const GenInitArgs a) {
     }
     a.n_active[0] = na;
     a.n_active[1] = na ? lmin : 0;
-    a.n_active[2] = 0;
+    a.n_active[2] = a.status ? atomicOr(a.status, 0) : 0;
     a.n_active[3] = na ? a.T - 1 : 0;  // tokens the longest-running sequence still needs
     a.stats[0] = a.stats[1] = a.stats[2] = 0;
   }

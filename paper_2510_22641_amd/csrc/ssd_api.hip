@@ -19,6 +19,8 @@ namespace {
 
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
+constexpr int MAX_LAYERS = 256;  // decoder layers a context holds descriptors for
+
 // T5 decoder relative-position bucket of a query-minus-key distance n >= 0: distances below
 // half the buckets are exact, larger ones are binned logarithmically up to max_dist.
 int t5_bucket(int n, int buckets, int max_dist) {
@@ -33,10 +35,10 @@ struct Layout {
   size_t x, x1, qkv, q, attn, ffn, inh, xi, stash, vis, part_val, part_idx, stats, bias_tab,
       p_x, p_attn, p_ffn, ssq, attn_part, fold_q, fold_o,
       bucket, rope_cos, rope_sin, status, cur_tok, g_pending, g_draft, g_target,
-      g_count, g_active, g_nactive, g_stats, g_draft2, g_guess, step_prog, step_arena, step_sync,
-      gplanes, total;
+      g_count, g_active, g_nactive, g_stats, gplanes, total;
   int rows_max, head_rows, parts_max, ctx_max, plane_rows, attn_rows;
   int gplane_rows = 0, gplane_ld = 0;  // tile-path input planes (0 rows: none)
+  bool fold = false;  // the folded cross-attention matrices are carved (fold_q, fold_o)
 };
 
 int ctx_len_max(const ssd_dims& d) {
@@ -52,53 +54,10 @@ bool fold_cross(const ssd_dims& d) {
          d.n_visual <= d.d_head && (size_t)d.n_heads * d.n_visual <= 6144 && d.d_model <= 6144;
 }
 
-// Persistent one-row passes (step.hip): one phase list per kind of pass.
-enum { STEP_DRAFT = 0, STEP_GREEDY = 1, STEP_VROW = 2, STEP_KINDS = 3 };
-
-// synchronisation area of the persistent passes (bytes from L.step_sync)
-constexpr size_t SYNC_FLAGS = 0, SYNC_ABORT = 1040, SYNC_COUNTER = 1044, SYNC_PART_VAL = 1280,
-                 SYNC_PART_IDX = 2304, SYNC_BYTES = 3328;
-
-int step_keys_per_split(const ssd_dims& d) {
-  return 16 * step_attn_passes(d.d_head, d.kvdtype == SSD_BF16 ? 2 : 4);
-}
-
-int step_splits(const ssd_dims& d) {
-  const int ks = step_keys_per_split(d);
-  return (d.max_seq + ks - 1) / ks;
-}
-
-int step_max_phases(const ssd_dims& d) { return d.n_layers * 8 + 4; }
-
-// Shapes the persistent pass handles: every staged row fits its LDS buffers, the residual row
-// its LDS copy, and (T5) the cross-attention is folded with a softmax group the stager supports.
-bool step_dims_ok(const ssd_dims& d) {
-  const int HD = d.n_heads * d.d_head;
-  auto kok = [](int K) { return K >= 8 && K <= STEP_XS_MAX && K % 8 == 0; };
-  if (d.d_model > STEP_XRES_MAX) return false;
-  if (!kok(d.d_model) || !kok(HD) || !kok(d.d_ff) || !kok(d.in_hidden)) return false;
-  if (d.arch == SSD_ARCH_T5) {
-    if (!fold_cross(d) || !kok(d.n_heads * d.n_visual)) return false;
-    if (d.n_visual != 8 && d.n_visual != 16 && d.n_visual != 32 && d.n_visual != 64) return false;
-  }
-  return step_splits(d) <= STEP_MAX_SPLITS;
-}
-
-// Upper bound of the floats one pass writes to its arena (every phase output at a fresh address).
-size_t step_arena_floats(const ssd_dims& d) {
-  const size_t HD = (size_t)d.n_heads * d.d_head, D = d.d_model, S = step_splits(d);
-  auto a = [](size_t n) { return align_up(n, 64); };
-  size_t per = a(HD) + a((size_t)d.n_heads * S * (d.d_head + 4)) + a(HD) + a(D) + a(d.d_ff) + a(D);
-  if (d.arch == SSD_ARCH_T5) per += a((size_t)d.n_heads * d.n_visual) + a(D);
-  return per * d.n_layers + a(d.in_hidden) + a(D) + 256;
-}
-
-// Workspace layout.  The scratch a chain of launches writes (residual rows, projections, operand
-// planes, argmax partials, the layer-k stash ...) comes in two lanes: lane 0 for every call on the
-// context's stream, lane 1 (sized for one-row steps of the batch) for the drafts made ahead on the
-// second stream while a verify pass runs (SSD_MODE_SPECULATIVE_AHEAD).  L1 is L with the lane
-// fields moved to lane 1; tables, folded cross-attention and the loop state are shared.
-bool make_layout(const ssd_dims& d, Layout& L, Layout& L1) {
+// Workspace layout: the scratch a chain of launches writes (residual rows, projections, operand
+// planes, argmax partials, the layer-k stash ...), the tables, the folded cross-attention and
+// the loop state of ssd_generate, each slice 256-byte aligned.
+bool make_layout(const ssd_dims& d, Layout& L, bool allow_fold = true) {
   const size_t B = d.max_batch, G = d.max_gamma, D = d.d_model, HD = (size_t)d.n_heads * d.d_head;
   L.ctx_max = ctx_len_max(d);
   size_t rows = B * (G + 1);
@@ -154,7 +113,8 @@ bool make_layout(const ssd_dims& d, Layout& L, Layout& L1) {
   }
   L.vis = take(d.arch == SSD_ARCH_T5 ? B * (size_t)d.n_visual * D * 4 : 0);
   {
-    const size_t fold = fold_cross(d) ? (size_t)d.n_layers * d.n_heads * d.n_visual * D * 4 : 0;
+    L.fold = allow_fold && fold_cross(d);
+    const size_t fold = L.fold ? (size_t)d.n_layers * d.n_heads * d.n_visual * D * 4 : 0;
     L.fold_q = take(fold);
     L.fold_o = take(fold);
   }
@@ -165,30 +125,20 @@ bool make_layout(const ssd_dims& d, Layout& L, Layout& L1) {
   L.status = take(4);
   L.g_pending = take(B * 4);
   L.g_draft = take(B * (G > 0 ? G : 1) * 4);
-  L.g_draft2 = take(B * (G > 0 ? G : 1) * 4);
-  L.g_guess = take(B * 4);
   L.g_target = take(B * (G + 1) * 4);
   L.g_count = take(B * 4);
   L.g_active = take(B * 4);
   L.g_nactive = take(16);
   L.g_stats = take(3 * 8);
-  {
-    const bool st = step_dims_ok(d);
-    L.step_prog = take(st ? (size_t)STEP_KINDS * step_max_phases(d) * sizeof(StepPhase) : 0);
-    L.step_arena = take(st ? step_arena_floats(d) * 4 : 0);
-    L.step_sync = take(st ? SYNC_BYTES : 0);
-  }
-  L1 = L;
-  lane(L1, B, B);
-  L1.gplane_rows = 0;  // the second stream runs one-row steps only
-  L.total = L1.total = off;
+  L.total = off;
   return true;
 }
 
 bool dims_ok(const ssd_dims* d) {
   if (!d) return false;
   if (d->arch != SSD_ARCH_T5 && d->arch != SSD_ARCH_LLAMA) return false;
-  if (d->n_layers < 1 || d->d_model < 64 || d->d_model % 64) return false;
+  if (d->n_layers < 1 || d->n_layers > MAX_LAYERS || d->d_model < 64 || d->d_model % 64)
+    return false;
   if (d->n_heads < 1 || (d->d_head != 64 && d->d_head != 128)) return false;
   if (d->d_ff < 64 || d->d_ff % 64 || d->vocab < 2) return false;
   if (d->in_hidden < 64 || d->in_hidden % 64) return false;
@@ -224,16 +174,11 @@ struct GraphKey {
 struct ssd_ctx {
   ssd_dims d;
   ssd_weights w;
-  std::vector<ssd_layer_weights> layers;
+  ssd_layer_weights layers[MAX_LAYERS];
   ssd_kv kv;
   hipStream_t stream;
   char* ws;
   Layout L;
-  // drafts made ahead while a verify pass runs: lane-1 scratch, a second stream (created on first
-  // use, default priority) and the fork / join events between the two streams
-  Layout L1;
-  hipStream_t stream1 = nullptr;
-  hipEvent_t ev_fork = nullptr, ev_join = nullptr;
   int32_t* h_status = nullptr;  // pinned [4]: ssd_generate's read-back of the active counts
   bool prefilled = false;
   bool fold_ready = false;  // fold_q / fold_o hold the prefilled sequence's cross-attention
@@ -249,12 +194,6 @@ struct ssd_ctx {
   float* ex_phi = nullptr;
   float* ex_xk = nullptr;
   float* ex_xl = nullptr;
-  // persistent one-row passes: built at creation when the shape and the device allow them;
-  // off unless asked for (slower than the chain of kernels on MI355X, see step.hip)
-  bool step_ok = false;
-  bool use_step = false;
-  int step_n[STEP_KINDS] = {0, 0, 0};
-  double step_bytes[STEP_KINDS] = {0.0, 0.0, 0.0};
   // kernel timing (ssd_profile_enable)
   bool profiling = false;
   std::vector<hipEvent_t> ev_pool;
@@ -279,21 +218,6 @@ struct ssd_ctx {
   } while (0)
 
 namespace {
-
-// The launches of its scope go to lane 1: the second stream and the lane-1 scratch.
-struct OnLane1 {
-  ssd_ctx* c;
-  Layout L;
-  hipStream_t s;
-  explicit OnLane1(ssd_ctx* ctx) : c(ctx), L(ctx->L), s(ctx->stream) {
-    c->L = c->L1;
-    c->stream = c->stream1;
-  }
-  ~OnLane1() {
-    c->L = L;
-    c->stream = s;
-  }
-};
 
 PagedKV paged(ssd_ctx* c, int l, int pos_off) {
   PagedKV p;
@@ -340,198 +264,6 @@ LinearArgs lin(ssd_ctx* c) {
   }
   a.eps = c->d.norm_eps;
   return a;
-}
-
-// Phase list of a persistent one-row pass (batch 1):
-//   STEP_DRAFT   embed(token) -> layers 1..k (the residual after layer k also to the stash) ->
-//                imitation network -> g -> argmax;
-//   STEP_GREEDY  embed(token) -> layers 1..L -> g -> argmax;
-//   STEP_VROW    embed(token) -> layers 1..k, the residual after layer k to x1.
-// Per layer: QKV (+ rotary, KV store) | attention split over keys | [merge] | W_o + residual |
-// (T5) folded cross-attention scores | folded cross-attention output + residual | gate/up |
-// down + residual.  Every phase output goes to a fresh address of the arena.
-std::vector<StepPhase> step_program(ssd_ctx* c, int kind, double* bytes, bool* fits) {
-  const ssd_dims& d = c->d;
-  const bool t5 = d.arch == SSD_ARCH_T5;
-  const int D = d.d_model, H = d.n_heads, dh = d.d_head, HD = H * dh;
-  const int S = step_splits(d);
-  float* arena = c->at<float>(c->L.step_arena);
-  size_t off = 0;
-  auto out = [&](size_t n) {
-    float* p = arena + off;
-    off += align_up(n, 64);
-    return p;
-  };
-  std::vector<StepPhase> P;
-  double total = 0.0;
-  auto push = [&](StepPhase ph) {
-    if (ph.type == SP_GEMV) {
-      const bool gated = ph.epi == EPI_GATED_GELU || ph.epi == EPI_GATED_SILU;
-      const double rows = gated ? 2.0 * ph.n_per : (double)ph.n_per * ph.n_mats;
-      const double outs = ph.epi == EPI_ARGMAX ? 0.0 : (gated ? (double)ph.n_per : rows);
-      ph.bytes = rows * ph.K * (ph.wdtype == SSD_F32 ? 4.0 : 2.0) + 4.0 * ph.K + 4.0 * outs +
-                 (ph.epi == EPI_RESID ? 4.0 * outs : 0.0);
-    }
-    total += ph.bytes;
-    P.push_back(ph);
-  };
-  auto pairs = [](int n) { return (n + 1) / 2; };
-  const int nl = kind == STEP_GREEDY ? d.n_layers : d.draft_layers;
-  const float* xcur = nullptr;  // the residual row; null: the token's embedding
-  for (int l = 0; l < nl; ++l) {
-    const ssd_layer_weights& lw = c->layers[l];
-    StepPhase q;
-    if (xcur) { q.in_kind = SI_VEC; q.x = xcur; } else { q.in_kind = SI_EMBED; }
-    q.K = D; q.norm = NORM_RMS; q.gain = lw.attn_norm; q.eps = d.norm_eps; q.in_resid = 1;
-    q.w[0] = lw.wq; q.w[1] = lw.wk; q.w[2] = lw.wv; q.n_mats = 3; q.n_per = HD;
-    q.wdtype = d.wdtype; q.epi = EPI_QKV; q.n_tasks = 3 * HD / 2; q.y = out(HD); q.layer = l;
-    push(q);
-    StepPhase at;
-    at.type = SP_ATTN; at.q = q.y; at.part = out((size_t)H * S * (dh + 4)); at.n_splits = S;
-    at.keys_per_split = step_keys_per_split(d); at.layer = l; at.n_tasks = H * S;
-    push(at);
-    StepPhase o;
-    if (S <= STEP_INLINE_SPLITS) {
-      o.in_kind = SI_ATTN; o.x = at.part; o.n_splits = S;
-    } else {
-      StepPhase cb;
-      cb.type = SP_COMBINE; cb.part = at.part; cb.n_splits = S; cb.n_tasks = H; cb.y = out(HD);
-      push(cb);
-      o.in_kind = SI_VEC; o.x = cb.y;
-    }
-    o.K = HD; o.norm = NORM_NONE; o.w[0] = lw.wo; o.n_per = D; o.wdtype = d.wdtype;
-    o.epi = EPI_RESID; o.n_tasks = pairs(D); o.y = out(D);
-    push(o);
-    xcur = o.y;
-    if (t5) {
-      const int HN = H * d.n_visual;
-      StepPhase fq;
-      fq.in_kind = SI_VEC; fq.x = xcur; fq.K = D; fq.norm = NORM_RMS; fq.gain = lw.xattn_norm;
-      fq.eps = d.norm_eps; fq.in_resid = 1;
-      fq.w[0] = c->at<float>(c->L.fold_q) + (size_t)l * c->fold_layer_elems(); fq.n_per = HN;
-      fq.wdtype = SSD_F32; fq.epi = EPI_STORE; fq.n_tasks = pairs(HN); fq.y = out(HN);
-      push(fq);
-      StepPhase fo;
-      fo.in_kind = SI_VEC; fo.x = fq.y; fo.K = HN; fo.norm = NORM_SOFTMAX; fo.group = d.n_visual;
-      fo.w[0] = c->at<float>(c->L.fold_o) + (size_t)l * c->fold_layer_elems(); fo.n_per = D;
-      fo.wdtype = SSD_F32; fo.epi = EPI_RESID; fo.n_tasks = pairs(D); fo.y = out(D);
-      push(fo);
-      xcur = fo.y;
-    }
-    StepPhase gu;
-    gu.in_kind = SI_VEC; gu.x = xcur; gu.K = D; gu.norm = NORM_RMS; gu.gain = lw.ffn_norm;
-    gu.eps = d.norm_eps; gu.in_resid = 1;
-    gu.w[0] = lw.w_gate; gu.w[1] = lw.w_up; gu.n_mats = 2; gu.n_per = d.d_ff; gu.wdtype = d.wdtype;
-    gu.epi = t5 ? EPI_GATED_GELU : EPI_GATED_SILU; gu.n_tasks = d.d_ff; gu.y = out(d.d_ff);
-    push(gu);
-    StepPhase dn;
-    dn.in_kind = SI_VEC; dn.x = gu.y; dn.K = d.d_ff; dn.norm = NORM_NONE;
-    dn.w[0] = lw.w_down; dn.n_per = D; dn.wdtype = d.wdtype; dn.epi = EPI_RESID;
-    dn.n_tasks = pairs(D);
-    dn.y = (kind == STEP_VROW && l == nl - 1) ? c->at<float>(c->L.x1) : out(D);
-    dn.to_stash = (kind == STEP_DRAFT && l == nl - 1) ? 1 : 0;
-    push(dn);
-    xcur = dn.y;
-  }
-  if (kind == STEP_DRAFT) {
-    // imitation network: LN -> FC1 + b1 -> GELU -> FC2 + b2 (+ the residual)
-    StepPhase i1;
-    i1.in_kind = SI_VEC; i1.x = xcur; i1.K = D; i1.norm = NORM_LN; i1.gain = c->w.in_ln_w;
-    i1.shift = c->w.in_ln_b; i1.eps = d.ln_eps; i1.in_resid = 1;
-    i1.w[0] = c->w.in_w1; i1.n_per = d.in_hidden; i1.wdtype = d.wdtype; i1.epi = EPI_BIAS_GELU;
-    i1.bias = c->w.in_b1; i1.n_tasks = pairs(d.in_hidden); i1.y = out(d.in_hidden);
-    push(i1);
-    StepPhase i2;
-    i2.in_kind = SI_VEC; i2.x = i1.y; i2.K = d.in_hidden; i2.norm = NORM_NONE;
-    i2.w[0] = c->w.in_w2; i2.n_per = D; i2.wdtype = d.wdtype; i2.epi = EPI_BIAS_RESID;
-    i2.bias = c->w.in_b2; i2.bias_resid = d.in_residual ? 1 : 0; i2.n_tasks = pairs(D);
-    i2.y = out(D);
-    push(i2);
-    xcur = i2.y;
-  }
-  if (kind != STEP_VROW) {
-    StepPhase hd;
-    hd.in_kind = SI_VEC; hd.x = xcur; hd.K = D; hd.norm = NORM_RMS; hd.gain = c->w.final_norm;
-    hd.eps = d.norm_eps; hd.w[0] = c->w.lm_head; hd.n_per = d.vocab; hd.wdtype = d.wdtype;
-    hd.epi = EPI_ARGMAX; hd.n_tasks = pairs(d.vocab);
-    push(hd);
-  }
-  *bytes = total;
-  *fits = off <= step_arena_floats(d) && (int)P.size() <= step_max_phases(d);
-  return P;
-}
-
-// Build the phase lists into the workspace and clear the synchronisation area.
-int build_step_programs(ssd_ctx* c) {
-  c->step_ok = false;
-  if (!step_dims_ok(c->d) || step_blocks() <= 0) return SSD_OK;
-  StepPhase* prog = c->at<StepPhase>(c->L.step_prog);
-  for (int kind = 0; kind < STEP_KINDS; ++kind) {
-    bool fits = false;
-    double bytes = 0.0;
-    std::vector<StepPhase> P = step_program(c, kind, &bytes, &fits);
-    if (!fits) return SSD_OK;
-    HIP_TRY(hipMemcpyAsync(prog + (size_t)kind * step_max_phases(c->d), P.data(),
-                           P.size() * sizeof(StepPhase), hipMemcpyHostToDevice, c->stream));
-    c->step_n[kind] = (int)P.size();
-    c->step_bytes[kind] = bytes;
-  }
-  HIP_TRY(hipMemsetAsync(c->ws + c->L.step_sync, 0, SYNC_BYTES, c->stream));
-  HIP_TRY(hipStreamSynchronize(c->stream));
-  c->step_ok = true;
-  return SSD_OK;
-}
-
-// One-row passes of a one-sequence call take the persistent kernel (T5 once the cross-attention
-// is folded, i.e. after prefill).
-bool use_step_now(const ssd_ctx* c, int B) {
-  return c->step_ok && c->use_step && B == 1 && !c->ex_phi &&
-         (c->d.arch == SSD_ARCH_LLAMA || c->fold_ready);
-}
-
-StepArgs step_args(ssd_ctx* c, int kind) {
-  const ssd_dims& d = c->d;
-  StepArgs a;
-  a.phases = c->at<StepPhase>(c->L.step_prog) + (size_t)kind * step_max_phases(d);
-  a.n_phases = c->step_n[kind];
-  char* sync = c->ws + c->L.step_sync;
-  a.flags = reinterpret_cast<uint32_t*>(sync + SYNC_FLAGS);
-  a.abort_word = reinterpret_cast<uint32_t*>(sync + SYNC_ABORT);
-  a.counter = reinterpret_cast<uint32_t*>(sync + SYNC_COUNTER);
-  a.part_val = reinterpret_cast<float*>(sync + SYNC_PART_VAL);
-  a.part_idx = reinterpret_cast<int*>(sync + SYNC_PART_IDX);
-  a.spin_limit = 1u << 21;
-  a.embed = c->w.embed; a.vocab = d.vocab; a.d_model = d.d_model; a.wdtype = d.wdtype;
-  a.seq_len = c->kv.seq_len;
-  a.k_pool = c->kv.k_pool; a.v_pool = c->kv.v_pool; a.layer_elems = c->kv_layer_elems();
-  a.page_table = c->kv.page_table; a.max_pages = d.max_pages; a.page_size = d.page_size;
-  a.n_pages = c->kv.n_pages; a.n_heads = d.n_heads; a.d_head = d.d_head; a.max_seq = d.max_seq;
-  const bool t5 = d.arch == SSD_ARCH_T5;
-  a.rope_cos = t5 ? nullptr : c->at<float>(c->L.rope_cos);
-  a.rope_sin = t5 ? nullptr : c->at<float>(c->L.rope_sin);
-  a.bias_tab = t5 ? c->at<float>(c->L.bias_tab) : nullptr;
-  a.attn_scale = t5 ? 1.0f : (float)(1.0 / std::sqrt((double)d.d_head));
-  a.status = c->at<int32_t>(c->L.status);
-  return a;
-}
-
-// Launch a persistent pass; when profiling, draft-step launches carry events bound to their own
-// dispatch and add the pass's algorithmic bytes (weights and rows; the KV reads are not counted).
-int run_step(ssd_ctx* c, int kind, const StepArgs& a) {
-  if (!c->profiling || kind != STEP_DRAFT) {
-    HIP_TRY(launch_step(a, c->d.kvdtype, c->stream));
-    return SSD_OK;
-  }
-  while (c->ev_pool.size() < c->ev_used + 2) {
-    hipEvent_t e;
-    HIP_TRY(hipEventCreate(&e));
-    c->ev_pool.push_back(e);
-  }
-  HIP_TRY(launch_step(a, c->d.kvdtype, c->stream, c->ev_pool[c->ev_used], c->ev_pool[c->ev_used + 1]));
-  c->ev_used += 2;
-  c->prof_bytes += c->step_bytes[kind];
-  c->prof_launches += 1;
-  return SSD_OK;
 }
 
 // Layers l0..l1-1 over rows r = b*C + j at positions seq_len[b] + pos_off + j.  When stash is set
@@ -734,34 +466,18 @@ int run_imitation(ssd_ctx* c, const float* xk, int B, F between) {
   return SSD_OK;
 }
 
-// gamma draft steps from `pending`; step i runs at positions seq_len + pos_base + i and leaves
-// its layer-k rows in stash_out (the lane's stash when null).  allow_step = false keeps the
-// chain of kernels (the persistent pass needs the whole device).
+// gamma draft steps from `pending`; step i runs at positions seq_len + i and leaves its layer-k
+// rows in the stash.
 int draft_launches(ssd_ctx* c, int B, int gamma, const int32_t* pending, int32_t* draft,
-                   float* logits, const float* u = nullptr, float tau = 0.f, int pos_base = 0,
-                   float* stash_out = nullptr, bool allow_step = true) {
+                   float* logits, const float* u = nullptr, float tau = 0.f) {
   const ssd_dims& d = c->d;
   const int D = d.d_model;
   float* x = c->at<float>(c->L.x);
   float* inh = c->at<float>(c->L.inh);
   float* xi = c->at<float>(c->L.xi);
-  float* stash = stash_out ? stash_out : c->at<float>(c->L.stash);
+  float* stash = c->at<float>(c->L.stash);
   int32_t* cur = c->at<int32_t>(c->L.cur_tok);
   const int ld_stash = (d.max_gamma + 1) * D;
-  if (allow_step && use_step_now(c, B) && !u) {
-    for (int i = 0; i < gamma; ++i) {
-      StepArgs a = step_args(c, STEP_DRAFT);
-      a.tok = i == 0 ? pending : cur;
-      a.pos_off = pos_base + i;
-      a.stash = stash + (size_t)i * D;
-      a.dst0 = draft + i;
-      a.dst1 = cur;
-      a.logits = logits ? logits + (size_t)i * d.vocab : nullptr;
-      const int rc = run_step(c, STEP_DRAFT, a);
-      if (rc) return rc;
-    }
-    return SSD_OK;
-  }
   // greedy drafts: the final argmax of step i also writes step i + 1's embedding rows into x
   const bool fuse_embed = !u;
   for (int i = 0; i < gamma; ++i) {
@@ -773,7 +489,7 @@ int draft_launches(ssd_ctx* c, int B, int gamma, const int32_t* pending, int32_t
       e.status = c->at<int32_t>(c->L.status);
       HIP_TRY(launch_embed(e, c->stream));
     }
-    int rc = run_layers(c, x, B, 1, pos_base + i, 0, d.draft_layers, d.draft_layers - 1,
+    int rc = run_layers(c, x, B, 1, i, 0, d.draft_layers, d.draft_layers - 1,
                         stash + (size_t)i * D, ld_stash);
     if (rc) return rc;
     rc = run_imitation(c, x, B, [&]() -> hipError_t {
@@ -794,32 +510,11 @@ int draft_launches(ssd_ctx* c, int B, int gamma, const int32_t* pending, int32_t
   return SSD_OK;
 }
 
-// The next round's drafts, made while the verify pass of this round runs (lane 1).  They assume
-// that every draft of this round passes and that the full model's extra token equals the draft
-// model's own next token: the imitation network and g on xk_last (the layer-k rows of this
-// round's last position, from the verify pass) give that token (`guess`); gamma draft steps from
-// it, at positions seq_len + gamma + 1 + i, fill `draft` and `stash`.
-int ahead_launches(ssd_ctx* c, int B, int gamma, const float* xk_last, int32_t* guess,
-                   int32_t* draft, float* stash) {
-  const int D = c->d.d_model;
-  int rc = run_imitation(c, xk_last, B, []() { return hipSuccess; });
-  if (rc) return rc;
-  rc = run_head(c, c->at<float>(c->L.xi), D, B, 1, nullptr, 0, guess, 1, 0, nullptr);
-  if (rc) return rc;
-  return draft_launches(c, B, gamma, guess, draft, nullptr, nullptr, 0.f, gamma + 1, stash, false);
-}
-
 // Verify with the layer-k reuse, first part: layers 1..k for the last position only (into x1);
 // the other positions' layer-k rows are the draft's.
 int verify_last_row(ssd_ctx* c, int B, int gamma, const int32_t* draft) {
   const ssd_dims& d = c->d;
   float* x1 = c->at<float>(c->L.x1);
-  if (use_step_now(c, B)) {
-    StepArgs a = step_args(c, STEP_VROW);
-    a.tok = draft + (gamma - 1);
-    a.pos_off = gamma;
-    return run_step(c, STEP_VROW, a);
-  }
   EmbedArgs e;
   e.x = x1; e.B = B; e.C = 1; e.d = d.d_model; e.embed = c->w.embed; e.vocab = d.vocab;
   e.wdtype = d.wdtype; e.t0 = nullptr; e.t1 = draft + (gamma - 1); e.ld1 = gamma;
@@ -851,16 +546,6 @@ int verify_launches(ssd_ctx* c, int B, int gamma, const int32_t* pending, const 
   const ssd_dims& d = c->d;
   const int D = d.d_model, C = gamma + 1;
   float* x = c->at<float>(c->L.x);
-  if (gamma == 0 && use_step_now(c, B)) {
-    // one greedy step: the whole decoder, g and the argmax in one persistent pass
-    StepArgs a = step_args(c, STEP_GREEDY);
-    a.tok = pending;
-    a.pos_off = 0;
-    a.dst0 = target;
-    a.dst1 = nullptr;
-    a.logits = logits;
-    return run_step(c, STEP_GREEDY, a);
-  }
   if (reuse) {
     const int rc = verify_last_row(c, B, gamma, draft);
     if (rc) return rc;
@@ -908,20 +593,9 @@ int launch_maybe_graph(ssd_ctx* c, const GraphKey& key, F fn) {
 
 }  // namespace
 
-extern "C" {
+namespace {
 
-size_t ssd_workspace_bytes(const ssd_dims* dims) {
-  if (!dims_ok(dims)) return 0;
-  Layout L, L1;
-  make_layout(*dims, L, L1);
-  return L.total;
-}
-
-int ssd_create(const ssd_dims* dims, const ssd_weights* w, const ssd_kv* kv, void* d_workspace,
-               size_t workspace_bytes, void* stream, ssd_ctx** out) {
-  if (!out) return SSD_ERR_ARG;
-  *out = nullptr;
-  if (!dims || !w || !kv || !d_workspace) return SSD_ERR_ARG;
+int check_create_args(const ssd_dims* dims, const ssd_weights* w, const ssd_kv* kv) {
   if (!dims_ok(dims)) return SSD_ERR_SHAPE;
   const ssd_dims& d = *dims;
   const bool t5 = d.arch == SSD_ARCH_T5;
@@ -939,54 +613,93 @@ int ssd_create(const ssd_dims* dims, const ssd_weights* w, const ssd_kv* kv, voi
   if (!kv->k_pool || !kv->v_pool || !kv->page_table || !kv->seq_len || kv->n_pages < 1)
     return SSD_ERR_ARG;
   if (t5 && (!kv->xk || !kv->xv)) return SSD_ERR_ARG;
-  Layout L, L1;
-  make_layout(d, L, L1);
-  if (workspace_bytes < L.total) return SSD_ERR_CAPACITY;
-  if (((uintptr_t)d_workspace) % 256) return SSD_ERR_ARG;
+  return SSD_OK;
+}
 
-  ssd_ctx* c = new (std::nothrow) ssd_ctx();
-  if (!c) return SSD_ERR_ARG;
+// Host-computed table of n values, value(i) for i < n, copied into device memory at dst through a
+// small stack buffer, one synchronous chunk at a time (no host heap).
+template <typename T, typename F>
+int upload_table(T* dst, size_t n, F value, hipStream_t s) {
+  constexpr size_t CHUNK = 1024;
+  T buf[CHUNK];
+  for (size_t i0 = 0; i0 < n; i0 += CHUNK) {
+    const size_t m = n - i0 < CHUNK ? n - i0 : CHUNK;
+    for (size_t i = 0; i < m; ++i) buf[i] = value(i0 + i);
+    HIP_TRY(hipMemcpyAsync(dst + i0, buf, m * sizeof(T), hipMemcpyHostToDevice, s));
+    HIP_TRY(hipStreamSynchronize(s));
+  }
+  return SSD_OK;
+}
+
+// Fill a context whose dimensions and descriptors were checked: copy them, point it at its
+// workspace, build the relative-bias (T5) or rotary (LLaMA) tables and clear the status word.
+int init_ctx(ssd_ctx* c, const ssd_dims& d, const ssd_weights* w, const ssd_kv* kv, char* ws,
+             const Layout& L, void* stream) {
   c->d = d;
   c->w = *w;
-  c->layers.assign(w->layers, w->layers + d.n_layers);
-  c->w.layers = c->layers.data();
+  for (int l = 0; l < d.n_layers; ++l) c->layers[l] = w->layers[l];
+  c->w.layers = c->layers;
   c->kv = *kv;
   c->stream = reinterpret_cast<hipStream_t>(stream);
-  c->ws = reinterpret_cast<char*>(d_workspace);
+  c->ws = ws;
   c->L = L;
-  c->L1 = L1;
-
-  int rc = SSD_OK;
-  if (t5) {
-    std::vector<int32_t> bucket(d.max_seq);
-    for (int n = 0; n < d.max_seq; ++n) bucket[n] = t5_bucket(n, d.rel_buckets, d.rel_max_dist);
-    if (hipMemcpyAsync(c->at<int32_t>(L.bucket), bucket.data(), bucket.size() * 4,
-                       hipMemcpyHostToDevice, c->stream) != hipSuccess ||
-        launch_bias_table(w->rel_bias, c->at<int32_t>(L.bucket), d.n_heads, d.max_seq,
-                          c->at<float>(L.bias_tab), c->stream) != hipSuccess ||
-        hipStreamSynchronize(c->stream) != hipSuccess)
-      rc = SSD_ERR_HIP;
+  if (d.arch == SSD_ARCH_T5) {
+    int rc = upload_table(c->at<int32_t>(L.bucket), (size_t)d.max_seq, [&](size_t n) {
+      return (int32_t)t5_bucket((int)n, d.rel_buckets, d.rel_max_dist);
+    }, c->stream);
+    if (rc) return rc;
+    HIP_TRY(launch_bias_table(w->rel_bias, c->at<int32_t>(L.bucket), d.n_heads, d.max_seq,
+                              c->at<float>(L.bias_tab), c->stream));
   } else {
     const int half = d.d_head / 2;
-    std::vector<float> cs((size_t)d.max_seq * half), sn((size_t)d.max_seq * half);
-    for (int p = 0; p < d.max_seq; ++p)
-      for (int i = 0; i < half; ++i) {
-        const double ang = (double)p * std::pow((double)d.rope_theta, -2.0 * i / d.d_head);
-        cs[(size_t)p * half + i] = (float)std::cos(ang);
-        sn[(size_t)p * half + i] = (float)std::sin(ang);
-      }
-    if (hipMemcpyAsync(c->at<float>(L.rope_cos), cs.data(), cs.size() * 4, hipMemcpyHostToDevice,
-                       c->stream) != hipSuccess ||
-        hipMemcpyAsync(c->at<float>(L.rope_sin), sn.data(), sn.size() * 4, hipMemcpyHostToDevice,
-                       c->stream) != hipSuccess ||
-        hipStreamSynchronize(c->stream) != hipSuccess)
-      rc = SSD_ERR_HIP;
+    auto angle = [&](size_t e) {
+      const size_t p = e / half, i = e % half;
+      return (double)p * std::pow((double)d.rope_theta, -2.0 * (double)i / d.d_head);
+    };
+    const size_t n = (size_t)d.max_seq * half;
+    int rc = upload_table(c->at<float>(L.rope_cos), n, [&](size_t e) { return (float)std::cos(angle(e)); },
+                          c->stream);
+    if (rc) return rc;
+    rc = upload_table(c->at<float>(L.rope_sin), n, [&](size_t e) { return (float)std::sin(angle(e)); },
+                      c->stream);
+    if (rc) return rc;
   }
+  HIP_TRY(hipMemsetAsync(c->at<int32_t>(L.status), 0, 4, c->stream));
+  HIP_TRY(hipStreamSynchronize(c->stream));
+  return SSD_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t ssd_workspace_bytes(const ssd_dims* dims) {
+  if (!dims_ok(dims)) return 0;
+  Layout L;
+  make_layout(*dims, L);
+  return L.total;
+}
+
+int ssd_create(const ssd_dims* dims, const ssd_weights* w, const ssd_kv* kv, void* d_workspace,
+               size_t workspace_bytes, void* stream, ssd_ctx** out) {
+  if (!out) return SSD_ERR_ARG;
+  *out = nullptr;
+  if (!dims || !w || !kv || !d_workspace) return SSD_ERR_ARG;
+  int rc = check_create_args(dims, w, kv);
+  if (rc) return rc;
+  Layout L;
+  make_layout(*dims, L);
+  if (workspace_bytes < L.total) return SSD_ERR_CAPACITY;
+  if (((uintptr_t)d_workspace) % 256) return SSD_ERR_ARG;
+  ssd_ctx* c = new (std::nothrow) ssd_ctx();
+  if (!c) return SSD_ERR_ARG;
+  rc = init_ctx(c, *dims, w, kv, reinterpret_cast<char*>(d_workspace), L, stream);
+  // ssd_generate's per-batch read-back lands in pinned host memory (pageable if unavailable)
   if (rc == SSD_OK &&
-      (hipMemsetAsync(c->at<int32_t>(L.status), 0, 4, c->stream) != hipSuccess ||
-       hipStreamSynchronize(c->stream) != hipSuccess))
-    rc = SSD_ERR_HIP;
-  if (rc == SSD_OK) rc = build_step_programs(c);
+      hipHostMalloc(reinterpret_cast<void**>(&c->h_status), 16, hipHostMallocDefault) != hipSuccess) {
+    c->h_status = nullptr;
+    (void)hipGetLastError();
+  }
   if (rc != SSD_OK) {
     delete c;
     return rc;
@@ -1040,7 +753,7 @@ int ssd_prefill(ssd_ctx* c, int B, int P, const int32_t* d_prompt, const void* d
         void* dst = (char*)(which ? c->kv.xv : c->kv.xk) + (size_t)l * c->xkv_layer_elems() * c->kv_elem();
         HIP_TRY(launch_scatter_cross(tmp, dst, B, d.n_visual, d.n_heads, d.d_head, d.kvdtype, s));
       }
-      if (fold_cross(d)) {
+      if (c->L.fold) {
         const size_t off = (size_t)l * c->xkv_layer_elems() * c->kv_elem();
         HIP_TRY(launch_cross_fold((char*)c->kv.xk + off, (char*)c->kv.xv + off, d.kvdtype,
                                   c->layers[l].xq, c->layers[l].xo, d.wdtype, d.n_heads,
@@ -1049,7 +762,7 @@ int ssd_prefill(ssd_ctx* c, int B, int P, const int32_t* d_prompt, const void* d
                                   c->at<float>(c->L.fold_o) + (size_t)l * c->fold_layer_elems(), s));
       }
     }
-    c->fold_ready = fold_cross(d);
+    c->fold_ready = c->L.fold;
   }
   EmbedArgs e;
   e.x = x; e.B = B; e.C = Cx; e.d = D; e.embed = c->w.embed; e.vocab = d.vocab; e.wdtype = d.wdtype;
@@ -1167,27 +880,14 @@ int ssd_generate(ssd_ctx* c, int B, int P, const int32_t* d_prompt, const void* 
                  int gamma, int mode, int reuse_hidden, int32_t* d_tokens, int64_t* h_stats) {
   if (!c || !d_tokens || T < 1) return SSD_ERR_ARG;
   if (mode != SSD_MODE_GREEDY && mode != SSD_MODE_SPECULATIVE &&
-      mode != SSD_MODE_SPECULATIVE_DYNAMIC && mode != SSD_MODE_SPECULATIVE_AHEAD)
+      mode != SSD_MODE_SPECULATIVE_DYNAMIC)
     return SSD_ERR_ARG;
   const bool dynamic = mode == SSD_MODE_SPECULATIVE_DYNAMIC;
-  const bool ahead = mode == SSD_MODE_SPECULATIVE_AHEAD;
   const int g_max = mode == SSD_MODE_GREEDY ? 0 : (dynamic ? gamma + 9 : gamma);
   if (mode != SSD_MODE_GREEDY && (gamma < 1 || g_max > c->d.max_gamma)) return SSD_ERR_SHAPE;
   if (B < 1 || B > c->d.max_batch) return SSD_ERR_SHAPE;
   const int Cx = P + (c->d.arch == SSD_ARCH_T5 ? 0 : c->d.n_visual);
   if (Cx + T + c->d.max_gamma > c->d.max_seq) return SSD_ERR_CAPACITY;
-  // drafts made ahead write up to 2 gamma positions past the round's start
-  if (ahead && Cx + T + 2 * gamma > c->d.max_seq) return SSD_ERR_CAPACITY;
-  if (ahead && c->ex_phi) return SSD_ERR_STATE;
-  if (ahead && !c->stream1) {
-    if (hipStreamCreateWithFlags(&c->stream1, hipStreamNonBlocking) != hipSuccess) {
-      c->stream1 = nullptr;
-      return SSD_ERR_HIP;
-    }
-    if (hipEventCreateWithFlags(&c->ev_fork, hipEventDisableTiming) != hipSuccess ||
-        hipEventCreateWithFlags(&c->ev_join, hipEventDisableTiming) != hipSuccess)
-      return SSD_ERR_HIP;
-  }
   int32_t* pending = c->at<int32_t>(c->L.g_pending);
   int32_t* draft = c->at<int32_t>(c->L.g_draft);
   int32_t* target = c->at<int32_t>(c->L.g_target);
@@ -1197,7 +897,8 @@ int ssd_generate(ssd_ctx* c, int B, int P, const int32_t* d_prompt, const void* 
   int64_t* stats = c->at<int64_t>(c->L.g_stats);
   int rc = ssd_prefill(c, B, P, d_prompt, d_visual, pending, nullptr);
   if (rc) return rc;
-  GenInitArgs gi{B, T, pending, d_tokens, count, active, stats, n_active, c->kv.seq_len};
+  GenInitArgs gi{B, T, pending, d_tokens, count, active, stats, n_active, c->kv.seq_len,
+                 c->at<int32_t>(c->L.status)};
   HIP_TRY(launch_gen_init(gi, c->stream));
   AcceptArgs a;
   std::memset(&a, 0, sizeof(a));
@@ -1206,71 +907,17 @@ int ssd_generate(ssd_ctx* c, int B, int P, const int32_t* d_prompt, const void* 
   a.status = c->at<int32_t>(c->L.status);
   a.tokens = d_tokens; a.count = count; a.active_rw = active; a.T = T; a.stats = stats;
   a.n_active = n_active;
-  // drafts made ahead: two (draft tokens, layer-k stash) pairs used in turn
-  int32_t* drafts[2] = {draft, c->at<int32_t>(c->L.g_draft2)};
-  float* stashes[2] = {c->at<float>(c->L.stash), c->at<float>(c->L1.stash)};
-  int32_t* guess = c->at<int32_t>(c->L.g_guess);
-  const float* x1 = c->at<float>(c->L.x1);
-  int cur = 0;
-  if (ahead) {
-    a.guess = guess;
-    a.next_need = 2 * gamma + 1;
-  }
-  // the read-back lands in pinned memory (allocated on first use), a direct copy
-  if (!c->h_status &&
-      hipHostMalloc(reinterpret_cast<void**>(&c->h_status), 16, hipHostMallocDefault) != hipSuccess) {
-    c->h_status = nullptr;  // pageable stack memory then
-    (void)hipGetLastError();
-  }
+  // the read-back lands in the context's pinned buffer (a direct copy), else on the stack
+  int32_t h_active[4] = {0, 0, 0, 0};
   int round = 0;
   while (round < T) {
-    int32_t h_active[4] = {0, 0, 0, 0};
     int32_t* dst = c->h_status ? c->h_status : h_active;
     HIP_TRY(hipMemcpyAsync(dst, n_active, 16, hipMemcpyDeviceToHost, c->stream));
     HIP_TRY(hipStreamSynchronize(c->stream));
     if (dst != h_active) std::memcpy(h_active, dst, 16);
+    // a device status bit (bad token id, position past the cache, unmapped page) ends the loop
+    if (h_active[2] != 0) return SSD_ERR_DEVICE;
     if (h_active[0] == 0) break;
-    if (ahead) {
-      // the previous round's drafts made ahead hold when it accepted everything and its extra
-      // token was the one they started from; otherwise draft from the new pending token
-      if (h_active[2]) {
-        cur ^= 1;
-      } else {
-        GraphKey kd{4, B, gamma, 0, pending, drafts[cur], stashes[cur], nullptr};
-        rc = launch_maybe_graph(c, kd, [&]() {
-          return draft_launches(c, B, gamma, pending, drafts[cur], nullptr, nullptr, 0.f, 0,
-                                stashes[cur]);
-        });
-        if (rc) return rc;
-      }
-      GraphKey kl{5, B, gamma, 0, drafts[cur], nullptr, nullptr, nullptr};
-      rc = launch_maybe_graph(c, kl, [&]() { return verify_last_row(c, B, gamma, drafts[cur]); });
-      if (rc) return rc;
-      HIP_TRY(hipEventRecord(c->ev_fork, c->stream));
-      HIP_TRY(hipStreamWaitEvent(c->stream1, c->ev_fork, 0));
-      {
-        OnLane1 lane1(c);
-        GraphKey ka{6, B, gamma, 1, guess, drafts[cur ^ 1], stashes[cur ^ 1], x1};
-        rc = launch_maybe_graph(c, ka, [&]() {
-          return ahead_launches(c, B, gamma, x1, guess, drafts[cur ^ 1], stashes[cur ^ 1]);
-        });
-      }
-      if (rc) return rc;
-      HIP_TRY(hipEventRecord(c->ev_join, c->stream1));
-      GraphKey kv{7, B, gamma, 0, stashes[cur], target, nullptr, nullptr};
-      rc = launch_maybe_graph(c, kv, [&]() {
-        return verify_deep(c, B, gamma, stashes[cur], target, nullptr);
-      });
-      if (rc) return rc;
-      // the accept moves seq_len, which the drafts made ahead read: after they finish
-      HIP_TRY(hipStreamWaitEvent(c->stream, c->ev_join, 0));
-      a.gamma = gamma;
-      a.draft = drafts[cur];
-      HIP_TRY(launch_accept(a, c->stream));
-      c->draft_valid = false;
-      ++round;
-      continue;
-    }
     const int g = mode == SSD_MODE_GREEDY ? 0
                   : (dynamic ? ssd_dynamic_gamma(h_active[1], gamma, c->d.max_seq) : gamma);
     if (g > c->d.max_gamma) return SSD_ERR_SHAPE;
@@ -1291,10 +938,15 @@ int ssd_generate(ssd_ctx* c, int B, int P, const int32_t* d_prompt, const void* 
       c->draft_valid = false;
     }
   }
-  if (h_stats) {
-    HIP_TRY(hipMemcpyAsync(h_stats, stats, 24, hipMemcpyDeviceToHost, c->stream));
+  // the status word of the last batch of rounds, read with the statistics
+  {
+    int32_t* dst = c->h_status ? c->h_status : h_active;
+    HIP_TRY(hipMemcpyAsync(dst, n_active, 16, hipMemcpyDeviceToHost, c->stream));
+    if (h_stats) HIP_TRY(hipMemcpyAsync(h_stats, stats, 24, hipMemcpyDeviceToHost, c->stream));
+    HIP_TRY(hipStreamSynchronize(c->stream));
+    if (dst != h_active) std::memcpy(h_active, dst, 16);
+    if (h_active[2] != 0) return SSD_ERR_DEVICE;
   }
-  HIP_TRY(hipStreamSynchronize(c->stream));
   return SSD_OK;
 }
 
@@ -1302,17 +954,6 @@ int ssd_set_graphs(ssd_ctx* c, int enable) {
   if (!c) return SSD_ERR_ARG;
   c->use_graphs = enable != 0;
   return SSD_OK;
-}
-
-int ssd_set_persistent(ssd_ctx* c, int enable) {
-  if (!c) return SSD_ERR_ARG;
-  if (c->use_step != (enable != 0)) {
-    // captured launch sequences differ between the two paths
-    for (auto& kv : c->graphs) (void)hipGraphExecDestroy(kv.second);
-    c->graphs.clear();
-  }
-  c->use_step = enable != 0;
-  return (c->step_ok && c->use_step) ? 1 : 0;
 }
 
 int ssd_set_hidden_export(ssd_ctx* c, float* d_phi, float* d_xk, float* d_xl) {
@@ -1383,12 +1024,9 @@ const char* ssd_status_string(int code) {
 
 void ssd_destroy(ssd_ctx* c) {
   if (!c) return;
-  if (c->stream1) (void)hipStreamSynchronize(c->stream1);
+  (void)hipStreamSynchronize(c->stream);
   for (auto& kv : c->graphs) (void)hipGraphExecDestroy(kv.second);
   for (hipEvent_t e : c->ev_pool) (void)hipEventDestroy(e);
-  if (c->ev_fork) (void)hipEventDestroy(c->ev_fork);
-  if (c->ev_join) (void)hipEventDestroy(c->ev_join);
-  if (c->stream1) (void)hipStreamDestroy(c->stream1);
   if (c->h_status) (void)hipHostFree(c->h_status);
   delete c;
 }

@@ -233,25 +233,17 @@ class DeviceDecoder:
         return out, alen
 
     def generate(self, prompt, visual, T: int, gamma: int, speculative: bool = True,
-                 reuse: bool = True, dynamic: bool = False, ahead: bool = False):
-        """ssd_generate; with dynamic=True gamma is d(0) of the context-length schedule; with
-        ahead=True the next round is drafted on a second stream during each verify pass."""
+                 reuse: bool = True, dynamic: bool = False):
+        """ssd_generate; with dynamic=True gamma is d(0) of the context-length schedule."""
         B, P = prompt.shape
         tokens = self.ivec(B, T)
-        if ahead and (dynamic or not speculative):
-            raise ValueError("drafting ahead takes a fixed draft length")
         mode = abi.SSD_MODE_GREEDY if not speculative else (
-            abi.SSD_MODE_SPECULATIVE_DYNAMIC if dynamic else
-            abi.SSD_MODE_SPECULATIVE_AHEAD if ahead else abi.SSD_MODE_SPECULATIVE)
+            abi.SSD_MODE_SPECULATIVE_DYNAMIC if dynamic else abi.SSD_MODE_SPECULATIVE)
         stats = self._call(abi.ssd_generate, self.ctx, B, P, prompt, visual, T, gamma, mode, reuse, tokens)
         return tokens, stats
 
     def set_graphs(self, enable: bool):
         abi.ssd_set_graphs(self.ctx, enable)
-
-    def set_persistent(self, enable: bool) -> bool:
-        """One-row passes of one-sequence calls as one persistent launch; True when active."""
-        return abi.ssd_set_persistent(self.ctx, enable)
 
     def sync_status(self):
         torch.cuda.current_stream(self.device).synchronize()

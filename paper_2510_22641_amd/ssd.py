@@ -18,8 +18,7 @@ SSD_OK, SSD_ERR_ARG, SSD_ERR_SHAPE, SSD_ERR_CAPACITY, SSD_ERR_HIP, SSD_ERR_STATE
 SSD_ARCH_T5, SSD_ARCH_LLAMA = 0, 1
 SSD_F32, SSD_BF16 = 0, 1
 SSD_MODE_GREEDY, SSD_MODE_SPECULATIVE, SSD_MODE_SPECULATIVE_DYNAMIC = 0, 1, 2
-SSD_MODE_SPECULATIVE_AHEAD = 3
-SSD_DEV_BAD_TOKEN, SSD_DEV_CAPACITY, SSD_DEV_BAD_PAGE, SSD_DEV_SYNC = 1, 2, 4, 8
+SSD_DEV_BAD_TOKEN, SSD_DEV_CAPACITY, SSD_DEV_BAD_PAGE = 1, 2, 4
 
 
 class ssd_dims(ctypes.Structure):
@@ -78,7 +77,6 @@ def _load():
                                  POINTER(c_int64)]),
         "ssd_dynamic_gamma": (c_int, [c_int, c_int, c_int]),
         "ssd_set_graphs": (c_int, [P, c_int]),
-        "ssd_set_persistent": (c_int, [P, c_int]),
         "ssd_set_hidden_export": (c_int, [P, P, P, P]),
         "ssd_profile_enable": (c_int, [P, c_int]),
         "ssd_profile_read": (c_int, [P, POINTER(c_int64), POINTER(ctypes.c_double),
@@ -96,7 +94,7 @@ def _load():
 
 _lib = _load()
 EXPORTS = ("ssd_workspace_bytes", "ssd_create", "ssd_prefill", "ssd_draft", "ssd_verify",
-           "ssd_accept", "ssd_draft_sample", "ssd_accept_sample", "ssd_generate", "ssd_dynamic_gamma", "ssd_set_graphs", "ssd_set_persistent", "ssd_set_hidden_export",
+           "ssd_accept", "ssd_draft_sample", "ssd_accept_sample", "ssd_generate", "ssd_dynamic_gamma", "ssd_set_graphs", "ssd_set_hidden_export",
            "ssd_profile_enable",
            "ssd_profile_read", "ssd_sync_status",
            "ssd_status_string", "ssd_destroy")
@@ -182,14 +180,6 @@ def ssd_dynamic_gamma(t: int, d0: int, n_max: int) -> int:
 
 def ssd_set_graphs(ctx, enable: bool):
     _check("ssd_set_graphs", _lib.ssd_set_graphs(ctx, int(bool(enable))))
-
-
-def ssd_set_persistent(ctx, enable: bool) -> bool:
-    """Whether one-row passes of one-sequence calls use the persistent kernel (True when active)."""
-    rc = _lib.ssd_set_persistent(ctx, int(bool(enable)))
-    if rc < 0:
-        raise SSDError("ssd_set_persistent", rc)
-    return rc == 1
 
 
 def ssd_set_hidden_export(ctx, d_phi, d_xk, d_xl):

@@ -142,6 +142,35 @@ def check_run_against_oracle(dec: Decoder, shape, prompt, visual, run: DevRun, b
     return ties
 
 
+def oracle_full_logits_along(dec: Decoder, prompt, visual, tokens, i: int) -> np.ndarray:
+    """The oracle's full-model logits that choose emitted token i of a stream whose tokens
+    0..i-1 are ``tokens[:i]`` (token 0 comes from the prefill)."""
+    cap = dec.shape.prefix_len() + len(prompt) + i + 2
+    st, _, lg = decode.prefill(dec, prompt, visual, cap)
+    for t in tokens[:i]:
+        if i == 0:
+            break
+        lg, _ = dec.full_step(st, int(t), st.seq_len)
+        st.seq_len += 1
+    return lg
+
+
+def check_streams_agree_until_near_tie(dec: Decoder, shape, prompt, visual, a, b,
+                                       what: str) -> int:
+    """Two device token streams of the same sequence (speculative and greedy decoding) must be
+    identical up to their first difference, and there the oracle's logits along the common
+    prefix must put both tokens within the tolerance of its top.  Returns the index of the first
+    difference (len(a) when none)."""
+    a, b = [int(t) for t in a], [int(t) for t in b]
+    assert len(a) == len(b), what
+    first = next((i for i, (x, y) in enumerate(zip(a, b)) if x != y), len(a))
+    if first < len(a):
+        lg = oracle_full_logits_along(dec, prompt, visual, a, first)
+        check_token(a[first], lg, shape, f"{what}: token {first} of the first stream")
+        check_token(b[first], lg, shape, f"{what}: token {first} of the second stream")
+    return first
+
+
 def workload_inputs(wl, seed: int, batch: Optional[int] = None):
     B = batch or wl.batch
     w = synth.workload_weights(wl, seed, threads=4)

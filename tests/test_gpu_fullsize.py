@@ -1,11 +1,14 @@
 """Device path vs the CPU oracle at the workloads' full sizes, in the launch configuration the
 benchmark times (HIP graphs on, verify reusing the draft's layer-k states).
 
-FlanT5-base (c2): the whole 64-token job, every draft and verify logit.  FlanT5-xl (c3): the
-whole 128-token job on the device, its first rounds replayed through the oracle logit by logit,
-and the benchmark's ``ssd_generate`` loop equal to the stepwise calls token for token.
-LLaVA-1.5-7B shape (c5): prefill over the 576-row visual prefix + 32 ids, then the first rounds
-(the float64 oracle holds 54 GB of weights and needs tens of seconds per prefill there).
+FlanT5-base (c2) and FlanT5-xl (c3): the whole job (64 and 128 tokens), every draft and verify
+logit replayed through the oracle, and the benchmark's ``ssd_generate`` loop equal to the
+stepwise calls token for token and round for round.  LLaVA-1.5-7B shape (c5): prefill over the
+576-row visual prefix + 32 ids, then the first ten rounds (the float64 oracle holds 54 GB of
+weights and needs tens of seconds per prefill there).  FlanT5-xl sweep points chosen by kernel
+path (one-row steps with 9-row verify chunks; batch 8 with 24- and 40-row verify chunks and
+72-row chunks on the two-plane skinny path): every sequence replayed for its first rounds, and
+every sequence of a batch against its own batch-1 run on the device.
 """
 import numpy as np
 import pytest
@@ -51,28 +54,42 @@ def test_c2_flant5_base_whole_job():
     assert stats["rounds"] == len(run.rounds)
 
 
+@pytest.mark.timeout(600)
 def test_c3_flant5_xl_bench_configuration():
     wl = synth.C3
-    dd, run, pt, vt = _check(wl, max_rounds=8)
+    dd, run, pt, vt = _check(wl)
     assert len(run.tokens[0]) == wl.new_tokens
     toks, stats = dd.generate(pt, vt, wl.new_tokens, wl.gamma, speculative=True, reuse=True)
     assert toks.cpu().numpy()[0].tolist() == run.tokens[0]
+    assert stats["rounds"] == len(run.rounds)
     assert stats["accepted"] == sum(int(r.accepted[0]) for r in run.rounds)
 
 
 @pytest.mark.timeout(900)
 def test_c5_llava_7b_prefill_and_first_rounds():
     wl = synth.C5
-    _check(wl, max_rounds=2, device_rounds=2)
+    _check(wl, max_rounds=10, device_rounds=10)
 
 
-def test_c4_batch8_ragged_point():
-    """A point of the FlanT5-xl sweep at batch 8 (k 4, gamma 8): the verify chunk is 72 rows
-    (tile MFMA path) and every sequence keeps its own length.  Two sequences are replayed through
-    the oracle for their first rounds; all eight are checked against the device's own batch-1
-    runs token for token where no near-tie intervenes (first divergence must be a near-tie)."""
+def _c4(b, k, g):
+    return next(p for p in synth.c4_points()
+                if p.batch == b and p.draft_layers == k and p.gamma == g)
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("b,k,g,rounds", [(1, 12, 8, 4), (8, 4, 8, 2), (8, 8, 2, 2),
+                                          (8, 12, 4, 2)],
+                         ids=["b1-k12-g8", "b8-k4-g8", "b8-k8-g2", "b8-k12-g4"])
+def test_c4_sweep_points(b, k, g, rounds):
+    """Points of the FlanT5-xl sweep (one decoder, deep layers damped from layer 7 on), chosen by
+    kernel path: at batch 1 a 9-row verify chunk (two-plane skinny MFMA); at batch 8 the draft
+    steps are 8-row skinny launches and the verify chunk is 24, 40 or 72 rows, each sequence at
+    its own length.  Every sequence is replayed through the oracle for its first rounds; the
+    ssd_generate loop equals the stepwise calls token for token and round for round; and every
+    sequence of the batch equals its own batch-1 run on the device up to a near-tie of the
+    oracle's logits (the batch and batch-1 paths round differently)."""
     from paper_2510_22641_amd import runtime
-    wl = next(p for p in synth.c4_points() if p.batch == 8 and p.draft_layers == 4 and p.gamma == 8)
+    wl = _c4(b, k, g)
     w, z, pr = parity.workload_inputs(wl, 0)
     # stepwise calls on a ragged batch: gamma positions of slack for finished sequences
     dd = runtime.from_workload(wl, 0, weights=w, extra_seq=wl.gamma)
@@ -83,10 +100,21 @@ def test_c4_batch8_ragged_point():
     run = parity.device_run(dd, pt, vt, wl.new_tokens, wl.gamma, reuse=True)
     assert dd.sync_status() == (0, 0)
     assert all(len(t) == wl.new_tokens for t in run.tokens)
-    lens = {len([r for r in run.rounds if r.active[b]]) for b in range(wl.batch)}
-    print(f"[{wl.name}] rounds per sequence {sorted(lens)}; oracle replay", flush=True)
-    for b in (0, 5):
-        parity.check_run_against_oracle(dec, wl.shape, pr[b], z[b], run, b, wl.gamma, max_rounds=3)
+    lens = [len([r for r in run.rounds if r.active[s]]) for s in range(wl.batch)]
+    print(f"[{wl.name}] rounds per sequence {lens}; oracle replay", flush=True)
+    for s in range(wl.batch):
+        parity.check_run_against_oracle(dec, wl.shape, pr[s], z[s], run, s, wl.gamma,
+                                        max_rounds=rounds)
     toks, stats = dd.generate(pt, vt, wl.new_tokens, wl.gamma, speculative=True, reuse=True)
     assert toks.cpu().numpy().tolist() == run.tokens
+    assert stats["rounds"] == len(run.rounds) == max(lens)
     assert dd.sync_status() == (0, 0)
+    if wl.batch > 1:
+        print(f"[{wl.name}] batch-1 runs", flush=True)
+        for s in range(wl.batch):
+            t1, _ = dd.generate(pt[s:s + 1], vt[s:s + 1], wl.new_tokens, wl.gamma,
+                                speculative=True, reuse=True)
+            parity.check_streams_agree_until_near_tie(
+                dec, wl.shape, pr[s], z[s], run.tokens[s], t1.cpu().numpy()[0].tolist(),
+                f"{wl.name} seq {s} batch vs batch-1")
+        assert dd.sync_status() == (0, 0)
