@@ -148,6 +148,30 @@ size_t ssd_workspace_bytes(const ssd_dims* dims);
 int ssd_create(const ssd_dims* dims, const ssd_weights* w, const ssd_kv* kv, void* d_workspace,
                size_t workspace_bytes, void* stream, ssd_ctx** out);
 
+/* For callers that cannot allocate device memory (code running under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc): ssd_create without a workspace argument.  The
+ * context's workspace is the library's own fixed device array of SSD_STATIC_SCRATCH_BYTES
+ * (64 MiB), one per GPU, which each GPU the library runs on holds until the process ends; it is
+ * the array of the device current at the call (that of `stream`).  Everything else is as
+ * ssd_create, except that:
+ *   - the T5 cross-attention is not folded (its per-layer float32 matrices would not fit), so
+ *     one-row steps take the query projection, attention and output projection instead (the
+ *     same decoder, within the same parity tolerances);
+ *   - HIP graphs are off (instantiating one allocates); ssd_set_graphs(ctx, 1) turns them on,
+ *     and then the first call of each shape allocates its graph;
+ *   - ssd_generate's read-back goes to host stack memory instead of a pinned buffer.
+ * Neither this call nor any later call on the context calls hipMalloc, hipHostMalloc, hipFree or
+ * another allocating routine, on the device or the host.  Dimensions whose workspace
+ * (ssd_workspace_bytes without the folded matrices) exceeds SSD_STATIC_SCRATCH_BYTES are refused
+ * with SSD_ERR_CAPACITY before anything runs.  At most one such context per device is alive at a
+ * time (a second call before ssd_destroy of the first returns SSD_ERR_STATE): every context made
+ * here on one GPU shares that GPU's array, which keeps the previous context's contents (this
+ * call rebuilds the tables and clears the status word; every other slice is written before it
+ * is read), and work of two of them that overlapped on one GPU would race. */
+#define SSD_STATIC_SCRATCH_BYTES ((size_t)64 << 20)
+int ssd_create_static(const ssd_dims* dims, const ssd_weights* w, const ssd_kv* kv, void* stream,
+                      ssd_ctx** out);
+
 /* Prefill (Algorithm 1's input: z and the context y^1..y^t).  d_prompt [B][P] int32 token ids;
  * d_visual [B][n_visual][d] wdtype.  T5: cross-attention K/V of every layer are projected from
  * z; the prompt occupies positions 0..P-1.  LLaMA: the visual rows are the inputs of positions

@@ -6,6 +6,7 @@
 #include <cstdint>
 #include <cstring>
 #include <map>
+#include <mutex>
 #include <new>
 #include <tuple>
 #include <vector>
@@ -180,6 +181,8 @@ struct ssd_ctx {
   char* ws;
   Layout L;
   int32_t* h_status = nullptr;  // pinned [4]: ssd_generate's read-back of the active counts
+  bool is_static = false;       // made by ssd_create_static: workspace = the device's scratch
+  int static_dev = -1;
   bool prefilled = false;
   bool fold_ready = false;  // fold_q / fold_o hold the prefilled sequence's cross-attention
   // reuse bookkeeping: the last ssd_draft's arguments
@@ -669,6 +672,36 @@ int init_ctx(ssd_ctx* c, const ssd_dims& d, const ssd_weights* w, const ssd_kv* 
   return SSD_OK;
 }
 
+// The workspace of contexts made by ssd_create_static: one fixed array per device, resident from
+// the library's load until the process ends.  Host code never passes `scratch` itself to a
+// kernel or a copy (on the host it only names the symbol); it uses the device address that
+// hipGetSymbolAddress returns for the current device, looked up once per device.
+constexpr int STATIC_MAX_DEVICES = 64;
+std::mutex g_static_mu;
+char* g_scratch_ptr[STATIC_MAX_DEVICES] = {};
+bool g_static_live[STATIC_MAX_DEVICES] = {};
+alignas(ssd_ctx) unsigned char g_static_ctx_mem[STATIC_MAX_DEVICES][sizeof(ssd_ctx)];
+
+}  // namespace
+
+__device__ __align__(256) unsigned char scratch[SSD_STATIC_SCRATCH_BYTES];
+
+namespace {
+
+// Device address of `scratch` on device dev (current), looked up on the device's first use.
+int static_scratch(int dev, char** out) {
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) {
+      (void)hipGetLastError();
+      return SSD_ERR_HIP;
+    }
+    g_scratch_ptr[dev] = reinterpret_cast<char*>(p);
+  }
+  *out = g_scratch_ptr[dev];
+  return SSD_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -704,6 +737,38 @@ int ssd_create(const ssd_dims* dims, const ssd_weights* w, const ssd_kv* kv, voi
     delete c;
     return rc;
   }
+  *out = c;
+  return SSD_OK;
+}
+
+int ssd_create_static(const ssd_dims* dims, const ssd_weights* w, const ssd_kv* kv, void* stream,
+                      ssd_ctx** out) {
+  if (!out) return SSD_ERR_ARG;
+  *out = nullptr;
+  if (!dims || !w || !kv) return SSD_ERR_ARG;
+  int rc = check_create_args(dims, w, kv);
+  if (rc) return rc;
+  Layout L;
+  make_layout(*dims, L, /*allow_fold=*/false);
+  if (L.total > SSD_STATIC_SCRATCH_BYTES) return SSD_ERR_CAPACITY;
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return SSD_ERR_HIP;
+  if (dev >= STATIC_MAX_DEVICES) return SSD_ERR_SHAPE;
+  std::lock_guard<std::mutex> lock(g_static_mu);
+  if (g_static_live[dev]) return SSD_ERR_STATE;
+  char* ws = nullptr;
+  rc = static_scratch(dev, &ws);
+  if (rc) return rc;
+  ssd_ctx* c = new (g_static_ctx_mem[dev]) ssd_ctx();
+  c->is_static = true;
+  c->static_dev = dev;
+  c->use_graphs = false;  // instantiating a graph allocates
+  rc = init_ctx(c, *dims, w, kv, ws, L, stream);
+  if (rc != SSD_OK) {
+    c->~ssd_ctx();
+    return rc;
+  }
+  g_static_live[dev] = true;
   *out = c;
   return SSD_OK;
 }
@@ -1028,6 +1093,13 @@ void ssd_destroy(ssd_ctx* c) {
   for (auto& kv : c->graphs) (void)hipGraphExecDestroy(kv.second);
   for (hipEvent_t e : c->ev_pool) (void)hipEventDestroy(e);
   if (c->h_status) (void)hipHostFree(c->h_status);
+  if (c->is_static) {
+    std::lock_guard<std::mutex> lock(g_static_mu);
+    const int dev = c->static_dev;
+    c->~ssd_ctx();
+    g_static_live[dev] = false;
+    return;
+  }
   delete c;
 }
 

@@ -93,7 +93,10 @@ class DeviceDecoder:
         d.max_pages = (cap.max_seq + cap.page_size - 1) // cap.page_size
         return d
 
-    def create(self) -> "DeviceDecoder":
+    def create(self, static: bool = False) -> "DeviceDecoder":
+        """Allocate the KV cache and the workspace, and create the context; with static=True the
+        context is made by ssd_create_static and uses the library's own fixed device array as
+        its workspace (no workspace tensor is allocated)."""
         sh, cap, dev = self.shape, self.cap, self.device
         dims = self.dims()
         self._dims = dims
@@ -116,8 +119,9 @@ class DeviceDecoder:
         nbytes = abi.ssd_workspace_bytes(dims)
         if nbytes == 0:
             raise ValueError("libssd rejected the dimensions")
-        self.workspace = torch.empty(nbytes + 256, dtype=torch.uint8, device=dev)
-        ws_ptr = (self.workspace.data_ptr() + 255) // 256 * 256
+        if not static:
+            self.workspace = torch.empty(nbytes + 256, dtype=torch.uint8, device=dev)
+            ws_ptr = (self.workspace.data_ptr() + 255) // 256 * 256
 
         self._layer_structs = (abi.ssd_layer_weights * L)()
         for l in range(L):
@@ -138,7 +142,10 @@ class DeviceDecoder:
         # a stream of its own (default priority): the null stream cannot be captured into graphs
         self.stream = torch.cuda.Stream(dev)
         torch.cuda.current_stream(dev).synchronize()
-        self.ctx = abi.ssd_create(dims, w, kv, ws_ptr, nbytes, self.stream.cuda_stream)
+        if static:
+            self.ctx = abi.ssd_create_static(dims, w, kv, self.stream.cuda_stream)
+        else:
+            self.ctx = abi.ssd_create(dims, w, kv, ws_ptr, nbytes, self.stream.cuda_stream)
         self._w_struct, self._kv_struct = w, kv
         return self
 
@@ -253,8 +260,10 @@ class DeviceDecoder:
 def from_workload(wl, seed: int, device: str = "cuda", max_batch: Optional[int] = None,
                   max_gamma: Optional[int] = None, extra_seq: int = 0, page_seed: Optional[int] = None,
                   kv_dtype: Optional[str] = None, weights: Optional[Dict] = None,
-                  draft_layers: Optional[int] = None, spare_pages: int = 0) -> DeviceDecoder:
-    """Build a DeviceDecoder for a synth workload, streaming its seeded tensors to the device."""
+                  draft_layers: Optional[int] = None, spare_pages: int = 0,
+                  static: bool = False) -> DeviceDecoder:
+    """Build a DeviceDecoder for a synth workload, streaming its seeded tensors to the device
+    (static=True: the context takes the library's fixed workspace, ssd_create_static)."""
     import synth
     sh = wl.shape
     mg = max_gamma if max_gamma is not None else max(wl.gamma, 1)
@@ -267,4 +276,4 @@ def from_workload(wl, seed: int, device: str = "cuda", max_batch: Optional[int] 
         dd.load_dict(weights)
     else:
         synth.make_weights(sh, seed, wl.deep_scale, wl.boundary, sink=dd.load)
-    return dd.create()
+    return dd.create(static=static)

@@ -67,6 +67,8 @@ def _load():
         "ssd_workspace_bytes": (c_size_t, [POINTER(ssd_dims)]),
         "ssd_create": (c_int, [POINTER(ssd_dims), POINTER(ssd_weights), POINTER(ssd_kv), P,
                                c_size_t, P, POINTER(P)]),
+        "ssd_create_static": (c_int, [POINTER(ssd_dims), POINTER(ssd_weights), POINTER(ssd_kv),
+                                      P, POINTER(P)]),
         "ssd_prefill": (c_int, [P, c_int, c_int, P, P, P, P]),
         "ssd_draft": (c_int, [P, c_int, c_int, P, P, P]),
         "ssd_verify": (c_int, [P, c_int, c_int, P, P, c_int, P, P]),
@@ -93,7 +95,7 @@ def _load():
 
 
 _lib = _load()
-EXPORTS = ("ssd_workspace_bytes", "ssd_create", "ssd_prefill", "ssd_draft", "ssd_verify",
+EXPORTS = ("ssd_workspace_bytes", "ssd_create", "ssd_create_static", "ssd_prefill", "ssd_draft", "ssd_verify",
            "ssd_accept", "ssd_draft_sample", "ssd_accept_sample", "ssd_generate", "ssd_dynamic_gamma", "ssd_set_graphs", "ssd_set_hidden_export",
            "ssd_profile_enable",
            "ssd_profile_read", "ssd_sync_status",
@@ -131,6 +133,18 @@ def ssd_create(dims: ssd_dims, weights: ssd_weights, kv: ssd_kv, d_workspace, wo
                                          ctypes.byref(kv), _p(d_workspace), workspace_bytes,
                                          _p(stream), ctypes.byref(ctx)))
     return ctx
+
+
+def ssd_create_static(dims: ssd_dims, weights: ssd_weights, kv: ssd_kv, stream) -> c_void_p:
+    """ssd_create with the library's fixed per-device array as the workspace (no allocation)."""
+    ctx = c_void_p()
+    _check("ssd_create_static", _lib.ssd_create_static(ctypes.byref(dims), ctypes.byref(weights),
+                                                       ctypes.byref(kv), _p(stream),
+                                                       ctypes.byref(ctx)))
+    return ctx
+
+
+SSD_STATIC_SCRATCH_BYTES = 64 << 20
 
 
 def ssd_prefill(ctx, B, P, d_prompt, d_visual, d_pending, d_logits=None):
