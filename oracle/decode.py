@@ -41,6 +41,14 @@ def dynamic_draft_length(t: int, d0: int, n_max: int) -> int:
     return d0 + math.floor(10.0 / (1.0 + e))
 
 
+def confidence(logits: np.ndarray) -> float:
+    """The confidence of a prediction: the largest softmax probability over the vocabulary,
+    max_v softmax(logits)_v = 1 / sum_v exp(logits_v - max logits) (the paper's C_l, appendix on
+    the choice of n)."""
+    lg = np.asarray(logits, dtype=np.float64)
+    return float(1.0 / np.sum(np.exp(lg - np.max(lg))))
+
+
 def accept_length(drafts: Sequence[int], targets: Sequence[int]) -> int:
     """Longest prefix of drafts that matches the full model: a = max{j : draft_i = target_{i-1}, i<=j}.
 
@@ -62,6 +70,7 @@ class Round:
     accepted: int  # a
     draft_logits: List[np.ndarray] = field(default_factory=list)
     target_logits: List[np.ndarray] = field(default_factory=list)
+    confidences: List[float] = field(default_factory=list)  # of each draft (confidence stop)
 
 
 @dataclass
@@ -118,7 +127,8 @@ def ssd(dec: Decoder, prompt, visual, T: int, gamma: int, capacity: Optional[int
         draft_policy: Optional[Callable[[int, int, np.ndarray], int]] = None,
         poison: bool = False, use_imitation: bool = True, eos_id: int = -1,
         max_rounds: Optional[int] = None,
-        gamma_fn: Optional[Callable[[int], int]] = None) -> Run:
+        gamma_fn: Optional[Callable[[int], int]] = None,
+        confidence_stop: Optional[float] = None) -> Run:
     """Algorithm 1: draft gamma tokens with layers 1..k + I + g, verify them with the full decoder,
     keep the longest matching prefix plus the full model's token at the first mismatch.
 
@@ -126,7 +136,11 @@ def ssd(dec: Decoder, prompt, visual, T: int, gamma: int, capacity: Optional[int
     ``poison`` overwrites every KV entry beyond the valid length with NaN after each acceptance;
     ``max_rounds`` stops early (a bounded sample of the loop, for timing);
     ``gamma_fn(l) -> d`` drafts d tokens in a round that starts at context length l (the dynamic
-    draft length; ``gamma`` then only sizes the cache).
+    draft length; ``gamma`` then only sizes the cache);
+    ``confidence_stop`` = tau stops a round's drafting after the first draft whose confidence (the
+    draft's largest softmax probability) is below tau, that draft still proposed (the Draft &
+    Verify rule the paper compares with, Sec. "Experiments", baselines): a round then drafts
+    between 1 and gamma tokens.
     """
     if gamma < 0:
         raise ValueError("gamma must be >= 0")
@@ -141,14 +155,19 @@ def ssd(dec: Decoder, prompt, visual, T: int, gamma: int, capacity: Optional[int
         g = gamma if gamma_fn is None else int(gamma_fn(l))
         # drafting stage: u_0 = pending, u_{i+1} = draft's argmax at position l+i
         u = [y]
-        drafts, dlog = [], []
+        drafts, dlog, conf = [], [], []
         for i in range(g):
             lg, _ = dec.draft_step(st, u[i], l + i, use_imitation)
             t = argmax(lg) if draft_policy is None else int(draft_policy(len(run.rounds), i, lg))
             drafts.append(t)
             dlog.append(lg)
             u.append(t)
-        # verification stage: the full decoder over u_0..u_g at positions l..l+g
+            if confidence_stop is not None:
+                conf.append(confidence(lg))
+                if conf[-1] < confidence_stop:
+                    break
+        # verification stage: the full decoder over u_0..u_n at positions l..l+n (n drafts)
+        g = len(drafts)
         targets, tlog = [], []
         for i in range(g + 1):
             lg, _ = dec.full_step(st, u[i], l + i)
@@ -163,7 +182,7 @@ def ssd(dec: Decoder, prompt, visual, T: int, gamma: int, capacity: Optional[int
                 done = (t == eos_id)
         st.seq_len = l + a + 1
         y = targets[a]
-        run.rounds.append(Round(l, u, drafts, targets, a, dlog, tlog))
+        run.rounds.append(Round(l, u, drafts, targets, a, dlog, tlog, conf))
         if poison:
             _poison(st)
     return run
@@ -173,10 +192,12 @@ def replay(dec: Decoder, prompt, visual, pending0: int, rounds, gamma: int,
            capacity: Optional[int] = None, use_imitation: bool = True):
     """Follow a device run's token stream and return the oracle's logits at every step.
 
-    ``rounds`` is a sequence of (drafts[gamma], targets[gamma+1]) produced by the device.  The
-    oracle feeds the device's tokens as inputs (u_0 = pending, u_i = device draft i), computes its
-    own draft and full logits for them, applies its own acceptance rule to the device's drafts and
-    targets, and advances exactly as the device did.  Returns (prefill logits, list of Round).
+    ``rounds`` is a sequence of (drafts[n], targets[n+1]) produced by the device (n = gamma, or
+    fewer for a round whose drafting stopped early).  The oracle feeds the device's tokens as
+    inputs (u_0 = pending, u_i = device draft i), computes its own draft and full logits for them
+    (and the confidence of each draft), applies its own acceptance rule to the device's drafts
+    and targets, and advances exactly as the device did.  Returns (prefill logits, list of
+    Round).
     """
     n_tok = sum(gamma + 1 for _ in rounds)
     capacity = capacity or (dec.shape.prefix_len() + len(prompt) + n_tok + gamma + 2)
@@ -186,12 +207,13 @@ def replay(dec: Decoder, prompt, visual, pending0: int, rounds, gamma: int,
     for drafts, targets in rounds:
         drafts = [int(t) for t in drafts]
         targets = [int(t) for t in targets]
+        n = len(drafts)
         l = st.seq_len
         u = [y] + drafts
-        dlog = [dec.draft_step(st, u[i], l + i, use_imitation)[0] for i in range(gamma)]
-        tlog = [dec.full_step(st, u[i], l + i)[0] for i in range(gamma + 1)]
+        dlog = [dec.draft_step(st, u[i], l + i, use_imitation)[0] for i in range(n)]
+        tlog = [dec.full_step(st, u[i], l + i)[0] for i in range(n + 1)]
         a = accept_length(drafts, targets)
         st.seq_len = l + a + 1
         y = targets[a]
-        out.append(Round(l, u, drafts, targets, a, dlog, tlog))
+        out.append(Round(l, u, drafts, targets, a, dlog, tlog, [confidence(lg) for lg in dlog]))
     return lg0, out

@@ -178,3 +178,56 @@ def test_dynamic_draft_length_ssd_equals_greedy(wl):
     for r in run.rounds:
         assert len(r.drafts) == fn(r.seq_len)
         assert 0 <= r.accepted <= len(r.drafts)
+
+
+def test_confidence_closed_forms():
+    # the largest softmax probability: 1/V for equal logits, 1/2 for two equal maxima far above
+    # the rest, -> 1 for one dominant logit, and invariant to a shift of every logit
+    V = 1000
+    assert decode.confidence(np.zeros(V)) == pytest.approx(1.0 / V, rel=1e-12)
+    lg = np.full(V, -800.0)
+    lg[[3, 700]] = 5.0
+    assert decode.confidence(lg) == pytest.approx(0.5, rel=1e-12)
+    lg = np.zeros(V)
+    lg[17] = 50.0
+    assert decode.confidence(lg) == pytest.approx(1.0 / (1.0 + (V - 1) * np.exp(-50.0)), rel=1e-12)
+    r = np.random.default_rng(1).standard_normal(V)
+    assert decode.confidence(r + 123.0) == pytest.approx(decode.confidence(r), rel=1e-12)
+    # brute force: the probability of the argmax under softmax computed term by term
+    e = [float(np.exp(x)) for x in r]
+    assert decode.confidence(r) == pytest.approx(max(e) / sum(e), rel=1e-12)
+
+
+@pytest.mark.parametrize("wl", SMALL, ids=lambda w: w.name)
+def test_confidence_stop_rule(wl):
+    """Threshold 0 never stops (the fixed-gamma run, bit for bit); threshold 1 stops after the
+    first draft of every round; any threshold keeps the greedy output; and in every round the
+    number of drafts is 1 + the leading drafts at or above the threshold, capped at gamma."""
+    dec, pr, z = _setup(wl, 4)
+    g = decode.greedy(dec, pr, z, wl.new_tokens)
+    fixed = decode.ssd(dec, pr, z, wl.new_tokens, wl.gamma)
+    zero = decode.ssd(dec, pr, z, wl.new_tokens, wl.gamma, confidence_stop=0.0)
+    assert zero.tokens == fixed.tokens
+    assert [r.accepted for r in zero.rounds] == [r.accepted for r in fixed.rounds]
+    for a, b in zip(zero.rounds, fixed.rounds):
+        assert a.drafts == b.drafts and len(a.confidences) == wl.gamma
+        assert all(np.array_equal(x, y) for x, y in zip(a.target_logits, b.target_logits))
+    one = decode.ssd(dec, pr, z, wl.new_tokens, wl.gamma, confidence_stop=1.0)
+    assert all(len(r.drafts) == 1 for r in one.rounds)
+    assert one.tokens == g.tokens
+    confs = sorted(c for r in zero.rounds for c in r.confidences)
+    for q in (0.2, 0.5, 0.8):
+        tau = confs[int(q * (len(confs) - 1))]
+        s = decode.ssd(dec, pr, z, wl.new_tokens, wl.gamma, confidence_stop=tau)
+        assert s.tokens == g.tokens
+        for r in s.rounds:
+            lead = 0
+            while lead < len(r.confidences) and r.confidences[lead] >= tau:
+                lead += 1
+            assert len(r.drafts) == min(wl.gamma, lead + 1) == len(r.confidences)
+            assert len(r.targets) == len(r.drafts) + 1
+            assert 0 <= r.accepted <= len(r.drafts)
+            # each recorded confidence is that of the draft logits it came with
+            for c, lg in zip(r.confidences, r.draft_logits):
+                p = np.exp(lg - lg.max())
+                assert c == pytest.approx(p.max() / p.sum(), rel=1e-12)
