@@ -235,6 +235,38 @@ int ssd_accept_sample(ssd_ctx* ctx, int B, int gamma, const int32_t* d_draft,
                       float temperature, int32_t* d_pending, int32_t* d_out,
                       int32_t* d_accept_len, const int32_t* d_active);
 
+/* Confidence-stopped drafting, the rule of Draft & Verify, the self-speculative baseline the
+ * paper compares with (Sec. "Experiments", baselines: drafting halts once the draft's confidence
+ * drops below a threshold).  The confidence of a draft is its largest softmax probability,
+ * max_v softmax(draft logits)_v (the paper's confidence C_l, appendix on the choice of n).
+ *
+ * ssd_draft_confident: ssd_draft, except that sequence b stops drafting after the first step
+ * whose confidence is below `threshold` (that step's token is still proposed), so it proposes
+ * d_ndraft[b] in [1, gamma] drafts (0 for a sequence with d_active[b] == 0; d_active may be
+ * NULL: all active).  Steps run while an active sequence still drafts: after every step but the
+ * last the stream is synchronised and the flags read back (not when threshold <= 0, where no
+ * sequence stops); *h_steps (host) receives the steps run, the largest d_ndraft.  d_draft
+ * receives [B][*h_steps] (row stride *h_steps; entries past d_ndraft[b] are the draft model's
+ * further tokens, not proposals); d_conf [B][gamma] float32 or NULL receives each step's
+ * confidence, d_draft_logits [B][gamma][V] or NULL the logits.  A following ssd_verify with
+ * gamma = *h_steps and the same d_pending / d_draft may reuse the layer-k states.
+ *
+ * ssd_accept_counts: ssd_accept with sequence b's acceptance limited to its d_ndraft[b] drafts
+ * (a[b] <= d_ndraft[b]; the emitted token at a[b] is target[b][a[b]]).
+ *
+ * ssd_generate_confident: ssd_generate (SSD_MODE_SPECULATIVE, gamma drafts at most) with
+ * confidence-stopped drafting at `threshold`; the stream is synchronised once per round and
+ * after each draft step as above; h_stats counts the drafts proposed. */
+int ssd_draft_confident(ssd_ctx* ctx, int B, int gamma, float threshold, const int32_t* d_pending,
+                        const int32_t* d_active, int32_t* d_draft, int32_t* d_ndraft,
+                        float* d_conf, float* d_draft_logits, int* h_steps);
+int ssd_accept_counts(ssd_ctx* ctx, int B, int gamma, const int32_t* d_draft,
+                      const int32_t* d_ndraft, const int32_t* d_target, int32_t* d_pending,
+                      int32_t* d_out, int32_t* d_accept_len, const int32_t* d_active);
+int ssd_generate_confident(ssd_ctx* ctx, int B, int P, const int32_t* d_prompt,
+                           const void* d_visual, int T, int gamma, float threshold,
+                           int reuse_hidden, int32_t* d_tokens, int64_t* h_stats);
+
 /* The whole loop: prefill, then rounds of draft + verify + accept (SSD_MODE_SPECULATIVE) or
  * verify(gamma = 0) + accept (SSD_MODE_GREEDY) until T tokens per sequence are emitted (the last
  * round truncated; a finished sequence's seq_len then counts only the positions it emitted, so

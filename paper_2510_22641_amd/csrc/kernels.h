@@ -219,6 +219,25 @@ hipError_t launch_cross_fold(const void* xk, const void* xv, int kvdtype, const 
 hipError_t launch_row_stats(const float* x, int ldx, int M, int K, int norm, float eps,
                             float2* stats, hipStream_t s);
 
+// Confidence-stopped drafting, evaluated by the final argmax of draft step `step` (row m =
+// sequence m): conf = the row's largest softmax probability, 1 / sum_n exp(logits[n] - max),
+// from its logits (logits + m * ldl, V of them), stored at conf[m * ldc + step] when conf is set.
+// Step 0 sets ndraft[m] = 1 and drafting[m] = (conf >= tau) for an active sequence (0 and 0 for
+// an inactive one); a later step counts itself in ndraft[m] = step + 1 and updates drafting[m]
+// only while drafting[m] is set.  logits == null: off.
+struct ConfArgs {
+  const float* logits = nullptr;
+  int ldl = 0;
+  int V = 0;
+  float* conf = nullptr;
+  int ldc = 0;
+  int step = 0;
+  float tau = 0.f;
+  int32_t* drafting = nullptr;
+  int32_t* ndraft = nullptr;
+  const int32_t* active = nullptr;
+};
+
 // Final argmax over partials: tok = argmax; written to dst0[row_map(m)] and dst1[m] if set.
 // Row m = b*C + j maps to dst0[b*ld0 + off0 + j].
 hipError_t launch_argmax_final(const float* part_val, const int* part_idx, int M, int n_parts,
@@ -229,6 +248,17 @@ hipError_t launch_argmax_final_embed(const float* part_val, const int* part_idx,
                                      int n_parts, int C, int32_t* dst0, int ld0, int off0,
                                      int32_t* dst1, const void* embed, int wdtype, int d,
                                      float* x_out, hipStream_t s);
+
+// The general form: the chosen token's embedding row into x_out when embed is set, and the
+// confidence bookkeeping when cf.logits is set.
+hipError_t launch_argmax_final_ex(const float* part_val, const int* part_idx, int M, int n_parts,
+                                  int C, int32_t* dst0, int ld0, int off0, int32_t* dst1,
+                                  const void* embed, int wdtype, int d, float* x_out,
+                                  const ConfArgs& cf, hipStream_t s);
+
+// dst[b * ld_dst + j] = src[b * ld_src + j] for b < B, j < n (token rows).
+hipError_t launch_copy_tokens(int32_t* dst, int ld_dst, const int32_t* src, int ld_src, int B,
+                              int n, hipStream_t s);
 
 // Cross-attention K or V at prefill: src [B*Nv][H*dh] float32 -> dst [B][H][Nv][dh] kvdtype.
 hipError_t launch_scatter_cross(const float* src, void* dst, int B, int Nv, int H, int dh,
@@ -252,6 +282,7 @@ struct AcceptArgs {
   int32_t* out;           // [B][gamma+1] or null
   int32_t* accept_len;    // [B] or null
   const int32_t* active;  // [B] or null
+  const int32_t* ndraft;  // [B] or null: drafts proposed by sequence b this round (<= gamma)
   int32_t* seq_len;
   int max_seq;
   int next_need;          // positions a following round needs beyond seq_len (0: none known)

@@ -79,11 +79,13 @@ template <typename WT>
 __global__ __launch_bounds__(256) void argmax_final_kernel(const float* pv, const int* pi, int M,
                                                            int n_parts, int C, int32_t* dst0,
                                                            int ld0, int off0, int32_t* dst1,
-                                                           const WT* embed, int d, float* x_out) {
+                                                           const WT* embed, int d, float* x_out,
+                                                           const ConfArgs cf) {
   constexpr int PER = 16;  // partials per thread requested together
   __shared__ float sv[4];
   __shared__ int si[4];
   __shared__ int tok;
+  __shared__ float vmax;
   const int m = blockIdx.x;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   float v = -INFINITY;
@@ -110,12 +112,47 @@ __global__ __launch_bounds__(256) void argmax_final_kernel(const float* pv, cons
     dst0[(size_t)b * ld0 + off0 + j] = i;
     if (dst1) dst1[m] = i;
     tok = i;
+    vmax = v;
+  }
+  if (cf.logits) {
+    // confidence: 1 / sum_n exp(logit_n - max) over the row
+    __syncthreads();
+    const float mx = vmax;
+    const float* row = cf.logits + (size_t)m * cf.ldl;
+    float s = 0.f;
+    for (int n = threadIdx.x; n < cf.V; n += blockDim.x) s += expf(row[n] - mx);
+    s = wave_sum(s);
+    __syncthreads();
+    if (lane == 0) sv[wave] = s;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      float tot = 0.f;
+      for (int w = 0; w < (int)(blockDim.x >> 6); ++w) tot += sv[w];
+      const float conf = 1.0f / tot;
+      if (cf.conf) cf.conf[(size_t)m * cf.ldc + cf.step] = conf;
+      const bool act = !cf.active || cf.active[m] != 0;
+      if (cf.step == 0) {
+        cf.ndraft[m] = act ? 1 : 0;
+        cf.drafting[m] = (act && conf >= cf.tau) ? 1 : 0;
+      } else if (cf.drafting[m]) {
+        cf.ndraft[m] = cf.step + 1;
+        cf.drafting[m] = conf >= cf.tau ? 1 : 0;
+      }
+    }
   }
   if (!x_out) return;
   // the chosen token's embedding row, the next draft step's input (row m of x_out)
   __syncthreads();
   const WT* src = embed + (size_t)tok * d;
   for (int k = threadIdx.x; k < d; k += blockDim.x) x_out[(size_t)m * d + k] = load_elem(src + k);
+}
+
+__global__ void copy_tokens_kernel(int32_t* dst, int ld_dst, const int32_t* src, int ld_src,
+                                   int B, int n) {
+  const int e = blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= B * n) return;
+  const int b = e / n, j = e - b * n;
+  dst[(size_t)b * ld_dst + j] = src[(size_t)b * ld_src + j];
 }
 
 template <typename KT>
@@ -153,6 +190,7 @@ __global__ void accept_kernel(const AcceptArgs a) {
   __shared__ int act_after[256];
   __shared__ int len_after[256];
   __shared__ int need_after[256];
+  __shared__ int prop_n[256];
   const int b = threadIdx.x;
   const int g = a.gamma;
   int n = 0;
@@ -165,7 +203,9 @@ __global__ void accept_kernel(const AcceptArgs a) {
       did = true;
       const int32_t* dr = a.draft + (size_t)b * g;
       const int32_t* tg = a.target + (size_t)b * (g + 1);
-      while (n < g && dr[n] == tg[n]) ++n;
+      // drafts this sequence proposed this round (confidence-stopped drafting: fewer than g)
+      const int gb = a.ndraft ? max(0, min(g, a.ndraft[b])) : g;
+      while (n < gb && dr[n] == tg[n]) ++n;
       if (a.out) {
         int32_t* o = a.out + (size_t)b * (g + 1);
         for (int i = 0; i < n; ++i) o[i] = dr[i];
@@ -196,6 +236,7 @@ __global__ void accept_kernel(const AcceptArgs a) {
     }
   }
   acc_n[b] = did ? n : -1;
+  prop_n[b] = did ? (a.ndraft ? max(0, min(g, a.ndraft[b])) : g) : 0;
   act_after[b] = still;
   len_after[b] = (b < a.B && still) ? a.seq_len[b] : INT_MAX;
   need_after[b] = (b < a.B && still && a.tokens) ? a.T - a.count[b] : 0;
@@ -204,7 +245,7 @@ __global__ void accept_kernel(const AcceptArgs a) {
     long long sa = 0, sd = 0;
     int na = 0, lmin = INT_MAX, need = 0;
     for (int t = 0; t < a.B && t < 256; ++t) {
-      if (acc_n[t] >= 0) { sa += acc_n[t]; sd += g; }
+      if (acc_n[t] >= 0) { sa += acc_n[t]; sd += prop_n[t]; }
       na += act_after[t];
       lmin = min(lmin, len_after[t]);
       need = max(need, need_after[t]);
@@ -272,29 +313,45 @@ hipError_t launch_rope_scatter(const RopeScatterArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
+hipError_t launch_argmax_final_ex(const float* part_val, const int* part_idx, int M, int n_parts,
+                                  int C, int32_t* dst0, int ld0, int off0, int32_t* dst1,
+                                  const void* embed, int wdtype, int d, float* x_out,
+                                  const ConfArgs& cf, hipStream_t s) {
+  if (M <= 0) return hipSuccess;
+  if (x_out && (!embed || d < 1)) return hipErrorInvalidValue;
+  if (cf.logits && (!cf.drafting || !cf.ndraft || cf.V < 1)) return hipErrorInvalidValue;
+  if (x_out && wdtype == 1)
+    hipLaunchKernelGGL(argmax_final_kernel<bf16_t>, dim3(M), dim3(256), 0, s, part_val, part_idx,
+                       M, n_parts, C, dst0, ld0, off0, dst1,
+                       reinterpret_cast<const bf16_t*>(embed), d, x_out, cf);
+  else
+    hipLaunchKernelGGL(argmax_final_kernel<float>, dim3(M), dim3(256), 0, s, part_val, part_idx,
+                       M, n_parts, C, dst0, ld0, off0, dst1,
+                       x_out ? reinterpret_cast<const float*>(embed) : nullptr, d, x_out, cf);
+  return hipGetLastError();
+}
+
 hipError_t launch_argmax_final(const float* part_val, const int* part_idx, int M, int n_parts,
                                int C, int32_t* dst0, int ld0, int off0, int32_t* dst1,
                                hipStream_t s) {
-  if (M <= 0) return hipSuccess;
-  hipLaunchKernelGGL(argmax_final_kernel<float>, dim3(M), dim3(256), 0, s, part_val, part_idx, M,
-                     n_parts, C, dst0, ld0, off0, dst1, nullptr, 0, nullptr);
-  return hipGetLastError();
+  return launch_argmax_final_ex(part_val, part_idx, M, n_parts, C, dst0, ld0, off0, dst1,
+                                nullptr, 0, 0, nullptr, ConfArgs(), s);
 }
 
 hipError_t launch_argmax_final_embed(const float* part_val, const int* part_idx, int M,
                                      int n_parts, int C, int32_t* dst0, int ld0, int off0,
                                      int32_t* dst1, const void* embed, int wdtype, int d,
                                      float* x_out, hipStream_t s) {
-  if (M <= 0) return hipSuccess;
   if (!embed || !x_out || d < 1) return hipErrorInvalidValue;
-  if (wdtype == 1)
-    hipLaunchKernelGGL(argmax_final_kernel<bf16_t>, dim3(M), dim3(256), 0, s, part_val, part_idx,
-                       M, n_parts, C, dst0, ld0, off0, dst1,
-                       reinterpret_cast<const bf16_t*>(embed), d, x_out);
-  else
-    hipLaunchKernelGGL(argmax_final_kernel<float>, dim3(M), dim3(256), 0, s, part_val, part_idx,
-                       M, n_parts, C, dst0, ld0, off0, dst1,
-                       reinterpret_cast<const float*>(embed), d, x_out);
+  return launch_argmax_final_ex(part_val, part_idx, M, n_parts, C, dst0, ld0, off0, dst1, embed,
+                                wdtype, d, x_out, ConfArgs(), s);
+}
+
+hipError_t launch_copy_tokens(int32_t* dst, int ld_dst, const int32_t* src, int ld_src, int B,
+                              int n, hipStream_t s) {
+  if (B * n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(copy_tokens_kernel, dim3((B * n + 255) / 256), dim3(256), 0, s, dst, ld_dst,
+                     src, ld_src, B, n);
   return hipGetLastError();
 }
 

@@ -36,7 +36,8 @@ struct Layout {
   size_t x, x1, qkv, q, attn, ffn, inh, xi, stash, vis, part_val, part_idx, stats, bias_tab,
       p_x, p_attn, p_ffn, ssq, attn_part, fold_q, fold_o,
       bucket, rope_cos, rope_sin, status, cur_tok, g_pending, g_draft, g_target,
-      g_count, g_active, g_nactive, g_stats, gplanes, total;
+      g_count, g_active, g_nactive, g_stats, g_ndraft, g_drafting, g_draft_w, conf_lg, gplanes,
+      total;
   int rows_max, head_rows, parts_max, ctx_max, plane_rows, attn_rows;
   int gplane_rows = 0, gplane_ld = 0;  // tile-path input planes (0 rows: none)
   bool fold = false;  // the folded cross-attention matrices are carved (fold_q, fold_o)
@@ -131,6 +132,12 @@ bool make_layout(const ssd_dims& d, Layout& L, bool allow_fold = true) {
   L.g_active = take(B * 4);
   L.g_nactive = take(16);
   L.g_stats = take(3 * 8);
+  // confidence-stopped drafting: per-sequence draft counts and flags, the drafts at row stride
+  // max_gamma, and a logits row per sequence for the confidence
+  L.g_ndraft = take(B * 4);
+  L.g_drafting = take(B * 4);
+  L.g_draft_w = take(B * (G > 0 ? G : 1) * 4);
+  L.conf_lg = take(B * (size_t)d.vocab * 4);
   L.total = off;
   return true;
 }
@@ -164,9 +171,11 @@ bool dims_ok(const ssd_dims* d) {
 struct GraphKey {
   int kind, B, gamma, reuse;
   const void *p0, *p1, *p2, *p3;
+  int i0 = 0, i1 = 0;
+  const void *p4 = nullptr, *p5 = nullptr;
   bool operator<(const GraphKey& o) const {
-    return std::tie(kind, B, gamma, reuse, p0, p1, p2, p3) <
-           std::tie(o.kind, o.B, o.gamma, o.reuse, o.p0, o.p1, o.p2, o.p3);
+    return std::tie(kind, B, gamma, reuse, p0, p1, p2, p3, i0, i1, p4, p5) <
+           std::tie(o.kind, o.B, o.gamma, o.reuse, o.p0, o.p1, o.p2, o.p3, o.i0, o.i1, o.p4, o.p5);
   }
 };
 
@@ -180,7 +189,8 @@ struct ssd_ctx {
   hipStream_t stream;
   char* ws;
   Layout L;
-  int32_t* h_status = nullptr;  // pinned [4]: ssd_generate's read-back of the active counts
+  int32_t* h_status = nullptr;  // pinned [4 + 256]: ssd_generate's read-back of the active counts,
+                                // then the drafting flags of confidence-stopped drafting
   bool is_static = false;       // made by ssd_create_static: workspace = the device's scratch
   int static_dev = -1;
   bool prefilled = false;
@@ -410,7 +420,8 @@ int run_layers(ssd_ctx* c, float* x, int B, int C, int pos_off, int l0, int l1, 
 // input, written by the final argmax.
 int run_head(ssd_ctx* c, const float* x, int ldx, int M, int C, float* logits, int ldl,
              int32_t* dst0, int ld0, int off0, int32_t* dst1, const float* u = nullptr,
-             int ldu = 0, int uoff = 0, float tau = 0.f, float* embed_out = nullptr) {
+             int ldu = 0, int uoff = 0, float tau = 0.f, float* embed_out = nullptr,
+             const ConfArgs* cf = nullptr) {
   const ssd_dims& d = c->d;
   LinearArgs a = lin(c);
   a.x = x; a.ldx = ldx; a.M = M; a.K = d.d_model;
@@ -437,9 +448,10 @@ int run_head(ssd_ctx* c, const float* x, int ldx, int M, int C, float* logits, i
                                dst1, c->stream));
     return SSD_OK;
   }
-  if (embed_out) {
-    HIP_TRY(launch_argmax_final_embed(a.part_val, a.part_idx, M, n_parts, C, dst0, ld0, off0, dst1,
-                                      c->w.embed, d.wdtype, d.d_model, embed_out, c->stream));
+  if (embed_out || cf) {
+    HIP_TRY(launch_argmax_final_ex(a.part_val, a.part_idx, M, n_parts, C, dst0, ld0, off0, dst1,
+                                   c->w.embed, d.wdtype, d.d_model, embed_out,
+                                   cf ? *cf : ConfArgs(), c->stream));
     return SSD_OK;
   }
   HIP_TRY(launch_argmax_final(a.part_val, a.part_idx, M, n_parts, C, dst0, ld0, off0, dst1,
@@ -511,6 +523,48 @@ int draft_launches(ssd_ctx* c, int B, int gamma, const int32_t* pending, int32_t
     if (rc) return rc;
   }
   return SSD_OK;
+}
+
+// Draft step i of confidence-stopped drafting (B sequences): the token of step i - 1 (or
+// `pending`) at positions seq_len + i through layers 1..k (stash row i), the imitation network
+// and g, with the logits kept (the caller's [B][gamma][V] when given, else a workspace row per
+// sequence) for the confidence; the final argmax writes the draft to dwork[b][i] (row stride
+// gamma), updates ndraft / drafting, and gathers step i + 1's embedding rows.
+int draft_conf_step(ssd_ctx* c, int B, int gamma, int i, float tau, const int32_t* pending,
+                    const int32_t* active, int32_t* dwork, float* logits, float* conf) {
+  const ssd_dims& d = c->d;
+  const int D = d.d_model;
+  float* x = c->at<float>(c->L.x);
+  float* stash = c->at<float>(c->L.stash);
+  int32_t* cur = c->at<int32_t>(c->L.cur_tok);
+  const int ld_stash = (d.max_gamma + 1) * D;
+  if (i == 0) {
+    EmbedArgs e;
+    e.x = x; e.B = B; e.C = 1; e.d = D; e.embed = c->w.embed; e.vocab = d.vocab;
+    e.wdtype = d.wdtype; e.t0 = nullptr; e.t1 = pending; e.ld1 = 1;
+    e.visual = nullptr; e.n_visual = d.n_visual; e.n_prefix = 0;
+    e.status = c->at<int32_t>(c->L.status);
+    HIP_TRY(launch_embed(e, c->stream));
+  }
+  int rc = run_layers(c, x, B, 1, i, 0, d.draft_layers, d.draft_layers - 1,
+                      stash + (size_t)i * D, ld_stash);
+  if (rc) return rc;
+  rc = run_imitation(c, x, B, []() { return hipSuccess; });
+  if (rc) return rc;
+  ConfArgs cf;
+  float* lg = logits ? logits + (size_t)i * d.vocab : c->at<float>(c->L.conf_lg);
+  cf.logits = lg;
+  cf.ldl = logits ? gamma * d.vocab : d.vocab;
+  cf.V = d.vocab;
+  cf.conf = conf;
+  cf.ldc = gamma;
+  cf.step = i;
+  cf.tau = tau;
+  cf.drafting = c->at<int32_t>(c->L.g_drafting);
+  cf.ndraft = c->at<int32_t>(c->L.g_ndraft);
+  cf.active = active;
+  return run_head(c, c->at<float>(c->L.xi), D, B, 1, lg, cf.ldl, dwork, gamma, i, cur, nullptr, 0,
+                  0, 0.f, i + 1 < gamma ? x : nullptr, &cf);
 }
 
 // Verify with the layer-k reuse, first part: layers 1..k for the last position only (into x1);
@@ -591,6 +645,41 @@ int launch_maybe_graph(ssd_ctx* c, const GraphKey& key, F fn) {
     it = c->graphs.emplace(key, ex).first;
   }
   HIP_TRY(hipGraphLaunch(it->second, c->stream));
+  return SSD_OK;
+}
+
+// Up to gamma confidence-stopped draft steps; after each step but the last, the drafting flags
+// are read back (unless tau <= 0, where no sequence stops) and the steps end once no active
+// sequence drafts.  The drafts of the steps run go to d_draft[b][0..steps) (row stride steps).
+// Returns the steps run in *steps.
+int draft_confident(ssd_ctx* c, int B, int gamma, float tau, const int32_t* pending,
+                    const int32_t* active, int32_t* d_draft, float* logits, float* conf,
+                    int* steps) {
+  int32_t* dwork = c->at<int32_t>(c->L.g_draft_w);
+  int32_t* drafting = c->at<int32_t>(c->L.g_drafting);
+  int tbits = 0;
+  std::memcpy(&tbits, &tau, sizeof(tbits));
+  int n = 0;
+  for (int i = 0; i < gamma; ++i) {
+    GraphKey key{8, B, gamma, i, pending, active, logits, conf};
+    key.i0 = tbits;
+    int rc = launch_maybe_graph(c, key, [&]() {
+      return draft_conf_step(c, B, gamma, i, tau, pending, active, dwork, logits, conf);
+    });
+    if (rc) return rc;
+    n = i + 1;
+    if (i + 1 < gamma && tau > 0.f) {
+      int32_t local[256];
+      int32_t* h = c->h_status ? c->h_status + 4 : local;
+      HIP_TRY(hipMemcpyAsync(h, drafting, (size_t)B * 4, hipMemcpyDeviceToHost, c->stream));
+      HIP_TRY(hipStreamSynchronize(c->stream));
+      bool any = false;
+      for (int b = 0; b < B; ++b) any = any || h[b] != 0;
+      if (!any) break;
+    }
+  }
+  HIP_TRY(launch_copy_tokens(d_draft, n, dwork, gamma, B, n, c->stream));
+  *steps = n;
   return SSD_OK;
 }
 
@@ -729,7 +818,7 @@ int ssd_create(const ssd_dims* dims, const ssd_weights* w, const ssd_kv* kv, voi
   rc = init_ctx(c, *dims, w, kv, reinterpret_cast<char*>(d_workspace), L, stream);
   // ssd_generate's per-batch read-back lands in pinned host memory (pageable if unavailable)
   if (rc == SSD_OK &&
-      hipHostMalloc(reinterpret_cast<void**>(&c->h_status), 16, hipHostMallocDefault) != hipSuccess) {
+      hipHostMalloc(reinterpret_cast<void**>(&c->h_status), 16 + 4 * 256, hipHostMallocDefault) != hipSuccess) {
     c->h_status = nullptr;
     (void)hipGetLastError();
   }
@@ -933,6 +1022,107 @@ int ssd_accept(ssd_ctx* c, int B, int gamma, const int32_t* d_draft, const int32
   a.status = c->at<int32_t>(c->L.status);
   HIP_TRY(launch_accept(a, c->stream));
   c->draft_valid = false;
+  return SSD_OK;
+}
+
+int ssd_draft_confident(ssd_ctx* c, int B, int gamma, float threshold, const int32_t* d_pending,
+                        const int32_t* d_active, int32_t* d_draft, int32_t* d_ndraft,
+                        float* d_conf, float* d_draft_logits, int* h_steps) {
+  if (!c || !d_pending || !d_draft || !d_ndraft || !h_steps) return SSD_ERR_ARG;
+  if (!std::isfinite(threshold)) return SSD_ERR_ARG;
+  if (B < 1 || B > c->d.max_batch || gamma < 1 || gamma > c->d.max_gamma) return SSD_ERR_SHAPE;
+  if (!c->prefilled) return SSD_ERR_STATE;
+  c->draft_valid = false;
+  int steps = 0;
+  int rc = draft_confident(c, B, gamma, threshold, d_pending, d_active, d_draft, d_draft_logits,
+                           d_conf, &steps);
+  if (rc) return rc;
+  HIP_TRY(hipMemcpyAsync(d_ndraft, c->at<int32_t>(c->L.g_ndraft), (size_t)B * 4,
+                         hipMemcpyDeviceToDevice, c->stream));
+  *h_steps = steps;
+  c->draft_valid = true;
+  c->draft_B = B;
+  c->draft_gamma = steps;
+  c->draft_pending = d_pending;
+  c->draft_out = d_draft;
+  return SSD_OK;
+}
+
+int ssd_accept_counts(ssd_ctx* c, int B, int gamma, const int32_t* d_draft,
+                      const int32_t* d_ndraft, const int32_t* d_target, int32_t* d_pending,
+                      int32_t* d_out, int32_t* d_accept_len, const int32_t* d_active) {
+  if (!c || !d_target || !d_pending || !d_ndraft || (gamma > 0 && !d_draft)) return SSD_ERR_ARG;
+  if (B < 1 || B > c->d.max_batch || gamma < 0 || gamma > c->d.max_gamma) return SSD_ERR_SHAPE;
+  if (!c->prefilled) return SSD_ERR_STATE;
+  AcceptArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.B = B; a.gamma = gamma; a.draft = d_draft; a.target = d_target; a.pending = d_pending;
+  a.out = d_out; a.accept_len = d_accept_len; a.active = d_active; a.ndraft = d_ndraft;
+  a.seq_len = c->kv.seq_len; a.max_seq = c->d.max_seq; a.next_need = 0;
+  a.status = c->at<int32_t>(c->L.status);
+  HIP_TRY(launch_accept(a, c->stream));
+  c->draft_valid = false;
+  return SSD_OK;
+}
+
+int ssd_generate_confident(ssd_ctx* c, int B, int P, const int32_t* d_prompt,
+                           const void* d_visual, int T, int gamma, float threshold,
+                           int reuse_hidden, int32_t* d_tokens, int64_t* h_stats) {
+  if (!c || !d_tokens || T < 1 || !std::isfinite(threshold)) return SSD_ERR_ARG;
+  if (gamma < 1 || gamma > c->d.max_gamma) return SSD_ERR_SHAPE;
+  if (B < 1 || B > c->d.max_batch) return SSD_ERR_SHAPE;
+  const int Cx = P + (c->d.arch == SSD_ARCH_T5 ? 0 : c->d.n_visual);
+  if (Cx + T + c->d.max_gamma > c->d.max_seq) return SSD_ERR_CAPACITY;
+  int32_t* pending = c->at<int32_t>(c->L.g_pending);
+  int32_t* draft = c->at<int32_t>(c->L.g_draft);
+  int32_t* target = c->at<int32_t>(c->L.g_target);
+  int32_t* count = c->at<int32_t>(c->L.g_count);
+  int32_t* active = c->at<int32_t>(c->L.g_active);
+  int32_t* n_active = c->at<int32_t>(c->L.g_nactive);
+  int64_t* stats = c->at<int64_t>(c->L.g_stats);
+  int rc = ssd_prefill(c, B, P, d_prompt, d_visual, pending, nullptr);
+  if (rc) return rc;
+  GenInitArgs gi{B, T, pending, d_tokens, count, active, stats, n_active, c->kv.seq_len,
+                 c->at<int32_t>(c->L.status)};
+  HIP_TRY(launch_gen_init(gi, c->stream));
+  AcceptArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.B = B; a.target = target; a.pending = pending; a.draft = draft;
+  a.ndraft = c->at<int32_t>(c->L.g_ndraft);
+  a.seq_len = c->kv.seq_len; a.max_seq = c->d.max_seq; a.next_need = gamma + 1;
+  a.status = c->at<int32_t>(c->L.status);
+  a.tokens = d_tokens; a.count = count; a.active_rw = active; a.T = T; a.stats = stats;
+  a.n_active = n_active;
+  int32_t h_active[4] = {0, 0, 0, 0};
+  for (int round = 0; round < T; ++round) {
+    int32_t* dst = c->h_status ? c->h_status : h_active;
+    HIP_TRY(hipMemcpyAsync(dst, n_active, 16, hipMemcpyDeviceToHost, c->stream));
+    HIP_TRY(hipStreamSynchronize(c->stream));
+    if (dst != h_active) std::memcpy(h_active, dst, 16);
+    if (h_active[2] != 0) return SSD_ERR_DEVICE;
+    if (h_active[0] == 0) break;
+    int steps = 0;
+    rc = draft_confident(c, B, gamma, threshold, pending, active, draft, nullptr, nullptr, &steps);
+    if (rc) return rc;
+    c->draft_valid = true;
+    c->draft_B = B;
+    c->draft_gamma = steps;
+    c->draft_pending = pending;
+    c->draft_out = draft;
+    rc = ssd_verify(c, B, steps, pending, draft, reuse_hidden, target, nullptr);
+    if (rc) return rc;
+    a.gamma = steps;
+    HIP_TRY(launch_accept(a, c->stream));
+    c->draft_valid = false;
+  }
+  {
+    int32_t* dst = c->h_status ? c->h_status : h_active;
+    HIP_TRY(hipMemcpyAsync(dst, n_active, 16, hipMemcpyDeviceToHost, c->stream));
+    if (h_stats) HIP_TRY(hipMemcpyAsync(h_stats, stats, 24, hipMemcpyDeviceToHost, c->stream));
+    HIP_TRY(hipStreamSynchronize(c->stream));
+    if (dst != h_active) std::memcpy(h_active, dst, 16);
+    if (h_active[2] != 0) return SSD_ERR_DEVICE;
+  }
   return SSD_OK;
 }
 

@@ -220,6 +220,35 @@ class DeviceDecoder:
         self._call(abi.ssd_accept, self.ctx, B, gamma, draft, target, pending, out, alen, active)
         return out, alen
 
+    def draft_confident(self, pending: torch.Tensor, gamma: int, threshold: float, active=None,
+                        logits: bool = False):
+        """Confidence-stopped drafting; returns (draft [B, steps], ndraft [B], conf [B, gamma],
+        draft logits [B, gamma, V] or None, steps)."""
+        B = pending.shape[0]
+        d = self.buf("draft_conf", (B * gamma,))
+        nd = self.buf("ndraft", (B,))
+        cf = self.buf("conf", (B, gamma), torch.float32)
+        lg = self.buf("draft_logits", (B, gamma, self.shape.vocab), torch.float32) if logits else None
+        steps = self._call(abi.ssd_draft_confident, self.ctx, B, gamma, threshold, pending, active,
+                           d, nd, cf, lg)
+        return d[:B * steps].view(B, steps), nd, cf, lg, steps
+
+    def accept_counts(self, draft, ndraft, target, pending, gamma: int, active=None):
+        B = pending.shape[0]
+        out = self.buf("accept_out", (B, gamma + 1))
+        alen = self.buf("accept_len", (B,))
+        self._call(abi.ssd_accept_counts, self.ctx, B, gamma, draft, ndraft, target, pending, out,
+                   alen, active)
+        return out, alen
+
+    def generate_confident(self, prompt, visual, T: int, gamma: int, threshold: float,
+                           reuse: bool = True):
+        B, P = prompt.shape
+        tokens = self.ivec(B, T)
+        stats = self._call(abi.ssd_generate_confident, self.ctx, B, P, prompt, visual, T, gamma,
+                           threshold, reuse, tokens)
+        return tokens, stats
+
     def draft_sample(self, pending: torch.Tensor, gamma: int, u: torch.Tensor, temperature: float):
         """Sampled drafts (u [B, gamma] float32 uniforms); returns (draft, draft logits)."""
         B = pending.shape[0]

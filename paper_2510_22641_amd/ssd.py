@@ -77,6 +77,11 @@ def _load():
         "ssd_accept_sample": (c_int, [P, c_int, c_int, P, P, P, P, ctypes.c_float, P, P, P, P]),
         "ssd_generate": (c_int, [P, c_int, c_int, P, P, c_int, c_int, c_int, c_int, P,
                                  POINTER(c_int64)]),
+        "ssd_draft_confident": (c_int, [P, c_int, c_int, ctypes.c_float, P, P, P, P, P, P,
+                                        POINTER(c_int)]),
+        "ssd_accept_counts": (c_int, [P, c_int, c_int, P, P, P, P, P, P, P]),
+        "ssd_generate_confident": (c_int, [P, c_int, c_int, P, P, c_int, c_int, ctypes.c_float,
+                                           c_int, P, POINTER(c_int64)]),
         "ssd_dynamic_gamma": (c_int, [c_int, c_int, c_int]),
         "ssd_set_graphs": (c_int, [P, c_int]),
         "ssd_set_hidden_export": (c_int, [P, P, P, P]),
@@ -96,7 +101,8 @@ def _load():
 
 _lib = _load()
 EXPORTS = ("ssd_workspace_bytes", "ssd_create", "ssd_create_static", "ssd_prefill", "ssd_draft", "ssd_verify",
-           "ssd_accept", "ssd_draft_sample", "ssd_accept_sample", "ssd_generate", "ssd_dynamic_gamma", "ssd_set_graphs", "ssd_set_hidden_export",
+           "ssd_accept", "ssd_draft_sample", "ssd_accept_sample", "ssd_generate", "ssd_draft_confident", "ssd_accept_counts",
+           "ssd_generate_confident", "ssd_dynamic_gamma", "ssd_set_graphs", "ssd_set_hidden_export",
            "ssd_profile_enable",
            "ssd_profile_read", "ssd_sync_status",
            "ssd_status_string", "ssd_destroy")
@@ -185,6 +191,32 @@ def ssd_generate(ctx, B, P, d_prompt, d_visual, T, gamma, mode, reuse_hidden, d_
     stats = (c_int64 * 3)()
     _check("ssd_generate", _lib.ssd_generate(ctx, B, P, _p(d_prompt), _p(d_visual), T, gamma,
                                              mode, int(reuse_hidden), _p(d_tokens), stats))
+    return {"rounds": int(stats[0]), "accepted": int(stats[1]), "drafted": int(stats[2])}
+
+
+def ssd_draft_confident(ctx, B, gamma, threshold, d_pending, d_active, d_draft, d_ndraft,
+                        d_conf=None, d_draft_logits=None) -> int:
+    """Confidence-stopped drafting; returns the draft steps run."""
+    steps = c_int(0)
+    _check("ssd_draft_confident", _lib.ssd_draft_confident(
+        ctx, B, gamma, float(threshold), _p(d_pending), _p(d_active), _p(d_draft), _p(d_ndraft),
+        _p(d_conf), _p(d_draft_logits), ctypes.byref(steps)))
+    return int(steps.value)
+
+
+def ssd_accept_counts(ctx, B, gamma, d_draft, d_ndraft, d_target, d_pending, d_out=None,
+                      d_accept_len=None, d_active=None):
+    _check("ssd_accept_counts", _lib.ssd_accept_counts(
+        ctx, B, gamma, _p(d_draft), _p(d_ndraft), _p(d_target), _p(d_pending), _p(d_out),
+        _p(d_accept_len), _p(d_active)))
+
+
+def ssd_generate_confident(ctx, B, P, d_prompt, d_visual, T, gamma, threshold, reuse_hidden,
+                           d_tokens):
+    stats = (c_int64 * 3)()
+    _check("ssd_generate_confident", _lib.ssd_generate_confident(
+        ctx, B, P, _p(d_prompt), _p(d_visual), T, gamma, float(threshold), int(reuse_hidden),
+        _p(d_tokens), stats))
     return {"rounds": int(stats[0]), "accepted": int(stats[1]), "drafted": int(stats[2])}
 
 

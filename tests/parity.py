@@ -171,6 +171,92 @@ def check_streams_agree_until_near_tie(dec: Decoder, shape, prompt, visual, a, b
     return first
 
 
+# ---- confidence-stopped drafting ------------------------------------------------------------
+
+@dataclass
+class ConfDevRound:
+    steps: int                # draft steps the device ran
+    drafts: np.ndarray        # [B, steps]
+    ndraft: np.ndarray        # [B] drafts proposed
+    conf: np.ndarray          # [B, steps] device confidences
+    targets: np.ndarray       # [B, steps + 1]
+    accepted: np.ndarray      # [B]
+    active: np.ndarray        # [B]
+    draft_logits: np.ndarray  # [B, steps, V]
+    target_logits: np.ndarray  # [B, steps + 1, V]
+
+
+def device_run_confident(dd, prompt_t, visual_t, T: int, gamma: int, tau: float,
+                         reuse: bool = True):
+    """Stepwise confidence-stopped decoding through the C ABI (ssd_draft_confident, ssd_verify,
+    ssd_accept_counts); returns (pending0, prefill logits, rounds, tokens per sequence)."""
+    import torch
+    B = prompt_t.shape[0]
+    pending, lg0 = dd.prefill(prompt_t, visual_t, logits=True)
+    pend0, lg0 = pending.cpu().numpy().copy(), lg0.cpu().numpy().copy()
+    tokens = [[int(t)] for t in pend0]
+    active = dd.buf("active_mask", (B,))
+    rounds = []
+    for _ in range(T):
+        act = np.array([len(t) < T for t in tokens])
+        if not act.any():
+            break
+        active.copy_(torch.from_numpy(act.astype(np.int32)))
+        d, nd, cf, dl, steps = dd.draft_confident(pending, gamma, tau, active, logits=True)
+        t, tl = dd.verify(pending, d, steps, reuse=reuse, logits=True)
+        out, alen = dd.accept_counts(d, nd, t, pending, steps, active)
+        r = ConfDevRound(steps, d.cpu().numpy().copy(), nd.cpu().numpy().copy(),
+                         cf.cpu().numpy()[:, :steps].copy(), t.cpu().numpy().copy(),
+                         alen.cpu().numpy().copy(), act, dl.cpu().numpy()[:, :steps].copy(),
+                         tl.cpu().numpy().copy())
+        rounds.append(r)
+        o = out.cpu().numpy()
+        for b in range(B):
+            if act[b]:
+                tokens[b].extend(int(x) for x in o[b, : r.accepted[b] + 1])
+    return pend0, lg0, rounds, [t[:T] for t in tokens]
+
+
+def check_confident_run(dec: Decoder, shape, prompt, visual, pend0, lg0, rounds, b: int,
+                        gamma: int, tau: float) -> int:
+    """Replay sequence b of a confidence-stopped device run through the oracle.  Logits within
+    the usual tolerance; each device confidence within the band that the logit tolerance allows
+    (log-confidence moves by at most twice the largest logit error); every stop decision the
+    device took on its own confidence, and the oracle's on its own except within that band; the
+    accepted length bit-exact.  Returns the count of decisions taken inside the band."""
+    mine = [r for r in rounds if r.active[b]]
+    orounds_in = [(r.drafts[b, :r.ndraft[b]], r.targets[b, :r.ndraft[b] + 1]) for r in mine]
+    o0, orounds = decode.replay(dec, prompt, visual, int(pend0[b]), orounds_in, gamma)
+    check_logits(lg0[b], o0, shape, f"seq {b} prefill logits")
+    near = 0
+    for k, (r, o) in enumerate(zip(mine, orounds)):
+        n = int(r.ndraft[b])
+        assert 1 <= n <= min(gamma, r.steps), f"seq {b} round {k}: {n} drafts of {r.steps} steps"
+        for i in range(n):
+            check_logits(r.draft_logits[b, i], o.draft_logits[i], shape, f"seq {b} r{k} draft {i}")
+            check_token(r.drafts[b, i], o.draft_logits[i], shape, f"seq {b} r{k} draft {i}")
+            band = 2.0 * tolerance(shape, o.draft_logits[i])
+            dc, oc = float(r.conf[b, i]), o.confidences[i]
+            assert abs(np.log(dc) - np.log(oc)) <= band + 1e-6, (
+                f"seq {b} r{k} draft {i}: confidence {dc:.6g} vs oracle {oc:.6g}")
+            stopped_here = i == n - 1 and n < gamma
+            # the device's own decision on its own confidence: exact
+            assert (dc < tau) == stopped_here or (i == n - 1 and n == gamma), (
+                f"seq {b} r{k} draft {i}: device conf {dc:.6g} vs tau {tau:.6g}, stopped "
+                f"{stopped_here}")
+            if i < n - 1 or stopped_here:
+                if (oc < tau) != stopped_here:
+                    assert abs(np.log(oc) - np.log(tau)) <= band + 1e-6, (
+                        f"seq {b} r{k} draft {i}: oracle conf {oc:.6g} on the other side of "
+                        f"tau {tau:.6g}")
+                    near += 1
+        for j in range(n + 1):
+            check_logits(r.target_logits[b, j], o.target_logits[j], shape, f"seq {b} r{k} verify {j}")
+            check_token(r.targets[b, j], o.target_logits[j], shape, f"seq {b} r{k} verify {j}")
+        assert int(r.accepted[b]) == o.accepted, f"seq {b} r{k}: {r.accepted[b]} != {o.accepted}"
+    return near
+
+
 def workload_inputs(wl, seed: int, batch: Optional[int] = None):
     B = batch or wl.batch
     w = synth.workload_weights(wl, seed, threads=4)
