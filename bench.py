@@ -86,6 +86,18 @@ def prefill_flops(shape, B: int, P: int) -> float:
     return B * (shape.n_layers * per_layer + 2.0 * V * d)
 
 
+def verify_flops(shape, B: int, gamma: int, ctx: int) -> float:
+    """Algorithmic flops of one verify pass: 2 per weight and row for every projection of all L
+    layers and the LM head over M = B (gamma + 1) rows, plus attention (QK and PV) over the
+    context, and T5 cross-attention over the visual keys."""
+    d, hd, f, V = shape.d_model, shape.hd, shape.d_ff, shape.vocab
+    M = B * (gamma + 1)
+    per_layer = 2.0 * (4 * d * hd + 3 * d * f) * M + 4.0 * M * (ctx + gamma) * hd
+    if shape.arch == "t5":
+        per_layer += 2.0 * 2 * d * hd * M + 4.0 * M * shape.n_visual * hd
+    return shape.n_layers * per_layer + 2.0 * V * d * M
+
+
 def prefill_timing(dd, pt, vt, reps: int = 3) -> float:
     """Median seconds of one prefill call (HIP events on the decoder's stream)."""
     import numpy as np
@@ -251,38 +263,160 @@ def sampled_decode(dd, pt, vt, T: int, gamma: int, tau: float, uniforms):
 
 
 def cpu_baseline(wl, weights, prompt, visual, budget_s: float):
-    """The float64 oracle's Algorithm 1 on the host, over as many rounds as fit the budget."""
+    """The float64 oracle on the host over a bounded sample of the workload: one prefill, as many
+    rounds of Algorithm 1 as fit about 60% of the budget and as many greedy steps as fit the rest
+    (each run restarts from the prefill, whose time is subtracted).  Decode-phase rates are
+    emitted tokens over decode time; end-to-end rates are T over the prefill plus T - 1 tokens at
+    the decode rate."""
     import numpy as np
     from oracle import decode
     from oracle.model import Decoder
     try:
         from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()
-                       if i.get("user_api") == "blas"] or [1])
+        info = [i for i in threadpool_info() if i.get("user_api") == "blas"]
+        threads = max([i.get("num_threads", 1) for i in info] or [1])
+        vendor = ",".join(sorted({str(i.get("internal_api")) for i in info})) or "unknown"
     except Exception:
-        threads = 1
+        threads, vendor = 1, "unknown"
     dec = Decoder(wl.shape, weights, wl.draft_layers)
-    t0 = time.perf_counter()
-    one = decode.ssd(dec, prompt, visual, wl.new_tokens, wl.gamma, max_rounds=1)
-    t_one = time.perf_counter() - t0
+    T, g = wl.new_tokens, wl.gamma
     t0 = time.perf_counter()
     decode.prefill(dec, prompt, visual, wl.max_seq())
     t_prefill = time.perf_counter() - t0
-    per_round = max(t_one - t_prefill, 1e-3)
-    rounds = int(max(1, min(wl.new_tokens, (budget_s - t_prefill) / per_round)))
-    # whole jobs (or one job cut to the budget's rounds) until about the budget is spent
-    dt, n, jobs, n_rounds = 0.0, 0, 0, 0
-    while True:
+    t0 = time.perf_counter()
+    one = decode.ssd(dec, prompt, visual, T, g, max_rounds=1)
+    per_round = max(time.perf_counter() - t0 - t_prefill, 1e-3)
+    rounds = int(max(1, min(T, (0.6 * budget_s - t_prefill) / per_round)))
+    t0 = time.perf_counter()
+    run = decode.ssd(dec, prompt, visual, T, g, max_rounds=rounds)
+    t_ssd = max(time.perf_counter() - t0 - t_prefill, 1e-6)
+    n_ssd = len(run.tokens) - 1
+    drafted = sum(len(r.drafts) for r in run.rounds)
+    alpha = sum(r.accepted for r in run.rounds) / max(1, drafted)
+    per_step = per_round / (g + 1 + g * wl.draft_layers / wl.shape.n_layers)
+    steps = int(max(1, min(T - 1, (0.4 * budget_s - t_prefill) / max(per_step, 1e-4))))
+    t0 = time.perf_counter()
+    gr = decode.greedy(dec, prompt, visual, steps + 1)
+    t_gr = max(time.perf_counter() - t0 - t_prefill, 1e-6)
+    ssd_dec = n_ssd / t_ssd
+    gr_dec = steps / t_gr
+    e2e = lambda rate: T / (t_prefill + (T - 1) / rate)
+    del one, gr
+    return {"value": round(e2e(ssd_dec), 4), "unit": "tokens/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": (f"{wl.name} seed 0: float64 oracle ({vendor} BLAS), one prefill "
+                       f"({t_prefill:.2f} s), {len(run.rounds)} rounds of Algorithm 1 (gamma {g}, "
+                       f"{n_ssd} tokens in {t_ssd:.1f} s) and {steps} greedy steps "
+                       f"({t_gr:.1f} s); end-to-end rates extrapolate the decode rate to the "
+                       f"{T}-token job; host affinity {len(os.sched_getaffinity(0))} cpus"),
+            "ssd": {"decode_tokens_per_s": round(ssd_dec, 4),
+                    "end_to_end_tokens_per_s": round(e2e(ssd_dec), 4),
+                    "acceptance_rate": round(alpha, 4), "rounds": len(run.rounds)},
+            "greedy": {"decode_tokens_per_s": round(gr_dec, 4),
+                       "end_to_end_tokens_per_s": round(e2e(gr_dec), 4), "steps": steps},
+            "prefill_s": round(t_prefill, 3), "blas": vendor}
+
+
+def read_ceiling(nbytes: int = 2 << 30) -> dict:
+    """The measured HBM read ceiling: a read-only stream kernel of the library over nbytes."""
+    import torch
+    from paper_2510_22641_amd import ssd as abi
+    buf = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    out = torch.empty(4096, dtype=torch.float32, device="cuda")
+    s = torch.cuda.current_stream()
+    gbps = abi.ssd_read_bandwidth(buf, nbytes, out, 5, s.cuda_stream)
+    del buf, out
+    return {"GBps": round(gbps, 1), "frac_of_nominal": round(gbps / HBM_PEAK_GBS, 4),
+            "bytes": nbytes, "kernel": "read_probe_kernel (one 16 KB chunk per block, 16-byte loads)"}
+
+
+def confidence_sweep(dd, pt, vt, wl, steps: int, greedy_toks, greedy_s: float):
+    """Confidence-stopped drafting at c3: the device's own draft confidences of one job at
+    threshold 0 give thresholds at their 5/10/20/30/50% quantiles; each threshold is timed with
+    ssd_generate_confident (threshold 0 too: no stop, no per-step read-back)."""
+    import numpy as np
+    import torch
+    B, T, g = wl.batch, wl.new_tokens, wl.gamma
+    pending, _ = dd.prefill(pt, vt)
+    confs, emitted = [], 1
+    while emitted < T:
+        d, nd, cf, _, st = dd.draft_confident(pending, g, 0.0)
+        t, _ = dd.verify(pending, d, st, reuse=True)
+        _, alen = dd.accept_counts(d, nd, t, pending, st)
+        confs.append(cf.cpu().numpy()[0, :st].copy())
+        emitted += int(alen.cpu()[0]) + 1
+    confs = np.concatenate(confs)
+    qs = [0.05, 0.1, 0.2, 0.3, 0.5]
+    out = {"confidence_quantiles": {str(q): float(np.quantile(confs, q)) for q in qs},
+           "confidence_range": [float(confs.min()), float(confs.max())], "points": []}
+    for q, tau in [(0.0, 0.0)] + [(q, float(np.quantile(confs, q))) for q in qs]:
+        dd.generate_confident(pt, vt, T, g, tau)
+        torch.cuda.synchronize()
         t0 = time.perf_counter()
-        run = decode.ssd(dec, prompt, visual, wl.new_tokens, wl.gamma, max_rounds=rounds)
-        t_job = time.perf_counter() - t0
-        dt, n, jobs, n_rounds = dt + t_job, n + len(run.tokens), jobs + 1, n_rounds + len(run.rounds)
-        if dt + t_job > 1.25 * budget_s:
-            break
-    return {"value": round(n / dt, 4), "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
-            "sample": (f"{wl.name} seed 0: float64 oracle, {jobs} job(s) of prefill + "
-                       f"{n_rounds // jobs} rounds of Algorithm 1 (gamma {wl.gamma}), {n} tokens "
-                       f"emitted in {dt:.1f} s; host affinity {len(os.sched_getaffinity(0))} cpus")}
+        for _ in range(steps):
+            toks, st = dd.generate_confident(pt, vt, T, g, tau)
+        torch.cuda.synchronize()
+        dt = time.perf_counter() - t0
+        out["points"].append({
+            "quantile": q, "threshold": tau, "tokens_per_s": round(B * T * steps / dt, 2),
+            "speedup_vs_greedy": round(greedy_s / (dt / steps), 3),
+            "acceptance_rate": round(st["accepted"] / max(1, st["drafted"]), 4),
+            "drafts_per_round": round(st["drafted"] / max(1, st["rounds"]), 3),
+            "rounds": st["rounds"], "equals_greedy_tokens": bool(torch.equal(toks, greedy_toks))})
+        print(f"[bench] confidence stop q={q} tau={tau:.3g}: {out['points'][-1]}", file=sys.stderr,
+              flush=True)
+    return out
+
+
+def per_config(seed: int, steps: int) -> dict:
+    """One whole job of each other single-GPU workload (c1, c2, c5): speculative and greedy
+    decode through ssd_generate, their tokens, acceptance, and the draft-step / verify times
+    against their byte rooflines."""
+    import torch
+    import synth
+    from paper_2510_22641_amd import runtime
+    res = {}
+    for wl in (synth.C1, synth.C2, synth.C5):
+        t_setup = time.time()
+        sh = wl.shape
+        dd = runtime.from_workload(wl, seed)
+        prompts = synth.make_prompts(sh, seed, wl.batch, wl.prompt_len)
+        visual = synth.make_visual(sh, seed, wl.batch)
+        pt, vt = dd.upload_inputs(prompts, visual)
+        B, T, g = wl.batch, wl.new_tokens, wl.gamma
+
+        def timed(spec):
+            dd.generate(pt, vt, T, g, speculative=spec, reuse=True)
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            for _ in range(steps):
+                toks, st = dd.generate(pt, vt, T, g, speculative=spec, reuse=True)
+            torch.cuda.synchronize()
+            return (time.perf_counter() - t0) / steps, st, toks
+
+        ds, st, toks = timed(True)
+        dg, _, gtoks = timed(False)
+        d_s, v_s, ctx = step_timings(dd, pt, vt, B, g)
+        db = draft_step_bytes(sh, wl.draft_layers, ctx, dd.k_pool.element_size(),
+                              cross_folded(sh, dd.cap.max_batch))
+        vb = verify_bytes(sh, B, g, ctx, dd.k_pool.element_size())
+        pf = prefill_timing(dd, pt, vt)
+        res[wl.name] = {
+            "tokens_per_s": round(B * T / ds, 2), "greedy_tokens_per_s": round(B * T / dg, 2),
+            "speedup_vs_greedy": round(dg / ds, 3),
+            "acceptance_rate": round(st["accepted"] / max(1, st["drafted"]), 4),
+            "rounds": st["rounds"], "ssd_equals_greedy_tokens": bool(torch.equal(toks, gtoks)),
+            "prefill_ms": round(pf * 1e3, 3),
+            "draft_step": {"us": round(d_s * 1e6, 2), "bytes": int(db),
+                           "frac": round(db / d_s / 1e9 / HBM_PEAK_GBS, 4)},
+            "verify": {"us": round(v_s * 1e6, 2), "bytes": int(vb),
+                       "frac": round(vb / v_s / 1e9 / HBM_PEAK_GBS, 4)},
+            "jobs": steps, "setup_s": round(time.time() - t_setup, 1)}
+        print(f"[bench] {wl.name}: {res[wl.name]}", file=sys.stderr, flush=True)
+        dd.close()
+        del dd
+        torch.cuda.empty_cache()
+    return res
 
 
 def main():
@@ -299,6 +433,10 @@ def main():
                          "layer before a second measurement (0: skip)")
     ap.add_argument("--sample-temps", default="1.0,0.1",
                     help="temperatures of the speculative-sampling measurement (empty: skip)")
+    ap.add_argument("--per-config", type=int, default=1,
+                    help="also time one whole job of c1, c2 and c5 (0: skip)")
+    ap.add_argument("--confidence", type=int, default=1,
+                    help="also sweep confidence-stopped drafting over thresholds (0: skip)")
     ap.add_argument("--sweep", choices=["c4"], default=None,
                     help="run the FlanT5-xl sweep instead (one JSON line per point)")
     ap.add_argument("--copy-bytes", type=int, default=0,
@@ -374,6 +512,11 @@ def main():
            "schedule": f"d(t) = {g} + floor(10 sigmoid(0.01 (t - {dd.cap.max_seq}/2)))"}
     print(f"[bench] dynamic d(t) {dyn['tokens_per_s']:.1f} tok/s", file=sys.stderr, flush=True)
 
+    conf = None
+    if args.confidence and B == 1:
+        conf = confidence_sweep(dd, pt, vt, wl, max(1, args.steps // 2), toks_greedy,
+                                dtg / args.steps)
+
     # prefill alone (its projections on MFMA tiles once the context exceeds the skinny chunk)
     pf_s = prefill_timing(dd, pt, vt)
     pf_flops = prefill_flops(sh, B, wl.prompt_len)
@@ -393,6 +536,15 @@ def main():
     verify = {"us": round(verify_s * 1e6, 2), "bytes": int(vbytes),
               "GBps": round(vbytes / verify_s / 1e9, 1),
               "frac": round(vbytes / verify_s / 1e9 / HBM_PEAK_GBS, 4)}
+    # MFMA utilisation of the verify pass: its flops over its time against the bf16 peak; the HBM
+    # roofline caps it at M / 312.5 for M rows (M flops per weight byte at 8 TB/s)
+    vfl = verify_flops(sh, B, g, ctx)
+    Mv = B * (g + 1)
+    verify["mfma"] = {"tflops_per_s": round(vfl / verify_s / 1e12, 2),
+                      "frac_of_bf16_peak": round(vfl / verify_s / 1e12 / MFMA_BF16_PEAK_TFS, 5),
+                      "hbm_bound_frac": round(Mv / 312.5, 5),
+                      "frac_of_bound": round(vfl / verify_s / 1e12 / MFMA_BF16_PEAK_TFS /
+                                             (Mv / 312.5), 4)}
 
     # dominant kernel: every launch of the one-row weight-streaming GEMV that streams the
     # RMS-normalised d_model-wide matrices, timed by events bound to its own dispatch
@@ -475,12 +627,18 @@ def main():
     if rc != 0:
         print(f"[bench] device status {status}", file=sys.stderr)
         sys.exit(1)
+    dd.close()
+    del dd
+    torch.cuda.empty_cache()
+
+    ceiling = read_ceiling()
+    print(f"[bench] read ceiling {ceiling}", file=sys.stderr, flush=True)
+    for part in (draft, verify):
+        part["frac_of_read_ceiling"] = round(part["GBps"] / ceiling["GBps"], 4)
+    others = per_config(args.seed, 3) if args.per_config and wl.name == "c3-flant5-xl" else None
 
     cpu = None
     if not args.no_cpu_baseline:
-        dd.close()
-        del dd
-        torch.cuda.empty_cache()
         cpu = cpu_baseline(wl, weights, prompts[0], visual[0], args.cpu_seconds)
 
     out = {
@@ -501,12 +659,15 @@ def main():
         "speedup_vs_greedy": round(ssd_tps / greedy_tps, 3),
         "ssd_equals_greedy_tokens": same,
         "dynamic_gamma": dyn,
+        "confidence_stop": conf,
         "speculative_sampling": sampling or None,
         "fitted_imitation": fit,
         "prefill": prefill,
         "draft_step": draft,
         "verify": verify,
         "roofline": roofline,
+        "read_ceiling": ceiling,
+        "per_config": others,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out))

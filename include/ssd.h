@@ -318,6 +318,15 @@ int ssd_set_hidden_export(ssd_ctx* ctx, float* d_phi, float* d_xk, float* d_xl);
 int ssd_profile_enable(ssd_ctx* ctx, int enable);
 int ssd_profile_read(ssd_ctx* ctx, int64_t* launches, double* seconds, double* bytes);
 
+/* Measurement utility, not on the decode path: the HBM read ceiling the kernels' byte rates are
+ * compared with.  Streams `bytes` (a multiple of 16; use far more than the 256 MB Infinity Cache)
+ * of device memory at d_buf through a read-only kernel (one 16 KB chunk per block of 256
+ * threads, 16-byte loads, four in flight per thread) reps + 1 times on `stream`, the first pass
+ * a warm-up, and returns the best rate in GB/s (HIP events around each pass) in *gbps.  d_out
+ * (4096 floats) is a sink the kernel may write.  Synchronises the stream. */
+int ssd_read_bandwidth(const void* d_buf, size_t bytes, float* d_out, int reps, void* stream,
+                       double* gbps);
+
 /* Synchronise the stream; SSD_OK, SSD_ERR_HIP, or SSD_ERR_DEVICE when the device status word is
  * non-zero (then *status, if not NULL, receives the SSD_DEV_* bits) — and clear the word. */
 int ssd_sync_status(ssd_ctx* ctx, int32_t* status);

@@ -256,6 +256,10 @@ hipError_t launch_argmax_final_ex(const float* part_val, const int* part_idx, in
                                   const void* embed, int wdtype, int d, float* x_out,
                                   const ConfArgs& cf, hipStream_t s);
 
+// Read-only stream of `bytes` (a multiple of 16) at buf, one 16 KB chunk per block of 256
+// threads; out (4096 floats) is a sink that keeps the loads.
+hipError_t launch_read_probe(const void* buf, size_t bytes, float* out, hipStream_t s);
+
 // dst[b * ld_dst + j] = src[b * ld_src + j] for b < B, j < n (token rows).
 hipError_t launch_copy_tokens(int32_t* dst, int ld_dst, const int32_t* src, int ld_src, int B,
                               int n, hipStream_t s);

@@ -147,6 +147,26 @@ __global__ __launch_bounds__(256) void argmax_final_kernel(const float* pv, cons
   for (int k = threadIdx.x; k < d; k += blockDim.x) x_out[(size_t)m * d + k] = load_elem(src + k);
 }
 
+// Read-only stream: block b reads the 16 KB chunk b of n16 16-byte words, four loads in flight
+// per thread (the form that streamed fastest among grid-stride and 16-128 KB chunk variants on
+// MI355X).  out[b % 4096] is written only when the XOR of the chunk hits a fixed word, which the
+// compiler cannot rule out, so the loads are kept.
+__global__ __launch_bounds__(256) void read_probe_kernel(const uint4* __restrict__ p, size_t n16,
+                                                         float* out) {
+  constexpr size_t CHUNK = 1024;  // 16-byte words per block
+  const size_t base = (size_t)blockIdx.x * CHUNK;
+  uint32_t acc = 0;
+  uint4 v[4];
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const size_t j = base + (size_t)u * 256 + threadIdx.x;
+    v[u] = j < n16 ? p[j] : make_uint4(0, 0, 0, 0);
+  }
+#pragma unroll
+  for (int u = 0; u < 4; ++u) acc ^= v[u].x ^ v[u].y ^ v[u].z ^ v[u].w;
+  if (acc == 0x9e3779b9u) out[blockIdx.x & 4095] = 1.f;
+}
+
 __global__ void copy_tokens_kernel(int32_t* dst, int ld_dst, const int32_t* src, int ld_src,
                                    int B, int n) {
   const int e = blockIdx.x * blockDim.x + threadIdx.x;
@@ -345,6 +365,15 @@ hipError_t launch_argmax_final_embed(const float* part_val, const int* part_idx,
   if (!embed || !x_out || d < 1) return hipErrorInvalidValue;
   return launch_argmax_final_ex(part_val, part_idx, M, n_parts, C, dst0, ld0, off0, dst1, embed,
                                 wdtype, d, x_out, ConfArgs(), s);
+}
+
+hipError_t launch_read_probe(const void* buf, size_t bytes, float* out, hipStream_t s) {
+  if (bytes < 16) return hipErrorInvalidValue;
+  const size_t blocks = (bytes / 16 + 1023) / 1024;
+  if (blocks > 0x7fffffff) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(read_probe_kernel, dim3((unsigned)blocks), dim3(256), 0, s,
+                     reinterpret_cast<const uint4*>(buf), bytes / 16, out);
+  return hipGetLastError();
 }
 
 hipError_t launch_copy_tokens(int32_t* dst, int ld_dst, const int32_t* src, int ld_src, int B,

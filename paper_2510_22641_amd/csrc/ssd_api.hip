@@ -1250,6 +1250,35 @@ int ssd_profile_read(ssd_ctx* c, int64_t* launches, double* seconds, double* byt
   return SSD_OK;
 }
 
+int ssd_read_bandwidth(const void* d_buf, size_t bytes, float* d_out, int reps, void* stream,
+                       double* gbps) {
+  if (!d_buf || !d_out || !gbps || reps < 1 || bytes < 16 || bytes % 16) return SSD_ERR_ARG;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  if (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess) {
+    if (e0) (void)hipEventDestroy(e0);
+    return SSD_ERR_HIP;
+  }
+  double best = 0.0;
+  int rc = SSD_OK;
+  for (int r = 0; r <= reps && rc == SSD_OK; ++r) {
+    float ms = 0.f;
+    if (hipEventRecord(e0, s) != hipSuccess ||
+        launch_read_probe(d_buf, bytes, d_out, s) != hipSuccess ||
+        hipEventRecord(e1, s) != hipSuccess || hipEventSynchronize(e1) != hipSuccess ||
+        hipEventElapsedTime(&ms, e0, e1) != hipSuccess) {
+      rc = SSD_ERR_HIP;
+      break;
+    }
+    const double rate = (double)bytes / (ms * 1e-3) / 1e9;
+    if (r > 0 && rate > best) best = rate;  // the first pass warms up
+  }
+  (void)hipEventDestroy(e0);
+  (void)hipEventDestroy(e1);
+  *gbps = best;
+  return rc;
+}
+
 int ssd_sync_status(ssd_ctx* c, int32_t* status) {
   if (!c) return SSD_ERR_ARG;
   int32_t v = 0;

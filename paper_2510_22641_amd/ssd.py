@@ -88,6 +88,7 @@ def _load():
         "ssd_profile_enable": (c_int, [P, c_int]),
         "ssd_profile_read": (c_int, [P, POINTER(c_int64), POINTER(ctypes.c_double),
                                      POINTER(ctypes.c_double)]),
+        "ssd_read_bandwidth": (c_int, [P, c_size_t, P, c_int, P, POINTER(ctypes.c_double)]),
         "ssd_sync_status": (c_int, [P, POINTER(c_int32)]),
         "ssd_status_string": (ctypes.c_char_p, [c_int]),
         "ssd_destroy": (None, [P]),
@@ -104,7 +105,7 @@ EXPORTS = ("ssd_workspace_bytes", "ssd_create", "ssd_create_static", "ssd_prefil
            "ssd_accept", "ssd_draft_sample", "ssd_accept_sample", "ssd_generate", "ssd_draft_confident", "ssd_accept_counts",
            "ssd_generate_confident", "ssd_dynamic_gamma", "ssd_set_graphs", "ssd_set_hidden_export",
            "ssd_profile_enable",
-           "ssd_profile_read", "ssd_sync_status",
+           "ssd_profile_read", "ssd_read_bandwidth", "ssd_sync_status",
            "ssd_status_string", "ssd_destroy")
 
 
@@ -242,6 +243,14 @@ def ssd_profile_read(ctx):
     _check("ssd_profile_read", _lib.ssd_profile_read(ctx, ctypes.byref(n), ctypes.byref(sec),
                                                      ctypes.byref(by)))
     return int(n.value), float(sec.value), float(by.value)
+
+
+def ssd_read_bandwidth(d_buf, nbytes: int, d_out, reps: int, stream) -> float:
+    """Best GB/s of a read-only stream over nbytes of device memory (measurement utility)."""
+    g = ctypes.c_double(0)
+    _check("ssd_read_bandwidth", _lib.ssd_read_bandwidth(_p(d_buf), int(nbytes), _p(d_out),
+                                                         int(reps), _p(stream), ctypes.byref(g)))
+    return float(g.value)
 
 
 def ssd_sync_status(ctx):
