@@ -365,13 +365,13 @@ int run_layers(ssd_ctx* c, float* x, int B, int C, int pos_off, int l0, int l1, 
       // folded: scores = fold_q . rmsnorm(x), then x += fold_o . softmax(scores) per head
       const int HN = d.n_heads * d.n_visual;
       a = lin(c);
-      a.x = x; a.ldx = D; a.M = 1; a.K = D;
+      a.x = x; a.ldx = D; a.M = R; a.K = D;
       a.norm = NORM_RMS; a.gain = lw.xattn_norm;
       a.w[0] = c->at<float>(c->L.fold_q) + (size_t)l * c->fold_layer_elems(); a.wdtype = SSD_F32;
       a.n_per = HN; a.epi = EPI_STORE; a.y = q; a.ldy = HD;
       HIP_TRY(run_linear(c, a));
       a = lin(c);
-      a.x = q; a.ldx = HD; a.M = 1; a.K = HN;
+      a.x = q; a.ldx = HD; a.M = R; a.K = HN;
       a.norm = NORM_SOFTMAX; a.group = d.n_visual;
       a.w[0] = c->at<float>(c->L.fold_o) + (size_t)l * c->fold_layer_elems(); a.wdtype = SSD_F32;
       a.n_per = D; a.epi = EPI_RESID; a.y = x; a.ldy = D;
