@@ -580,8 +580,143 @@ hipError_t launch_fold_nv(const void* xk, const void* xv, int kvdtype, const voi
 
 }  // namespace
 
+// fg[j][n] = fold_q[j][n] g[n] for n < d; fg[j][d + c] = sum_n fold_q[j][n] g[n] wo[n][c].
+// A 64 x 64 tile of the product per block on v_mfma_f32_16x16x32_bf16: each wave owns 32 x 32
+// (2 x 2 MFMA tiles).  Per K step of 64 the scaled fold_q rows are split into bf16 hi / lo planes
+// in LDS (two MFMAs, about 16 mantissa bits) and the W_o rows are stored transposed, so that both
+// operand fragments are 16-byte LDS reads; the next step's global loads are issued before the
+// current step's MFMAs.  Rows, columns and K past the matrix read as zeros.
+template <typename WT>
+struct FgRegs {
+  float a[16];   // fold_q[row][k .. k + 16) * g[k ..]
+  float b[16];   // wo[k row][c .. c + 16)
+};
+
+template <typename WT>
+__device__ __forceinline__ void fg_load(FgRegs<WT>& r, const float* __restrict__ fq,
+                                        const float* __restrict__ g, const WT* __restrict__ wo,
+                                        int HN, int d, int HD, int jrow, int kcol, int krow,
+                                        int ccol) {
+  if (jrow < HN && kcol + 16 <= d) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const float4 v = *reinterpret_cast<const float4*>(fq + (size_t)jrow * d + kcol + 4 * u);
+      const float4 w = *reinterpret_cast<const float4*>(g + kcol + 4 * u);
+      r.a[4 * u] = v.x * w.x; r.a[4 * u + 1] = v.y * w.y;
+      r.a[4 * u + 2] = v.z * w.z; r.a[4 * u + 3] = v.w * w.w;
+    }
+  } else {
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      const int k = kcol + e;
+      r.a[e] = (jrow < HN && k < d) ? fq[(size_t)jrow * d + k] * g[k] : 0.f;
+    }
+  }
+  if (krow < d && ccol + 16 <= HD) {
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      Vec8<WT> v;
+      v.load(wo + (size_t)krow * HD + ccol + 8 * u);
+      v.to_f32(r.b + 8 * u);
+    }
+  } else {
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      const int c = ccol + e;
+      r.b[e] = (krow < d && c < HD) ? load_elem(wo + (size_t)krow * HD + c) : 0.f;
+    }
+  }
+}
+
+template <typename WT>
+__global__ __launch_bounds__(256) void fold_fg_kernel(const float* __restrict__ fq,
+                                                      const float* __restrict__ g,
+                                                      const WT* __restrict__ wo, int HN, int d,
+                                                      int HD, float* __restrict__ fg) {
+  constexpr int KS = 64, LDK = KS + 8;  // K per step; bf16 per LDS row (with padding)
+  __shared__ __attribute__((aligned(16))) bf16_t Ah[64 * LDK], Al[64 * LDK], Bt[64 * LDK];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int j0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
+  const int wr = (wave >> 1) * 32, wc = (wave & 1) * 32;
+  const size_t ldg = (size_t)d + HD;
+  f32x4_t acc[2][2];
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int b = 0; b < 2; ++b) acc[a][b] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  const int ar = tid >> 2, ak = (tid & 3) * 16;  // A: row, first K element of this thread
+  const int bk = tid >> 2, bc = (tid & 3) * 16;  // B: K row, first column of this thread
+  FgRegs<WT> r;
+  fg_load(r, fq, g, wo, HN, d, HD, j0 + ar, ak, bk, c0 + bc);
+  for (int n0 = 0; n0 < d; n0 += KS) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      uint4 hi, lo;
+      split_bf16x8(r.a + 8 * h, hi, lo);
+      *reinterpret_cast<uint4*>(Ah + ar * LDK + ak + 8 * h) = hi;
+      *reinterpret_cast<uint4*>(Al + ar * LDK + ak + 8 * h) = lo;
+    }
+#pragma unroll
+    for (int e = 0; e < 16; ++e) Bt[(bc + e) * LDK + bk] = (bf16_t)f32_to_bf16(r.b[e]);
+    __syncthreads();
+    if (n0 + KS < d) fg_load(r, fq, g, wo, HN, d, HD, j0 + ar, n0 + KS + ak, n0 + KS + bk, c0 + bc);
+#pragma unroll
+    for (int kk = 0; kk < KS; kk += 32) {
+      const int kq = kk + 8 * (lane >> 4);
+#pragma unroll
+      for (int a = 0; a < 2; ++a) {
+        const int row = wr + 16 * a + (lane & 15);
+        const bf16x8_t ah = *reinterpret_cast<const bf16x8_t*>(Ah + row * LDK + kq);
+        const bf16x8_t al = *reinterpret_cast<const bf16x8_t*>(Al + row * LDK + kq);
+#pragma unroll
+        for (int b = 0; b < 2; ++b) {
+          const int col = wc + 16 * b + (lane & 15);
+          const bf16x8_t bv = *reinterpret_cast<const bf16x8_t*>(Bt + col * LDK + kq);
+          acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, bv, acc[a][b], 0, 0, 0);
+          acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al, bv, acc[a][b], 0, 0, 0);
+        }
+      }
+    }
+    __syncthreads();
+  }
+  // D[row][col]: lane holds rows 4 (lane / 16) + e, column lane % 16 of each tile
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int j = j0 + wr + 16 * a + 4 * (lane >> 4) + e, c = c0 + wc + 16 * b + (lane & 15);
+        if (j < HN && c < HD) fg[(size_t)j * ldg + d + c] = acc[a][b][e];
+      }
+  // the scaled F part: row j0 + jr goes to the column block jr % gridDim.x (d % 4 == 0)
+  for (int jr = blockIdx.x; jr < 64; jr += gridDim.x) {
+    const int j = j0 + jr;
+    if (j >= HN) break;
+    for (int n = tid * 4; n < d; n += 1024) {
+      const float4 v = *reinterpret_cast<const float4*>(fq + (size_t)j * d + n);
+      const float4 w = *reinterpret_cast<const float4*>(g + n);
+      float* o = fg + (size_t)j * ldg + n;
+      o[0] = v.x * w.x; o[1] = v.y * w.y; o[2] = v.z * w.z; o[3] = v.w * w.w;
+    }
+  }
+}
+
 bool cross_fold_ok(int nv, int dh) {
   return (nv == 8 || nv == 16 || nv == 32 || nv == 64) && dh <= 128;
+}
+
+hipError_t launch_fold_fg(const float* fold_q, const float* gain, const void* wo, int wdtype,
+                          int HN, int d, int HD, float* fg, hipStream_t s) {
+  if (HN < 1 || d < 1 || HD < 1) return hipErrorInvalidValue;
+  dim3 grid((HD + 63) / 64, (HN + 63) / 64);
+  if (wdtype == 1)
+    hipLaunchKernelGGL(fold_fg_kernel<bf16_t>, grid, dim3(256), 0, s, fold_q, gain,
+                       reinterpret_cast<const bf16_t*>(wo), HN, d, HD, fg);
+  else
+    hipLaunchKernelGGL(fold_fg_kernel<float>, grid, dim3(256), 0, s, fold_q, gain,
+                       reinterpret_cast<const float*>(wo), HN, d, HD, fg);
+  return hipGetLastError();
 }
 
 hipError_t launch_cross_fold(const void* xk, const void* xv, int kvdtype, const void* wq,

@@ -280,7 +280,7 @@ __device__ __forceinline__ void gemv_finish(const LinearArgs& a, const RowPair<W
         } else if (a.epi == EPI_BIAS_GELU) {
           *yp = gelu_tanh(v + a.bias[n]);
         } else if (a.epi == EPI_BIAS_RESID) {
-          *yp = yold[s][m] + (v + a.bias[n]);
+          *yp = yold[s][m] + (v + (a.bias ? a.bias[n] : 0.f));
         }
       }
     }

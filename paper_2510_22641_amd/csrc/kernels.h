@@ -33,7 +33,7 @@ enum Epi {
   EPI_GATED_GELU = 2,  // y[m][n] = gelu_tanh(acc_gate) * acc_up  (w[0] = gate, w[1] = up)
   EPI_GATED_SILU = 3,  // y[m][n] = silu(acc_gate) * acc_up
   EPI_BIAS_GELU = 4,   // y[m][n] = gelu_tanh(acc + bias[n])
-  EPI_BIAS_RESID = 5,  // y[m][n] = (resid ? resid[m][n] : 0) + acc + bias[n]
+  EPI_BIAS_RESID = 5,  // y[m][n] = (resid ? resid[m][n] : 0) + acc + (bias ? bias[n] : 0)
   EPI_ARGMAX = 6,      // per-block (max, argmax) over n for each m; logits[m][n] = acc if wanted
   EPI_QKV = 7          // w = (wq, wk, wv): rotary on q and k (when rope_cos is set), q -> y[m][.],
                        // k and v into the paged pools at the row's position (vector path only)
@@ -51,6 +51,11 @@ struct LinearArgs {
   const float* shift = nullptr;
   float eps = 0.f;
   int group = 0;  // NORM_SOFTMAX: inputs per softmax group (8, 16, 32 or 64)
+  // NORM_SOFTMAX (one-row path): when set, the inputs are first multiplied by
+  // 1 / sqrt(mean(pre_row[0..pre_len)^2) + eps) (the RMS normalisation of the row the scores were
+  // projected from); 4 <= pre_len <= 2048, a multiple of 4
+  const float* pre_row = nullptr;
+  int pre_len = 0;
   const void* w[3] = {nullptr, nullptr, nullptr};  // [n_per][K] each, wdtype
   int n_mats = 1;
   int n_per = 0;
@@ -121,6 +126,12 @@ int gemv_pieces(int K);
 // per row written to part_val / part_idx (their row stride).
 hipError_t launch_linear(LinearArgs a, hipStream_t s, int* n_parts = nullptr,
                          LaunchTiming* timing = nullptr);
+
+// Two one-row GEMVs that read the same inputs, in one launch (the blocks of `a` first, then those
+// of `b`): `a` with bf16 weights and K <= 2048, `b` with float32 weights and K <= 4096, no input
+// transform, store / residual / bias epilogues only.
+bool linear_pair_ok(const LinearArgs& a, const LinearArgs& b);
+hipError_t launch_linear_pair(const LinearArgs& a, const LinearArgs& b, hipStream_t s);
 
 // Upper bound of the partials per row for n_out outputs (workspace sizing).
 int argmax_parts_max(int n_out);
@@ -214,6 +225,14 @@ bool cross_fold_ok(int nv, int dh);
 hipError_t launch_cross_fold(const void* xk, const void* xv, int kvdtype, const void* wq,
                              const void* wo, int wdtype, int H, int nv, int dh, int d, float* fq,
                              float* fo, hipStream_t s);
+
+// The scores of the folded cross-attention taken from the layer's input and attention output
+// instead of its post-attention residual (one-row steps): with F = fold_q diag(g) (g the
+// cross-attention RMSNorm gain) and W_o the self-attention output matrix, fg[j] = [F[j] | (F W_o)[j]]
+// ([HN][d + HD] float32), so fg . [x; o] = F (x + W_o o).  fold_q [HN][d] float32, wo [d][HD] in
+// wdtype.
+hipError_t launch_fold_fg(const float* fold_q, const float* gain, const void* wo, int wdtype,
+                          int HN, int d, int HD, float* fg, hipStream_t s);
 
 // Row statistics for normalisation: stats[m] = (mean, 1/sqrt(var+eps)) (LN) or (0, 1/rms) (RMS).
 hipError_t launch_row_stats(const float* x, int ldx, int M, int K, int norm, float eps,

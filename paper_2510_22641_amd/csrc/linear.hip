@@ -216,6 +216,17 @@ __global__ __launch_bounds__(256) void gemv1_kernel(const LinearArgs a) {
     xv[p][0] = x0.x; xv[p][1] = x0.y; xv[p][2] = x0.z; xv[p][3] = x0.w;
     xv[p][4] = x1.x; xv[p][5] = x1.y; xv[p][6] = x1.z; xv[p][7] = x1.w;
   }
+  // NORM_SOFTMAX with a pre-scale row: that row (at most 2048 floats) is requested with the
+  // inputs, before the weights, so that its reduction and the softmax overlap the weight stream
+  constexpr int PRE = NORM == NORM_SOFTMAX ? 8 : 1;
+  float4 prev[PRE];
+  if (NORM == NORM_SOFTMAX && a.pre_row) {
+#pragma unroll
+    for (int u = 0; u < PRE; ++u) {
+      const int e = min(lane * 4 + u * 256, a.pre_len - 4);
+      prev[u] = *reinterpret_cast<const float4*>(a.pre_row + e);
+    }
+  }
   const RowPair<WT> r = row_pair<WT>(a, gated, n_total, pr < n_pairs ? pr : 0);
   const bool live = pr < n_pairs;
   const bool qkv = a.epi == EPI_QKV;
@@ -247,6 +258,22 @@ __global__ __launch_bounds__(256) void gemv1_kernel(const LinearArgs a) {
     // softmax over groups of a.group inputs: a group is a.group / 8 consecutive lanes of a piece
     // (512 is a multiple of the group, so groups never straddle pieces, and K of whole groups)
     const int gl = a.group >> 3;
+    if (a.pre_row) {
+      // scale by 1 / rms of the row the scores came from (every wave reads that row in full;
+      // clamped re-reads past pre_len count as zero)
+      float s2 = 0.f;
+#pragma unroll
+      for (int u = 0; u < PRE; ++u)
+        if (lane * 4 + u * 256 < a.pre_len)
+          s2 += (prev[u].x * prev[u].x + prev[u].y * prev[u].y) +
+                (prev[u].z * prev[u].z + prev[u].w * prev[u].w);
+      s2 = wave_sum(s2);
+      const float sc = 1.0f / sqrtf(s2 / (float)a.pre_len + a.eps);
+#pragma unroll
+      for (int p = 0; p < KP; ++p)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) xv[p][e] *= sc;
+    }
 #pragma unroll
     for (int p = 0; p < KP; ++p) {
       float m = xv[p][0];
@@ -349,7 +376,7 @@ __global__ __launch_bounds__(256) void gemv1_kernel(const LinearArgs a) {
 // folded as in gemv1 with the sum of squares reduced the same way.  Wave w finishes row pair w
 // with gemv1's epilogue.
 template <typename WT, int KP, int NORM>
-__global__ __launch_bounds__(256) void gemv1k_kernel(const LinearArgs a) {
+__device__ __forceinline__ void gemv1k_body(const LinearArgs& a, const int blk) {
   static_assert(NORM != NORM_LN, "LayerNorm rows take gemv1_kernel");
   __shared__ float part[GV_WAVES][9];
   __shared__ float rv[GV_WAVES][1];
@@ -372,7 +399,7 @@ __global__ __launch_bounds__(256) void gemv1k_kernel(const LinearArgs a) {
     xv[p][0] = x0.x; xv[p][1] = x0.y; xv[p][2] = x0.z; xv[p][3] = x0.w;
     xv[p][4] = x1.x; xv[p][5] = x1.y; xv[p][6] = x1.z; xv[p][7] = x1.w;
   }
-  const int pr = blockIdx.x * GV_WAVES + wave;
+  const int pr = blk * GV_WAVES + wave;
   const RowPair<WT> r = row_pair<WT>(a, gated, n_total, pr < n_pairs ? pr : 0);
   const bool live = pr < n_pairs;
   const bool qkv = a.epi == EPI_QKV;
@@ -386,7 +413,7 @@ __global__ __launch_bounds__(256) void gemv1k_kernel(const LinearArgs a) {
   Vec8<WT> w[GV_WAVES][2][KP];
 #pragma unroll
   for (int q = 0; q < GV_WAVES; ++q) {
-    const int pq = blockIdx.x * GV_WAVES + q;
+    const int pq = blk * GV_WAVES + q;
     const RowPair<WT> rq = row_pair<WT>(a, gated, n_total, pq < n_pairs ? pq : 0);
 #pragma unroll
     for (int p = 0; p < KP; ++p) {
@@ -481,6 +508,21 @@ __global__ __launch_bounds__(256) void gemv1k_kernel(const LinearArgs a) {
   res[1][0] = ((part[0][2 * wave + 1] + part[1][2 * wave + 1]) + (part[2][2 * wave + 1] + part[3][2 * wave + 1])) * rscale;
   gemv_finish<WT, 1>(a, r, res, yold, live, gated, argmax, 0, 1, tid, lane, wave, rv, ri, pre,
                      qkv);
+}
+
+template <typename WT, int KP, int NORM>
+__global__ __launch_bounds__(256) void gemv1k_kernel(const LinearArgs a) {
+  gemv1k_body<WT, KP, NORM>(a, blockIdx.x);
+}
+
+// Two one-row GEMVs over the same inputs in one launch: blocks [0, na) run `a` (bf16 weights,
+// K <= 2048 * KPA), the others `b` (float32 weights, K <= 2048 * KPB); no input transform.
+template <int KPA, int KPB>
+__global__ __launch_bounds__(256) void gemv1k_pair_kernel(const LinearArgs a, const LinearArgs b,
+                                                          const int na) {
+  const int blk = blockIdx.x;
+  if (blk < na) gemv1k_body<bf16_t, KPA, NORM_NONE>(a, blk);
+  else gemv1k_body<float, KPB, NORM_NONE>(b, blk - na);
 }
 
 // ---------------------------------------------------------------------------------------------
@@ -1546,6 +1588,21 @@ bool want_mfma(const LinearArgs& a) {
 }
 
 }  // namespace
+
+bool linear_pair_ok(const LinearArgs& a, const LinearArgs& b) {
+  auto plain = [](const LinearArgs& x) {
+    return x.M == 1 && x.norm == NORM_NONE && x.K >= 8 && x.K % 8 == 0 &&
+           (x.epi == EPI_STORE || x.epi == EPI_RESID || x.epi == EPI_BIAS_RESID) && x.n_per > 0;
+  };
+  return plain(a) && plain(b) && a.wdtype == 1 && a.K <= 2048 && b.wdtype == 0 && b.K <= 4096;
+}
+
+hipError_t launch_linear_pair(const LinearArgs& a, const LinearArgs& b, hipStream_t s) {
+  if (!linear_pair_ok(a, b)) return hipErrorInvalidValue;
+  const int na = gv_plan(a).blocks, nb = gv_plan(b).blocks;
+  hipLaunchKernelGGL((gemv1k_pair_kernel<1, 2>), dim3(na + nb), dim3(256), 0, s, a, b, na);
+  return hipGetLastError();
+}
 
 int argmax_parts_max(int n_out) {
   const int groups = ((n_out + 1) / 2 + GV_WAVES - 1) / GV_WAVES;

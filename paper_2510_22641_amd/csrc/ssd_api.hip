@@ -37,10 +37,11 @@ struct Layout {
       p_x, p_attn, p_ffn, ssq, attn_part, fold_q, fold_o,
       bucket, rope_cos, rope_sin, status, cur_tok, g_pending, g_draft, g_target,
       g_count, g_active, g_nactive, g_stats, g_ndraft, g_drafting, g_draft_w, conf_lg, gplanes,
-      total;
+      fold_fg, total;
   int rows_max, head_rows, parts_max, ctx_max, plane_rows, attn_rows;
   int gplane_rows = 0, gplane_ld = 0;  // tile-path input planes (0 rows: none)
   bool fold = false;  // the folded cross-attention matrices are carved (fold_q, fold_o)
+  bool fg = false;    // and the scores-from-the-layer-input matrices of layers 1..k (fold_fg)
 };
 
 int ctx_len_max(const ssd_dims& d) {
@@ -54,6 +55,19 @@ int ctx_len_max(const ssd_dims& d) {
 bool fold_cross(const ssd_dims& d) {
   return d.arch == SSD_ARCH_T5 && d.max_batch == 1 && cross_fold_ok(d.n_visual, d.d_head) &&
          d.n_visual <= d.d_head && (size_t)d.n_heads * d.n_visual <= 6144 && d.d_model <= 6144;
+}
+
+// With the cross-attention folded, the one-row steps of layers 1..k (draft steps, the verify's
+// last row, greedy steps) also take the folded scores from the layer's input and its attention
+// output, fg . [x; o] = F (x + W_o o) with F = fold_q diag(g): the output projection and the scores
+// then run in one launch, and the 1 / rms of the new residual is applied to the scores inside the
+// softmax of the next launch.  Needs bf16 weights, HD <= 2048 and d <= 2048 (the two halves of
+// the launch; the next launch reads the new residual row whole) and d_ff >= d (the row is kept
+// in the FFN buffer until the FFN).
+bool fold_fg_ok(const ssd_dims& d) {
+  const int HD = d.n_heads * d.d_head;
+  return fold_cross(d) && d.wdtype == SSD_BF16 && HD <= 2048 && d.d_model <= 2048 &&
+         d.d_ff >= d.d_model && d.d_model % 8 == 0 && HD % 8 == 0;
 }
 
 // Workspace layout: the scratch a chain of launches writes (residual rows, projections, operand
@@ -85,7 +99,7 @@ bool make_layout(const ssd_dims& d, Layout& L, bool allow_fold = true) {
   auto lane = [&](Layout& X, size_t R, size_t head_rows) {
     const size_t PRz = (size_t)L.plane_rows;
     X.x = take(R * D * 4);
-    X.x1 = take(B * D * 4);
+    X.x1 = take((B * D + HD) * 4);  // room for a one-row attention output right after the row
     X.qkv = take(R * 3 * HD * 4);
     X.q = take(R * HD * 4);
     X.attn = take(R * HD * 4);
@@ -119,6 +133,8 @@ bool make_layout(const ssd_dims& d, Layout& L, bool allow_fold = true) {
     const size_t fold = L.fold ? (size_t)d.n_layers * d.n_heads * d.n_visual * D * 4 : 0;
     L.fold_q = take(fold);
     L.fold_o = take(fold);
+    L.fg = L.fold && fold_fg_ok(d);
+    L.fold_fg = take(L.fg ? (size_t)d.draft_layers * d.n_heads * d.n_visual * (D + HD) * 4 : 0);
   }
   L.bias_tab = take(d.arch == SSD_ARCH_T5 ? (size_t)d.n_heads * d.max_seq * 4 : 0);
   L.bucket = take(d.arch == SSD_ARCH_T5 ? (size_t)d.max_seq * 4 : 0);
@@ -191,10 +207,14 @@ struct ssd_ctx {
   Layout L;
   int32_t* h_status = nullptr;  // pinned [4 + 256]: ssd_generate's read-back of the active counts,
                                 // then the drafting flags of confidence-stopped drafting
+  // the prefill's second stream (folded-scores products, created on first use, default priority)
+  hipStream_t side = nullptr;
+  hipEvent_t ev_fork = nullptr, ev_join = nullptr;
   bool is_static = false;       // made by ssd_create_static: workspace = the device's scratch
   int static_dev = -1;
   bool prefilled = false;
   bool fold_ready = false;  // fold_q / fold_o hold the prefilled sequence's cross-attention
+  bool fg_ready = false;    // fold_fg too (layers 1..k)
   // reuse bookkeeping: the last ssd_draft's arguments
   bool draft_valid = false;
   int draft_B = 0, draft_gamma = 0;
@@ -223,6 +243,10 @@ struct ssd_ctx {
   }
   size_t kv_elem() const { return d.kvdtype == SSD_BF16 ? 2 : 4; }
   size_t fold_layer_elems() const { return (size_t)d.n_heads * d.n_visual * d.d_model; }
+  float* fg_layer(int l) {
+    return reinterpret_cast<float*>(ws + L.fold_fg) +
+           (size_t)l * d.n_heads * d.n_visual * (d.d_model + d.n_heads * d.d_head);
+  }
 };
 
 #define HIP_TRY(expr)                          \
@@ -344,8 +368,12 @@ int run_layers(ssd_ctx* c, float* x, int B, int C, int pos_off, int l0, int l1, 
       rs.max_seq = d.max_seq; rs.status = status;
       HIP_TRY(launch_rope_scatter(rs, s));
     }
+    // one-row steps of layers 1..k with fold_fg: the attention output goes right after the
+    // residual row, so that [x; o] is one input row of the folded-scores GEMV
+    const bool fg = t5 && c->fg_ready && R == 1 && l < d.draft_layers;
     AttnArgs at;
-    at.q = q; at.out = attn; at.out_planes = skinny ? p_attn : nullptr; at.plane_rows = PR;
+    at.q = q; at.out = fg ? x + D : attn; at.out_planes = skinny ? p_attn : nullptr;
+    at.plane_rows = PR;
     at.part = c->at<float>(c->L.attn_part); at.part_rows = c->L.attn_rows;
     at.B = B; at.C = C; at.H = d.n_heads; at.dh = d.d_head;
     at.kvdtype = d.kvdtype; at.cross = 0; at.kv = paged(c, l, pos_off);
@@ -354,6 +382,27 @@ int run_layers(ssd_ctx* c, float* x, int B, int C, int pos_off, int l0, int l1, 
     at.scale = t5 ? 1.0f : (float)(1.0 / std::sqrt((double)d.d_head));
     at.status = status;
     HIP_TRY(launch_attention(at, s));
+    if (fg) {
+      // y = x + W_o o into the FFN buffer and the unnormalised scores fg . [x; o] in one launch,
+      // then x = y + fold_o . softmax(scores / rms(y)) per head
+      const int HN = d.n_heads * d.n_visual;
+      float* ybuf = ffn;
+      LinearArgs wo = lin(c);
+      wo.x = x + D; wo.ldx = HD; wo.M = 1; wo.K = HD;
+      wo.w[0] = lw.wo; wo.n_per = D; wo.epi = EPI_BIAS_RESID; wo.resid = x; wo.ldr = D;
+      wo.y = ybuf; wo.ldy = D;
+      LinearArgs sc = lin(c);
+      sc.x = x; sc.ldx = D + HD; sc.M = 1; sc.K = D + HD;
+      sc.w[0] = c->fg_layer(l); sc.wdtype = SSD_F32; sc.n_per = HN; sc.epi = EPI_STORE;
+      sc.y = q; sc.ldy = HD;
+      HIP_TRY(launch_linear_pair(wo, sc, s));
+      a = lin(c);
+      a.x = q; a.ldx = HD; a.M = 1; a.K = HN;
+      a.norm = NORM_SOFTMAX; a.group = d.n_visual; a.pre_row = ybuf; a.pre_len = D;
+      a.w[0] = c->at<float>(c->L.fold_o) + (size_t)l * c->fold_layer_elems(); a.wdtype = SSD_F32;
+      a.n_per = D; a.epi = EPI_BIAS_RESID; a.resid = ybuf; a.ldr = D; a.y = x; a.ldy = D;
+      HIP_TRY(run_linear(c, a));
+    } else {
     a = lin(c);
     a.x = attn; a.ldx = HD; a.M = R; a.K = HD;
     a.w[0] = lw.wo; a.n_per = D; a.epi = EPI_RESID; a.y = x; a.ldy = D;
@@ -395,6 +444,7 @@ int run_layers(ssd_ctx* c, float* x, int B, int C, int pos_off, int l0, int l1, 
       a.w[0] = lw.xo; a.n_per = D; a.epi = EPI_RESID; a.y = x; a.ldy = D;
       resid_out(a, lw.ffn_norm);
       HIP_TRY(linear(a, p_attn, HD));
+    }
     }
     // feed-forward
     a = lin(c);
@@ -876,6 +926,7 @@ int ssd_prefill(ssd_ctx* c, int B, int P, const int32_t* d_prompt, const void* d
   float* x = c->at<float>(c->L.x);
   int32_t* status = c->at<int32_t>(c->L.status);
   c->draft_valid = false;
+  bool side_used = false;
   HIP_TRY(launch_set_seq_len(c->kv.seq_len, B, 0, s));
   if (t5) {
     // cross-attention K/V of every layer from z
@@ -915,8 +966,31 @@ int ssd_prefill(ssd_ctx* c, int B, int P, const int32_t* d_prompt, const void* d
                                   c->at<float>(c->L.fold_q) + (size_t)l * c->fold_layer_elems(),
                                   c->at<float>(c->L.fold_o) + (size_t)l * c->fold_layer_elems(), s));
       }
+      if (c->L.fg && l + 1 == d.draft_layers) {
+        // the products of layers 1..k on a second stream, beside the prompt's pass through the
+        // decoder (which leaves most of the device idle); the context's stream waits for them
+        // before the prefill ends
+        if (!c->side) {
+          if (hipStreamCreateWithFlags(&c->side, hipStreamNonBlocking) != hipSuccess) {
+            c->side = nullptr;
+            return SSD_ERR_HIP;
+          }
+          if (hipEventCreateWithFlags(&c->ev_fork, hipEventDisableTiming) != hipSuccess ||
+              hipEventCreateWithFlags(&c->ev_join, hipEventDisableTiming) != hipSuccess)
+            return SSD_ERR_HIP;
+        }
+        HIP_TRY(hipEventRecord(c->ev_fork, s));
+        HIP_TRY(hipStreamWaitEvent(c->side, c->ev_fork, 0));
+        for (int f = 0; f < d.draft_layers; ++f)
+          HIP_TRY(launch_fold_fg(c->at<float>(c->L.fold_q) + (size_t)f * c->fold_layer_elems(),
+                                 c->layers[f].xattn_norm, c->layers[f].wo, d.wdtype,
+                                 d.n_heads * d.n_visual, D, HD, c->fg_layer(f), c->side));
+        HIP_TRY(hipEventRecord(c->ev_join, c->side));
+        side_used = true;
+      }
     }
     c->fold_ready = c->L.fold;
+    c->fg_ready = c->L.fg;
   }
   EmbedArgs e;
   e.x = x; e.B = B; e.C = Cx; e.d = D; e.embed = c->w.embed; e.vocab = d.vocab; e.wdtype = d.wdtype;
@@ -929,6 +1003,7 @@ int ssd_prefill(ssd_ctx* c, int B, int P, const int32_t* d_prompt, const void* d
                 nullptr);
   if (rc) return rc;
   HIP_TRY(launch_set_seq_len(c->kv.seq_len, B, Cx, s));
+  if (side_used) HIP_TRY(hipStreamWaitEvent(s, c->ev_join, 0));
   c->prefilled = true;
   return SSD_OK;
 }
@@ -1312,6 +1387,12 @@ void ssd_destroy(ssd_ctx* c) {
   for (auto& kv : c->graphs) (void)hipGraphExecDestroy(kv.second);
   for (hipEvent_t e : c->ev_pool) (void)hipEventDestroy(e);
   if (c->h_status) (void)hipHostFree(c->h_status);
+  if (c->side) {
+    (void)hipStreamSynchronize(c->side);
+    (void)hipStreamDestroy(c->side);
+  }
+  if (c->ev_fork) (void)hipEventDestroy(c->ev_fork);
+  if (c->ev_join) (void)hipEventDestroy(c->ev_join);
   if (c->is_static) {
     std::lock_guard<std::mutex> lock(g_static_mu);
     const int dev = c->static_dev;

@@ -392,3 +392,33 @@ def test_wide_ffn_rows_take_the_k_split_gemv():
     greedy = parity.device_run(dd, pt, vt, wl.new_tokens, 0)
     parity.check_run_against_oracle(dec, wl.shape, pr[0], z[0], greedy, 0, 0)
     assert dd.sync_status() == (0, 0)
+
+
+def test_folded_scores_from_layer_input_at_d2048():
+    """A T5-style decoder of FlanT5-xl width (d 2048, 32 heads of 64, 32 visual tokens), three
+    layers: the one-row steps of layers 1..k take the output projection and the folded
+    cross-attention scores from [x; o] in one launch (the scores matrix F and its product with
+    W_o, built at prefill) and apply 1 / rms of the new residual inside the next launch's softmax.
+    Drafts, verify logits and greedy steps follow the oracle, and the run agrees with an
+    unfolded two-sequence context within the tolerance while the token streams agree."""
+    from dataclasses import replace
+    wide = replace(synth.SMALL_T5_BF16, name="t5-d2048", n_layers=3, d_model=2048, n_heads=32,
+                   d_head=64, d_ff=2048, vocab=2000, n_visual=32)
+    wl = synth.S_T5.with_(name="s-t5-d2048", shape=wide, draft_layers=2, new_tokens=20)
+    runs = []
+    for mb in (1, 2):
+        dd, dec, pr, z, pt, vt = _setup(wl, seed=14, page_seed=4, max_batch=mb)
+        run = parity.device_run(dd, pt, vt, wl.new_tokens, wl.gamma, reuse=True)
+        parity.check_run_against_oracle(dec, wl.shape, pr[0], z[0], run, 0, wl.gamma)
+        if mb == 1:
+            greedy = parity.device_run(dd, pt, vt, wl.new_tokens, 0)
+            parity.check_run_against_oracle(dec, wl.shape, pr[0], z[0], greedy, 0, 0)
+        assert dd.sync_status() == (0, 0)
+        runs.append(run)
+    folded, unfolded = runs
+    for i, (ra, rb) in enumerate(zip(folded.rounds, unfolded.rounds)):
+        if not (np.array_equal(ra.drafts, rb.drafts) and np.array_equal(ra.targets, rb.targets)):
+            break
+        for j in range(ra.draft_logits.shape[1]):
+            parity.check_logits(ra.draft_logits[0, j], rb.draft_logits[0, j].astype(np.float64),
+                                wl.shape, f"round {i} draft {j}")
