@@ -419,6 +419,36 @@ def per_config(seed: int, steps: int) -> dict:
     return res
 
 
+def counter_pass(args):
+    """A short uncaptured pass for rocprofv3 --pmc: the workload's prefill and, for 'verify', three
+    speculative rounds (draft, verify reusing the layer-k states, accept)."""
+    import torch
+    import synth
+    from paper_2510_22641_amd import runtime
+    wl = synth.ALL[args.workload]
+    dd = runtime.from_workload(wl, args.seed)
+    dd.set_graphs(False)
+    pr = synth.make_prompts(wl.shape, args.seed, wl.batch, wl.prompt_len)
+    z = synth.make_visual(wl.shape, args.seed, wl.batch)
+    pt, vt = dd.upload_inputs(pr, z)
+    torch.cuda.synchronize()
+    print(f"[counter pass] {wl.name} set up", file=sys.stderr, flush=True)
+    pending, _ = dd.prefill(pt, vt)
+    torch.cuda.synchronize()
+    print(f"[counter pass] {wl.name} prefill done", file=sys.stderr, flush=True)
+    rounds = 3 if args.counter_pass == "verify" else 0
+    for _ in range(rounds):
+        d, _ = dd.draft(pending, wl.gamma)
+        t, _ = dd.verify(pending, d, wl.gamma, reuse=True)
+        dd.accept(d, t, pending, wl.gamma)
+    torch.cuda.synchronize()
+    status = dd.sync_status()
+    print(json.dumps({"counter_pass": args.counter_pass, "workload": wl.name, "rounds": rounds,
+                      "status": list(status)}), flush=True)
+    if tuple(status) != (0, 0):
+        raise RuntimeError(f"device status {status}")
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -442,6 +472,10 @@ def main():
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="only copy this many bytes device to device three times (the reference "
                          "reading for the HBM byte counters) and exit")
+    ap.add_argument("--counter-pass", choices=["verify", "prefill"], default=None,
+                    help="only run a short pass of --workload for hardware counters and exit, "
+                         "graphs off so that every kernel is its own dispatch: 'verify' = prefill "
+                         "and three speculative rounds, 'prefill' = one prefill")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU: the decode loop is not sharded (asked for {args.gpus})",
@@ -466,6 +500,10 @@ def main():
     import synth
     from paper_2510_22641_amd import runtime
     from paper_2510_22641_amd import ssd as abi
+
+    if args.counter_pass:
+        counter_pass(args)
+        return
 
     wl = synth.ALL[args.workload]
     sh = wl.shape
