@@ -395,6 +395,276 @@ __global__ __launch_bounds__(DH) void attn_combine_kernel(const AttnArgs a, cons
   }
 }
 
+// Causal self-attention of a prefill block on MFMA (float32 cache, no position bias): one block of
+// four waves per (64 query rows, head, sequence), wave w owning rows 16w..16w+15.  Keys advance in
+// tiles of 64 staged in LDS as bf16 hi / lo planes (K by key row, V transposed by dimension); the
+// next tile is loaded into registers while the current one is used.  Per 16-key sub-tile a wave
+// computes S^T = K . Q^T with v_mfma_f32_16x16x32_bf16 (hi.hi + hi.lo + lo.hi, about 16 mantissa
+// bits per operand), so lane l holds the scores of query l % 16; the online softmax (running max
+// and sum per query) therefore stays in the lane, and O^T += V^T . P^T takes the lane's own
+// probabilities as its B operand (the K index of the product runs over keys 4g..4g+3 of two
+// sub-tiles, g = l / 16, and the V^T operand is read in the same order).  Blocks are issued longest
+// (last query rows) first.
+template <int DH>
+__global__ __launch_bounds__(256, 2) void attn_mfma_kernel(const AttnArgs a, const int n_qt) {
+  constexpr int KT = 64;        // keys per tile
+  constexpr int KLD = DH + 8;   // bf16 per key row of the K planes
+  constexpr int VLD = KT + 4;   // bf16 per dimension row of the V^T planes (34 dwords: the
+                                // transposed stores of a wave hit 64 distinct banks)
+  constexpr int NC = DH / 32;   // head-dim chunks of the score products
+  constexpr int ND = DH / 16;   // output dimension tiles per wave
+  constexpr int KF = DH / 4;    // K floats a thread stages (4 threads per key)
+  constexpr int VF = DH / 8;    // V floats per key a thread stages (8 threads per key pair)
+  extern __shared__ __attribute__((aligned(16))) bf16_t am_s[];
+  bf16_t* Ks = am_s;                   // [2][KT][KLD]  hi, lo
+  bf16_t* Vt = am_s + 2 * KT * KLD;    // [2][DH][VLD]  hi, lo
+  int* pg = reinterpret_cast<int*>(Vt + 2 * DH * VLD);  // [n_pg] page-table entries of the keys
+
+  const int qt = n_qt - 1 - (int)blockIdx.x;
+  const int h = blockIdx.y, b = blockIdx.z;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int g = lane >> 4, c16 = lane & 15;
+  const int j0 = qt * 64;
+  const int nq = min(64, a.C - j0);
+  const int HD = a.H * DH;
+  const int base = a.kv.seq_len[b] + a.kv.pos_off;
+  int nk = base + j0 + nq;
+  if (nk > a.max_seq) {
+    if (tid == 0) atomicOr(a.status, SSD_DEV_CAPACITY);
+    nk = a.max_seq;
+  }
+  const int n_kt = (nk + KT - 1) / KT;
+  const float* Kp = reinterpret_cast<const float*>(a.kv.k);
+  const float* Vp = reinterpret_cast<const float*>(a.kv.v);
+  // the page-table entries of keys 0..nk-1 in LDS once, so that a tile's loads depend on one
+  // memory round trip, not two (-1: past the table)
+  const int n_pg = (nk + a.kv.page_size - 1) / a.kv.page_size;
+  for (int i = tid; i < n_pg; i += 256)
+    pg[i] = i < a.kv.max_pages ? a.kv.page_table[(size_t)b * a.kv.max_pages + i] : -1;
+  __syncthreads();
+
+  // staging roles: K key tid / 4, floats (tid % 4) * KF ..; V keys 2 (tid % 32) and + 1, floats
+  // (tid / 32) * VF .. (a wave's transposed stores then cover 32 key pairs of two dimension
+  // groups: 64 distinct banks)
+  const int kk_l = tid >> 2, kd0 = (tid & 3) * KF;
+  const int vp_l = tid & 31, vd0 = (tid >> 5) * VF;
+  float4 kr[KF / 4], vr[2][VF / 4];
+  bool kok = false, vok[2] = {false, false};
+  // pages hold a power of two of keys dividing the tile: a thread's keys sit at fixed page
+  // offsets and slots in every tile
+  const int lps = __builtin_ctz(a.kv.page_size), ppt = KT >> lps;
+  const int k_pg = kk_l >> lps, k_slot = kk_l & (a.kv.page_size - 1);
+  const int v_pg = (2 * vp_l) >> lps, v_slot = (2 * vp_l) & (a.kv.page_size - 1);
+  const size_t pstride = (size_t)a.H * a.kv.page_size * DH, hoff = (size_t)h * a.kv.page_size * DH;
+  auto fetch = [&](int kt) {
+    int page = pg[min(kt * ppt + k_pg, n_pg - 1)];
+    kok = kt * KT + kk_l < nk && page >= 0 && page < a.kv.n_pages;
+    const float* src = Kp + (size_t)(kok ? page : 0) * pstride + hoff + (size_t)k_slot * DH + kd0;
+#pragma unroll
+    for (int q = 0; q < KF / 4; ++q) kr[q] = reinterpret_cast<const float4*>(src)[q];
+    page = pg[min(kt * ppt + v_pg, n_pg - 1)];
+    const bool vp_ok = page >= 0 && page < a.kv.n_pages;
+    const float* vs = Vp + (size_t)(vp_ok ? page : 0) * pstride + hoff + (size_t)v_slot * DH + vd0;
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      vok[u] = vp_ok && kt * KT + 2 * vp_l + u < nk;
+#pragma unroll
+      for (int q = 0; q < VF / 4; ++q) vr[u][q] = reinterpret_cast<const float4*>(vs + u * DH)[q];
+    }
+  };
+  fetch(0);
+
+  // this wave's query rows as the B operand (hi / lo), pre-scaled; rows past nq repeat the last
+  bf16x8_t qh[NC], ql[NC];
+  {
+    const float* qrow = a.q + (size_t)(b * a.C + j0 + min(16 * wave + c16, nq - 1)) * HD + h * DH;
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      const float4 u0 = reinterpret_cast<const float4*>(qrow + 32 * c + 8 * g)[0];
+      const float4 u1 = reinterpret_cast<const float4*>(qrow + 32 * c + 8 * g)[1];
+      float f[8] = {u0.x, u0.y, u0.z, u0.w, u1.x, u1.y, u1.z, u1.w};
+#pragma unroll
+      for (int e = 0; e < 8; ++e) f[e] *= a.scale;
+      uint4 hi, lo;
+      split_bf16x8(f, hi, lo);
+      qh[c] = __builtin_bit_cast(bf16x8_t, hi);
+      ql[c] = __builtin_bit_cast(bf16x8_t, lo);
+    }
+  }
+  const int pq = base + j0 + 16 * wave + c16;  // position of this lane's query row
+  float m_run = -INFINITY, l_run = 0.f;
+  f32x4_t acc_o[ND];
+#pragma unroll
+  for (int t = 0; t < ND; ++t) acc_o[t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  for (int kt = 0; kt < n_kt; ++kt) {
+    __syncthreads();  // the previous tile's reads are done
+    {
+      // keys past the context (or on a missing page) stage as zeros: stale entries may hold
+      // anything, and a value row enters the products even with probability 0
+      if (__any(!kok || !vok[0] || !vok[1])) {
+#pragma unroll
+        for (int q = 0; q < KF / 4; ++q)
+          if (!kok) kr[q] = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+        for (int u = 0; u < 2; ++u)
+#pragma unroll
+          for (int q = 0; q < VF / 4; ++q)
+            if (!vok[u]) vr[u][q] = make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+#pragma unroll
+      for (int q = 0; q < KF / 8; ++q) {
+        const float4 u0 = kr[2 * q], u1 = kr[2 * q + 1];
+        const float f[8] = {u0.x, u0.y, u0.z, u0.w, u1.x, u1.y, u1.z, u1.w};
+        uint4 hi, lo;
+        split_bf16x8(f, hi, lo);
+        *reinterpret_cast<uint4*>(Ks + (size_t)kk_l * KLD + kd0 + 8 * q) = hi;
+        *reinterpret_cast<uint4*>(Ks + (size_t)(KT + kk_l) * KLD + kd0 + 8 * q) = lo;
+      }
+#pragma unroll
+      for (int q = 0; q < VF / 4; ++q) {
+        const float a0[4] = {vr[0][q].x, vr[0][q].y, vr[0][q].z, vr[0][q].w};
+        const float a1[4] = {vr[1][q].x, vr[1][q].y, vr[1][q].z, vr[1][q].w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const uint32_t hh = pack_bf16x2(a0[e], a1[e]);
+          const uint32_t ll = pack_bf16x2(a0[e] - __uint_as_float(hh << 16),
+                                          a1[e] - __uint_as_float(hh & 0xffff0000u));
+          const int dd = vd0 + 4 * q + e;
+          *reinterpret_cast<uint32_t*>(Vt + (size_t)dd * VLD + 2 * vp_l) = hh;
+          *reinterpret_cast<uint32_t*>(Vt + (size_t)(DH + dd) * VLD + 2 * vp_l) = ll;
+        }
+      }
+    }
+    __syncthreads();
+    if (kt + 1 < n_kt) fetch(kt + 1);
+
+    // scores S^T of the four 16-key sub-tiles; lane: keys 16 st + 4 g + e, query c16
+    f32x4_t sc[4];
+#pragma unroll
+    for (int st = 0; st < 4; ++st) {
+      f32x4_t acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      const bf16_t* kh = Ks + (size_t)(16 * st + c16) * KLD + 8 * g;
+      const bf16_t* kl = kh + (size_t)KT * KLD;
+#pragma unroll
+      for (int c = 0; c < NC; ++c) {
+        const bf16x8_t ah = *reinterpret_cast<const bf16x8_t*>(kh + 32 * c);
+        const bf16x8_t al = *reinterpret_cast<const bf16x8_t*>(kl + 32 * c);
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, qh[c], acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, ql[c], acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al, qh[c], acc, 0, 0, 0);
+      }
+      sc[st] = acc;
+    }
+    // causal mask (and keys past the context) where the tile reaches the wave's first query
+    // position or the end of the context; tile max per query
+    if (kt * KT + KT - 1 > base + j0 + 16 * wave || kt * KT + KT > nk) {
+#pragma unroll
+      for (int st = 0; st < 4; ++st)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int ki = kt * KT + 16 * st + 4 * g + e;
+          if (ki > pq || ki >= nk) sc[st][e] = -INFINITY;
+        }
+    }
+    float mt = -INFINITY;
+#pragma unroll
+    for (int st = 0; st < 4; ++st)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) mt = fmaxf(mt, sc[st][e]);
+    mt = fmaxf(mt, __shfl_xor(mt, 16, SSD_WAVE));
+    mt = fmaxf(mt, __shfl_xor(mt, 32, SSD_WAVE));
+    const float m_new = fmaxf(m_run, mt);
+    const float alpha = m_run == -INFINITY ? 0.f : expf(m_run - m_new);
+    float ls = 0.f;
+#pragma unroll
+    for (int st = 0; st < 4; ++st)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float pv = sc[st][e] == -INFINITY ? 0.f : expf(sc[st][e] - m_new);
+        sc[st][e] = pv;
+        ls += pv;
+      }
+    ls += __shfl_xor(ls, 16, SSD_WAVE);
+    ls += __shfl_xor(ls, 32, SSD_WAVE);
+    l_run = l_run * alpha + ls;
+    m_run = m_new;
+#pragma unroll
+    for (int t = 0; t < ND; ++t) acc_o[t] *= alpha;
+
+    // O^T += V^T . P^T over two 32-key chunks (sub-tiles 2kc, 2kc + 1)
+#pragma unroll
+    for (int kc = 0; kc < 2; ++kc) {
+      float pf[8];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        pf[e] = sc[2 * kc][e];
+        pf[4 + e] = sc[2 * kc + 1][e];
+      }
+      uint4 phu, plu;
+      split_bf16x8(pf, phu, plu);
+      const bf16x8_t ph = __builtin_bit_cast(bf16x8_t, phu), pl = __builtin_bit_cast(bf16x8_t, plu);
+#pragma unroll
+      for (int t = 0; t < ND; ++t) {
+        const bf16_t* vh = Vt + (size_t)(16 * t + c16) * VLD + 32 * kc + 4 * g;
+        const bf16_t* vl = vh + (size_t)DH * VLD;
+        const uint2 h0 = *reinterpret_cast<const uint2*>(vh);
+        const uint2 h1 = *reinterpret_cast<const uint2*>(vh + 16);
+        const uint2 l0 = *reinterpret_cast<const uint2*>(vl);
+        const uint2 l1 = *reinterpret_cast<const uint2*>(vl + 16);
+        const bf16x8_t ah = __builtin_bit_cast(bf16x8_t, make_uint4(h0.x, h0.y, h1.x, h1.y));
+        const bf16x8_t al = __builtin_bit_cast(bf16x8_t, make_uint4(l0.x, l0.y, l1.x, l1.y));
+        acc_o[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, ph, acc_o[t], 0, 0, 0);
+        acc_o[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, pl, acc_o[t], 0, 0, 0);
+        acc_o[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al, ph, acc_o[t], 0, 0, 0);
+      }
+    }
+  }
+
+  // lane: O^T[16 t + 4 g + e][query c16]
+  if (16 * wave + c16 < nq) {
+    const float inv = l_run > 0.f ? 1.0f / l_run : 0.f;
+    float* orow = a.out + (size_t)(b * a.C + j0 + 16 * wave + c16) * HD + h * DH;
+#pragma unroll
+    for (int t = 0; t < ND; ++t)
+      *reinterpret_cast<float4*>(orow + 16 * t + 4 * g) =
+          make_float4(acc_o[t][0] * inv, acc_o[t][1] * inv, acc_o[t][2] * inv, acc_o[t][3] * inv);
+  }
+}
+
+// LDS of attn_mfma_kernel: the K and V^T planes, then one page-table entry per page of max_seq.
+template <int DH>
+size_t attn_mfma_shm(const AttnArgs& a) {
+  const size_t planes = ((size_t)2 * 64 * (DH + 8) + (size_t)2 * DH * (64 + 4)) * sizeof(bf16_t);
+  return planes + (size_t)((a.max_seq + a.kv.page_size - 1) / a.kv.page_size) * sizeof(int);
+}
+
+// The MFMA prefill attention applies: self-attention of more than 16 rows a sequence over a
+// float32 cache whose pages hold 2..64 keys dividing 64, no position bias, no output planes.
+bool attn_mfma_ok(const AttnArgs& a) {
+  if (a.cross || a.C <= 16 || a.kvdtype != 0 || a.bias || a.out_planes || a.kv.page_size < 2 ||
+      64 % a.kv.page_size || (a.dh != 64 && a.dh != 128))
+    return false;
+  const size_t shm = a.dh == 64 ? attn_mfma_shm<64>(a) : attn_mfma_shm<128>(a);
+  return shm <= 80 * 1024;
+}
+
+template <int DH>
+hipError_t launch_attn_mfma(const AttnArgs& a, hipStream_t s) {
+  const size_t shm = attn_mfma_shm<DH>(a);
+  // the attribute is raised once to the largest size any launch may take (80 KB: two blocks a
+  // compute unit)
+  static bool attr = false;
+  if (!attr) {
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_mfma_kernel<DH>),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, 80 * 1024);
+    attr = true;
+  }
+  const int n_qt = (a.C + 63) / 64;
+  hipLaunchKernelGGL((attn_mfma_kernel<DH>), dim3(n_qt, a.H, a.B), dim3(256), shm, s, a, n_qt);
+  return hipGetLastError();
+}
+
 // Key splits of a launch with `groups` query blocks per sequence: long self-attention contexts
 // (capacity of 256 keys and more, up to 16 query rows) are split so that about 512 blocks share
 // the keys, at least 128 keys a split.
@@ -449,6 +719,7 @@ hipError_t launch_attn_dh(const AttnArgs& a, hipStream_t s) {
 
 template <typename KT>
 hipError_t launch_attn_t(const AttnArgs& a, hipStream_t s) {
+  if (attn_mfma_ok(a)) return a.dh == 64 ? launch_attn_mfma<64>(a, s) : launch_attn_mfma<128>(a, s);
   return a.dh == 64 ? launch_attn_dh<KT, 64>(a, s) : launch_attn_dh<KT, 128>(a, s);
 }
 

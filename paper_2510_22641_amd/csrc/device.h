@@ -13,12 +13,16 @@ typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ float bf16_to_f32(uint32_t h) { return __uint_as_float(h << 16); }
 
-// float -> bfloat16, round to nearest even (NaN kept quiet)
+// float -> bfloat16, round to nearest even (NaN kept quiet): gfx950's v_cvt_pk_bf16_f32
 __device__ __forceinline__ uint32_t f32_to_bf16(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return u >> 16;
+  return __builtin_bit_cast(uint16_t, (__bf16)f);
+}
+
+// Two floats -> two bfloat16 (a in the low half), one v_cvt_pk_bf16_f32.
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
+  typedef __bf16 bf16x2_v __attribute__((ext_vector_type(2)));
+  const bf16x2_v v = {(__bf16)a, (__bf16)b};
+  return __builtin_bit_cast(uint32_t, v);
 }
 
 // Unpack a 16-byte vector of 8 bf16 into floats.
@@ -32,14 +36,15 @@ __device__ __forceinline__ void unpack_bf16x8(const uint4& r, float* f) {
 // Split eight floats into bf16 planes hi = bf16(f), lo = bf16(f - hi): hi + lo carries about 16
 // mantissa bits, so two bf16 MFMAs over (hi, lo) act on near-fp32 activations.
 __device__ __forceinline__ void split_bf16x8(const float* f, uint4& hi, uint4& lo) {
-  uint32_t h[8], l[8];
+  uint32_t h[4], l[4];
 #pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    h[e] = f32_to_bf16(f[e]);
-    l[e] = f32_to_bf16(f[e] - bf16_to_f32(h[e]));
+  for (int e = 0; e < 4; ++e) {
+    h[e] = pack_bf16x2(f[2 * e], f[2 * e + 1]);
+    l[e] = pack_bf16x2(f[2 * e] - __uint_as_float(h[e] << 16),
+                       f[2 * e + 1] - __uint_as_float(h[e] & 0xffff0000u));
   }
-  hi = make_uint4(h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16), h[6] | (h[7] << 16));
-  lo = make_uint4(l[0] | (l[1] << 16), l[2] | (l[3] << 16), l[4] | (l[5] << 16), l[6] | (l[7] << 16));
+  hi = make_uint4(h[0], h[1], h[2], h[3]);
+  lo = make_uint4(l[0], l[1], l[2], l[3]);
 }
 
 // Eight consecutive elements of a weight (or KV) row, as raw registers until converted.

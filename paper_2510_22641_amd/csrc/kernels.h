@@ -104,6 +104,13 @@ struct LinearArgs {
   bf16_t* gemm_planes = nullptr;
   int gemm_plane_rows = 0;
   int gemm_plane_ld = 0;
+  // Tile path, residual projections (y += W . x): partial products over ranges of K, float32
+  // [kpart_max][gemm_plane_rows][kpart_ld], which a second launch adds to y in range order; null
+  // keeps one pass over K.  ksplit is set by the launcher.
+  float* kpart = nullptr;
+  int kpart_max = 0;
+  int kpart_ld = 0;
+  int ksplit = 1;
 };
 
 // Kernel-level timing of the one-row GEMV launches with K inputs, input normalisation `norm` and

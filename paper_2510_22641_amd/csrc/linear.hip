@@ -1046,9 +1046,30 @@ __global__ __launch_bounds__(256) void gemm3_kernel(const LinearArgs a) {
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
-  // row tiles vary fastest: the blocks that share a weight tile run back to back
-  const int m0 = blockIdx.x * TMR, n0 = blockIdx.y * BN;
+  // Tile of this block.  Workgroups are dealt to the 8 XCDs round-robin by linear id, and each
+  // XCD has its own L2, so the linear id is mapped to a contiguous range of tiles per XCD
+  // (row tiles fastest, then K ranges, then weight tiles): the blocks that share a weight tile,
+  // or a range of the input planes, run on one XCD and read it through one L2.
+  int rt, zs, ct;
+  {
+    const int nx = gridDim.x, nz = gridDim.z, T = nx * gridDim.y * nz;
+    const int id = blockIdx.x + nx * (blockIdx.y + gridDim.y * blockIdx.z);
+    const int xcd = id & 7, slot = id >> 3;
+    const int t = xcd * (T >> 3) + min(xcd, T & 7) + slot;
+    rt = t % nx;
+    const int rest = t / nx;
+    zs = rest % nz;
+    ct = rest / nz;
+  }
+  const int m0 = rt * TMR, n0 = ct * BN;
   const int K = a.K, M = a.M;
+  // K range of this block: all of K, or range zs of a.ksplit (whole steps each)
+  int nk = K / G3K, kb = 0;
+  if (!GATED && a.ksplit > 1) {
+    const int per = (nk + a.ksplit - 1) / a.ksplit;
+    kb = zs * per * G3K;
+    nk = min(per, nk - zs * per);
+  }
   const int n_out = GATED ? a.n_per : a.n_per * a.n_mats;
   const int mat = GATED ? 0 : n0 / a.n_per;  // tiles never straddle matrices (n_per % BN == 0)
   const int nbase = GATED ? n0 : n0 - mat * a.n_per;
@@ -1059,11 +1080,11 @@ __global__ __launch_bounds__(256) void gemm3_kernel(const LinearArgs a) {
   // elements from ak; weight row br, BQ * 8 elements from bk
   const int ar = tid / ATPR, ak = (tid % ATPR) * (AQ * 8);
   const int br = tid / BTPR, bk = (tid % BTPR) * (BQ * 8);
-  const bf16_t* hrow = a.in_planes + (size_t)min(m0 + ar, M - 1) * a.in_ld + ak;
+  const bf16_t* hrow = a.in_planes + (size_t)min(m0 + ar, M - 1) * a.in_ld + kb + ak;
   const bf16_t* lrow = hrow + (size_t)a.plane_rows * a.in_ld;
   const int bn = min(nbase + br, a.n_per - 1);
-  const bf16_t* wrow0 = w0 + (size_t)bn * K + bk;
-  const bf16_t* wrow1 = w1 + (size_t)bn * K + bk;
+  const bf16_t* wrow0 = w0 + (size_t)bn * K + kb + bk;
+  const bf16_t* wrow1 = w1 + (size_t)bn * K + kb + bk;
 
   f32x4_t acc[NB][IF][TJ];
 #pragma unroll
@@ -1073,7 +1094,6 @@ __global__ __launch_bounds__(256) void gemm3_kernel(const LinearArgs a) {
 #pragma unroll
       for (int j = 0; j < TJ; ++j) acc[b][i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  const int nk = K / G3K;
   typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
   u32x4_t rh[G3D][AQ], rl[G3D][AQ], rw[G3D][NB][BQ];
   // (macros, so that every slot index is a constant and the ring stays in registers)
@@ -1166,6 +1186,10 @@ __global__ __launch_bounds__(256) void gemm3_kernel(const LinearArgs a) {
         const int n = n0 + wn * (BN / 2) + 16 * j + (lane & 15);
         if (n >= n_out) continue;
         const float v = acc[0][i][j][e] * rsc;
+        if (!GATED && a.ksplit > 1) {
+          a.kpart[((size_t)zs * a.gemm_plane_rows + m) * a.kpart_ld + n] = v;
+          continue;
+        }
         float* yp = a.y + (size_t)m * a.ldy + n;
         if (GATED) {
           *yp = apply_epi_act(a.epi, v, acc[NB - 1][i][j][e] * rsc);
@@ -1223,6 +1247,29 @@ __global__ __launch_bounds__(256) void plane_prep_kernel(const float* __restrict
   if (lane == 0) red[wave] = s2;
   __syncthreads();
   if (tid == 0) stats[m] = make_float2(0.f, 1.0f / sqrtf(((red[0] + red[1]) + (red[2] + red[3])) / (float)K + eps));
+}
+
+// y[m][n] += (p_0 + p_1 + ... + p_{S-1})[m][n] over the K-range partials of the tile path, added
+// in range order (the stash, when set, receives the new y too); four outputs per thread.
+__global__ __launch_bounds__(256) void ksum_kernel(const LinearArgs a, int n_out) {
+  const int q = blockIdx.x * 256 + threadIdx.x;  // float4 index over M x n_out
+  const int per_row = n_out >> 2;
+  if (q >= a.M * per_row) return;
+  const int m = q / per_row, n = (q - m * per_row) * 4;
+  float4 p[4];
+#pragma unroll
+  for (int s = 0; s < 4; ++s)
+    if (s < a.ksplit)
+      p[s] = *reinterpret_cast<const float4*>(a.kpart + ((size_t)s * a.gemm_plane_rows + m) * a.kpart_ld + n);
+  float4 t = p[0];
+#pragma unroll
+  for (int s = 1; s < 4; ++s)
+    if (s < a.ksplit) { t.x += p[s].x; t.y += p[s].y; t.z += p[s].z; t.w += p[s].w; }
+  float4* yp = reinterpret_cast<float4*>(a.y + (size_t)m * a.ldy + n);
+  float4 y = *yp;
+  y.x += t.x; y.y += t.y; y.z += t.z; y.w += t.w;
+  *yp = y;
+  if (a.stash) *reinterpret_cast<float4*>(a.stash + (size_t)m * a.lds + n) = y;
 }
 
 template <bool GATED>
@@ -1735,9 +1782,22 @@ void launch_gemm3_t(const LinearArgs& a, bool rms, hipStream_t s) {
   constexpr int NB = GATED ? 2 : 1;
   const size_t shm = ((size_t)2 * TMR * G3KP * 2 + (size_t)2 * NB * BN * G3KP) * sizeof(bf16_t);
   const int n_out = GATED ? a.n_per : a.n_per * a.n_mats;
-  const dim3 grid((a.M + TMR - 1) / TMR, (n_out + BN - 1) / BN);
+  const dim3 grid((a.M + TMR - 1) / TMR, (n_out + BN - 1) / BN, GATED ? 1 : a.ksplit);
   if (rms) hipLaunchKernelGGL((gemm3_kernel<GATED, TMR, BN, true>), grid, dim3(256), shm, s, a);
   else hipLaunchKernelGGL((gemm3_kernel<GATED, TMR, BN, false>), grid, dim3(256), shm, s, a);
+}
+
+// Ranges of K for the tile path's residual projections: as many as keep every block of the grid
+// resident at once (two 128 x 128 blocks per compute unit: 61 KB of LDS each).  At the
+// LLaMA-7B shape's 608-row prefix (160 tiles over 4096 outputs) that is 3, measured faster than
+// 2 or 4 (whose fourth range spills into a second round of blocks) and than the 64 x 64 tiles.
+int ksplit_choice(int tiles) {
+  int dev = 0, n_cu = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      n_cu <= 0)
+    n_cu = 256;
+  return (2 * n_cu) / tiles;
 }
 
 // The plane GEMM when its buffer is there and the shape fits: RMSNorm or no norm, no argmax, K in
@@ -1759,6 +1819,26 @@ bool try_gemm3(LinearArgs a, hipStream_t s, hipError_t* err) {
   a.in_planes = a.gemm_planes;
   a.in_ld = a.gemm_plane_ld;
   a.plane_rows = a.gemm_plane_rows;
+  a.ksplit = 1;
+  // residual projections with too few 128 x 128 tiles: 128 x 128 tiles over S ranges of K, then
+  // the ordered sum of the S partials into y
+  if (!gated && !big && a.epi == EPI_RESID && a.kpart && a.M > 128 && n_out % 4 == 0 &&
+      n_out <= a.kpart_ld && a.ldy % 4 == 0 && (!a.stash || a.lds % 4 == 0)) {
+    const int tiles = ((a.M + 127) / 128) * ((n_out + 127) / 128);
+    const int nk = a.K / G3K;
+    int S = ksplit_choice(tiles);
+    if (S > a.kpart_max) S = a.kpart_max;
+    if (S > 4) S = 4;
+    while (S > 1 && (nk + S - 1) / S * (S - 1) >= nk) --S;  // every range holds a step
+    if (S > 1) {
+      a.ksplit = S;
+      launch_gemm3_t<false, 128, 128>(a, rms, s);
+      const int nq = a.M * (n_out / 4);
+      hipLaunchKernelGGL(ksum_kernel, dim3((nq + 255) / 256), dim3(256), 0, s, a, n_out);
+      *err = hipGetLastError();
+      return true;
+    }
+  }
   if (gated) launch_gemm3_t<true, 128, 64>(a, rms, s);
   else if (big) launch_gemm3_t<false, 128, 128>(a, rms, s);
   else launch_gemm3_t<false, 64, 64>(a, rms, s);

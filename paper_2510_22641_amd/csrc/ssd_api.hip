@@ -37,9 +37,10 @@ struct Layout {
       p_x, p_attn, p_ffn, ssq, attn_part, fold_q, fold_o,
       bucket, rope_cos, rope_sin, status, cur_tok, g_pending, g_draft, g_target,
       g_count, g_active, g_nactive, g_stats, g_ndraft, g_drafting, g_draft_w, conf_lg, gplanes,
-      fold_fg, total;
+      fold_fg, kpart, total;
   int rows_max, head_rows, parts_max, ctx_max, plane_rows, attn_rows;
   int gplane_rows = 0, gplane_ld = 0;  // tile-path input planes (0 rows: none)
+  int kpart_max = 0;                   // K-range partials of the tile path's residual projections
   bool fold = false;  // the folded cross-attention matrices are carved (fold_q, fold_o)
   bool fg = false;    // and the scores-from-the-layer-input matrices of layers 1..k (fold_fg)
 };
@@ -126,6 +127,9 @@ bool make_layout(const ssd_dims& d, Layout& L, bool allow_fold = true) {
     L.gplane_ld = (ld + 7) / 8 * 8;
     L.gplane_rows = (int)rows;
     L.gplanes = take((size_t)2 * rows * L.gplane_ld * 2);
+    // contexts beyond the skinny capacity and one 128-row tile: room for four K-range partials
+    L.kpart_max = (rows > (size_t)L.plane_rows && rows > 128) ? 4 : 0;
+    L.kpart = take((size_t)L.kpart_max * rows * D * 4);
   }
   L.vis = take(d.arch == SSD_ARCH_T5 ? B * (size_t)d.n_visual * D * 4 : 0);
   {
@@ -298,6 +302,11 @@ LinearArgs lin(ssd_ctx* c) {
     a.gemm_planes = c->at<bf16_t>(c->L.gplanes);
     a.gemm_plane_rows = c->L.gplane_rows;
     a.gemm_plane_ld = c->L.gplane_ld;
+    if (c->L.kpart_max > 0) {
+      a.kpart = c->at<float>(c->L.kpart);
+      a.kpart_max = c->L.kpart_max;
+      a.kpart_ld = (int)c->d.d_model;
+    }
   }
   a.eps = c->d.norm_eps;
   return a;

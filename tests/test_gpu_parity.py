@@ -422,3 +422,23 @@ def test_folded_scores_from_layer_input_at_d2048():
         for j in range(ra.draft_logits.shape[1]):
             parity.check_logits(ra.draft_logits[0, j], rb.draft_logits[0, j].astype(np.float64),
                                 wl.shape, f"round {i} draft {j}")
+
+
+@pytest.mark.parametrize("heads,d_head", [(2, 128), (4, 64)], ids=["dh128", "dh64"])
+def test_long_prefix_prefill_splits_residual_projections_over_k(heads, d_head):
+    """A LLaMA-style decoder with a 300-row visual prefix: the prefill's context block (307 rows)
+    is past the skinny capacity, so its projections take the tile GEMM, and the residual
+    projections (W_o, down) with few 128 x 128 tiles run over four ranges of K whose partial
+    products are added to the residual in range order; its causal self-attention takes the MFMA
+    kernel (five 64-row query tiles, keys in 64-key tiles, the last one ragged).  Prefill logits,
+    drafts, verify logits and greedy steps follow the oracle."""
+    from dataclasses import replace
+    long = replace(synth.SMALL_LLAMA_BF16, name="small-llama-long-prefix", n_visual=300,
+                   n_heads=heads, d_head=d_head)
+    wl = synth.S_LLAMA.with_(name="s-llama-long-prefix", shape=long, new_tokens=12)
+    dd, dec, pr, z, pt, vt = _setup(wl, seed=15, page_seed=6)
+    run = parity.device_run(dd, pt, vt, wl.new_tokens, wl.gamma, reuse=True)
+    parity.check_run_against_oracle(dec, wl.shape, pr[0], z[0], run, 0, wl.gamma)
+    greedy = parity.device_run(dd, pt, vt, wl.new_tokens, 0)
+    parity.check_run_against_oracle(dec, wl.shape, pr[0], z[0], greedy, 0, 0)
+    assert dd.sync_status() == (0, 0)
