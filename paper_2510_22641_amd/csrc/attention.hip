@@ -403,10 +403,13 @@ __global__ __launch_bounds__(DH) void attn_combine_kernel(const AttnArgs a, cons
 // bits per operand), so lane l holds the scores of query l % 16; the online softmax (running max
 // and sum per query) therefore stays in the lane, and O^T += V^T . P^T takes the lane's own
 // probabilities as its B operand (the K index of the product runs over keys 4g..4g+3 of two
-// sub-tiles, g = l / 16, and the V^T operand is read in the same order).  Blocks are issued longest
-// (last query rows) first.
+// sub-tiles, g = l / 16, and the V^T operand is read in the same order).  The block's 8 waves are
+// two halves over the same query rows: half 0 takes the even key tiles, half 1 the odd ones, each
+// with its own LDS stage, and the two running (max, sum, output) triples are merged through LDS at
+// the end, which halves the longest chain of key tiles.  Blocks are issued longest (last query
+// rows) first.
 template <int DH>
-__global__ __launch_bounds__(256, 2) void attn_mfma_kernel(const AttnArgs a, const int n_qt) {
+__global__ __launch_bounds__(512) void attn_mfma_kernel(const AttnArgs a, const int n_qt) {
   constexpr int KT = 64;        // keys per tile
   constexpr int KLD = DH + 8;   // bf16 per key row of the K planes
   constexpr int VLD = KT + 4;   // bf16 per dimension row of the V^T planes (34 dwords: the
@@ -415,14 +418,36 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(const AttnArgs a, con
   constexpr int ND = DH / 16;   // output dimension tiles per wave
   constexpr int KF = DH / 4;    // K floats a thread stages (4 threads per key)
   constexpr int VF = DH / 8;    // V floats per key a thread stages (8 threads per key pair)
+  constexpr int STAGE = 2 * KT * KLD + 2 * DH * VLD;  // bf16 of one half's stage
   extern __shared__ __attribute__((aligned(16))) bf16_t am_s[];
-  bf16_t* Ks = am_s;                   // [2][KT][KLD]  hi, lo
-  bf16_t* Vt = am_s + 2 * KT * KLD;    // [2][DH][VLD]  hi, lo
-  int* pg = reinterpret_cast<int*>(Vt + 2 * DH * VLD);  // [n_pg] page-table entries of the keys
+  const int half = threadIdx.x >> 8;
+  bf16_t* Ks = am_s + half * STAGE;    // [2][KT][KLD]  hi, lo
+  bf16_t* Vt = Ks + 2 * KT * KLD;      // [2][DH][VLD]  hi, lo
+  int* pg = reinterpret_cast<int*>(am_s + 2 * STAGE);  // [n_pg] page-table entries of the keys
 
-  const int qt = n_qt - 1 - (int)blockIdx.x;
-  const int h = blockIdx.y, b = blockIdx.z;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // (query tile, head, sequence) of this block: workgroups are dealt to the 8 XCDs round-robin
+  // by linear id, so the id is mapped to a contiguous range of tiles per XCD, query tiles fastest
+  // (longest first): the query tiles of a head share its keys and values in one XCD's L2
+  // (longest first); when an XCD's range is whole heads, its blocks go level by level over those
+  // heads, so that the blocks left for a second round on the XCD's compute units are short ones
+  int qt, h, b;
+  {
+    const int T = n_qt * gridDim.y * gridDim.z;
+    const int id = blockIdx.x + n_qt * (blockIdx.y + gridDim.y * blockIdx.z);
+    const int xcd = id & 7;
+    int slot = id >> 3;
+    const int start = xcd * (T >> 3) + min(xcd, T & 7), cnt = (T >> 3) + (xcd < (T & 7) ? 1 : 0);
+    if (start % n_qt == 0 && cnt % n_qt == 0) {
+      const int nh = cnt / n_qt;
+      slot = (slot % nh) * n_qt + slot / nh;
+    }
+    const int t = start + slot;
+    qt = n_qt - 1 - t % n_qt;
+    const int rest = t / n_qt;
+    h = rest % gridDim.y;
+    b = rest / gridDim.y;
+  }
+  const int tid = threadIdx.x & 255, lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 4, c16 = lane & 15;
   const int j0 = qt * 64;
   const int nq = min(64, a.C - j0);
@@ -439,7 +464,7 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(const AttnArgs a, con
   // the page-table entries of keys 0..nk-1 in LDS once, so that a tile's loads depend on one
   // memory round trip, not two (-1: past the table)
   const int n_pg = (nk + a.kv.page_size - 1) / a.kv.page_size;
-  for (int i = tid; i < n_pg; i += 256)
+  for (int i = threadIdx.x; i < n_pg; i += 512)
     pg[i] = i < a.kv.max_pages ? a.kv.page_table[(size_t)b * a.kv.max_pages + i] : -1;
   __syncthreads();
 
@@ -472,7 +497,7 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(const AttnArgs a, con
       for (int q = 0; q < VF / 4; ++q) vr[u][q] = reinterpret_cast<const float4*>(vs + u * DH)[q];
     }
   };
-  fetch(0);
+  if (half < n_kt) fetch(half);
 
   // this wave's query rows as the B operand (hi / lo), pre-scaled; rows past nq repeat the last
   bf16x8_t qh[NC], ql[NC];
@@ -497,9 +522,11 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(const AttnArgs a, con
 #pragma unroll
   for (int t = 0; t < ND; ++t) acc_o[t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  for (int kt = 0; kt < n_kt; ++kt) {
+  for (int it = 0; 2 * it < n_kt; ++it) {
+    const int kt = 2 * it + half;  // this half's tile (past n_kt: none, barriers only)
+    const bool live = kt < n_kt;
     __syncthreads();  // the previous tile's reads are done
-    {
+    if (live) {
       // keys past the context (or on a missing page) stage as zeros: stale entries may hold
       // anything, and a value row enters the products even with probability 0
       if (__any(!kok || !vok[0] || !vok[1])) {
@@ -537,7 +564,8 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(const AttnArgs a, con
       }
     }
     __syncthreads();
-    if (kt + 1 < n_kt) fetch(kt + 1);
+    if (!live) continue;
+    if (kt + 2 < n_kt) fetch(kt + 2);
 
     // scores S^T of the four 16-key sub-tiles; lane: keys 16 st + 4 g + e, query c16
     f32x4_t sc[4];
@@ -621,6 +649,31 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(const AttnArgs a, con
     }
   }
 
+  // half 1 hands its (max, sum, output) to half 0 through its own stage: lane-major, so that the
+  // same (wave, lane) of half 0 reads it back without bank conflicts
+  __syncthreads();
+  float* xo = reinterpret_cast<float*>(am_s + STAGE) + (size_t)wave * (ND * 4 + 2) * 64;
+  if (half == 1) {
+#pragma unroll
+    for (int t = 0; t < ND; ++t)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) xo[(4 * t + e) * 64 + lane] = acc_o[t][e];
+    xo[ND * 4 * 64 + lane] = m_run;
+    xo[(ND * 4 + 1) * 64 + lane] = l_run;
+  }
+  __syncthreads();
+  if (half == 1) return;
+  {
+    const float m2 = xo[ND * 4 * 64 + lane], l2 = xo[(ND * 4 + 1) * 64 + lane];
+    const float m = fmaxf(m_run, m2);
+    const float w1 = m_run == -INFINITY ? 0.f : expf(m_run - m);
+    const float w2 = m2 == -INFINITY ? 0.f : expf(m2 - m);
+    l_run = w1 * l_run + w2 * l2;
+#pragma unroll
+    for (int t = 0; t < ND; ++t)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) acc_o[t][e] = w1 * acc_o[t][e] + w2 * xo[(4 * t + e) * 64 + lane];
+  }
   // lane: O^T[16 t + 4 g + e][query c16]
   if (16 * wave + c16 < nq) {
     const float inv = l_run > 0.f ? 1.0f / l_run : 0.f;
@@ -632,11 +685,15 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(const AttnArgs a, con
   }
 }
 
+// LDS limit of attn_mfma_kernel (one block a compute unit: two 68 KB stages at dh 128 and the
+// page-table entries of up to 5120 pages)
+constexpr int ATTN_MFMA_LDS = 156 * 1024;
+
 // LDS of attn_mfma_kernel: the K and V^T planes, then one page-table entry per page of max_seq.
 template <int DH>
 size_t attn_mfma_shm(const AttnArgs& a) {
-  const size_t planes = ((size_t)2 * 64 * (DH + 8) + (size_t)2 * DH * (64 + 4)) * sizeof(bf16_t);
-  return planes + (size_t)((a.max_seq + a.kv.page_size - 1) / a.kv.page_size) * sizeof(int);
+  const size_t stage = ((size_t)2 * 64 * (DH + 8) + (size_t)2 * DH * (64 + 4)) * sizeof(bf16_t);
+  return 2 * stage + (size_t)((a.max_seq + a.kv.page_size - 1) / a.kv.page_size) * sizeof(int);
 }
 
 // The MFMA prefill attention applies: self-attention of more than 16 rows a sequence over a
@@ -646,22 +703,21 @@ bool attn_mfma_ok(const AttnArgs& a) {
       64 % a.kv.page_size || (a.dh != 64 && a.dh != 128))
     return false;
   const size_t shm = a.dh == 64 ? attn_mfma_shm<64>(a) : attn_mfma_shm<128>(a);
-  return shm <= 80 * 1024;
+  return shm <= (size_t)ATTN_MFMA_LDS;
 }
 
 template <int DH>
 hipError_t launch_attn_mfma(const AttnArgs& a, hipStream_t s) {
   const size_t shm = attn_mfma_shm<DH>(a);
-  // the attribute is raised once to the largest size any launch may take (80 KB: two blocks a
-  // compute unit)
+  // the attribute is raised once to the largest size any launch may take (ATTN_MFMA_LDS)
   static bool attr = false;
   if (!attr) {
     (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_mfma_kernel<DH>),
-                              hipFuncAttributeMaxDynamicSharedMemorySize, 80 * 1024);
+                              hipFuncAttributeMaxDynamicSharedMemorySize, ATTN_MFMA_LDS);
     attr = true;
   }
   const int n_qt = (a.C + 63) / 64;
-  hipLaunchKernelGGL((attn_mfma_kernel<DH>), dim3(n_qt, a.H, a.B), dim3(256), shm, s, a, n_qt);
+  hipLaunchKernelGGL((attn_mfma_kernel<DH>), dim3(n_qt, a.H, a.B), dim3(512), shm, s, a, n_qt);
   return hipGetLastError();
 }
 
