@@ -967,40 +967,43 @@ int ssd_prefill(ssd_ctx* c, int B, int P, const int32_t* d_prompt, const void* d
         void* dst = (char*)(which ? c->kv.xv : c->kv.xk) + (size_t)l * c->xkv_layer_elems() * c->kv_elem();
         HIP_TRY(launch_scatter_cross(tmp, dst, B, d.n_visual, d.n_heads, d.d_head, d.kvdtype, s));
       }
-      if (c->L.fold) {
+    }
+    // The folded cross-attention of every layer (and the folded-scores products of layers 1..k)
+    // on a second stream, beside the prompt's pass through the decoder, which leaves most of the
+    // device idle and does not read them (that pass runs the cross-attention unfolded); the
+    // context's stream waits for them before the prefill ends.  (Forking per layer, as soon as
+    // each layer's cross K/V exist, measured no faster.)
+    if (c->L.fold) {
+      if (!c->side) {
+        if (hipStreamCreateWithFlags(&c->side, hipStreamNonBlocking) != hipSuccess) {
+          c->side = nullptr;
+          return SSD_ERR_HIP;
+        }
+        if (hipEventCreateWithFlags(&c->ev_fork, hipEventDisableTiming) != hipSuccess ||
+            hipEventCreateWithFlags(&c->ev_join, hipEventDisableTiming) != hipSuccess)
+          return SSD_ERR_HIP;
+      }
+      HIP_TRY(hipEventRecord(c->ev_fork, s));
+      HIP_TRY(hipStreamWaitEvent(c->side, c->ev_fork, 0));
+      for (int l = 0; l < d.n_layers; ++l) {
         const size_t off = (size_t)l * c->xkv_layer_elems() * c->kv_elem();
+        float* fq = c->at<float>(c->L.fold_q) + (size_t)l * c->fold_layer_elems();
         HIP_TRY(launch_cross_fold((char*)c->kv.xk + off, (char*)c->kv.xv + off, d.kvdtype,
                                   c->layers[l].xq, c->layers[l].xo, d.wdtype, d.n_heads,
-                                  d.n_visual, d.d_head, D,
-                                  c->at<float>(c->L.fold_q) + (size_t)l * c->fold_layer_elems(),
-                                  c->at<float>(c->L.fold_o) + (size_t)l * c->fold_layer_elems(), s));
+                                  d.n_visual, d.d_head, D, fq,
+                                  c->at<float>(c->L.fold_o) + (size_t)l * c->fold_layer_elems(),
+                                  c->side));
+        if (c->L.fg && l < d.draft_layers)
+          HIP_TRY(launch_fold_fg(fq, c->layers[l].xattn_norm, c->layers[l].wo, d.wdtype,
+                                 d.n_heads * d.n_visual, D, HD, c->fg_layer(l), c->side));
       }
-      if (c->L.fg && l + 1 == d.draft_layers) {
-        // the products of layers 1..k on a second stream, beside the prompt's pass through the
-        // decoder (which leaves most of the device idle); the context's stream waits for them
-        // before the prefill ends
-        if (!c->side) {
-          if (hipStreamCreateWithFlags(&c->side, hipStreamNonBlocking) != hipSuccess) {
-            c->side = nullptr;
-            return SSD_ERR_HIP;
-          }
-          if (hipEventCreateWithFlags(&c->ev_fork, hipEventDisableTiming) != hipSuccess ||
-              hipEventCreateWithFlags(&c->ev_join, hipEventDisableTiming) != hipSuccess)
-            return SSD_ERR_HIP;
-        }
-        HIP_TRY(hipEventRecord(c->ev_fork, s));
-        HIP_TRY(hipStreamWaitEvent(c->side, c->ev_fork, 0));
-        for (int f = 0; f < d.draft_layers; ++f)
-          HIP_TRY(launch_fold_fg(c->at<float>(c->L.fold_q) + (size_t)f * c->fold_layer_elems(),
-                                 c->layers[f].xattn_norm, c->layers[f].wo, d.wdtype,
-                                 d.n_heads * d.n_visual, D, HD, c->fg_layer(f), c->side));
-        HIP_TRY(hipEventRecord(c->ev_join, c->side));
-        side_used = true;
-      }
+      HIP_TRY(hipEventRecord(c->ev_join, c->side));
+      side_used = true;
     }
-    c->fold_ready = c->L.fold;
-    c->fg_ready = c->L.fg;
   }
+  // the prompt's pass reads the cross K/V, never the folds (which are still being formed)
+  c->fold_ready = false;
+  c->fg_ready = false;
   EmbedArgs e;
   e.x = x; e.B = B; e.C = Cx; e.d = D; e.embed = c->w.embed; e.vocab = d.vocab; e.wdtype = d.wdtype;
   e.t0 = nullptr; e.t1 = d_prompt; e.ld1 = P; e.visual = d_visual; e.n_visual = d.n_visual;
@@ -1013,6 +1016,8 @@ int ssd_prefill(ssd_ctx* c, int B, int P, const int32_t* d_prompt, const void* d
   if (rc) return rc;
   HIP_TRY(launch_set_seq_len(c->kv.seq_len, B, Cx, s));
   if (side_used) HIP_TRY(hipStreamWaitEvent(s, c->ev_join, 0));
+  c->fold_ready = t5 && c->L.fold;
+  c->fg_ready = t5 && c->L.fg;
   c->prefilled = true;
   return SSD_OK;
 }

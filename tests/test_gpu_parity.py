@@ -442,3 +442,23 @@ def test_long_prefix_prefill_splits_residual_projections_over_k(heads, d_head):
     greedy = parity.device_run(dd, pt, vt, wl.new_tokens, 0)
     parity.check_run_against_oracle(dec, wl.shape, pr[0], z[0], greedy, 0, 0)
     assert dd.sync_status() == (0, 0)
+
+
+@pytest.mark.parametrize("width", [256, 2048], ids=["d256", "d2048"])
+def test_one_token_prompt_with_folded_cross_attention(width):
+    """A one-sequence T5 context prefilled from a one-token prompt: the prompt's pass through the
+    decoder is a single row, the case the one-row folded paths serve, while the folded
+    cross-attention (and, at d 2048, the folded-scores products) are still being formed on the
+    prefill's second stream; that pass must read the cross K/V instead.  Prefill logits, drafts,
+    verify logits and greedy steps follow the oracle."""
+    from dataclasses import replace
+    sh = replace(synth.SMALL_T5_BF16, name=f"t5-d{width}-p1", n_layers=3, d_model=width,
+                 n_heads=width // 64, d_head=64, d_ff=width, vocab=2000, n_visual=32)
+    wl = synth.S_T5.with_(name=f"s-t5-d{width}-p1", shape=sh, draft_layers=2, new_tokens=14,
+                          prompt_len=1)
+    dd, dec, pr, z, pt, vt = _setup(wl, seed=16, page_seed=2, max_batch=1)
+    run = parity.device_run(dd, pt, vt, wl.new_tokens, wl.gamma, reuse=True)
+    parity.check_run_against_oracle(dec, wl.shape, pr[0], z[0], run, 0, wl.gamma)
+    greedy = parity.device_run(dd, pt, vt, wl.new_tokens, 0)
+    parity.check_run_against_oracle(dec, wl.shape, pr[0], z[0], greedy, 0, 0)
+    assert dd.sync_status() == (0, 0)
