@@ -129,21 +129,32 @@ def dominant_kernel_name(sh) -> str:
     return "gemv1_kernel<%s, %d, 1>" % ("unsigned short" if sh.dtype == "bf16" else "float", kp)
 
 
+# the sources that define the one-row GEMV kernels (their hash ties a counter summary to them)
+GEMV_SOURCES = ("device.h", "gemv_common.h", "kernels.h", "linear.hip")
+
+
+def kernel_sources_sha256() -> str:
+    """sha256 over the GEMV kernel sources, concatenated in GEMV_SOURCES order."""
+    import hashlib
+    h = hashlib.sha256()
+    for name in GEMV_SOURCES:
+        h.update(open(os.path.join(ROOT, "paper_2510_22641_amd", "csrc", name), "rb").read())
+    return h.hexdigest()
+
+
 def counted_traffic(kernel: str):
     """HBM bytes per launch of the dominant kernel from the committed rocprofv3 counter summary
     (FETCH_SIZE and WRITE_SIZE runs scaled by a copy-kernel reading), or None when the summary is
-    missing or the kernel source has changed since the counters were taken."""
-    import hashlib
+    missing or the kernel sources have changed since the counters were taken."""
     import re
     path = os.path.join(ROOT, "profiles", "gemv1k_c3_flant5_xl_hbm_traffic.md")
-    src = os.path.join(ROOT, "paper_2510_22641_amd", "csrc", "linear.hip")
     if not os.path.exists(path):
         return None
     text = open(path).read()
     if f"`{kernel}`" not in text:
         return None
     fields = dict(re.findall(r"^([a-z_0-9]+): (\S+)$", text, re.M))
-    if fields.get("kernel_source_sha256") != hashlib.sha256(open(src, "rb").read()).hexdigest():
+    if fields.get("kernel_sources_sha256") != kernel_sources_sha256():
         return None
     return {"bytes": int(fields["traffic_bytes_per_launch"]),
             "algorithmic_bytes": int(fields["algorithmic_bytes_per_launch"]),
@@ -421,7 +432,8 @@ def per_config(seed: int, steps: int) -> dict:
 
 def counter_pass(args):
     """A short uncaptured pass for rocprofv3 --pmc: the workload's prefill and, for 'verify', three
-    speculative rounds (draft, verify reusing the layer-k states, accept)."""
+    speculative rounds (draft, verify reusing the layer-k states, accept), or, for 'generate', one
+    whole speculative job through ssd_generate (prefill included)."""
     import torch
     import synth
     from paper_2510_22641_amd import runtime
@@ -433,6 +445,15 @@ def counter_pass(args):
     pt, vt = dd.upload_inputs(pr, z)
     torch.cuda.synchronize()
     print(f"[counter pass] {wl.name} set up", file=sys.stderr, flush=True)
+    if args.counter_pass == "generate":
+        toks, st = dd.generate(pt, vt, wl.new_tokens, wl.gamma, speculative=True, reuse=True)
+        torch.cuda.synchronize()
+        status = dd.sync_status()
+        print(json.dumps({"counter_pass": "generate", "workload": wl.name, "rounds": st["rounds"],
+                          "status": list(status)}), flush=True)
+        if tuple(status) != (0, 0):
+            raise RuntimeError(f"device status {status}")
+        return
     pending, _ = dd.prefill(pt, vt)
     torch.cuda.synchronize()
     print(f"[counter pass] {wl.name} prefill done", file=sys.stderr, flush=True)
@@ -472,10 +493,11 @@ def main():
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="only copy this many bytes device to device three times (the reference "
                          "reading for the HBM byte counters) and exit")
-    ap.add_argument("--counter-pass", choices=["verify", "prefill"], default=None,
+    ap.add_argument("--counter-pass", choices=["verify", "prefill", "generate"], default=None,
                     help="only run a short pass of --workload for hardware counters and exit, "
                          "graphs off so that every kernel is its own dispatch: 'verify' = prefill "
-                         "and three speculative rounds, 'prefill' = one prefill")
+                         "and three speculative rounds, 'prefill' = one prefill, 'generate' = one "
+                         "whole speculative job through ssd_generate")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU: the decode loop is not sharded (asked for {args.gpus})",
