@@ -5,7 +5,8 @@ FlanT5-base (c2) and FlanT5-xl (c3): the whole job (64 and 128 tokens), every dr
 logit replayed through the oracle, and the benchmark's ``ssd_generate`` loop equal to the
 stepwise calls token for token and round for round.  LLaVA-1.5-7B shape (c5): prefill over the
 576-row visual prefix + 32 ids, then the first ten rounds (the float64 oracle holds 54 GB of
-weights and needs tens of seconds per prefill there).  FlanT5-xl sweep points chosen by kernel
+weights and needs tens of seconds per prefill there), and the whole 256-token job against the
+stepwise calls and the device's greedy decoding.  FlanT5-xl sweep points chosen by kernel
 path (one-row steps with 9-row verify chunks; batch 8 with 24- and 40-row verify chunks and
 72-row chunks on the two-plane skinny path): every sequence replayed for its first rounds, and
 every sequence of a batch against its own batch-1 run on the device.
@@ -67,8 +68,29 @@ def test_c3_flant5_xl_bench_configuration():
 
 @pytest.mark.timeout(900)
 def test_c5_llava_7b_prefill_and_first_rounds():
+    """The 608-row prefill and the first ten rounds replayed through the oracle; then the whole
+    256-token job: ssd_generate equal to the stepwise calls (tokens, rounds, accepted drafts) and
+    to the device's greedy decoding up to a near-tie of the oracle's logits."""
     wl = synth.C5
-    _check(wl, max_rounds=10, device_rounds=10)
+    dd, run10, pt, vt = _check(wl, max_rounds=10, device_rounds=10)
+    full = parity.device_run(dd, pt, vt, wl.new_tokens, wl.gamma, reuse=True, logits=False)
+    toks, stats = dd.generate(pt, vt, wl.new_tokens, wl.gamma, speculative=True, reuse=True)
+    assert toks.cpu().numpy()[0].tolist() == full.tokens[0]
+    assert stats["rounds"] == len(full.rounds)
+    assert stats["accepted"] == sum(int(r.accepted[0]) for r in full.rounds)
+    assert [int(r.accepted[0]) for r in full.rounds[:10]] == [int(r.accepted[0]) for r in run10.rounds]
+    gtoks, _ = dd.generate(pt, vt, wl.new_tokens, wl.gamma, speculative=False)
+    assert dd.sync_status() == (0, 0)
+    greedy = gtoks.cpu().numpy()[0].tolist()
+    print(f"[{wl.name}] whole job: {len(full.rounds)} rounds, speculative == greedy: "
+          f"{full.tokens[0] == greedy}", flush=True)
+    if full.tokens[0] != greedy:
+        # (the float64 oracle is built only to judge a difference: 54 GB and tens of seconds)
+        w, z, pr = parity.workload_inputs(wl, 0)
+        dec = Decoder(wl.shape, w, wl.draft_layers)
+        del w
+        parity.check_streams_agree_until_near_tie(dec, wl.shape, pr[0], z[0], full.tokens[0],
+                                                  greedy, "c5 ssd vs greedy")
 
 
 def _c4(b, k, g):
