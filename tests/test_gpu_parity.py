@@ -462,3 +462,17 @@ def test_one_token_prompt_with_folded_cross_attention(width):
     greedy = parity.device_run(dd, pt, vt, wl.new_tokens, 0)
     parity.check_run_against_oracle(dec, wl.shape, pr[0], z[0], greedy, 0, 0)
     assert dd.sync_status() == (0, 0)
+
+
+def test_verify_chunks_past_the_skinny_capacity_take_the_tile_path():
+    """Batch 8 with gamma = 16: a verify chunk is 8 x 17 = 136 rows, past the skinny path's 128, so
+    the verify's projections run on the tile GEMM (the residual ones over ranges of K) and each
+    sequence's 17-row causal self-attention on the MFMA kernel, its keys starting at that
+    sequence's cached length.  Every sequence's drafts and verify logits follow the oracle round
+    by round, with the accepted lengths bit-exact."""
+    wl = synth.S_LLAMA.with_(name="s-llama-b8-g16", gamma=16, new_tokens=40)
+    dd, dec, pr, z, pt, vt = _setup(wl, seed=17, batch=8, page_seed=7, extra_seq=wl.gamma)
+    run = parity.device_run(dd, pt, vt, wl.new_tokens, wl.gamma, reuse=True)
+    assert dd.sync_status() == (0, 0)
+    for s in range(8):
+        parity.check_run_against_oracle(dec, wl.shape, pr[s], z[s], run, s, wl.gamma)
