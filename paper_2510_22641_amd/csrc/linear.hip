@@ -1031,7 +1031,7 @@ __global__ __launch_bounds__(256) void gemm2_kernel(const LinearArgs a) {
 constexpr int G3K = 32, G3KP = G3K + 8, G3D = 4;  // G3D: the slot code below assumes 4
 
 template <bool GATED, int TMR, int BN, bool RMS>
-__global__ __launch_bounds__(256) void gemm3_kernel(const LinearArgs a) {
+__global__ __launch_bounds__(256, 2) void gemm3_kernel(const LinearArgs a) {
   constexpr int NB = GATED ? 2 : 1;
   constexpr int IF = TMR / 32;        // 16-row fragments per wave (the wave covers TMR / 2 rows)
   constexpr int TJ = BN / 32;         // 16-feature fragments per wave (BN / 2 features)
@@ -1161,7 +1161,44 @@ __global__ __launch_bounds__(256) void gemm3_kernel(const LinearArgs a) {
     }                                                                                      \
     __syncthreads();                                                                       \
   }
-  for (int kt = 0; kt < nk; kt += G3D) {
+  // Full groups of four steps whose next step exists run as straight-line code: with no branch
+  // between them the compiler can wait for just the slot it stages (a branch would make it wait
+  // for every load in flight, the whole ring).  The last group takes the guarded bodies.
+#define G3_BODY_U(NEXT)                                                                    \
+  {                                                                                        \
+    const int buf = step & 1;                                                              \
+    bf16x8_t fh[IF], fl[IF], fb[NB][TJ];                                                   \
+    _Pragma("unroll") for (int i = 0; i < IF; ++i) {                                       \
+      const size_t r = ((size_t)buf * TMR + wm * (TMR / 2) + 16 * i + (lane & 15)) * G3KP + kk; \
+      fh[i] = *reinterpret_cast<const bf16x8_t*>(Ah + r);                                  \
+      fl[i] = *reinterpret_cast<const bf16x8_t*>(Al + r);                                  \
+    }                                                                                      \
+    _Pragma("unroll") for (int b = 0; b < NB; ++b)                                         \
+    _Pragma("unroll") for (int j = 0; j < TJ; ++j)                                         \
+      fb[b][j] = *reinterpret_cast<const bf16x8_t*>(                                       \
+          Bs + (((size_t)buf * NB + b) * BN + wn * (BN / 2) + 16 * j + (lane & 15)) * G3KP + kk); \
+    _Pragma("unroll") for (int b = 0; b < NB; ++b)                                         \
+    _Pragma("unroll") for (int i = 0; i < IF; ++i)                                         \
+    _Pragma("unroll") for (int j = 0; j < TJ; ++j) {                                       \
+      acc[b][i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fh[i], fb[b][j], acc[b][i][j], 0, 0, 0); \
+      acc[b][i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fl[i], fb[b][j], acc[b][i][j], 0, 0, 0); \
+    }                                                                                      \
+    G3_STAGE(NEXT, buf ^ 1);                                                               \
+    G3_FETCH(NEXT, step + 1 + G3D);                                                        \
+    __syncthreads();                                                                       \
+  }
+  int kt = 0;
+  for (; kt + G3D < nk; kt += G3D) {
+    int step = kt;
+    G3_BODY_U(1)
+    step = kt + 1;
+    G3_BODY_U(2)
+    step = kt + 2;
+    G3_BODY_U(3)
+    step = kt + 3;
+    G3_BODY_U(0)
+  }
+  {
     int step = kt;
     G3_BODY(1)
     step = kt + 1;
@@ -1171,6 +1208,7 @@ __global__ __launch_bounds__(256) void gemm3_kernel(const LinearArgs a) {
     step = kt + 3;
     G3_BODY(0)
   }
+#undef G3_BODY_U
 #undef G3_BODY
 
   // epilogue: lane holds D[4 * (lane / 16) + e][lane % 16] of each 16x16 tile
