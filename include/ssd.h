@@ -139,7 +139,11 @@ typedef struct {
 
 typedef struct ssd_ctx ssd_ctx;
 
-/* Workspace bytes a context with these dimensions needs (0 if the dimensions are invalid). */
+/* Workspace bytes a context with these dimensions needs (0 if the dimensions are invalid): the
+ * residual rows, the staged layer-k states, the operand planes of the MFMA paths, argmax and
+ * attention partials, the bias / rotary tables, the folded T5 cross-attention of a one-sequence
+ * context, and, when a context block can exceed 128 rows, four float32 K-range partials of the
+ * prefill's residual projections. */
 size_t ssd_workspace_bytes(const ssd_dims* dims);
 
 /* Validate dimensions, copy the weight and KV descriptors, carve the workspace and build the
@@ -177,7 +181,10 @@ int ssd_create_static(const ssd_dims* dims, const ssd_weights* w, const ssd_kv* 
  * z; the prompt occupies positions 0..P-1.  LLaMA: the visual rows are the inputs of positions
  * 0..n_visual-1, the prompt follows.  Sets seq_len[b] to the context length and writes the full
  * model's argmax at the last context position to d_pending[b] (emitted token #1).
- * d_logits [B][V] float32 receives those logits when not NULL. */
+ * d_logits [B][V] float32 receives those logits when not NULL.  For a one-sequence T5 context
+ * the folded cross-attention of every layer is formed on a second stream of the context
+ * (created at the first prefill, default priority) beside the prompt's own pass; the context's
+ * stream waits for it before the call's work ends, so stream order holds for the caller. */
 int ssd_prefill(ssd_ctx* ctx, int B, int P, const int32_t* d_prompt, const void* d_visual,
                 int32_t* d_pending, float* d_logits);
 
