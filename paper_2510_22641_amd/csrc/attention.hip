@@ -721,6 +721,263 @@ hipError_t launch_attn_mfma(const AttnArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
+// One key split of a verify chunk's causal self-attention on MFMA (float32 cache, no position
+// bias; a chunk of at most 16 rows over a long context): one block of four waves per (head,
+// sequence, key split).  The split's keys are staged 128 at a time in LDS as bf16 hi / lo planes
+// (K by key row, V transposed); wave w takes keys 32w..32w+31 of each tile for all the chunk's
+// rows, with the scores S^T = K . Q^T and the output O^T += V^T . P^T of attn_mfma_kernel and a
+// running max and sum per query lane.  The four waves' triples are merged through LDS into the
+// split's partial (unnormalised output, max, sum), which attn_combine_kernel merges over the
+// splits as it does for attn_kernel.
+template <int DH>
+__global__ __launch_bounds__(256) void attn_mfma_chunk_kernel(const AttnArgs a, const int ks) {
+  constexpr int KT = 128;       // keys per tile
+  constexpr int KLD = DH + 8;   // bf16 per key row of the K planes
+  constexpr int VLD = KT + 4;   // bf16 per dimension row of the V^T planes (66 dwords: the
+                                // transposed stores of a wave hit 64 distinct banks)
+  constexpr int NC = DH / 32, ND = DH / 16;
+  constexpr int KF = DH / 2;    // K floats a thread stages (2 threads per key)
+  constexpr int VF = DH / 4;    // V floats per key a thread stages (4 threads per key pair)
+  extern __shared__ __attribute__((aligned(16))) bf16_t ac_s[];
+  bf16_t* Ks = ac_s;                   // [2][KT][KLD]
+  bf16_t* Vt = ac_s + 2 * KT * KLD;    // [2][DH][VLD]
+  int* pg = reinterpret_cast<int*>(Vt + 2 * DH * VLD);
+
+  const int h = blockIdx.x, b = blockIdx.y, split = blockIdx.z;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int g = lane >> 4, c16 = lane & 15;
+  const int C = a.C, HD = a.H * DH, ps = a.kv.page_size;
+  const int base = a.kv.seq_len[b] + a.kv.pos_off;
+  int nk_all = base + C;
+  if (nk_all > a.max_seq) {
+    if (tid == 0 && split == 0) atomicOr(a.status, SSD_DEV_CAPACITY);
+    nk_all = a.max_seq;
+  }
+  const int kfix = (a.max_seq + ks - 1) / ks;
+  const int k0 = split * kfix, k_end = min(nk_all, k0 + kfix);
+  const int nks = k_end > k0 ? k_end - k0 : 0;
+  const int p0 = k0 / ps;
+  const int n_pg = nks > 0 ? (k_end - 1) / ps - p0 + 1 : 0;
+  for (int i = tid; i < n_pg; i += 256)
+    pg[i] = p0 + i < a.kv.max_pages ? a.kv.page_table[(size_t)b * a.kv.max_pages + p0 + i] : -1;
+
+  // the chunk's rows as the B operand (hi / lo), pre-scaled; rows past C repeat the last
+  const int jq = min(c16, C - 1);
+  bf16x8_t qh[NC], ql[NC];
+  {
+    const float* qrow = a.q + (size_t)(b * C + jq) * HD + h * DH;
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      const float4 u0 = reinterpret_cast<const float4*>(qrow + 32 * c + 8 * g)[0];
+      const float4 u1 = reinterpret_cast<const float4*>(qrow + 32 * c + 8 * g)[1];
+      float f[8] = {u0.x, u0.y, u0.z, u0.w, u1.x, u1.y, u1.z, u1.w};
+#pragma unroll
+      for (int e = 0; e < 8; ++e) f[e] *= a.scale;
+      uint4 hi, lo;
+      split_bf16x8(f, hi, lo);
+      qh[c] = __builtin_bit_cast(bf16x8_t, hi);
+      ql[c] = __builtin_bit_cast(bf16x8_t, lo);
+    }
+  }
+  const int pq = base + jq;
+  float m_run = -INFINITY, l_run = 0.f;
+  f32x4_t acc_o[ND];
+#pragma unroll
+  for (int t = 0; t < ND; ++t) acc_o[t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  const float* Kp = reinterpret_cast<const float*>(a.kv.k);
+  const float* Vp = reinterpret_cast<const float*>(a.kv.v);
+  const int kk_l = tid >> 1, kd0 = (tid & 1) * KF;   // K staging: key, first float
+  const int vp_l = tid & 63, vd0 = (tid >> 6) * VF;  // V staging: key pair, first float
+  __syncthreads();  // page entries
+
+  for (int t0 = 0; t0 < nks; t0 += KT) {
+    if (t0 > 0) __syncthreads();  // the previous tile's reads are done
+    {
+      // key ki = k0 + t0 + key of the tile: its page entry pg[ki / ps - p0]; keys past the split
+      // (or on a missing page) stage as zeros
+      int ki = k0 + t0 + kk_l;
+      bool ok = ki < k_end;
+      int pe = pg[min(ki, k_end - 1) / ps - p0];
+      ok = ok && pe >= 0 && pe < a.kv.n_pages;
+      const float* src = Kp + (((size_t)(ok ? pe : 0) * a.H + h) * ps + (ok ? ki % ps : 0)) * DH + kd0;
+#pragma unroll
+      for (int q = 0; q < KF / 8; ++q) {
+        const float4 u0 = ok ? reinterpret_cast<const float4*>(src)[2 * q] : make_float4(0.f, 0.f, 0.f, 0.f);
+        const float4 u1 = ok ? reinterpret_cast<const float4*>(src)[2 * q + 1] : make_float4(0.f, 0.f, 0.f, 0.f);
+        const float f[8] = {u0.x, u0.y, u0.z, u0.w, u1.x, u1.y, u1.z, u1.w};
+        uint4 hi, lo;
+        split_bf16x8(f, hi, lo);
+        *reinterpret_cast<uint4*>(Ks + (size_t)kk_l * KLD + kd0 + 8 * q) = hi;
+        *reinterpret_cast<uint4*>(Ks + (size_t)(KT + kk_l) * KLD + kd0 + 8 * q) = lo;
+      }
+      float4 vr[2][VF / 4];
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        ki = k0 + t0 + 2 * vp_l + u;
+        ok = ki < k_end;
+        pe = pg[min(ki, k_end - 1) / ps - p0];
+        ok = ok && pe >= 0 && pe < a.kv.n_pages;
+        const float* vs = Vp + (((size_t)(ok ? pe : 0) * a.H + h) * ps + (ok ? ki % ps : 0)) * DH + vd0;
+#pragma unroll
+        for (int q = 0; q < VF / 4; ++q)
+          vr[u][q] = ok ? reinterpret_cast<const float4*>(vs)[q] : make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+#pragma unroll
+      for (int q = 0; q < VF / 4; ++q) {
+        const float a0[4] = {vr[0][q].x, vr[0][q].y, vr[0][q].z, vr[0][q].w};
+        const float a1[4] = {vr[1][q].x, vr[1][q].y, vr[1][q].z, vr[1][q].w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const uint32_t hh = pack_bf16x2(a0[e], a1[e]);
+          const uint32_t ll = pack_bf16x2(a0[e] - __uint_as_float(hh << 16),
+                                          a1[e] - __uint_as_float(hh & 0xffff0000u));
+          const int dd = vd0 + 4 * q + e;
+          *reinterpret_cast<uint32_t*>(Vt + (size_t)dd * VLD + 2 * vp_l) = hh;
+          *reinterpret_cast<uint32_t*>(Vt + (size_t)(DH + dd) * VLD + 2 * vp_l) = ll;
+        }
+      }
+    }
+    __syncthreads();
+
+    // this wave's two 16-key sub-tiles (keys 32 wave + 16 s + 4 g + e of the tile)
+    f32x4_t sc[2];
+#pragma unroll
+    for (int s2 = 0; s2 < 2; ++s2) {
+      f32x4_t acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      const bf16_t* kh = Ks + (size_t)(32 * wave + 16 * s2 + c16) * KLD + 8 * g;
+      const bf16_t* kl = kh + (size_t)KT * KLD;
+#pragma unroll
+      for (int c = 0; c < NC; ++c) {
+        const bf16x8_t ah = *reinterpret_cast<const bf16x8_t*>(kh + 32 * c);
+        const bf16x8_t al = *reinterpret_cast<const bf16x8_t*>(kl + 32 * c);
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, qh[c], acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, ql[c], acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al, qh[c], acc, 0, 0, 0);
+      }
+      sc[s2] = acc;
+    }
+    float mt = -INFINITY;
+#pragma unroll
+    for (int s2 = 0; s2 < 2; ++s2)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int ki = k0 + t0 + 32 * wave + 16 * s2 + 4 * g + e;
+        if (ki >= k_end || ki > pq) sc[s2][e] = -INFINITY;
+        mt = fmaxf(mt, sc[s2][e]);
+      }
+    mt = fmaxf(mt, __shfl_xor(mt, 16, SSD_WAVE));
+    mt = fmaxf(mt, __shfl_xor(mt, 32, SSD_WAVE));
+    const float m_new = fmaxf(m_run, mt);
+    const float alpha = m_run == -INFINITY ? 0.f : expf(m_run - m_new);
+    float ls = 0.f, pf[8];
+#pragma unroll
+    for (int s2 = 0; s2 < 2; ++s2)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float pv = sc[s2][e] == -INFINITY ? 0.f : expf(sc[s2][e] - m_new);
+        pf[4 * s2 + e] = pv;
+        ls += pv;
+      }
+    ls += __shfl_xor(ls, 16, SSD_WAVE);
+    ls += __shfl_xor(ls, 32, SSD_WAVE);
+    l_run = l_run * alpha + ls;
+    m_run = m_new;
+    uint4 phu, plu;
+    split_bf16x8(pf, phu, plu);
+    const bf16x8_t ph = __builtin_bit_cast(bf16x8_t, phu), pl = __builtin_bit_cast(bf16x8_t, plu);
+#pragma unroll
+    for (int t = 0; t < ND; ++t) {
+      acc_o[t] *= alpha;
+      const bf16_t* vh = Vt + (size_t)(16 * t + c16) * VLD + 32 * wave + 4 * g;
+      const bf16_t* vl = vh + (size_t)DH * VLD;
+      const uint2 h0 = *reinterpret_cast<const uint2*>(vh);
+      const uint2 h1 = *reinterpret_cast<const uint2*>(vh + 16);
+      const uint2 l0 = *reinterpret_cast<const uint2*>(vl);
+      const uint2 l1 = *reinterpret_cast<const uint2*>(vl + 16);
+      const bf16x8_t ah = __builtin_bit_cast(bf16x8_t, make_uint4(h0.x, h0.y, h1.x, h1.y));
+      const bf16x8_t al = __builtin_bit_cast(bf16x8_t, make_uint4(l0.x, l0.y, l1.x, l1.y));
+      acc_o[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, ph, acc_o[t], 0, 0, 0);
+      acc_o[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, pl, acc_o[t], 0, 0, 0);
+      acc_o[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al, ph, acc_o[t], 0, 0, 0);
+    }
+  }
+
+  // merge the four waves' (max, sum, output) through LDS (lane-major), then the split's partial
+  __syncthreads();
+  float* xo = reinterpret_cast<float*>(ac_s);
+  float* mine = xo + (size_t)wave * (ND * 4 + 2) * 64;
+#pragma unroll
+  for (int t = 0; t < ND; ++t)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) mine[(4 * t + e) * 64 + lane] = acc_o[t][e];
+  mine[ND * 4 * 64 + lane] = m_run;
+  mine[(ND * 4 + 1) * 64 + lane] = l_run;
+  __syncthreads();
+  if (wave != 0 || c16 >= C) return;
+  float mw[4], M = -INFINITY;
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    mw[w] = xo[(size_t)w * (ND * 4 + 2) * 64 + ND * 4 * 64 + lane];
+    M = fmaxf(M, mw[w]);
+  }
+  float fw[4], L = 0.f;
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    fw[w] = mw[w] == -INFINITY ? 0.f : expf(mw[w] - M);
+    L = fmaf(fw[w], xo[(size_t)w * (ND * 4 + 2) * 64 + (ND * 4 + 1) * 64 + lane], L);
+  }
+  float* pp = a.part + (((size_t)(b * C + c16) * a.H + h) * ks + split) * (DH + 2);
+#pragma unroll
+  for (int t = 0; t < ND; ++t) {
+    float o4[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      float v = 0.f;
+#pragma unroll
+      for (int w = 0; w < 4; ++w) v = fmaf(fw[w], xo[(size_t)w * (ND * 4 + 2) * 64 + (4 * t + e) * 64 + lane], v);
+      o4[e] = v;
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e) pp[16 * t + 4 * g + e] = o4[e];
+  }
+  if (g == 0) {
+    pp[DH] = M;
+    pp[DH + 1] = L;
+  }
+}
+
+// LDS of attn_mfma_chunk_kernel: the K and V^T planes of a 128-key tile, then the page entries of
+// one split's keys.
+template <int DH>
+size_t attn_chunk_shm(const AttnArgs& a, int ks) {
+  const size_t planes = ((size_t)2 * 128 * (DH + 8) + (size_t)2 * DH * (128 + 4)) * sizeof(bf16_t);
+  const int kfix = (a.max_seq + ks - 1) / ks;
+  return planes + (size_t)(kfix / a.kv.page_size + 2) * sizeof(int);
+}
+
+// The MFMA chunk attention applies: self-attention of 2..16 rows a sequence over a long float32
+// cache split into ks > 1 key ranges (partials merged by attn_combine_kernel), even pages, no
+// position bias.
+bool attn_chunk_ok(const AttnArgs& a, int ks) {
+  if (a.cross || a.C < 2 || a.C > 16 || ks < 2 || a.kvdtype != 0 || a.bias || !a.part ||
+      a.kv.page_size < 2 || (a.dh != 64 && a.dh != 128))
+    return false;
+  const size_t shm = a.dh == 64 ? attn_chunk_shm<64>(a, ks) : attn_chunk_shm<128>(a, ks);
+  return shm <= (size_t)156 * 1024;
+}
+
+template <int DH>
+void launch_attn_chunk(const AttnArgs& a, int ks, hipStream_t s) {
+  static bool attr = false;
+  if (!attr) {
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_mfma_chunk_kernel<DH>),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, 156 * 1024);
+    attr = true;
+  }
+  hipLaunchKernelGGL((attn_mfma_chunk_kernel<DH>), dim3(a.H, a.B, ks), dim3(256),
+                     attn_chunk_shm<DH>(a, ks), s, a, ks);
+}
+
 // Key splits of a launch with `groups` query blocks per sequence: long self-attention contexts
 // (capacity of 256 keys and more, up to 16 query rows) are split so that about 512 blocks share
 // the keys, at least 128 keys a split.
@@ -760,7 +1017,9 @@ hipError_t launch_attn_dh(const AttnArgs& a, hipStream_t s) {
     const int s_stride = (((nk_max + ks - 1) / ks) + 63) & ~63;
     dim3 grid(a.H, a.B, groups * ks);
     const size_t shm = (size_t)QB * s_stride * sizeof(float);
-    if (rs)
+    if (sizeof(KT) == 4 && attn_chunk_ok(a, ks))
+      launch_attn_chunk<DH>(a, ks, s);
+    else if (rs)
       hipLaunchKernelGGL((attn_kernel<KT, DH, QB, true>), grid, dim3(256), shm, s, a, s_stride, ks);
     else
       hipLaunchKernelGGL((attn_kernel<KT, DH, QB, false>), grid, dim3(256), shm, s, a, s_stride, ks);
