@@ -529,10 +529,10 @@ __global__ __launch_bounds__(256) void gemv1k_pair_kernel(const LinearArgs a, co
 // Skinny MFMA path: 2..128 input rows (the verify chunk), bf16 weights, 16 rows per grid row.
 // A block owns NT tiles of 16 output features (the A rows of v_mfma_f32_16x16x32_bf16) and its 4
 // waves split K; the input rows are the B columns, and every activation fragment a wave loads
-// feeds the MFMAs of all NT tiles.  One tile per block for the projections (their grids, 128-384
-// blocks, need the parallelism); four for the many tiles of the LM head, where the shared
-// activation loads pay (measured at the FlanT5-xl verify shapes, 6 rows: W_o 7.0 us with one tile
-// against 15.7 with four; LM head 39 against 35).  The inputs arrive as two bf16 planes
+// feeds the MFMAs of all NT tiles.  One tile per block for the projections whose tiles do not
+// outnumber the compute units (their grids need the parallelism), up to three for those that do,
+// four for the many tiles of the LM head (the launcher below; measured at the FlanT5-xl verify
+// shapes, 6 rows: W_o 7.0 us with one tile against 15.7 with four; LM head 39 against 35).  The inputs arrive as two bf16 planes
 // hi = bf16(v), lo = bf16(v - hi) of v = g * x (g the RMSNorm gain, or 1), written once by their
 // producer; multiplying both planes keeps the activations at about 16 mantissa bits while the
 // weights are read once.  RMSNorm is folded: 1/rms of each row comes from partial sums of squares
@@ -1699,42 +1699,57 @@ bool skinny_ok(int M, int K, int wdtype) { return wdtype == 1 && M >= 2 && M <= 
 
 int skinny_blocks(int n_out) { return (n_out + 15) / 16; }
 
+// Steps per batch of loads that the registers hold, by weight tiles per wave (tiles x matrices,
+// nm): PACK, with one input plane, 12 for one, 8 for two, 4 for three or four, 2 for six; the
+// two-plane form 8 / nm.  0: no such variant (several projection tiles per block are PACK only).
+constexpr int skinny_cap(bool pack, int nm, int nt) {
+  return pack ? (nm == 1 ? 12 : (nm == 2 ? 8 : (nm <= 4 ? 4 : 2)))
+              : (nt > 1 && nt < 4 ? 0 : (8 / nm > 0 ? 8 / nm : 1));
+}
+
 // (only the depths the launcher can pick for each variant are instantiated)
-template <bool PACK, int SK>
-void launch_skinny_sk(const LinearArgs& b, bool gated, bool rms, int tiles, dim3 block,
-                      hipStream_t s) {
-  constexpr int cap1 = PACK ? 12 : 8, cap_g = PACK ? 8 : 4, cap4 = PACK ? 4 : 2;
-  if (b.epi == EPI_ARGMAX) {
-    if constexpr (SK <= cap4) {
-      const dim3 grid((tiles + 3) / 4, (b.M + 15) / 16);
-      if (rms) hipLaunchKernelGGL((gemv_mfma_kernel<false, true, 4, PACK, SK>), grid, block, 0, s, b);
-      else hipLaunchKernelGGL((gemv_mfma_kernel<false, false, 4, PACK, SK>), grid, block, 0, s, b);
-    }
-    return;
-  }
-  const dim3 grid(tiles, (b.M + 15) / 16);
-  if (gated) {
-    if constexpr (SK <= cap_g) {
-      if (rms) hipLaunchKernelGGL((gemv_mfma_kernel<true, true, 1, PACK, SK>), grid, block, 0, s, b);
-      else hipLaunchKernelGGL((gemv_mfma_kernel<true, false, 1, PACK, SK>), grid, block, 0, s, b);
-    }
-    return;
-  }
-  if constexpr (SK <= cap1) {
-    if (rms) hipLaunchKernelGGL((gemv_mfma_kernel<false, true, 1, PACK, SK>), grid, block, 0, s, b);
-    else hipLaunchKernelGGL((gemv_mfma_kernel<false, false, 1, PACK, SK>), grid, block, 0, s, b);
+template <bool PACK, int SK, int NT, bool G>
+void launch_skinny_nt(const LinearArgs& b, bool rms, int tiles, dim3 block, hipStream_t s) {
+  if constexpr (SK <= skinny_cap(PACK, NT * (G ? 2 : 1), NT)) {
+    const dim3 grid((tiles + NT - 1) / NT, (b.M + 15) / 16);
+    if (rms) hipLaunchKernelGGL((gemv_mfma_kernel<G, true, NT, PACK, SK>), grid, block, 0, s, b);
+    else hipLaunchKernelGGL((gemv_mfma_kernel<G, false, NT, PACK, SK>), grid, block, 0, s, b);
   }
 }
 
-// Steps per batch: as many as the registers allow (the two-plane form: 8 weight-and-input steps
-// per tile and matrix; PACK, with one input plane: 12 for one weight matrix, 8 for the gated
-// pair, 4 for the LM head's four tiles), then balanced so that the wave's last batch is not a
-// short one padded with clamped re-reads.
+template <bool PACK, int SK>
+void launch_skinny_sk(const LinearArgs& b, bool gated, bool rms, int tiles, int nt, dim3 block,
+                      hipStream_t s) {
+  if (b.epi == EPI_ARGMAX) return launch_skinny_nt<PACK, SK, 4, false>(b, rms, tiles, block, s);
+  switch (nt) {
+    case 1:
+      return gated ? launch_skinny_nt<PACK, SK, 1, true>(b, rms, tiles, block, s)
+                   : launch_skinny_nt<PACK, SK, 1, false>(b, rms, tiles, block, s);
+    case 2:
+      return gated ? launch_skinny_nt<PACK, SK, 2, true>(b, rms, tiles, block, s)
+                   : launch_skinny_nt<PACK, SK, 2, false>(b, rms, tiles, block, s);
+    default:
+      return gated ? launch_skinny_nt<PACK, SK, 3, true>(b, rms, tiles, block, s)
+                   : launch_skinny_nt<PACK, SK, 3, false>(b, rms, tiles, block, s);
+  }
+}
+
+// Tiles per block: four for the LM head's argmax launch; for a projection one, unless its tiles
+// outnumber the compute units, then as many as bring the grid down to one block per unit (at most
+// three, PACK only).  Every input fragment a wave loads then feeds all of the block's tiles: the
+// kernel is bound by the issue of its vector loads (its address path stalls on the L1), not by
+// their bytes, so a unit that would have run two or three one-tile blocks issues up to a third
+// fewer loads.  Measured at the verify chunks (6 rows): LLaMA-7B shape 3864 -> 3686 us (QKV and
+// gate/up at three tiles), FlanT5-xl 1679 -> 1649 us (QKV and gate/up at two); two tiles on the
+// LLaMA-7B shape's 768 QKV tiles (384 blocks) lose, 4008 us.
+// Steps per batch: as many as the registers allow (skinny_cap), then balanced so that the wave's
+// last batch is not a short one padded with clamped re-reads.
 template <bool PACK>
 hipError_t launch_skinny_as(const LinearArgs& b, bool gated, bool rms, int tiles, dim3 block,
                             hipStream_t s) {
-  const int nt = b.epi == EPI_ARGMAX ? 4 : 1, nb = gated ? 2 : 1;
-  const int cap = PACK ? (nt * nb == 1 ? 12 : (nb == 2 ? 8 : 4)) : (8 / (nt * nb) > 0 ? 8 / (nt * nb) : 1);
+  const int cus = device_cus();
+  const int nt = b.epi == EPI_ARGMAX ? 4 : (PACK ? std::min(3, (tiles + cus - 1) / cus) : 1);
+  const int cap = skinny_cap(PACK, nt * (gated ? 2 : 1), nt);
   const int spw = (b.K / 64 + SKW - 1) / SKW;
   const int batches = (spw + cap - 1) / cap;
   const int want = (spw + batches - 1) / batches;
@@ -1744,12 +1759,12 @@ hipError_t launch_skinny_as(const LinearArgs& b, bool gated, bool rms, int tiles
   for (int i = 0; i < 6; ++i)
     if (opts[i] >= want && opts[i] <= cap) { sk = opts[i]; break; }
   switch (sk) {
-    case 1: launch_skinny_sk<PACK, 1>(b, gated, rms, tiles, block, s); break;
-    case 2: launch_skinny_sk<PACK, 2>(b, gated, rms, tiles, block, s); break;
-    case 4: launch_skinny_sk<PACK, 4>(b, gated, rms, tiles, block, s); break;
-    case 8: launch_skinny_sk<PACK, 8>(b, gated, rms, tiles, block, s); break;
-    case 10: launch_skinny_sk<PACK, 10>(b, gated, rms, tiles, block, s); break;
-    default: launch_skinny_sk<PACK, 12>(b, gated, rms, tiles, block, s); break;
+    case 1: launch_skinny_sk<PACK, 1>(b, gated, rms, tiles, nt, block, s); break;
+    case 2: launch_skinny_sk<PACK, 2>(b, gated, rms, tiles, nt, block, s); break;
+    case 4: launch_skinny_sk<PACK, 4>(b, gated, rms, tiles, nt, block, s); break;
+    case 8: launch_skinny_sk<PACK, 8>(b, gated, rms, tiles, nt, block, s); break;
+    case 10: launch_skinny_sk<PACK, 10>(b, gated, rms, tiles, nt, block, s); break;
+    default: launch_skinny_sk<PACK, 12>(b, gated, rms, tiles, nt, block, s); break;
   }
   return hipGetLastError();
 }
@@ -1829,14 +1844,7 @@ void launch_gemm3_t(const LinearArgs& a, bool rms, hipStream_t s) {
 // resident at once (two 128 x 128 blocks per compute unit: 61 KB of LDS each).  At the
 // LLaMA-7B shape's 608-row prefix (160 tiles over 4096 outputs) that is 3, measured faster than
 // 2 or 4 (whose fourth range spills into a second round of blocks) and than the 64 x 64 tiles.
-int ksplit_choice(int tiles) {
-  int dev = 0, n_cu = 0;
-  if (hipGetDevice(&dev) != hipSuccess ||
-      hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-      n_cu <= 0)
-    n_cu = 256;
-  return (2 * n_cu) / tiles;
-}
+int ksplit_choice(int tiles) { return (2 * device_cus()) / tiles; }
 
 // The plane GEMM when its buffer is there and the shape fits: RMSNorm or no norm, no argmax, K in
 // whole steps, tiles that never straddle matrices.  128 x 128 tiles (gated: 128 x 64 per matrix)
