@@ -479,7 +479,7 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--cpu-seconds", type=float, default=20.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--fit-prompts", type=int, default=16,
+    ap.add_argument("--fit-prompts", type=int, default=32,
                     help="sequences (seeds 1000..) whose states fit the imitation network's second "
                          "layer before a second measurement (0: skip)")
     ap.add_argument("--sample-temps", default="1.0,0.1",

@@ -157,8 +157,11 @@ hipError_t launch_linear_skinny(const LinearArgs& a, hipStream_t s, int* n_parts
 hipError_t launch_skinny_prep(const float* x, int ldx, int M, int K, const float* gain,
                               bf16_t* out, int ldo, int plane_rows, float* ssq, hipStream_t s);
 
-// Partial sums of squares per block of a skinny residual epilogue (the in_nssq of its consumer).
+// 16-feature tiles of a skinny launch.
 int skinny_blocks(int n_out);
+// Partial sums of squares a skinny residual epilogue of n_out features over M rows leaves (the
+// in_nssq of its consumer): one per tile, or two with half tiles.
+int skinny_ssq_parts(int n_out, int M);
 
 // True when launch_linear takes the weight-streaming vector path (the one that has EPI_QKV).
 bool linear_is_vector(const LinearArgs& a);

@@ -547,12 +547,24 @@ __global__ __launch_bounds__(256) void gemv1k_pair_kernel(const LinearArgs a, co
 // columns 0..7 and the lo plane in columns 8..15, so one activation load and one MFMA per 32
 // elements cover both planes (half the loads and MFMAs of the two-plane form); the epilogue adds
 // column t + 8 to column t.
+// HM (half tiles; PACK, one tile, no gated / QKV / argmax epilogue): for a projection with fewer
+// tiles than compute units, two blocks share a tile, block 2v + s taking features 8s..8s+7 of tile
+// v.  Its A operand holds those 8 features twice, A row i being feature i & 7 over elements
+// 0..31 (i < 8) or 32..63 (i >= 8) of a 64-element step, and the B operand's columns are the 8
+// input rows over the same two halves, so lane l reads the 16 bytes at element
+// 32 ((l >> 3) & 1) + 8 (l >> 4) of row (or feature) l & 7: eight lanes cover a row's whole 128
+// bytes.  D[f][t] + D[f + 8][t + 8] is the step's dot product (the other quadrants are cross terms
+// and are dropped); the hi and lo planes take two loads and two MFMAs a step.  Per compute unit
+// that is half the weight loads and the same activation loads, on twice the units (the kernel is
+// bound by the issue of its loads: see launch_skinny_as).  The residual epilogue's partial sums
+// of squares are then per half tile.
 constexpr int SKW = 4;  // waves per skinny block
 constexpr int SSQ_MAX = 256;  // partial sums of squares a skinny consumer reads (d_model <= 4096)
 
 // SK: 64-element steps per batch of loads (chosen by the launcher from the steps of a wave).
-template <bool GATED, bool RMS, int NT, bool PACK, int SK>
+template <bool GATED, bool RMS, int NT, bool PACK, int SK, bool HM = false>
 __global__ __launch_bounds__(64 * SKW) void gemv_mfma_kernel(const LinearArgs a) {
+  static_assert(!HM || (PACK && NT == 1 && !GATED), "half tiles: PACK, one tile, one matrix");
   constexpr int NB = GATED ? 2 : 1;
   constexpr int NG = 4 * SKW;                                 // groups of 16 threads
   __shared__ float part[SKW][NB][NT][16][17];
@@ -568,7 +580,8 @@ __global__ __launch_bounds__(64 * SKW) void gemv_mfma_kernel(const LinearArgs a)
   const int n_out = GATED ? a.n_per : a.n_per * a.n_mats;
   const int tiles = (n_out + 15) / 16;
   const bool qkv = !GATED && a.epi == EPI_QKV;
-  const int grp = blockIdx.x;
+  const int grp = HM ? (int)(blockIdx.x >> 1) : (int)blockIdx.x;
+  const int hsel = HM ? (int)(blockIdx.x & 1) : 0;  // HM: this block's half of the tile
   const int steps = K / 64;
   const int s_beg = (steps * wave) / SKW, s_end = (steps * (wave + 1)) / SKW;
   const int half = a.d_head >> 1, per_head = qkv ? half / 8 : 1;
@@ -581,7 +594,8 @@ __global__ __launch_bounds__(64 * SKW) void gemv_mfma_kernel(const LinearArgs a)
     mat = m;
     c = h * a.d_head + 8 * jb;
   };
-  const int r16 = lane & 15;
+  // this lane's weight row: feature lane % 16 of each tile, or (HM) 8 hsel + lane % 8
+  const int r16 = HM ? 8 * hsel + (lane & 7) : (lane & 15);
   const bf16_t* wrow[NB][NT];
 #pragma unroll
   for (int j = 0; j < NT; ++j) {
@@ -605,14 +619,17 @@ __global__ __launch_bounds__(64 * SKW) void gemv_mfma_kernel(const LinearArgs a)
       wrow[0][j] = reinterpret_cast<const bf16_t*>(base) + (size_t)v * K;
     }
   }
-  const int kq = (lane >> 4) * 16;  // this lane's 16 elements within a step
+  // this lane's elements within a 64-element step: 16 from 16 (lane / 16), or (HM) 8 from
+  // 32 ((lane / 8) % 2) + 8 (lane / 16)
+  const int kq = HM ? ((lane >> 3) & 1) * 32 + (lane >> 4) * 8 : (lane >> 4) * 16;
   const int t0 = blockIdx.y * 16;   // this block's first input row
   // B column lane % 16: input row t0 + lane % 16, or (PACK) row lane % 8 of the hi (columns
-  // 0..7) or lo (columns 8..15) plane
+  // 0..7) or lo (columns 8..15) plane, or (HM) row lane % 8 with its hi and lo planes in two loads
   const int tok = PACK ? (lane & 7) : t0 + (lane & 15);
   const bool tok_ok = tok < M;
   const int PR = a.plane_rows;
-  const bf16_t* brow = a.in_planes + ((size_t)(PACK && (lane & 8) ? PR : 0) + (tok_ok ? tok : 0)) * a.in_ld;
+  const bf16_t* brow =
+      a.in_planes + ((size_t)(PACK && !HM && (lane & 8) ? PR : 0) + (tok_ok ? tok : 0)) * a.in_ld;
   const bf16_t* brow_lo = brow + (size_t)PR * a.in_ld;
 
   // values the epilogue needs, requested before the main batch (the wait counter retires loads
@@ -643,6 +660,7 @@ __global__ __launch_bounds__(64 * SKW) void gemv_mfma_kernel(const LinearArgs a)
 #pragma unroll
     for (int j = 0; j < NT; ++j) acc[b][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   for (int s0 = s_beg; s0 < s_end; s0 += SK) {
+    // bv: 32 bytes of the (PACK: packed) hi plane, or (HM) 16 of the hi and 16 of the lo plane
     uint4 wv[NB][NT][SK][2], bv[SK][2], bl[SK][2];
     // inputs first (L2-resident, they arrive early), then the weights in step order: the wait
     // counter retires loads in issue order, so step u waits only for its own weights
@@ -650,10 +668,10 @@ __global__ __launch_bounds__(64 * SKW) void gemv_mfma_kernel(const LinearArgs a)
     for (int u = 0; u < SK; ++u) {
       const int k0 = min(s0 + u, s_end - 1) * 64 + kq;
       const uint4* bp = reinterpret_cast<const uint4*>(brow + k0);
+      const uint4* bq = reinterpret_cast<const uint4*>(brow_lo + k0);
       bv[u][0] = bp[0];
-      bv[u][1] = bp[1];
+      bv[u][1] = HM ? bq[0] : bp[1];
       if (!PACK) {
-        const uint4* bq = reinterpret_cast<const uint4*>(brow_lo + k0);
         bl[u][0] = bq[0];
         bl[u][1] = bq[1];
       }
@@ -667,7 +685,7 @@ __global__ __launch_bounds__(64 * SKW) void gemv_mfma_kernel(const LinearArgs a)
         for (int b = 0; b < NB; ++b) {
           const uint4* wp = reinterpret_cast<const uint4*>(wrow[b][j] + k0);
           wv[b][j][u][0] = wp[0];
-          wv[b][j][u][1] = wp[1];
+          if (!HM) wv[b][j][u][1] = wp[1];
         }
     }
     __builtin_amdgcn_sched_barrier(0);  // keep the whole batch in flight before the first MFMA
@@ -685,6 +703,11 @@ __global__ __launch_bounds__(64 * SKW) void gemv_mfma_kernel(const LinearArgs a)
 #pragma unroll
         for (int b = 0; b < NB; ++b) {
           const bf16x8_t w0 = *reinterpret_cast<const bf16x8_t*>(&wv[b][j][u][0]);
+          if (HM) {  // the half tile's 8 features against the hi (b0) and lo (b1) planes
+            acc[b][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w0, *reinterpret_cast<const bf16x8_t*>(&b0), acc[b][j], 0, 0, 0);
+            acc[b][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w0, *reinterpret_cast<const bf16x8_t*>(&b1), acc[b][j], 0, 0, 0);
+            continue;
+          }
           const bf16x8_t w1 = *reinterpret_cast<const bf16x8_t*>(&wv[b][j][u][1]);
           acc[b][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w0, *reinterpret_cast<const bf16x8_t*>(&b0), acc[b][j], 0, 0, 0);
           if (!PACK)
@@ -700,13 +723,26 @@ __global__ __launch_bounds__(64 * SKW) void gemv_mfma_kernel(const LinearArgs a)
 #pragma unroll
     for (int i = 0; i < SSQ_MAX / NG; ++i) sp += ((tid >> 4) + NG * i < a.in_nssq) ? sv[i] : 0.f;
   }
-  // D[feature][token]: lane holds features 4 * (lane / 16) + e, token lane % 16
+  // D[feature][token]: lane holds D rows 4 * (lane / 16) + e, column lane % 16.  HM: the useful
+  // quadrants are rows 0..7 x columns 0..7 (lanes 0..7 and 16..23) and rows 8..15 x columns 8..15
+  // (those lanes + 40); their sum is feature 8 hsel + 4 (lane / 16) + e, row lane % 8, stored in
+  // column lane % 8 (the PACK epilogue's hi column; its lo column, + 8, gets 0)
 #pragma unroll
   for (int b = 0; b < NB; ++b)
 #pragma unroll
     for (int j = 0; j < NT; ++j)
 #pragma unroll
-      for (int e = 0; e < 4; ++e) part[wave][b][j][4 * (lane >> 4) + e][lane & 15] = acc[b][j][e];
+      for (int e = 0; e < 4; ++e) {
+        if (HM) {
+          const float v = acc[b][j][e] + __shfl_down(acc[b][j][e], 40, SSD_WAVE);
+          if (lane < 24 && !(lane & 8)) {
+            part[wave][b][j][8 * hsel + 4 * (lane >> 4) + e][lane & 7] = v;
+            part[wave][b][j][8 * hsel + 4 * (lane >> 4) + e][8 + (lane & 7)] = 0.f;
+          }
+        } else {
+          part[wave][b][j][4 * (lane >> 4) + e][lane & 15] = acc[b][j][e];
+        }
+      }
   if (RMS) ssq_red[tid >> 4][tid & 15] = sp;
   __syncthreads();
 
@@ -744,6 +780,7 @@ __global__ __launch_bounds__(64 * SKW) void gemv_mfma_kernel(const LinearArgs a)
   __syncthreads();
 
   const float rscale = RMS ? rs[t] : 1.f;
+  const bool mine = !HM || (f >> 3) == hsel;  // HM: features of this block's half tile
   for (int j = 0; j < NT; ++j) {
     const int vt = grp * NT + j;
     if (vt >= tiles) break;  // uniform over the block
@@ -770,7 +807,7 @@ __global__ __launch_bounds__(64 * SKW) void gemv_mfma_kernel(const LinearArgs a)
     if (a.epi == EPI_RESID) {
       // y_new, the next planes and this tile's partial sums of squares (all threads take part in
       // the reduction; rows past M or features past n_out contribute zero)
-      const bool ok = lead && tg < M && n < n_out;
+      const bool ok = lead && mine && tg < M && n < n_out;
       float y2 = 0.f;
       if (ok) {
         const float tt = y_old[j] + v;
@@ -790,12 +827,13 @@ __global__ __launch_bounds__(64 * SKW) void gemv_mfma_kernel(const LinearArgs a)
         y2 += __shfl_xor(y2, 32, SSD_WAVE);
         if (lead && lane < 16) sq[wave][lane] = y2;
         __syncthreads();
-        if (tid < 16) a.out_ssq[(size_t)vt * PR + t0 + tid] = (sq[0][tid] + sq[1][tid]) + (sq[2][tid] + sq[3][tid]);
+        const int slot = HM ? 2 * vt + hsel : vt;
+        if (tid < 16) a.out_ssq[(size_t)slot * PR + t0 + tid] = (sq[0][tid] + sq[1][tid]) + (sq[2][tid] + sq[3][tid]);
         __syncthreads();
       }
       continue;
     }
-    if (!lead || tg >= M) continue;
+    if (!lead || !mine || tg >= M) continue;
     if (qkv) {
       int m, c;
       qkv_tile(vt, m, c);
@@ -1699,6 +1737,19 @@ bool skinny_ok(int M, int K, int wdtype) { return wdtype == 1 && M >= 2 && M <= 
 
 int skinny_blocks(int n_out) { return (n_out + 15) / 16; }
 
+// Half tiles (gemv_mfma_kernel's HM): at most 8 rows, a single-matrix projection without the QKV,
+// gated or argmax epilogue, fewer tiles than compute units, and room for a partial sum of squares
+// per half tile.
+bool skinny_half(int n_out, int M, int epi, bool gated) {
+  const int tiles = skinny_blocks(n_out);
+  return M <= 8 && !gated && epi != EPI_QKV && epi != EPI_ARGMAX && tiles < device_cus() &&
+         2 * tiles <= SSQ_MAX;
+}
+
+int skinny_ssq_parts(int n_out, int M) {
+  return (skinny_half(n_out, M, EPI_RESID, false) ? 2 : 1) * skinny_blocks(n_out);
+}
+
 // Steps per batch of loads that the registers hold, by weight tiles per wave (tiles x matrices,
 // nm): PACK, with one input plane, 12 for one, 8 for two, 4 for three or four, 2 for six; the
 // two-plane form 8 / nm.  0: no such variant (several projection tiles per block are PACK only).
@@ -1711,6 +1762,14 @@ constexpr int skinny_cap(bool pack, int nm, int nt) {
 template <bool PACK, int SK, int NT, bool G>
 void launch_skinny_nt(const LinearArgs& b, bool rms, int tiles, dim3 block, hipStream_t s) {
   if constexpr (SK <= skinny_cap(PACK, NT * (G ? 2 : 1), NT)) {
+    if constexpr (PACK && NT == 1 && !G) {
+      if (skinny_half(b.n_per * b.n_mats, b.M, b.epi, false)) {
+        const dim3 grid(2 * tiles, 1);
+        if (rms) hipLaunchKernelGGL((gemv_mfma_kernel<false, true, 1, true, SK, true>), grid, block, 0, s, b);
+        else hipLaunchKernelGGL((gemv_mfma_kernel<false, false, 1, true, SK, true>), grid, block, 0, s, b);
+        return;
+      }
+    }
     const dim3 grid((tiles + NT - 1) / NT, (b.M + 15) / 16);
     if (rms) hipLaunchKernelGGL((gemv_mfma_kernel<G, true, NT, PACK, SK>), grid, block, 0, s, b);
     else hipLaunchKernelGGL((gemv_mfma_kernel<G, false, NT, PACK, SK>), grid, block, 0, s, b);
@@ -1736,7 +1795,9 @@ void launch_skinny_sk(const LinearArgs& b, bool gated, bool rms, int tiles, int 
 
 // Tiles per block: four for the LM head's argmax launch; for a projection one, unless its tiles
 // outnumber the compute units, then as many as bring the grid down to one block per unit (at most
-// three, PACK only).  Every input fragment a wave loads then feeds all of the block's tiles: the
+// three, PACK only); a PACK projection with fewer tiles than units runs half tiles (skinny_half),
+// two blocks a tile: at the FlanT5-xl verify chunk (6 rows, 128 tiles) W_o 7.5 -> 7.0 us, the
+// cross-attention query 6.9 -> 6.2 us, down (K 5120) 12.7 -> 10.8 us.  Every input fragment a wave loads then feeds all of the block's tiles: the
 // kernel is bound by the issue of its vector loads (its address path stalls on the L1), not by
 // their bytes, so a unit that would have run two or three one-tile blocks issues up to a third
 // fewer loads.  Measured at the verify chunks (6 rows): LLaMA-7B shape 3864 -> 3686 us (QKV and

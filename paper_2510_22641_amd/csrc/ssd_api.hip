@@ -114,7 +114,7 @@ bool make_layout(const ssd_dims& d, Layout& L, bool allow_fold = true) {
     X.p_x = take(2 * PRz * D * 2);
     X.p_attn = take(2 * PRz * HD * 2);
     X.p_ffn = take(2 * PRz * (size_t)d.d_ff * 2);
-    X.ssq = take((size_t)skinny_blocks((int)D) * PRz * 4);
+    X.ssq = take((size_t)2 * skinny_blocks((int)D) * PRz * 4);  // up to two partials per tile
     X.attn_part = take((size_t)L.attn_rows * d.n_heads * ATTN_SPLITS_MAX * (d.d_head + 2) * 4);
     X.cur_tok = take(B * 4);
   };
@@ -335,7 +335,7 @@ int run_layers(ssd_ctx* c, float* x, int B, int C, int pos_off, int l0, int l1, 
   bf16_t* p_attn = c->at<bf16_t>(c->L.p_attn);
   bf16_t* p_ffn = c->at<bf16_t>(c->L.p_ffn);
   float* ssq = c->at<float>(c->L.ssq);
-  const int nssq_resid = skinny_blocks(D);
+  const int nssq_resid = skinny_ssq_parts(D, R);
   int nssq = 1;  // partials behind the current p_x
   // one linear layer: the skinny MFMA path for a verify chunk, else the vector / tile paths
   auto linear = [&](LinearArgs& a, const bf16_t* in, int in_ld) -> hipError_t {
