@@ -1752,16 +1752,15 @@ int skinny_ssq_parts(int n_out, int M) {
 
 // Steps per batch of loads that the registers hold, by weight tiles per wave (tiles x matrices,
 // nm): PACK, with one input plane, 12 for one, 8 for two, 4 for three or four, 2 for six; the
-// two-plane form 8 / nm.  0: no such variant (several projection tiles per block are PACK only).
-constexpr int skinny_cap(bool pack, int nm, int nt) {
-  return pack ? (nm == 1 ? 12 : (nm == 2 ? 8 : (nm <= 4 ? 4 : 2)))
-              : (nt > 1 && nt < 4 ? 0 : (8 / nm > 0 ? 8 / nm : 1));
+// two-plane form 8 / nm.
+constexpr int skinny_cap(bool pack, int nm) {
+  return pack ? (nm == 1 ? 12 : (nm == 2 ? 8 : (nm <= 4 ? 4 : 2))) : (8 / nm > 0 ? 8 / nm : 1);
 }
 
 // (only the depths the launcher can pick for each variant are instantiated)
 template <bool PACK, int SK, int NT, bool G>
 void launch_skinny_nt(const LinearArgs& b, bool rms, int tiles, dim3 block, hipStream_t s) {
-  if constexpr (SK <= skinny_cap(PACK, NT * (G ? 2 : 1), NT)) {
+  if constexpr (SK <= skinny_cap(PACK, NT * (G ? 2 : 1))) {
     if constexpr (PACK && NT == 1 && !G) {
       if (skinny_half(b.n_per * b.n_mats, b.M, b.epi, false)) {
         const dim3 grid(2 * tiles, 1);
@@ -1793,24 +1792,27 @@ void launch_skinny_sk(const LinearArgs& b, bool gated, bool rms, int tiles, int 
   }
 }
 
-// Tiles per block: four for the LM head's argmax launch; for a projection one, unless its tiles
-// outnumber the compute units, then as many as bring the grid down to one block per unit (at most
-// three, PACK only); a PACK projection with fewer tiles than units runs half tiles (skinny_half),
-// two blocks a tile: at the FlanT5-xl verify chunk (6 rows, 128 tiles) W_o 7.5 -> 7.0 us, the
-// cross-attention query 6.9 -> 6.2 us, down (K 5120) 12.7 -> 10.8 us.  Every input fragment a wave loads then feeds all of the block's tiles: the
-// kernel is bound by the issue of its vector loads (its address path stalls on the L1), not by
-// their bytes, so a unit that would have run two or three one-tile blocks issues up to a third
-// fewer loads.  Measured at the verify chunks (6 rows): LLaMA-7B shape 3864 -> 3686 us (QKV and
-// gate/up at three tiles), FlanT5-xl 1679 -> 1649 us (QKV and gate/up at two); two tiles on the
-// LLaMA-7B shape's 768 QKV tiles (384 blocks) lose, 4008 us.
+// Tiles per block: four for the LM head's argmax launch; for a projection one, unless its blocks
+// (tiles x 16-row groups) outnumber the compute units, then as many as bring the grid down to one
+// block per unit (at most three).  Every input fragment a wave loads then feeds all of the block's
+// tiles: the kernel is bound by the issue of its vector loads (its address path stalls on the
+// L1), not by their bytes, so a unit that would have run two or three one-tile blocks issues up to
+// a third fewer loads.  Measured at the verify chunks (6 rows): LLaMA-7B shape 3864 -> 3686 us
+// (QKV and gate/up at three tiles), FlanT5-xl 1679 -> 1649 us (QKV and gate/up at two); two tiles
+// on the LLaMA-7B shape's 768 QKV tiles (384 blocks) lose, 4008 us.  A PACK projection with fewer
+// tiles than units runs half tiles instead (skinny_half: two blocks a tile): at the FlanT5-xl
+// verify chunk (128 tiles) W_o 7.5 -> 7.0 us, the cross-attention query 6.9 -> 6.2 us, down
+// (K 5120) 12.7 -> 10.8 us.
 // Steps per batch: as many as the registers allow (skinny_cap), then balanced so that the wave's
 // last batch is not a short one padded with clamped re-reads.
 template <bool PACK>
 hipError_t launch_skinny_as(const LinearArgs& b, bool gated, bool rms, int tiles, dim3 block,
                             hipStream_t s) {
   const int cus = device_cus();
-  const int nt = b.epi == EPI_ARGMAX ? 4 : (PACK ? std::min(3, (tiles + cus - 1) / cus) : 1);
-  const int cap = skinny_cap(PACK, nt * (gated ? 2 : 1), nt);
+  // blocks of one tile: a grid row per 16 input rows (one with PACK)
+  const long long blocks1 = (long long)tiles * (PACK ? 1 : (b.M + 15) / 16);
+  const int nt = b.epi == EPI_ARGMAX ? 4 : (int)std::min<long long>(3, (blocks1 + cus - 1) / cus);
+  const int cap = skinny_cap(PACK, nt * (gated ? 2 : 1));
   const int spw = (b.K / 64 + SKW - 1) / SKW;
   const int batches = (spw + cap - 1) / cap;
   const int want = (spw + batches - 1) / batches;

@@ -478,15 +478,16 @@ def test_verify_chunks_past_the_skinny_capacity_take_the_tile_path():
         parity.check_run_against_oracle(dec, wl.shape, pr[s], z[s], run, s, wl.gamma)
 
 
-@pytest.mark.parametrize("arch,batch", [("t5", 1), ("llama", 1), ("llama", 2)],
-                         ids=["t5-b1", "llama-b1", "llama-b2"])
+@pytest.mark.parametrize("arch,batch", [("t5", 1), ("llama", 1), ("llama", 2), ("llama", 3)],
+                         ids=["t5-b1", "llama-b1", "llama-b2", "llama-b3"])
 def test_wide_skinny_projections_share_input_loads_over_tiles(arch, batch):
     """Decoders 1536 wide with an 8704-wide FFN: at a chunk of at most 8 rows the QKV projection
     has 288 tiles of 16 features and the gated FFN 544, more than a 256-unit device has compute
     units, so their skinny MFMA blocks take two and three tiles (the QKV epilogue with rotary or
     without, the gated epilogue), while W_o, the cross-attention projections and the down
-    projection (96 tiles) keep one.  Batch 2 also runs the draft steps (2 rows) on that path.
-    Every sequence's drafts, verify logits and accepted lengths follow the oracle."""
+    projection (96 tiles) run half tiles.  Batch 2 also runs the draft steps (2 rows) on that
+    path; batch 3 verifies 12-row chunks on the two-plane form with several tiles a block.  Every
+    sequence's drafts, verify logits and accepted lengths follow the oracle."""
     from dataclasses import replace
     if arch == "t5":
         sh = replace(synth.SMALL_T5_BF16, name="t5-wide-skinny", n_layers=3, d_model=1536,
