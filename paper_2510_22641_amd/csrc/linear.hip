@@ -547,24 +547,12 @@ __global__ __launch_bounds__(256) void gemv1k_pair_kernel(const LinearArgs a, co
 // columns 0..7 and the lo plane in columns 8..15, so one activation load and one MFMA per 32
 // elements cover both planes (half the loads and MFMAs of the two-plane form); the epilogue adds
 // column t + 8 to column t.
-// HM (half tiles; PACK, one tile, no gated / QKV / argmax epilogue): for a projection with fewer
-// tiles than compute units, two blocks share a tile, block 2v + s taking features 8s..8s+7 of tile
-// v.  Its A operand holds those 8 features twice, A row i being feature i & 7 over elements
-// 0..31 (i < 8) or 32..63 (i >= 8) of a 64-element step, and the B operand's columns are the 8
-// input rows over the same two halves, so lane l reads the 16 bytes at element
-// 32 ((l >> 3) & 1) + 8 (l >> 4) of row (or feature) l & 7: eight lanes cover a row's whole 128
-// bytes.  D[f][t] + D[f + 8][t + 8] is the step's dot product (the other quadrants are cross terms
-// and are dropped); the hi and lo planes take two loads and two MFMAs a step.  Per compute unit
-// that is half the weight loads and the same activation loads, on twice the units (the kernel is
-// bound by the issue of its loads: see launch_skinny_as).  The residual epilogue's partial sums
-// of squares are then per half tile.
 constexpr int SKW = 4;  // waves per skinny block
 constexpr int SSQ_MAX = 256;  // partial sums of squares a skinny consumer reads (d_model <= 4096)
 
 // SK: 64-element steps per batch of loads (chosen by the launcher from the steps of a wave).
-template <bool GATED, bool RMS, int NT, bool PACK, int SK, bool HM = false>
+template <bool GATED, bool RMS, int NT, bool PACK, int SK>
 __global__ __launch_bounds__(64 * SKW) void gemv_mfma_kernel(const LinearArgs a) {
-  static_assert(!HM || (PACK && NT == 1 && !GATED), "half tiles: PACK, one tile, one matrix");
   constexpr int NB = GATED ? 2 : 1;
   constexpr int NG = 4 * SKW;                                 // groups of 16 threads
   __shared__ float part[SKW][NB][NT][16][17];
@@ -580,8 +568,7 @@ __global__ __launch_bounds__(64 * SKW) void gemv_mfma_kernel(const LinearArgs a)
   const int n_out = GATED ? a.n_per : a.n_per * a.n_mats;
   const int tiles = (n_out + 15) / 16;
   const bool qkv = !GATED && a.epi == EPI_QKV;
-  const int grp = HM ? (int)(blockIdx.x >> 1) : (int)blockIdx.x;
-  const int hsel = HM ? (int)(blockIdx.x & 1) : 0;  // HM: this block's half of the tile
+  const int grp = blockIdx.x;
   const int steps = K / 64;
   const int s_beg = (steps * wave) / SKW, s_end = (steps * (wave + 1)) / SKW;
   const int half = a.d_head >> 1, per_head = qkv ? half / 8 : 1;
@@ -594,8 +581,7 @@ __global__ __launch_bounds__(64 * SKW) void gemv_mfma_kernel(const LinearArgs a)
     mat = m;
     c = h * a.d_head + 8 * jb;
   };
-  // this lane's weight row: feature lane % 16 of each tile, or (HM) 8 hsel + lane % 8
-  const int r16 = HM ? 8 * hsel + (lane & 7) : (lane & 15);
+  const int r16 = lane & 15;
   const bf16_t* wrow[NB][NT];
 #pragma unroll
   for (int j = 0; j < NT; ++j) {
@@ -619,17 +605,14 @@ __global__ __launch_bounds__(64 * SKW) void gemv_mfma_kernel(const LinearArgs a)
       wrow[0][j] = reinterpret_cast<const bf16_t*>(base) + (size_t)v * K;
     }
   }
-  // this lane's elements within a 64-element step: 16 from 16 (lane / 16), or (HM) 8 from
-  // 32 ((lane / 8) % 2) + 8 (lane / 16)
-  const int kq = HM ? ((lane >> 3) & 1) * 32 + (lane >> 4) * 8 : (lane >> 4) * 16;
+  const int kq = (lane >> 4) * 16;  // this lane's 16 elements within a step
   const int t0 = blockIdx.y * 16;   // this block's first input row
   // B column lane % 16: input row t0 + lane % 16, or (PACK) row lane % 8 of the hi (columns
-  // 0..7) or lo (columns 8..15) plane, or (HM) row lane % 8 with its hi and lo planes in two loads
+  // 0..7) or lo (columns 8..15) plane
   const int tok = PACK ? (lane & 7) : t0 + (lane & 15);
   const bool tok_ok = tok < M;
   const int PR = a.plane_rows;
-  const bf16_t* brow =
-      a.in_planes + ((size_t)(PACK && !HM && (lane & 8) ? PR : 0) + (tok_ok ? tok : 0)) * a.in_ld;
+  const bf16_t* brow = a.in_planes + ((size_t)(PACK && (lane & 8) ? PR : 0) + (tok_ok ? tok : 0)) * a.in_ld;
   const bf16_t* brow_lo = brow + (size_t)PR * a.in_ld;
 
   // values the epilogue needs, requested before the main batch (the wait counter retires loads
@@ -660,7 +643,6 @@ __global__ __launch_bounds__(64 * SKW) void gemv_mfma_kernel(const LinearArgs a)
 #pragma unroll
     for (int j = 0; j < NT; ++j) acc[b][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   for (int s0 = s_beg; s0 < s_end; s0 += SK) {
-    // bv: 32 bytes of the (PACK: packed) hi plane, or (HM) 16 of the hi and 16 of the lo plane
     uint4 wv[NB][NT][SK][2], bv[SK][2], bl[SK][2];
     // inputs first (L2-resident, they arrive early), then the weights in step order: the wait
     // counter retires loads in issue order, so step u waits only for its own weights
@@ -668,10 +650,10 @@ __global__ __launch_bounds__(64 * SKW) void gemv_mfma_kernel(const LinearArgs a)
     for (int u = 0; u < SK; ++u) {
       const int k0 = min(s0 + u, s_end - 1) * 64 + kq;
       const uint4* bp = reinterpret_cast<const uint4*>(brow + k0);
-      const uint4* bq = reinterpret_cast<const uint4*>(brow_lo + k0);
       bv[u][0] = bp[0];
-      bv[u][1] = HM ? bq[0] : bp[1];
+      bv[u][1] = bp[1];
       if (!PACK) {
+        const uint4* bq = reinterpret_cast<const uint4*>(brow_lo + k0);
         bl[u][0] = bq[0];
         bl[u][1] = bq[1];
       }
@@ -685,7 +667,7 @@ __global__ __launch_bounds__(64 * SKW) void gemv_mfma_kernel(const LinearArgs a)
         for (int b = 0; b < NB; ++b) {
           const uint4* wp = reinterpret_cast<const uint4*>(wrow[b][j] + k0);
           wv[b][j][u][0] = wp[0];
-          if (!HM) wv[b][j][u][1] = wp[1];
+          wv[b][j][u][1] = wp[1];
         }
     }
     __builtin_amdgcn_sched_barrier(0);  // keep the whole batch in flight before the first MFMA
@@ -703,11 +685,6 @@ __global__ __launch_bounds__(64 * SKW) void gemv_mfma_kernel(const LinearArgs a)
 #pragma unroll
         for (int b = 0; b < NB; ++b) {
           const bf16x8_t w0 = *reinterpret_cast<const bf16x8_t*>(&wv[b][j][u][0]);
-          if (HM) {  // the half tile's 8 features against the hi (b0) and lo (b1) planes
-            acc[b][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w0, *reinterpret_cast<const bf16x8_t*>(&b0), acc[b][j], 0, 0, 0);
-            acc[b][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w0, *reinterpret_cast<const bf16x8_t*>(&b1), acc[b][j], 0, 0, 0);
-            continue;
-          }
           const bf16x8_t w1 = *reinterpret_cast<const bf16x8_t*>(&wv[b][j][u][1]);
           acc[b][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w0, *reinterpret_cast<const bf16x8_t*>(&b0), acc[b][j], 0, 0, 0);
           if (!PACK)
@@ -723,26 +700,13 @@ __global__ __launch_bounds__(64 * SKW) void gemv_mfma_kernel(const LinearArgs a)
 #pragma unroll
     for (int i = 0; i < SSQ_MAX / NG; ++i) sp += ((tid >> 4) + NG * i < a.in_nssq) ? sv[i] : 0.f;
   }
-  // D[feature][token]: lane holds D rows 4 * (lane / 16) + e, column lane % 16.  HM: the useful
-  // quadrants are rows 0..7 x columns 0..7 (lanes 0..7 and 16..23) and rows 8..15 x columns 8..15
-  // (those lanes + 40); their sum is feature 8 hsel + 4 (lane / 16) + e, row lane % 8, stored in
-  // column lane % 8 (the PACK epilogue's hi column; its lo column, + 8, gets 0)
+  // D[feature][token]: lane holds features 4 * (lane / 16) + e, token lane % 16
 #pragma unroll
   for (int b = 0; b < NB; ++b)
 #pragma unroll
     for (int j = 0; j < NT; ++j)
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        if (HM) {
-          const float v = acc[b][j][e] + __shfl_down(acc[b][j][e], 40, SSD_WAVE);
-          if (lane < 24 && !(lane & 8)) {
-            part[wave][b][j][8 * hsel + 4 * (lane >> 4) + e][lane & 7] = v;
-            part[wave][b][j][8 * hsel + 4 * (lane >> 4) + e][8 + (lane & 7)] = 0.f;
-          }
-        } else {
-          part[wave][b][j][4 * (lane >> 4) + e][lane & 15] = acc[b][j][e];
-        }
-      }
+      for (int e = 0; e < 4; ++e) part[wave][b][j][4 * (lane >> 4) + e][lane & 15] = acc[b][j][e];
   if (RMS) ssq_red[tid >> 4][tid & 15] = sp;
   __syncthreads();
 
@@ -780,7 +744,6 @@ __global__ __launch_bounds__(64 * SKW) void gemv_mfma_kernel(const LinearArgs a)
   __syncthreads();
 
   const float rscale = RMS ? rs[t] : 1.f;
-  const bool mine = !HM || (f >> 3) == hsel;  // HM: features of this block's half tile
   for (int j = 0; j < NT; ++j) {
     const int vt = grp * NT + j;
     if (vt >= tiles) break;  // uniform over the block
@@ -807,7 +770,7 @@ __global__ __launch_bounds__(64 * SKW) void gemv_mfma_kernel(const LinearArgs a)
     if (a.epi == EPI_RESID) {
       // y_new, the next planes and this tile's partial sums of squares (all threads take part in
       // the reduction; rows past M or features past n_out contribute zero)
-      const bool ok = lead && mine && tg < M && n < n_out;
+      const bool ok = lead && tg < M && n < n_out;
       float y2 = 0.f;
       if (ok) {
         const float tt = y_old[j] + v;
@@ -827,13 +790,12 @@ __global__ __launch_bounds__(64 * SKW) void gemv_mfma_kernel(const LinearArgs a)
         y2 += __shfl_xor(y2, 32, SSD_WAVE);
         if (lead && lane < 16) sq[wave][lane] = y2;
         __syncthreads();
-        const int slot = HM ? 2 * vt + hsel : vt;
-        if (tid < 16) a.out_ssq[(size_t)slot * PR + t0 + tid] = (sq[0][tid] + sq[1][tid]) + (sq[2][tid] + sq[3][tid]);
+        if (tid < 16) a.out_ssq[(size_t)vt * PR + t0 + tid] = (sq[0][tid] + sq[1][tid]) + (sq[2][tid] + sq[3][tid]);
         __syncthreads();
       }
       continue;
     }
-    if (!lead || !mine || tg >= M) continue;
+    if (!lead || tg >= M) continue;
     if (qkv) {
       int m, c;
       qkv_tile(vt, m, c);
@@ -858,6 +820,231 @@ __global__ __launch_bounds__(64 * SKW) void gemv_mfma_kernel(const LinearArgs a)
       case EPI_BIAS_RESID: *yp = (a.resid ? a.resid[(size_t)tg * a.ldr + n] : 0.f) + (v + a.bias[n]); break;
       default: break;
     }
+  }
+}
+
+// Half tiles: the skinny path for at most 8 input rows when a compute unit would otherwise issue
+// more loads (launch_skinny_as compares the forms).  A half tile is 8 of a tile's 16 features:
+// feature f (0..7) of half s is tile row 4 s + (f & 3) + 8 (f >> 2), so a half tile holds four
+// whole rotary pairs of a QKV tile (features f and f + 4).  The A operand holds a half tile's 8
+// features twice, A row i being feature i & 7 over elements 0..31 (i < 8) or 32..63 (i >= 8) of a
+// 64-element step, and the B operand's columns are the 8 input rows over the same two halves; lane
+// l then reads the 16 bytes at element 32 ((l >> 3) & 1) + 8 (l >> 4) of row l & 7, so the eight
+// lanes of a row cover its whole 128 bytes.  D[f][t] + D[f + 8][t + 8] is the step's dot product
+// (the other two quadrants are cross terms and are dropped); the hi and lo planes take one load
+// each and every weight load feeds two MFMAs.  A block takes NH half tiles (h = NH * block + i)
+// whose weight loads share the block's input loads.  The epilogue runs on 64 threads per half tile
+// (feature (tid / 8) % 8, row tid % 8); a residual epilogue leaves one partial sum of squares per
+// half tile.
+template <bool GATED, bool RMS, int NH, int SK>
+__global__ __launch_bounds__(64 * SKW, 2) void gemv_mfma_half_kernel(const LinearArgs a) {
+  constexpr int NB = GATED ? 2 : 1;
+  constexpr int NG = 4 * SKW;  // groups of 16 threads
+  static_assert(NH <= SKW, "one wave per half tile in the epilogue");
+  __shared__ float part[SKW][NB][NH][8][9];
+  __shared__ float rs[16];
+  __shared__ float ssq_red[4 * SKW][16];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int K = a.K, M = a.M;
+  const int n_out = GATED ? a.n_per : a.n_per * a.n_mats;
+  const int halves = 2 * ((n_out + 15) / 16);
+  const bool qkv = !GATED && a.epi == EPI_QKV;
+  const int steps = K / 64;
+  const int s_beg = (steps * wave) / SKW, s_end = (steps * (wave + 1)) / SKW;
+  const int dhalf = a.d_head >> 1, per_head = qkv ? dhalf / 8 : 1;
+  const int h0 = blockIdx.x * NH;
+
+  // QKV tiles: matrix, head and 8-column group of the rotary pairs
+  auto qkv_tile = [&](int vt, int& mat, int& c) {
+    const int m = vt / (a.n_heads * per_head);
+    const int rem = vt - m * a.n_heads * per_head;
+    const int hh = rem / per_head, jb = rem - hh * per_head;
+    mat = m;
+    c = hh * a.d_head + 8 * jb;
+  };
+  auto tile_row = [](int s, int f) { return 4 * s + (f & 3) + 8 * (f >> 2); };
+  // output feature (or QKV weight row) of feature f of half tile h
+  auto feature = [&](int h, int f) {
+    const int vt = h >> 1, r16 = tile_row(h & 1, f);
+    if (qkv) {
+      int m, c;
+      qkv_tile(vt, m, c);
+      return m * a.n_per + c + (r16 & 7) + (r16 >= 8 ? dhalf : 0);
+    }
+    return vt * 16 + r16;
+  };
+  // this lane's weight rows: feature lane % 8 of each of the block's half tiles
+  const bf16_t* wrow[NB][NH];
+#pragma unroll
+  for (int i = 0; i < NH; ++i) {
+    const int h = h0 + i;
+    const int row = h < halves ? feature(h, lane & 7) : 0;
+    const int rr = row < n_out ? row : 0;
+    if (GATED) {
+      wrow[0][i] = reinterpret_cast<const bf16_t*>(a.w[0]) + (size_t)rr * K;
+      wrow[NB - 1][i] = reinterpret_cast<const bf16_t*>(a.w[1]) + (size_t)rr * K;
+    } else {
+      int v = rr;
+      const void* base = a.w[0];
+      if (v >= a.n_per) { v -= a.n_per; base = a.w[1]; if (v >= a.n_per) { v -= a.n_per; base = a.w[2]; } }
+      wrow[0][i] = reinterpret_cast<const bf16_t*>(base) + (size_t)v * K;
+    }
+  }
+  const int kq = ((lane >> 3) & 1) * 32 + (lane >> 4) * 8;  // this lane's 8 elements of a step
+  const int tok = lane & 7;
+  const bool tok_ok = tok < M;
+  const int PR = a.plane_rows;
+  const bf16_t* brow = a.in_planes + (size_t)(tok_ok ? tok : 0) * a.in_ld;
+  const bf16_t* brow_lo = brow + (size_t)PR * a.in_ld;
+
+  // epilogue thread: half tile ei, feature ef, row et
+  const int ei = tid >> 6, ef = (tid >> 3) & 7, et = tid & 7;
+  const int eh = h0 + ei;
+  const bool elive = ei < NH && eh < halves;
+  const int en = elive ? feature(eh, ef) : 0;
+
+  // values the epilogue needs, requested before the main batch (the wait counter retires loads in
+  // issue order): the producer's partial sums of squares (thread: row tid % 16, partials
+  // tid / 16 + NG j) and the old residual value of this thread's output
+  float sv[RMS ? SSQ_MAX / NG : 1];
+  if (RMS) {
+#pragma unroll
+    for (int j = 0; j < SSQ_MAX / NG; ++j) {
+      const int pp = (tid >> 4) + NG * j;
+      sv[j] = a.in_ssq[(size_t)min(pp, a.in_nssq - 1) * PR + (tid & 15)];
+    }
+  }
+  float y_old = 0.f;
+  if (a.epi == EPI_RESID) y_old = a.y[(size_t)min(et, M - 1) * a.ldy + min(en, n_out - 1)];
+
+  f32x4_t acc[NB][NH];
+#pragma unroll
+  for (int b = 0; b < NB; ++b)
+#pragma unroll
+    for (int i = 0; i < NH; ++i) acc[b][i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  for (int s0 = s_beg; s0 < s_end; s0 += SK) {
+    uint4 wv[NB][NH][SK], bv[SK][2];  // bv: the hi and lo planes' 16 bytes
+    // inputs first (L2-resident, they arrive early), then the weights in step order
+#pragma unroll
+    for (int u = 0; u < SK; ++u) {
+      const int k0 = min(s0 + u, s_end - 1) * 64 + kq;
+      bv[u][0] = *reinterpret_cast<const uint4*>(brow + k0);
+      bv[u][1] = *reinterpret_cast<const uint4*>(brow_lo + k0);
+    }
+#pragma unroll
+    for (int u = 0; u < SK; ++u) {
+      const int k0 = min(s0 + u, s_end - 1) * 64 + kq;
+#pragma unroll
+      for (int i = 0; i < NH; ++i)
+#pragma unroll
+        for (int b = 0; b < NB; ++b) wv[b][i][u] = *reinterpret_cast<const uint4*>(wrow[b][i] + k0);
+    }
+    __builtin_amdgcn_sched_barrier(0);  // keep the whole batch in flight before the first MFMA
+#pragma unroll
+    for (int u = 0; u < SK; ++u) {
+      // a step past this wave's range, or a row past M, re-read valid data: zero operands
+      const bool use = tok_ok && (s0 + u < s_end);
+      const uint4 z = make_uint4(0, 0, 0, 0);
+      const uint4 b0 = use ? bv[u][0] : z, b1 = use ? bv[u][1] : z;
+      // every weight fragment against the hi plane, then against the lo plane (independent
+      // products back to back)
+#pragma unroll
+      for (int pl = 0; pl < 2; ++pl) {
+        const bf16x8_t B = *reinterpret_cast<const bf16x8_t*>(pl ? &b1 : &b0);
+#pragma unroll
+        for (int i = 0; i < NH; ++i)
+#pragma unroll
+          for (int b = 0; b < NB; ++b)
+            acc[b][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                *reinterpret_cast<const bf16x8_t*>(&wv[b][i][u]), B, acc[b][i], 0, 0, 0);
+      }
+    }
+  }
+  float sp = 0.f;
+  if (RMS) {
+#pragma unroll
+    for (int j = 0; j < SSQ_MAX / NG; ++j) sp += ((tid >> 4) + NG * j < a.in_nssq) ? sv[j] : 0.f;
+  }
+  // lane holds D rows 4 (lane / 16) + e, column lane % 16: the useful quadrants are rows 0..7 x
+  // columns 0..7 (lanes 0..7 and 16..23) and rows 8..15 x columns 8..15 (those lanes + 40)
+#pragma unroll
+  for (int b = 0; b < NB; ++b)
+#pragma unroll
+    for (int i = 0; i < NH; ++i)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float v = acc[b][i][e] + __shfl_down(acc[b][i][e], 40, SSD_WAVE);
+        if (lane < 24 && !(lane & 8)) part[wave][b][i][4 * (lane >> 4) + e][lane & 7] = v;
+      }
+  if (RMS) ssq_red[tid >> 4][tid & 15] = sp;
+  __syncthreads();
+  if (RMS && tid < 16) {
+    float s2 = 0.f;
+#pragma unroll
+    for (int g = 0; g < NG; ++g) s2 += ssq_red[g][tid];
+    rs[tid] = 1.0f / sqrtf(s2 / (float)K + a.eps);
+  }
+  __syncthreads();
+
+  if (ei >= NH) return;  // whole waves
+  const float rscale = RMS ? rs[et] : 1.f;
+  auto sum_at = [&](int b, int f) {
+    float v = 0.f;
+#pragma unroll
+    for (int w = 0; w < SKW; ++w) v += part[w][b][ei][f][et];
+    return v * rscale;
+  };
+  const float v0 = sum_at(0, ef);
+  const bool ok = elive && et < M && en < n_out;
+  if (a.epi == EPI_RESID) {
+    float y2 = 0.f;
+    if (ok) {
+      const float tt = y_old + v0;
+      a.y[(size_t)et * a.ldy + en] = tt;
+      if (a.stash) a.stash[(size_t)et * a.lds + en] = tt;
+      if (a.out_planes) {
+        const float gv = a.out_gain ? a.out_gain[en] * tt : tt;
+        const uint32_t hi = f32_to_bf16(gv);
+        a.out_planes[(size_t)et * a.out_ld + en] = (bf16_t)hi;
+        a.out_planes[(size_t)(PR + et) * a.out_ld + en] = (bf16_t)f32_to_bf16(gv - bf16_to_f32(hi));
+      }
+      y2 = tt * tt;
+    }
+    if (a.out_ssq) {
+      // the half tile's 8 features of row et: lanes et + 8 f of this wave
+      y2 += __shfl_xor(y2, 8, SSD_WAVE);
+      y2 += __shfl_xor(y2, 16, SSD_WAVE);
+      y2 += __shfl_xor(y2, 32, SSD_WAVE);
+      if (elive && lane < 8) a.out_ssq[(size_t)eh * PR + et] = y2;
+    }
+    return;
+  }
+  if (!ok) return;
+  if (qkv) {
+    if (ef < 4) {
+      int m, c;
+      qkv_tile(eh >> 1, m, c);
+      qkv_store_pair(a, m, c + tile_row(eh & 1, ef), et, v0, sum_at(0, ef + 4));
+    }
+    return;
+  }
+  if (GATED) {
+    const float act = apply_epi_act(a.epi, v0, sum_at(NB - 1, ef));
+    if (a.y) a.y[(size_t)et * a.ldy + en] = act;
+    if (a.out_planes) {
+      const uint32_t hi = f32_to_bf16(act);
+      a.out_planes[(size_t)et * a.out_ld + en] = (bf16_t)hi;
+      a.out_planes[(size_t)(PR + et) * a.out_ld + en] = (bf16_t)f32_to_bf16(act - bf16_to_f32(hi));
+    }
+    return;
+  }
+  float* yp = a.y + (size_t)et * a.ldy + en;
+  switch (a.epi) {
+    case EPI_STORE: *yp = v0; break;
+    case EPI_BIAS_GELU: *yp = gelu_tanh(v0 + a.bias[en]); break;
+    case EPI_BIAS_RESID: *yp = (a.resid ? a.resid[(size_t)et * a.ldr + en] : 0.f) + (v0 + a.bias[en]); break;
+    default: break;
   }
 }
 
@@ -1737,49 +1924,98 @@ bool skinny_ok(int M, int K, int wdtype) { return wdtype == 1 && M >= 2 && M <= 
 
 int skinny_blocks(int n_out) { return (n_out + 15) / 16; }
 
-// Half tiles (gemv_mfma_kernel's HM): at most 8 rows, a single-matrix projection without the QKV,
-// gated or argmax epilogue, fewer tiles than compute units, and room for a partial sum of squares
-// per half tile.
-bool skinny_half(int n_out, int M, int epi, bool gated) {
-  const int tiles = skinny_blocks(n_out);
-  return M <= 8 && !gated && epi != EPI_QKV && epi != EPI_ARGMAX && tiles < device_cus() &&
-         2 * tiles <= SSQ_MAX;
+// The skinny launch shape.  The kernels are bound by the issue of their vector loads (their
+// address path stalls on the L1), not by the loads' bytes, so the shape is the one that issues the
+// fewest loads on the busiest compute unit: (blocks per unit, rounded up) x (loads per wave and
+// K step of a block).  Whole tiles, NT per block (grid rows of 16 input rows): NT x matrices x 2
+// weight loads and 2 input loads (PACK) or 4 (two planes).  Half tiles (at most 8 rows), NH per
+// block: NH x matrices weight loads and 2 input loads.  Ties go to whole tiles, then to fewer
+// blocks.  Measured at the verify chunks (6 rows) against one tile per block, FlanT5-xl: W_o, the
+// cross-attention projections and down (128 tiles) on one half tile a block 7.5 -> 7.0, 6.9 ->
+// 6.2 and 12.7 -> 10.8 us, QKV (384 tiles) on two tiles 12.0 -> 11.5 us; LLaMA-7B shape: QKV
+// (768 tiles) and gate/up (688 per matrix) on three tiles, verify 3864 -> 3686 us, where two tiles
+// (the model's 12 against 8 loads) lose: 4008 us.  The LM head's argmax launch keeps four tiles.
+struct SkinnyShape {
+  bool half;
+  int n;  // tiles or half tiles per block
+};
+
+SkinnyShape skinny_shape(int n_out, int M, int epi, bool gated) {
+  const int tiles = skinny_blocks(n_out), nb = gated ? 2 : 1;
+  if (epi == EPI_ARGMAX) return {false, 4};
+  const bool pack = M <= 8;
+  const long long cus = device_cus(), groups = pack ? 1 : (M + 15) / 16;
+  SkinnyShape best = {false, 1};
+  long long best_cost = -1;
+  for (int nt = 1; nt <= 3; ++nt) {
+    const long long blocks = (long long)((tiles + nt - 1) / nt) * groups;
+    const long long cost = ((blocks + cus - 1) / cus) * (nt * nb * 2 + (pack ? 2 : 4));
+    if (best_cost < 0 || cost < best_cost) { best = {false, nt}; best_cost = cost; }
+  }
+  // a residual epilogue on half tiles leaves a partial sum of squares per half tile (at most
+  // SSQ_MAX for its consumer)
+  if (pack && (epi != EPI_RESID || 2 * tiles <= SSQ_MAX)) {
+    for (int nh = 1; nh <= 3; ++nh) {
+      const long long blocks = (2LL * tiles + nh - 1) / nh;
+      const long long cost = ((blocks + cus - 1) / cus) * (nh * nb + 2);
+      if (cost < best_cost) { best = {true, nh}; best_cost = cost; }
+    }
+  }
+  return best;
 }
 
 int skinny_ssq_parts(int n_out, int M) {
-  return (skinny_half(n_out, M, EPI_RESID, false) ? 2 : 1) * skinny_blocks(n_out);
+  return (skinny_shape(n_out, M, EPI_RESID, false).half ? 2 : 1) * skinny_blocks(n_out);
 }
 
-// Steps per batch of loads that the registers hold, by weight tiles per wave (tiles x matrices,
-// nm): PACK, with one input plane, 12 for one, 8 for two, 4 for three or four, 2 for six; the
-// two-plane form 8 / nm.
-constexpr int skinny_cap(bool pack, int nm) {
-  return pack ? (nm == 1 ? 12 : (nm == 2 ? 8 : (nm <= 4 ? 4 : 2))) : (8 / nm > 0 ? 8 / nm : 1);
+// Steps per batch of loads that the registers hold, by 16-byte weight loads per lane and step
+// (wl: whole tiles NT x matrices x 2, half tiles NH x matrices) and input loads per step (il):
+// with one input plane about 48 loads of 16 bytes per lane and batch (12, 8, 4 or 2 steps); the
+// two-plane form (il = 4) 16 / wl steps.
+constexpr int skinny_cap(int wl, int il) {
+  return il == 4 ? (16 / wl > 0 ? 16 / wl : 1)
+                 : (48 / (wl + il) >= 12 ? 12 : (48 / (wl + il) >= 8 ? 8 : (48 / (wl + il) >= 4 ? 4 : 2)));
 }
 
 // (only the depths the launcher can pick for each variant are instantiated)
 template <bool PACK, int SK, int NT, bool G>
 void launch_skinny_nt(const LinearArgs& b, bool rms, int tiles, dim3 block, hipStream_t s) {
-  if constexpr (SK <= skinny_cap(PACK, NT * (G ? 2 : 1))) {
-    if constexpr (PACK && NT == 1 && !G) {
-      if (skinny_half(b.n_per * b.n_mats, b.M, b.epi, false)) {
-        const dim3 grid(2 * tiles, 1);
-        if (rms) hipLaunchKernelGGL((gemv_mfma_kernel<false, true, 1, true, SK, true>), grid, block, 0, s, b);
-        else hipLaunchKernelGGL((gemv_mfma_kernel<false, false, 1, true, SK, true>), grid, block, 0, s, b);
-        return;
-      }
-    }
+  if constexpr (SK <= skinny_cap(NT * (G ? 2 : 1) * 2, PACK ? 2 : 4)) {
     const dim3 grid((tiles + NT - 1) / NT, (b.M + 15) / 16);
     if (rms) hipLaunchKernelGGL((gemv_mfma_kernel<G, true, NT, PACK, SK>), grid, block, 0, s, b);
     else hipLaunchKernelGGL((gemv_mfma_kernel<G, false, NT, PACK, SK>), grid, block, 0, s, b);
   }
 }
 
+template <int SK, int NH, bool G>
+void launch_skinny_nh(const LinearArgs& b, bool rms, int tiles, dim3 block, hipStream_t s) {
+  if constexpr (SK <= skinny_cap(NH * (G ? 2 : 1), 2)) {
+    const dim3 grid((2 * tiles + NH - 1) / NH, 1);
+    if (rms) hipLaunchKernelGGL((gemv_mfma_half_kernel<G, true, NH, SK>), grid, block, 0, s, b);
+    else hipLaunchKernelGGL((gemv_mfma_half_kernel<G, false, NH, SK>), grid, block, 0, s, b);
+  }
+}
+
 template <bool PACK, int SK>
-void launch_skinny_sk(const LinearArgs& b, bool gated, bool rms, int tiles, int nt, dim3 block,
-                      hipStream_t s) {
+void launch_skinny_sk(const LinearArgs& b, bool gated, bool rms, int tiles, SkinnyShape sh,
+                      dim3 block, hipStream_t s) {
   if (b.epi == EPI_ARGMAX) return launch_skinny_nt<PACK, SK, 4, false>(b, rms, tiles, block, s);
-  switch (nt) {
+  if constexpr (PACK) {
+    if (sh.half) {
+      switch (sh.n) {
+        case 1:
+          return gated ? launch_skinny_nh<SK, 1, true>(b, rms, tiles, block, s)
+                       : launch_skinny_nh<SK, 1, false>(b, rms, tiles, block, s);
+        case 2:
+          return gated ? launch_skinny_nh<SK, 2, true>(b, rms, tiles, block, s)
+                       : launch_skinny_nh<SK, 2, false>(b, rms, tiles, block, s);
+        default:
+          return gated ? launch_skinny_nh<SK, 3, true>(b, rms, tiles, block, s)
+                       : launch_skinny_nh<SK, 3, false>(b, rms, tiles, block, s);
+      }
+    }
+  }
+  switch (sh.n) {
     case 1:
       return gated ? launch_skinny_nt<PACK, SK, 1, true>(b, rms, tiles, block, s)
                    : launch_skinny_nt<PACK, SK, 1, false>(b, rms, tiles, block, s);
@@ -1792,27 +2028,14 @@ void launch_skinny_sk(const LinearArgs& b, bool gated, bool rms, int tiles, int 
   }
 }
 
-// Tiles per block: four for the LM head's argmax launch; for a projection one, unless its blocks
-// (tiles x 16-row groups) outnumber the compute units, then as many as bring the grid down to one
-// block per unit (at most three).  Every input fragment a wave loads then feeds all of the block's
-// tiles: the kernel is bound by the issue of its vector loads (its address path stalls on the
-// L1), not by their bytes, so a unit that would have run two or three one-tile blocks issues up to
-// a third fewer loads.  Measured at the verify chunks (6 rows): LLaMA-7B shape 3864 -> 3686 us
-// (QKV and gate/up at three tiles), FlanT5-xl 1679 -> 1649 us (QKV and gate/up at two); two tiles
-// on the LLaMA-7B shape's 768 QKV tiles (384 blocks) lose, 4008 us.  A PACK projection with fewer
-// tiles than units runs half tiles instead (skinny_half: two blocks a tile): at the FlanT5-xl
-// verify chunk (128 tiles) W_o 7.5 -> 7.0 us, the cross-attention query 6.9 -> 6.2 us, down
-// (K 5120) 12.7 -> 10.8 us.
 // Steps per batch: as many as the registers allow (skinny_cap), then balanced so that the wave's
 // last batch is not a short one padded with clamped re-reads.
 template <bool PACK>
 hipError_t launch_skinny_as(const LinearArgs& b, bool gated, bool rms, int tiles, dim3 block,
                             hipStream_t s) {
-  const int cus = device_cus();
-  // blocks of one tile: a grid row per 16 input rows (one with PACK)
-  const long long blocks1 = (long long)tiles * (PACK ? 1 : (b.M + 15) / 16);
-  const int nt = b.epi == EPI_ARGMAX ? 4 : (int)std::min<long long>(3, (blocks1 + cus - 1) / cus);
-  const int cap = skinny_cap(PACK, nt * (gated ? 2 : 1));
+  const SkinnyShape sh = skinny_shape(gated ? b.n_per : b.n_per * b.n_mats, b.M, b.epi, gated);
+  const int nb = gated ? 2 : 1;
+  const int cap = sh.half ? skinny_cap(sh.n * nb, 2) : skinny_cap(sh.n * nb * 2, PACK ? 2 : 4);
   const int spw = (b.K / 64 + SKW - 1) / SKW;
   const int batches = (spw + cap - 1) / cap;
   const int want = (spw + batches - 1) / batches;
@@ -1822,12 +2045,12 @@ hipError_t launch_skinny_as(const LinearArgs& b, bool gated, bool rms, int tiles
   for (int i = 0; i < 6; ++i)
     if (opts[i] >= want && opts[i] <= cap) { sk = opts[i]; break; }
   switch (sk) {
-    case 1: launch_skinny_sk<PACK, 1>(b, gated, rms, tiles, nt, block, s); break;
-    case 2: launch_skinny_sk<PACK, 2>(b, gated, rms, tiles, nt, block, s); break;
-    case 4: launch_skinny_sk<PACK, 4>(b, gated, rms, tiles, nt, block, s); break;
-    case 8: launch_skinny_sk<PACK, 8>(b, gated, rms, tiles, nt, block, s); break;
-    case 10: launch_skinny_sk<PACK, 10>(b, gated, rms, tiles, nt, block, s); break;
-    default: launch_skinny_sk<PACK, 12>(b, gated, rms, tiles, nt, block, s); break;
+    case 1: launch_skinny_sk<PACK, 1>(b, gated, rms, tiles, sh, block, s); break;
+    case 2: launch_skinny_sk<PACK, 2>(b, gated, rms, tiles, sh, block, s); break;
+    case 4: launch_skinny_sk<PACK, 4>(b, gated, rms, tiles, sh, block, s); break;
+    case 8: launch_skinny_sk<PACK, 8>(b, gated, rms, tiles, sh, block, s); break;
+    case 10: launch_skinny_sk<PACK, 10>(b, gated, rms, tiles, sh, block, s); break;
+    default: launch_skinny_sk<PACK, 12>(b, gated, rms, tiles, sh, block, s); break;
   }
   return hipGetLastError();
 }
