@@ -478,25 +478,26 @@ def test_verify_chunks_past_the_skinny_capacity_take_the_tile_path():
         parity.check_run_against_oracle(dec, wl.shape, pr[s], z[s], run, s, wl.gamma)
 
 
-@pytest.mark.parametrize("arch,batch", [("t5", 1), ("llama", 1), ("llama", 2), ("llama", 3)],
-                         ids=["t5-b1", "llama-b1", "llama-b2", "llama-b3"])
-def test_wide_skinny_projections_share_input_loads_over_tiles(arch, batch):
-    """Decoders 1536 wide with an 8704-wide FFN: at a chunk of at most 8 rows the QKV projection
-    has 288 tiles of 16 features and the gated FFN 544, more than a 256-unit device has compute
-    units, so their skinny MFMA blocks take two and three tiles (the QKV epilogue with rotary or
-    without, the gated epilogue), while W_o, the cross-attention projections and the down
-    projection (96 tiles) run half tiles.  Batch 2 also runs the draft steps (2 rows) on that
-    path; batch 3 verifies 12-row chunks on the two-plane form with several tiles a block.  Every
-    sequence's drafts, verify logits and accepted lengths follow the oracle."""
+@pytest.mark.parametrize("arch,batch,d_ff", [("t5", 1, 8704), ("t5", 1, 5120), ("llama", 1, 8704),
+                                             ("llama", 2, 8704), ("llama", 3, 8704)],
+                         ids=["t5-b1", "t5-b1-ff5120", "llama-b1", "llama-b2", "llama-b3"])
+def test_wide_skinny_projections_share_input_loads_over_tiles(arch, batch, d_ff):
+    """Decoders 1536 wide: at a chunk of at most 8 rows on a 256-unit device the QKV projection
+    (288 tiles of 16 features) takes three half tiles a block (QKV epilogue with rotary or
+    without), a gated FFN 8704 wide (544 tiles) three whole tiles, one 5120 wide (320 tiles) three
+    half tiles of both matrices, and W_o, the cross-attention projections and the down projection
+    (96 tiles) one half tile.  Batch 2 also runs the draft steps (2 rows) on those paths; batch 3
+    verifies 12-row chunks on the two-plane form with several tiles a block.  Every sequence's
+    drafts, verify logits and accepted lengths follow the oracle."""
     from dataclasses import replace
     if arch == "t5":
         sh = replace(synth.SMALL_T5_BF16, name="t5-wide-skinny", n_layers=3, d_model=1536,
-                     n_heads=24, d_head=64, d_ff=8704, vocab=2000, n_visual=16)
+                     n_heads=24, d_head=64, d_ff=d_ff, vocab=2000, n_visual=16)
         wl = synth.S_T5.with_(name="s-t5-wide-skinny", shape=sh, draft_layers=2, gamma=5,
                               new_tokens=16)
     else:
         sh = replace(synth.SMALL_LLAMA_BF16, name="llama-wide-skinny", n_layers=3, d_model=1536,
-                     n_heads=12, d_head=128, d_ff=8704, vocab=2000, n_visual=24)
+                     n_heads=12, d_head=128, d_ff=d_ff, vocab=2000, n_visual=24)
         wl = synth.S_LLAMA.with_(name="s-llama-wide-skinny", shape=sh, draft_layers=2, gamma=3,
                                  new_tokens=16)
     # stepwise rounds keep drafting a finished sequence at its last length: gamma more positions
