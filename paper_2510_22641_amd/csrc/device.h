@@ -47,6 +47,17 @@ __device__ __forceinline__ void split_bf16x8(const float* f, uint4& hi, uint4& l
   lo = make_uint4(l[0], l[1], l[2], l[3]);
 }
 
+// split_bf16x8 on values: hi / lo bf16 of the eight floats (a0.x .. a1.w).
+__device__ __forceinline__ void split_bf16x8_v(const float4& a0, const float4& a1, uint4& hi, uint4& lo) {
+  const uint32_t h0 = pack_bf16x2(a0.x, a0.y), h1 = pack_bf16x2(a0.z, a0.w);
+  const uint32_t h2 = pack_bf16x2(a1.x, a1.y), h3 = pack_bf16x2(a1.z, a1.w);
+  hi = make_uint4(h0, h1, h2, h3);
+  lo = make_uint4(pack_bf16x2(a0.x - __uint_as_float(h0 << 16), a0.y - __uint_as_float(h0 & 0xffff0000u)),
+                  pack_bf16x2(a0.z - __uint_as_float(h1 << 16), a0.w - __uint_as_float(h1 & 0xffff0000u)),
+                  pack_bf16x2(a1.x - __uint_as_float(h2 << 16), a1.y - __uint_as_float(h2 & 0xffff0000u)),
+                  pack_bf16x2(a1.z - __uint_as_float(h3 << 16), a1.w - __uint_as_float(h3 & 0xffff0000u)));
+}
+
 // Eight consecutive elements of a weight (or KV) row, as raw registers until converted.
 template <typename T> struct Vec8;
 template <> struct Vec8<bf16_t> {

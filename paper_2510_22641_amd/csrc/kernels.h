@@ -92,6 +92,9 @@ struct LinearArgs {
   int in_ld = 0;
   const float* in_ssq = nullptr;
   int in_nssq = 0;
+  // launch_linear_skinny_fold with NORM_SOFTMAX: float32 input rows (row m at in_f32 + m * in_ld)
+  // turned into softmax probabilities over groups of `group` consecutive inputs.
+  const float* in_f32 = nullptr;
   // Output planes for the next skinny launch (EPI_RESID: of out_gain * y_new, plus per-block
   // partial sums of squares of y_new in out_ssq[block * plane_rows + m]; gated: of y; null: none).
   bf16_t* out_planes = nullptr;
@@ -159,6 +162,12 @@ hipError_t launch_skinny_prep(const float* x, int ldx, int M, int K, const float
 
 // 16-feature tiles of a skinny launch.
 int skinny_blocks(int n_out);
+// The folded cross-attention of a verify chunk (at most 8 rows, float32 weights) on half tiles:
+// the scores fold_q . rms(x) (NORM_RMS, EPI_STORE, input planes as launch_linear_skinny's) or the
+// output y += fold_o . softmax(scores) per group (NORM_SOFTMAX, EPI_RESID, float32 input rows
+// in_f32).  skinny_fold_ok tells whether a chunk of M rows with these sizes takes this path.
+bool skinny_fold_ok(int d_model, int n_fold, int group, int M);
+hipError_t launch_linear_skinny_fold(const LinearArgs& a, hipStream_t s);
 // Partial sums of squares a skinny residual epilogue of n_out features over M rows leaves (the
 // in_nssq of its consumer): one per tile, or two with half tiles.
 int skinny_ssq_parts(int n_out, int M);

@@ -836,11 +836,19 @@ __global__ __launch_bounds__(64 * SKW) void gemv_mfma_kernel(const LinearArgs a)
 // whose weight loads share the block's input loads.  The epilogue runs on 64 threads per half tile
 // (feature (tid / 8) % 8, row tid % 8); a residual epilogue leaves one partial sum of squares per
 // half tile.
-template <bool GATED, bool RMS, int NH, int SK>
+// MODE 1 and 2 take float32 weights (the folded cross-attention matrices of a verify chunk): a lane
+// reads its 8 elements as 32 bytes and splits them into bf16 hi / lo, and a step takes the products
+// hi.hi, hi.lo and lo.hi (about 16 mantissa bits on both sides).  MODE 2 also takes its input as
+// float32 rows (in_f32) and turns them into softmax probabilities over groups of a.group
+// consecutive inputs (8, 16 or 32: the group of a lane's 8 elements spans the 1, 2 or 4 lanes
+// l, l ^ 16, l ^ 32, l ^ 48 of one row and step half), split into hi / lo as the B operand.
+template <bool GATED, bool RMS, int NH, int SK, int MODE = 0>
 __global__ __launch_bounds__(64 * SKW, 2) void gemv_mfma_half_kernel(const LinearArgs a) {
   constexpr int NB = GATED ? 2 : 1;
   constexpr int NG = 4 * SKW;  // groups of 16 threads
+  constexpr bool WF = MODE >= 1, SMX = MODE == 2;
   static_assert(NH <= SKW, "one wave per half tile in the epilogue");
+  static_assert(!WF || !GATED, "float32 weights: one matrix");
   __shared__ float part[SKW][NB][NH][8][9];
   __shared__ float rs[16];
   __shared__ float ssq_red[4 * SKW][16];
@@ -876,11 +884,13 @@ __global__ __launch_bounds__(64 * SKW, 2) void gemv_mfma_half_kernel(const Linea
   };
   // this lane's weight rows: feature lane % 8 of each of the block's half tiles
   const bf16_t* wrow[NB][NH];
+  const float* wrowf[NH];
 #pragma unroll
   for (int i = 0; i < NH; ++i) {
     const int h = h0 + i;
     const int row = h < halves ? feature(h, lane & 7) : 0;
     const int rr = row < n_out ? row : 0;
+    wrowf[i] = reinterpret_cast<const float*>(a.w[0]) + (size_t)rr * K;
     if (GATED) {
       wrow[0][i] = reinterpret_cast<const bf16_t*>(a.w[0]) + (size_t)rr * K;
       wrow[NB - 1][i] = reinterpret_cast<const bf16_t*>(a.w[1]) + (size_t)rr * K;
@@ -897,6 +907,8 @@ __global__ __launch_bounds__(64 * SKW, 2) void gemv_mfma_half_kernel(const Linea
   const int PR = a.plane_rows;
   const bf16_t* brow = a.in_planes + (size_t)(tok_ok ? tok : 0) * a.in_ld;
   const bf16_t* brow_lo = brow + (size_t)PR * a.in_ld;
+  const float* frow = SMX ? a.in_f32 + (size_t)(tok_ok ? tok : 0) * a.in_ld : nullptr;
+  const int gsh = SMX ? (a.group >= 32 ? 2 : (a.group >= 16 ? 1 : 0)) : 0;  // exchanges per group
 
   // epilogue thread: half tile ei, feature ef, row et
   const int ei = tid >> 6, ef = (tid >> 3) & 7, et = tid & 7;
@@ -924,21 +936,37 @@ __global__ __launch_bounds__(64 * SKW, 2) void gemv_mfma_half_kernel(const Linea
 #pragma unroll
     for (int i = 0; i < NH; ++i) acc[b][i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   for (int s0 = s_beg; s0 < s_end; s0 += SK) {
-    uint4 wv[NB][NH][SK], bv[SK][2];  // bv: the hi and lo planes' 16 bytes
+    // bv: the hi and lo planes' 16 bytes (SMX: 32 bytes of the float32 row); wv: bf16 weights,
+    // wf: float32 weights (WF)
+    uint4 wv[NB][NH][WF ? 1 : SK], bv[SK][2];
+    float4 wf[NH][WF ? SK : 1][2];
     // inputs first (L2-resident, they arrive early), then the weights in step order
 #pragma unroll
     for (int u = 0; u < SK; ++u) {
       const int k0 = min(s0 + u, s_end - 1) * 64 + kq;
-      bv[u][0] = *reinterpret_cast<const uint4*>(brow + k0);
-      bv[u][1] = *reinterpret_cast<const uint4*>(brow_lo + k0);
+      if (SMX) {
+        const float4 f0 = *reinterpret_cast<const float4*>(frow + k0);
+        const float4 f1 = *reinterpret_cast<const float4*>(frow + k0 + 4);
+        bv[u][0] = make_uint4(__float_as_uint(f0.x), __float_as_uint(f0.y), __float_as_uint(f0.z), __float_as_uint(f0.w));
+        bv[u][1] = make_uint4(__float_as_uint(f1.x), __float_as_uint(f1.y), __float_as_uint(f1.z), __float_as_uint(f1.w));
+      } else {
+        bv[u][0] = *reinterpret_cast<const uint4*>(brow + k0);
+        bv[u][1] = *reinterpret_cast<const uint4*>(brow_lo + k0);
+      }
     }
 #pragma unroll
     for (int u = 0; u < SK; ++u) {
       const int k0 = min(s0 + u, s_end - 1) * 64 + kq;
 #pragma unroll
-      for (int i = 0; i < NH; ++i)
+      for (int i = 0; i < NH; ++i) {
+        if constexpr (WF) {
+          wf[i][u][0] = *reinterpret_cast<const float4*>(wrowf[i] + k0);
+          wf[i][u][1] = *reinterpret_cast<const float4*>(wrowf[i] + k0 + 4);
+        } else {
 #pragma unroll
-        for (int b = 0; b < NB; ++b) wv[b][i][u] = *reinterpret_cast<const uint4*>(wrow[b][i] + k0);
+          for (int b = 0; b < NB; ++b) wv[b][i][u] = *reinterpret_cast<const uint4*>(wrow[b][i] + k0);
+        }
+      }
     }
     __builtin_amdgcn_sched_barrier(0);  // keep the whole batch in flight before the first MFMA
 #pragma unroll
@@ -946,18 +974,58 @@ __global__ __launch_bounds__(64 * SKW, 2) void gemv_mfma_half_kernel(const Linea
       // a step past this wave's range, or a row past M, re-read valid data: zero operands
       const bool use = tok_ok && (s0 + u < s_end);
       const uint4 z = make_uint4(0, 0, 0, 0);
-      const uint4 b0 = use ? bv[u][0] : z, b1 = use ? bv[u][1] : z;
-      // every weight fragment against the hi plane, then against the lo plane (independent
-      // products back to back)
+      uint4 b0 = bv[u][0], b1 = bv[u][1];
+      if constexpr (SMX) {
+        // softmax over the lane's group: max and sum over its 8 elements and the group's other
+        // lanes (every lane takes part in the exchanges), then hi / lo of the probabilities
+        float f[8] = {__uint_as_float(b0.x), __uint_as_float(b0.y), __uint_as_float(b0.z), __uint_as_float(b0.w),
+                      __uint_as_float(b1.x), __uint_as_float(b1.y), __uint_as_float(b1.z), __uint_as_float(b1.w)};
+        float m = f[0];
 #pragma unroll
-      for (int pl = 0; pl < 2; ++pl) {
-        const bf16x8_t B = *reinterpret_cast<const bf16x8_t*>(pl ? &b1 : &b0);
+        for (int e = 1; e < 8; ++e) m = fmaxf(m, f[e]);
+        const float m16 = fmaxf(m, __shfl_xor(m, 16, SSD_WAVE));
+        const float m32 = fmaxf(m16, __shfl_xor(m16, 32, SSD_WAVE));
+        m = gsh == 0 ? m : (gsh == 1 ? m16 : m32);
+        float sum = 0.f;
 #pragma unroll
-        for (int i = 0; i < NH; ++i)
+        for (int e = 0; e < 8; ++e) {
+          f[e] = expf(f[e] - m);
+          sum += f[e];
+        }
+        const float s16 = sum + __shfl_xor(sum, 16, SSD_WAVE);
+        const float s32 = s16 + __shfl_xor(s16, 32, SSD_WAVE);
+        sum = gsh == 0 ? sum : (gsh == 1 ? s16 : s32);
+        const float inv = 1.0f / sum;
+        split_bf16x8_v(make_float4(f[0] * inv, f[1] * inv, f[2] * inv, f[3] * inv),
+                       make_float4(f[4] * inv, f[5] * inv, f[6] * inv, f[7] * inv), b0, b1);
+      }
+      // operands as values (no address taken, so that nothing of the batch lives in memory)
+      const bf16x8_t B0 = __builtin_bit_cast(bf16x8_t, use ? b0 : z);
+      const bf16x8_t B1 = __builtin_bit_cast(bf16x8_t, use ? b1 : z);
+      if constexpr (WF) {
+        // float32 weights: hi.hi, hi.lo and lo.hi
 #pragma unroll
-          for (int b = 0; b < NB; ++b)
-            acc[b][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                *reinterpret_cast<const bf16x8_t*>(&wv[b][i][u]), B, acc[b][i], 0, 0, 0);
+        for (int i = 0; i < NH; ++i) {
+          uint4 whi, wlo;
+          split_bf16x8_v(wf[i][u][0], wf[i][u][1], whi, wlo);
+          const bf16x8_t Ah = __builtin_bit_cast(bf16x8_t, whi);
+          const bf16x8_t Al = __builtin_bit_cast(bf16x8_t, wlo);
+          acc[0][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(Ah, B0, acc[0][i], 0, 0, 0);
+          acc[0][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(Ah, B1, acc[0][i], 0, 0, 0);
+          acc[0][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(Al, B0, acc[0][i], 0, 0, 0);
+        }
+      } else {
+        // every weight fragment against the hi plane, then against the lo plane (independent
+        // products back to back)
+#pragma unroll
+        for (int pl = 0; pl < 2; ++pl) {
+#pragma unroll
+          for (int i = 0; i < NH; ++i)
+#pragma unroll
+            for (int b = 0; b < NB; ++b)
+              acc[b][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                  __builtin_bit_cast(bf16x8_t, wv[b][i][u]), pl ? B1 : B0, acc[b][i], 0, 0, 0);
+        }
       }
     }
   }
@@ -2029,22 +2097,25 @@ void launch_skinny_sk(const LinearArgs& b, bool gated, bool rms, int tiles, Skin
 }
 
 // Steps per batch: as many as the registers allow (skinny_cap), then balanced so that the wave's
-// last batch is not a short one padded with clamped re-reads.
+// last batch is not a short one padded with clamped re-reads.  Instantiated depths: 1, 2, 4, 8,
+// 10, 12 (the smallest not below the balanced depth, at most the cap).
+int skinny_depth(int K, int cap) {
+  const int spw = (K / 64 + SKW - 1) / SKW;
+  const int batches = (spw + cap - 1) / cap;
+  const int want = (spw + batches - 1) / batches;
+  const int opts[6] = {1, 2, 4, 8, 10, 12};
+  for (int i = 0; i < 6; ++i)
+    if (opts[i] >= want && opts[i] <= cap) return opts[i];
+  return cap;
+}
+
 template <bool PACK>
 hipError_t launch_skinny_as(const LinearArgs& b, bool gated, bool rms, int tiles, dim3 block,
                             hipStream_t s) {
   const SkinnyShape sh = skinny_shape(gated ? b.n_per : b.n_per * b.n_mats, b.M, b.epi, gated);
   const int nb = gated ? 2 : 1;
   const int cap = sh.half ? skinny_cap(sh.n * nb, 2) : skinny_cap(sh.n * nb * 2, PACK ? 2 : 4);
-  const int spw = (b.K / 64 + SKW - 1) / SKW;
-  const int batches = (spw + cap - 1) / cap;
-  const int want = (spw + batches - 1) / batches;
-  // instantiated depths: 1, 2, 4, 8, 10, 12 (the smallest not below `want`, at most the cap)
-  const int opts[6] = {1, 2, 4, 8, 10, 12};
-  int sk = cap;
-  for (int i = 0; i < 6; ++i)
-    if (opts[i] >= want && opts[i] <= cap) { sk = opts[i]; break; }
-  switch (sk) {
+  switch (skinny_depth(b.K, cap)) {
     case 1: launch_skinny_sk<PACK, 1>(b, gated, rms, tiles, sh, block, s); break;
     case 2: launch_skinny_sk<PACK, 2>(b, gated, rms, tiles, sh, block, s); break;
     case 4: launch_skinny_sk<PACK, 4>(b, gated, rms, tiles, sh, block, s); break;
@@ -2069,6 +2140,53 @@ hipError_t launch_linear_skinny(const LinearArgs& a, hipStream_t s, int* n_parts
   const dim3 block(64 * SKW);
   if (a.M <= 8) return launch_skinny_as<true>(b, gated, rms, tiles, block, s);
   return launch_skinny_as<false>(b, gated, rms, tiles, block, s);
+}
+
+bool skinny_fold_ok(int d_model, int n_fold, int group, int M) {
+  // the output projection's partial sums of squares must be those of half tiles, which the
+  // chunk's other residual launches leave too
+  return M >= 2 && M <= 8 && d_model % 64 == 0 && n_fold % 64 == 0 &&
+         (group == 8 || group == 16 || group == 32) && n_fold % group == 0 &&
+         skinny_shape(d_model, M, EPI_RESID, false).half;
+}
+
+template <int MODE, bool RMS, int SK>
+void launch_fold_sk(const LinearArgs& b, int tiles, hipStream_t s) {
+  hipLaunchKernelGGL((gemv_mfma_half_kernel<false, RMS, 1, SK, MODE>), dim3(2 * tiles), dim3(64 * SKW),
+                     0, s, b);
+}
+
+template <int MODE, bool RMS>
+void launch_fold_mode(const LinearArgs& b, int tiles, int sk, hipStream_t s) {
+  switch (sk) {
+    case 1: launch_fold_sk<MODE, RMS, 1>(b, tiles, s); break;
+    case 2: launch_fold_sk<MODE, RMS, 2>(b, tiles, s); break;
+    case 4: launch_fold_sk<MODE, RMS, 4>(b, tiles, s); break;
+    case 8: launch_fold_sk<MODE, RMS, 8>(b, tiles, s); break;
+    case 10: launch_fold_sk<MODE, RMS, 10>(b, tiles, s); break;
+    default: launch_fold_sk<MODE, RMS, 12>(b, tiles, s); break;
+  }
+}
+
+hipError_t launch_linear_skinny_fold(const LinearArgs& a, hipStream_t s) {
+  const bool smx = a.norm == NORM_SOFTMAX;
+  if (a.wdtype != SSD_F32 || a.n_mats != 1 || a.M < 2 || a.M > 8 || a.M > a.plane_rows ||
+      a.K % 64 || a.n_per < 1)
+    return hipErrorInvalidValue;
+  if (smx) {
+    if (a.epi != EPI_RESID || !a.in_f32 || a.in_ld % 4 ||
+        (a.group != 8 && a.group != 16 && a.group != 32) || a.K % a.group)
+      return hipErrorInvalidValue;
+  } else if (a.norm != NORM_RMS || a.epi != EPI_STORE || !a.in_planes || !a.in_ssq ||
+             a.in_nssq < 1 || a.in_nssq > SSQ_MAX) {
+    return hipErrorInvalidValue;
+  }
+  const int tiles = skinny_blocks(a.n_per);
+  // a half tile a block; 32 bytes of float32 weights and two input loads a step
+  const int sk = skinny_depth(a.K, skinny_cap(2, 2));
+  if (smx) launch_fold_mode<2, false>(a, tiles, sk, s);
+  else launch_fold_mode<1, true>(a, tiles, sk, s);
+  return hipGetLastError();
 }
 
 hipError_t launch_skinny_prep(const float* x, int ldx, int M, int K, const float* gain, bf16_t* out,

@@ -434,6 +434,27 @@ int run_layers(ssd_ctx* c, float* x, int B, int C, int pos_off, int l0, int l1, 
       a.w[0] = c->at<float>(c->L.fold_o) + (size_t)l * c->fold_layer_elems(); a.wdtype = SSD_F32;
       a.n_per = D; a.epi = EPI_RESID; a.y = x; a.ldy = D;
       HIP_TRY(run_linear(c, a));
+    } else if (t5 && skinny && c->fold_ready &&
+               skinny_fold_ok(D, d.n_heads * d.n_visual, d.n_visual, R)) {
+      // folded, for a verify chunk on half tiles (float32 matrices split into bf16 hi / lo in the
+      // kernel): scores = fold_q . rmsnorm(x) per row, then x += fold_o . softmax(scores) per head
+      // with the softmax taken in the second launch's input loads
+      const int HN = d.n_heads * d.n_visual;
+      a = lin(c);
+      a.x = x; a.ldx = D; a.M = R; a.K = D;
+      a.norm = NORM_RMS; a.gain = lw.xattn_norm;
+      a.w[0] = c->at<float>(c->L.fold_q) + (size_t)l * c->fold_layer_elems(); a.wdtype = SSD_F32;
+      a.n_per = HN; a.epi = EPI_STORE; a.y = q; a.ldy = HD;
+      a.in_planes = p_x; a.in_ld = D; a.plane_rows = PR; a.in_ssq = ssq; a.in_nssq = nssq;
+      HIP_TRY(launch_linear_skinny_fold(a, s));
+      a = lin(c);
+      a.x = q; a.ldx = HD; a.M = R; a.K = HN;
+      a.norm = NORM_SOFTMAX; a.group = d.n_visual;
+      a.w[0] = c->at<float>(c->L.fold_o) + (size_t)l * c->fold_layer_elems(); a.wdtype = SSD_F32;
+      a.n_per = D; a.epi = EPI_RESID; a.y = x; a.ldy = D;
+      a.in_f32 = q; a.in_ld = HD; a.plane_rows = PR;
+      resid_out(a, lw.ffn_norm);
+      HIP_TRY(launch_linear_skinny_fold(a, s));
     } else if (t5) {
       a = lin(c);
       a.x = x; a.ldx = D; a.M = R; a.K = D;

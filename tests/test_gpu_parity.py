@@ -506,3 +506,36 @@ def test_wide_skinny_projections_share_input_loads_over_tiles(arch, batch, d_ff)
     assert dd.sync_status() == (0, 0)
     for s in range(batch):
         parity.check_run_against_oracle(dec, wl.shape, pr[s], z[s], run, s, wl.gamma)
+
+
+@pytest.mark.parametrize("n_visual", [8, 16, 32], ids=["nv8", "nv16", "nv32"])
+def test_verify_chunk_folded_cross_attention(n_visual):
+    """A one-sequence T5 context (8 heads, n_visual 8, 16 or 32 visual keys): the verify chunk's
+    cross-attention runs folded on half tiles, the scores fold_q . rmsnorm(x) with the float32
+    matrix split into bf16 hi / lo in the kernel, then x += fold_o . softmax(scores), the softmax
+    over groups of n_visual taken in the second launch's input loads.  A two-sequence context of
+    the same decoder keeps the query projection, attention launch and output projection.  Both
+    runs follow the oracle, and while their token streams agree their verify logits agree within
+    the tolerance."""
+    from dataclasses import replace
+    sh = replace(synth.SMALL_T5_BF16, name=f"t5-fold-chunk-nv{n_visual}", n_layers=4, d_model=512,
+                 n_heads=8, d_head=64, d_ff=1024, vocab=2000, n_visual=n_visual)
+    wl = synth.S_T5.with_(name=f"s-t5-fold-chunk-nv{n_visual}", shape=sh, draft_layers=2,
+                          gamma=5, new_tokens=20)
+    runs = []
+    for mb in (1, 2):
+        dd, dec, pr, z, pt, vt = _setup(wl, seed=23, page_seed=6, max_batch=mb)
+        run = parity.device_run(dd, pt, vt, wl.new_tokens, wl.gamma, reuse=True)
+        parity.check_run_against_oracle(dec, wl.shape, pr[0], z[0], run, 0, wl.gamma)
+        assert dd.sync_status() == (0, 0)
+        runs.append(run)
+    folded, unfolded = runs
+    compared = 0
+    for i, (ra, rb) in enumerate(zip(folded.rounds, unfolded.rounds)):
+        if not (np.array_equal(ra.drafts, rb.drafts) and np.array_equal(ra.targets, rb.targets)):
+            break
+        for j in range(ra.target_logits.shape[1]):
+            parity.check_logits(ra.target_logits[0, j], rb.target_logits[0, j].astype(np.float64),
+                                wl.shape, f"round {i} verify {j}")
+        compared += 1
+    assert compared >= 1
