@@ -539,3 +539,25 @@ def test_verify_chunk_folded_cross_attention(n_visual):
                                 wl.shape, f"round {i} verify {j}")
         compared += 1
     assert compared >= 1
+
+
+@pytest.mark.parametrize("wl", [synth.S_T5, synth.S_LLAMA], ids=lambda w: w.name)
+def test_longest_draft_and_one_token_jobs(wl):
+    """gamma = 32, the largest draft length a context accepts: the verify chunk is 33 rows, three
+    16-row groups of the two-plane skinny path with a one-row tail, and a round drafts 32 tokens
+    through the captured draft step.  Every draft and verify logit follows the oracle, the
+    accepted lengths are bit-exact and the generate loop equals the stepwise calls.  A job of one
+    token (T = 1) is the prefill's token alone: no round runs."""
+    wl = wl.with_(name=wl.name + "-g32", gamma=32, new_tokens=40)
+    dd, dec, pr, z, pt, vt = _setup(wl, seed=21, page_seed=4)
+    run = parity.device_run(dd, pt, vt, wl.new_tokens, wl.gamma, reuse=True)
+    assert dd.sync_status() == (0, 0)
+    parity.check_run_against_oracle(dec, wl.shape, pr[0], z[0], run, 0, wl.gamma)
+    toks, stats = dd.generate(pt, vt, wl.new_tokens, wl.gamma, speculative=True, reuse=True)
+    assert toks.cpu().numpy()[0].tolist() == run.tokens[0]
+    assert stats["rounds"] == len(run.rounds)
+    assert stats["drafted"] == wl.gamma * stats["rounds"]
+    one, st1 = dd.generate(pt, vt, 1, wl.gamma, speculative=True, reuse=True)
+    assert one.cpu().numpy()[0].tolist() == run.tokens[0][:1]
+    assert st1["rounds"] == 0 and st1["drafted"] == 0
+    assert dd.sync_status() == (0, 0)
