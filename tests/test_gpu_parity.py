@@ -561,3 +561,22 @@ def test_longest_draft_and_one_token_jobs(wl):
     assert one.cpu().numpy()[0].tolist() == run.tokens[0][:1]
     assert st1["rounds"] == 0 and st1["drafted"] == 0
     assert dd.sync_status() == (0, 0)
+
+
+@pytest.mark.parametrize("wl", [synth.S_T5, synth.S_LLAMA], ids=lambda w: w.name)
+def test_verify_chunk_at_the_skinny_capacity(wl):
+    """Batch 32 with gamma = 3: the verify chunk is 32 x 4 = 128 rows, the most the skinny MFMA
+    path takes (eight 16-row groups of the two-plane form), and the draft steps are 32-row skinny
+    launches; the T5 cross-attention runs unfolded (more than one sequence).  Every sequence's
+    drafts and verify logits follow the oracle round by round, with the accepted lengths
+    bit-exact, and the generate loop equals the stepwise calls."""
+    wl = wl.with_(name=wl.name + "-b32", gamma=3, new_tokens=10)
+    dd, dec, pr, z, pt, vt = _setup(wl, seed=23, batch=32, page_seed=9, extra_seq=wl.gamma)
+    run = parity.device_run(dd, pt, vt, wl.new_tokens, wl.gamma, reuse=True)
+    assert dd.sync_status() == (0, 0)
+    for s in range(32):
+        parity.check_run_against_oracle(dec, wl.shape, pr[s], z[s], run, s, wl.gamma)
+    toks, stats = dd.generate(pt, vt, wl.new_tokens, wl.gamma, speculative=True, reuse=True)
+    assert toks.cpu().numpy().tolist() == run.tokens
+    assert stats["rounds"] == len(run.rounds)
+    assert dd.sync_status() == (0, 0)
